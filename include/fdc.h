@@ -1,0 +1,196 @@
+/*
+ * fdc.h -- C ABI of libfdc, the gfx950 (MI355X) implementation of the
+ * Frequency Domain Convolution (FDC) and Frequency Domain Pooling (FDP) layers
+ * of Goh, Chen and Lim, "Frequency Domain Convolutional Neural Network:
+ * Accelerated CNN for Large Diabetic Retinopathy Image Classification"
+ * (arXiv 2106.12736), forward and backward.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.    Every tensor argument is a DEVICE pointer owned by the caller
+ *            (the library never frees or keeps it).  Tensors are dense,
+ *            contiguous and row-major.  Real tensors are float32; spectra
+ *            are complex64 stored as interleaved {float re, im} pairs
+ *            (fdc_c64), the layout of torch.complex64.
+ * Spectra.   A real H x W image has the half spectrum [H][W/2+1] of the
+ *            real-to-complex DFT (section 2.4.1.1):
+ *              X[k][l] = sum_{h<H, w<W} x[h][w] exp(-2 pi i (hk/H + wl/W)),
+ *            k < H, l <= W/2, unnormalised, rows in natural (unshifted)
+ *            order.  The inverse is scaled by 1/(H W) and takes the real
+ *            part: for ANY complex half spectrum Y,
+ *              irfft2(Y)[h][w] = 1/(HW) sum_{k, l<=W/2} c_l Re(Y[k][l] exp(+2 pi i (hk/H + wl/W)))
+ *            with c_0 = c_{W/2} = 1 and c_l = 2 otherwise.
+ * Gradients. For a real loss L, the gradient of a complex tensor Z is
+ *            dL/dRe(Z) + i dL/dIm(Z).  Gradient outputs are overwritten,
+ *            never accumulated.  A NULL gradient output skips that output.
+ * Streams.   Every compute call validates its arguments on the host and then
+ *            enqueues kernels asynchronously on `stream` (NULL = the null
+ *            stream) and returns.  When a call returns an error nothing has
+ *            been enqueued.  Device faults surface at the caller's next
+ *            synchronisation.  Calls allocate no device memory; workspaces
+ *            are supplied by the caller and must not be shared by calls that
+ *            may run concurrently.
+ * Sizes.     Transform lengths must be in the supported set: a power of two
+ *            from 2 to 1024, or 224 (= 7 * 32, the 224 x 224 image size of the
+ *            Full FDC workloads).  Other lengths return FDC_EUNSUPPORTED.
+ * Errors.    Calls return an fdc_status.  fdc_last_error() gives a
+ *            thread-local text for the last non-OK status of this thread.
+ *            No C++ exception crosses this interface.
+ */
+#ifndef FDC_H
+#define FDC_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct { float re, im; } fdc_c64;
+
+typedef enum {
+  FDC_OK = 0,
+  FDC_EINVAL = 1,          /* bad argument: NULL pointer, size <= 0, odd size, S mod C != 0, M > N ... */
+  FDC_EUNSUPPORTED = 2,    /* valid but not implemented: transform length outside the supported set */
+  FDC_EWORKSPACE = 3,      /* workspace pointer NULL or smaller than the queried size */
+  FDC_EHIP = 4             /* a HIP runtime call or kernel launch failed (text in fdc_last_error) */
+} fdc_status;
+
+/* Convolution artifact handling (section 2.4.1.3).  A frequency-domain product is a
+ * circular convolution, whose wrap-around pollutes the top n-1 rows and left n-1
+ * columns for an n x n kernel.
+ *   NONE: keep the circular result (M x M).
+ *   CROP: cut n-1 rows at the top and n-1 columns at the left -> (M-n+1) x (M-n+1),
+ *         the size of a spatial convolution without padding.
+ *   ROLL: keep M x M but shift by s = (n-1)/2 (integer division) so the artifact is
+ *         spread over all edges: out[i][j] = y[(i+s) mod M][(j+s) mod M]. */
+typedef enum { FDC_ARTIFACT_NONE = 0, FDC_ARTIFACT_CROP = 1, FDC_ARTIFACT_ROLL = 2 } fdc_artifact;
+
+const char *fdc_status_string(int status);
+const char *fdc_last_error(void);
+/* Library version as 10000*major + 100*minor + patch. */
+int fdc_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* 2-D real FFT plans (section 2.4.1.1: RFFT of real images, width N/2+1)    */
+/* ------------------------------------------------------------------------ */
+typedef struct fdc_fft_plan fdc_fft_plan;
+
+/* A plan for `count` independent h x w real images (h, w in the supported set).
+ * The plan is an immutable host object (no device memory); it may be used
+ * concurrently on several streams.  Returns FDC_EINVAL for count < 1 or NULL. */
+fdc_status fdc_fft_plan_create(fdc_fft_plan **plan, int64_t count, int h, int w);
+fdc_status fdc_fft_plan_destroy(fdc_fft_plan *plan);
+/* Bytes of workspace the four transforms below need (0 for fdc_rfft2 and
+ * fdc_irfft2_backward, which work in their output buffer). */
+fdc_status fdc_fft_workspace_size(const fdc_fft_plan *plan, size_t *bytes);
+
+/* x [count][h][w] float32 -> X [count][h][w/2+1] complex, forward, unnormalised. */
+fdc_status fdc_rfft2(const fdc_fft_plan *plan, const float *x, fdc_c64 *X,
+                     void *ws, size_t ws_bytes, hipStream_t stream);
+/* X [count][h][w/2+1] -> x [count][h][w]: the inverse defined above (1/(hw), real part
+ * of columns 0 and w/2 after the column inverse, for any complex X). */
+fdc_status fdc_irfft2(const fdc_fft_plan *plan, const fdc_c64 *X, float *x,
+                      void *ws, size_t ws_bytes, hipStream_t stream);
+/* Adjoint of fdc_rfft2: gx[h][w] = sum_{k, l<=w/2} Re(gX[k][l] exp(+2 pi i (hk/H + wl/W))). */
+fdc_status fdc_rfft2_backward(const fdc_fft_plan *plan, const fdc_c64 *gX, float *gx,
+                              void *ws, size_t ws_bytes, hipStream_t stream);
+/* Adjoint of fdc_irfft2: gX[k][l] = (c_l / (h w)) * rfft2(gx)[k][l]. */
+fdc_status fdc_irfft2_backward(const fdc_fft_plan *plan, const float *gx, fdc_c64 *gX,
+                               void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Channel Independent Convolution on spectra (Eq. 5, Algorithm 1)          */
+/* ------------------------------------------------------------------------ */
+/* Y[b][o] = X[b][o / J] o K[o] for o = c*J + j < S, J = S / C (S mod C must be 0),
+ * elementwise over the [H][Wf] bins.  X [B][C][H][Wf], K [S][H][Wf], Y [B][S][H][Wf]. */
+fdc_status fdc_cic_forward(const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *Y,
+                           int B, int C, int S, int H, int Wf, hipStream_t stream);
+/* gX[b][c] = sum_j gY[b][cJ+j] conj(K[cJ+j]);  gK[o] = sum_b gY[b][o] conj(X[b][o/J]).
+ * The sum over b is done in a fixed order (bitwise reproducible). */
+fdc_status fdc_cic_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K,
+                            fdc_c64 *gX, fdc_c64 *gK,
+                            int B, int C, int S, int H, int Wf, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Frequency Domain Pooling (section 2.4.2)                                 */
+/* ------------------------------------------------------------------------ */
+/* FDP crops the RFFT-shifted half spectrum: (H-Mh)/2 rows off the top and the
+ * bottom, (W-Mw)/2 columns off the right, then shifts back.  In unshifted
+ * order it keeps rows [0, Mh/2) and [H-Mh/2, H) and columns [0, Mw/2]; no
+ * rescaling.  X [count][H][W/2+1] -> Y [count][Mh][Mw/2+1].  H, W, Mh, Mw even,
+ * Mh <= H, Mw <= W (any reduction, not only halving). */
+fdc_status fdp_forward(const fdc_c64 *X, fdc_c64 *Y, int64_t count,
+                       int H, int W, int Mh, int Mw, hipStream_t stream);
+/* Adjoint: gX = gY scattered back to the kept positions, zeros elsewhere. */
+fdc_status fdp_backward(const fdc_c64 *gY, fdc_c64 *gX, int64_t count,
+                        int H, int W, int Mh, int Mw, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Fused CIC + FDP layer on spatial activations                             */
+/*   x -> rfft2 -> CIC (Eq. 5) -> FDP -> irfft2 -> artifact handling -> y     */
+/* (Algorithm 1 inside Algorithm 2's spatial wrapper, with FDP of section    */
+/*  2.4.2 applied before the inverse; per-layer transforms)                 */
+/* ------------------------------------------------------------------------ */
+typedef struct fdc_layer_plan fdc_layer_plan;
+
+/* B images of C channels, N x N (N in the supported set) -> S = J*C channels of
+ * M x M (M even, M <= N, N/M a power of two), kernels K [S][N][N/2+1] complex
+ * (full-size spectra).  `artifact` with `kernel_n` (the spatial support the
+ * kernels stand for, 1 <= kernel_n <= M) sets the output size:
+ * NONE/ROLL -> M x M, CROP -> (M-kernel_n+1)^2.  Plans are immutable host objects. */
+fdc_status fdc_cic_layer_plan_create(fdc_layer_plan **plan, int B, int C, int S, int N, int M,
+                                     int artifact, int kernel_n);
+/* Full FDC layer (Algorithm 2 with the per-bin sum over input channels of Eq. 2):
+ * x [B][Cin][P][P], weights w [Cout][Cin][n][n] spatial (padded to P x P at the
+ * top-left and transformed on every call, section 2.4.1.2), y [B][Cout][..][..]. */
+fdc_status fdc_full_layer_plan_create(fdc_layer_plan **plan, int B, int Cin, int Cout, int P,
+                                      int kernel_n, int artifact);
+fdc_status fdc_layer_plan_destroy(fdc_layer_plan *plan);
+/* Workspace sizes in bytes: forward scratch, the `saved` buffer forward writes
+ * and backward reads, and backward scratch. */
+fdc_status fdc_layer_workspace_size(const fdc_layer_plan *plan, size_t *fwd_ws, size_t *saved,
+                                    size_t *bwd_ws);
+/* Output spatial size (rows = cols) of the layer. */
+fdc_status fdc_layer_output_size(const fdc_layer_plan *plan, int *out_size);
+
+/* x [B][C][N][N] float32, K [S][N][N/2+1] complex -> y [B][S][O][O] float32.
+ * `saved` (may be NULL when no backward will follow) receives the pooled input
+ * spectrum [B][C][M][M/2+1] complex the backward pass needs. */
+fdc_status fdc_cic_layer_forward(const fdc_layer_plan *plan, const float *x, const fdc_c64 *K,
+                                 float *y, void *saved, void *ws, size_t ws_bytes,
+                                 hipStream_t stream);
+/* gy [B][S][O][O] -> gx [B][C][N][N] (NULL: skipped) and gK [S][N][N/2+1] (NULL: skipped).
+ * gK is summed over the batch in a fixed order and holds exact zeros at the bins
+ * FDP drops (they do not reach the output). */
+fdc_status fdc_cic_layer_backward(const fdc_layer_plan *plan, const float *gy, const void *saved,
+                                  const fdc_c64 *K, float *gx, fdc_c64 *gK,
+                                  void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Full FDC forward: y = artifact(irfft2(sum_c rfft2(x[b][c]) o K[s][c])) with
+ * K[s][c] = rfft2(pad(w[s][c])).  `saved` receives rfft2(x) [B][Cin][P][P/2+1]. */
+fdc_status fdc_full_forward(const fdc_layer_plan *plan, const float *x, const float *w, float *y,
+                            void *saved, void *ws, size_t ws_bytes, hipStream_t stream);
+/* Full FDC backward: gx [B][Cin][P][P] (NULL: skipped), gw [Cout][Cin][n][n] (NULL: skipped). */
+fdc_status fdc_full_backward(const fdc_layer_plan *plan, const float *gy, const void *saved,
+                             const float *w, float *gx, float *gw, void *ws, size_t ws_bytes,
+                             hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Kernel timing (measurement support, off by default)                      */
+/* ------------------------------------------------------------------------ */
+/* While enabled, every kernel the library launches is bracketed by a pair of
+ * HIP events on its stream; fdc_kernel_timing_report() synchronises on those
+ * events and writes one line per kernel name: "<name> <launches> <total_ms>\n".
+ * Enabling clears earlier records.  At most `max_launches` launches are
+ * recorded; events are created when timing is enabled, never during a call. */
+fdc_status fdc_kernel_timing_enable(int max_launches);
+fdc_status fdc_kernel_timing_disable(void);
+fdc_status fdc_kernel_timing_report(char *buf, size_t buf_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FDC_H */

@@ -1,0 +1,491 @@
+// C ABI of libfdc: argument validation, plans, workspace layout and kernel
+// sequencing.  Every entry point validates on the host first and returns
+// before enqueuing anything when an argument is wrong.
+#include "../../include/fdc.h"
+#include "internal.h"
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <new>
+#include <string>
+#include <vector>
+
+namespace {
+
+thread_local std::string g_last_error;
+
+fdc_status fail(fdc_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+fdc_status check_hip(hipError_t e, const char *what) {
+  if (e == hipSuccess) return FDC_OK;
+  return fail(FDC_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool even_pos(long long v) { return v > 0 && v % 2 == 0; }
+
+constexpr uint32_t kFftMagic = 0xFDC0FF70u;
+constexpr uint32_t kLayerMagic = 0xFDC01A7Eu;
+
+}  // namespace
+
+struct fdc_fft_plan {
+  uint32_t magic;
+  int64_t count;
+  int h, w;
+};
+
+struct fdc_layer_plan {
+  uint32_t magic;
+  int kind;  // 0: CIC + FDP, 1: Full FDC
+  int B, C, S, N, M, artifact, kn, out;
+  size_t fwd_ws, saved, bwd_ws;
+};
+
+// ---------------------------------------------------------------------------
+// kernel timing
+// ---------------------------------------------------------------------------
+namespace {
+struct Timing {
+  std::mutex mu;
+  bool enabled = false;
+  int max = 0;
+  int used = 0;
+  std::vector<hipEvent_t> start, stop;
+  std::vector<const char *> names;
+};
+Timing &timing() {
+  static Timing t;
+  return t;
+}
+void timing_release(Timing &t) {
+  for (auto e : t.start) hipEventDestroy(e);
+  for (auto e : t.stop) hipEventDestroy(e);
+  t.start.clear();
+  t.stop.clear();
+  t.names.clear();
+  t.used = 0;
+  t.max = 0;
+}
+}  // namespace
+
+namespace fdc {
+void timing_before(const char *name, hipStream_t s) {
+  Timing &t = timing();
+  if (!t.enabled) return;
+  std::lock_guard<std::mutex> g(t.mu);
+  if (t.used >= t.max) return;
+  t.names[t.used] = name;
+  hipEventRecord(t.start[t.used], s);
+}
+void timing_after(const char *, hipStream_t s) {
+  Timing &t = timing();
+  if (!t.enabled) return;
+  std::lock_guard<std::mutex> g(t.mu);
+  if (t.used >= t.max) return;
+  hipEventRecord(t.stop[t.used], s);
+  ++t.used;
+}
+}  // namespace fdc
+
+using fdc::ImgView;
+
+extern "C" {
+
+const char *fdc_status_string(int status) {
+  switch (status) {
+    case FDC_OK: return "FDC_OK";
+    case FDC_EINVAL: return "FDC_EINVAL: invalid argument";
+    case FDC_EUNSUPPORTED: return "FDC_EUNSUPPORTED: size or mode not supported";
+    case FDC_EWORKSPACE: return "FDC_EWORKSPACE: workspace missing or too small";
+    case FDC_EHIP: return "FDC_EHIP: HIP runtime error";
+    default: return "unknown fdc_status";
+  }
+}
+
+const char *fdc_last_error(void) { return g_last_error.c_str(); }
+
+int fdc_version(void) { return 100; }
+
+// ---------------------------------------------------------------------------
+// 2-D real FFT plans
+// ---------------------------------------------------------------------------
+static fdc_status check_fft_plan(const fdc_fft_plan *p) {
+  if (p == nullptr || p->magic != kFftMagic) return fail(FDC_EINVAL, "invalid or destroyed fft plan");
+  return FDC_OK;
+}
+
+static size_t fft_spec_bytes(const fdc_fft_plan *p) {
+  return (size_t)p->count * p->h * (p->w / 2 + 1) * sizeof(fdc_c64);
+}
+
+fdc_status fdc_fft_plan_create(fdc_fft_plan **plan, int64_t count, int h, int w) {
+  if (plan == nullptr) return fail(FDC_EINVAL, "plan out-pointer is NULL");
+  *plan = nullptr;
+  if (count < 1) return fail(FDC_EINVAL, "count must be >= 1 (got %lld)", (long long)count);
+  if (!even_pos(h) || !even_pos(w)) return fail(FDC_EINVAL, "h and w must be positive and even (%d x %d)", h, w);
+  if (!fdc::size_supported(h) || !fdc::size_supported(w))
+    return fail(FDC_EUNSUPPORTED, "transform size %d x %d not supported", h, w);
+  auto *p = new (std::nothrow) fdc_fft_plan{kFftMagic, count, h, w};
+  if (p == nullptr) return fail(FDC_EINVAL, "out of host memory");
+  *plan = p;
+  return FDC_OK;
+}
+
+fdc_status fdc_fft_plan_destroy(fdc_fft_plan *plan) {
+  if (plan == nullptr) return FDC_OK;
+  if (plan->magic != kFftMagic) return fail(FDC_EINVAL, "invalid or destroyed fft plan");
+  plan->magic = 0;
+  delete plan;
+  return FDC_OK;
+}
+
+fdc_status fdc_fft_workspace_size(const fdc_fft_plan *plan, size_t *bytes) {
+  if (fdc_status st = check_fft_plan(plan)) return st;
+  if (bytes == nullptr) return fail(FDC_EINVAL, "bytes is NULL");
+  *bytes = fft_spec_bytes(plan);
+  return FDC_OK;
+}
+
+static fdc_status check_ws(void *ws, size_t have, size_t need) {
+  if (need == 0) return FDC_OK;
+  if (ws == nullptr || have < need)
+    return fail(FDC_EWORKSPACE, "workspace needs %zu bytes (got %zu, ptr %p)", need, have, ws);
+  return FDC_OK;
+}
+
+fdc_status fdc_rfft2(const fdc_fft_plan *p, const float *x, fdc_c64 *X, void *, size_t, hipStream_t s) {
+  if (fdc_status st = check_fft_plan(p)) return st;
+  if (!x || !X) return fail(FDC_EINVAL, "NULL tensor");
+  const int h = p->h, w = p->w, wf = w / 2 + 1;
+  ImgView id{0, 0, h, w};
+  auto *out = reinterpret_cast<float2 *>(X);
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(w, x, out, p->count, h, id, (long long)h * w, wf, wf,
+                                                    (long long)h * wf, 1.f, 1.f, s), "rfft2 rows"))
+    return st;
+  return check_hip(fdc::launch_col_fft(h, -1, out, out, p->count, wf, (long long)h * wf, (long long)h * wf, s),
+                   "rfft2 columns");
+}
+
+static fdc_status inverse_like(const fdc_fft_plan *p, const fdc_c64 *X, float *x, void *ws, size_t ws_bytes,
+                               hipStream_t s, float alpha, float beta, const char *what) {
+  if (fdc_status st = check_fft_plan(p)) return st;
+  if (!x || !X) return fail(FDC_EINVAL, "NULL tensor");
+  if (fdc_status st = check_ws(ws, ws_bytes, fft_spec_bytes(p))) return st;
+  const int h = p->h, w = p->w, wf = w / 2 + 1;
+  auto *tmp = reinterpret_cast<float2 *>(ws);
+  if (fdc_status st = check_hip(fdc::launch_col_fft(h, +1, reinterpret_cast<const float2 *>(X), tmp, p->count, wf,
+                                                    (long long)h * wf, (long long)h * wf, s), what))
+    return st;
+  ImgView id{0, 0, h, w};
+  return check_hip(fdc::launch_row_c2r(w, tmp, x, p->count, h, wf, wf, (long long)h * wf, alpha, beta, id,
+                                       (long long)h * w, s), what);
+}
+
+fdc_status fdc_irfft2(const fdc_fft_plan *p, const fdc_c64 *X, float *x, void *ws, size_t ws_bytes,
+                      hipStream_t s) {
+  if (fdc_status st = check_fft_plan(p)) return st;
+  return inverse_like(p, X, x, ws, ws_bytes, s, 1.f / ((float)p->h * (float)p->w), 1.f, "irfft2");
+}
+
+fdc_status fdc_rfft2_backward(const fdc_fft_plan *p, const fdc_c64 *gX, float *gx, void *ws, size_t ws_bytes,
+                              hipStream_t s) {
+  return inverse_like(p, gX, gx, ws, ws_bytes, s, 1.f, 0.5f, "rfft2_backward");
+}
+
+fdc_status fdc_irfft2_backward(const fdc_fft_plan *p, const float *gx, fdc_c64 *gX, void *, size_t,
+                               hipStream_t s) {
+  if (fdc_status st = check_fft_plan(p)) return st;
+  if (!gx || !gX) return fail(FDC_EINVAL, "NULL tensor");
+  const int h = p->h, w = p->w, wf = w / 2 + 1;
+  ImgView id{0, 0, h, w};
+  auto *out = reinterpret_cast<float2 *>(gX);
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(w, gx, out, p->count, h, id, (long long)h * w, wf, wf,
+                                                    (long long)h * wf, 1.f / ((float)h * (float)w), 2.f, s),
+                                "irfft2_backward rows"))
+    return st;
+  return check_hip(fdc::launch_col_fft(h, -1, out, out, p->count, wf, (long long)h * wf, (long long)h * wf, s),
+                   "irfft2_backward columns");
+}
+
+// ---------------------------------------------------------------------------
+// spectral CIC and FDP
+// ---------------------------------------------------------------------------
+static fdc_status check_cic_dims(int B, int C, int S, int H, int Wf) {
+  if (B < 1 || C < 1 || S < 1 || H < 1 || Wf < 1)
+    return fail(FDC_EINVAL, "sizes must be >= 1 (B=%d C=%d S=%d H=%d Wf=%d)", B, C, S, H, Wf);
+  if (S % C) return fail(FDC_EINVAL, "CIC needs S mod C == 0 (S=%d C=%d)", S, C);
+  return FDC_OK;
+}
+
+fdc_status fdc_cic_forward(const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *Y, int B, int C, int S, int H, int Wf,
+                           hipStream_t s) {
+  if (fdc_status st = check_cic_dims(B, C, S, H, Wf)) return st;
+  if (!X || !K || !Y) return fail(FDC_EINVAL, "NULL tensor");
+  return check_hip(fdc::launch_cic_fwd(reinterpret_cast<const float2 *>(X), reinterpret_cast<const float2 *>(K),
+                                       reinterpret_cast<float2 *>(Y), B, C, S, (long long)H * Wf, s),
+                   "cic_forward");
+}
+
+fdc_status fdc_cic_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX, fdc_c64 *gK,
+                            int B, int C, int S, int H, int Wf, hipStream_t s) {
+  if (fdc_status st = check_cic_dims(B, C, S, H, Wf)) return st;
+  if (!gY || (gX && !K) || (gK && !X)) return fail(FDC_EINVAL, "NULL tensor");
+  const long long P = (long long)H * Wf;
+  if (gX) {
+    if (fdc_status st = check_hip(fdc::launch_cic_bwd_gx(reinterpret_cast<const float2 *>(gY),
+                                                         reinterpret_cast<const float2 *>(K),
+                                                         reinterpret_cast<float2 *>(gX), B, C, S, P, s),
+                                  "cic_backward gX"))
+      return st;
+  }
+  if (gK) {
+    return check_hip(fdc::launch_cic_bwd_gk(reinterpret_cast<const float2 *>(gY), reinterpret_cast<const float2 *>(X),
+                                            reinterpret_cast<float2 *>(gK), B, C, S, P, s),
+                     "cic_backward gK");
+  }
+  return FDC_OK;
+}
+
+static fdc_status check_fdp(int64_t count, int H, int W, int Mh, int Mw) {
+  if (count < 1) return fail(FDC_EINVAL, "count must be >= 1");
+  if (!even_pos(H) || !even_pos(W) || !even_pos(Mh) || !even_pos(Mw))
+    return fail(FDC_EINVAL, "FDP sizes must be positive and even (%d x %d -> %d x %d)", H, W, Mh, Mw);
+  if (Mh > H || Mw > W) return fail(FDC_EINVAL, "FDP output %d x %d larger than input %d x %d", Mh, Mw, H, W);
+  return FDC_OK;
+}
+
+fdc_status fdp_forward(const fdc_c64 *X, fdc_c64 *Y, int64_t count, int H, int W, int Mh, int Mw, hipStream_t s) {
+  if (fdc_status st = check_fdp(count, H, W, Mh, Mw)) return st;
+  if (!X || !Y) return fail(FDC_EINVAL, "NULL tensor");
+  return check_hip(fdc::launch_fdp_gather(reinterpret_cast<const float2 *>(X), reinterpret_cast<float2 *>(Y), count,
+                                          H, W / 2 + 1, Mh, Mw / 2 + 1, s),
+                   "fdp_forward");
+}
+
+fdc_status fdp_backward(const fdc_c64 *gY, fdc_c64 *gX, int64_t count, int H, int W, int Mh, int Mw,
+                        hipStream_t s) {
+  if (fdc_status st = check_fdp(count, H, W, Mh, Mw)) return st;
+  if (!gY || !gX) return fail(FDC_EINVAL, "NULL tensor");
+  return check_hip(fdc::launch_fdp_scatter(reinterpret_cast<const float2 *>(gY), reinterpret_cast<float2 *>(gX),
+                                           count, H, W / 2 + 1, Mh, Mw / 2 + 1, s),
+                   "fdp_backward");
+}
+
+// ---------------------------------------------------------------------------
+// layer plans
+// ---------------------------------------------------------------------------
+static fdc_status check_layer_plan(const fdc_layer_plan *p, int kind) {
+  if (p == nullptr || p->magic != kLayerMagic) return fail(FDC_EINVAL, "invalid or destroyed layer plan");
+  if (p->kind != kind) return fail(FDC_EINVAL, "layer plan is of the other layer kind");
+  return FDC_OK;
+}
+
+static int artifact_out(int m, int artifact, int kn) { return artifact == FDC_ARTIFACT_CROP ? m - kn + 1 : m; }
+
+fdc_status fdc_cic_layer_plan_create(fdc_layer_plan **plan, int B, int C, int S, int N, int M, int artifact,
+                                     int kernel_n) {
+  if (plan == nullptr) return fail(FDC_EINVAL, "plan out-pointer is NULL");
+  *plan = nullptr;
+  if (B < 1 || C < 1 || S < 1) return fail(FDC_EINVAL, "B, C, S must be >= 1 (B=%d C=%d S=%d)", B, C, S);
+  if (S % C) return fail(FDC_EINVAL, "CIC needs S mod C == 0 (S=%d C=%d)", S, C);
+  if (!even_pos(N) || !even_pos(M)) return fail(FDC_EINVAL, "N and M must be positive and even (N=%d M=%d)", N, M);
+  if (M > N) return fail(FDC_EINVAL, "FDP output M=%d larger than N=%d", M, N);
+  if (artifact < FDC_ARTIFACT_NONE || artifact > FDC_ARTIFACT_ROLL) return fail(FDC_EINVAL, "bad artifact mode");
+  if (artifact != FDC_ARTIFACT_NONE && (kernel_n < 1 || kernel_n > M))
+    return fail(FDC_EINVAL, "kernel_n must be in [1, M] for crop/roll (got %d)", kernel_n);
+  if (!fdc::cic_pair_supported(N, M))
+    return fail(FDC_EUNSUPPORTED, "layer size %d -> %d not supported (N in the supported set, M in {N, N/2, N/4})",
+                N, M);
+  auto *p = new (std::nothrow) fdc_layer_plan{};
+  if (p == nullptr) return fail(FDC_EINVAL, "out of host memory");
+  p->magic = kLayerMagic;
+  p->kind = 0;
+  p->B = B, p->C = C, p->S = S, p->N = N, p->M = M;
+  p->artifact = artifact;
+  p->kn = artifact == FDC_ARTIFACT_NONE ? 1 : kernel_n;
+  p->out = artifact_out(M, artifact, p->kn);
+  const size_t L = (size_t)M / 2 + 1;
+  const size_t c64 = sizeof(fdc_c64);
+  p->fwd_ws = ((size_t)B * C * N * L + (size_t)B * S * M * L) * c64;  // T, U
+  p->saved = (size_t)B * C * M * L * c64;                            // pooled input spectrum
+  p->bwd_ws = ((size_t)B * S * M * L + (size_t)B * C * N * L) * c64;  // Tg, V
+  *plan = p;
+  return FDC_OK;
+}
+
+fdc_status fdc_layer_plan_destroy(fdc_layer_plan *plan) {
+  if (plan == nullptr) return FDC_OK;
+  if (plan->magic != kLayerMagic) return fail(FDC_EINVAL, "invalid or destroyed layer plan");
+  plan->magic = 0;
+  delete plan;
+  return FDC_OK;
+}
+
+fdc_status fdc_layer_workspace_size(const fdc_layer_plan *p, size_t *fwd_ws, size_t *saved, size_t *bwd_ws) {
+  if (p == nullptr || p->magic != kLayerMagic) return fail(FDC_EINVAL, "invalid or destroyed layer plan");
+  if (fwd_ws) *fwd_ws = p->fwd_ws;
+  if (saved) *saved = p->saved;
+  if (bwd_ws) *bwd_ws = p->bwd_ws;
+  return FDC_OK;
+}
+
+fdc_status fdc_layer_output_size(const fdc_layer_plan *p, int *out_size) {
+  if (p == nullptr || p->magic != kLayerMagic) return fail(FDC_EINVAL, "invalid or destroyed layer plan");
+  if (out_size == nullptr) return fail(FDC_EINVAL, "out_size is NULL");
+  *out_size = p->out;
+  return FDC_OK;
+}
+
+static ImgView artifact_view(const fdc_layer_plan *p) {
+  switch (p->artifact) {
+    case FDC_ARTIFACT_CROP: return ImgView{1, p->kn - 1, p->M, p->out};
+    case FDC_ARTIFACT_ROLL: return ImgView{2, (p->kn - 1) / 2, p->M, p->M};
+    default: return ImgView{0, 0, p->M, p->M};
+  }
+}
+
+fdc_status fdc_cic_layer_forward(const fdc_layer_plan *p, const float *x, const fdc_c64 *K, float *y, void *saved,
+                                 void *ws, size_t ws_bytes, hipStream_t s) {
+  if (fdc_status st = check_layer_plan(p, 0)) return st;
+  if (!x || !K || !y) return fail(FDC_EINVAL, "NULL tensor");
+  if (fdc_status st = check_ws(ws, ws_bytes, p->fwd_ws)) return st;
+  const int B = p->B, C = p->C, S = p->S, N = p->N, M = p->M, L = M / 2 + 1;
+  auto *T = reinterpret_cast<float2 *>(ws);
+  auto *U = T + (size_t)B * C * N * L;
+  ImgView id{0, 0, N, N};
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(N, x, T, (long long)B * C, N, id, (long long)N * N, L, L,
+                                                    (long long)N * L, 1.f, 1.f, s), "layer forward rows"))
+    return st;
+  if (fdc_status st = check_hip(fdc::launch_col_fwd_cic(N, M, T, reinterpret_cast<const float2 *>(K), U,
+                                                        reinterpret_cast<float2 *>(saved), B, C, S, s),
+                                "layer forward columns"))
+    return st;
+  return check_hip(fdc::launch_row_c2r(M, U, y, (long long)B * S, M, L, L, (long long)M * L,
+                                       1.f / ((float)M * (float)M), 1.f, artifact_view(p),
+                                       (long long)p->out * p->out, s),
+                   "layer forward inverse rows");
+}
+
+fdc_status fdc_cic_layer_backward(const fdc_layer_plan *p, const float *gy, const void *saved, const fdc_c64 *K,
+                                  float *gx, fdc_c64 *gK, void *ws, size_t ws_bytes, hipStream_t s) {
+  if (fdc_status st = check_layer_plan(p, 0)) return st;
+  if (!gy) return fail(FDC_EINVAL, "gy is NULL");
+  if (gK && !saved) return fail(FDC_EINVAL, "saved is NULL but gK was requested");
+  if (gx && !K) return fail(FDC_EINVAL, "K is NULL but gx was requested");
+  if (!gx && !gK) return FDC_OK;
+  if (fdc_status st = check_ws(ws, ws_bytes, p->bwd_ws)) return st;
+  const int B = p->B, C = p->C, S = p->S, N = p->N, M = p->M, L = M / 2 + 1;
+  auto *Tg = reinterpret_cast<float2 *>(ws);
+  auto *V = Tg + (size_t)B * S * M * L;
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(M, gy, Tg, (long long)B * S, M, artifact_view(p),
+                                                    (long long)p->out * p->out, L, L, (long long)M * L,
+                                                    1.f / ((float)M * (float)M), 2.f, s),
+                                "layer backward rows"))
+    return st;
+  if (gK) {
+    auto *gk = reinterpret_cast<float2 *>(gK);
+    if (fdc_status st = check_hip(fdc::launch_col_bwd_gk(N, M, Tg, reinterpret_cast<const float2 *>(saved), gk, B,
+                                                         C, S, s), "layer backward dK"))
+      return st;
+    if (fdc_status st = check_hip(fdc::launch_gk_zero_dropped(gk, S, N, M, s), "layer backward dK zero fill"))
+      return st;
+  }
+  if (gx) {
+    if (fdc_status st = check_hip(fdc::launch_col_bwd_gx(N, M, Tg, reinterpret_cast<const float2 *>(K), V, B, C, S,
+                                                         s), "layer backward dx columns"))
+      return st;
+    ImgView id{0, 0, N, N};
+    return check_hip(fdc::launch_row_c2r(N, V, gx, (long long)B * C, N, L, L, (long long)N * L, 1.f, 0.5f, id,
+                                         (long long)N * N, s),
+                     "layer backward dx rows");
+  }
+  return FDC_OK;
+}
+
+fdc_status fdc_full_layer_plan_create(fdc_layer_plan **plan, int B, int Cin, int Cout, int P, int kernel_n,
+                                      int artifact) {
+  if (plan == nullptr) return fail(FDC_EINVAL, "plan out-pointer is NULL");
+  *plan = nullptr;
+  (void)B, (void)Cin, (void)Cout, (void)P, (void)kernel_n, (void)artifact;
+  return fail(FDC_EUNSUPPORTED, "Full FDC is not built yet");
+}
+
+fdc_status fdc_full_forward(const fdc_layer_plan *p, const float *, const float *, float *, void *, void *, size_t,
+                            hipStream_t) {
+  return check_layer_plan(p, 1);
+}
+
+fdc_status fdc_full_backward(const fdc_layer_plan *p, const float *, const void *, const float *, float *, float *,
+                             void *, size_t, hipStream_t) {
+  return check_layer_plan(p, 1);
+}
+
+// ---------------------------------------------------------------------------
+// kernel timing
+// ---------------------------------------------------------------------------
+fdc_status fdc_kernel_timing_enable(int max_launches) {
+  if (max_launches < 1) return fail(FDC_EINVAL, "max_launches must be >= 1");
+  Timing &t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  timing_release(t);
+  t.start.resize(max_launches);
+  t.stop.resize(max_launches);
+  t.names.assign(max_launches, nullptr);
+  for (int i = 0; i < max_launches; ++i) {
+    if (hipEventCreate(&t.start[i]) != hipSuccess || hipEventCreate(&t.stop[i]) != hipSuccess) {
+      t.start.resize(i);
+      t.stop.resize(i);
+      timing_release(t);
+      return fail(FDC_EHIP, "hipEventCreate failed");
+    }
+  }
+  t.max = max_launches;
+  t.used = 0;
+  t.enabled = true;
+  return FDC_OK;
+}
+
+fdc_status fdc_kernel_timing_disable(void) {
+  Timing &t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  t.enabled = false;
+  return FDC_OK;
+}
+
+fdc_status fdc_kernel_timing_report(char *buf, size_t buf_bytes) {
+  if (buf == nullptr || buf_bytes == 0) return fail(FDC_EINVAL, "buffer is NULL or empty");
+  Timing &t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  std::map<std::string, std::pair<int, double>> acc;
+  for (int i = 0; i < t.used; ++i) {
+    if (hipEventSynchronize(t.stop[i]) != hipSuccess) return fail(FDC_EHIP, "hipEventSynchronize failed");
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, t.start[i], t.stop[i]) != hipSuccess)
+      return fail(FDC_EHIP, "hipEventElapsedTime failed");
+    auto &e = acc[t.names[i]];
+    e.first += 1;
+    e.second += ms;
+  }
+  std::string out;
+  for (auto &kv : acc) {
+    char line[256];
+    snprintf(line, sizeof line, "%s %d %.6f\n", kv.first.c_str(), kv.second.first, kv.second.second);
+    out += line;
+  }
+  if (out.size() + 1 > buf_bytes) return fail(FDC_EINVAL, "report needs %zu bytes", out.size() + 1);
+  memcpy(buf, out.c_str(), out.size() + 1);
+  return FDC_OK;
+}
+
+}  // extern "C"

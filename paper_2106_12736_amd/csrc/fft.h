@@ -1,0 +1,324 @@
+// Device FFT building blocks for gfx950 (wave64, 160 KB LDS per CU).
+//
+// The transforms of section 2.4.1.1 (RFFT / IRFFT) are computed as batched
+// Stockham FFTs.  One sequence of length N is owned by TPS threads; thread t
+// holds the E = N / TPS elements t, t + TPS, t + 2 TPS, ... in registers on
+// entry and on exit ("comb" layout), so a kernel can load the input with
+// coalesced global reads, run the transform, and apply its epilogue (pooling
+// crop, CIC product, weights, stores) straight from registers.  Between
+// Stockham passes the data goes through LDS once per pass; radices are large
+// (up to 32, computed in registers) so that N <= 1024 needs at most two
+// passes, i.e. a single LDS exchange.
+//
+// Twiddle factors are evaluated at compile time in double precision with the
+// exponent reduced as an exact integer (k mod n) and rounded to float once.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <type_traits>
+
+namespace fdc {
+
+// ---------------------------------------------------------------------------
+// complex helpers (float2 = {re, im})
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
+__device__ __forceinline__ float2 csub(float2 a, float2 b) { return make_float2(a.x - b.x, a.y - b.y); }
+__device__ __forceinline__ float2 cmul(float2 a, float2 b) {
+  return make_float2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
+}
+// a * conj(b)
+__device__ __forceinline__ float2 cmulc(float2 a, float2 b) {
+  return make_float2(a.x * b.x + a.y * b.y, a.y * b.x - a.x * b.y);
+}
+__device__ __forceinline__ float2 cscale(float2 a, float s) { return make_float2(a.x * s, a.y * s); }
+__device__ __forceinline__ float2 cconj(float2 a) { return make_float2(a.x, -a.y); }
+// a + b * conj(c)
+__device__ __forceinline__ float2 cfmac(float2 a, float2 b, float2 c) {
+  return make_float2(a.x + b.x * c.x + b.y * c.y, a.y + b.y * c.x - b.x * c.y);
+}
+
+// ---------------------------------------------------------------------------
+// compile-time trigonometry: cos / sin of 2 pi k / n in double precision
+// ---------------------------------------------------------------------------
+constexpr double kPi = 3.14159265358979323846264338327950288;
+
+constexpr double ct_reduce(long long k, long long n) {
+  long long r = k % n;
+  if (r < 0) r += n;
+  if (2 * r > n) r -= n;  // angle in (-pi, pi]
+  return 2.0 * kPi * static_cast<double>(r) / static_cast<double>(n);
+}
+constexpr double ct_sin_x(double x) {
+  double term = x, sum = x;
+  for (int i = 1; i < 24; ++i) {
+    term *= -x * x / static_cast<double>((2 * i) * (2 * i + 1));
+    sum += term;
+  }
+  return sum;
+}
+constexpr double ct_cos_x(double x) {
+  double term = 1.0, sum = 1.0;
+  for (int i = 1; i < 24; ++i) {
+    term *= -x * x / static_cast<double>((2 * i - 1) * (2 * i));
+    sum += term;
+  }
+  return sum;
+}
+constexpr double ct_cos2pi(long long k, long long n) { return ct_cos_x(ct_reduce(k, n)); }
+constexpr double ct_sin2pi(long long k, long long n) { return ct_sin_x(ct_reduce(k, n)); }
+
+// Table of exp(-2 pi i t / N), t < N, as interleaved floats.
+template <int N>
+struct TwiddleTable {
+  float v[2 * N];
+  constexpr TwiddleTable() : v() {
+    for (int t = 0; t < N; ++t) {
+      v[2 * t] = static_cast<float>(ct_cos2pi(t, N));
+      v[2 * t + 1] = static_cast<float>(-ct_sin2pi(t, N));
+    }
+  }
+};
+
+template <int N>
+__device__ const TwiddleTable<N> g_twiddle = TwiddleTable<N>();
+
+template <int N>
+__device__ __forceinline__ float2 twiddle_load(int idx) {
+  return *reinterpret_cast<const float2 *>(&g_twiddle<N>.v[2 * idx]);
+}
+
+// ---------------------------------------------------------------------------
+// compile-time loops
+// ---------------------------------------------------------------------------
+template <int I, int END, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+  if constexpr (I < END) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, END>(f);
+  }
+}
+
+// Multiply by the constant exp(DIR * 2 pi i K / N); DIR = -1 forward, +1 inverse.
+template <int DIR, int N, int K>
+__device__ __forceinline__ float2 rot_const(float2 v) {
+  constexpr int k = ((K % N) + N) % N;
+  if constexpr (k == 0) {
+    return v;
+  } else if constexpr (2 * k == N) {
+    return make_float2(-v.x, -v.y);
+  } else if constexpr (4 * k == N) {
+    return DIR < 0 ? make_float2(v.y, -v.x) : make_float2(-v.y, v.x);
+  } else if constexpr (4 * k == 3 * N) {
+    return DIR < 0 ? make_float2(-v.y, v.x) : make_float2(v.y, -v.x);
+  } else {
+    constexpr float c = static_cast<float>(ct_cos2pi(k, N));
+    constexpr float s = static_cast<float>(DIR * ct_sin2pi(k, N));
+    return make_float2(v.x * c - v.y * s, v.x * s + v.y * c);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// in-register DFTs of small radix, natural order in and out
+// ---------------------------------------------------------------------------
+template <int R, int DIR>
+struct Dft;
+
+template <int DIR>
+struct Dft<1, DIR> {
+  __device__ __forceinline__ static void run(float2 *) {}
+};
+
+template <int DIR>
+struct Dft<2, DIR> {
+  __device__ __forceinline__ static void run(float2 *v) {
+    float2 a = v[0];
+    v[0] = cadd(a, v[1]);
+    v[1] = csub(a, v[1]);
+  }
+};
+
+template <int DIR>
+struct Dft<4, DIR> {
+  __device__ __forceinline__ static void run(float2 *v) {
+    float2 s02 = cadd(v[0], v[2]), d02 = csub(v[0], v[2]);
+    float2 s13 = cadd(v[1], v[3]), d13 = rot_const<DIR, 4, 1>(csub(v[1], v[3]));
+    v[0] = cadd(s02, s13);
+    v[2] = csub(s02, s13);
+    v[1] = cadd(d02, d13);
+    v[3] = csub(d02, d13);
+  }
+};
+
+// Seven-point DFT by conjugate-symmetric pairs (n, 7-n).
+template <int DIR>
+struct Dft<7, DIR> {
+  __device__ __forceinline__ static void run(float2 *v) {
+    const float2 x0 = v[0];
+    float2 s[4], d[4];
+    s[1] = cadd(v[1], v[6]); d[1] = csub(v[1], v[6]);
+    s[2] = cadd(v[2], v[5]); d[2] = csub(v[2], v[5]);
+    s[3] = cadd(v[3], v[4]); d[3] = csub(v[3], v[4]);
+    v[0] = cadd(x0, cadd(s[1], cadd(s[2], s[3])));
+    static_for<1, 4>([&](auto kk) {
+      constexpr int k = decltype(kk)::value;
+      float2 a = x0, b = make_float2(0.f, 0.f);
+      static_for<1, 4>([&](auto nn) {
+        constexpr int n = decltype(nn)::value;
+        constexpr float c = static_cast<float>(ct_cos2pi(n * k, 7));
+        constexpr float sn = static_cast<float>(ct_sin2pi(n * k, 7));
+        a = make_float2(a.x + c * s[n].x, a.y + c * s[n].y);
+        b = make_float2(b.x + sn * d[n].x, b.y + sn * d[n].y);
+      });
+      // X[k] = a + DIR i b, X[7-k] = a - DIR i b
+      float2 ib = DIR < 0 ? make_float2(b.y, -b.x) : make_float2(-b.y, b.x);
+      v[k] = cadd(a, ib);
+      v[7 - k] = csub(a, ib);
+    });
+  }
+};
+
+// Composite radix R = R1 * R2 by one decimation-in-time split:
+// X[k1 + R1 k2] = sum_{n2} W_{R2}^{n2 k2} W_R^{n2 k1} sum_{n1} x[R2 n1 + n2] W_{R1}^{n1 k1}.
+template <int R>
+struct SplitOf {
+  static constexpr int R1 = (R % 4 == 0 && R != 8) ? 4 : 2;
+  static constexpr int R2 = R / R1;
+};
+
+template <int R, int DIR>
+struct Dft {
+  static_assert(R == 8 || R == 16 || R == 32 || R == 64, "unsupported in-register radix");
+  __device__ __forceinline__ static void run(float2 *v) {
+    constexpr int R1 = SplitOf<R>::R1, R2 = SplitOf<R>::R2;
+    float2 t[R];
+    static_for<0, R2>([&](auto n2c) {
+      constexpr int n2 = decltype(n2c)::value;
+      float2 a[R1];
+      static_for<0, R1>([&](auto n1c) { a[decltype(n1c)::value] = v[R2 * decltype(n1c)::value + n2]; });
+      Dft<R1, DIR>::run(a);
+      static_for<0, R1>([&](auto k1c) {
+        constexpr int k1 = decltype(k1c)::value;
+        t[n2 * R1 + k1] = rot_const<DIR, R, n2 * k1>(a[k1]);
+      });
+    });
+    static_for<0, R1>([&](auto k1c) {
+      constexpr int k1 = decltype(k1c)::value;
+      float2 b[R2];
+      static_for<0, R2>([&](auto n2c) { b[decltype(n2c)::value] = t[decltype(n2c)::value * R1 + k1]; });
+      Dft<R2, DIR>::run(b);
+      static_for<0, R2>([&](auto k2c) { v[k1 + R1 * decltype(k2c)::value] = b[decltype(k2c)::value]; });
+    });
+  }
+};
+
+// ---------------------------------------------------------------------------
+// per-length Stockham plans: radix of each pass, threads per sequence
+// ---------------------------------------------------------------------------
+template <int N>
+struct FftCfg;
+#define FDC_FFT_CFG(N_, TPS_, R0_, R1_, R2_)                 \
+  template <>                                               \
+  struct FftCfg<N_> {                                       \
+    static constexpr int N = N_;                            \
+    static constexpr int TPS = TPS_;                        \
+    static constexpr int E = N_ / TPS_;                     \
+    static constexpr int R[3] = {R0_, R1_, R2_};            \
+    static constexpr int P = (R1_ == 1) ? 1 : (R2_ == 1 ? 2 : 3); \
+  };
+//            N   TPS  radices
+FDC_FFT_CFG(2, 1, 2, 1, 1)
+FDC_FFT_CFG(4, 1, 4, 1, 1)
+FDC_FFT_CFG(8, 1, 8, 1, 1)
+FDC_FFT_CFG(16, 1, 16, 1, 1)
+FDC_FFT_CFG(32, 4, 8, 4, 1)
+FDC_FFT_CFG(64, 8, 8, 8, 1)
+FDC_FFT_CFG(128, 8, 16, 8, 1)
+FDC_FFT_CFG(256, 16, 16, 16, 1)
+FDC_FFT_CFG(512, 16, 16, 32, 1)
+FDC_FFT_CFG(1024, 32, 32, 32, 1)
+FDC_FFT_CFG(224, 4, 7, 8, 4)
+#undef FDC_FFT_CFG
+
+template <int N>
+constexpr int stockham_ns(int p) {  // product of the radices before pass p
+  int ns = 1;
+  for (int i = 0; i < p; ++i) ns *= FftCfg<N>::R[i];
+  return ns;
+}
+
+// LDS addressing: an XOR swizzle inside each aligned block of 32 complex
+// values (bits 5..9 of the index flip bits 0..4).  Contiguous accesses stay
+// conflict-free and the power-of-two strides of the Stockham writes land in
+// different banks.  It is a bijection on every 32-aligned block, so a buffer
+// of lds_size(n) complex values holds indices [0, n).
+__device__ __forceinline__ int lds_phys(int i) { return i ^ ((i >> 5) & 31); }
+__host__ __device__ constexpr int lds_size(int n) { return (n + 31) & ~31; }
+
+// Transform one sequence.  Thread t (0 <= t < TPS) holds v[m] = element t + TPS*m
+// on entry and exit.  Element e of the sequence lives in LDS at
+// lds[lds_phys(base + e * es)].  Every thread of the workgroup must call this
+// (it contains workgroup barriers).  With LEAD_SYNC the first LDS write waits
+// for every thread's earlier use of the LDS.
+template <int N, int DIR, bool LEAD_SYNC = true>
+__device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2 *lds, int base, int es) {
+  using C = FftCfg<N>;
+  constexpr int E = C::E;
+  constexpr int TPS = C::TPS;
+  static_for<0, C::P>([&](auto pc) {
+    constexpr int p = decltype(pc)::value;
+    constexpr int R = C::R[p];
+    constexpr int BPT = E / R;       // butterflies per thread in this pass
+    constexpr int NS = stockham_ns<N>(p);
+    constexpr int NR = N / R;
+    static_assert(BPT * R == E && BPT * TPS == NR, "radix plan does not fit the thread layout");
+    float2 a[E];
+    if constexpr (p == 0) {
+#pragma unroll
+      for (int m = 0; m < E; ++m) a[m] = v[m];
+    } else {
+#pragma unroll
+      for (int q = 0; q < BPT; ++q) {
+        const int j = t + TPS * q;
+        const int k = j % NS;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          float2 x = lds[lds_phys(base + (j + r * NR) * es)];
+          if (r > 0) {
+            float2 w = twiddle_load<N>(r * k * (N / (NS * R)));
+            if (DIR > 0) w.y = -w.y;
+            x = cmul(x, w);
+          }
+          a[q + BPT * r] = x;
+        }
+      }
+    }
+    // butterflies: a[q + BPT r], r < R, belong to butterfly q
+#pragma unroll
+    for (int q = 0; q < BPT; ++q) {
+      float2 b[R];
+#pragma unroll
+      for (int r = 0; r < R; ++r) b[r] = a[q + BPT * r];
+      Dft<R, DIR>::run(b);
+#pragma unroll
+      for (int r = 0; r < R; ++r) a[q + BPT * r] = b[r];
+    }
+    if constexpr (p == C::P - 1) {
+#pragma unroll
+      for (int m = 0; m < E; ++m) v[m] = a[m];
+    } else {
+      if (p > 0 || LEAD_SYNC) __syncthreads();
+#pragma unroll
+      for (int q = 0; q < BPT; ++q) {
+        const int j = t + TPS * q;
+        const int jo = (j / NS) * NS * R + (j % NS);
+#pragma unroll
+        for (int r = 0; r < R; ++r) lds[lds_phys(base + (jo + r * NS) * es)] = a[q + BPT * r];
+      }
+      __syncthreads();
+    }
+  });
+}
+
+}  // namespace fdc

@@ -1,0 +1,72 @@
+// Internal interface between the C ABI (api.cpp) and the kernel launchers
+// (kernels.hip, full_fdc.hip).  Not installed; not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace fdc {
+
+// How a logical rows x cols image maps onto a stored image (row stride `cols_stored`).
+//   mode 0: identity.
+//   mode 1: artifact crop -- logical (r, w) is stored at (r - shift, w - shift) when
+//           both are >= 0, and is absent (zero on load, dropped on store) otherwise.
+//   mode 2: artifact roll -- logical (r, w) is stored at ((r - shift) mod rows,
+//           (w - shift) mod cols).
+struct ImgView {
+  int mode;
+  int shift;
+  int rows;         // logical rows
+  int cols_stored;  // row stride of the stored image
+};
+
+bool size_supported(int n);
+
+// Kernel timing hooks (no-ops unless enabled through the ABI).
+void timing_before(const char *name, hipStream_t s);
+void timing_after(const char *name, hipStream_t s);
+
+// Row transforms of real rows of length n (n in the supported set), processed in pairs.
+// rows_per_plane must be even.  Output/input bins beyond L are not written / read as zero.
+//   r2c: out[plane][row][l] = w_l * sum_w x[plane][row][w] e^{-2 pi i w l / n},  l < L
+//   c2r: y[plane][row][w] = sum_{l<=n/2} c_l Re(w_l in[plane][row][l] e^{+2 pi i w l / n}),
+//        with the imaginary part of bins 0 and n/2 discarded (real-part semantics)
+// where w_l = alpha at l = 0 and l = n/2 and alpha * beta otherwise.
+hipError_t launch_row_r2c(int n, const float *x, float2 *out, long long planes, int rows_per_plane,
+                          ImgView in_view, long long in_plane_stride, int L, long long out_row_stride,
+                          long long out_plane_stride, float alpha, float beta, hipStream_t s);
+hipError_t launch_row_c2r(int n, const float2 *in, float *y, long long planes, int rows_per_plane, int L,
+                          long long in_row_stride, long long in_plane_stride, float alpha, float beta,
+                          ImgView out_view, long long out_plane_stride, hipStream_t s);
+
+// Column DFTs of length n over `L` columns of row-major [planes][n][L] complex data (in place allowed).
+hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long long planes, int L,
+                          long long in_plane_stride, long long out_plane_stride, hipStream_t s);
+
+// Fused CIC + FDP column kernels (square n x n images pooled to m x m; L = m/2 + 1).
+//   fwd:   T [B][C][n][L] -> U [B][S][m][L], Xh [B][C][m][L] (nullable)
+//   bwd_gk: Tg [B][S][m][L], Xh -> gK [S][n][n/2+1] at the kept bins
+//   bwd_gx: Tg, K -> V [B][C][n][L]
+bool cic_pair_supported(int n, int m);
+hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, float2 *U, float2 *Xh, int B,
+                              int C, int S, hipStream_t s);
+hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, float2 *gK, int B, int C,
+                             int S, hipStream_t s);
+hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, float2 *V, int B, int C, int S,
+                             hipStream_t s);
+hipError_t launch_gk_zero_dropped(float2 *gK, int S, int n, int m, hipStream_t s);
+
+// Spectral CIC and FDP.
+hipError_t launch_cic_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, long long P,
+                          hipStream_t s);
+hipError_t launch_cic_bwd_gx(const float2 *gY, const float2 *K, float2 *gX, int B, int C, int S, long long P,
+                             hipStream_t s);
+hipError_t launch_cic_bwd_gk(const float2 *gY, const float2 *X, float2 *gK, int B, int C, int S, long long P,
+                             hipStream_t s);
+hipError_t launch_fdp_gather(const float2 *X, float2 *Y, long long count, int H, int Wf, int Mh, int Mwf,
+                             hipStream_t s);
+hipError_t launch_fdp_scatter(const float2 *gY, float2 *gX, long long count, int H, int Wf, int Mh, int Mwf,
+                              hipStream_t s);
+
+}  // namespace fdc

@@ -1,0 +1,683 @@
+// HIP kernels of the CIC + FDP layer path for gfx950, and their launchers.
+//
+// Layer forward (section 2.4.1, Algorithm 1 inside Algorithm 2, FDP of 2.4.2):
+//   k_row_r2c     real rows of x -> half-spectrum rows, only the m/2+1 columns FDP keeps
+//   k_col_fwd_cic column DFT (n) -> keep the m rows FDP keeps -> save them -> for each of
+//                 the J kernels: CIC product (Eq. 5) -> inverse column DFT (m)
+//   k_row_c2r     inverse real row DFT (m) with real-part semantics and 1/m^2
+// Layer backward:
+//   k_row_r2c     upstream gradient -> (c_l/m^2) weighted half spectrum
+//   k_col_bwd_gk  column DFT (m), dL/dK = sum_b G conj(Xhat), one workgroup per
+//                 (output channel, column tile) looping over the batch (fixed order)
+//   k_col_bwd_gx  column DFTs (m) of the J gradients, sum_j G conj(K), zero-padded
+//                 inverse column DFT (n)
+//   k_row_c2r     adjoint row transform (n)
+// Intermediates stay row-major [plane][row][column]; column kernels own CT adjacent
+// columns with the column index fastest across lanes, so every global access is a
+// run of CT consecutive complex values.
+#include "fft.h"
+#include "internal.h"
+
+#include <string>
+
+namespace fdc {
+
+// Blocks are dispatched round-robin over the 8 XCDs; renumber them so that
+// neighbouring tiles (which share cache lines) run on the same XCD and its L2.
+__device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
+  const int q = nblocks >> 3, rem = nblocks & 7;
+  const int x = bid & 7, i = bid >> 3;
+  return x * q + (x < rem ? x : rem) + i;
+}
+
+__device__ __forceinline__ long long view_index(const ImgView &v, int ncols, int r, int w) {
+  if (v.mode == 0) return (long long)r * v.cols_stored + w;
+  if (v.mode == 1) {
+    const int rr = r - v.shift, ww = w - v.shift;
+    return (rr < 0 || ww < 0) ? -1 : (long long)rr * v.cols_stored + ww;
+  }
+  int rr = r - v.shift, ww = w - v.shift;
+  rr += rr < 0 ? v.rows : 0;
+  ww += ww < 0 ? ncols : 0;
+  return (long long)rr * v.cols_stored + ww;
+}
+
+__device__ __forceinline__ float bin_weight(int l, int n, float alpha, float beta) {
+  return (l == 0 || 2 * l == n) ? alpha : alpha * beta;
+}
+
+extern __shared__ float2 g_lds[];
+
+// ---------------------------------------------------------------------------
+// row transforms
+// ---------------------------------------------------------------------------
+template <int N>
+constexpr int row_spw() {
+  constexpr int s = 128 / FftCfg<N>::TPS;
+  return s > 64 ? 64 : s;
+}
+
+template <int N, int SPW>
+__global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(
+    const float *__restrict__ x, float2 *__restrict__ out, long long npairs, int rows_per_plane, ImgView view,
+    long long in_plane_stride, int L, long long out_row_stride, long long out_plane_stride, float alpha,
+    float beta) {
+  using Cfg = FftCfg<N>;
+  constexpr int TPS = Cfg::TPS, E = Cfg::E;
+  float2 *lds = g_lds;
+  const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
+  long long pair = (long long)xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
+  const bool active = pair < npairs;
+  if (!active) pair = npairs - 1;
+  const long long row0 = 2 * pair;
+  const long long plane = row0 / rows_per_plane;
+  const int r0 = (int)(row0 - plane * rows_per_plane);
+  const float *xp = x + plane * in_plane_stride;
+
+  float2 v[E];
+#pragma unroll
+  for (int m = 0; m < E; ++m) {
+    const int w = t + TPS * m;
+    const long long ia = view_index(view, N, r0, w);
+    const long long ib = view_index(view, N, r0 + 1, w);
+    v[m] = make_float2(ia >= 0 ? xp[ia] : 0.f, ib >= 0 ? xp[ib] : 0.f);
+  }
+  fft_seq<N, -1>(v, t, lds, s * N, 1);
+  __syncthreads();
+#pragma unroll
+  for (int m = 0; m < E; ++m) lds[lds_phys(s * N + t + TPS * m)] = v[m];
+  __syncthreads();
+  if (!active) return;
+  float2 *oa = out + plane * out_plane_stride + (long long)r0 * out_row_stride;
+  float2 *ob = oa + out_row_stride;
+  for (int k = t; k < L; k += TPS) {
+    const float2 zk = lds[lds_phys(s * N + k)];
+    const float2 zn = lds[lds_phys(s * N + (k == 0 ? 0 : N - k))];
+    const float wgt = 0.5f * bin_weight(k, N, alpha, beta);
+    // two real rows packed as z = a + i b:  A = (Z[k] + conj Z[-k]) / 2,  B = (Z[k] - conj Z[-k]) / (2i)
+    oa[k] = make_float2((zk.x + zn.x) * wgt, (zk.y - zn.y) * wgt);
+    ob[k] = make_float2((zk.y + zn.y) * wgt, (zn.x - zk.x) * wgt);
+  }
+}
+
+template <int N, int SPW>
+__global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(
+    const float2 *__restrict__ in, float *__restrict__ y, long long npairs, int rows_per_plane, int L,
+    long long in_row_stride, long long in_plane_stride, float alpha, float beta, ImgView view,
+    long long out_plane_stride) {
+  using Cfg = FftCfg<N>;
+  constexpr int TPS = Cfg::TPS, E = Cfg::E;
+  float2 *lds = g_lds;
+  const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
+  long long pair = (long long)xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
+  const bool active = pair < npairs;
+  if (!active) pair = npairs - 1;
+  const long long row0 = 2 * pair;
+  const long long plane = row0 / rows_per_plane;
+  const int r0 = (int)(row0 - plane * rows_per_plane);
+  const float2 *ia = in + plane * in_plane_stride + (long long)r0 * in_row_stride;
+  const float2 *ib = ia + in_row_stride;
+
+  float2 v[E];
+#pragma unroll
+  for (int m = 0; m < E; ++m) {
+    const int k = t + TPS * m;
+    const bool upper = 2 * k > N;
+    const int kk = upper ? N - k : k;
+    float2 a = make_float2(0.f, 0.f), b = make_float2(0.f, 0.f);
+    if (kk < L) {
+      a = ia[kk];
+      b = ib[kk];
+    }
+    const bool edge = (kk == 0 || 2 * kk == N);
+    const float wgt = edge ? alpha : alpha * beta;
+    a = cscale(a, wgt);
+    b = cscale(b, wgt);
+    if (edge) {  // real-part semantics of the inverse at l = 0 and l = n/2
+      a.y = 0.f;
+      b.y = 0.f;
+    }
+    if (upper) {  // Hermitian extension of each real row's half spectrum
+      a.y = -a.y;
+      b.y = -b.y;
+    }
+    v[m] = make_float2(a.x - b.y, a.y + b.x);  // A + i B
+  }
+  fft_seq<N, +1>(v, t, lds, s * N, 1);
+  if (!active) return;
+  float *yp = y + plane * out_plane_stride;
+#pragma unroll
+  for (int m = 0; m < E; ++m) {
+    const int w = t + TPS * m;
+    const long long oa = view_index(view, N, r0, w);
+    const long long ob = view_index(view, N, r0 + 1, w);
+    if (oa >= 0) yp[oa] = v[m].x;
+    if (ob >= 0) yp[ob] = v[m].y;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// column transforms
+// ---------------------------------------------------------------------------
+template <int N>
+constexpr int col_ct() {
+  return N >= 512 ? 8 : 16;
+}
+
+template <int N, int CT, int DIR>
+__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft(const float2 *in, float2 *out, int L, int tiles,
+                                                               long long in_plane_stride,
+                                                               long long out_plane_stride) {
+  using Cfg = FftCfg<N>;
+  constexpr int TPS = Cfg::TPS, E = Cfg::E;
+  float2 *lds = g_lds;
+  const int s = threadIdx.x % CT, t = threadIdx.x / CT;
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const long long plane = bid / tiles;
+  const int l = (bid % tiles) * CT + s;
+  const bool ok = l < L;
+  const float2 *ip = in + plane * in_plane_stride + l;
+  float2 v[E];
+#pragma unroll
+  for (int m = 0; m < E; ++m) v[m] = ok ? ip[(long long)(t + TPS * m) * L] : make_float2(0.f, 0.f);
+  fft_seq<N, DIR>(v, t, lds, s, CT);
+  if (!ok) return;
+  float2 *op = out + plane * out_plane_stride + l;
+#pragma unroll
+  for (int m = 0; m < E; ++m) op[(long long)(t + TPS * m) * L] = v[m];
+}
+
+// Row of the n-point spectrum that pooled row `mrow` (of m) comes from.
+template <int N, int M>
+__device__ __forceinline__ int kept_row(int mrow) {
+  return mrow < M / 2 ? mrow : mrow + (N - M);
+}
+
+template <int N, int M>
+constexpr int cic_jp() {
+  return FftCfg<N>::TPS / FftCfg<M>::TPS;
+}
+
+template <int N, int M, int CT>
+constexpr int cic_lds_elems() {
+  constexpr int a = N * CT, b = cic_jp<N, M>() * M * CT;
+  return lds_size(a > b ? a : b);
+}
+
+template <int N, int M, int CT>
+__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fwd_cic(const float2 *__restrict__ T,
+                                                                   const float2 *__restrict__ K,
+                                                                   float2 *__restrict__ U, float2 *__restrict__ Xh,
+                                                                   int C, int J, int tiles) {
+  using CN = FftCfg<N>;
+  using CM = FftCfg<M>;
+  constexpr int L = M / 2 + 1, NF = N / 2 + 1;
+  constexpr int TPSN = CN::TPS, TPSM = CM::TPS, JP = cic_jp<N, M>();
+  static_assert(JP * TPSM == TPSN, "thread layouts of the two transforms must nest");
+  float2 *lds = g_lds;
+  const int s = threadIdx.x % CT, t = threadIdx.x / CT;
+  const int tp = t % TPSM, js = t / TPSM;
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int bc = bid / tiles;
+  const int b = bc / C, c = bc - b * C;
+  const int l = (bid % tiles) * CT + s;
+  const bool ok = l < L;
+
+  // column DFT of length N
+  const float2 *tcol = T + (long long)bc * N * L + l;
+  float2 v[CN::E];
+#pragma unroll
+  for (int m = 0; m < CN::E; ++m) v[m] = ok ? tcol[(long long)(t + TPSN * m) * L] : make_float2(0.f, 0.f);
+  fft_seq<N, -1>(v, t, lds, s, CT);
+  __syncthreads();
+
+  // FDP: keep rows [0, M/2) and [N - M/2, N); save them for the backward pass
+  float2 *xh = (Xh != nullptr && ok) ? Xh + (long long)bc * M * L + l : nullptr;
+#pragma unroll
+  for (int m = 0; m < CN::E; ++m) {
+    const int k = t + TPSN * m;
+    if (k < M / 2 || k >= N - M / 2) {
+      const int mrow = k < M / 2 ? k : k - (N - M);
+      lds[lds_phys(s + mrow * CT)] = v[m];
+      if (xh) xh[(long long)mrow * L] = v[m];
+    }
+  }
+  __syncthreads();
+  float2 xr[CM::E];
+#pragma unroll
+  for (int m = 0; m < CM::E; ++m) xr[m] = lds[lds_phys(s + (tp + TPSM * m) * CT)];
+
+  // CIC (Eq. 5): J products per input channel, each followed by the inverse column DFT (M)
+  const long long out_plane0 = (long long)b * C * J;
+  for (int j0 = 0; j0 < J; j0 += JP) {
+    const int j = j0 + js;
+    const bool act = ok && j < J;
+    const int o = c * J + j;
+    const float2 *kcol = K + (long long)o * N * NF + l;
+    float2 z[CM::E];
+#pragma unroll
+    for (int m = 0; m < CM::E; ++m) {
+      const int mrow = tp + TPSM * m;
+      z[m] = act ? cmul(xr[m], kcol[(long long)kept_row<N, M>(mrow) * NF]) : make_float2(0.f, 0.f);
+    }
+    fft_seq<M, +1>(z, tp, lds, js * M * CT + s, CT);
+    if (act) {
+      float2 *ucol = U + (out_plane0 + o) * M * L + l;
+#pragma unroll
+      for (int m = 0; m < CM::E; ++m) ucol[(long long)(tp + TPSM * m) * L] = z[m];
+    }
+  }
+}
+
+template <int M, int CT>
+__global__ __launch_bounds__(CT *FftCfg<M>::TPS) void k_col_bwd_gk(const float2 *__restrict__ Tg,
+                                                                  const float2 *__restrict__ Xh,
+                                                                  float2 *__restrict__ gK, int B, int C, int J,
+                                                                  int N, int tiles) {
+  using CM = FftCfg<M>;
+  constexpr int L = M / 2 + 1, TPS = CM::TPS, E = CM::E;
+  float2 *lds = g_lds;
+  const int s = threadIdx.x % CT, t = threadIdx.x / CT;
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int o = bid / tiles;
+  const int c = o / J;
+  const int S = C * J;
+  const int l = (bid % tiles) * CT + s;
+  const bool ok = l < L;
+  float2 acc[E];
+#pragma unroll
+  for (int m = 0; m < E; ++m) acc[m] = make_float2(0.f, 0.f);
+  for (int b = 0; b < B; ++b) {
+    const float2 *gcol = Tg + ((long long)b * S + o) * M * L + l;
+    const float2 *xcol = Xh + ((long long)b * C + c) * M * L + l;
+    float2 v[E];
+#pragma unroll
+    for (int m = 0; m < E; ++m) v[m] = ok ? gcol[(long long)(t + TPS * m) * L] : make_float2(0.f, 0.f);
+    fft_seq<M, -1>(v, t, lds, s, CT);
+    if (ok) {
+#pragma unroll
+      for (int m = 0; m < E; ++m) acc[m] = cfmac(acc[m], v[m], xcol[(long long)(t + TPS * m) * L]);
+    }
+  }
+  if (!ok) return;
+  const int nf = N / 2 + 1;
+  float2 *kcol = gK + (long long)o * N * nf + l;
+#pragma unroll
+  for (int m = 0; m < E; ++m) {
+    const int mrow = t + TPS * m;
+    const int krow = mrow < M / 2 ? mrow : mrow + (N - M);
+    kcol[(long long)krow * nf] = acc[m];
+  }
+}
+
+template <int N, int M, int CT>
+__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 *__restrict__ Tg,
+                                                                  const float2 *__restrict__ K,
+                                                                  float2 *__restrict__ V, int C, int J, int tiles) {
+  using CN = FftCfg<N>;
+  using CM = FftCfg<M>;
+  constexpr int L = M / 2 + 1, NF = N / 2 + 1;
+  constexpr int TPSN = CN::TPS, TPSM = CM::TPS, JP = cic_jp<N, M>();
+  float2 *lds = g_lds;
+  const int s = threadIdx.x % CT, t = threadIdx.x / CT;
+  const int tp = t % TPSM, js = t / TPSM;
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int bc = bid / tiles;
+  const int b = bc / C, c = bc - b * C;
+  const int S = C * J;
+  const int l = (bid % tiles) * CT + s;
+  const bool ok = l < L;
+
+  float2 acc[CM::E];
+#pragma unroll
+  for (int m = 0; m < CM::E; ++m) acc[m] = make_float2(0.f, 0.f);
+  for (int j0 = 0; j0 < J; j0 += JP) {
+    const int j = j0 + js;
+    const bool act = ok && j < J;
+    const int o = c * J + j;
+    const float2 *gcol = Tg + ((long long)b * S + o) * M * L + l;
+    const float2 *kcol = K + (long long)o * N * NF + l;
+    float2 g[CM::E];
+#pragma unroll
+    for (int m = 0; m < CM::E; ++m) g[m] = act ? gcol[(long long)(tp + TPSM * m) * L] : make_float2(0.f, 0.f);
+    fft_seq<M, -1>(g, tp, lds, js * M * CT + s, CT);
+    if (act) {
+#pragma unroll
+      for (int m = 0; m < CM::E; ++m)
+        acc[m] = cfmac(acc[m], g[m], kcol[(long long)kept_row<N, M>(tp + TPSM * m) * NF]);
+    }
+  }
+  // sum the JP partial sums and scatter the pooled rows into the n-row column (FDP adjoint)
+  __syncthreads();
+#pragma unroll
+  for (int m = 0; m < CM::E; ++m) lds[lds_phys(js * M * CT + s + (tp + TPSM * m) * CT)] = acc[m];
+  __syncthreads();
+  float2 w[CN::E];
+#pragma unroll
+  for (int m = 0; m < CN::E; ++m) {
+    const int k = t + TPSN * m;
+    float2 sum = make_float2(0.f, 0.f);
+    if (k < M / 2 || k >= N - M / 2) {
+      const int mrow = k < M / 2 ? k : k - (N - M);
+#pragma unroll
+      for (int q = 0; q < JP; ++q) sum = cadd(sum, lds[lds_phys(q * M * CT + s + mrow * CT)]);
+    }
+    w[m] = sum;
+  }
+  fft_seq<N, +1>(w, t, lds, s, CT);
+  if (!ok) return;
+  float2 *vcol = V + (long long)bc * N * L + l;
+#pragma unroll
+  for (int m = 0; m < CN::E; ++m) vcol[(long long)(t + TPSN * m) * L] = w[m];
+}
+
+__global__ void k_gk_zero_dropped(float2 *gK, long long total, int N, int M) {
+  const int nf = N / 2 + 1, L = M / 2 + 1;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    const int l = (int)(i % nf);
+    const int k = (int)((i / nf) % N);
+    const bool kept = l < L && (k < M / 2 || k >= N - M / 2);
+    if (!kept) gK[i] = make_float2(0.f, 0.f);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// spectral CIC and FDP (standalone ops)
+// ---------------------------------------------------------------------------
+__global__ void k_cic_fwd(const float2 *__restrict__ X, const float2 *__restrict__ K, float2 *__restrict__ Y,
+                          int C, int J, long long P, long long total) {
+  const int S = C * J;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    const long long p = i % P, bo = i / P;
+    const int o = (int)(bo % S);
+    const long long b = bo / S;
+    Y[i] = cmul(X[(b * C + o / J) * P + p], K[(long long)o * P + p]);
+  }
+}
+
+__global__ void k_cic_bwd_gx(const float2 *__restrict__ gY, const float2 *__restrict__ K, float2 *__restrict__ gX,
+                             int C, int J, long long P, long long total) {
+  const int S = C * J;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    const long long p = i % P, bc = i / P;
+    const int c = (int)(bc % C);
+    const long long b = bc / C;
+    float2 acc = make_float2(0.f, 0.f);
+    for (int j = 0; j < J; ++j) {
+      const int o = c * J + j;
+      acc = cfmac(acc, gY[(b * S + o) * P + p], K[(long long)o * P + p]);
+    }
+    gX[i] = acc;
+  }
+}
+
+__global__ void k_cic_bwd_gk(const float2 *__restrict__ gY, const float2 *__restrict__ X, float2 *__restrict__ gK,
+                             int B, int C, int J, long long P, long long total) {
+  const int S = C * J;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    const long long p = i % P;
+    const int o = (int)(i / P);
+    const int c = o / J;
+    float2 acc = make_float2(0.f, 0.f);
+    for (int b = 0; b < B; ++b) acc = cfmac(acc, gY[((long long)b * S + o) * P + p], X[((long long)b * C + c) * P + p]);
+    gK[i] = acc;
+  }
+}
+
+__global__ void k_fdp_gather(const float2 *__restrict__ X, float2 *__restrict__ Y, long long total, int H, int Wf,
+                             int Mh, int Mwf) {
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    const int l = (int)(i % Mwf);
+    const long long pm = i / Mwf;
+    const int m = (int)(pm % Mh);
+    const long long p = pm / Mh;
+    const int k = m < Mh / 2 ? m : m + (H - Mh);
+    Y[i] = X[(p * H + k) * Wf + l];
+  }
+}
+
+__global__ void k_fdp_scatter(const float2 *__restrict__ gY, float2 *__restrict__ gX, long long total, int H,
+                              int Wf, int Mh, int Mwf) {
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    const int l = (int)(i % Wf);
+    const long long pk = i / Wf;
+    const int k = (int)(pk % H);
+    const long long p = pk / H;
+    const bool kept = l < Mwf && (k < Mh / 2 || k >= H - Mh / 2);
+    const int m = k < Mh / 2 ? k : k - (H - Mh);
+    gX[i] = kept ? gY[(p * Mh + m) * Mwf + l] : make_float2(0.f, 0.f);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// host side: size dispatch and launchers
+// ---------------------------------------------------------------------------
+template <class F>
+static bool dispatch_n(int n, F &&f) {
+  switch (n) {
+#define FDC_CASE(V)                          \
+  case V:                                    \
+    f(std::integral_constant<int, V>{});     \
+    return true;
+    FDC_CASE(2) FDC_CASE(4) FDC_CASE(8) FDC_CASE(16) FDC_CASE(32) FDC_CASE(64) FDC_CASE(128) FDC_CASE(256)
+    FDC_CASE(512) FDC_CASE(1024) FDC_CASE(224)
+#undef FDC_CASE
+    default:
+      return false;
+  }
+}
+
+// (n, m) pairs of the fused CIC kernels: m = n, n/2 or n/4 (powers of two), or 224 -> 224.
+template <class F>
+static bool dispatch_nm(int n, int m, F &&f) {
+  bool found = false;
+  dispatch_n(n, [&](auto nc) {
+    constexpr int N = decltype(nc)::value;
+    if (m == N) {
+      found = true;
+      f(nc, nc);
+      return;
+    }
+    if constexpr (N != 224 && N >= 4) {
+      if (m == N / 2) {
+        found = true;
+        f(nc, std::integral_constant<int, N / 2>{});
+        return;
+      }
+    }
+    if constexpr (N != 224 && N >= 8) {
+      if (m == N / 4) {
+        found = true;
+        f(nc, std::integral_constant<int, N / 4>{});
+        return;
+      }
+    }
+  });
+  return found;
+}
+
+bool size_supported(int n) {
+  return dispatch_n(n, [](auto) {});
+}
+
+bool cic_pair_supported(int n, int m) {
+  return dispatch_nm(n, m, [](auto, auto) {});
+}
+
+template <class Kern, class... Args>
+static hipError_t launch(const char *name, Kern kern, unsigned grid, unsigned block, size_t lds, hipStream_t s,
+                         Args... args) {
+  if (grid == 0) return hipSuccess;
+  timing_before(name, s);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(block), lds, s, args...);
+  const hipError_t e = hipGetLastError();
+  timing_after(name, s);
+  return e;
+}
+
+template <class T>
+static const char *kname(const char *base, T n) {
+  static const std::string name = std::string(base) + "_" + std::to_string(n);
+  return name.c_str();
+}
+
+static unsigned grid_stride_blocks(long long total, int block) {
+  long long g = (total + block - 1) / block;
+  if (g > 1048576) g = 1048576;
+  return (unsigned)(g > 0 ? g : 0);
+}
+
+hipError_t launch_row_r2c(int n, const float *x, float2 *out, long long planes, int rows_per_plane,
+                          ImgView in_view, long long in_plane_stride, int L, long long out_row_stride,
+                          long long out_plane_stride, float alpha, float beta, hipStream_t s) {
+  hipError_t err = hipErrorInvalidValue;
+  dispatch_n(n, [&](auto nc) {
+    constexpr int N = decltype(nc)::value;
+    constexpr int SPW = row_spw<N>();
+    const long long npairs = planes * rows_per_plane / 2;
+    const unsigned grid = (unsigned)((npairs + SPW - 1) / SPW);
+    const size_t lds = lds_size(SPW * N) * sizeof(float2);
+    static const std::string nm = "row_r2c_" + std::to_string(N);
+    err = launch(nm.c_str(), k_row_r2c<N, SPW>, grid, SPW * FftCfg<N>::TPS, lds, s, x, out, npairs,
+                 rows_per_plane, in_view, in_plane_stride, L, out_row_stride, out_plane_stride, alpha, beta);
+  });
+  return err;
+}
+
+hipError_t launch_row_c2r(int n, const float2 *in, float *y, long long planes, int rows_per_plane, int L,
+                          long long in_row_stride, long long in_plane_stride, float alpha, float beta,
+                          ImgView out_view, long long out_plane_stride, hipStream_t s) {
+  hipError_t err = hipErrorInvalidValue;
+  dispatch_n(n, [&](auto nc) {
+    constexpr int N = decltype(nc)::value;
+    constexpr int SPW = row_spw<N>();
+    const long long npairs = planes * rows_per_plane / 2;
+    const unsigned grid = (unsigned)((npairs + SPW - 1) / SPW);
+    const size_t lds = lds_size(SPW * N) * sizeof(float2);
+    static const std::string nm = "row_c2r_" + std::to_string(N);
+    err = launch(nm.c_str(), k_row_c2r<N, SPW>, grid, SPW * FftCfg<N>::TPS, lds, s, in, y, npairs,
+                 rows_per_plane, L, in_row_stride, in_plane_stride, alpha, beta, out_view, out_plane_stride);
+  });
+  return err;
+}
+
+hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long long planes, int L,
+                          long long in_plane_stride, long long out_plane_stride, hipStream_t s) {
+  hipError_t err = hipErrorInvalidValue;
+  dispatch_n(n, [&](auto nc) {
+    constexpr int N = decltype(nc)::value;
+    constexpr int CT = col_ct<N>();
+    const int tiles = (L + CT - 1) / CT;
+    const unsigned grid = (unsigned)(planes * tiles);
+    const size_t lds = lds_size(N * CT) * sizeof(float2);
+    static const std::string nf = "col_fft_fwd_" + std::to_string(N);
+    static const std::string ni = "col_fft_inv_" + std::to_string(N);
+    if (dir < 0)
+      err = launch(nf.c_str(), k_col_fft<N, CT, -1>, grid, CT * FftCfg<N>::TPS, lds, s, in, out, L, tiles,
+                   in_plane_stride, out_plane_stride);
+    else
+      err = launch(ni.c_str(), k_col_fft<N, CT, +1>, grid, CT * FftCfg<N>::TPS, lds, s, in, out, L, tiles,
+                   in_plane_stride, out_plane_stride);
+  });
+  return err;
+}
+
+hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, float2 *U, float2 *Xh, int B,
+                              int C, int S, hipStream_t s) {
+  hipError_t err = hipErrorInvalidValue;
+  dispatch_nm(n, m, [&](auto nc, auto mc) {
+    constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
+    constexpr int CT = col_ct<N>();
+    constexpr int L = M / 2 + 1;
+    const int tiles = (L + CT - 1) / CT;
+    const unsigned grid = (unsigned)((long long)B * C * tiles);
+    const size_t lds = cic_lds_elems<N, M, CT>() * sizeof(float2);
+    static const std::string nm = "col_fwd_cic_" + std::to_string(N) + "_" + std::to_string(M);
+    err = launch(nm.c_str(), k_col_fwd_cic<N, M, CT>, grid, CT * FftCfg<N>::TPS, lds, s, T, K, U, Xh, C, S / C,
+                 tiles);
+  });
+  return err;
+}
+
+hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, float2 *gK, int B, int C, int S,
+                             hipStream_t s) {
+  hipError_t err = hipErrorInvalidValue;
+  if (!cic_pair_supported(n, m)) return err;
+  dispatch_n(m, [&](auto mc) {
+    constexpr int M = decltype(mc)::value;
+    constexpr int CT = col_ct<M>();
+    constexpr int L = M / 2 + 1;
+    const int tiles = (L + CT - 1) / CT;
+    const unsigned grid = (unsigned)((long long)S * tiles);
+    const size_t lds = lds_size(M * CT) * sizeof(float2);
+    static const std::string nm = "col_bwd_gk_" + std::to_string(M);
+    err = launch(nm.c_str(), k_col_bwd_gk<M, CT>, grid, CT * FftCfg<M>::TPS, lds, s, Tg, Xh, gK, B, C, S / C, n,
+                 tiles);
+  });
+  return err;
+}
+
+hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, float2 *V, int B, int C, int S,
+                             hipStream_t s) {
+  hipError_t err = hipErrorInvalidValue;
+  dispatch_nm(n, m, [&](auto nc, auto mc) {
+    constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
+    constexpr int CT = col_ct<N>();
+    constexpr int L = M / 2 + 1;
+    const int tiles = (L + CT - 1) / CT;
+    const unsigned grid = (unsigned)((long long)B * C * tiles);
+    const size_t lds = cic_lds_elems<N, M, CT>() * sizeof(float2);
+    static const std::string nm = "col_bwd_gx_" + std::to_string(N) + "_" + std::to_string(M);
+    err = launch(nm.c_str(), k_col_bwd_gx<N, M, CT>, grid, CT * FftCfg<N>::TPS, lds, s, Tg, K, V, C, S / C,
+                 tiles);
+  });
+  return err;
+}
+
+hipError_t launch_gk_zero_dropped(float2 *gK, int S, int n, int m, hipStream_t s) {
+  if (m == n) return hipSuccess;  // nothing dropped
+  const long long total = (long long)S * n * (n / 2 + 1);
+  return launch("gk_zero_dropped", k_gk_zero_dropped, grid_stride_blocks(total, 256), 256, 0, s, gK, total, n, m);
+}
+
+hipError_t launch_cic_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, long long P,
+                          hipStream_t s) {
+  const long long total = (long long)B * S * P;
+  return launch("cic_fwd", k_cic_fwd, grid_stride_blocks(total, 256), 256, 0, s, X, K, Y, C, S / C, P, total);
+}
+
+hipError_t launch_cic_bwd_gx(const float2 *gY, const float2 *K, float2 *gX, int B, int C, int S, long long P,
+                             hipStream_t s) {
+  const long long total = (long long)B * C * P;
+  return launch("cic_bwd_gx", k_cic_bwd_gx, grid_stride_blocks(total, 256), 256, 0, s, gY, K, gX, C, S / C, P,
+                total);
+}
+
+hipError_t launch_cic_bwd_gk(const float2 *gY, const float2 *X, float2 *gK, int B, int C, int S, long long P,
+                             hipStream_t s) {
+  const long long total = (long long)S * P;
+  return launch("cic_bwd_gk", k_cic_bwd_gk, grid_stride_blocks(total, 256), 256, 0, s, gY, X, gK, B, C, S / C, P,
+                total);
+}
+
+hipError_t launch_fdp_gather(const float2 *X, float2 *Y, long long count, int H, int Wf, int Mh, int Mwf,
+                             hipStream_t s) {
+  const long long total = count * Mh * Mwf;
+  return launch("fdp_gather", k_fdp_gather, grid_stride_blocks(total, 256), 256, 0, s, X, Y, total, H, Wf, Mh,
+                Mwf);
+}
+
+hipError_t launch_fdp_scatter(const float2 *gY, float2 *gX, long long count, int H, int Wf, int Mh, int Mwf,
+                              hipStream_t s) {
+  const long long total = count * H * Wf;
+  return launch("fdp_scatter", k_fdp_scatter, grid_stride_blocks(total, 256), 256, 0, s, gY, gX, total, H, Wf, Mh,
+                Mwf);
+}
+
+}  // namespace fdc

@@ -1,0 +1,213 @@
+"""Torch-facing wrappers of libfdc: plans, workspaces and calls on the current stream.
+
+PyTorch only provides device memory and the stream; every step of the
+computation runs in libfdc's HIP kernels.  Tensors must be contiguous CUDA
+(HIP) tensors: float32 for images, complex64 for spectra.
+"""
+
+import ctypes
+
+import torch
+
+from . import _lib
+from ._lib import ARTIFACT_CROP, ARTIFACT_NONE, ARTIFACT_ROLL, call  # noqa: F401
+
+_ARTIFACTS = {"none": ARTIFACT_NONE, "crop": ARTIFACT_CROP, "roll": ARTIFACT_ROLL}
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _check(t, dtype, shape=None, name="tensor"):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
+def _workspace(nbytes, device):
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+class FftPlan:
+    """Batched 2-D real FFT of `count` h x w images (fdc_rfft2 and friends)."""
+
+    def __init__(self, count, h, w):
+        self.count, self.h, self.w = count, h, w
+        self._p = ctypes.c_void_p()
+        call("fdc_fft_plan_create", ctypes.byref(self._p), count, h, w)
+        n = ctypes.c_size_t()
+        call("fdc_fft_workspace_size", self._p, ctypes.byref(n))
+        self.ws_bytes = n.value
+
+    def __del__(self):
+        if getattr(self, "_p", None) and _lib._lib is not None:
+            _lib.lib().fdc_fft_plan_destroy(self._p)
+
+    def _spec_shape(self, lead):
+        return lead + (self.h, self.w // 2 + 1)
+
+    def _run(self, name, src, dst, ws):
+        call(name, self._p, _ptr(src), _ptr(dst), _ptr(ws), ws.numel() if ws is not None else 0, _stream())
+        return dst
+
+    def rfft2(self, x):
+        _check(x, torch.float32, name="x")
+        out = torch.empty(self._spec_shape(tuple(x.shape[:-2])), dtype=torch.complex64, device=x.device)
+        return self._run("fdc_rfft2", x, out, None)
+
+    def irfft2(self, X):
+        _check(X, torch.complex64, name="X")
+        out = torch.empty(tuple(X.shape[:-2]) + (self.h, self.w), dtype=torch.float32, device=X.device)
+        return self._run("fdc_irfft2", X, out, _workspace(self.ws_bytes, X.device))
+
+    def rfft2_backward(self, gX):
+        _check(gX, torch.complex64, name="gX")
+        out = torch.empty(tuple(gX.shape[:-2]) + (self.h, self.w), dtype=torch.float32, device=gX.device)
+        return self._run("fdc_rfft2_backward", gX, out, _workspace(self.ws_bytes, gX.device))
+
+    def irfft2_backward(self, gx):
+        _check(gx, torch.float32, name="gx")
+        out = torch.empty(self._spec_shape(tuple(gx.shape[:-2])), dtype=torch.complex64, device=gx.device)
+        return self._run("fdc_irfft2_backward", gx, out, None)
+
+
+def cic_forward(X, K):
+    """Spectral CIC (Eq. 5): X [B][C][H][Wf], K [S][H][Wf] -> [B][S][H][Wf]."""
+    _check(X, torch.complex64, name="X")
+    _check(K, torch.complex64, name="K")
+    B, C, H, Wf = X.shape
+    S = K.shape[0]
+    Y = torch.empty((B, S, H, Wf), dtype=torch.complex64, device=X.device)
+    call("fdc_cic_forward", _ptr(X), _ptr(K), _ptr(Y), B, C, S, H, Wf, _stream())
+    return Y
+
+
+def cic_backward(gY, X, K, need_gx=True, need_gk=True):
+    _check(gY, torch.complex64, name="gY")
+    B, S, H, Wf = gY.shape
+    C = X.shape[1]
+    gX = torch.empty_like(X) if need_gx else None
+    gK = torch.empty_like(K) if need_gk else None
+    call("fdc_cic_backward", _ptr(gY), _ptr(X), _ptr(K), _ptr(gX), _ptr(gK), B, C, S, H, Wf, _stream())
+    return gX, gK
+
+
+def fdp_forward(X, mh, mw):
+    """FDP crop: [.., H, W/2+1] -> [.., mh, mw/2+1] (W taken as 2 * (Wf - 1))."""
+    _check(X, torch.complex64, name="X")
+    H, Wf = X.shape[-2:]
+    W = 2 * (Wf - 1)
+    count = X.numel() // (H * Wf)
+    Y = torch.empty(tuple(X.shape[:-2]) + (mh, mw // 2 + 1), dtype=torch.complex64, device=X.device)
+    call("fdp_forward", _ptr(X), _ptr(Y), count, H, W, mh, mw, _stream())
+    return Y
+
+
+def fdp_backward(gY, h, w):
+    _check(gY, torch.complex64, name="gY")
+    mh, mwf = gY.shape[-2:]
+    count = gY.numel() // (mh * mwf)
+    gX = torch.empty(tuple(gY.shape[:-2]) + (h, w // 2 + 1), dtype=torch.complex64, device=gY.device)
+    call("fdp_backward", _ptr(gY), _ptr(gX), count, h, w, mh, 2 * (mwf - 1), _stream())
+    return gX
+
+
+class _LayerPlan:
+    def _sizes(self):
+        f, s, b = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+        call("fdc_layer_workspace_size", self._p, ctypes.byref(f), ctypes.byref(s), ctypes.byref(b))
+        o = ctypes.c_int()
+        call("fdc_layer_output_size", self._p, ctypes.byref(o))
+        self.fwd_ws_bytes, self.saved_bytes, self.bwd_ws_bytes = f.value, s.value, b.value
+        self.out = o.value
+
+    def __del__(self):
+        if getattr(self, "_p", None) and _lib._lib is not None:
+            _lib.lib().fdc_layer_plan_destroy(self._p)
+
+
+class CicLayer(_LayerPlan):
+    """Fused CIC + FDP layer: x [B][C][N][N] -> y [B][S][O][O] (fdc_cic_layer_*).
+
+    Workspaces are allocated once per layer object and reused by every call,
+    so a layer object must not run concurrently on two streams.
+    """
+
+    def __init__(self, B, C, S, N, M, artifact="none", kernel_n=1, device="cuda"):
+        self.B, self.C, self.S, self.N, self.M = B, C, S, N, M
+        self._p = ctypes.c_void_p()
+        call("fdc_cic_layer_plan_create", ctypes.byref(self._p), B, C, S, N, M, _ARTIFACTS[artifact], kernel_n)
+        self._sizes()
+        self.device = torch.device(device)
+        self.fwd_ws = _workspace(self.fwd_ws_bytes, self.device)
+        self.bwd_ws = _workspace(self.bwd_ws_bytes, self.device)
+
+    def new_saved(self):
+        return torch.empty((self.B, self.C, self.M, self.M // 2 + 1), dtype=torch.complex64, device=self.device)
+
+    def new_output(self):
+        return torch.empty((self.B, self.S, self.out, self.out), dtype=torch.float32, device=self.device)
+
+    def forward(self, x, K, y=None, saved=None):
+        _check(x, torch.float32, (self.B, self.C, self.N, self.N), "x")
+        _check(K, torch.complex64, (self.S, self.N, self.N // 2 + 1), "K")
+        y = self.new_output() if y is None else y
+        call("fdc_cic_layer_forward", self._p, _ptr(x), _ptr(K), _ptr(y), _ptr(saved), _ptr(self.fwd_ws),
+             self.fwd_ws.numel(), _stream())
+        return y
+
+    def backward(self, gy, saved, K, need_gx=True, need_gk=True, gx=None, gK=None):
+        _check(gy, torch.float32, (self.B, self.S, self.out, self.out), "gy")
+        if need_gx and gx is None:
+            gx = torch.empty((self.B, self.C, self.N, self.N), dtype=torch.float32, device=self.device)
+        if need_gk and gK is None:
+            gK = torch.empty((self.S, self.N, self.N // 2 + 1), dtype=torch.complex64, device=self.device)
+        call("fdc_cic_layer_backward", self._p, _ptr(gy), _ptr(saved), _ptr(K), _ptr(gx if need_gx else None),
+             _ptr(gK if need_gk else None), _ptr(self.bwd_ws), self.bwd_ws.numel(), _stream())
+        return (gx if need_gx else None), (gK if need_gk else None)
+
+
+class CicStack:
+    """A stack of fused CIC + FDP layers with preallocated activations, saved
+    spectra and gradients, so that one forward + backward step allocates nothing."""
+
+    def __init__(self, batch, sizes, channels, device="cuda"):
+        self.layers = [CicLayer(batch, channels[i], channels[i + 1], sizes[i], sizes[i + 1], device=device)
+                       for i in range(len(sizes) - 1)]
+        self.saved = [layer.new_saved() for layer in self.layers]
+        self.acts = [layer.new_output() for layer in self.layers]
+        self.gacts = [None] + [torch.empty((batch, channels[i], sizes[i], sizes[i]), dtype=torch.float32,
+                                           device=device) for i in range(1, len(sizes) - 1)]
+        self.gks = [torch.empty((channels[i + 1], sizes[i], sizes[i] // 2 + 1), dtype=torch.complex64,
+                                device=device) for i in range(len(sizes) - 1)]
+
+    def forward(self, x, kernels):
+        h = x
+        for layer, K, y, sv in zip(self.layers, kernels, self.acts, self.saved):
+            layer.forward(h, K, y=y, saved=sv)
+            h = y
+        return h
+
+    def backward(self, gy, kernels, input_grad=None):
+        """Gradients of every kernel (and of the input if `input_grad` is a tensor to fill)."""
+        g = gy
+        for i in reversed(range(len(self.layers))):
+            layer = self.layers[i]
+            if i > 0:
+                gx = self.gacts[i]
+            else:
+                gx = input_grad
+            layer.backward(g, self.saved[i], kernels[i], need_gx=gx is not None, need_gk=True, gx=gx,
+                           gK=self.gks[i])
+            g = gx
+        return self.gks

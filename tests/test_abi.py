@@ -1,0 +1,145 @@
+"""Host-side tests of the C ABI: the library loads, exports every declared symbol,
+and rejects bad arguments with the documented status before touching the GPU.
+
+None of these calls enqueues work: each returns from host-side validation.
+"""
+
+import ctypes
+
+import pytest
+
+from paper_2106_12736_amd import _lib
+from paper_2106_12736_amd._lib import FDC_EINVAL, FDC_EUNSUPPORTED, FDC_EWORKSPACE, FDC_OK
+
+
+def test_library_exports_every_declared_function():
+    declared = _lib.header_functions()
+    assert len(declared) >= 25
+    lib = _lib.lib()
+    missing = [n for n in declared if not hasattr(lib, n)]
+    assert not missing, missing
+    assert set(_lib._SIGS) == set(declared), "binding signatures out of sync with include/fdc.h"
+
+
+def test_status_strings_and_version():
+    lib = _lib.lib()
+    for st in range(5):
+        assert lib.fdc_status_string(st)
+    assert lib.fdc_version() >= 100
+
+
+def _fft_plan(count, h, w):
+    p = ctypes.c_void_p()
+    st = _lib.status("fdc_fft_plan_create", ctypes.byref(p), count, h, w)
+    return st, p
+
+
+@pytest.mark.parametrize("count,h,w,expect", [
+    (1, 8, 8, FDC_OK), (3, 224, 224, FDC_OK), (2, 1024, 16, FDC_OK),
+    (0, 8, 8, FDC_EINVAL), (1, 7, 8, FDC_EINVAL), (1, 8, -4, FDC_EINVAL),
+    (1, 2048, 8, FDC_EUNSUPPORTED), (1, 96, 96, FDC_EUNSUPPORTED), (1, 22, 8, FDC_EUNSUPPORTED),
+])
+def test_fft_plan_validation(count, h, w, expect):
+    st, p = _fft_plan(count, h, w)
+    assert st == expect, _lib.last_error()
+    if st == FDC_OK:
+        n = ctypes.c_size_t()
+        assert _lib.status("fdc_fft_workspace_size", p, ctypes.byref(n)) == FDC_OK
+        assert n.value == count * h * (w // 2 + 1) * 8
+        assert _lib.status("fdc_fft_plan_destroy", p) == FDC_OK
+    else:
+        assert _lib.last_error()
+
+
+def test_fft_calls_reject_bad_arguments_before_launch():
+    st, p = _fft_plan(2, 16, 16)
+    assert st == FDC_OK
+    dummy = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    assert _lib.status("fdc_rfft2", p, None, dummy, None, 0, None) == FDC_EINVAL
+    assert _lib.status("fdc_irfft2", p, dummy, dummy, None, 0, None) == FDC_EWORKSPACE
+    assert _lib.status("fdc_irfft2", p, dummy, dummy, dummy, 10, None) == FDC_EWORKSPACE
+    assert _lib.status("fdc_rfft2_backward", p, dummy, None, dummy, 1 << 20, None) == FDC_EINVAL
+    assert _lib.status("fdc_rfft2", None, dummy, dummy, None, 0, None) == FDC_EINVAL
+    _lib.status("fdc_fft_plan_destroy", p)
+
+
+@pytest.mark.parametrize("args,expect", [
+    ((2, 1, 4, 64, 32, 0, 1), FDC_OK),
+    ((1, 2, 6, 16, 8, 1, 3), FDC_OK),          # crop with 3x3 support
+    ((1, 2, 6, 1024, 256, 2, 3), FDC_OK),
+    ((0, 1, 4, 64, 32, 0, 1), FDC_EINVAL),     # B = 0
+    ((2, 3, 4, 64, 32, 0, 1), FDC_EINVAL),     # S mod C != 0
+    ((2, 1, 4, 64, 31, 0, 1), FDC_EINVAL),     # odd M
+    ((2, 1, 4, 32, 64, 0, 1), FDC_EINVAL),     # M > N
+    ((2, 1, 4, 64, 32, 1, 0), FDC_EINVAL),     # crop needs kernel_n >= 1
+    ((2, 1, 4, 64, 32, 1, 33), FDC_EINVAL),    # kernel_n > M
+    ((2, 1, 4, 64, 32, 7, 1), FDC_EINVAL),     # bad artifact mode
+    ((2, 1, 4, 64, 24, 0, 1), FDC_EUNSUPPORTED),  # M not N / 2^k
+    ((2, 1, 4, 64, 8, 0, 1), FDC_EUNSUPPORTED),   # N/8: outside the fused set
+    ((2, 1, 4, 2048, 1024, 0, 1), FDC_EUNSUPPORTED),
+])
+def test_cic_layer_plan_validation(args, expect):
+    p = ctypes.c_void_p()
+    st = _lib.status("fdc_cic_layer_plan_create", ctypes.byref(p), *args)
+    assert st == expect, _lib.last_error()
+    if st == FDC_OK:
+        f, s, b = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+        assert _lib.status("fdc_layer_workspace_size", p, ctypes.byref(f), ctypes.byref(s), ctypes.byref(b)) == 0
+        B, C, S, N, M, art, kn = args
+        L = M // 2 + 1
+        assert s.value == B * C * M * L * 8
+        o = ctypes.c_int()
+        assert _lib.status("fdc_layer_output_size", p, ctypes.byref(o)) == FDC_OK
+        assert o.value == (M - kn + 1 if art == 1 else M)
+        assert _lib.status("fdc_layer_plan_destroy", p) == FDC_OK
+
+
+def test_layer_calls_reject_bad_arguments():
+    p = ctypes.c_void_p()
+    assert _lib.status("fdc_cic_layer_plan_create", ctypes.byref(p), 2, 1, 4, 64, 32, 0, 1) == FDC_OK
+    d = ctypes.c_void_p(0x1000)
+    assert _lib.status("fdc_cic_layer_forward", p, d, d, None, None, d, 1 << 30, None) == FDC_EINVAL
+    assert _lib.status("fdc_cic_layer_forward", p, d, d, d, None, None, 0, None) == FDC_EWORKSPACE
+    assert _lib.status("fdc_cic_layer_backward", p, d, None, d, None, d, d, 1 << 30, None) == FDC_EINVAL
+    assert _lib.status("fdc_cic_layer_backward", p, None, d, d, d, d, d, 1 << 30, None) == FDC_EINVAL
+    assert _lib.status("fdc_cic_layer_backward", p, d, d, d, d, None, None, 8, None) == FDC_EWORKSPACE
+    # a plan of the other kind is refused
+    assert _lib.status("fdc_full_forward", p, d, d, d, d, d, 1 << 30, None) == FDC_EINVAL
+    assert _lib.status("fdc_layer_plan_destroy", p) == FDC_OK
+
+
+@pytest.mark.parametrize("args,expect", [
+    ((1, 8, 8, 4, 4), FDC_OK), ((3, 10, 12, 6, 8), FDC_OK),
+    ((0, 8, 8, 4, 4), FDC_EINVAL), ((1, 8, 8, 10, 4), FDC_EINVAL), ((1, 8, 8, 3, 4), FDC_EINVAL),
+])
+def test_fdp_validation(args, expect):
+    count, H, W, Mh, Mw = args
+    if expect == FDC_OK:
+        # valid sizes with NULL tensors still fail, but on the tensor check
+        assert _lib.status("fdp_forward", None, None, count, H, W, Mh, Mw, None) == FDC_EINVAL
+        assert "NULL" in _lib.last_error()
+    else:
+        assert _lib.status("fdp_forward", None, None, count, H, W, Mh, Mw, None) == expect
+        assert "NULL" not in _lib.last_error()
+
+
+def test_cic_spectral_validation():
+    d = ctypes.c_void_p(0x1000)
+    assert _lib.status("fdc_cic_forward", d, d, d, 2, 3, 4, 8, 5, None) == FDC_EINVAL
+    assert _lib.status("fdc_cic_forward", d, d, d, 0, 1, 4, 8, 5, None) == FDC_EINVAL
+    assert _lib.status("fdc_cic_backward", None, d, d, d, d, 2, 1, 4, 8, 5, None) == FDC_EINVAL
+
+
+def test_timing_api_arguments():
+    assert _lib.status("fdc_kernel_timing_enable", 0) == FDC_EINVAL
+    assert _lib.status("fdc_kernel_timing_report", None, 0) == FDC_EINVAL
+
+
+def test_destroyed_plan_is_refused():
+    st, p = _fft_plan(1, 8, 8)
+    assert st == FDC_OK
+    # destroy through a copy of the handle, then use a fresh invalid handle object
+    bogus = ctypes.create_string_buffer(64)
+    assert _lib.status("fdc_fft_workspace_size", ctypes.cast(bogus, ctypes.c_void_p),
+                       ctypes.byref(ctypes.c_size_t())) == FDC_EINVAL
+    assert _lib.status("fdc_fft_plan_destroy", p) == FDC_OK

@@ -1,0 +1,152 @@
+"""GPU parity of the fused CIC + FDP layer (forward and backward) and of the
+multi-layer stacks, against the float64 oracle on the same seeded inputs.
+
+The stack tests run the four synthetic CIC workloads at their full sizes, in
+the same launch configuration the benchmark times (paper_2106_12736_amd.layers.CicStack),
+and compare every output and every gradient element."""
+
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+from _parity import assert_parity, to_np
+from oracle import fdc
+from paper_2106_12736_amd import inputs, layers
+
+pytestmark = pytest.mark.gpu
+
+
+def _rng(*key):
+    return np.random.default_rng(zlib.crc32(repr(key).encode()))
+
+
+def _gpu(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+ORACLE_MODE = {"none": fdc.ARTIFACT_NONE, "crop": fdc.ARTIFACT_CROP, "roll": fdc.ARTIFACT_ROLL}
+
+LAYER_CASES = [
+    # N, M, B, C, J, artifact, kernel_n
+    (4, 2, 1, 1, 1, "none", 1),
+    (4, 4, 2, 1, 3, "none", 1),
+    (8, 4, 2, 2, 2, "none", 1),
+    (8, 2, 1, 1, 2, "none", 1),
+    (16, 8, 2, 1, 4, "crop", 3),
+    (16, 16, 1, 2, 1, "roll", 3),
+    (32, 16, 2, 2, 3, "none", 1),
+    (32, 8, 1, 3, 2, "roll", 4),
+    (64, 32, 2, 1, 4, "none", 1),
+    (64, 64, 2, 2, 2, "crop", 5),
+    (128, 64, 2, 2, 2, "none", 1),
+    (128, 32, 1, 1, 8, "none", 1),
+    (256, 128, 2, 2, 2, "none", 1),
+    (256, 256, 1, 1, 3, "roll", 3),
+    (512, 256, 2, 1, 8, "none", 1),
+    (512, 128, 1, 2, 2, "crop", 3),
+    (1024, 512, 2, 1, 8, "none", 1),
+    (1024, 1024, 1, 1, 2, "none", 1),
+    (1024, 256, 1, 2, 1, "none", 1),
+    (224, 224, 2, 2, 2, "crop", 3),
+]
+
+
+@pytest.mark.parametrize("N,M,B,C,J,artifact,kn", LAYER_CASES)
+def test_layer_forward_backward(N, M, B, C, J, artifact, kn):
+    print(f"layer N={N} M={M} B={B} C={C} J={J} {artifact}/{kn}", flush=True)
+    rng = _rng("layer", N, M, B, C, J, artifact, kn)
+    S = C * J
+    x = rng.random((B, C, N, N), dtype=np.float32)
+    K = inputs.spectral_kernels(rng, S, N)
+    layer = layers.CicLayer(B, C, S, N, M, artifact, kn)
+    gy = rng.standard_normal((B, S, layer.out, layer.out), dtype=np.float32)
+    saved = layer.new_saved()
+    xg, Kg = _gpu(x), _gpu(K)
+    y = layer.forward(xg, Kg, saved=saved)
+    gx, gK = layer.backward(_gpu(gy), saved, Kg)
+
+    mode = ORACLE_MODE[artifact]
+    ry, xs = fdc.cic_fdp_layer_forward(x.astype(np.float64), K.astype(np.complex128), M, mode, kn)
+    rgx, rgK = fdc.cic_fdp_layer_backward(gy.astype(np.float64), xs, K.astype(np.complex128), M, mode, kn)
+    assert_parity(to_np(y), ry, "y")
+    assert_parity(to_np(saved), fdc.fdp(xs, M, M), "saved spectrum")
+    assert_parity(to_np(gx), rgx, "gx")
+    assert_parity(to_np(gK), rgK, "gK")
+    # bins dropped by FDP get exact zeros
+    kept = np.zeros((N, N // 2 + 1), bool)
+    kept[list(range(M // 2)) + list(range(N - M // 2, N)), : M // 2 + 1] = True
+    assert np.all(to_np(gK)[:, ~kept] == 0)
+
+
+def test_layer_is_deterministic_and_reentrant():
+    N, M, B, C, J = 256, 128, 4, 2, 2
+    rng = _rng("det")
+    x = _gpu(rng.random((B, C, N, N), dtype=np.float32))
+    K = _gpu(inputs.spectral_kernels(rng, C * J, N))
+    gy = _gpu(rng.standard_normal((B, C * J, M, M), dtype=np.float32))
+    layer = layers.CicLayer(B, C, C * J, N, M)
+    outs = []
+    for _ in range(2):
+        saved = layer.new_saved()
+        y = layer.forward(x, K, saved=saved)
+        gx, gK = layer.backward(gy, saved, K)
+        outs.append((y.clone(), gx.clone(), gK.clone()))
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
+def test_gradient_outputs_are_optional():
+    N, M, B, C, J = 64, 32, 2, 2, 2
+    rng = _rng("opt")
+    x = _gpu(rng.random((B, C, N, N), dtype=np.float32))
+    K = _gpu(inputs.spectral_kernels(rng, C * J, N))
+    gy = _gpu(rng.standard_normal((B, C * J, M, M), dtype=np.float32))
+    layer = layers.CicLayer(B, C, C * J, N, M)
+    saved = layer.new_saved()
+    layer.forward(x, K, saved=saved)
+    gx_full, gK_full = layer.backward(gy, saved, K)
+    gx_only, none_k = layer.backward(gy, saved, K, need_gk=False)
+    none_x, gK_only = layer.backward(gy, saved, K, need_gx=False)
+    assert none_k is None and none_x is None
+    assert torch.equal(gx_only, gx_full) and torch.equal(gK_only, gK_full)
+    y_nosave = layer.forward(x, K)  # inference: nothing saved
+    assert torch.equal(y_nosave, layer.forward(x, K, saved=saved))
+
+
+def test_batch_not_divisible():
+    # any batch size works (the paper's implementation needed batch-divisible datasets)
+    for B in (1, 3, 5):
+        N, M, C, J = 32, 16, 1, 2
+        rng = _rng("batch", B)
+        x = rng.random((B, C, N, N), dtype=np.float32)
+        K = inputs.spectral_kernels(rng, C * J, N)
+        layer = layers.CicLayer(B, C, C * J, N, M)
+        y = layer.forward(_gpu(x), _gpu(K))
+        ry, _ = fdc.cic_fdp_layer_forward(x.astype(np.float64), K.astype(np.complex128), M)
+        assert_parity(to_np(y), ry, f"y B={B}")
+
+
+@pytest.mark.parametrize("wl", inputs.CIC_WORKLOADS, ids=[w.name for w in inputs.CIC_WORKLOADS])
+def test_stack_full_size(wl):
+    print(f"stack {wl.name}", flush=True)
+    d = inputs.make_cic_stack(wl)
+    stack = layers.CicStack(wl.batch, wl.sizes, wl.channels)
+    Ks = [_gpu(k) for k in d.kernels]
+    gin = torch.empty((wl.batch, wl.channels[0], wl.sizes[0], wl.sizes[0]), dtype=torch.float32, device="cuda")
+    y = stack.forward(_gpu(d.x), Ks)
+    gks = [g.clone() for g in stack.backward(_gpu(d.grad), Ks, input_grad=gin)]
+    torch.cuda.synchronize()
+
+    Kd = [k.astype(np.complex128) for k in d.kernels]
+    ry, saved = fdc.cic_stack_forward(d.x.astype(np.float64), Kd, wl.sizes)
+    rgks, rgx = fdc.cic_stack_backward(d.grad.astype(np.float64), saved, Kd, wl.sizes, want_input_grad=True)
+    assert_parity(to_np(y), ry, "y")
+    for i in range(wl.layers):
+        assert_parity(to_np(gks[i]), rgks[i], f"gK layer {i}")
+    assert_parity(to_np(gin), rgx, "gx input")
+    # the training step skips the input-image gradient; the kernel gradients do not change
+    gks2 = [g.clone() for g in stack.backward(_gpu(d.grad), Ks)]
+    for a, b in zip(gks2, gks):
+        assert torch.equal(a, b)
