@@ -1,0 +1,274 @@
+#!/usr/bin/env python3
+"""Throughput of the fused CIC + FDP layer stack, forward + backward, on one GPU.
+
+Workload (the paper's large-image setting, section 2.5.1 / 3.2, with synthetic
+fundus-like inputs in place of the APTOS 2019 photographs): batch 8 of 1024 x 1024
+grayscale images, five CIC + FDP layers with channel fan-out
+1 -> 8 -> 16 -> 32 -> 64 -> 128 and FDP halving the size after each layer
+(1024 -> 512 -> 256 -> 128 -> 64 -> 32).  One step = every layer forward
+(rfft2 -> CIC -> FDP -> irfft2) and every layer backward (kernel gradients of
+all layers, activation gradients of layers 2..5; the gradient of the input
+image is not part of a training step).  Inputs are resident in HBM before the
+timed region starts.
+
+Prints ONE JSON line (see --help).  Besides the step time it reports, for the
+kernel that takes most of the step, its algorithmic bytes per launch divided by
+its average launch duration (HIP events around that kernel's launches on the
+stream it runs on, recorded during the timed steps), and the float64 CPU oracle
+timed on a bounded sample of the same workload.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published peak
+METRIC = "images/sec fwd+bwd of FDC/FDP stack at 1024² fp32; % peak HBM GB/s (and MFMA %)"
+C64, F32 = 8, 4
+
+
+# ----------------------------------------------------------------------------
+# algorithmic bytes: each tensor a kernel must read or write, counted once
+# ----------------------------------------------------------------------------
+
+def layer_dims(wl, i):
+    N, M = wl.sizes[i], wl.sizes[i + 1]
+    C, S = wl.channels[i], wl.channels[i + 1]
+    return wl.batch, C, S, N, M, M // 2 + 1, N // 2 + 1
+
+
+def step_launches(wl, input_grad=False):
+    """(kernel name, algorithmic bytes) of every launch of one step, in launch order."""
+    out = []
+    for i in range(wl.layers):
+        B, C, S, N, M, L, _ = layer_dims(wl, i)
+        out.append((f"row_r2c_{N}", F32 * B * C * N * N + C64 * B * C * N * L))
+        out.append((f"col_fwd_cic_{N}_{M}", C64 * (B * C * N * L + S * M * L + B * S * M * L + B * C * M * L)))
+        out.append((f"row_c2r_{M}", C64 * B * S * M * L + F32 * B * S * M * M))
+    for i in reversed(range(wl.layers)):
+        B, C, S, N, M, L, NF = layer_dims(wl, i)
+        out.append((f"row_r2c_{M}", F32 * B * S * M * M + C64 * B * S * M * L))
+        out.append((f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + S * M * L)))
+        if M < N:
+            out.append(("gk_zero_dropped", C64 * S * (N * NF - M * L)))
+        if i > 0 or input_grad:
+            out.append((f"col_bwd_gx_{N}_{M}", C64 * (B * S * M * L + S * M * L + B * C * N * L)))
+            out.append((f"row_c2r_{N}", C64 * B * C * N * L + F32 * B * C * N * N))
+    return out
+
+
+def step_api_bytes(wl, input_grad=False):
+    """Bytes of the tensors that cross the layer interface in one step, each counted once:
+    forward x, K at the kept bins, y; backward g, K, the saved pooled spectrum, gx, gK at kept bins."""
+    total = 0
+    for i in range(wl.layers):
+        B, C, S, N, M, L, _ = layer_dims(wl, i)
+        total += F32 * B * C * N * N + C64 * S * M * L + F32 * B * S * M * M
+        total += F32 * B * S * M * M + C64 * S * M * L + C64 * B * C * M * L + C64 * S * M * L
+        if i > 0 or input_grad:
+            total += F32 * B * C * N * N
+    return total
+
+
+def kernel_source_digest():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2106_12736_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h")):
+            with open(os.path.join(csrc, f), "rb") as fh:
+                h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary of this kernel,
+    or None when there is none or the kernel sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_sha256") != kernel_source_digest():
+        return None
+    return rec["hbm_bytes_per_launch"]
+
+
+# ----------------------------------------------------------------------------
+# CPU baseline: the float64 oracle on the host cores
+# ----------------------------------------------------------------------------
+
+def cpu_baseline(wl, data, min_seconds=10.0, max_reps=3):
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import fdc
+
+    x = data.x.astype(np.float64)
+    kd = [k.astype(np.complex128) for k in data.kernels]
+    g = data.grad.astype(np.float64)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        _, saved = fdc.cic_stack_forward(x, kd, wl.sizes)
+        fdc.cic_stack_backward(g, saved, kd, wl.sizes, want_input_grad=False)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds or reps >= max_reps:
+            break
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {
+        "value": reps * wl.batch / el,
+        "unit": "images/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{reps} full step(s) of the same workload (batch {wl.batch}, all {wl.layers} layers, "
+                  f"fwd+bwd, float64) in {el:.1f} s on {os.cpu_count()} host CPUs visible",
+    }
+
+
+# ----------------------------------------------------------------------------
+# main
+# ----------------------------------------------------------------------------
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="cic_stack_1024",
+                    help="CIC stack workload (default: the 1024 x 1024 headline stack)")
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
+    ap.add_argument("--input-grad", action="store_true", help="also compute the input-image gradient")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the method shards over the batch "
+              "with one all-reduce of the kernel gradients per layer, which this build does not run.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2106_12736_amd import _lib, inputs, layers
+
+    wl = {w.name: w for w in inputs.CIC_WORKLOADS}[args.workload]
+    if not torch.cuda.is_available():
+        sys.exit("bench.py needs a GPU")
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    _lib.lib()  # fails loudly if libfdc.so is not built
+
+    data = inputs.make_cic_stack(wl)
+    x = torch.from_numpy(data.x).to(dev)
+    Ks = [torch.from_numpy(k).to(dev) for k in data.kernels]
+    g = torch.from_numpy(data.grad).to(dev)
+    stack = layers.CicStack(wl.batch, wl.sizes, wl.channels, device=dev)
+    gin = (torch.empty((wl.batch, wl.channels[0], wl.sizes[0], wl.sizes[0]), dtype=torch.float32, device=dev)
+           if args.input_grad else None)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        stack.forward(x, Ks)
+        stack.backward(g, Ks, input_grad=gin)
+
+    for _ in range(max(args.warmup, 1)):
+        step()
+    torch.cuda.synchronize()
+
+    # one instrumented step: per-kernel durations, to find the kernel that dominates
+    launches = step_launches(wl, args.input_grad)
+    _lib.call("fdc_kernel_timing_enable", len(launches) + 8, None)
+    step()
+    torch.cuda.synchronize()
+    buf = ctypes_buf(1 << 16)
+    _lib.call("fdc_kernel_timing_launches", buf, len(buf))
+    _lib.call("fdc_kernel_timing_disable")
+    recs = [ln.rsplit(" ", 1) for ln in buf.value.decode().strip().splitlines()]
+    names = [r[0] for r in recs]
+    if names != [n for n, _ in launches]:
+        sys.exit(f"launch sequence differs from the byte model:\n{names}\n{[n for n, _ in launches]}")
+    per_name = {}
+    for (name, nbytes), (_, ms) in zip(launches, recs):
+        t, b, n = per_name.get(name, (0.0, 0, 0))
+        per_name[name] = (t + float(ms), b + nbytes, n + 1)
+    dominant = max(per_name, key=lambda k: per_name[k][0])
+    dom_bytes_per_step, dom_launches_per_step = per_name[dominant][1], per_name[dominant][2]
+
+    # timed region: K steps, HIP events on the stream, the dominant kernel bracketed by its own events
+    _lib.call("fdc_kernel_timing_enable", args.steps * dom_launches_per_step, dominant.encode())
+    torch.cuda.synchronize()
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for _ in range(args.steps):
+        step()
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    _lib.call("fdc_kernel_timing_disable")
+    buf = ctypes_buf(1 << 20)
+    _lib.call("fdc_kernel_timing_launches", buf, len(buf))
+    dom_ms = [float(ln.rsplit(" ", 1)[1]) for ln in buf.value.decode().strip().splitlines()]
+    ms_per_step = t_start.elapsed_time(t_end) / args.steps
+
+    dom_avg_ms = sum(dom_ms) / len(dom_ms)
+    dom_bytes_per_launch = dom_bytes_per_step / dom_launches_per_step
+    achieved = dom_bytes_per_launch / (dom_avg_ms * 1e-3) / 1e9
+    api_bytes = step_api_bytes(wl, args.input_grad)
+
+    out = {
+        "metric": METRIC,
+        "value": wl.batch / (ms_per_step * 1e-3),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name,
+            "batch": wl.batch,
+            "sizes": list(wl.sizes),
+            "channels": list(wl.channels),
+            "input_grad": bool(args.input_grad),
+            "launches_per_step": len(launches),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": dominant,
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": measured_traffic(dominant, wl.name),
+            "bytes_per_launch": dom_bytes_per_launch,
+            "avg_launch_ms": dom_avg_ms,
+            "share_of_step": sum(dom_ms) / args.steps / ms_per_step,
+        },
+        "step_api_bytes": api_bytes,
+        "step_effective_gbps": api_bytes / (ms_per_step * 1e-3) / 1e9,
+        "step_kernel_ms": {k: round(v[0], 5) for k, v in sorted(per_name.items(), key=lambda kv: -kv[1][0])},
+        "wall_ms_per_step": wall * 1e3 / args.steps,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, data)
+    print(json.dumps(out), flush=True)
+
+
+def ctypes_buf(n):
+    import ctypes
+    return ctypes.create_string_buffer(n)
+
+
+if __name__ == "__main__":
+    main()

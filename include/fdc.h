@@ -181,14 +181,19 @@ fdc_status fdc_full_backward(const fdc_layer_plan *plan, const float *gy, const 
 /* ------------------------------------------------------------------------ */
 /* Kernel timing (measurement support, off by default)                      */
 /* ------------------------------------------------------------------------ */
-/* While enabled, every kernel the library launches is bracketed by a pair of
- * HIP events on its stream; fdc_kernel_timing_report() synchronises on those
- * events and writes one line per kernel name: "<name> <launches> <total_ms>\n".
+/* While enabled, every kernel the library launches (only those named
+ * `only_kernel` when it is not NULL) is bracketed by a pair of HIP events on
+ * its stream; fdc_kernel_timing_report() synchronises on those events and
+ * writes one line per kernel name: "<name> <launches> <total_ms>\n".
  * Enabling clears earlier records.  At most `max_launches` launches are
- * recorded; events are created when timing is enabled, never during a call. */
-fdc_status fdc_kernel_timing_enable(int max_launches);
+ * recorded; events are created when timing is enabled, never during a call.
+ * Timing is process-wide and not meant for use under stream capture. */
+fdc_status fdc_kernel_timing_enable(int max_launches, const char *only_kernel);
 fdc_status fdc_kernel_timing_disable(void);
 fdc_status fdc_kernel_timing_report(char *buf, size_t buf_bytes);
+/* The same records one line per launch, in launch order: "<name> <ms>\n".
+ * FDC_EINVAL when the text (with its terminating NUL) exceeds buf_bytes. */
+fdc_status fdc_kernel_timing_launches(char *buf, size_t buf_bytes);
 
 #ifdef __cplusplus
 }

@@ -48,9 +48,10 @@ _SIGS = {
     "fdc_cic_layer_backward": [_P, _P, _P, _P, _P, _P, _P, _SZ, _P],
     "fdc_full_forward": [_P, _P, _P, _P, _P, _P, _SZ, _P],
     "fdc_full_backward": [_P, _P, _P, _P, _P, _P, _P, _SZ, _P],
-    "fdc_kernel_timing_enable": [_I],
+    "fdc_kernel_timing_enable": [_I, ctypes.c_char_p],
     "fdc_kernel_timing_disable": [],
     "fdc_kernel_timing_report": [ctypes.c_char_p, _SZ],
+    "fdc_kernel_timing_launches": [ctypes.c_char_p, _SZ],
 }
 _RESTYPES = {"fdc_status_string": ctypes.c_char_p, "fdc_last_error": ctypes.c_char_p, "fdc_version": _I}
 

@@ -63,6 +63,7 @@ struct Timing {
   int used = 0;
   std::vector<hipEvent_t> start, stop;
   std::vector<const char *> names;
+  std::string only;  // record only launches of this kernel name (empty: all)
 };
 Timing &timing() {
   static Timing t;
@@ -85,14 +86,16 @@ void timing_before(const char *name, hipStream_t s) {
   if (!t.enabled) return;
   std::lock_guard<std::mutex> g(t.mu);
   if (t.used >= t.max) return;
+  if (!t.only.empty() && t.only != name) return;
   t.names[t.used] = name;
   hipEventRecord(t.start[t.used], s);
 }
-void timing_after(const char *, hipStream_t s) {
+void timing_after(const char *name, hipStream_t s) {
   Timing &t = timing();
   if (!t.enabled) return;
   std::lock_guard<std::mutex> g(t.mu);
   if (t.used >= t.max) return;
+  if (!t.only.empty() && t.only != name) return;
   hipEventRecord(t.stop[t.used], s);
   ++t.used;
 }
@@ -434,7 +437,7 @@ fdc_status fdc_full_backward(const fdc_layer_plan *p, const float *, const void 
 // ---------------------------------------------------------------------------
 // kernel timing
 // ---------------------------------------------------------------------------
-fdc_status fdc_kernel_timing_enable(int max_launches) {
+fdc_status fdc_kernel_timing_enable(int max_launches, const char *only_kernel) {
   if (max_launches < 1) return fail(FDC_EINVAL, "max_launches must be >= 1");
   Timing &t = timing();
   std::lock_guard<std::mutex> g(t.mu);
@@ -452,6 +455,7 @@ fdc_status fdc_kernel_timing_enable(int max_launches) {
   }
   t.max = max_launches;
   t.used = 0;
+  t.only = only_kernel ? only_kernel : "";
   t.enabled = true;
   return FDC_OK;
 }
@@ -481,6 +485,25 @@ fdc_status fdc_kernel_timing_report(char *buf, size_t buf_bytes) {
   for (auto &kv : acc) {
     char line[256];
     snprintf(line, sizeof line, "%s %d %.6f\n", kv.first.c_str(), kv.second.first, kv.second.second);
+    out += line;
+  }
+  if (out.size() + 1 > buf_bytes) return fail(FDC_EINVAL, "report needs %zu bytes", out.size() + 1);
+  memcpy(buf, out.c_str(), out.size() + 1);
+  return FDC_OK;
+}
+
+fdc_status fdc_kernel_timing_launches(char *buf, size_t buf_bytes) {
+  if (buf == nullptr || buf_bytes == 0) return fail(FDC_EINVAL, "buffer is NULL or empty");
+  Timing &t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  std::string out;
+  for (int i = 0; i < t.used; ++i) {
+    if (hipEventSynchronize(t.stop[i]) != hipSuccess) return fail(FDC_EHIP, "hipEventSynchronize failed");
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, t.start[i], t.stop[i]) != hipSuccess)
+      return fail(FDC_EHIP, "hipEventElapsedTime failed");
+    char line[256];
+    snprintf(line, sizeof line, "%s %.6f\n", t.names[i], ms);
     out += line;
   }
   if (out.size() + 1 > buf_bytes) return fail(FDC_EINVAL, "report needs %zu bytes", out.size() + 1);

@@ -131,8 +131,10 @@ def test_cic_spectral_validation():
 
 
 def test_timing_api_arguments():
-    assert _lib.status("fdc_kernel_timing_enable", 0) == FDC_EINVAL
+    assert _lib.status("fdc_kernel_timing_enable", 0, None) == FDC_EINVAL
+    assert _lib.status("fdc_kernel_timing_enable", -3, b"row_r2c_64") == FDC_EINVAL
     assert _lib.status("fdc_kernel_timing_report", None, 0) == FDC_EINVAL
+    assert _lib.status("fdc_kernel_timing_launches", None, 0) == FDC_EINVAL
 
 
 def test_destroyed_plan_is_refused():
