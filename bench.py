@@ -50,7 +50,8 @@ def step_launches(wl, input_grad=False):
     for i in range(wl.layers):
         B, C, S, N, M, L, _ = layer_dims(wl, i)
         out.append((f"row_r2c_{N}", F32 * B * C * N * N + C64 * B * C * N * L))
-        out.append((f"col_fwd_cic_{N}_{M}", C64 * (B * C * N * L + S * M * L + B * S * M * L + B * C * M * L)))
+        out.append((f"col_fwd_crop_{N}_{M}", C64 * (B * C * N * L + B * C * M * L)))
+        out.append((f"col_cic_inv_{N}_{M}", C64 * (B * C * M * L + S * M * L + B * S * M * L)))
         out.append((f"row_c2r_{M}", C64 * B * S * M * L + F32 * B * S * M * M))
     for i in reversed(range(wl.layers)):
         B, C, S, N, M, L, NF = layer_dims(wl, i)

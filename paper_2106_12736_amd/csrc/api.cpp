@@ -320,7 +320,7 @@ fdc_status fdc_cic_layer_plan_create(fdc_layer_plan **plan, int B, int C, int S,
   p->out = artifact_out(M, artifact, p->kn);
   const size_t L = (size_t)M / 2 + 1;
   const size_t c64 = sizeof(fdc_c64);
-  p->fwd_ws = ((size_t)B * C * N * L + (size_t)B * S * M * L) * c64;  // T, U
+  p->fwd_ws = ((size_t)B * C * N * L + (size_t)B * S * M * L + (size_t)B * C * M * L) * c64;  // T, U, Xh
   p->saved = (size_t)B * C * M * L * c64;                            // pooled input spectrum
   p->bwd_ws = ((size_t)B * S * M * L + (size_t)B * C * N * L) * c64;  // Tg, V
   *plan = p;
@@ -366,12 +366,14 @@ fdc_status fdc_cic_layer_forward(const fdc_layer_plan *p, const float *x, const 
   const int B = p->B, C = p->C, S = p->S, N = p->N, M = p->M, L = M / 2 + 1;
   auto *T = reinterpret_cast<float2 *>(ws);
   auto *U = T + (size_t)B * C * N * L;
+  // the pooled input spectrum goes to `saved` when the caller keeps it, else to the workspace
+  auto *Xh = saved != nullptr ? reinterpret_cast<float2 *>(saved) : U + (size_t)B * S * M * L;
   ImgView id{0, 0, N, N};
   if (fdc_status st = check_hip(fdc::launch_row_r2c(N, x, T, (long long)B * C, N, id, (long long)N * N, L, L,
                                                     (long long)N * L, 1.f, 1.f, s), "layer forward rows"))
     return st;
-  if (fdc_status st = check_hip(fdc::launch_col_fwd_cic(N, M, T, reinterpret_cast<const float2 *>(K), U,
-                                                        reinterpret_cast<float2 *>(saved), B, C, S, s),
+  if (fdc_status st = check_hip(fdc::launch_col_fwd_cic(N, M, T, reinterpret_cast<const float2 *>(K), U, Xh, B, C,
+                                                        S, s),
                                 "layer forward columns"))
     return st;
   return check_hip(fdc::launch_row_c2r(M, U, y, (long long)B * S, M, L, L, (long long)M * L,

@@ -218,27 +218,33 @@ struct Dft {
 // ---------------------------------------------------------------------------
 template <int N>
 struct FftCfg;
-#define FDC_FFT_CFG(N_, TPS_, R0_, R1_, R2_)                 \
-  template <>                                               \
-  struct FftCfg<N_> {                                       \
-    static constexpr int N = N_;                            \
-    static constexpr int TPS = TPS_;                        \
-    static constexpr int E = N_ / TPS_;                     \
-    static constexpr int R[3] = {R0_, R1_, R2_};            \
-    static constexpr int P = (R1_ == 1) ? 1 : (R2_ == 1 ? 2 : 3); \
+// TPS threads per sequence, E = N / TPS elements per thread, radices of the
+// Stockham passes in order (1 = unused).  Every radix must divide E so that
+// each thread runs whole butterflies in every pass.  E is kept at 8..16 (16..32
+// VGPRs of data) so that kernels stay at 4 or more waves per SIMD; TPS grows
+// with N, which lets the thread layouts of an N- and an M-point transform
+// (M < N) nest inside one workgroup.
+#define FDC_FFT_CFG(N_, TPS_, R0_, R1_, R2_, R3_)                                  \
+  template <>                                                                     \
+  struct FftCfg<N_> {                                                             \
+    static constexpr int N = N_;                                                  \
+    static constexpr int TPS = TPS_;                                              \
+    static constexpr int E = N_ / TPS_;                                           \
+    static constexpr int R[4] = {R0_, R1_, R2_, R3_};                             \
+    static constexpr int P = (R1_ == 1) ? 1 : (R2_ == 1 ? 2 : (R3_ == 1 ? 3 : 4)); \
   };
 //            N   TPS  radices
-FDC_FFT_CFG(2, 1, 2, 1, 1)
-FDC_FFT_CFG(4, 1, 4, 1, 1)
-FDC_FFT_CFG(8, 1, 8, 1, 1)
-FDC_FFT_CFG(16, 1, 16, 1, 1)
-FDC_FFT_CFG(32, 4, 8, 4, 1)
-FDC_FFT_CFG(64, 8, 8, 8, 1)
-FDC_FFT_CFG(128, 8, 16, 8, 1)
-FDC_FFT_CFG(256, 16, 16, 16, 1)
-FDC_FFT_CFG(512, 16, 16, 32, 1)
-FDC_FFT_CFG(1024, 32, 32, 32, 1)
-FDC_FFT_CFG(224, 4, 7, 8, 4)
+FDC_FFT_CFG(2, 1, 2, 1, 1, 1)
+FDC_FFT_CFG(4, 1, 4, 1, 1, 1)
+FDC_FFT_CFG(8, 1, 8, 1, 1, 1)
+FDC_FFT_CFG(16, 2, 8, 2, 1, 1)
+FDC_FFT_CFG(32, 4, 8, 4, 1, 1)
+FDC_FFT_CFG(64, 8, 8, 8, 1, 1)
+FDC_FFT_CFG(128, 8, 16, 8, 1, 1)
+FDC_FFT_CFG(256, 32, 8, 8, 4, 1)
+FDC_FFT_CFG(512, 64, 8, 8, 8, 1)
+FDC_FFT_CFG(1024, 64, 16, 8, 8, 1)
+FDC_FFT_CFG(224, 8, 7, 4, 4, 2)
 #undef FDC_FFT_CFG
 
 template <int N>

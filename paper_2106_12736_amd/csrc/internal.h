@@ -45,7 +45,7 @@ hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long lo
                           long long in_plane_stride, long long out_plane_stride, hipStream_t s);
 
 // Fused CIC + FDP column kernels (square n x n images pooled to m x m; L = m/2 + 1).
-//   fwd:   T [B][C][n][L] -> U [B][S][m][L], Xh [B][C][m][L] (nullable)
+//   fwd:   T [B][C][n][L] -> Xh [B][C][m][L] (written, then read) -> U [B][S][m][L]
 //   bwd_gk: Tg [B][S][m][L], Xh -> gK [S][n][n/2+1] at the kept bins
 //   bwd_gx: Tg, K -> V [B][C][n][L]
 bool cic_pair_supported(int n, int m);

@@ -1,20 +1,20 @@
 // HIP kernels of the CIC + FDP layer path for gfx950, and their launchers.
 //
 // Layer forward (section 2.4.1, Algorithm 1 inside Algorithm 2, FDP of 2.4.2):
-//   k_row_r2c     real rows of x -> half-spectrum rows, only the m/2+1 columns FDP keeps
-//   k_col_fwd_cic column DFT (n) -> keep the m rows FDP keeps -> save them -> for each of
-//                 the J kernels: CIC product (Eq. 5) -> inverse column DFT (m)
-//   k_row_c2r     inverse real row DFT (m) with real-part semantics and 1/m^2
+//   k_row_r2c      real rows of x -> half-spectrum rows, only the m/2+1 columns FDP keeps
+//   k_col_fwd_crop column DFT (n) -> keep the m rows FDP keeps (the saved spectrum)
+//   k_col_cic_inv  for each output channel: CIC product (Eq. 5) -> inverse column DFT (m)
+//   k_row_c2r      inverse real row DFT (m) with real-part semantics and 1/m^2
 // Layer backward:
 //   k_row_r2c     upstream gradient -> (c_l/m^2) weighted half spectrum
-//   k_col_bwd_gk  column DFT (m), dL/dK = sum_b G conj(Xhat), one workgroup per
-//                 (output channel, column tile) looping over the batch (fixed order)
+//   k_col_bwd_gk  column DFT (m), dL/dK = sum_b G conj(Xhat); the batch is split over
+//                 wave groups of one workgroup and summed in a fixed order
 //   k_col_bwd_gx  column DFTs (m) of the J gradients, sum_j G conj(K), zero-padded
 //                 inverse column DFT (n)
 //   k_row_c2r     adjoint row transform (n)
 // Intermediates stay row-major [plane][row][column]; column kernels own CT adjacent
-// columns with the column index fastest across lanes, so every global access is a
-// run of CT consecutive complex values.
+// columns (numbered across planes) with the column index fastest across lanes, so
+// every global access is a run of up to CT consecutive complex values.
 #include "fft.h"
 #include "internal.h"
 
@@ -51,9 +51,10 @@ extern __shared__ float2 g_lds[];
 // ---------------------------------------------------------------------------
 // row transforms
 // ---------------------------------------------------------------------------
+// Row pairs per workgroup: 256 threads, at most 64 pairs.
 template <int N>
 constexpr int row_spw() {
-  constexpr int s = 128 / FftCfg<N>::TPS;
+  constexpr int s = 256 / FftCfg<N>::TPS;
   return s > 64 ? 64 : s;
 }
 
@@ -158,31 +159,52 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(
 
 // ---------------------------------------------------------------------------
 // column transforms
+//
+// Column kernels see their input as `planes` row-major [rows][L] complex
+// images and number the columns of all planes consecutively, q = plane * L + l.
+// A workgroup owns CT consecutive columns (which may straddle two planes), so
+// only the last tile of a launch is ragged, whatever L is.  Lanes run fastest
+// along the columns: each global access is a run of up to CT consecutive
+// complex values of one row.
 // ---------------------------------------------------------------------------
 template <int N>
 constexpr int col_ct() {
-  return N >= 512 ? 8 : 16;
+  return FftCfg<N>::TPS >= 64 ? 8 : (FftCfg<N>::TPS >= 32 ? 16 : 32);
+}
+
+struct ColRef {
+  long long plane;
+  int l;
+  bool ok;
+};
+
+template <int CT>
+__device__ __forceinline__ ColRef column_ref(long long tile, int s, int L, long long ncols) {
+  const long long q = tile * CT + s;
+  ColRef r;
+  r.ok = q < ncols;
+  const long long qq = r.ok ? q : ncols - 1;
+  r.plane = qq / L;
+  r.l = (int)(qq - r.plane * L);
+  return r;
 }
 
 template <int N, int CT, int DIR>
-__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft(const float2 *in, float2 *out, int L, int tiles,
-                                                               long long in_plane_stride,
+__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft(const float2 *in, float2 *out, int L,
+                                                               long long ncols, long long in_plane_stride,
                                                                long long out_plane_stride) {
   using Cfg = FftCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   float2 *lds = g_lds;
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  const long long plane = bid / tiles;
-  const int l = (bid % tiles) * CT + s;
-  const bool ok = l < L;
-  const float2 *ip = in + plane * in_plane_stride + l;
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, ncols);
+  const float2 *ip = in + c.plane * in_plane_stride + c.l;
   float2 v[E];
 #pragma unroll
-  for (int m = 0; m < E; ++m) v[m] = ok ? ip[(long long)(t + TPS * m) * L] : make_float2(0.f, 0.f);
+  for (int m = 0; m < E; ++m) v[m] = c.ok ? ip[(long long)(t + TPS * m) * L] : make_float2(0.f, 0.f);
   fft_seq<N, DIR>(v, t, lds, s, CT);
-  if (!ok) return;
-  float2 *op = out + plane * out_plane_stride + l;
+  if (!c.ok) return;
+  float2 *op = out + c.plane * out_plane_stride + c.l;
 #pragma unroll
   for (int m = 0; m < E; ++m) op[(long long)(t + TPS * m) * L] = v[m];
 }
@@ -191,6 +213,129 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft(const float2 *in
 template <int N, int M>
 __device__ __forceinline__ int kept_row(int mrow) {
   return mrow < M / 2 ? mrow : mrow + (N - M);
+}
+
+// Forward, first half: column DFT (N) of the pruned row spectra, keep the M rows
+// FDP keeps.  T [planes][N][L] -> Xh [planes][M][L] (the pooled input spectrum).
+template <int N, int M, int CT>
+__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fwd_crop(const float2 *__restrict__ T,
+                                                                    float2 *__restrict__ Xh, long long ncols) {
+  using CN = FftCfg<N>;
+  constexpr int L = M / 2 + 1, TPS = CN::TPS, E = CN::E;
+  float2 *lds = g_lds;
+  const int s = threadIdx.x % CT, t = threadIdx.x / CT;
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, ncols);
+  const float2 *tcol = T + c.plane * N * L + c.l;
+  float2 v[E];
+#pragma unroll
+  for (int m = 0; m < E; ++m) v[m] = c.ok ? tcol[(long long)(t + TPS * m) * L] : make_float2(0.f, 0.f);
+  fft_seq<N, -1>(v, t, lds, s, CT);
+  if (!c.ok) return;
+  float2 *xh = Xh + c.plane * M * L + c.l;
+#pragma unroll
+  for (int m = 0; m < E; ++m) {
+    const int k = t + TPS * m;
+    if (k < M / 2) xh[(long long)k * L] = v[m];
+    else if (k >= N - M / 2) xh[(long long)(k - (N - M)) * L] = v[m];
+  }
+}
+
+// Forward, second half: for every output channel o = c*J + j, the CIC product
+// (Eq. 5) of the pooled spectrum with kernel o at the kept bins, then the inverse
+// column DFT (M).  Xh [B][C][M][L], K [S][N][N/2+1] -> U [B][S][M][L].
+template <int N, int M, int CT>
+__global__ __launch_bounds__(CT *FftCfg<M>::TPS) void k_col_cic_inv(const float2 *__restrict__ Xh,
+                                                                   const float2 *__restrict__ K,
+                                                                   float2 *__restrict__ U, int C, int J,
+                                                                   long long ncols) {
+  using CM = FftCfg<M>;
+  constexpr int L = M / 2 + 1, NF = N / 2 + 1, TPS = CM::TPS, E = CM::E;
+  float2 *lds = g_lds;
+  const int s = threadIdx.x % CT, t = threadIdx.x / CT;
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, ncols);
+  const int S = C * J;
+  const long long b = c.plane / S;
+  const int o = (int)(c.plane - b * S);
+  const float2 *xcol = Xh + (b * C + o / J) * M * L + c.l;
+  const float2 *kcol = K + (long long)o * N * NF + c.l;
+  float2 z[E];
+#pragma unroll
+  for (int m = 0; m < E; ++m) {
+    const int mrow = t + TPS * m;
+    z[m] = c.ok ? cmul(xcol[(long long)mrow * L], kcol[(long long)kept_row<N, M>(mrow) * NF])
+                : make_float2(0.f, 0.f);
+  }
+  fft_seq<M, +1>(z, t, lds, s, CT);
+  if (!c.ok) return;
+  float2 *ucol = U + c.plane * M * L + c.l;
+#pragma unroll
+  for (int m = 0; m < E; ++m) ucol[(long long)(t + TPS * m) * L] = z[m];
+}
+
+// Batch groups of the dK kernel: BP groups of CT x TPS threads split the batch,
+// up to 512 threads per workgroup.
+template <int M>
+constexpr int gk_bp() {
+  constexpr int bp = 512 / (col_ct<M>() * FftCfg<M>::TPS);
+  return bp < 1 ? 1 : (bp > 8 ? 8 : bp);
+}
+
+// Backward, dL/dK: for columns q = o * L + l of the kernel gradient, column DFT (M)
+// of each upstream-gradient column Tg[b][o] and dK += G conj(Xh[b][o/J]).
+// Group g of the BP groups sums b = g, g + BP, ...; the BP partial sums are then
+// added in group order, so the result does not depend on scheduling.
+// Writes gK [S][N][N/2+1] at the kept bins only.
+template <int M, int CT, int BP>
+__global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const float2 *__restrict__ Tg,
+                                                                      const float2 *__restrict__ Xh,
+                                                                      float2 *__restrict__ gK, int B, int C,
+                                                                      int J, int N, long long ncols) {
+  using CM = FftCfg<M>;
+  constexpr int L = M / 2 + 1, TPS = CM::TPS, E = CM::E;
+  float2 *lds = g_lds;
+  const int s = threadIdx.x % CT, t = (threadIdx.x / CT) % TPS, g = threadIdx.x / (CT * TPS);
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, ncols);
+  const int o = (int)c.plane, ci = o / J, S = C * J;
+  float2 acc[E];
+#pragma unroll
+  for (int m = 0; m < E; ++m) acc[m] = make_float2(0.f, 0.f);
+  for (int b0 = 0; b0 < B; b0 += BP) {
+    const int b = b0 + g;
+    const bool act = c.ok && b < B;
+    const float2 *gcol = Tg + ((long long)b * S + o) * M * L + c.l;
+    const float2 *xcol = Xh + ((long long)b * C + ci) * M * L + c.l;
+    float2 v[E];
+#pragma unroll
+    for (int m = 0; m < E; ++m) v[m] = act ? gcol[(long long)(t + TPS * m) * L] : make_float2(0.f, 0.f);
+    fft_seq<M, -1>(v, t, lds, g * M * CT + s, CT);
+    if (act) {
+#pragma unroll
+      for (int m = 0; m < E; ++m) acc[m] = cfmac(acc[m], v[m], xcol[(long long)(t + TPS * m) * L]);
+    }
+  }
+  if constexpr (BP > 1) {
+    __syncthreads();
+#pragma unroll
+    for (int m = 0; m < E; ++m) lds[lds_phys(g * M * CT + s + (t + TPS * m) * CT)] = acc[m];
+    __syncthreads();
+    if (g != 0) return;
+#pragma unroll
+    for (int m = 0; m < E; ++m) {
+      float2 sum = lds[lds_phys(s + (t + TPS * m) * CT)];
+#pragma unroll
+      for (int q = 1; q < BP; ++q) sum = cadd(sum, lds[lds_phys(q * M * CT + s + (t + TPS * m) * CT)]);
+      acc[m] = sum;
+    }
+  }
+  if (!c.ok) return;
+  const int nf = N / 2 + 1;
+  float2 *kcol = gK + (long long)o * N * nf + c.l;
+#pragma unroll
+  for (int m = 0; m < E; ++m) {
+    const int mrow = t + TPS * m;
+    const int krow = mrow < M / 2 ? mrow : mrow + (N - M);
+    kcol[(long long)krow * nf] = acc[m];
+  }
 }
 
 template <int N, int M>
@@ -204,11 +349,16 @@ constexpr int cic_lds_elems() {
   return lds_size(a > b ? a : b);
 }
 
+// Backward, dL/dx: for columns q = (b*C + c) * L + l, column DFTs (M) of the J
+// upstream-gradient columns Tg[b][cJ+j], dXh = sum_j G conj(K[cJ+j]) at the kept
+// bins, FDP adjoint (zero rows at the dropped frequencies), inverse column DFT (N).
+// The thread layout of the N-point transform holds JP = TPS_N / TPS_M groups of
+// the M-point layout, which take the J products in turns.
 template <int N, int M, int CT>
-__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fwd_cic(const float2 *__restrict__ T,
-                                                                   const float2 *__restrict__ K,
-                                                                   float2 *__restrict__ U, float2 *__restrict__ Xh,
-                                                                   int C, int J, int tiles) {
+__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 *__restrict__ Tg,
+                                                                  const float2 *__restrict__ K,
+                                                                  float2 *__restrict__ V, int C, int J,
+                                                                  long long ncols) {
   using CN = FftCfg<N>;
   using CM = FftCfg<M>;
   constexpr int L = M / 2 + 1, NF = N / 2 + 1;
@@ -217,126 +367,20 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fwd_cic(const float2
   float2 *lds = g_lds;
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   const int tp = t % TPSM, js = t / TPSM;
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  const int bc = bid / tiles;
-  const int b = bc / C, c = bc - b * C;
-  const int l = (bid % tiles) * CT + s;
-  const bool ok = l < L;
-
-  // column DFT of length N
-  const float2 *tcol = T + (long long)bc * N * L + l;
-  float2 v[CN::E];
-#pragma unroll
-  for (int m = 0; m < CN::E; ++m) v[m] = ok ? tcol[(long long)(t + TPSN * m) * L] : make_float2(0.f, 0.f);
-  fft_seq<N, -1>(v, t, lds, s, CT);
-  __syncthreads();
-
-  // FDP: keep rows [0, M/2) and [N - M/2, N); save them for the backward pass
-  float2 *xh = (Xh != nullptr && ok) ? Xh + (long long)bc * M * L + l : nullptr;
-#pragma unroll
-  for (int m = 0; m < CN::E; ++m) {
-    const int k = t + TPSN * m;
-    if (k < M / 2 || k >= N - M / 2) {
-      const int mrow = k < M / 2 ? k : k - (N - M);
-      lds[lds_phys(s + mrow * CT)] = v[m];
-      if (xh) xh[(long long)mrow * L] = v[m];
-    }
-  }
-  __syncthreads();
-  float2 xr[CM::E];
-#pragma unroll
-  for (int m = 0; m < CM::E; ++m) xr[m] = lds[lds_phys(s + (tp + TPSM * m) * CT)];
-
-  // CIC (Eq. 5): J products per input channel, each followed by the inverse column DFT (M)
-  const long long out_plane0 = (long long)b * C * J;
-  for (int j0 = 0; j0 < J; j0 += JP) {
-    const int j = j0 + js;
-    const bool act = ok && j < J;
-    const int o = c * J + j;
-    const float2 *kcol = K + (long long)o * N * NF + l;
-    float2 z[CM::E];
-#pragma unroll
-    for (int m = 0; m < CM::E; ++m) {
-      const int mrow = tp + TPSM * m;
-      z[m] = act ? cmul(xr[m], kcol[(long long)kept_row<N, M>(mrow) * NF]) : make_float2(0.f, 0.f);
-    }
-    fft_seq<M, +1>(z, tp, lds, js * M * CT + s, CT);
-    if (act) {
-      float2 *ucol = U + (out_plane0 + o) * M * L + l;
-#pragma unroll
-      for (int m = 0; m < CM::E; ++m) ucol[(long long)(tp + TPSM * m) * L] = z[m];
-    }
-  }
-}
-
-template <int M, int CT>
-__global__ __launch_bounds__(CT *FftCfg<M>::TPS) void k_col_bwd_gk(const float2 *__restrict__ Tg,
-                                                                  const float2 *__restrict__ Xh,
-                                                                  float2 *__restrict__ gK, int B, int C, int J,
-                                                                  int N, int tiles) {
-  using CM = FftCfg<M>;
-  constexpr int L = M / 2 + 1, TPS = CM::TPS, E = CM::E;
-  float2 *lds = g_lds;
-  const int s = threadIdx.x % CT, t = threadIdx.x / CT;
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  const int o = bid / tiles;
-  const int c = o / J;
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, ncols);
+  const long long b = c.plane / C;
+  const int ci = (int)(c.plane - b * C);
   const int S = C * J;
-  const int l = (bid % tiles) * CT + s;
-  const bool ok = l < L;
-  float2 acc[E];
-#pragma unroll
-  for (int m = 0; m < E; ++m) acc[m] = make_float2(0.f, 0.f);
-  for (int b = 0; b < B; ++b) {
-    const float2 *gcol = Tg + ((long long)b * S + o) * M * L + l;
-    const float2 *xcol = Xh + ((long long)b * C + c) * M * L + l;
-    float2 v[E];
-#pragma unroll
-    for (int m = 0; m < E; ++m) v[m] = ok ? gcol[(long long)(t + TPS * m) * L] : make_float2(0.f, 0.f);
-    fft_seq<M, -1>(v, t, lds, s, CT);
-    if (ok) {
-#pragma unroll
-      for (int m = 0; m < E; ++m) acc[m] = cfmac(acc[m], v[m], xcol[(long long)(t + TPS * m) * L]);
-    }
-  }
-  if (!ok) return;
-  const int nf = N / 2 + 1;
-  float2 *kcol = gK + (long long)o * N * nf + l;
-#pragma unroll
-  for (int m = 0; m < E; ++m) {
-    const int mrow = t + TPS * m;
-    const int krow = mrow < M / 2 ? mrow : mrow + (N - M);
-    kcol[(long long)krow * nf] = acc[m];
-  }
-}
-
-template <int N, int M, int CT>
-__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 *__restrict__ Tg,
-                                                                  const float2 *__restrict__ K,
-                                                                  float2 *__restrict__ V, int C, int J, int tiles) {
-  using CN = FftCfg<N>;
-  using CM = FftCfg<M>;
-  constexpr int L = M / 2 + 1, NF = N / 2 + 1;
-  constexpr int TPSN = CN::TPS, TPSM = CM::TPS, JP = cic_jp<N, M>();
-  float2 *lds = g_lds;
-  const int s = threadIdx.x % CT, t = threadIdx.x / CT;
-  const int tp = t % TPSM, js = t / TPSM;
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  const int bc = bid / tiles;
-  const int b = bc / C, c = bc - b * C;
-  const int S = C * J;
-  const int l = (bid % tiles) * CT + s;
-  const bool ok = l < L;
 
   float2 acc[CM::E];
 #pragma unroll
   for (int m = 0; m < CM::E; ++m) acc[m] = make_float2(0.f, 0.f);
   for (int j0 = 0; j0 < J; j0 += JP) {
     const int j = j0 + js;
-    const bool act = ok && j < J;
-    const int o = c * J + j;
-    const float2 *gcol = Tg + ((long long)b * S + o) * M * L + l;
-    const float2 *kcol = K + (long long)o * N * NF + l;
+    const bool act = c.ok && j < J;
+    const int o = ci * J + (act ? j : 0);
+    const float2 *gcol = Tg + (b * S + o) * M * L + c.l;
+    const float2 *kcol = K + (long long)o * N * NF + c.l;
     float2 g[CM::E];
 #pragma unroll
     for (int m = 0; m < CM::E; ++m) g[m] = act ? gcol[(long long)(tp + TPSM * m) * L] : make_float2(0.f, 0.f);
@@ -365,8 +409,8 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
     w[m] = sum;
   }
   fft_seq<N, +1>(w, t, lds, s, CT);
-  if (!ok) return;
-  float2 *vcol = V + (long long)bc * N * L + l;
+  if (!c.ok) return;
+  float2 *vcol = V + c.plane * N * L + c.l;
 #pragma unroll
   for (int m = 0; m < CN::E; ++m) vcol[(long long)(t + TPSN * m) * L] = w[m];
 }
@@ -521,12 +565,6 @@ static hipError_t launch(const char *name, Kern kern, unsigned grid, unsigned bl
   return e;
 }
 
-template <class T>
-static const char *kname(const char *base, T n) {
-  static const std::string name = std::string(base) + "_" + std::to_string(n);
-  return name.c_str();
-}
-
 static unsigned grid_stride_blocks(long long total, int block) {
   long long g = (total + block - 1) / block;
   if (g > 1048576) g = 1048576;
@@ -567,23 +605,24 @@ hipError_t launch_row_c2r(int n, const float2 *in, float *y, long long planes, i
   return err;
 }
 
+static unsigned col_tiles(long long ncols, int ct) { return (unsigned)((ncols + ct - 1) / ct); }
+
 hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long long planes, int L,
                           long long in_plane_stride, long long out_plane_stride, hipStream_t s) {
   hipError_t err = hipErrorInvalidValue;
   dispatch_n(n, [&](auto nc) {
     constexpr int N = decltype(nc)::value;
     constexpr int CT = col_ct<N>();
-    const int tiles = (L + CT - 1) / CT;
-    const unsigned grid = (unsigned)(planes * tiles);
+    const long long ncols = planes * L;
     const size_t lds = lds_size(N * CT) * sizeof(float2);
     static const std::string nf = "col_fft_fwd_" + std::to_string(N);
     static const std::string ni = "col_fft_inv_" + std::to_string(N);
     if (dir < 0)
-      err = launch(nf.c_str(), k_col_fft<N, CT, -1>, grid, CT * FftCfg<N>::TPS, lds, s, in, out, L, tiles,
-                   in_plane_stride, out_plane_stride);
+      err = launch(nf.c_str(), k_col_fft<N, CT, -1>, col_tiles(ncols, CT), CT * FftCfg<N>::TPS, lds, s, in, out, L,
+                   ncols, in_plane_stride, out_plane_stride);
     else
-      err = launch(ni.c_str(), k_col_fft<N, CT, +1>, grid, CT * FftCfg<N>::TPS, lds, s, in, out, L, tiles,
-                   in_plane_stride, out_plane_stride);
+      err = launch(ni.c_str(), k_col_fft<N, CT, +1>, col_tiles(ncols, CT), CT * FftCfg<N>::TPS, lds, s, in, out, L,
+                   ncols, in_plane_stride, out_plane_stride);
   });
   return err;
 }
@@ -593,14 +632,16 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
   hipError_t err = hipErrorInvalidValue;
   dispatch_nm(n, m, [&](auto nc, auto mc) {
     constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
-    constexpr int CT = col_ct<N>();
     constexpr int L = M / 2 + 1;
-    const int tiles = (L + CT - 1) / CT;
-    const unsigned grid = (unsigned)((long long)B * C * tiles);
-    const size_t lds = cic_lds_elems<N, M, CT>() * sizeof(float2);
-    static const std::string nm = "col_fwd_cic_" + std::to_string(N) + "_" + std::to_string(M);
-    err = launch(nm.c_str(), k_col_fwd_cic<N, M, CT>, grid, CT * FftCfg<N>::TPS, lds, s, T, K, U, Xh, C, S / C,
-                 tiles);
+    constexpr int CTN = col_ct<N>(), CTM = col_ct<M>();
+    static const std::string n1 = "col_fwd_crop_" + std::to_string(N) + "_" + std::to_string(M);
+    static const std::string n2 = "col_cic_inv_" + std::to_string(N) + "_" + std::to_string(M);
+    const long long nin = (long long)B * C * L, nout = (long long)B * S * L;
+    err = launch(n1.c_str(), k_col_fwd_crop<N, M, CTN>, col_tiles(nin, CTN), CTN * FftCfg<N>::TPS,
+                 lds_size(N * CTN) * sizeof(float2), s, T, Xh, nin);
+    if (err != hipSuccess) return;
+    err = launch(n2.c_str(), k_col_cic_inv<N, M, CTM>, col_tiles(nout, CTM), CTM * FftCfg<M>::TPS,
+                 lds_size(M * CTM) * sizeof(float2), s, Xh, K, U, C, S / C, nout);
   });
   return err;
 }
@@ -611,14 +652,13 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
   if (!cic_pair_supported(n, m)) return err;
   dispatch_n(m, [&](auto mc) {
     constexpr int M = decltype(mc)::value;
-    constexpr int CT = col_ct<M>();
+    constexpr int CT = col_ct<M>(), BP = gk_bp<M>();
     constexpr int L = M / 2 + 1;
-    const int tiles = (L + CT - 1) / CT;
-    const unsigned grid = (unsigned)((long long)S * tiles);
-    const size_t lds = lds_size(M * CT) * sizeof(float2);
+    const long long ncols = (long long)S * L;
+    const size_t lds = lds_size(BP * M * CT) * sizeof(float2);
     static const std::string nm = "col_bwd_gk_" + std::to_string(M);
-    err = launch(nm.c_str(), k_col_bwd_gk<M, CT>, grid, CT * FftCfg<M>::TPS, lds, s, Tg, Xh, gK, B, C, S / C, n,
-                 tiles);
+    err = launch(nm.c_str(), k_col_bwd_gk<M, CT, BP>, col_tiles(ncols, CT), CT * FftCfg<M>::TPS * BP, lds, s, Tg,
+                 Xh, gK, B, C, S / C, n, ncols);
   });
   return err;
 }
@@ -630,12 +670,11 @@ hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, fl
     constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
     constexpr int CT = col_ct<N>();
     constexpr int L = M / 2 + 1;
-    const int tiles = (L + CT - 1) / CT;
-    const unsigned grid = (unsigned)((long long)B * C * tiles);
+    const long long ncols = (long long)B * C * L;
     const size_t lds = cic_lds_elems<N, M, CT>() * sizeof(float2);
     static const std::string nm = "col_bwd_gx_" + std::to_string(N) + "_" + std::to_string(M);
-    err = launch(nm.c_str(), k_col_bwd_gx<N, M, CT>, grid, CT * FftCfg<N>::TPS, lds, s, Tg, K, V, C, S / C,
-                 tiles);
+    err = launch(nm.c_str(), k_col_bwd_gx<N, M, CT>, col_tiles(ncols, CT), CT * FftCfg<N>::TPS, lds, s, Tg, K, V, C,
+                 S / C, ncols);
   });
   return err;
 }
