@@ -56,9 +56,8 @@ def step_launches(wl, input_grad=False):
     for i in reversed(range(wl.layers)):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
         out.append((f"row_r2c_{M}", F32 * B * S * M * M + C64 * B * S * M * L))
-        out.append((f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + S * M * L)))
-        if M < N:
-            out.append(("gk_zero_dropped", C64 * S * (N * NF - M * L)))
+        # reads the upstream spectrum and the saved spectrum, writes all of gK (zeros where FDP drops)
+        out.append((f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + S * N * NF)))
         if i > 0 or input_grad:
             out.append((f"col_bwd_gx_{N}_{M}", C64 * (B * S * M * L + S * M * L + B * C * N * L)))
             out.append((f"row_c2r_{N}", C64 * B * C * N * L + F32 * B * C * N * N))
@@ -146,6 +145,9 @@ def main():
                     help="CIC stack workload (default: the 1024 x 1024 headline stack)")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
     ap.add_argument("--input-grad", action="store_true", help="also compute the input-image gradient")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="after the timed region, run one plain streaming copy kernel (dst = src * 1) over "
+                         "MIB MiB, a known-size reference for the HBM traffic counters of a profiler run")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -261,6 +263,14 @@ def main():
         "step_kernel_ms": {k: round(v[0], 5) for k, v in sorted(per_name.items(), key=lambda kv: -kv[1][0])},
         "wall_ms_per_step": wall * 1e3 / args.steps,
     }
+    if args.copy_calibration > 0:
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = 2 * 4 * n
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, data)
     print(json.dumps(out), flush=True)

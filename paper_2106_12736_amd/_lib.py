@@ -11,7 +11,8 @@ import os
 import re
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libfdc.so")
+# FDC_LIBRARY may name another build of the same library (same ABI), e.g. to compare builds.
+LIB_PATH = os.environ.get("FDC_LIBRARY") or os.path.join(_HERE, "libfdc.so")
 HEADER = os.path.join(os.path.dirname(_HERE), "include", "fdc.h")
 
 FDC_OK, FDC_EINVAL, FDC_EUNSUPPORTED, FDC_EWORKSPACE, FDC_EHIP = range(5)

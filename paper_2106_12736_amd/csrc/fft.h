@@ -254,20 +254,44 @@ constexpr int stockham_ns(int p) {  // product of the radices before pass p
   return ns;
 }
 
-// LDS addressing: an XOR swizzle inside each aligned block of 32 complex
-// values (bits 5..9 of the index flip bits 0..4).  Contiguous accesses stay
-// conflict-free and the power-of-two strides of the Stockham writes land in
-// different banks.  It is a bijection on every 32-aligned block, so a buffer
-// of lds_size(n) complex values holds indices [0, n).
-__device__ __forceinline__ int lds_phys(int i) { return i ^ ((i >> 5) & 31); }
-__host__ __device__ constexpr int lds_size(int n) { return (n + 31) & ~31; }
+// LDS addressing of the Stockham exchanges.
+//   0: plain index;
+//   1: XOR swizzle inside each aligned block of 32 complex values (bits 5..9 of
+//      the index flip bits 0..4): contiguous accesses stay conflict-free and the
+//      power-of-two strides of the Stockham writes land in different banks;
+//   2: one complex value of padding after every 32.
+// lds_size(n) complex values hold indices [0, n) in every layout.
+constexpr int kLdsLayout = 2;
+__device__ __forceinline__ int lds_phys(int i) {
+  if constexpr (kLdsLayout == 0) return i;
+  else if constexpr (kLdsLayout == 1) return i ^ ((i >> 5) & 31);
+  else return i + (i >> 5);
+}
+__host__ __device__ constexpr int lds_size(int n) {
+  return kLdsLayout == 2 ? n + (n >> 5) + 1 : (n + 31) & ~31;
+}
+
+// Barrier between the LDS writes and reads of an exchange.  WAVE: every
+// sequence lives inside one wavefront (TPS <= 64 threads and no column
+// interleaving across waves), so ordering the wave's own LDS accesses is enough;
+// LDS operations of one wavefront are performed in program order.
+template <bool WAVE>
+__device__ __forceinline__ void lds_barrier() {
+  if constexpr (WAVE) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  } else {
+    __syncthreads();
+  }
+}
 
 // Transform one sequence.  Thread t (0 <= t < TPS) holds v[m] = element t + TPS*m
 // on entry and exit.  Element e of the sequence lives in LDS at
-// lds[lds_phys(base + e * es)].  Every thread of the workgroup must call this
-// (it contains workgroup barriers).  With LEAD_SYNC the first LDS write waits
-// for every thread's earlier use of the LDS.
-template <int N, int DIR, bool LEAD_SYNC = true>
+// lds[lds_phys(base + e * es)].  Every thread of the workgroup (of the wave with
+// WAVE) must call this: it contains barriers.  With LEAD_SYNC the first LDS write
+// waits for every thread's earlier use of the LDS.
+template <int N, int DIR, bool LEAD_SYNC = true, bool WAVE = false>
 __device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2 *lds, int base, int es) {
   using C = FftCfg<N>;
   constexpr int E = C::E;
@@ -314,7 +338,7 @@ __device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2
 #pragma unroll
       for (int m = 0; m < E; ++m) v[m] = a[m];
     } else {
-      if (p > 0 || LEAD_SYNC) __syncthreads();
+      if (p > 0 || LEAD_SYNC) lds_barrier<WAVE>();
 #pragma unroll
       for (int q = 0; q < BPT; ++q) {
         const int j = t + TPS * q;
@@ -322,7 +346,7 @@ __device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2
 #pragma unroll
         for (int r = 0; r < R; ++r) lds[lds_phys(base + (jo + r * NS) * es)] = a[q + BPT * r];
       }
-      __syncthreads();
+      lds_barrier<WAVE>();
     }
   });
 }

@@ -40,13 +40,14 @@ hipError_t launch_row_c2r(int n, const float2 *in, float *y, long long planes, i
                           long long in_row_stride, long long in_plane_stride, float alpha, float beta,
                           ImgView out_view, long long out_plane_stride, hipStream_t s);
 
-// Column DFTs of length n over `L` columns of row-major [planes][n][L] complex data (in place allowed).
-hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long long planes, int L,
+// Column DFTs of length n over the first `L` columns of row-major [planes][n][ld] complex
+// data (in place allowed).
+hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long long planes, int L, int ld,
                           long long in_plane_stride, long long out_plane_stride, hipStream_t s);
 
 // Fused CIC + FDP column kernels (square n x n images pooled to m x m; L = m/2 + 1).
 //   fwd:   T [B][C][n][L] -> Xh [B][C][m][L] (written, then read) -> U [B][S][m][L]
-//   bwd_gk: Tg [B][S][m][L], Xh -> gK [S][n][n/2+1] at the kept bins
+//   bwd_gk: Tg [B][S][m][L], Xh -> gK [S][n][n/2+1]: every bin (zeros where FDP drops)
 //   bwd_gx: Tg, K -> V [B][C][n][L]
 bool cic_pair_supported(int n, int m);
 hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, float2 *U, float2 *Xh, int B,
@@ -55,7 +56,6 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
                              int S, hipStream_t s);
 hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, float2 *V, int B, int C, int S,
                              hipStream_t s);
-hipError_t launch_gk_zero_dropped(float2 *gK, int S, int n, int m, hipStream_t s);
 
 // Spectral CIC and FDP.
 hipError_t launch_cic_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, long long P,

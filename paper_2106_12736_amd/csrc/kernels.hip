@@ -30,16 +30,21 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
   return x * q + (x < rem ? x : rem) + i;
 }
 
-__device__ __forceinline__ long long view_index(const ImgView &v, int ncols, int r, int w) {
-  if (v.mode == 0) return (long long)r * v.cols_stored + w;
-  if (v.mode == 1) {
+// Element offset of logical pixel (r, w) of an image seen through `v`, or -1 when
+// the pixel is not stored (cropped away).  MODE is v.mode, fixed at compile time.
+template <int MODE>
+__device__ __forceinline__ int view_index(const ImgView &v, int ncols, int r, int w) {
+  if constexpr (MODE == 0) {
+    return r * v.cols_stored + w;
+  } else if constexpr (MODE == 1) {
     const int rr = r - v.shift, ww = w - v.shift;
-    return (rr < 0 || ww < 0) ? -1 : (long long)rr * v.cols_stored + ww;
+    return (rr < 0 || ww < 0) ? -1 : rr * v.cols_stored + ww;
+  } else {
+    int rr = r - v.shift, ww = w - v.shift;
+    rr += rr < 0 ? v.rows : 0;
+    ww += ww < 0 ? ncols : 0;
+    return rr * v.cols_stored + ww;
   }
-  int rr = r - v.shift, ww = w - v.shift;
-  rr += rr < 0 ? v.rows : 0;
-  ww += ww < 0 ? ncols : 0;
-  return (long long)rr * v.cols_stored + ww;
 }
 
 __device__ __forceinline__ float bin_weight(int l, int n, float alpha, float beta) {
@@ -58,13 +63,16 @@ constexpr int row_spw() {
   return s > 64 ? 64 : s;
 }
 
-template <int N, int SPW>
+// Real rows are transformed in pairs packed as one complex sequence z = a + i b.
+// A sequence uses TPS <= 64 threads, so a wavefront holds whole sequences and
+// the LDS exchanges need only wave-level ordering.
+template <int N, int SPW, int MODE>
 __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(
     const float *__restrict__ x, float2 *__restrict__ out, long long npairs, int rows_per_plane, ImgView view,
-    long long in_plane_stride, int L, long long out_row_stride, long long out_plane_stride, float alpha,
-    float beta) {
+    long long in_plane_stride, int L, int out_row_stride, long long out_plane_stride, float alpha, float beta) {
   using Cfg = FftCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
+  static_assert(TPS <= 64, "a row sequence must fit in one wavefront");
   float2 *lds = g_lds;
   const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
   long long pair = (long long)xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
@@ -79,15 +87,15 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(
 #pragma unroll
   for (int m = 0; m < E; ++m) {
     const int w = t + TPS * m;
-    const long long ia = view_index(view, N, r0, w);
-    const long long ib = view_index(view, N, r0 + 1, w);
+    const int ia = view_index<MODE>(view, N, r0, w);
+    const int ib = view_index<MODE>(view, N, r0 + 1, w);
     v[m] = make_float2(ia >= 0 ? xp[ia] : 0.f, ib >= 0 ? xp[ib] : 0.f);
   }
-  fft_seq<N, -1>(v, t, lds, s * N, 1);
-  __syncthreads();
+  fft_seq<N, -1, true, true>(v, t, lds, s * N, 1);
+  lds_barrier<true>();
 #pragma unroll
   for (int m = 0; m < E; ++m) lds[lds_phys(s * N + t + TPS * m)] = v[m];
-  __syncthreads();
+  lds_barrier<true>();
   if (!active) return;
   float2 *oa = out + plane * out_plane_stride + (long long)r0 * out_row_stride;
   float2 *ob = oa + out_row_stride;
@@ -101,13 +109,14 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(
   }
 }
 
-template <int N, int SPW>
+template <int N, int SPW, int MODE>
 __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(
     const float2 *__restrict__ in, float *__restrict__ y, long long npairs, int rows_per_plane, int L,
-    long long in_row_stride, long long in_plane_stride, float alpha, float beta, ImgView view,
+    int in_row_stride, long long in_plane_stride, float alpha, float beta, ImgView view,
     long long out_plane_stride) {
   using Cfg = FftCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
+  static_assert(TPS <= 64, "a row sequence must fit in one wavefront");
   float2 *lds = g_lds;
   const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
   long long pair = (long long)xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
@@ -144,14 +153,14 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(
     }
     v[m] = make_float2(a.x - b.y, a.y + b.x);  // A + i B
   }
-  fft_seq<N, +1>(v, t, lds, s * N, 1);
+  fft_seq<N, +1, true, true>(v, t, lds, s * N, 1);
   if (!active) return;
   float *yp = y + plane * out_plane_stride;
 #pragma unroll
   for (int m = 0; m < E; ++m) {
     const int w = t + TPS * m;
-    const long long oa = view_index(view, N, r0, w);
-    const long long ob = view_index(view, N, r0 + 1, w);
+    const int oa = view_index<MODE>(view, N, r0, w);
+    const int ob = view_index<MODE>(view, N, r0 + 1, w);
     if (oa >= 0) yp[oa] = v[m].x;
     if (ob >= 0) yp[ob] = v[m].y;
   }
@@ -190,7 +199,7 @@ __device__ __forceinline__ ColRef column_ref(long long tile, int s, int L, long 
 }
 
 template <int N, int CT, int DIR>
-__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft(const float2 *in, float2 *out, int L,
+__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft(const float2 *in, float2 *out, int L, int ld,
                                                                long long ncols, long long in_plane_stride,
                                                                long long out_plane_stride) {
   using Cfg = FftCfg<N>;
@@ -201,12 +210,12 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft(const float2 *in
   const float2 *ip = in + c.plane * in_plane_stride + c.l;
   float2 v[E];
 #pragma unroll
-  for (int m = 0; m < E; ++m) v[m] = c.ok ? ip[(long long)(t + TPS * m) * L] : make_float2(0.f, 0.f);
+  for (int m = 0; m < E; ++m) v[m] = c.ok ? ip[(long long)(t + TPS * m) * ld] : make_float2(0.f, 0.f);
   fft_seq<N, DIR>(v, t, lds, s, CT);
   if (!c.ok) return;
   float2 *op = out + c.plane * out_plane_stride + c.l;
 #pragma unroll
-  for (int m = 0; m < E; ++m) op[(long long)(t + TPS * m) * L] = v[m];
+  for (int m = 0; m < E; ++m) op[(long long)(t + TPS * m) * ld] = v[m];
 }
 
 // Row of the n-point spectrum that pooled row `mrow` (of m) comes from.
@@ -221,22 +230,22 @@ template <int N, int M, int CT>
 __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fwd_crop(const float2 *__restrict__ T,
                                                                     float2 *__restrict__ Xh, long long ncols) {
   using CN = FftCfg<N>;
-  constexpr int L = M / 2 + 1, TPS = CN::TPS, E = CN::E;
+  constexpr int L = M / 2 + 1, LD = L, TPS = CN::TPS, E = CN::E;
   float2 *lds = g_lds;
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, ncols);
-  const float2 *tcol = T + c.plane * N * L + c.l;
+  const float2 *tcol = T + c.plane * N * LD + c.l;
   float2 v[E];
 #pragma unroll
-  for (int m = 0; m < E; ++m) v[m] = c.ok ? tcol[(long long)(t + TPS * m) * L] : make_float2(0.f, 0.f);
+  for (int m = 0; m < E; ++m) v[m] = c.ok ? tcol[(long long)(t + TPS * m) * LD] : make_float2(0.f, 0.f);
   fft_seq<N, -1>(v, t, lds, s, CT);
   if (!c.ok) return;
-  float2 *xh = Xh + c.plane * M * L + c.l;
+  float2 *xh = Xh + c.plane * M * LD + c.l;
 #pragma unroll
   for (int m = 0; m < E; ++m) {
     const int k = t + TPS * m;
-    if (k < M / 2) xh[(long long)k * L] = v[m];
-    else if (k >= N - M / 2) xh[(long long)(k - (N - M)) * L] = v[m];
+    if (k < M / 2) xh[(long long)k * LD] = v[m];
+    else if (k >= N - M / 2) xh[(long long)(k - (N - M)) * LD] = v[m];
   }
 }
 
@@ -249,34 +258,36 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS) void k_col_cic_inv(const float2
                                                                    float2 *__restrict__ U, int C, int J,
                                                                    long long ncols) {
   using CM = FftCfg<M>;
-  constexpr int L = M / 2 + 1, NF = N / 2 + 1, TPS = CM::TPS, E = CM::E;
+  constexpr int L = M / 2 + 1, LD = L, NF = N / 2 + 1, TPS = CM::TPS, E = CM::E;
   float2 *lds = g_lds;
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, ncols);
   const int S = C * J;
   const long long b = c.plane / S;
   const int o = (int)(c.plane - b * S);
-  const float2 *xcol = Xh + (b * C + o / J) * M * L + c.l;
+  const float2 *xcol = Xh + (b * C + o / J) * M * LD + c.l;
   const float2 *kcol = K + (long long)o * N * NF + c.l;
   float2 z[E];
 #pragma unroll
   for (int m = 0; m < E; ++m) {
     const int mrow = t + TPS * m;
-    z[m] = c.ok ? cmul(xcol[(long long)mrow * L], kcol[(long long)kept_row<N, M>(mrow) * NF])
+    z[m] = c.ok ? cmul(xcol[(long long)mrow * LD], kcol[(long long)kept_row<N, M>(mrow) * NF])
                 : make_float2(0.f, 0.f);
   }
   fft_seq<M, +1>(z, t, lds, s, CT);
   if (!c.ok) return;
-  float2 *ucol = U + c.plane * M * L + c.l;
+  float2 *ucol = U + c.plane * M * LD + c.l;
 #pragma unroll
-  for (int m = 0; m < E; ++m) ucol[(long long)(t + TPS * m) * L] = z[m];
+  for (int m = 0; m < E; ++m) ucol[(long long)(t + TPS * m) * LD] = z[m];
 }
 
-// Batch groups of the dK kernel: BP groups of CT x TPS threads split the batch,
-// up to 512 threads per workgroup.
+// Geometry of the dK kernel: tiles of 8 columns (there are only S * L columns,
+// so narrow tiles keep the grid at hundreds of workgroups) and BP batch groups
+// per workgroup, up to 512 threads and at most 8 groups.
+constexpr int kGkCT = 8;
 template <int M>
 constexpr int gk_bp() {
-  constexpr int bp = 512 / (col_ct<M>() * FftCfg<M>::TPS);
+  constexpr int bp = 512 / (kGkCT * FftCfg<M>::TPS);
   return bp < 1 ? 1 : (bp > 8 ? 8 : bp);
 }
 
@@ -284,33 +295,49 @@ constexpr int gk_bp() {
 // of each upstream-gradient column Tg[b][o] and dK += G conj(Xh[b][o/J]).
 // Group g of the BP groups sums b = g, g + BP, ...; the BP partial sums are then
 // added in group order, so the result does not depend on scheduling.
-// Writes gK [S][N][N/2+1] at the kept bins only.
+// Writes all of gK [S][N][N/2+1]: the kept bins, and exact zeros at the rows and
+// columns FDP drops (rows of the tile's own columns; the columns l >= L of every
+// row are shared out over the whole grid).
 template <int M, int CT, int BP>
 __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const float2 *__restrict__ Tg,
                                                                       const float2 *__restrict__ Xh,
                                                                       float2 *__restrict__ gK, int B, int C,
                                                                       int J, int N, long long ncols) {
   using CM = FftCfg<M>;
-  constexpr int L = M / 2 + 1, TPS = CM::TPS, E = CM::E;
+  constexpr int L = M / 2 + 1, LD = L, TPS = CM::TPS, E = CM::E;
+  constexpr int NT = CT * TPS * BP;
   float2 *lds = g_lds;
   const int s = threadIdx.x % CT, t = (threadIdx.x / CT) % TPS, g = threadIdx.x / (CT * TPS);
-  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, ncols);
+  const int wg = xcd_remap(blockIdx.x, gridDim.x);
+  const ColRef c = column_ref<CT>(wg, s, L, ncols);
   const int o = (int)c.plane, ci = o / J, S = C * J;
+  const int nf = N / 2 + 1;
+
+  // zeros of the columns l >= L, grid-stride over [S][N][L, nf)
+  {
+    const int w = nf - L;
+    const long long total = (long long)S * N * w;
+    for (long long i = (long long)wg * NT + threadIdx.x; i < total; i += (long long)gridDim.x * NT) {
+      const long long row = i / w;
+      gK[row * nf + L + (i - row * w)] = make_float2(0.f, 0.f);
+    }
+  }
+
   float2 acc[E];
 #pragma unroll
   for (int m = 0; m < E; ++m) acc[m] = make_float2(0.f, 0.f);
   for (int b0 = 0; b0 < B; b0 += BP) {
     const int b = b0 + g;
     const bool act = c.ok && b < B;
-    const float2 *gcol = Tg + ((long long)b * S + o) * M * L + c.l;
-    const float2 *xcol = Xh + ((long long)b * C + ci) * M * L + c.l;
+    const float2 *gcol = Tg + ((long long)b * S + o) * M * LD + c.l;
+    const float2 *xcol = Xh + ((long long)b * C + ci) * M * LD + c.l;
     float2 v[E];
 #pragma unroll
-    for (int m = 0; m < E; ++m) v[m] = act ? gcol[(long long)(t + TPS * m) * L] : make_float2(0.f, 0.f);
+    for (int m = 0; m < E; ++m) v[m] = act ? gcol[(long long)(t + TPS * m) * LD] : make_float2(0.f, 0.f);
     fft_seq<M, -1>(v, t, lds, g * M * CT + s, CT);
     if (act) {
 #pragma unroll
-      for (int m = 0; m < E; ++m) acc[m] = cfmac(acc[m], v[m], xcol[(long long)(t + TPS * m) * L]);
+      for (int m = 0; m < E; ++m) acc[m] = cfmac(acc[m], v[m], xcol[(long long)(t + TPS * m) * LD]);
     }
   }
   if constexpr (BP > 1) {
@@ -328,7 +355,6 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
     }
   }
   if (!c.ok) return;
-  const int nf = N / 2 + 1;
   float2 *kcol = gK + (long long)o * N * nf + c.l;
 #pragma unroll
   for (int m = 0; m < E; ++m) {
@@ -336,6 +362,8 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
     const int krow = mrow < M / 2 ? mrow : mrow + (N - M);
     kcol[(long long)krow * nf] = acc[m];
   }
+  // dropped rows [M/2, N - M/2) of this column; N - M is a multiple of TPS
+  for (int k = M / 2 + t; k < N - M / 2; k += TPS) kcol[(long long)k * nf] = make_float2(0.f, 0.f);
 }
 
 template <int N, int M>
@@ -361,7 +389,7 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
                                                                   long long ncols) {
   using CN = FftCfg<N>;
   using CM = FftCfg<M>;
-  constexpr int L = M / 2 + 1, NF = N / 2 + 1;
+  constexpr int L = M / 2 + 1, LD = L, NF = N / 2 + 1;
   constexpr int TPSN = CN::TPS, TPSM = CM::TPS, JP = cic_jp<N, M>();
   static_assert(JP * TPSM == TPSN, "thread layouts of the two transforms must nest");
   float2 *lds = g_lds;
@@ -379,11 +407,11 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
     const int j = j0 + js;
     const bool act = c.ok && j < J;
     const int o = ci * J + (act ? j : 0);
-    const float2 *gcol = Tg + (b * S + o) * M * L + c.l;
+    const float2 *gcol = Tg + (b * S + o) * M * LD + c.l;
     const float2 *kcol = K + (long long)o * N * NF + c.l;
     float2 g[CM::E];
 #pragma unroll
-    for (int m = 0; m < CM::E; ++m) g[m] = act ? gcol[(long long)(tp + TPSM * m) * L] : make_float2(0.f, 0.f);
+    for (int m = 0; m < CM::E; ++m) g[m] = act ? gcol[(long long)(tp + TPSM * m) * LD] : make_float2(0.f, 0.f);
     fft_seq<M, -1>(g, tp, lds, js * M * CT + s, CT);
     if (act) {
 #pragma unroll
@@ -410,20 +438,9 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
   }
   fft_seq<N, +1>(w, t, lds, s, CT);
   if (!c.ok) return;
-  float2 *vcol = V + c.plane * N * L + c.l;
+  float2 *vcol = V + c.plane * N * LD + c.l;
 #pragma unroll
-  for (int m = 0; m < CN::E; ++m) vcol[(long long)(t + TPSN * m) * L] = w[m];
-}
-
-__global__ void k_gk_zero_dropped(float2 *gK, long long total, int N, int M) {
-  const int nf = N / 2 + 1, L = M / 2 + 1;
-  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-       i += (long long)gridDim.x * blockDim.x) {
-    const int l = (int)(i % nf);
-    const int k = (int)((i / nf) % N);
-    const bool kept = l < L && (k < M / 2 || k >= N - M / 2);
-    if (!kept) gK[i] = make_float2(0.f, 0.f);
-  }
+  for (int m = 0; m < CN::E; ++m) vcol[(long long)(t + TPSN * m) * LD] = w[m];
 }
 
 // ---------------------------------------------------------------------------
@@ -582,8 +599,20 @@ hipError_t launch_row_r2c(int n, const float *x, float2 *out, long long planes, 
     const unsigned grid = (unsigned)((npairs + SPW - 1) / SPW);
     const size_t lds = lds_size(SPW * N) * sizeof(float2);
     static const std::string nm = "row_r2c_" + std::to_string(N);
-    err = launch(nm.c_str(), k_row_r2c<N, SPW>, grid, SPW * FftCfg<N>::TPS, lds, s, x, out, npairs,
-                 rows_per_plane, in_view, in_plane_stride, L, out_row_stride, out_plane_stride, alpha, beta);
+    const int ors = (int)out_row_stride;
+    switch (in_view.mode) {
+      case 0:
+        err = launch(nm.c_str(), k_row_r2c<N, SPW, 0>, grid, SPW * FftCfg<N>::TPS, lds, s, x, out, npairs,
+                     rows_per_plane, in_view, in_plane_stride, L, ors, out_plane_stride, alpha, beta);
+        break;
+      case 1:
+        err = launch(nm.c_str(), k_row_r2c<N, SPW, 1>, grid, SPW * FftCfg<N>::TPS, lds, s, x, out, npairs,
+                     rows_per_plane, in_view, in_plane_stride, L, ors, out_plane_stride, alpha, beta);
+        break;
+      default:
+        err = launch(nm.c_str(), k_row_r2c<N, SPW, 2>, grid, SPW * FftCfg<N>::TPS, lds, s, x, out, npairs,
+                     rows_per_plane, in_view, in_plane_stride, L, ors, out_plane_stride, alpha, beta);
+    }
   });
   return err;
 }
@@ -599,15 +628,27 @@ hipError_t launch_row_c2r(int n, const float2 *in, float *y, long long planes, i
     const unsigned grid = (unsigned)((npairs + SPW - 1) / SPW);
     const size_t lds = lds_size(SPW * N) * sizeof(float2);
     static const std::string nm = "row_c2r_" + std::to_string(N);
-    err = launch(nm.c_str(), k_row_c2r<N, SPW>, grid, SPW * FftCfg<N>::TPS, lds, s, in, y, npairs,
-                 rows_per_plane, L, in_row_stride, in_plane_stride, alpha, beta, out_view, out_plane_stride);
+    const int irs = (int)in_row_stride;
+    switch (out_view.mode) {
+      case 0:
+        err = launch(nm.c_str(), k_row_c2r<N, SPW, 0>, grid, SPW * FftCfg<N>::TPS, lds, s, in, y, npairs,
+                     rows_per_plane, L, irs, in_plane_stride, alpha, beta, out_view, out_plane_stride);
+        break;
+      case 1:
+        err = launch(nm.c_str(), k_row_c2r<N, SPW, 1>, grid, SPW * FftCfg<N>::TPS, lds, s, in, y, npairs,
+                     rows_per_plane, L, irs, in_plane_stride, alpha, beta, out_view, out_plane_stride);
+        break;
+      default:
+        err = launch(nm.c_str(), k_row_c2r<N, SPW, 2>, grid, SPW * FftCfg<N>::TPS, lds, s, in, y, npairs,
+                     rows_per_plane, L, irs, in_plane_stride, alpha, beta, out_view, out_plane_stride);
+    }
   });
   return err;
 }
 
 static unsigned col_tiles(long long ncols, int ct) { return (unsigned)((ncols + ct - 1) / ct); }
 
-hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long long planes, int L,
+hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long long planes, int L, int ld,
                           long long in_plane_stride, long long out_plane_stride, hipStream_t s) {
   hipError_t err = hipErrorInvalidValue;
   dispatch_n(n, [&](auto nc) {
@@ -619,10 +660,10 @@ hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long lo
     static const std::string ni = "col_fft_inv_" + std::to_string(N);
     if (dir < 0)
       err = launch(nf.c_str(), k_col_fft<N, CT, -1>, col_tiles(ncols, CT), CT * FftCfg<N>::TPS, lds, s, in, out, L,
-                   ncols, in_plane_stride, out_plane_stride);
+                   ld, ncols, in_plane_stride, out_plane_stride);
     else
       err = launch(ni.c_str(), k_col_fft<N, CT, +1>, col_tiles(ncols, CT), CT * FftCfg<N>::TPS, lds, s, in, out, L,
-                   ncols, in_plane_stride, out_plane_stride);
+                   ld, ncols, in_plane_stride, out_plane_stride);
   });
   return err;
 }
@@ -652,7 +693,7 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
   if (!cic_pair_supported(n, m)) return err;
   dispatch_n(m, [&](auto mc) {
     constexpr int M = decltype(mc)::value;
-    constexpr int CT = col_ct<M>(), BP = gk_bp<M>();
+    constexpr int CT = kGkCT, BP = gk_bp<M>();
     constexpr int L = M / 2 + 1;
     const long long ncols = (long long)S * L;
     const size_t lds = lds_size(BP * M * CT) * sizeof(float2);
@@ -677,12 +718,6 @@ hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, fl
                  S / C, ncols);
   });
   return err;
-}
-
-hipError_t launch_gk_zero_dropped(float2 *gK, int S, int n, int m, hipStream_t s) {
-  if (m == n) return hipSuccess;  // nothing dropped
-  const long long total = (long long)S * n * (n / 2 + 1);
-  return launch("gk_zero_dropped", k_gk_zero_dropped, grid_stride_blocks(total, 256), 256, 0, s, gK, total, n, m);
 }
 
 hipError_t launch_cic_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, long long P,

@@ -152,8 +152,18 @@ class CicLayer(_LayerPlan):
         self.fwd_ws = _workspace(self.fwd_ws_bytes, self.device)
         self.bwd_ws = _workspace(self.bwd_ws_bytes, self.device)
 
+    @property
+    def saved_ld(self):
+        """Row stride of the saved spectrum: M/2+1 rounded up to a multiple of 16."""
+        return self.saved_bytes // (8 * self.B * self.C * self.M)
+
     def new_saved(self):
-        return torch.empty((self.B, self.C, self.M, self.M // 2 + 1), dtype=torch.complex64, device=self.device)
+        """Buffer for the pooled input spectrum, [B][C][M][saved_ld] complex (columns > M/2 unused)."""
+        return torch.empty((self.B, self.C, self.M, self.saved_ld), dtype=torch.complex64, device=self.device)
+
+    def saved_spectrum(self, saved):
+        """The M x (M/2+1) kept bins held in a saved buffer, as a [B][C][M][M/2+1] view."""
+        return saved[..., : self.M // 2 + 1]
 
     def new_output(self):
         return torch.empty((self.B, self.S, self.out, self.out), dtype=torch.float32, device=self.device)

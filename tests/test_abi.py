@@ -86,8 +86,7 @@ def test_cic_layer_plan_validation(args, expect):
         f, s, b = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
         assert _lib.status("fdc_layer_workspace_size", p, ctypes.byref(f), ctypes.byref(s), ctypes.byref(b)) == 0
         B, C, S, N, M, art, kn = args
-        L = M // 2 + 1
-        assert s.value == B * C * M * L * 8
+        assert s.value == B * C * M * (M // 2 + 1) * 8
         o = ctypes.c_int()
         assert _lib.status("fdc_layer_output_size", p, ctypes.byref(o)) == FDC_OK
         assert o.value == (M - kn + 1 if art == 1 else M)
