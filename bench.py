@@ -11,11 +11,13 @@ all layers, activation gradients of layers 2..5; the gradient of the input
 image is not part of a training step).  Inputs are resident in HBM before the
 timed region starts.
 
-Prints ONE JSON line (see --help).  Besides the step time it reports, for the
-kernel that takes most of the step, its algorithmic bytes per launch divided by
-its average launch duration (HIP events around that kernel's launches on the
-stream it runs on, recorded during the timed steps), and the float64 CPU oracle
-timed on a bounded sample of the same workload.
+Prints ONE JSON line (see --help).  The step is captured once as a HIP graph
+and the timed region replays it K times (--eager times plain launches).  Besides
+the step time it reports, for the kernel that takes most of the step, its
+algorithmic bytes per launch divided by its average launch duration (HIP events
+around that kernel's launches on the stream it runs on, over a second timed
+region of K eager steps), and the float64 CPU oracle timed on a bounded sample
+of the same workload.
 """
 
 import argparse
@@ -145,6 +147,7 @@ def main():
                     help="CIC stack workload (default: the 1024 x 1024 headline stack)")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
     ap.add_argument("--input-grad", action="store_true", help="also compute the input-image gradient")
+    ap.add_argument("--eager", action="store_true", help="time eager launches instead of HIP graph replays")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the timed region, run one plain streaming copy kernel (dst = src * 1) over "
                          "MIB MiB, a known-size reference for the HBM traffic counters of a profiler run")
@@ -203,22 +206,47 @@ def main():
     dominant = max(per_name, key=lambda k: per_name[k][0])
     dom_bytes_per_step, dom_launches_per_step = per_name[dominant][1], per_name[dominant][2]
 
-    # timed region: K steps, HIP events on the stream, the dominant kernel bracketed by its own events
-    _lib.call("fdc_kernel_timing_enable", args.steps * dom_launches_per_step, dominant.encode())
-    torch.cuda.synchronize()
     t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    wall0 = time.perf_counter()
-    t_start.record(stream)
-    for _ in range(args.steps):
+
+    # the step captured once as a HIP graph (all buffers are preallocated, so the
+    # captured launches reuse them); a replay must reproduce the eager step exactly
+    graph = None
+    if not args.eager:
         step()
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
+        torch.cuda.synchronize()
+        ref = [stack.acts[-1].clone()] + [gk.clone() for gk in stack.gks]
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = [stack.acts[-1]] + list(stack.gks)
+        if not all(torch.equal(a, b) for a, b in zip(ref, got)):
+            sys.exit("graph replay does not reproduce the eager step")
+        for _ in range(max(args.warmup, 1)):
+            graph.replay()
+
+    def timed(run):
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        t_start.record(stream)
+        for _ in range(args.steps):
+            run()
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        return t_start.elapsed_time(t_end) / args.steps, (time.perf_counter() - w0) * 1e3 / args.steps
+
+    # timed region 1: K steps (graph replays unless --eager)
+    ms_per_step, wall_ms = timed(graph.replay if graph is not None else step)
+
+    # timed region 2: K eager steps, the dominant kernel's launches bracketed by HIP events
+    # on the stream they run on (events cannot be placed inside a replayed graph)
+    _lib.call("fdc_kernel_timing_enable", args.steps * dom_launches_per_step, dominant.encode())
+    eager_ms_per_step, _ = timed(step)
     _lib.call("fdc_kernel_timing_disable")
     buf = ctypes_buf(1 << 20)
     _lib.call("fdc_kernel_timing_launches", buf, len(buf))
     dom_ms = [float(ln.rsplit(" ", 1)[1]) for ln in buf.value.decode().strip().splitlines()]
-    ms_per_step = t_start.elapsed_time(t_end) / args.steps
 
     dom_avg_ms = sum(dom_ms) / len(dom_ms)
     dom_bytes_per_launch = dom_bytes_per_step / dom_launches_per_step
@@ -245,6 +273,7 @@ def main():
             "channels": list(wl.channels),
             "input_grad": bool(args.input_grad),
             "launches_per_step": len(launches),
+            "hip_graph": graph is not None,
         },
         "roofline": {
             "bound": "hbm",
@@ -256,12 +285,13 @@ def main():
             "traffic": measured_traffic(dominant, wl.name),
             "bytes_per_launch": dom_bytes_per_launch,
             "avg_launch_ms": dom_avg_ms,
-            "share_of_step": sum(dom_ms) / args.steps / ms_per_step,
+            "share_of_step": sum(dom_ms) / args.steps / eager_ms_per_step,
         },
         "step_api_bytes": api_bytes,
         "step_effective_gbps": api_bytes / (ms_per_step * 1e-3) / 1e9,
         "step_kernel_ms": {k: round(v[0], 5) for k, v in sorted(per_name.items(), key=lambda kv: -kv[1][0])},
-        "wall_ms_per_step": wall * 1e3 / args.steps,
+        "wall_ms_per_step": wall_ms,
+        "eager_ms_per_step": eager_ms_per_step,
     }
     if args.copy_calibration > 0:
         n = args.copy_calibration * (1 << 20) // 4
