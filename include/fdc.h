@@ -159,7 +159,8 @@ fdc_status fdc_layer_output_size(const fdc_layer_plan *plan, int *out_size);
 /* x [B][C][N][N] float32, K [S][N][N/2+1] complex -> y [B][S][O][O] float32.
  * `saved` (may be NULL when no backward will follow; fdc_layer_workspace_size
  * gives its size) receives the pooled input spectrum the backward pass needs:
- * the M x (M/2+1) bins FDP keeps, complex, [B][C][M][M/2+1]. */
+ * the M x (M/2+1) bins FDP keeps, complex, as columns 0..M/2-1 in a block
+ * [B][C][M][M/2] followed by column M/2 in a block [B][C][M]. */
 fdc_status fdc_cic_layer_forward(const fdc_layer_plan *plan, const float *x, const fdc_c64 *K,
                                  float *y, void *saved, void *ws, size_t ws_bytes,
                                  hipStream_t stream);

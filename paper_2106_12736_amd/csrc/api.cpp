@@ -173,8 +173,8 @@ fdc_status fdc_rfft2(const fdc_fft_plan *p, const float *x, fdc_c64 *X, void *, 
   const int h = p->h, w = p->w, wf = w / 2 + 1;
   ImgView id{0, 0, h, w};
   auto *out = reinterpret_cast<float2 *>(X);
-  if (fdc_status st = check_hip(fdc::launch_row_r2c(w, x, out, p->count, h, id, (long long)h * w, wf, wf,
-                                                    (long long)h * wf, 1.f, 1.f, s), "rfft2 rows"))
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(w, x, fdc::plain_layout(out, h, wf), p->count, h, id,
+                                                    (long long)h * w, wf, 1.f, 1.f, s), "rfft2 rows"))
     return st;
   return check_hip(fdc::launch_col_fft(h, -1, out, out, p->count, wf, wf, (long long)h * wf, (long long)h * wf, s),
                    "rfft2 columns");
@@ -191,7 +191,7 @@ static fdc_status inverse_like(const fdc_fft_plan *p, const fdc_c64 *X, float *x
                                                     wf, (long long)h * wf, (long long)h * wf, s), what))
     return st;
   ImgView id{0, 0, h, w};
-  return check_hip(fdc::launch_row_c2r(w, tmp, x, p->count, h, wf, wf, (long long)h * wf, alpha, beta, id,
+  return check_hip(fdc::launch_row_c2r(w, fdc::plain_layout(tmp, h, wf), x, p->count, h, wf, alpha, beta, id,
                                        (long long)h * w, s), what);
 }
 
@@ -213,8 +213,8 @@ fdc_status fdc_irfft2_backward(const fdc_fft_plan *p, const float *gx, fdc_c64 *
   const int h = p->h, w = p->w, wf = w / 2 + 1;
   ImgView id{0, 0, h, w};
   auto *out = reinterpret_cast<float2 *>(gX);
-  if (fdc_status st = check_hip(fdc::launch_row_r2c(w, gx, out, p->count, h, id, (long long)h * w, wf, wf,
-                                                    (long long)h * wf, 1.f / ((float)h * (float)w), 2.f, s),
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(w, gx, fdc::plain_layout(out, h, wf), p->count, h, id,
+                                                    (long long)h * w, wf, 1.f / ((float)h * (float)w), 2.f, s),
                                 "irfft2_backward rows"))
     return st;
   return check_hip(fdc::launch_col_fft(h, -1, out, out, p->count, wf, wf, (long long)h * wf, (long long)h * wf, s),
@@ -318,11 +318,12 @@ fdc_status fdc_cic_layer_plan_create(fdc_layer_plan **plan, int B, int C, int S,
   p->artifact = artifact;
   p->kn = artifact == FDC_ARTIFACT_NONE ? 1 : kernel_n;
   p->out = artifact_out(M, artifact, p->kn);
-  const size_t LD = (size_t)M / 2 + 1;
+  // split-layout spectra (fdc::SpecLayout) of L = M/2 + 1 bins per row
+  const size_t L = (size_t)M / 2 + 1;
   const size_t c64 = sizeof(fdc_c64);
-  p->fwd_ws = ((size_t)B * C * N * LD + (size_t)B * S * M * LD + (size_t)B * C * M * LD) * c64;  // T, U, Xh
-  p->saved = (size_t)B * C * M * LD * c64;                              // pooled input spectrum
-  p->bwd_ws = ((size_t)B * S * M * LD + (size_t)B * C * N * LD) * c64;  // Tg, V
+  p->fwd_ws = ((size_t)B * C * N * L + (size_t)B * S * M * L + (size_t)B * C * M * L) * c64;  // T, U, Xh
+  p->saved = (size_t)B * C * M * L * c64;                             // pooled input spectrum
+  p->bwd_ws = ((size_t)B * S * M * L + (size_t)B * C * N * L) * c64;  // Tg, V
   *plan = p;
   return FDC_OK;
 }
@@ -363,20 +364,21 @@ fdc_status fdc_cic_layer_forward(const fdc_layer_plan *p, const float *x, const 
   if (fdc_status st = check_layer_plan(p, 0)) return st;
   if (!x || !K || !y) return fail(FDC_EINVAL, "NULL tensor");
   if (fdc_status st = check_ws(ws, ws_bytes, p->fwd_ws)) return st;
-  const int B = p->B, C = p->C, S = p->S, N = p->N, M = p->M, L = M / 2 + 1, LD = L;
+  const int B = p->B, C = p->C, S = p->S, N = p->N, M = p->M, L = M / 2 + 1;
   auto *T = reinterpret_cast<float2 *>(ws);
-  auto *U = T + (size_t)B * C * N * LD;
+  auto *U = T + (size_t)B * C * N * L;
   // the pooled input spectrum goes to `saved` when the caller keeps it, else to the workspace
-  auto *Xh = saved != nullptr ? reinterpret_cast<float2 *>(saved) : U + (size_t)B * S * M * LD;
+  auto *Xh = saved != nullptr ? reinterpret_cast<float2 *>(saved) : U + (size_t)B * S * M * L;
   ImgView id{0, 0, N, N};
-  if (fdc_status st = check_hip(fdc::launch_row_r2c(N, x, T, (long long)B * C, N, id, (long long)N * N, L, LD,
-                                                    (long long)N * LD, 1.f, 1.f, s), "layer forward rows"))
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(N, x, fdc::split_layout(T, (long long)B * C, N, L),
+                                                    (long long)B * C, N, id, (long long)N * N, L, 1.f, 1.f, s),
+                                "layer forward rows"))
     return st;
   if (fdc_status st = check_hip(fdc::launch_col_fwd_cic(N, M, T, reinterpret_cast<const float2 *>(K), U, Xh, B, C,
                                                         S, s),
                                 "layer forward columns"))
     return st;
-  return check_hip(fdc::launch_row_c2r(M, U, y, (long long)B * S, M, L, LD, (long long)M * LD,
+  return check_hip(fdc::launch_row_c2r(M, fdc::split_layout(U, (long long)B * S, M, L), y, (long long)B * S, M, L,
                                        1.f / ((float)M * (float)M), 1.f, artifact_view(p),
                                        (long long)p->out * p->out, s),
                    "layer forward inverse rows");
@@ -390,12 +392,13 @@ fdc_status fdc_cic_layer_backward(const fdc_layer_plan *p, const float *gy, cons
   if (gx && !K) return fail(FDC_EINVAL, "K is NULL but gx was requested");
   if (!gx && !gK) return FDC_OK;
   if (fdc_status st = check_ws(ws, ws_bytes, p->bwd_ws)) return st;
-  const int B = p->B, C = p->C, S = p->S, N = p->N, M = p->M, L = M / 2 + 1, LD = L;
+  const int B = p->B, C = p->C, S = p->S, N = p->N, M = p->M, L = M / 2 + 1;
   auto *Tg = reinterpret_cast<float2 *>(ws);
-  auto *V = Tg + (size_t)B * S * M * LD;
-  if (fdc_status st = check_hip(fdc::launch_row_r2c(M, gy, Tg, (long long)B * S, M, artifact_view(p),
-                                                    (long long)p->out * p->out, L, LD, (long long)M * LD,
-                                                    1.f / ((float)M * (float)M), 2.f, s),
+  auto *V = Tg + (size_t)B * S * M * L;
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(M, gy, fdc::split_layout(Tg, (long long)B * S, M, L),
+                                                    (long long)B * S, M, artifact_view(p),
+                                                    (long long)p->out * p->out, L, 1.f / ((float)M * (float)M),
+                                                    2.f, s),
                                 "layer backward rows"))
     return st;
   if (gK) {
@@ -409,8 +412,8 @@ fdc_status fdc_cic_layer_backward(const fdc_layer_plan *p, const float *gy, cons
                                                          s), "layer backward dx columns"))
       return st;
     ImgView id{0, 0, N, N};
-    return check_hip(fdc::launch_row_c2r(N, V, gx, (long long)B * C, N, L, LD, (long long)N * LD, 1.f, 0.5f, id,
-                                         (long long)N * N, s),
+    return check_hip(fdc::launch_row_c2r(N, fdc::split_layout(V, (long long)B * C, N, L), gx, (long long)B * C, N,
+                                         L, 1.f, 0.5f, id, (long long)N * N, s),
                      "layer backward dx rows");
   }
   return FDC_OK;

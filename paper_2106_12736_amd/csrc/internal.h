@@ -23,22 +23,46 @@ struct ImgView {
 
 bool size_supported(int n);
 
+// Storage of a half spectrum of `planes` images with `rows` rows and L stored bins
+// per row.  Bins l < L-1 of row r of plane p are at main[p*ps + r*rs + l]; the last
+// bin, l = L-1, is at side[p*sps + r*srs].
+//   plain: the row-major [planes][rows][L] array (side = main + L - 1).
+//   split: a main block [planes][rows][L-1] followed by the last column as a
+//          [planes][rows] block.  With L - 1 = n/2 a power of two every main row
+//          starts on an aligned boundary, and the odd last column is contiguous
+//          along the rows, so column tiles read whole aligned runs everywhere.
+struct SpecLayout {
+  float2 *main;
+  long long ps;
+  int rs;
+  float2 *side;
+  long long sps;
+  int srs;
+};
+inline SpecLayout plain_layout(const float2 *p, int rows, int L) {
+  float2 *q = const_cast<float2 *>(p);
+  return SpecLayout{q, (long long)rows * L, L, q + (L - 1), (long long)rows * L, L};
+}
+inline SpecLayout split_layout(const float2 *p, long long planes, int rows, int L) {
+  float2 *q = const_cast<float2 *>(p);
+  return SpecLayout{q, (long long)rows * (L - 1), L - 1, q + planes * rows * (L - 1), rows, 1};
+}
+
 // Kernel timing hooks (no-ops unless enabled through the ABI).
 void timing_before(const char *name, hipStream_t s);
 void timing_after(const char *name, hipStream_t s);
 
 // Row transforms of real rows of length n (n in the supported set), processed in pairs.
-// rows_per_plane must be even.  Output/input bins beyond L are not written / read as zero.
+// rows_per_plane must be even.  Output/input bins beyond L are not written / read as zero;
+// the L stored bins are laid out as `spec` says.
 //   r2c: out[plane][row][l] = w_l * sum_w x[plane][row][w] e^{-2 pi i w l / n},  l < L
 //   c2r: y[plane][row][w] = sum_{l<=n/2} c_l Re(w_l in[plane][row][l] e^{+2 pi i w l / n}),
 //        with the imaginary part of bins 0 and n/2 discarded (real-part semantics)
 // where w_l = alpha at l = 0 and l = n/2 and alpha * beta otherwise.
-hipError_t launch_row_r2c(int n, const float *x, float2 *out, long long planes, int rows_per_plane,
-                          ImgView in_view, long long in_plane_stride, int L, long long out_row_stride,
-                          long long out_plane_stride, float alpha, float beta, hipStream_t s);
-hipError_t launch_row_c2r(int n, const float2 *in, float *y, long long planes, int rows_per_plane, int L,
-                          long long in_row_stride, long long in_plane_stride, float alpha, float beta,
-                          ImgView out_view, long long out_plane_stride, hipStream_t s);
+hipError_t launch_row_r2c(int n, const float *x, SpecLayout out, long long planes, int rows_per_plane,
+                          ImgView in_view, long long in_plane_stride, int L, float alpha, float beta, hipStream_t s);
+hipError_t launch_row_c2r(int n, SpecLayout in, float *y, long long planes, int rows_per_plane, int L, float alpha,
+                          float beta, ImgView out_view, long long out_plane_stride, hipStream_t s);
 
 // Column DFTs of length n over the first `L` columns of row-major [planes][n][ld] complex
 // data (in place allowed).
@@ -46,9 +70,10 @@ hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long lo
                           long long in_plane_stride, long long out_plane_stride, hipStream_t s);
 
 // Fused CIC + FDP column kernels (square n x n images pooled to m x m; L = m/2 + 1).
-//   fwd:   T [B][C][n][L] -> Xh [B][C][m][L] (written, then read) -> U [B][S][m][L]
-//   bwd_gk: Tg [B][S][m][L], Xh -> gK [S][n][n/2+1]: every bin (zeros where FDP drops)
-//   bwd_gx: Tg, K -> V [B][C][n][L]
+// T, Xh, U, Tg and V are split-layout spectra (SpecLayout) with L bins per row.
+//   fwd:   T [B*C][n rows] -> Xh [B*C][m rows] (written, then read) -> U [B*S][m rows]
+//   bwd_gk: Tg [B*S][m rows], Xh -> gK [S][n][n/2+1]: every bin (zeros where FDP drops)
+//   bwd_gx: Tg, K -> V [B*C][n rows]
 bool cic_pair_supported(int n, int m);
 hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, float2 *U, float2 *Xh, int B,
                               int C, int S, hipStream_t s);

@@ -67,9 +67,10 @@ constexpr int row_spw() {
 // A sequence uses TPS <= 64 threads, so a wavefront holds whole sequences and
 // the LDS exchanges need only wave-level ordering.
 template <int N, int SPW, int MODE>
-__global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(
-    const float *__restrict__ x, float2 *__restrict__ out, long long npairs, int rows_per_plane, ImgView view,
-    long long in_plane_stride, int L, int out_row_stride, long long out_plane_stride, float alpha, float beta) {
+__global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(const float *__restrict__ x, SpecLayout out,
+                                                                long long npairs, int rows_per_plane, ImgView view,
+                                                                long long in_plane_stride, int L, float alpha,
+                                                                float beta) {
   using Cfg = FftCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   static_assert(TPS <= 64, "a row sequence must fit in one wavefront");
@@ -97,23 +98,31 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(
   for (int m = 0; m < E; ++m) lds[lds_phys(s * N + t + TPS * m)] = v[m];
   lds_barrier<true>();
   if (!active) return;
-  float2 *oa = out + plane * out_plane_stride + (long long)r0 * out_row_stride;
-  float2 *ob = oa + out_row_stride;
+  float2 *oa = out.main + plane * out.ps + (long long)r0 * out.rs;
+  float2 *ob = oa + out.rs;
   for (int k = t; k < L; k += TPS) {
     const float2 zk = lds[lds_phys(s * N + k)];
     const float2 zn = lds[lds_phys(s * N + (k == 0 ? 0 : N - k))];
     const float wgt = 0.5f * bin_weight(k, N, alpha, beta);
     // two real rows packed as z = a + i b:  A = (Z[k] + conj Z[-k]) / 2,  B = (Z[k] - conj Z[-k]) / (2i)
-    oa[k] = make_float2((zk.x + zn.x) * wgt, (zk.y - zn.y) * wgt);
-    ob[k] = make_float2((zk.y + zn.y) * wgt, (zn.x - zk.x) * wgt);
+    const float2 A = make_float2((zk.x + zn.x) * wgt, (zk.y - zn.y) * wgt);
+    const float2 Bv = make_float2((zk.y + zn.y) * wgt, (zn.x - zk.x) * wgt);
+    if (k < L - 1) {
+      oa[k] = A;
+      ob[k] = Bv;
+    } else {
+      float2 *sa = out.side + plane * out.sps + (long long)r0 * out.srs;
+      sa[0] = A;
+      sa[out.srs] = Bv;
+    }
   }
 }
 
 template <int N, int SPW, int MODE>
-__global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(
-    const float2 *__restrict__ in, float *__restrict__ y, long long npairs, int rows_per_plane, int L,
-    int in_row_stride, long long in_plane_stride, float alpha, float beta, ImgView view,
-    long long out_plane_stride) {
+__global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(SpecLayout in, float *__restrict__ y,
+                                                                long long npairs, int rows_per_plane, int L,
+                                                                float alpha, float beta, ImgView view,
+                                                                long long out_plane_stride) {
   using Cfg = FftCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   static_assert(TPS <= 64, "a row sequence must fit in one wavefront");
@@ -125,8 +134,9 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(
   const long long row0 = 2 * pair;
   const long long plane = row0 / rows_per_plane;
   const int r0 = (int)(row0 - plane * rows_per_plane);
-  const float2 *ia = in + plane * in_plane_stride + (long long)r0 * in_row_stride;
-  const float2 *ib = ia + in_row_stride;
+  const float2 *ia = in.main + plane * in.ps + (long long)r0 * in.rs;
+  const float2 *ib = ia + in.rs;
+  const float2 *sa = in.side + plane * in.sps + (long long)r0 * in.srs;
 
   float2 v[E];
 #pragma unroll
@@ -135,9 +145,12 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(
     const bool upper = 2 * k > N;
     const int kk = upper ? N - k : k;
     float2 a = make_float2(0.f, 0.f), b = make_float2(0.f, 0.f);
-    if (kk < L) {
+    if (kk < L - 1) {
       a = ia[kk];
       b = ib[kk];
+    } else if (kk == L - 1) {
+      a = sa[0];
+      b = sa[in.srs];
     }
     const bool edge = (kk == 0 || 2 * kk == N);
     const float wgt = edge ? alpha : alpha * beta;
@@ -169,44 +182,69 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(
 // ---------------------------------------------------------------------------
 // column transforms
 //
-// Column kernels see their input as `planes` row-major [rows][L] complex
-// images and number the columns of all planes consecutively, q = plane * L + l.
-// A workgroup owns CT consecutive columns (which may straddle two planes), so
-// only the last tile of a launch is ragged, whatever L is.  Lanes run fastest
-// along the columns: each global access is a run of up to CT consecutive
-// complex values of one row.
+// Column kernels see their input as `planes` row-major [rows][L] complex images.
+// A workgroup owns CT columns, with lanes running fastest along the columns so
+// that each global access is a run of CT consecutive complex values of one row.
+// Tiling: the first MAIN = ((L-1)/CT)*CT columns of every plane form aligned
+// tiles (run starts on a multiple of CT, never straddling planes); the remaining
+// L - MAIN columns of all planes -- for L = 2^k + 1 only the last, Nyquist,
+// column -- are packed CT at a time into tail tiles numbered after the main
+// tiles.  Tiles that start off the CT grid split every row access into two
+// transactions and run at about half the bandwidth.
 // ---------------------------------------------------------------------------
 template <int N>
 constexpr int col_ct() {
   return FftCfg<N>::TPS >= 64 ? 8 : (FftCfg<N>::TPS >= 32 ? 16 : 32);
 }
 
+// CT for columns [0, L): at most `ct` and a divisor of L - 1 when L - 1 > 0.
+__host__ __device__ constexpr int col_ct_for(int ct, int L) {
+  const int lm1 = L - 1;
+  const int low = lm1 > 0 ? (lm1 & -lm1) : ct;
+  return low < ct ? low : ct;
+}
+
+__host__ __device__ constexpr long long col_tile_count(long long planes, int L, int ct) {
+  return planes * ((L - 1) / ct) + (planes * (L - (L - 1) / ct * ct) + ct - 1) / ct;
+}
+
 struct ColRef {
-  long long plane;
+  int plane;
   int l;
   bool ok;
 };
 
+// Column `s` of tile w.  Out-of-range lanes of the last tail tile get ok = false
+// and a valid (repeated) column, so their loads stay in bounds.
 template <int CT>
-__device__ __forceinline__ ColRef column_ref(long long tile, int s, int L, long long ncols) {
-  const long long q = tile * CT + s;
+__device__ __forceinline__ ColRef column_ref(int w, int s, int L, int planes) {
+  const int mpp = (L - 1) / CT, rt = L - mpp * CT;
+  const int main_tiles = planes * mpp;
   ColRef r;
-  r.ok = q < ncols;
-  const long long qq = r.ok ? q : ncols - 1;
-  r.plane = qq / L;
-  r.l = (int)(qq - r.plane * L);
+  if (w < main_tiles) {
+    r.plane = w / mpp;
+    r.l = (w - r.plane * mpp) * CT + s;
+    r.ok = true;
+  } else {
+    int q = (w - main_tiles) * CT + s;
+    const int total = planes * rt;
+    r.ok = q < total;
+    if (!r.ok) q = total - 1;
+    r.plane = q / rt;
+    r.l = mpp * CT + (q - r.plane * rt);
+  }
   return r;
 }
 
 template <int N, int CT, int DIR>
 __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft(const float2 *in, float2 *out, int L, int ld,
-                                                               long long ncols, long long in_plane_stride,
+                                                               int planes, long long in_plane_stride,
                                                                long long out_plane_stride) {
   using Cfg = FftCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   float2 *lds = g_lds;
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
-  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, ncols);
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
   const float2 *ip = in + c.plane * in_plane_stride + c.l;
   float2 v[E];
 #pragma unroll
@@ -224,61 +262,75 @@ __device__ __forceinline__ int kept_row(int mrow) {
   return mrow < M / 2 ? mrow : mrow + (N - M);
 }
 
+// Column (plane, l) of a split-layout spectrum (see SpecLayout) of `planes`
+// images with ROWS rows and L bins per row: row r is at p[r * stride].
+struct ColPtr {
+  float2 *p;
+  int stride;
+};
+template <int ROWS, int L>
+__device__ __forceinline__ ColPtr split_col(const float2 *base, int planes, int plane, int l) {
+  constexpr int H = L - 1;
+  float2 *b = const_cast<float2 *>(base);
+  if (l < H) return ColPtr{b + (long long)plane * ROWS * H + l, H};
+  return ColPtr{b + (long long)planes * ROWS * H + (long long)plane * ROWS, 1};
+}
+
 // Forward, first half: column DFT (N) of the pruned row spectra, keep the M rows
-// FDP keeps.  T [planes][N][L] -> Xh [planes][M][L] (the pooled input spectrum).
+// FDP keeps.  T [planes][N rows] -> Xh [planes][M rows], both split layout with
+// L = M/2 + 1 bins per row (Xh is the pooled input spectrum the backward reads).
 template <int N, int M, int CT>
 __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fwd_crop(const float2 *__restrict__ T,
-                                                                    float2 *__restrict__ Xh, long long ncols) {
+                                                                    float2 *__restrict__ Xh, int planes) {
   using CN = FftCfg<N>;
-  constexpr int L = M / 2 + 1, LD = L, TPS = CN::TPS, E = CN::E;
+  constexpr int L = M / 2 + 1, TPS = CN::TPS, E = CN::E;
   float2 *lds = g_lds;
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
-  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, ncols);
-  const float2 *tcol = T + c.plane * N * LD + c.l;
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
+  const ColPtr tc = split_col<N, L>(T, planes, c.plane, c.l);
   float2 v[E];
 #pragma unroll
-  for (int m = 0; m < E; ++m) v[m] = c.ok ? tcol[(long long)(t + TPS * m) * LD] : make_float2(0.f, 0.f);
+  for (int m = 0; m < E; ++m) v[m] = c.ok ? tc.p[(t + TPS * m) * tc.stride] : make_float2(0.f, 0.f);
   fft_seq<N, -1>(v, t, lds, s, CT);
   if (!c.ok) return;
-  float2 *xh = Xh + c.plane * M * LD + c.l;
+  const ColPtr xc = split_col<M, L>(Xh, planes, c.plane, c.l);
 #pragma unroll
   for (int m = 0; m < E; ++m) {
     const int k = t + TPS * m;
-    if (k < M / 2) xh[(long long)k * LD] = v[m];
-    else if (k >= N - M / 2) xh[(long long)(k - (N - M)) * LD] = v[m];
+    if (k < M / 2) xc.p[k * xc.stride] = v[m];
+    else if (k >= N - M / 2) xc.p[(k - (N - M)) * xc.stride] = v[m];
   }
 }
 
 // Forward, second half: for every output channel o = c*J + j, the CIC product
 // (Eq. 5) of the pooled spectrum with kernel o at the kept bins, then the inverse
-// column DFT (M).  Xh [B][C][M][L], K [S][N][N/2+1] -> U [B][S][M][L].
+// column DFT (M).  Xh [B*C][M rows], K [S][N][N/2+1] -> U [B*S][M rows].
 template <int N, int M, int CT>
 __global__ __launch_bounds__(CT *FftCfg<M>::TPS) void k_col_cic_inv(const float2 *__restrict__ Xh,
                                                                    const float2 *__restrict__ K,
                                                                    float2 *__restrict__ U, int C, int J,
-                                                                   long long ncols) {
+                                                                   int planes) {
   using CM = FftCfg<M>;
-  constexpr int L = M / 2 + 1, LD = L, NF = N / 2 + 1, TPS = CM::TPS, E = CM::E;
+  constexpr int L = M / 2 + 1, NF = N / 2 + 1, TPS = CM::TPS, E = CM::E;
   float2 *lds = g_lds;
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
-  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, ncols);
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
   const int S = C * J;
-  const long long b = c.plane / S;
-  const int o = (int)(c.plane - b * S);
-  const float2 *xcol = Xh + (b * C + o / J) * M * LD + c.l;
+  const int b = c.plane / S;
+  const int o = c.plane - b * S;
+  const ColPtr xc = split_col<M, L>(Xh, planes / J, b * C + o / J, c.l);
   const float2 *kcol = K + (long long)o * N * NF + c.l;
   float2 z[E];
 #pragma unroll
   for (int m = 0; m < E; ++m) {
     const int mrow = t + TPS * m;
-    z[m] = c.ok ? cmul(xcol[(long long)mrow * LD], kcol[(long long)kept_row<N, M>(mrow) * NF])
-                : make_float2(0.f, 0.f);
+    z[m] = c.ok ? cmul(xc.p[mrow * xc.stride], kcol[kept_row<N, M>(mrow) * NF]) : make_float2(0.f, 0.f);
   }
   fft_seq<M, +1>(z, t, lds, s, CT);
   if (!c.ok) return;
-  float2 *ucol = U + c.plane * M * LD + c.l;
+  const ColPtr uc = split_col<M, L>(U, planes, c.plane, c.l);
 #pragma unroll
-  for (int m = 0; m < E; ++m) ucol[(long long)(t + TPS * m) * LD] = z[m];
+  for (int m = 0; m < E; ++m) uc.p[(t + TPS * m) * uc.stride] = z[m];
 }
 
 // Geometry of the dK kernel: tiles of 8 columns (there are only S * L columns,
@@ -291,8 +343,8 @@ constexpr int gk_bp() {
   return bp < 1 ? 1 : (bp > 8 ? 8 : bp);
 }
 
-// Backward, dL/dK: for columns q = o * L + l of the kernel gradient, column DFT (M)
-// of each upstream-gradient column Tg[b][o] and dK += G conj(Xh[b][o/J]).
+// Backward, dL/dK: for the kernel-gradient columns (o, l), column DFT (M) of each
+// upstream-gradient column Tg[b][o] and dK += G conj(Xh[b][o/J]).
 // Group g of the BP groups sums b = g, g + BP, ...; the BP partial sums are then
 // added in group order, so the result does not depend on scheduling.
 // Writes all of gK [S][N][N/2+1]: the kept bins, and exact zeros at the rows and
@@ -302,15 +354,15 @@ template <int M, int CT, int BP>
 __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const float2 *__restrict__ Tg,
                                                                       const float2 *__restrict__ Xh,
                                                                       float2 *__restrict__ gK, int B, int C,
-                                                                      int J, int N, long long ncols) {
+                                                                      int J, int N, int S) {
   using CM = FftCfg<M>;
-  constexpr int L = M / 2 + 1, LD = L, TPS = CM::TPS, E = CM::E;
+  constexpr int L = M / 2 + 1, TPS = CM::TPS, E = CM::E;
   constexpr int NT = CT * TPS * BP;
   float2 *lds = g_lds;
   const int s = threadIdx.x % CT, t = (threadIdx.x / CT) % TPS, g = threadIdx.x / (CT * TPS);
   const int wg = xcd_remap(blockIdx.x, gridDim.x);
-  const ColRef c = column_ref<CT>(wg, s, L, ncols);
-  const int o = (int)c.plane, ci = o / J, S = C * J;
+  const ColRef c = column_ref<CT>(wg, s, L, S);
+  const int o = c.plane, ci = o / J;
   const int nf = N / 2 + 1;
 
   // zeros of the columns l >= L, grid-stride over [S][N][L, nf)
@@ -329,15 +381,15 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
   for (int b0 = 0; b0 < B; b0 += BP) {
     const int b = b0 + g;
     const bool act = c.ok && b < B;
-    const float2 *gcol = Tg + ((long long)b * S + o) * M * LD + c.l;
-    const float2 *xcol = Xh + ((long long)b * C + ci) * M * LD + c.l;
+    const ColPtr gc = split_col<M, L>(Tg, B * S, (act ? b : 0) * S + o, c.l);
+    const ColPtr xc = split_col<M, L>(Xh, B * C, (act ? b : 0) * C + ci, c.l);
     float2 v[E];
 #pragma unroll
-    for (int m = 0; m < E; ++m) v[m] = act ? gcol[(long long)(t + TPS * m) * LD] : make_float2(0.f, 0.f);
+    for (int m = 0; m < E; ++m) v[m] = act ? gc.p[(t + TPS * m) * gc.stride] : make_float2(0.f, 0.f);
     fft_seq<M, -1>(v, t, lds, g * M * CT + s, CT);
     if (act) {
 #pragma unroll
-      for (int m = 0; m < E; ++m) acc[m] = cfmac(acc[m], v[m], xcol[(long long)(t + TPS * m) * LD]);
+      for (int m = 0; m < E; ++m) acc[m] = cfmac(acc[m], v[m], xc.p[(t + TPS * m) * xc.stride]);
     }
   }
   if constexpr (BP > 1) {
@@ -377,7 +429,7 @@ constexpr int cic_lds_elems() {
   return lds_size(a > b ? a : b);
 }
 
-// Backward, dL/dx: for columns q = (b*C + c) * L + l, column DFTs (M) of the J
+// Backward, dL/dx: for the columns (b, c, l), column DFTs (M) of the J
 // upstream-gradient columns Tg[b][cJ+j], dXh = sum_j G conj(K[cJ+j]) at the kept
 // bins, FDP adjoint (zero rows at the dropped frequencies), inverse column DFT (N).
 // The thread layout of the N-point transform holds JP = TPS_N / TPS_M groups of
@@ -386,18 +438,18 @@ template <int N, int M, int CT>
 __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 *__restrict__ Tg,
                                                                   const float2 *__restrict__ K,
                                                                   float2 *__restrict__ V, int C, int J,
-                                                                  long long ncols) {
+                                                                  int planes) {
   using CN = FftCfg<N>;
   using CM = FftCfg<M>;
-  constexpr int L = M / 2 + 1, LD = L, NF = N / 2 + 1;
+  constexpr int L = M / 2 + 1, NF = N / 2 + 1;
   constexpr int TPSN = CN::TPS, TPSM = CM::TPS, JP = cic_jp<N, M>();
   static_assert(JP * TPSM == TPSN, "thread layouts of the two transforms must nest");
   float2 *lds = g_lds;
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   const int tp = t % TPSM, js = t / TPSM;
-  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, ncols);
-  const long long b = c.plane / C;
-  const int ci = (int)(c.plane - b * C);
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
+  const int b = c.plane / C;
+  const int ci = c.plane - b * C;
   const int S = C * J;
 
   float2 acc[CM::E];
@@ -407,11 +459,11 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
     const int j = j0 + js;
     const bool act = c.ok && j < J;
     const int o = ci * J + (act ? j : 0);
-    const float2 *gcol = Tg + (b * S + o) * M * LD + c.l;
+    const ColPtr gc = split_col<M, L>(Tg, planes * J, b * S + o, c.l);
     const float2 *kcol = K + (long long)o * N * NF + c.l;
     float2 g[CM::E];
 #pragma unroll
-    for (int m = 0; m < CM::E; ++m) g[m] = act ? gcol[(long long)(tp + TPSM * m) * LD] : make_float2(0.f, 0.f);
+    for (int m = 0; m < CM::E; ++m) g[m] = act ? gc.p[(tp + TPSM * m) * gc.stride] : make_float2(0.f, 0.f);
     fft_seq<M, -1>(g, tp, lds, js * M * CT + s, CT);
     if (act) {
 #pragma unroll
@@ -438,9 +490,9 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
   }
   fft_seq<N, +1>(w, t, lds, s, CT);
   if (!c.ok) return;
-  float2 *vcol = V + c.plane * N * LD + c.l;
+  const ColPtr vc = split_col<N, L>(V, planes, c.plane, c.l);
 #pragma unroll
-  for (int m = 0; m < CN::E; ++m) vcol[(long long)(t + TPSN * m) * LD] = w[m];
+  for (int m = 0; m < CN::E; ++m) vc.p[(t + TPSN * m) * vc.stride] = w[m];
 }
 
 // ---------------------------------------------------------------------------
@@ -588,9 +640,8 @@ static unsigned grid_stride_blocks(long long total, int block) {
   return (unsigned)(g > 0 ? g : 0);
 }
 
-hipError_t launch_row_r2c(int n, const float *x, float2 *out, long long planes, int rows_per_plane,
-                          ImgView in_view, long long in_plane_stride, int L, long long out_row_stride,
-                          long long out_plane_stride, float alpha, float beta, hipStream_t s) {
+hipError_t launch_row_r2c(int n, const float *x, SpecLayout out, long long planes, int rows_per_plane,
+                          ImgView in_view, long long in_plane_stride, int L, float alpha, float beta, hipStream_t s) {
   hipError_t err = hipErrorInvalidValue;
   dispatch_n(n, [&](auto nc) {
     constexpr int N = decltype(nc)::value;
@@ -599,27 +650,25 @@ hipError_t launch_row_r2c(int n, const float *x, float2 *out, long long planes, 
     const unsigned grid = (unsigned)((npairs + SPW - 1) / SPW);
     const size_t lds = lds_size(SPW * N) * sizeof(float2);
     static const std::string nm = "row_r2c_" + std::to_string(N);
-    const int ors = (int)out_row_stride;
     switch (in_view.mode) {
       case 0:
         err = launch(nm.c_str(), k_row_r2c<N, SPW, 0>, grid, SPW * FftCfg<N>::TPS, lds, s, x, out, npairs,
-                     rows_per_plane, in_view, in_plane_stride, L, ors, out_plane_stride, alpha, beta);
+                     rows_per_plane, in_view, in_plane_stride, L, alpha, beta);
         break;
       case 1:
         err = launch(nm.c_str(), k_row_r2c<N, SPW, 1>, grid, SPW * FftCfg<N>::TPS, lds, s, x, out, npairs,
-                     rows_per_plane, in_view, in_plane_stride, L, ors, out_plane_stride, alpha, beta);
+                     rows_per_plane, in_view, in_plane_stride, L, alpha, beta);
         break;
       default:
         err = launch(nm.c_str(), k_row_r2c<N, SPW, 2>, grid, SPW * FftCfg<N>::TPS, lds, s, x, out, npairs,
-                     rows_per_plane, in_view, in_plane_stride, L, ors, out_plane_stride, alpha, beta);
+                     rows_per_plane, in_view, in_plane_stride, L, alpha, beta);
     }
   });
   return err;
 }
 
-hipError_t launch_row_c2r(int n, const float2 *in, float *y, long long planes, int rows_per_plane, int L,
-                          long long in_row_stride, long long in_plane_stride, float alpha, float beta,
-                          ImgView out_view, long long out_plane_stride, hipStream_t s) {
+hipError_t launch_row_c2r(int n, SpecLayout in, float *y, long long planes, int rows_per_plane, int L, float alpha,
+                          float beta, ImgView out_view, long long out_plane_stride, hipStream_t s) {
   hipError_t err = hipErrorInvalidValue;
   dispatch_n(n, [&](auto nc) {
     constexpr int N = decltype(nc)::value;
@@ -628,25 +677,29 @@ hipError_t launch_row_c2r(int n, const float2 *in, float *y, long long planes, i
     const unsigned grid = (unsigned)((npairs + SPW - 1) / SPW);
     const size_t lds = lds_size(SPW * N) * sizeof(float2);
     static const std::string nm = "row_c2r_" + std::to_string(N);
-    const int irs = (int)in_row_stride;
     switch (out_view.mode) {
       case 0:
         err = launch(nm.c_str(), k_row_c2r<N, SPW, 0>, grid, SPW * FftCfg<N>::TPS, lds, s, in, y, npairs,
-                     rows_per_plane, L, irs, in_plane_stride, alpha, beta, out_view, out_plane_stride);
+                     rows_per_plane, L, alpha, beta, out_view, out_plane_stride);
         break;
       case 1:
         err = launch(nm.c_str(), k_row_c2r<N, SPW, 1>, grid, SPW * FftCfg<N>::TPS, lds, s, in, y, npairs,
-                     rows_per_plane, L, irs, in_plane_stride, alpha, beta, out_view, out_plane_stride);
+                     rows_per_plane, L, alpha, beta, out_view, out_plane_stride);
         break;
       default:
         err = launch(nm.c_str(), k_row_c2r<N, SPW, 2>, grid, SPW * FftCfg<N>::TPS, lds, s, in, y, npairs,
-                     rows_per_plane, L, irs, in_plane_stride, alpha, beta, out_view, out_plane_stride);
+                     rows_per_plane, L, alpha, beta, out_view, out_plane_stride);
     }
   });
   return err;
 }
 
-static unsigned col_tiles(long long ncols, int ct) { return (unsigned)((ncols + ct - 1) / ct); }
+// Grid of a column launch; 0 (nothing launched, error reported) when the tile or
+// column count does not fit the kernels' 32-bit tile arithmetic.
+static unsigned col_grid(long long planes, int L, int ct) {
+  const long long t = col_tile_count(planes, L, ct);
+  return (planes * L >= (1LL << 31) || t >= (1LL << 31)) ? 0u : (unsigned)t;
+}
 
 hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long long planes, int L, int ld,
                           long long in_plane_stride, long long out_plane_stride, hipStream_t s) {
@@ -654,16 +707,17 @@ hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long lo
   dispatch_n(n, [&](auto nc) {
     constexpr int N = decltype(nc)::value;
     constexpr int CT = col_ct<N>();
-    const long long ncols = planes * L;
     const size_t lds = lds_size(N * CT) * sizeof(float2);
+    const unsigned grid = col_grid(planes, L, CT);
+    if (grid == 0) return;
     static const std::string nf = "col_fft_fwd_" + std::to_string(N);
     static const std::string ni = "col_fft_inv_" + std::to_string(N);
     if (dir < 0)
-      err = launch(nf.c_str(), k_col_fft<N, CT, -1>, col_tiles(ncols, CT), CT * FftCfg<N>::TPS, lds, s, in, out, L,
-                   ld, ncols, in_plane_stride, out_plane_stride);
+      err = launch(nf.c_str(), k_col_fft<N, CT, -1>, grid, CT * FftCfg<N>::TPS, lds, s, in, out, L, ld, (int)planes,
+                   in_plane_stride, out_plane_stride);
     else
-      err = launch(ni.c_str(), k_col_fft<N, CT, +1>, col_tiles(ncols, CT), CT * FftCfg<N>::TPS, lds, s, in, out, L,
-                   ld, ncols, in_plane_stride, out_plane_stride);
+      err = launch(ni.c_str(), k_col_fft<N, CT, +1>, grid, CT * FftCfg<N>::TPS, lds, s, in, out, L, ld, (int)planes,
+                   in_plane_stride, out_plane_stride);
   });
   return err;
 }
@@ -674,15 +728,16 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
   dispatch_nm(n, m, [&](auto nc, auto mc) {
     constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
-    constexpr int CTN = col_ct<N>(), CTM = col_ct<M>();
+    constexpr int CTN = col_ct_for(col_ct<N>(), L), CTM = col_ct_for(col_ct<M>(), L);
     static const std::string n1 = "col_fwd_crop_" + std::to_string(N) + "_" + std::to_string(M);
     static const std::string n2 = "col_cic_inv_" + std::to_string(N) + "_" + std::to_string(M);
-    const long long nin = (long long)B * C * L, nout = (long long)B * S * L;
-    err = launch(n1.c_str(), k_col_fwd_crop<N, M, CTN>, col_tiles(nin, CTN), CTN * FftCfg<N>::TPS,
-                 lds_size(N * CTN) * sizeof(float2), s, T, Xh, nin);
+    const unsigned g1 = col_grid((long long)B * C, L, CTN), g2 = col_grid((long long)B * S, L, CTM);
+    if (g1 == 0 || g2 == 0) return;
+    err = launch(n1.c_str(), k_col_fwd_crop<N, M, CTN>, g1, CTN * FftCfg<N>::TPS, lds_size(N * CTN) * sizeof(float2),
+                 s, T, Xh, B * C);
     if (err != hipSuccess) return;
-    err = launch(n2.c_str(), k_col_cic_inv<N, M, CTM>, col_tiles(nout, CTM), CTM * FftCfg<M>::TPS,
-                 lds_size(M * CTM) * sizeof(float2), s, Xh, K, U, C, S / C, nout);
+    err = launch(n2.c_str(), k_col_cic_inv<N, M, CTM>, g2, CTM * FftCfg<M>::TPS, lds_size(M * CTM) * sizeof(float2),
+                 s, Xh, K, U, C, S / C, B * S);
   });
   return err;
 }
@@ -693,13 +748,14 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
   if (!cic_pair_supported(n, m)) return err;
   dispatch_n(m, [&](auto mc) {
     constexpr int M = decltype(mc)::value;
-    constexpr int CT = kGkCT, BP = gk_bp<M>();
     constexpr int L = M / 2 + 1;
-    const long long ncols = (long long)S * L;
+    constexpr int CT = col_ct_for(kGkCT, L), BP = gk_bp<M>();
     const size_t lds = lds_size(BP * M * CT) * sizeof(float2);
+    const unsigned grid = col_grid(S, L, CT);
+    if (grid == 0) return;
     static const std::string nm = "col_bwd_gk_" + std::to_string(M);
-    err = launch(nm.c_str(), k_col_bwd_gk<M, CT, BP>, col_tiles(ncols, CT), CT * FftCfg<M>::TPS * BP, lds, s, Tg,
-                 Xh, gK, B, C, S / C, n, ncols);
+    err = launch(nm.c_str(), k_col_bwd_gk<M, CT, BP>, grid, CT * FftCfg<M>::TPS * BP, lds, s, Tg, Xh, gK, B, C,
+                 S / C, n, S);
   });
   return err;
 }
@@ -709,13 +765,14 @@ hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, fl
   hipError_t err = hipErrorInvalidValue;
   dispatch_nm(n, m, [&](auto nc, auto mc) {
     constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
-    constexpr int CT = col_ct<N>();
     constexpr int L = M / 2 + 1;
-    const long long ncols = (long long)B * C * L;
+    constexpr int CT = col_ct_for(col_ct<N>(), L);
     const size_t lds = cic_lds_elems<N, M, CT>() * sizeof(float2);
+    const unsigned grid = col_grid((long long)B * C, L, CT);
+    if (grid == 0) return;
     static const std::string nm = "col_bwd_gx_" + std::to_string(N) + "_" + std::to_string(M);
-    err = launch(nm.c_str(), k_col_bwd_gx<N, M, CT>, col_tiles(ncols, CT), CT * FftCfg<N>::TPS, lds, s, Tg, K, V, C,
-                 S / C, ncols);
+    err = launch(nm.c_str(), k_col_bwd_gx<N, M, CT>, grid, CT * FftCfg<N>::TPS, lds, s, Tg, K, V, C, S / C,
+                 B * C);
   });
   return err;
 }

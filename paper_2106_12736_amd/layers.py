@@ -152,18 +152,18 @@ class CicLayer(_LayerPlan):
         self.fwd_ws = _workspace(self.fwd_ws_bytes, self.device)
         self.bwd_ws = _workspace(self.bwd_ws_bytes, self.device)
 
-    @property
-    def saved_ld(self):
-        """Row stride of the saved spectrum: M/2+1 rounded up to a multiple of 16."""
-        return self.saved_bytes // (8 * self.B * self.C * self.M)
-
     def new_saved(self):
-        """Buffer for the pooled input spectrum, [B][C][M][saved_ld] complex (columns > M/2 unused)."""
-        return torch.empty((self.B, self.C, self.M, self.saved_ld), dtype=torch.complex64, device=self.device)
+        """Buffer for the pooled input spectrum (see fdc_cic_layer_forward for its layout)."""
+        return torch.empty(self.saved_bytes // 8, dtype=torch.complex64, device=self.device)
 
     def saved_spectrum(self, saved):
-        """The M x (M/2+1) kept bins held in a saved buffer, as a [B][C][M][M/2+1] view."""
-        return saved[..., : self.M // 2 + 1]
+        """The M x (M/2+1) kept bins held in a saved buffer, as a [B][C][M][M/2+1] tensor:
+        columns 0..M/2-1 come from the main block, column M/2 from the block after it."""
+        B, C, M = self.B, self.C, self.M
+        h = M // 2
+        main = saved[: B * C * M * h].view(B, C, M, h)
+        side = saved[B * C * M * h:].view(B, C, M, 1)
+        return torch.cat([main, side], dim=-1)
 
     def new_output(self):
         return torch.empty((self.B, self.S, self.out, self.out), dtype=torch.float32, device=self.device)
