@@ -254,21 +254,25 @@ constexpr int stockham_ns(int p) {  // product of the radices before pass p
   return ns;
 }
 
-// LDS addressing of the Stockham exchanges.
-//   0: plain index;
-//   1: XOR swizzle inside each aligned block of 32 complex values (bits 5..9 of
-//      the index flip bits 0..4): contiguous accesses stay conflict-free and the
-//      power-of-two strides of the Stockham writes land in different banks;
-//   2: one complex value of padding after every 32.
-// lds_size(n) complex values hold indices [0, n) in every layout.
-constexpr int kLdsLayout = 2;
+// LDS addressing of the Stockham exchanges, chosen per kernel family:
+//   kLdsPlain: plain index.  With CT columns interleaved (element stride CT) the
+//              exchanges of the column kernels spread over the banks already, and
+//              constant offsets fold into the LDS instructions;
+//   kLdsXor:   XOR swizzle inside each aligned block of 32 complex values (bits 5..9
+//              of the index flip bits 0..4);
+//   kLdsPad:   one complex value of padding after every 32, which breaks up the
+//              power-of-two strides of the row kernels' exchanges (element stride 1).
+// lds_size<LAYOUT>(n) complex values hold indices [0, n).
+enum { kLdsPlain = 0, kLdsXor = 1, kLdsPad = 2 };
+template <int LAYOUT>
 __device__ __forceinline__ int lds_phys(int i) {
-  if constexpr (kLdsLayout == 0) return i;
-  else if constexpr (kLdsLayout == 1) return i ^ ((i >> 5) & 31);
+  if constexpr (LAYOUT == kLdsPlain) return i;
+  else if constexpr (LAYOUT == kLdsXor) return i ^ ((i >> 5) & 31);
   else return i + (i >> 5);
 }
+template <int LAYOUT>
 __host__ __device__ constexpr int lds_size(int n) {
-  return kLdsLayout == 2 ? n + (n >> 5) + 1 : (n + 31) & ~31;
+  return LAYOUT == kLdsPad ? n + (n >> 5) + 1 : (n + 31) & ~31;
 }
 
 // Barrier between the LDS writes and reads of an exchange.  WAVE: every
@@ -290,8 +294,8 @@ __device__ __forceinline__ void lds_barrier() {
 // on entry and exit.  Element e of the sequence lives in LDS at
 // lds[lds_phys(base + e * es)].  Every thread of the workgroup (of the wave with
 // WAVE) must call this: it contains barriers.  With LEAD_SYNC the first LDS write
-// waits for every thread's earlier use of the LDS.
-template <int N, int DIR, bool LEAD_SYNC = true, bool WAVE = false>
+// waits for every thread's earlier use of the LDS.  LAYOUT: lds_phys layout.
+template <int N, int DIR, bool LEAD_SYNC = true, bool WAVE = false, int LAYOUT = kLdsPlain>
 __device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2 *lds, int base, int es) {
   using C = FftCfg<N>;
   constexpr int E = C::E;
@@ -314,7 +318,7 @@ __device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2
         const int k = j % NS;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-          float2 x = lds[lds_phys(base + (j + r * NR) * es)];
+          float2 x = lds[lds_phys<LAYOUT>(base + (j + r * NR) * es)];
           if (r > 0) {
             float2 w = twiddle_load<N>(r * k * (N / (NS * R)));
             if (DIR > 0) w.y = -w.y;
@@ -344,7 +348,7 @@ __device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2
         const int j = t + TPS * q;
         const int jo = (j / NS) * NS * R + (j % NS);
 #pragma unroll
-        for (int r = 0; r < R; ++r) lds[lds_phys(base + (jo + r * NS) * es)] = a[q + BPT * r];
+        for (int r = 0; r < R; ++r) lds[lds_phys<LAYOUT>(base + (jo + r * NS) * es)] = a[q + BPT * r];
       }
       lds_barrier<WAVE>();
     }

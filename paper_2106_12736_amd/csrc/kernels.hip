@@ -53,6 +53,11 @@ __device__ __forceinline__ float bin_weight(int l, int n, float alpha, float bet
 
 extern __shared__ float2 g_lds[];
 
+// LDS layouts (see lds_phys): padded for the row transforms, plain for the column
+// transforms.
+constexpr int kRowLds = kLdsPad;
+constexpr int kColLds = kLdsPlain;
+
 // ---------------------------------------------------------------------------
 // row transforms
 // ---------------------------------------------------------------------------
@@ -90,19 +95,22 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(const float *__
     const int w = t + TPS * m;
     const int ia = view_index<MODE>(view, N, r0, w);
     const int ib = view_index<MODE>(view, N, r0 + 1, w);
-    v[m] = make_float2(ia >= 0 ? xp[ia] : 0.f, ib >= 0 ? xp[ib] : 0.f);
+    // unconditional loads (a cropped-away pixel reads element 0), zeroed afterwards: a load
+    // under a lane condition would be issued in its own branch and wait for its data alone
+    const float xa = xp[ia < 0 ? 0 : ia], xb = xp[ib < 0 ? 0 : ib];
+    v[m] = make_float2(ia >= 0 ? xa : 0.f, ib >= 0 ? xb : 0.f);
   }
-  fft_seq<N, -1, true, true>(v, t, lds, s * N, 1);
+  fft_seq<N, -1, true, true, kRowLds>(v, t, lds, s * N, 1);
   lds_barrier<true>();
 #pragma unroll
-  for (int m = 0; m < E; ++m) lds[lds_phys(s * N + t + TPS * m)] = v[m];
+  for (int m = 0; m < E; ++m) lds[lds_phys<kRowLds>(s * N + t + TPS * m)] = v[m];
   lds_barrier<true>();
   if (!active) return;
   float2 *oa = out.main + plane * out.ps + (long long)r0 * out.rs;
   float2 *ob = oa + out.rs;
   for (int k = t; k < L; k += TPS) {
-    const float2 zk = lds[lds_phys(s * N + k)];
-    const float2 zn = lds[lds_phys(s * N + (k == 0 ? 0 : N - k))];
+    const float2 zk = lds[lds_phys<kRowLds>(s * N + k)];
+    const float2 zn = lds[lds_phys<kRowLds>(s * N + (k == 0 ? 0 : N - k))];
     const float wgt = 0.5f * bin_weight(k, N, alpha, beta);
     // two real rows packed as z = a + i b:  A = (Z[k] + conj Z[-k]) / 2,  B = (Z[k] - conj Z[-k]) / (2i)
     const float2 A = make_float2((zk.x + zn.x) * wgt, (zk.y - zn.y) * wgt);
@@ -144,16 +152,14 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
     const int k = t + TPS * m;
     const bool upper = 2 * k > N;
     const int kk = upper ? N - k : k;
-    float2 a = make_float2(0.f, 0.f), b = make_float2(0.f, 0.f);
-    if (kk < L - 1) {
-      a = ia[kk];
-      b = ib[kk];
-    } else if (kk == L - 1) {
-      a = sa[0];
-      b = sa[in.srs];
-    }
+    // unconditional loads from valid addresses; bins beyond L get weight 0 (the loaded
+    // value is always used, so the load is not sunk into a per-lane branch)
+    const bool in_main = kk < L - 1;
+    const float2 *pa = in_main ? ia + kk : sa;
+    const float2 *pb = in_main ? ib + kk : sa + in.srs;
+    float2 a = *pa, b = *pb;
     const bool edge = (kk == 0 || 2 * kk == N);
-    const float wgt = edge ? alpha : alpha * beta;
+    const float wgt = kk < L ? (edge ? alpha : alpha * beta) : 0.f;
     a = cscale(a, wgt);
     b = cscale(b, wgt);
     if (edge) {  // real-part semantics of the inverse at l = 0 and l = n/2
@@ -166,7 +172,7 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
     }
     v[m] = make_float2(a.x - b.y, a.y + b.x);  // A + i B
   }
-  fft_seq<N, +1, true, true>(v, t, lds, s * N, 1);
+  fft_seq<N, +1, true, true, kRowLds>(v, t, lds, s * N, 1);
   if (!active) return;
   float *yp = y + plane * out_plane_stride;
 #pragma unroll
@@ -248,7 +254,7 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft(const float2 *in
   const float2 *ip = in + c.plane * in_plane_stride + c.l;
   float2 v[E];
 #pragma unroll
-  for (int m = 0; m < E; ++m) v[m] = c.ok ? ip[(long long)(t + TPS * m) * ld] : make_float2(0.f, 0.f);
+  for (int m = 0; m < E; ++m) v[m] = ip[(long long)(t + TPS * m) * ld];  // lanes past the end read a valid column
   fft_seq<N, DIR>(v, t, lds, s, CT);
   if (!c.ok) return;
   float2 *op = out + c.plane * out_plane_stride + c.l;
@@ -290,7 +296,7 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fwd_crop(const float
   const ColPtr tc = split_col<N, L>(T, planes, c.plane, c.l);
   float2 v[E];
 #pragma unroll
-  for (int m = 0; m < E; ++m) v[m] = c.ok ? tc.p[(t + TPS * m) * tc.stride] : make_float2(0.f, 0.f);
+  for (int m = 0; m < E; ++m) v[m] = tc.p[(t + TPS * m) * tc.stride];  // lanes past the end read a valid column
   fft_seq<N, -1>(v, t, lds, s, CT);
   if (!c.ok) return;
   const ColPtr xc = split_col<M, L>(Xh, planes, c.plane, c.l);
@@ -324,7 +330,7 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS) void k_col_cic_inv(const float2
 #pragma unroll
   for (int m = 0; m < E; ++m) {
     const int mrow = t + TPS * m;
-    z[m] = c.ok ? cmul(xc.p[mrow * xc.stride], kcol[kept_row<N, M>(mrow) * NF]) : make_float2(0.f, 0.f);
+    z[m] = cmul(xc.p[mrow * xc.stride], kcol[kept_row<N, M>(mrow) * NF]);  // valid column on every lane
   }
   fft_seq<M, +1>(z, t, lds, s, CT);
   if (!c.ok) return;
@@ -383,26 +389,28 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
     const bool act = c.ok && b < B;
     const ColPtr gc = split_col<M, L>(Tg, B * S, (act ? b : 0) * S + o, c.l);
     const ColPtr xc = split_col<M, L>(Xh, B * C, (act ? b : 0) * C + ci, c.l);
+    // loads are unconditional (inactive lanes read a valid column); inactive lanes add nothing
     float2 v[E];
 #pragma unroll
-    for (int m = 0; m < E; ++m) v[m] = act ? gc.p[(t + TPS * m) * gc.stride] : make_float2(0.f, 0.f);
+    for (int m = 0; m < E; ++m) v[m] = gc.p[(t + TPS * m) * gc.stride];
     fft_seq<M, -1>(v, t, lds, g * M * CT + s, CT);
-    if (act) {
 #pragma unroll
-      for (int m = 0; m < E; ++m) acc[m] = cfmac(acc[m], v[m], xc.p[(t + TPS * m) * xc.stride]);
+    for (int m = 0; m < E; ++m) {
+      const float2 sum = cfmac(acc[m], v[m], xc.p[(t + TPS * m) * xc.stride]);
+      acc[m] = act ? sum : acc[m];
     }
   }
   if constexpr (BP > 1) {
     __syncthreads();
 #pragma unroll
-    for (int m = 0; m < E; ++m) lds[lds_phys(g * M * CT + s + (t + TPS * m) * CT)] = acc[m];
+    for (int m = 0; m < E; ++m) lds[lds_phys<kColLds>(g * M * CT + s + (t + TPS * m) * CT)] = acc[m];
     __syncthreads();
     if (g != 0) return;
 #pragma unroll
     for (int m = 0; m < E; ++m) {
-      float2 sum = lds[lds_phys(s + (t + TPS * m) * CT)];
+      float2 sum = lds[lds_phys<kColLds>(s + (t + TPS * m) * CT)];
 #pragma unroll
-      for (int q = 1; q < BP; ++q) sum = cadd(sum, lds[lds_phys(q * M * CT + s + (t + TPS * m) * CT)]);
+      for (int q = 1; q < BP; ++q) sum = cadd(sum, lds[lds_phys<kColLds>(q * M * CT + s + (t + TPS * m) * CT)]);
       acc[m] = sum;
     }
   }
@@ -426,7 +434,7 @@ constexpr int cic_jp() {
 template <int N, int M, int CT>
 constexpr int cic_lds_elems() {
   constexpr int a = N * CT, b = cic_jp<N, M>() * M * CT;
-  return lds_size(a > b ? a : b);
+  return lds_size<kColLds>(a > b ? a : b);
 }
 
 // Backward, dL/dx: for the columns (b, c, l), column DFTs (M) of the J
@@ -461,20 +469,21 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
     const int o = ci * J + (act ? j : 0);
     const ColPtr gc = split_col<M, L>(Tg, planes * J, b * S + o, c.l);
     const float2 *kcol = K + (long long)o * N * NF + c.l;
+    // loads are unconditional (inactive lanes read a valid column); inactive lanes add nothing
     float2 g[CM::E];
 #pragma unroll
-    for (int m = 0; m < CM::E; ++m) g[m] = act ? gc.p[(tp + TPSM * m) * gc.stride] : make_float2(0.f, 0.f);
+    for (int m = 0; m < CM::E; ++m) g[m] = gc.p[(tp + TPSM * m) * gc.stride];
     fft_seq<M, -1>(g, tp, lds, js * M * CT + s, CT);
-    if (act) {
 #pragma unroll
-      for (int m = 0; m < CM::E; ++m)
-        acc[m] = cfmac(acc[m], g[m], kcol[(long long)kept_row<N, M>(tp + TPSM * m) * NF]);
+    for (int m = 0; m < CM::E; ++m) {
+      const float2 sum = cfmac(acc[m], g[m], kcol[(long long)kept_row<N, M>(tp + TPSM * m) * NF]);
+      acc[m] = act ? sum : acc[m];
     }
   }
   // sum the JP partial sums and scatter the pooled rows into the n-row column (FDP adjoint)
   __syncthreads();
 #pragma unroll
-  for (int m = 0; m < CM::E; ++m) lds[lds_phys(js * M * CT + s + (tp + TPSM * m) * CT)] = acc[m];
+  for (int m = 0; m < CM::E; ++m) lds[lds_phys<kColLds>(js * M * CT + s + (tp + TPSM * m) * CT)] = acc[m];
   __syncthreads();
   float2 w[CN::E];
 #pragma unroll
@@ -484,7 +493,7 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
     if (k < M / 2 || k >= N - M / 2) {
       const int mrow = k < M / 2 ? k : k - (N - M);
 #pragma unroll
-      for (int q = 0; q < JP; ++q) sum = cadd(sum, lds[lds_phys(q * M * CT + s + mrow * CT)]);
+      for (int q = 0; q < JP; ++q) sum = cadd(sum, lds[lds_phys<kColLds>(q * M * CT + s + mrow * CT)]);
     }
     w[m] = sum;
   }
@@ -648,7 +657,7 @@ hipError_t launch_row_r2c(int n, const float *x, SpecLayout out, long long plane
     constexpr int SPW = row_spw<N>();
     const long long npairs = planes * rows_per_plane / 2;
     const unsigned grid = (unsigned)((npairs + SPW - 1) / SPW);
-    const size_t lds = lds_size(SPW * N) * sizeof(float2);
+    const size_t lds = lds_size<kRowLds>(SPW * N) * sizeof(float2);
     static const std::string nm = "row_r2c_" + std::to_string(N);
     switch (in_view.mode) {
       case 0:
@@ -675,7 +684,7 @@ hipError_t launch_row_c2r(int n, SpecLayout in, float *y, long long planes, int 
     constexpr int SPW = row_spw<N>();
     const long long npairs = planes * rows_per_plane / 2;
     const unsigned grid = (unsigned)((npairs + SPW - 1) / SPW);
-    const size_t lds = lds_size(SPW * N) * sizeof(float2);
+    const size_t lds = lds_size<kRowLds>(SPW * N) * sizeof(float2);
     static const std::string nm = "row_c2r_" + std::to_string(N);
     switch (out_view.mode) {
       case 0:
@@ -707,7 +716,7 @@ hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long lo
   dispatch_n(n, [&](auto nc) {
     constexpr int N = decltype(nc)::value;
     constexpr int CT = col_ct<N>();
-    const size_t lds = lds_size(N * CT) * sizeof(float2);
+    const size_t lds = lds_size<kColLds>(N * CT) * sizeof(float2);
     const unsigned grid = col_grid(planes, L, CT);
     if (grid == 0) return;
     static const std::string nf = "col_fft_fwd_" + std::to_string(N);
@@ -733,10 +742,10 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
     static const std::string n2 = "col_cic_inv_" + std::to_string(N) + "_" + std::to_string(M);
     const unsigned g1 = col_grid((long long)B * C, L, CTN), g2 = col_grid((long long)B * S, L, CTM);
     if (g1 == 0 || g2 == 0) return;
-    err = launch(n1.c_str(), k_col_fwd_crop<N, M, CTN>, g1, CTN * FftCfg<N>::TPS, lds_size(N * CTN) * sizeof(float2),
+    err = launch(n1.c_str(), k_col_fwd_crop<N, M, CTN>, g1, CTN * FftCfg<N>::TPS, lds_size<kColLds>(N * CTN) * sizeof(float2),
                  s, T, Xh, B * C);
     if (err != hipSuccess) return;
-    err = launch(n2.c_str(), k_col_cic_inv<N, M, CTM>, g2, CTM * FftCfg<M>::TPS, lds_size(M * CTM) * sizeof(float2),
+    err = launch(n2.c_str(), k_col_cic_inv<N, M, CTM>, g2, CTM * FftCfg<M>::TPS, lds_size<kColLds>(M * CTM) * sizeof(float2),
                  s, Xh, K, U, C, S / C, B * S);
   });
   return err;
@@ -750,7 +759,7 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
     constexpr int M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
     constexpr int CT = col_ct_for(kGkCT, L), BP = gk_bp<M>();
-    const size_t lds = lds_size(BP * M * CT) * sizeof(float2);
+    const size_t lds = lds_size<kColLds>(BP * M * CT) * sizeof(float2);
     const unsigned grid = col_grid(S, L, CT);
     if (grid == 0) return;
     static const std::string nm = "col_bwd_gk_" + std::to_string(M);
