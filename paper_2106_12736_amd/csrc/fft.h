@@ -89,6 +89,20 @@ __device__ __forceinline__ float2 twiddle_load(int idx) {
   return *reinterpret_cast<const float2 *>(&g_twiddle<N>.v[2 * idx]);
 }
 
+// Kernels copy the twiddle table of their longest transform into LDS once and
+// read every twiddle from there: a table read from global memory costs a vector
+// memory instruction per twiddle, and the address unit, not DRAM, is what limits
+// these kernels.  A transform of length N / tws reads entry i * tws.
+template <int N>
+__host__ __device__ constexpr int twiddle_lds_elems() {
+  return (N + 31) & ~31;
+}
+template <int N>
+__device__ __forceinline__ void stage_twiddles(float2 *tw, int tid, int nthreads) {
+  for (int i = tid; i < N; i += nthreads) tw[i] = twiddle_load<N>(i);
+  __syncthreads();
+}
+
 // ---------------------------------------------------------------------------
 // compile-time loops
 // ---------------------------------------------------------------------------
@@ -295,8 +309,10 @@ __device__ __forceinline__ void lds_barrier() {
 // lds[lds_phys(base + e * es)].  Every thread of the workgroup (of the wave with
 // WAVE) must call this: it contains barriers.  With LEAD_SYNC the first LDS write
 // waits for every thread's earlier use of the LDS.  LAYOUT: lds_phys layout.
+// tw: twiddle table in LDS (stage_twiddles) of length N * tws.
 template <int N, int DIR, bool LEAD_SYNC = true, bool WAVE = false, int LAYOUT = kLdsPlain>
-__device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2 *lds, int base, int es) {
+__device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2 *lds, int base, int es,
+                                        const float2 *tw, int tws) {
   using C = FftCfg<N>;
   constexpr int E = C::E;
   constexpr int TPS = C::TPS;
@@ -320,7 +336,7 @@ __device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2
         for (int r = 0; r < R; ++r) {
           float2 x = lds[lds_phys<LAYOUT>(base + (j + r * NR) * es)];
           if (r > 0) {
-            float2 w = twiddle_load<N>(r * k * (N / (NS * R)));
+            float2 w = tw[r * k * (N / (NS * R)) * tws];
             if (DIR > 0) w.y = -w.y;
             x = cmul(x, w);
           }

@@ -79,7 +79,8 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(const float *__
   using Cfg = FftCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   static_assert(TPS <= 64, "a row sequence must fit in one wavefront");
-  float2 *lds = g_lds;
+  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
+  stage_twiddles<N>(tw, threadIdx.x, SPW * TPS);
   const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
   long long pair = (long long)xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
   const bool active = pair < npairs;
@@ -100,7 +101,7 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(const float *__
     const float xa = xp[ia < 0 ? 0 : ia], xb = xp[ib < 0 ? 0 : ib];
     v[m] = make_float2(ia >= 0 ? xa : 0.f, ib >= 0 ? xb : 0.f);
   }
-  fft_seq<N, -1, true, true, kRowLds>(v, t, lds, s * N, 1);
+  fft_seq<N, -1, true, true, kRowLds>(v, t, lds, s * N, 1, tw, 1);
   lds_barrier<true>();
 #pragma unroll
   for (int m = 0; m < E; ++m) lds[lds_phys<kRowLds>(s * N + t + TPS * m)] = v[m];
@@ -134,7 +135,8 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
   using Cfg = FftCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   static_assert(TPS <= 64, "a row sequence must fit in one wavefront");
-  float2 *lds = g_lds;
+  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
+  stage_twiddles<N>(tw, threadIdx.x, SPW * TPS);
   const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
   long long pair = (long long)xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
   const bool active = pair < npairs;
@@ -172,7 +174,7 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
     }
     v[m] = make_float2(a.x - b.y, a.y + b.x);  // A + i B
   }
-  fft_seq<N, +1, true, true, kRowLds>(v, t, lds, s * N, 1);
+  fft_seq<N, +1, true, true, kRowLds>(v, t, lds, s * N, 1, tw, 1);
   if (!active) return;
   float *yp = y + plane * out_plane_stride;
 #pragma unroll
@@ -248,14 +250,15 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft(const float2 *in
                                                                long long out_plane_stride) {
   using Cfg = FftCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
-  float2 *lds = g_lds;
+  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
+  stage_twiddles<N>(tw, threadIdx.x, CT * TPS);
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
   const float2 *ip = in + c.plane * in_plane_stride + c.l;
   float2 v[E];
 #pragma unroll
   for (int m = 0; m < E; ++m) v[m] = ip[(long long)(t + TPS * m) * ld];  // lanes past the end read a valid column
-  fft_seq<N, DIR>(v, t, lds, s, CT);
+  fft_seq<N, DIR>(v, t, lds, s, CT, tw, 1);
   if (!c.ok) return;
   float2 *op = out + c.plane * out_plane_stride + c.l;
 #pragma unroll
@@ -290,14 +293,15 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fwd_crop(const float
                                                                     float2 *__restrict__ Xh, int planes) {
   using CN = FftCfg<N>;
   constexpr int L = M / 2 + 1, TPS = CN::TPS, E = CN::E;
-  float2 *lds = g_lds;
+  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
+  stage_twiddles<N>(tw, threadIdx.x, CT * TPS);
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
   const ColPtr tc = split_col<N, L>(T, planes, c.plane, c.l);
   float2 v[E];
 #pragma unroll
   for (int m = 0; m < E; ++m) v[m] = tc.p[(t + TPS * m) * tc.stride];  // lanes past the end read a valid column
-  fft_seq<N, -1>(v, t, lds, s, CT);
+  fft_seq<N, -1>(v, t, lds, s, CT, tw, 1);
   if (!c.ok) return;
   const ColPtr xc = split_col<M, L>(Xh, planes, c.plane, c.l);
 #pragma unroll
@@ -318,7 +322,8 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS) void k_col_cic_inv(const float2
                                                                    int planes) {
   using CM = FftCfg<M>;
   constexpr int L = M / 2 + 1, NF = N / 2 + 1, TPS = CM::TPS, E = CM::E;
-  float2 *lds = g_lds;
+  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<M>();
+  stage_twiddles<M>(tw, threadIdx.x, CT * TPS);
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
   const int S = C * J;
@@ -332,7 +337,7 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS) void k_col_cic_inv(const float2
     const int mrow = t + TPS * m;
     z[m] = cmul(xc.p[mrow * xc.stride], kcol[kept_row<N, M>(mrow) * NF]);  // valid column on every lane
   }
-  fft_seq<M, +1>(z, t, lds, s, CT);
+  fft_seq<M, +1>(z, t, lds, s, CT, tw, 1);
   if (!c.ok) return;
   const ColPtr uc = split_col<M, L>(U, planes, c.plane, c.l);
 #pragma unroll
@@ -364,7 +369,8 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
   using CM = FftCfg<M>;
   constexpr int L = M / 2 + 1, TPS = CM::TPS, E = CM::E;
   constexpr int NT = CT * TPS * BP;
-  float2 *lds = g_lds;
+  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<M>();
+  stage_twiddles<M>(tw, threadIdx.x, NT);
   const int s = threadIdx.x % CT, t = (threadIdx.x / CT) % TPS, g = threadIdx.x / (CT * TPS);
   const int wg = xcd_remap(blockIdx.x, gridDim.x);
   const ColRef c = column_ref<CT>(wg, s, L, S);
@@ -393,7 +399,7 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
     float2 v[E];
 #pragma unroll
     for (int m = 0; m < E; ++m) v[m] = gc.p[(t + TPS * m) * gc.stride];
-    fft_seq<M, -1>(v, t, lds, g * M * CT + s, CT);
+    fft_seq<M, -1>(v, t, lds, g * M * CT + s, CT, tw, 1);
 #pragma unroll
     for (int m = 0; m < E; ++m) {
       const float2 sum = cfmac(acc[m], v[m], xc.p[(t + TPS * m) * xc.stride]);
@@ -452,7 +458,8 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
   constexpr int L = M / 2 + 1, NF = N / 2 + 1;
   constexpr int TPSN = CN::TPS, TPSM = CM::TPS, JP = cic_jp<N, M>();
   static_assert(JP * TPSM == TPSN, "thread layouts of the two transforms must nest");
-  float2 *lds = g_lds;
+  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
+  stage_twiddles<N>(tw, threadIdx.x, CT * TPSN);
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   const int tp = t % TPSM, js = t / TPSM;
   const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
@@ -473,7 +480,7 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
     float2 g[CM::E];
 #pragma unroll
     for (int m = 0; m < CM::E; ++m) g[m] = gc.p[(tp + TPSM * m) * gc.stride];
-    fft_seq<M, -1>(g, tp, lds, js * M * CT + s, CT);
+    fft_seq<M, -1>(g, tp, lds, js * M * CT + s, CT, tw, N / M);
 #pragma unroll
     for (int m = 0; m < CM::E; ++m) {
       const float2 sum = cfmac(acc[m], g[m], kcol[(long long)kept_row<N, M>(tp + TPSM * m) * NF]);
@@ -497,7 +504,7 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
     }
     w[m] = sum;
   }
-  fft_seq<N, +1>(w, t, lds, s, CT);
+  fft_seq<N, +1>(w, t, lds, s, CT, tw, 1);
   if (!c.ok) return;
   const ColPtr vc = split_col<N, L>(V, planes, c.plane, c.l);
 #pragma unroll
@@ -657,7 +664,7 @@ hipError_t launch_row_r2c(int n, const float *x, SpecLayout out, long long plane
     constexpr int SPW = row_spw<N>();
     const long long npairs = planes * rows_per_plane / 2;
     const unsigned grid = (unsigned)((npairs + SPW - 1) / SPW);
-    const size_t lds = lds_size<kRowLds>(SPW * N) * sizeof(float2);
+    const size_t lds = (twiddle_lds_elems<N>() + lds_size<kRowLds>(SPW * N)) * sizeof(float2);
     static const std::string nm = "row_r2c_" + std::to_string(N);
     switch (in_view.mode) {
       case 0:
@@ -684,7 +691,7 @@ hipError_t launch_row_c2r(int n, SpecLayout in, float *y, long long planes, int 
     constexpr int SPW = row_spw<N>();
     const long long npairs = planes * rows_per_plane / 2;
     const unsigned grid = (unsigned)((npairs + SPW - 1) / SPW);
-    const size_t lds = lds_size<kRowLds>(SPW * N) * sizeof(float2);
+    const size_t lds = (twiddle_lds_elems<N>() + lds_size<kRowLds>(SPW * N)) * sizeof(float2);
     static const std::string nm = "row_c2r_" + std::to_string(N);
     switch (out_view.mode) {
       case 0:
@@ -716,7 +723,7 @@ hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long lo
   dispatch_n(n, [&](auto nc) {
     constexpr int N = decltype(nc)::value;
     constexpr int CT = col_ct<N>();
-    const size_t lds = lds_size<kColLds>(N * CT) * sizeof(float2);
+    const size_t lds = (twiddle_lds_elems<N>() + lds_size<kColLds>(N * CT)) * sizeof(float2);
     const unsigned grid = col_grid(planes, L, CT);
     if (grid == 0) return;
     static const std::string nf = "col_fft_fwd_" + std::to_string(N);
@@ -742,10 +749,10 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
     static const std::string n2 = "col_cic_inv_" + std::to_string(N) + "_" + std::to_string(M);
     const unsigned g1 = col_grid((long long)B * C, L, CTN), g2 = col_grid((long long)B * S, L, CTM);
     if (g1 == 0 || g2 == 0) return;
-    err = launch(n1.c_str(), k_col_fwd_crop<N, M, CTN>, g1, CTN * FftCfg<N>::TPS, lds_size<kColLds>(N * CTN) * sizeof(float2),
+    err = launch(n1.c_str(), k_col_fwd_crop<N, M, CTN>, g1, CTN * FftCfg<N>::TPS, (twiddle_lds_elems<N>() + lds_size<kColLds>(N * CTN)) * sizeof(float2),
                  s, T, Xh, B * C);
     if (err != hipSuccess) return;
-    err = launch(n2.c_str(), k_col_cic_inv<N, M, CTM>, g2, CTM * FftCfg<M>::TPS, lds_size<kColLds>(M * CTM) * sizeof(float2),
+    err = launch(n2.c_str(), k_col_cic_inv<N, M, CTM>, g2, CTM * FftCfg<M>::TPS, (twiddle_lds_elems<M>() + lds_size<kColLds>(M * CTM)) * sizeof(float2),
                  s, Xh, K, U, C, S / C, B * S);
   });
   return err;
@@ -759,7 +766,7 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
     constexpr int M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
     constexpr int CT = col_ct_for(kGkCT, L), BP = gk_bp<M>();
-    const size_t lds = lds_size<kColLds>(BP * M * CT) * sizeof(float2);
+    const size_t lds = (twiddle_lds_elems<M>() + lds_size<kColLds>(BP * M * CT)) * sizeof(float2);
     const unsigned grid = col_grid(S, L, CT);
     if (grid == 0) return;
     static const std::string nm = "col_bwd_gk_" + std::to_string(M);
@@ -776,7 +783,7 @@ hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, fl
     constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
     constexpr int CT = col_ct_for(col_ct<N>(), L);
-    const size_t lds = cic_lds_elems<N, M, CT>() * sizeof(float2);
+    const size_t lds = (twiddle_lds_elems<N>() + cic_lds_elems<N, M, CT>()) * sizeof(float2);
     const unsigned grid = col_grid((long long)B * C, L, CT);
     if (grid == 0) return;
     static const std::string nm = "col_bwd_gx_" + std::to_string(N) + "_" + std::to_string(M);
