@@ -145,7 +145,12 @@ fdc_status fdc_cic_layer_plan_create(fdc_layer_plan **plan, int B, int C, int S,
                                      int artifact, int kernel_n);
 /* Full FDC layer (Algorithm 2 with the per-bin sum over input channels of Eq. 2):
  * x [B][Cin][P][P], weights w [Cout][Cin][n][n] spatial (padded to P x P at the
- * top-left and transformed on every call, section 2.4.1.2), y [B][Cout][..][..]. */
+ * top-left and transformed on every call, section 2.4.1.2), y [B][Cout][O][O] with
+ * O = P - n + 1 for CROP and P for NONE/ROLL.  P even and in the supported FFT
+ * set, 1 <= n <= 5 (FDC_EUNSUPPORTED otherwise).  No FDP: the layer keeps its
+ * spatial size.  The plan owns a P-entry device table of twiddle factors, so it
+ * is created on (and must be used with) the device current at creation;
+ * FDC_EHIP if that allocation fails. */
 fdc_status fdc_full_layer_plan_create(fdc_layer_plan **plan, int B, int Cin, int Cout, int P,
                                       int kernel_n, int artifact);
 fdc_status fdc_layer_plan_destroy(fdc_layer_plan *plan);
@@ -172,10 +177,15 @@ fdc_status fdc_cic_layer_backward(const fdc_layer_plan *plan, const float *gy, c
                                   void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* Full FDC forward: y = artifact(irfft2(sum_c rfft2(x[b][c]) o K[s][c])) with
- * K[s][c] = rfft2(pad(w[s][c])).  `saved` receives rfft2(x) [B][Cin][P][P/2+1]. */
+ * K[s][c] = rfft2(pad(w[s][c])).  K is generated per bin inside the contraction
+ * and never stored.  `saved` (may be NULL) receives rfft2(x) as a plain complex
+ * [B][Cin][P][P/2+1] array; the backward pass reads it for dL/dw. */
 fdc_status fdc_full_forward(const fdc_layer_plan *plan, const float *x, const float *w, float *y,
                             void *saved, void *ws, size_t ws_bytes, hipStream_t stream);
-/* Full FDC backward: gx [B][Cin][P][P] (NULL: skipped), gw [Cout][Cin][n][n] (NULL: skipped). */
+/* Full FDC backward: gy [B][Cout][O][O] -> gx [B][Cin][P][P] (NULL: skipped) and
+ * gw [Cout][Cin][n][n] (NULL: skipped; needs `saved`).  w is needed only for gx.
+ * gw is summed over bins in fixed-size chunks and then over chunks in order, so
+ * repeated calls give identical results. */
 fdc_status fdc_full_backward(const fdc_layer_plan *plan, const float *gy, const void *saved,
                              const float *w, float *gx, float *gw, void *ws, size_t ws_bytes,
                              hipStream_t stream);

@@ -4,6 +4,7 @@
 #include "../../include/fdc.h"
 #include "internal.h"
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -50,6 +51,7 @@ struct fdc_layer_plan {
   int kind;  // 0: CIC + FDP, 1: Full FDC
   int B, C, S, N, M, artifact, kn, out;
   size_t fwd_ws, saved, bwd_ws;
+  float2 *tw;  // Full FDC: device table W^j = exp(-2 pi i j / N), j < N (owned by the plan)
 };
 
 // ---------------------------------------------------------------------------
@@ -332,6 +334,7 @@ fdc_status fdc_layer_plan_destroy(fdc_layer_plan *plan) {
   if (plan == nullptr) return FDC_OK;
   if (plan->magic != kLayerMagic) return fail(FDC_EINVAL, "invalid or destroyed layer plan");
   plan->magic = 0;
+  if (plan->tw != nullptr) hipFree(plan->tw);
   delete plan;
   return FDC_OK;
 }
@@ -419,22 +422,152 @@ fdc_status fdc_cic_layer_backward(const fdc_layer_plan *p, const float *gy, cons
   return FDC_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Full FDC
+// ---------------------------------------------------------------------------
+namespace {
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+struct FullWs {  // byte offsets inside the forward / backward workspaces
+  size_t x, y, wf;         // forward: X (when `saved` is NULL), Y, rearranged weights
+  size_t g, gx, wg, part;  // backward: G, dL/dX spectrum, rearranged weights, dL/dw partials
+};
+FullWs full_layout(int B, int Cin, int Cout, int P, int kn, size_t *fwd, size_t *bwd) {
+  const size_t spec = (size_t)P * (P / 2 + 1) * sizeof(fdc_c64);
+  const size_t wsz = (size_t)Cout * Cin * kn * kn * sizeof(float);
+  FullWs w{};
+  w.x = 0;
+  w.y = align256(w.x + (size_t)B * Cin * spec);
+  w.wf = align256(w.y + (size_t)B * Cout * spec);
+  *fwd = align256(w.wf + wsz);
+  w.g = 0;
+  w.gx = align256(w.g + (size_t)B * Cout * spec);
+  w.wg = align256(w.gx + (size_t)B * Cin * spec);
+  w.part = align256(w.wg + wsz);
+  *bwd = align256(w.part + (size_t)fdc::full_gw_chunks(B, Cout, Cin, P) * wsz);
+  return w;
+}
+}  // namespace
+
 fdc_status fdc_full_layer_plan_create(fdc_layer_plan **plan, int B, int Cin, int Cout, int P, int kernel_n,
                                       int artifact) {
   if (plan == nullptr) return fail(FDC_EINVAL, "plan out-pointer is NULL");
   *plan = nullptr;
-  (void)B, (void)Cin, (void)Cout, (void)P, (void)kernel_n, (void)artifact;
-  return fail(FDC_EUNSUPPORTED, "Full FDC is not built yet");
+  if (B < 1 || Cin < 1 || Cout < 1) return fail(FDC_EINVAL, "B, Cin, Cout must be >= 1 (%d, %d, %d)", B, Cin, Cout);
+  if (B > 65535 * 16) return fail(FDC_EUNSUPPORTED, "B = %d exceeds the contraction grid (at most %d)", B, 65535 * 16);
+  if (!even_pos(P)) return fail(FDC_EINVAL, "P must be positive and even (got %d)", P);
+  if (artifact < FDC_ARTIFACT_NONE || artifact > FDC_ARTIFACT_ROLL) return fail(FDC_EINVAL, "bad artifact mode");
+  if (kernel_n < 1 || kernel_n > P) return fail(FDC_EINVAL, "kernel_n must be in [1, P] (got %d)", kernel_n);
+  if (!fdc::size_supported(P)) return fail(FDC_EUNSUPPORTED, "image size %d not supported", P);
+  if (!fdc::full_kernel_size_supported(kernel_n))
+    return fail(FDC_EUNSUPPORTED, "Full FDC supports kernel_n 1..5 (got %d)", kernel_n);
+  auto *p = new (std::nothrow) fdc_layer_plan{};
+  if (p == nullptr) return fail(FDC_EINVAL, "out of host memory");
+  p->magic = kLayerMagic;
+  p->kind = 1;
+  p->B = B, p->C = Cin, p->S = Cout, p->N = P, p->M = P;
+  p->artifact = artifact;
+  p->kn = kernel_n;
+  p->out = artifact == FDC_ARTIFACT_CROP ? P - kernel_n + 1 : P;
+  full_layout(B, Cin, Cout, P, kernel_n, &p->fwd_ws, &p->bwd_ws);
+  p->saved = (size_t)B * Cin * P * (P / 2 + 1) * sizeof(fdc_c64);
+  std::vector<float2> tw(P);
+  for (int j = 0; j < P; ++j) {
+    const double ang = -2.0 * 3.14159265358979323846 * (double)j / (double)P;
+    tw[j] = make_float2((float)std::cos(ang), (float)std::sin(ang));
+  }
+  if (hipMalloc(&p->tw, P * sizeof(float2)) != hipSuccess) {
+    delete p;
+    return fail(FDC_EHIP, "hipMalloc of the %d-entry twiddle table failed", P);
+  }
+  if (hipMemcpy(p->tw, tw.data(), P * sizeof(float2), hipMemcpyHostToDevice) != hipSuccess) {
+    hipFree(p->tw);
+    delete p;
+    return fail(FDC_EHIP, "copy of the twiddle table failed");
+  }
+  *plan = p;
+  return FDC_OK;
 }
 
-fdc_status fdc_full_forward(const fdc_layer_plan *p, const float *, const float *, float *, void *, void *, size_t,
-                            hipStream_t) {
-  return check_layer_plan(p, 1);
+fdc_status fdc_full_forward(const fdc_layer_plan *p, const float *x, const float *w, float *y, void *saved, void *ws,
+                            size_t ws_bytes, hipStream_t s) {
+  if (fdc_status st = check_layer_plan(p, 1)) return st;
+  if (!x || !w || !y) return fail(FDC_EINVAL, "NULL tensor");
+  if (fdc_status st = check_ws(ws, ws_bytes, p->fwd_ws)) return st;
+  const int B = p->B, Cin = p->C, Cout = p->S, P = p->N, Pf = P / 2 + 1;
+  size_t fwd, bwd;
+  const FullWs L = full_layout(B, Cin, Cout, P, p->kn, &fwd, &bwd);
+  char *base = static_cast<char *>(ws);
+  auto *X = saved != nullptr ? static_cast<float2 *>(saved) : reinterpret_cast<float2 *>(base + L.x);
+  auto *Y = reinterpret_cast<float2 *>(base + L.y);
+  auto *wf = reinterpret_cast<float *>(base + L.wf);
+  const long long spec = (long long)P * Pf;
+  ImgView id{0, 0, P, P};
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(P, x, fdc::plain_layout(X, P, Pf), (long long)B * Cin, P, id,
+                                                    (long long)P * P, Pf, 1.f, 1.f, s), "full forward rows"))
+    return st;
+  if (fdc_status st = check_hip(fdc::launch_col_fft(P, -1, X, X, (long long)B * Cin, Pf, Pf, spec, spec, s),
+                                "full forward columns"))
+    return st;
+  if (fdc_status st = check_hip(fdc::launch_full_weights(w, wf, nullptr, Cout, Cin, p->kn, s), "full weights"))
+    return st;
+  if (fdc_status st = check_hip(fdc::launch_full_contract(false, p->kn, X, wf, p->tw, Y, B, Cin, Cout, P, s),
+                                "full forward contraction"))
+    return st;
+  if (fdc_status st = check_hip(fdc::launch_col_fft(P, +1, Y, Y, (long long)B * Cout, Pf, Pf, spec, spec, s),
+                                "full forward inverse columns"))
+    return st;
+  return check_hip(fdc::launch_row_c2r(P, fdc::plain_layout(Y, P, Pf), y, (long long)B * Cout, P, Pf,
+                                       1.f / ((float)P * (float)P), 1.f, artifact_view(p), (long long)p->out * p->out, s),
+                   "full forward inverse rows");
 }
 
-fdc_status fdc_full_backward(const fdc_layer_plan *p, const float *, const void *, const float *, float *, float *,
-                             void *, size_t, hipStream_t) {
-  return check_layer_plan(p, 1);
+fdc_status fdc_full_backward(const fdc_layer_plan *p, const float *gy, const void *saved, const float *w, float *gx,
+                             float *gw, void *ws, size_t ws_bytes, hipStream_t s) {
+  if (fdc_status st = check_layer_plan(p, 1)) return st;
+  if (!gy) return fail(FDC_EINVAL, "gy is NULL");
+  if (gx && !w) return fail(FDC_EINVAL, "w is NULL but gx was requested");
+  if (gw && !saved) return fail(FDC_EINVAL, "saved is NULL but gw was requested");
+  if (!gx && !gw) return FDC_OK;
+  if (fdc_status st = check_ws(ws, ws_bytes, p->bwd_ws)) return st;
+  const int B = p->B, Cin = p->C, Cout = p->S, P = p->N, Pf = P / 2 + 1;
+  size_t fwd, bwd;
+  const FullWs L = full_layout(B, Cin, Cout, P, p->kn, &fwd, &bwd);
+  char *base = static_cast<char *>(ws);
+  auto *G = reinterpret_cast<float2 *>(base + L.g);
+  auto *gX = reinterpret_cast<float2 *>(base + L.gx);
+  auto *wg = reinterpret_cast<float *>(base + L.wg);
+  auto *part = reinterpret_cast<float *>(base + L.part);
+  const long long spec = (long long)P * Pf;
+  // G = adjoint of the inverse transform and the artifact step: (c_l / P^2) rfft2 of gy placed in P x P
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(P, gy, fdc::plain_layout(G, P, Pf), (long long)B * Cout, P,
+                                                    artifact_view(p), (long long)p->out * p->out, Pf,
+                                                    1.f / ((float)P * (float)P), 2.f, s),
+                                "full backward rows"))
+    return st;
+  if (fdc_status st = check_hip(fdc::launch_col_fft(P, -1, G, G, (long long)B * Cout, Pf, Pf, spec, spec, s),
+                                "full backward columns"))
+    return st;
+  if (gw) {
+    if (fdc_status st = check_hip(fdc::launch_full_gw(p->kn, G, static_cast<const float2 *>(saved), p->tw, part, gw, B,
+                                                      Cout, Cin, P, s), "full backward dw"))
+      return st;
+  }
+  if (gx) {
+    if (fdc_status st = check_hip(fdc::launch_full_weights(w, nullptr, wg, Cout, Cin, p->kn, s), "full weights"))
+      return st;
+    if (fdc_status st = check_hip(fdc::launch_full_contract(true, p->kn, G, wg, p->tw, gX, B, Cout, Cin, P, s),
+                                  "full backward dx contraction"))
+      return st;
+    // rfft2 adjoint: P^2 irfft2(gX / c_l)
+    if (fdc_status st = check_hip(fdc::launch_col_fft(P, +1, gX, gX, (long long)B * Cin, Pf, Pf, spec, spec, s),
+                                  "full backward dx columns"))
+      return st;
+    ImgView id{0, 0, P, P};
+    return check_hip(fdc::launch_row_c2r(P, fdc::plain_layout(gX, P, Pf), gx, (long long)B * Cin, P, Pf, 1.f, 0.5f, id,
+                                         (long long)P * P, s),
+                     "full backward dx rows");
+  }
+  return FDC_OK;
 }
 
 // ---------------------------------------------------------------------------

@@ -82,6 +82,16 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
 hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, float2 *V, int B, int C, int S,
                              hipStream_t s);
 
+// Full FDC (full_fdc.hip).  Spectra in the plain layout [planes][P][P/2+1]; tw is the
+// device table W^j = exp(-2 pi i j / P), j < P.
+bool full_kernel_size_supported(int nk);
+int full_gw_chunks(int B, int S, int C, int P);
+hipError_t launch_full_weights(const float *w, float *wf, float *wg, int S, int C, int nk, hipStream_t s);
+hipError_t launch_full_contract(bool gx, int nk, const float2 *in, const float *wt, const float2 *tw, float2 *out,
+                                int B, int KD, int ND, int P, hipStream_t s);
+hipError_t launch_full_gw(int nk, const float2 *G, const float2 *X, const float2 *tw, float *part, float *gw, int B,
+                          int S, int C, int P, hipStream_t s);
+
 // Spectral CIC and FDP.
 hipError_t launch_cic_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, long long P,
                           hipStream_t s);

@@ -187,6 +187,48 @@ class CicLayer(_LayerPlan):
         return (gx if need_gx else None), (gK if need_gk else None)
 
 
+class FullLayer(_LayerPlan):
+    """Full FDC layer: x [B][Cin][P][P], w [Cout][Cin][n][n] -> y [B][Cout][O][O]
+    (fdc_full_layer_*).  Workspaces are allocated once per layer object."""
+
+    def __init__(self, B, Cin, Cout, P, kernel_n=3, artifact="crop", device="cuda"):
+        self.B, self.Cin, self.Cout, self.P, self.n = B, Cin, Cout, P, kernel_n
+        self._p = ctypes.c_void_p()
+        call("fdc_full_layer_plan_create", ctypes.byref(self._p), B, Cin, Cout, P, kernel_n, _ARTIFACTS[artifact])
+        self._sizes()
+        self.device = torch.device(device)
+        self.fwd_ws = _workspace(self.fwd_ws_bytes, self.device)
+        self.bwd_ws = _workspace(self.bwd_ws_bytes, self.device)
+
+    def new_saved(self):
+        """Buffer for rfft2(x), [B][Cin][P][P/2+1] complex."""
+        return torch.empty((self.B, self.Cin, self.P, self.P // 2 + 1), dtype=torch.complex64, device=self.device)
+
+    def new_output(self):
+        return torch.empty((self.B, self.Cout, self.out, self.out), dtype=torch.float32, device=self.device)
+
+    def forward(self, x, w, y=None, saved=None):
+        _check(x, torch.float32, (self.B, self.Cin, self.P, self.P), "x")
+        _check(w, torch.float32, (self.Cout, self.Cin, self.n, self.n), "w")
+        if saved is not None:
+            _check(saved, torch.complex64, (self.B, self.Cin, self.P, self.P // 2 + 1), "saved")
+        y = self.new_output() if y is None else y
+        _check(y, torch.float32, (self.B, self.Cout, self.out, self.out), "y")
+        call("fdc_full_forward", self._p, _ptr(x), _ptr(w), _ptr(y), _ptr(saved), _ptr(self.fwd_ws),
+             self.fwd_ws.numel(), _stream())
+        return y
+
+    def backward(self, gy, saved, w, need_gx=True, need_gw=True, gx=None, gw=None):
+        _check(gy, torch.float32, (self.B, self.Cout, self.out, self.out), "gy")
+        if need_gx and gx is None:
+            gx = torch.empty((self.B, self.Cin, self.P, self.P), dtype=torch.float32, device=self.device)
+        if need_gw and gw is None:
+            gw = torch.empty((self.Cout, self.Cin, self.n, self.n), dtype=torch.float32, device=self.device)
+        call("fdc_full_backward", self._p, _ptr(gy), _ptr(saved), _ptr(w), _ptr(gx if need_gx else None),
+             _ptr(gw if need_gw else None), _ptr(self.bwd_ws), self.bwd_ws.numel(), _stream())
+        return (gx if need_gx else None), (gw if need_gw else None)
+
+
 class CicStack:
     """A stack of fused CIC + FDP layers with preallocated activations, saved
     spectra and gradients, so that one forward + backward step allocates nothing."""

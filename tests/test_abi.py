@@ -9,7 +9,7 @@ import ctypes
 import pytest
 
 from paper_2106_12736_amd import _lib
-from paper_2106_12736_amd._lib import FDC_EINVAL, FDC_EUNSUPPORTED, FDC_EWORKSPACE, FDC_OK
+from paper_2106_12736_amd._lib import FDC_EHIP, FDC_EINVAL, FDC_EUNSUPPORTED, FDC_EWORKSPACE, FDC_OK
 
 
 def test_library_exports_every_declared_function():
@@ -104,6 +104,47 @@ def test_layer_calls_reject_bad_arguments():
     assert _lib.status("fdc_cic_layer_backward", p, d, d, d, d, None, None, 8, None) == FDC_EWORKSPACE
     # a plan of the other kind is refused
     assert _lib.status("fdc_full_forward", p, d, d, d, d, d, 1 << 30, None) == FDC_EINVAL
+    assert _lib.status("fdc_layer_plan_destroy", p) == FDC_OK
+
+
+@pytest.mark.parametrize("args,expect", [
+    ((2, 3, 4, 16, 6, 1), FDC_EUNSUPPORTED),   # kernel_n beyond the generated-spectrum set
+    ((2, 3, 4, 15, 3, 1), FDC_EINVAL),         # odd P
+    ((2, 3, 4, 16, 17, 1), FDC_EINVAL),        # kernel larger than the image
+    ((2, 3, 4, 16, 0, 1), FDC_EINVAL),
+    ((2, 3, 4, 16, 3, 7), FDC_EINVAL),         # artifact mode
+    ((0, 3, 4, 16, 3, 1), FDC_EINVAL),
+    ((2, 0, 4, 16, 3, 1), FDC_EINVAL),
+    ((2, 3, 0, 16, 3, 1), FDC_EINVAL),
+    ((2, 3, 4, 2048, 3, 1), FDC_EUNSUPPORTED),  # outside the FFT length set
+])
+def test_full_plan_validation(args, expect):
+    """Arguments are checked before the plan touches the device."""
+    p = ctypes.c_void_p(0x1234)
+    assert _lib.status("fdc_full_layer_plan_create", ctypes.byref(p), *args) == expect
+    assert p.value is None
+
+
+def test_full_plan_valid_sizes_reach_the_device():
+    """Valid sizes pass validation; without a device the twiddle-table allocation fails
+    with FDC_EHIP, with a device the plan is made and reports its sizes."""
+    p = ctypes.c_void_p()
+    st = _lib.status("fdc_full_layer_plan_create", ctypes.byref(p), 2, 3, 4, 16, 3, 1)
+    assert st in (FDC_OK, FDC_EHIP)
+    if st == FDC_EHIP:
+        assert "twiddle" in _lib.last_error()
+        return
+    f, sv, b = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+    assert _lib.status("fdc_layer_workspace_size", p, ctypes.byref(f), ctypes.byref(sv), ctypes.byref(b)) == FDC_OK
+    assert sv.value == 2 * 3 * 16 * 9 * 8
+    o = ctypes.c_int()
+    assert _lib.status("fdc_layer_output_size", p, ctypes.byref(o)) == FDC_OK
+    assert o.value == 14
+    d = ctypes.c_void_p(0x1000)
+    # a plan of the other kind is refused
+    assert _lib.status("fdc_cic_layer_forward", p, d, d, d, None, d, 1 << 30, None) == FDC_EINVAL
+    assert _lib.status("fdc_full_forward", p, d, d, d, None, None, 0, None) == FDC_EWORKSPACE
+    assert _lib.status("fdc_full_backward", p, d, None, d, None, d, d, 1 << 30, None) == FDC_EINVAL
     assert _lib.status("fdc_layer_plan_destroy", p) == FDC_OK
 
 

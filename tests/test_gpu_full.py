@@ -1,0 +1,159 @@
+"""GPU parity of the Full FDC layer (Algorithm 2 with the per-bin channel sum of
+Eq. 2; kernel spectra generated from n x n weights as in section 2.4.1.2) and its
+backward, against the float64 oracle on the same seeded inputs.
+
+Small cases are compared element by element; they span several batch tiles, output
+blocks, contraction steps and dL/dw channel blocks, each with a ragged edge.  The
+six 16-image VGG-block layers (224 and 512 pixels, 64/128/256 channels) run at full
+size in the same launch configuration the benchmark times, and are checked on
+sampled (image, channel) slices, each of which the oracle computes on its own."""
+
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+from _parity import assert_parity, to_np
+from oracle import dft, fdc
+from paper_2106_12736_amd import inputs, layers
+
+pytestmark = pytest.mark.gpu
+
+ORACLE_MODE = {"none": fdc.ARTIFACT_NONE, "crop": fdc.ARTIFACT_CROP, "roll": fdc.ARTIFACT_ROLL}
+
+
+def _rng(*key):
+    return np.random.default_rng(zlib.crc32(repr(key).encode()))
+
+
+def _gpu(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _out_size(P, n, artifact):
+    return P - n + 1 if artifact == "crop" else P
+
+
+SMALL_CASES = [
+    # B, Cin, Cout, P, n, artifact
+    (1, 1, 1, 4, 3, "crop"),
+    (2, 3, 5, 8, 3, "crop"),
+    (3, 2, 4, 8, 2, "roll"),
+    (17, 6, 9, 16, 3, "crop"),     # two batch tiles, ragged
+    (2, 5, 300, 16, 1, "none"),    # two forward output blocks
+    (2, 300, 3, 16, 3, "none"),    # two dL/dX output blocks, 75 contraction steps
+    (5, 33, 40, 32, 5, "roll"),    # two dL/dw channel blocks each way
+    (40, 3, 4, 16, 3, "crop"),     # three dL/dw batch chunks, ragged
+    (2, 4, 4, 64, 4, "crop"),
+    (16, 8, 8, 128, 3, "crop"),
+    (4, 3, 5, 224, 3, "crop"),
+    (2, 2, 3, 256, 3, "roll"),
+    (1, 2, 2, 512, 5, "none"),
+    (1, 1, 2, 1024, 3, "crop"),
+]
+
+
+@pytest.mark.parametrize("B,Cin,Cout,P,n,artifact", SMALL_CASES)
+def test_full_layer_forward_backward(B, Cin, Cout, P, n, artifact):
+    print(f"full B={B} Cin={Cin} Cout={Cout} P={P} n={n} {artifact}", flush=True)
+    rng = _rng("full", B, Cin, Cout, P, n, artifact)
+    O = _out_size(P, n, artifact)
+    x = inputs.normal(rng, (B, Cin, P, P))
+    w = inputs.he_normal_weights(rng, Cout, Cin, n)
+    gy = inputs.normal(rng, (B, Cout, O, O))
+
+    layer = layers.FullLayer(B, Cin, Cout, P, kernel_n=n, artifact=artifact)
+    assert layer.out == O
+    xd, wd = _gpu(x), _gpu(w)
+    saved = layer.new_saved()
+    y = layer.forward(xd, wd, saved=saved)
+    gx, gw = layer.backward(_gpu(gy), saved, wd)
+    torch.cuda.synchronize()
+
+    mode = ORACLE_MODE[artifact]
+    y_ref, xs_ref = fdc.full_fdc_forward(x.astype(np.float64), w.astype(np.float64), mode)
+    gx_ref, gw_ref = fdc.full_fdc_backward(gy.astype(np.float64), xs_ref, w.astype(np.float64), mode)
+    assert_parity(to_np(saved), xs_ref, "saved rfft2(x)")
+    assert_parity(to_np(y), y_ref, "y")
+    assert_parity(to_np(gx), gx_ref, "gx")
+    assert_parity(to_np(gw), gw_ref, "gw")
+
+
+def test_full_layer_optional_outputs_and_repeatability():
+    """Forward without `saved`, backward with only one of the two gradients, and
+    bit-identical results on a second call (fixed reduction order)."""
+    B, Cin, Cout, P, n = 3, 5, 7, 32, 3
+    rng = _rng("full-optional")
+    x = inputs.normal(rng, (B, Cin, P, P))
+    w = inputs.he_normal_weights(rng, Cout, Cin, n)
+    gy = inputs.normal(rng, (B, Cout, P - n + 1, P - n + 1))
+    layer = layers.FullLayer(B, Cin, Cout, P, kernel_n=n, artifact="crop")
+    xd, wd, gyd = _gpu(x), _gpu(w), _gpu(gy)
+    y0 = layer.forward(xd, wd)
+    saved = layer.new_saved()
+    y1 = layer.forward(xd, wd, saved=saved)
+    assert torch.equal(y0, y1)
+    gx_only, none_w = layer.backward(gyd, None, wd, need_gw=False)
+    assert none_w is None
+    none_x, gw_only = layer.backward(gyd, saved, None, need_gx=False)
+    assert none_x is None
+    gx, gw = layer.backward(gyd, saved, wd)
+    gx2, gw2 = layer.backward(gyd, saved, wd)
+    torch.cuda.synchronize()
+    assert torch.equal(gx_only, gx) and torch.equal(gw_only, gw)
+    assert torch.equal(gx, gx2) and torch.equal(gw, gw2)
+    y_ref, xs_ref = fdc.full_fdc_forward(x.astype(np.float64), w.astype(np.float64), fdc.ARTIFACT_CROP)
+    gx_ref, gw_ref = fdc.full_fdc_backward(gy.astype(np.float64), xs_ref, w.astype(np.float64),
+                                           fdc.ARTIFACT_CROP)
+    assert_parity(to_np(y0), y_ref, "y")
+    assert_parity(to_np(gx), gx_ref, "gx")
+    assert_parity(to_np(gw), gw_ref, "gw")
+
+
+def test_full_layer_cic_special_case():
+    """With Cin = Cout = 1 and a 1 x 1 kernel the layer scales the image by w."""
+    x = inputs.normal(_rng("full-1x1"), (4, 1, 64, 64))
+    layer = layers.FullLayer(4, 1, 1, 64, kernel_n=1, artifact="none")
+    w = torch.full((1, 1, 1, 1), -1.75, device="cuda")
+    y = layer.forward(_gpu(x), w)
+    torch.cuda.synchronize()
+    assert_parity(to_np(y), -1.75 * x.astype(np.float64), "y")
+
+
+@pytest.mark.parametrize("wl", inputs.FULL_FDC_WORKLOADS, ids=lambda w: w.name)
+def test_full_layer_workload_sampled(wl):
+    """Full-size layer in the benchmark's configuration; the oracle checks sampled
+    slices: y[b][s], gx[b][c], saved[b][c] for sampled images b and channels, and
+    gw[s][c] (a sum over the whole batch) for sampled channel pairs."""
+    print(f"full workload {wl.name}", flush=True)
+    d = inputs.make_full_fdc(wl)
+    B, Cin, Cout, P, n = wl.batch, wl.cin, wl.cout, wl.size, wl.n
+    layer = layers.FullLayer(B, Cin, Cout, P, kernel_n=n, artifact="crop")
+    xd, wd, gyd = _gpu(d.x), _gpu(d.w), _gpu(d.grad)
+    saved = layer.new_saved()
+    y = layer.forward(xd, wd, saved=saved)
+    gx, gw = layer.backward(gyd, saved, wd)
+    torch.cuda.synchronize()
+    print("  gpu done", flush=True)
+
+    bs = [0, B - 1]
+    ss = [0, Cout // 2 + 1, Cout - 1]
+    cs = [0, Cin // 3, Cin - 1]
+    x64 = d.x.astype(np.float64)
+    w64 = d.w.astype(np.float64)
+    g64 = d.grad.astype(np.float64)
+    crop = fdc.ARTIFACT_CROP
+    for b in bs:
+        # forward slice y[b][ss] needs every input channel of image b
+        y_ref, xs_b = fdc.full_fdc_forward(x64[b:b + 1], w64[ss], crop)
+        assert_parity(to_np(y[b, ss]), y_ref[0], f"y[{b}]")
+        assert_parity(to_np(saved[b, cs]), xs_b[0, cs], f"saved[{b}]")
+        # dL/dx slice gx[b][cs] needs every output channel of image b
+        gx_ref, _ = fdc.full_fdc_backward(g64[b:b + 1], xs_b[:, cs], w64[:, cs], crop)
+        assert_parity(to_np(gx[b, cs]), gx_ref[0], f"gx[{b}]")
+    # dL/dw slice gw[ss][cs] needs every image of the batch
+    xs_c = dft.rfft2(x64[:, cs])
+    _, gw_ref = fdc.full_fdc_backward(g64[:, ss], xs_c, w64[ss][:, cs], crop, want_gx=False)
+    assert_parity(to_np(gw[ss][:, cs]), gw_ref, "gw")
+    assert torch.isfinite(y).all() and torch.isfinite(gx).all() and torch.isfinite(gw).all()
