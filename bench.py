@@ -11,6 +11,10 @@ all layers, activation gradients of layers 2..5; the gradient of the input
 image is not part of a training step).  Inputs are resident in HBM before the
 timed region starts.
 
+With --workload full_fdc_<P>_c<C> it times one Full FDC layer instead (16 images of
+P x P, C -> C channels, 3 x 3 weights, crop): forward, then dL/dx and dL/dw; the
+roofline of its dominant kernel is then taken against the fp32 matrix-core peak.
+
 Prints ONE JSON line (see --help).  The step is captured once as a HIP graph
 and the timed region replays it K times (--eager times plain launches).  Besides
 the step time it reports, for the kernel that takes most of the step, its
@@ -32,6 +36,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published peak
+MFMA_F32_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix-core peak
 METRIC = "images/sec fwd+bwd of FDC/FDP stack at 1024² fp32; % peak HBM GB/s (and MFMA %)"
 C64, F32 = 8, 4
 
@@ -77,6 +82,42 @@ def step_api_bytes(wl, input_grad=False):
         if i > 0 or input_grad:
             total += F32 * B * C * N * N
     return total
+
+
+def full_step_launches(wl):
+    """(kernel name, algorithmic amount, unit) of every launch of one Full FDC step
+    (forward, dL/dw, dL/dx).  Matrix-core kernels count flops (8 per complex
+    multiply-add of the per-bin contraction), the others HBM bytes."""
+    B, Ci, Co, P, n = wl.batch, wl.cin, wl.cout, wl.size, wl.n
+    NB = P * (P // 2 + 1)
+    O = P - n + 1
+    wbytes = F32 * Co * Ci * n * n
+    flops = 8 * B * Ci * Co * NB
+    return [
+        (f"row_r2c_{P}", F32 * B * Ci * P * P + C64 * B * Ci * NB, "B"),
+        (f"col_fft_fwd_{P}", 2 * C64 * B * Ci * NB, "B"),
+        ("full_weights", 2 * wbytes, "B"),
+        ("full_contract_fwd", flops, "flop"),
+        (f"col_fft_inv_{P}", 2 * C64 * B * Co * NB, "B"),
+        (f"row_c2r_{P}", C64 * B * Co * NB + F32 * B * Co * O * O, "B"),
+        (f"row_r2c_{P}", F32 * B * Co * O * O + C64 * B * Co * NB, "B"),
+        (f"col_fft_fwd_{P}", 2 * C64 * B * Co * NB, "B"),
+        ("full_gw", flops, "flop"),
+        ("full_gw_reduce", wbytes, "B"),  # dL/dw written once; its per-chunk partial sums are scratch
+        ("full_weights", 2 * wbytes, "B"),
+        ("full_contract_gx", flops, "flop"),
+        (f"col_fft_inv_{P}", 2 * C64 * B * Ci * NB, "B"),
+        (f"row_c2r_{P}", C64 * B * Ci * NB + F32 * B * Ci * P * P, "B"),
+    ]
+
+
+def full_api_bytes(wl):
+    """x, w, y forward; gy, saved rfft2(x), w, gx, gw backward."""
+    B, Ci, Co, P, n = wl.batch, wl.cin, wl.cout, wl.size, wl.n
+    O = P - n + 1
+    w = F32 * Co * Ci * n * n
+    spec = C64 * B * Ci * P * (P // 2 + 1)
+    return (F32 * B * Ci * P * P + w + F32 * B * Co * O * O) + (F32 * B * Co * O * O + spec + 2 * w + F32 * B * Ci * P * P)
 
 
 def kernel_source_digest():
@@ -138,15 +179,117 @@ def cpu_baseline(wl, data, min_seconds=10.0, max_reps=3):
 # main
 # ----------------------------------------------------------------------------
 
+class CicStackRun:
+    """The CIC + FDP stack step on preallocated buffers."""
+
+    def __init__(self, wl, args, dev):
+        import torch
+
+        from paper_2106_12736_amd import inputs, layers
+        self.wl = wl
+        self.data = inputs.make_cic_stack(wl)
+        self.x = torch.from_numpy(self.data.x).to(dev)
+        self.Ks = [torch.from_numpy(k).to(dev) for k in self.data.kernels]
+        self.g = torch.from_numpy(self.data.grad).to(dev)
+        self.stack = layers.CicStack(wl.batch, wl.sizes, wl.channels, device=dev)
+        self.gin = (torch.empty((wl.batch, wl.channels[0], wl.sizes[0], wl.sizes[0]), dtype=torch.float32,
+                                device=dev) if args.input_grad else None)
+        self.input_grad = args.input_grad
+        self.launches = [(name, nbytes, "B") for name, nbytes in step_launches(wl, args.input_grad)]
+        self.api_bytes = step_api_bytes(wl, args.input_grad)
+
+    def step(self):
+        self.stack.forward(self.x, self.Ks)
+        self.stack.backward(self.g, self.Ks, input_grad=self.gin)
+
+    def outputs(self):
+        return [self.stack.acts[-1]] + list(self.stack.gks)
+
+    def config(self):
+        wl = self.wl
+        return {"workload": wl.name, "batch": wl.batch, "sizes": list(wl.sizes), "channels": list(wl.channels),
+                "input_grad": bool(self.input_grad)}
+
+    def cpu_baseline(self):
+        return cpu_baseline(self.wl, self.data)
+
+
+class FullFdcRun:
+    """One Full FDC layer step (forward, dL/dx, dL/dw) on preallocated buffers."""
+
+    def __init__(self, wl, args, dev):
+        import torch
+
+        from paper_2106_12736_amd import inputs, layers
+        self.wl = wl
+        self.data = inputs.make_full_fdc(wl)
+        self.x = torch.from_numpy(self.data.x).to(dev)
+        self.w = torch.from_numpy(self.data.w).to(dev)
+        self.g = torch.from_numpy(self.data.grad).to(dev)
+        self.layer = layers.FullLayer(wl.batch, wl.cin, wl.cout, wl.size, kernel_n=wl.n, artifact="crop",
+                                      device=dev)
+        self.saved = self.layer.new_saved()
+        self.y = self.layer.new_output()
+        self.gx = torch.empty_like(self.x)
+        self.gw = torch.empty_like(self.w)
+        self.launches = full_step_launches(wl)
+        self.api_bytes = full_api_bytes(wl)
+
+    def step(self):
+        self.layer.forward(self.x, self.w, y=self.y, saved=self.saved)
+        self.layer.backward(self.g, self.saved, self.w, gx=self.gx, gw=self.gw)
+
+    def outputs(self):
+        return [self.y, self.gx, self.gw]
+
+    def config(self):
+        wl = self.wl
+        return {"workload": wl.name, "batch": wl.batch, "size": wl.size, "cin": wl.cin, "cout": wl.cout,
+                "kernel": wl.n, "artifact": "crop"}
+
+    def cpu_baseline(self, min_seconds=10.0):
+        """The oracle on one image and a slice of the output channels (the layer's work
+        grows linearly with the output channels), scaled to the whole layer."""
+        import numpy as np
+        from threadpoolctl import threadpool_info
+
+        from oracle import fdc
+
+        wl = self.wl
+        cs = max(1, wl.cout // 32)
+        x = self.data.x[:1].astype(np.float64)
+        w = self.data.w[:cs].astype(np.float64)
+        g = self.data.grad[:1, :cs].astype(np.float64)
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            _, xs = fdc.full_fdc_forward(x, w, fdc.ARTIFACT_CROP)
+            fdc.full_fdc_backward(g, xs, w, fdc.ARTIFACT_CROP)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= min_seconds or reps >= 3:
+                break
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        return {
+            "value": reps * (cs / wl.cout) / el,
+            "unit": "images/s",
+            "cores": threads,
+            "kind": "oracle",
+            "sample": f"{reps} step(s) of one image with {cs} of {wl.cout} output channels (fwd, dL/dx, dL/dw, "
+                      f"float64) in {el:.1f} s, scaled by {wl.cout // cs} to all output channels; "
+                      f"{os.cpu_count()} host CPUs visible",
+        }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="cic_stack_1024",
-                    help="CIC stack workload (default: the 1024 x 1024 headline stack)")
+                    help="CIC stack (cic_stack_1024 [default], cic_stack_512, ...) or Full FDC layer "
+                         "(full_fdc_512_c256, ...) workload")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
-    ap.add_argument("--input-grad", action="store_true", help="also compute the input-image gradient")
+    ap.add_argument("--input-grad", action="store_true", help="CIC stack: also compute the input-image gradient")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of HIP graph replays")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the timed region, run one plain streaming copy kernel (dst = src * 1) over "
@@ -161,34 +304,28 @@ def main():
 
     import torch
 
-    from paper_2106_12736_amd import _lib, inputs, layers
+    from paper_2106_12736_amd import _lib, inputs
 
-    wl = {w.name: w for w in inputs.CIC_WORKLOADS}[args.workload]
+    workloads = {w.name: w for w in inputs.CIC_WORKLOADS + inputs.FULL_FDC_WORKLOADS}
+    if args.workload not in workloads:
+        sys.exit(f"unknown workload {args.workload}; one of {sorted(workloads)}")
+    wl = workloads[args.workload]
     if not torch.cuda.is_available():
         sys.exit("bench.py needs a GPU")
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     _lib.lib()  # fails loudly if libfdc.so is not built
 
-    data = inputs.make_cic_stack(wl)
-    x = torch.from_numpy(data.x).to(dev)
-    Ks = [torch.from_numpy(k).to(dev) for k in data.kernels]
-    g = torch.from_numpy(data.grad).to(dev)
-    stack = layers.CicStack(wl.batch, wl.sizes, wl.channels, device=dev)
-    gin = (torch.empty((wl.batch, wl.channels[0], wl.sizes[0], wl.sizes[0]), dtype=torch.float32, device=dev)
-           if args.input_grad else None)
+    run = (FullFdcRun if isinstance(wl, inputs.FullFdcLayer) else CicStackRun)(wl, args, dev)
+    step = run.step
     stream = torch.cuda.current_stream()
-
-    def step():
-        stack.forward(x, Ks)
-        stack.backward(g, Ks, input_grad=gin)
 
     for _ in range(max(args.warmup, 1)):
         step()
     torch.cuda.synchronize()
 
     # one instrumented step: per-kernel durations, to find the kernel that dominates
-    launches = step_launches(wl, args.input_grad)
+    launches = run.launches
     _lib.call("fdc_kernel_timing_enable", len(launches) + 8, None)
     step()
     torch.cuda.synchronize()
@@ -197,14 +334,14 @@ def main():
     _lib.call("fdc_kernel_timing_disable")
     recs = [ln.rsplit(" ", 1) for ln in buf.value.decode().strip().splitlines()]
     names = [r[0] for r in recs]
-    if names != [n for n, _ in launches]:
-        sys.exit(f"launch sequence differs from the byte model:\n{names}\n{[n for n, _ in launches]}")
+    if names != [n for n, _, _ in launches]:
+        sys.exit(f"launch sequence differs from the work model:\n{names}\n{[n for n, _, _ in launches]}")
     per_name = {}
-    for (name, nbytes), (_, ms) in zip(launches, recs):
-        t, b, n = per_name.get(name, (0.0, 0, 0))
-        per_name[name] = (t + float(ms), b + nbytes, n + 1)
+    for (name, amount, unit), (_, ms) in zip(launches, recs):
+        t, a, n, _ = per_name.get(name, (0.0, 0, 0, unit))
+        per_name[name] = (t + float(ms), a + amount, n + 1, unit)
     dominant = max(per_name, key=lambda k: per_name[k][0])
-    dom_bytes_per_step, dom_launches_per_step = per_name[dominant][1], per_name[dominant][2]
+    dom_amount_per_step, dom_launches_per_step, dom_unit = per_name[dominant][1:]
 
     t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
@@ -214,24 +351,24 @@ def main():
     if not args.eager:
         step()
         torch.cuda.synchronize()
-        ref = [stack.acts[-1].clone()] + [gk.clone() for gk in stack.gks]
+        ref = [t.clone() for t in run.outputs()]
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
             step()
         graph.replay()
         torch.cuda.synchronize()
-        got = [stack.acts[-1]] + list(stack.gks)
-        if not all(torch.equal(a, b) for a, b in zip(ref, got)):
+        if not all(torch.equal(a, b) for a, b in zip(ref, run.outputs())):
             sys.exit("graph replay does not reproduce the eager step")
+        del ref
         for _ in range(max(args.warmup, 1)):
             graph.replay()
 
-    def timed(run):
+    def timed(fn):
         torch.cuda.synchronize()
         w0 = time.perf_counter()
         t_start.record(stream)
         for _ in range(args.steps):
-            run()
+            fn()
         t_end.record(stream)
         torch.cuda.synchronize()
         return t_start.elapsed_time(t_end) / args.steps, (time.perf_counter() - w0) * 1e3 / args.steps
@@ -249,10 +386,22 @@ def main():
     dom_ms = [float(ln.rsplit(" ", 1)[1]) for ln in buf.value.decode().strip().splitlines()]
 
     dom_avg_ms = sum(dom_ms) / len(dom_ms)
-    dom_bytes_per_launch = dom_bytes_per_step / dom_launches_per_step
-    achieved = dom_bytes_per_launch / (dom_avg_ms * 1e-3) / 1e9
-    api_bytes = step_api_bytes(wl, args.input_grad)
+    per_launch = dom_amount_per_step / dom_launches_per_step
+    if dom_unit == "flop":
+        achieved = per_launch / (dom_avg_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "kernel": dominant, "achieved": achieved, "peak": MFMA_F32_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": achieved / MFMA_F32_PEAK_TFLOPS, "traffic": None,
+                "flops_per_launch": per_launch}
+    else:
+        achieved = per_launch / (dom_avg_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBPS, "traffic": measured_traffic(dominant, wl.name),
+                "bytes_per_launch": per_launch}
+    roof["avg_launch_ms"] = dom_avg_ms
+    roof["share_of_step"] = sum(dom_ms) / args.steps / eager_ms_per_step
 
+    cfg = run.config()
+    cfg.update({"launches_per_step": len(launches), "hip_graph": graph is not None})
     out = {
         "metric": METRIC,
         "value": wl.batch / (ms_per_step * 1e-3),
@@ -266,29 +415,10 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {
-            "workload": wl.name,
-            "batch": wl.batch,
-            "sizes": list(wl.sizes),
-            "channels": list(wl.channels),
-            "input_grad": bool(args.input_grad),
-            "launches_per_step": len(launches),
-            "hip_graph": graph is not None,
-        },
-        "roofline": {
-            "bound": "hbm",
-            "kernel": dominant,
-            "achieved": achieved,
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": measured_traffic(dominant, wl.name),
-            "bytes_per_launch": dom_bytes_per_launch,
-            "avg_launch_ms": dom_avg_ms,
-            "share_of_step": sum(dom_ms) / args.steps / eager_ms_per_step,
-        },
-        "step_api_bytes": api_bytes,
-        "step_effective_gbps": api_bytes / (ms_per_step * 1e-3) / 1e9,
+        "config": cfg,
+        "roofline": roof,
+        "step_api_bytes": run.api_bytes,
+        "step_effective_gbps": run.api_bytes / (ms_per_step * 1e-3) / 1e9,
         "step_kernel_ms": {k: round(v[0], 5) for k, v in sorted(per_name.items(), key=lambda kv: -kv[1][0])},
         "wall_ms_per_step": wall_ms,
         "eager_ms_per_step": eager_ms_per_step,
@@ -302,7 +432,7 @@ def main():
         torch.cuda.synchronize()
         out["copy_calibration_bytes"] = 2 * 4 * n
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, data)
+        out["cpu_baseline"] = run.cpu_baseline()
     print(json.dumps(out), flush=True)
 
 

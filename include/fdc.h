@@ -146,8 +146,8 @@ fdc_status fdc_cic_layer_plan_create(fdc_layer_plan **plan, int B, int C, int S,
 /* Full FDC layer (Algorithm 2 with the per-bin sum over input channels of Eq. 2):
  * x [B][Cin][P][P], weights w [Cout][Cin][n][n] spatial (padded to P x P at the
  * top-left and transformed on every call, section 2.4.1.2), y [B][Cout][O][O] with
- * O = P - n + 1 for CROP and P for NONE/ROLL.  P even and in the supported FFT
- * set, 1 <= n <= 5 (FDC_EUNSUPPORTED otherwise).  No FDP: the layer keeps its
+ * O = P - n + 1 for CROP and P for NONE/ROLL.  P a multiple of 8 in the supported
+ * FFT set, 1 <= n <= 5 (FDC_EUNSUPPORTED otherwise).  No FDP: the layer keeps its
  * spatial size.  The plan owns a P-entry device table of twiddle factors, so it
  * is created on (and must be used with) the device current at creation;
  * FDC_EHIP if that allocation fails. */
@@ -176,10 +176,20 @@ fdc_status fdc_cic_layer_backward(const fdc_layer_plan *plan, const float *gy, c
                                   const fdc_c64 *K, float *gx, fdc_c64 *gK,
                                   void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* Plane strides, in complex elements, of the Full FDC spectrum blocks (the `saved`
+ * buffer below): each P x P/2 main plane is followed by 64 unused elements and each
+ * P-element Nyquist-column plane by 8, so that one frequency bin of successive planes
+ * does not map onto one memory channel. */
+#define FDC_FULL_MAIN_PLANE(P) ((int64_t)(P) * ((P) / 2) + 64)
+#define FDC_FULL_SIDE_PLANE(P) ((int64_t)(P) + 8)
+
 /* Full FDC forward: y = artifact(irfft2(sum_c rfft2(x[b][c]) o K[s][c])) with
  * K[s][c] = rfft2(pad(w[s][c])).  K is generated per bin inside the contraction
- * and never stored.  `saved` (may be NULL) receives rfft2(x) as a plain complex
- * [B][Cin][P][P/2+1] array; the backward pass reads it for dL/dw. */
+ * and never stored.  `saved` (may be NULL) receives rfft2(x), complex: for plane
+ * i = b * Cin + c, columns 0..P/2-1 as a row-major P x P/2 array at element
+ * i * FDC_FULL_MAIN_PLANE(P), then column P/2 (P elements) at element
+ * B * Cin * FDC_FULL_MAIN_PLANE(P) + i * FDC_FULL_SIDE_PLANE(P); the backward pass
+ * reads it for dL/dw. */
 fdc_status fdc_full_forward(const fdc_layer_plan *plan, const float *x, const float *w, float *y,
                             void *saved, void *ws, size_t ws_bytes, hipStream_t stream);
 /* Full FDC backward: gy [B][Cout][O][O] -> gx [B][Cin][P][P] (NULL: skipped) and

@@ -432,18 +432,18 @@ struct FullWs {  // byte offsets inside the forward / backward workspaces
   size_t g, gx, wg, part;  // backward: G, dL/dX spectrum, rearranged weights, dL/dw partials
 };
 FullWs full_layout(int B, int Cin, int Cout, int P, int kn, size_t *fwd, size_t *bwd) {
-  const size_t spec = (size_t)P * (P / 2 + 1) * sizeof(fdc_c64);
-  const size_t wsz = (size_t)Cout * Cin * kn * kn * sizeof(float);
+  const size_t xs = (size_t)fdc::full_spec_elems((long long)B * Cin, P) * sizeof(fdc_c64);
+  const size_t ys = (size_t)fdc::full_spec_elems((long long)B * Cout, P) * sizeof(fdc_c64);
   FullWs w{};
   w.x = 0;
-  w.y = align256(w.x + (size_t)B * Cin * spec);
-  w.wf = align256(w.y + (size_t)B * Cout * spec);
-  *fwd = align256(w.wf + wsz);
+  w.y = align256(w.x + xs);
+  w.wf = align256(w.y + ys);
+  *fwd = align256(w.wf + fdc::full_weight_floats(Cin, Cout, kn) * sizeof(float));
   w.g = 0;
-  w.gx = align256(w.g + (size_t)B * Cout * spec);
-  w.wg = align256(w.gx + (size_t)B * Cin * spec);
-  w.part = align256(w.wg + wsz);
-  *bwd = align256(w.part + (size_t)fdc::full_gw_chunks(B, Cout, Cin, P) * wsz);
+  w.gx = align256(w.g + ys);
+  w.wg = align256(w.gx + xs);
+  w.part = align256(w.wg + fdc::full_weight_floats(Cout, Cin, kn) * sizeof(float));
+  *bwd = align256(w.part + (size_t)fdc::full_gw_chunks(B, Cout, Cin, P, kn) * Cout * Cin * kn * kn * sizeof(float));
   return w;
 }
 }  // namespace
@@ -457,7 +457,8 @@ fdc_status fdc_full_layer_plan_create(fdc_layer_plan **plan, int B, int Cin, int
   if (!even_pos(P)) return fail(FDC_EINVAL, "P must be positive and even (got %d)", P);
   if (artifact < FDC_ARTIFACT_NONE || artifact > FDC_ARTIFACT_ROLL) return fail(FDC_EINVAL, "bad artifact mode");
   if (kernel_n < 1 || kernel_n > P) return fail(FDC_EINVAL, "kernel_n must be in [1, P] (got %d)", kernel_n);
-  if (!fdc::size_supported(P)) return fail(FDC_EUNSUPPORTED, "image size %d not supported", P);
+  if (!fdc::size_supported(P) || P % 8 != 0)
+    return fail(FDC_EUNSUPPORTED, "image size %d not supported (Full FDC needs a multiple of 8 in the FFT set)", P);
   if (!fdc::full_kernel_size_supported(kernel_n))
     return fail(FDC_EUNSUPPORTED, "Full FDC supports kernel_n 1..5 (got %d)", kernel_n);
   auto *p = new (std::nothrow) fdc_layer_plan{};
@@ -469,7 +470,7 @@ fdc_status fdc_full_layer_plan_create(fdc_layer_plan **plan, int B, int Cin, int
   p->kn = kernel_n;
   p->out = artifact == FDC_ARTIFACT_CROP ? P - kernel_n + 1 : P;
   full_layout(B, Cin, Cout, P, kernel_n, &p->fwd_ws, &p->bwd_ws);
-  p->saved = (size_t)B * Cin * P * (P / 2 + 1) * sizeof(fdc_c64);
+  p->saved = (size_t)fdc::full_spec_elems((long long)B * Cin, P) * sizeof(fdc_c64);
   std::vector<float2> tw(P);
   for (int j = 0; j < P; ++j) {
     const double ang = -2.0 * 3.14159265358979323846 * (double)j / (double)P;
@@ -500,24 +501,22 @@ fdc_status fdc_full_forward(const fdc_layer_plan *p, const float *x, const float
   auto *X = saved != nullptr ? static_cast<float2 *>(saved) : reinterpret_cast<float2 *>(base + L.x);
   auto *Y = reinterpret_cast<float2 *>(base + L.y);
   auto *wf = reinterpret_cast<float *>(base + L.wf);
-  const long long spec = (long long)P * Pf;
+  const long long Xp = (long long)B * Cin, Yp = (long long)B * Cout;
+  const fdc::SpecLayout XL = fdc::full_spec_layout(X, Xp, P), YL = fdc::full_spec_layout(Y, Yp, P);
   ImgView id{0, 0, P, P};
-  if (fdc_status st = check_hip(fdc::launch_row_r2c(P, x, fdc::plain_layout(X, P, Pf), (long long)B * Cin, P, id,
-                                                    (long long)P * P, Pf, 1.f, 1.f, s), "full forward rows"))
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(P, x, XL, Xp, P, id, (long long)P * P, Pf, 1.f, 1.f, s),
+                                "full forward rows"))
     return st;
-  if (fdc_status st = check_hip(fdc::launch_col_fft(P, -1, X, X, (long long)B * Cin, Pf, Pf, spec, spec, s),
-                                "full forward columns"))
+  if (fdc_status st = check_hip(fdc::launch_col_fft_split(P, -1, XL, XL, Xp, s), "full forward columns")) return st;
+  if (fdc_status st = check_hip(fdc::launch_full_weights(w, wf, false, Cout, Cin, p->kn, s), "full weights"))
     return st;
-  if (fdc_status st = check_hip(fdc::launch_full_weights(w, wf, nullptr, Cout, Cin, p->kn, s), "full weights"))
-    return st;
-  if (fdc_status st = check_hip(fdc::launch_full_contract(false, p->kn, X, wf, p->tw, Y, B, Cin, Cout, P, s),
+  if (fdc_status st = check_hip(fdc::launch_full_contract(false, p->kn, XL, wf, p->tw, YL, B, Cin, Cout, P, s),
                                 "full forward contraction"))
     return st;
-  if (fdc_status st = check_hip(fdc::launch_col_fft(P, +1, Y, Y, (long long)B * Cout, Pf, Pf, spec, spec, s),
-                                "full forward inverse columns"))
+  if (fdc_status st = check_hip(fdc::launch_col_fft_split(P, +1, YL, YL, Yp, s), "full forward inverse columns"))
     return st;
-  return check_hip(fdc::launch_row_c2r(P, fdc::plain_layout(Y, P, Pf), y, (long long)B * Cout, P, Pf,
-                                       1.f / ((float)P * (float)P), 1.f, artifact_view(p), (long long)p->out * p->out, s),
+  return check_hip(fdc::launch_row_c2r(P, YL, y, Yp, P, Pf, 1.f / ((float)P * (float)P), 1.f, artifact_view(p),
+                                       (long long)p->out * p->out, s),
                    "full forward inverse rows");
 }
 
@@ -537,34 +536,31 @@ fdc_status fdc_full_backward(const fdc_layer_plan *p, const float *gy, const voi
   auto *gX = reinterpret_cast<float2 *>(base + L.gx);
   auto *wg = reinterpret_cast<float *>(base + L.wg);
   auto *part = reinterpret_cast<float *>(base + L.part);
-  const long long spec = (long long)P * Pf;
+  const long long Xp = (long long)B * Cin, Gp = (long long)B * Cout;
+  const fdc::SpecLayout GL = fdc::full_spec_layout(G, Gp, P), gXL = fdc::full_spec_layout(gX, Xp, P);
   // G = adjoint of the inverse transform and the artifact step: (c_l / P^2) rfft2 of gy placed in P x P
-  if (fdc_status st = check_hip(fdc::launch_row_r2c(P, gy, fdc::plain_layout(G, P, Pf), (long long)B * Cout, P,
-                                                    artifact_view(p), (long long)p->out * p->out, Pf,
-                                                    1.f / ((float)P * (float)P), 2.f, s),
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(P, gy, GL, Gp, P, artifact_view(p), (long long)p->out * p->out,
+                                                    Pf, 1.f / ((float)P * (float)P), 2.f, s),
                                 "full backward rows"))
     return st;
-  if (fdc_status st = check_hip(fdc::launch_col_fft(P, -1, G, G, (long long)B * Cout, Pf, Pf, spec, spec, s),
-                                "full backward columns"))
-    return st;
+  if (fdc_status st = check_hip(fdc::launch_col_fft_split(P, -1, GL, GL, Gp, s), "full backward columns")) return st;
   if (gw) {
-    if (fdc_status st = check_hip(fdc::launch_full_gw(p->kn, G, static_cast<const float2 *>(saved), p->tw, part, gw, B,
-                                                      Cout, Cin, P, s), "full backward dw"))
+    const fdc::SpecLayout XL = fdc::full_spec_layout(static_cast<const float2 *>(saved), Xp, P);
+    if (fdc_status st = check_hip(fdc::launch_full_gw(p->kn, GL, XL, p->tw, part, gw, B, Cout, Cin, P, s),
+                                  "full backward dw"))
       return st;
   }
   if (gx) {
-    if (fdc_status st = check_hip(fdc::launch_full_weights(w, nullptr, wg, Cout, Cin, p->kn, s), "full weights"))
+    if (fdc_status st = check_hip(fdc::launch_full_weights(w, wg, true, Cout, Cin, p->kn, s), "full weights"))
       return st;
-    if (fdc_status st = check_hip(fdc::launch_full_contract(true, p->kn, G, wg, p->tw, gX, B, Cout, Cin, P, s),
+    if (fdc_status st = check_hip(fdc::launch_full_contract(true, p->kn, GL, wg, p->tw, gXL, B, Cout, Cin, P, s),
                                   "full backward dx contraction"))
       return st;
     // rfft2 adjoint: P^2 irfft2(gX / c_l)
-    if (fdc_status st = check_hip(fdc::launch_col_fft(P, +1, gX, gX, (long long)B * Cin, Pf, Pf, spec, spec, s),
-                                  "full backward dx columns"))
+    if (fdc_status st = check_hip(fdc::launch_col_fft_split(P, +1, gXL, gXL, Xp, s), "full backward dx columns"))
       return st;
     ImgView id{0, 0, P, P};
-    return check_hip(fdc::launch_row_c2r(P, fdc::plain_layout(gX, P, Pf), gx, (long long)B * Cin, P, Pf, 1.f, 0.5f, id,
-                                         (long long)P * P, s),
+    return check_hip(fdc::launch_row_c2r(P, gXL, gx, Xp, P, Pf, 1.f, 0.5f, id, (long long)P * P, s),
                      "full backward dx rows");
   }
   return FDC_OK;

@@ -14,10 +14,16 @@
 // n x n support, dL/dw[s][c][a][b] = Re sum_bins gK[s][c] conj(W^(k a) W^(l b)),
 // accumulated per bin chunk and reduced in a fixed order.
 //
+// Spectra use the split layout of a P x (P/2+1) half spectrum: a main block of
+// P x P/2 planes (columns 0..P/2-1) followed by a side block of P-element planes (the
+// Nyquist column l = P/2), so that runs of 4 bins are 32-byte aligned; plane strides
+// are padded (full_spec_layout).
+//
 // Complex products use four real v_mfma_f32_16x16x4f32 per 4-deep K step:
 //   re += Ar Br - Ai Bi,  im += Ar Bi + Ai Br.
 // Lane layout of v_mfma_f32_16x16x4f32 (A 16x4, B 4x16, D 16x16): lane l holds
 // A[l % 16][l / 16], B[l / 16][l % 16] and D[4 (l / 16) + j][l % 16] in register j.
+#include "device.h"
 #include "internal.h"
 
 #include <hip/hip_runtime.h>
@@ -32,236 +38,324 @@ __device__ __forceinline__ v4f mfma4(float a, float b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
-// Phases of bin `bin` (flat index k * Pf + l): u[a] = W^(k a), v[b] = W^(l b), a, b < NK,
-// from the twiddle table tw[j] = W^j, j < P (exponents reduced mod P exactly).
+// Taps of an n x n kernel, padded to a multiple of 4 for whole 16-byte loads.
 template <int NK>
-__device__ __forceinline__ void bin_phases(const float2 *tw, int P, int Pf, int bin, float2 (&u)[NK],
-                                           float2 (&v)[NK]) {
-  const int k = bin / Pf, l = bin - (bin / Pf) * Pf;
-#pragma unroll
-  for (int a = 0; a < NK; ++a) {
-    u[a] = tw[(k * a) % P];
-    v[a] = tw[(l * a) % P];
-  }
-}
-
-// K = sum_a u[a] sum_b w[a][b] v[b] for one (s, c) pair.
-template <int NK>
-__device__ __forceinline__ float2 kernel_value(const float (&w)[NK * NK], const float2 (&u)[NK],
-                                               const float2 (&v)[NK]) {
-  float2 acc = make_float2(0.f, 0.f);
-#pragma unroll
-  for (int a = 0; a < NK; ++a) {
-    float rx = 0.f, ry = 0.f;
-#pragma unroll
-    for (int b = 0; b < NK; ++b) {
-      rx += w[a * NK + b] * v[b].x;
-      ry += w[a * NK + b] * v[b].y;
-    }
-    acc.x += u[a].x * rx - u[a].y * ry;
-    acc.y += u[a].x * ry + u[a].y * rx;
-  }
-  return acc;
+__host__ __device__ constexpr int tap_pad() {
+  return (NK * NK + 3) & ~3;
 }
 
 // ---------------------------------------------------------------------------
-// Forward (GX = false) and dL/dX (GX = true) contraction.
-//   in  [B][KD][NB] complex: X (KD = Cin) or G (KD = Cout)
-//   wt  weights rearranged as [KD][NK*NK][ND] (forward: [c][tap][s]; dL/dX: [s][tap][c])
-//   out [B][ND][NB] complex: Y (ND = Cout) or gX (ND = Cin)
-// A workgroup (4 waves) computes 16 batch rows x 4 consecutive bins x 256 outputs; wave
-// w owns outputs [64 w, 64 w + 64) as four 16-wide tiles.  The K dimension is staged
-// in LDS 4 at a time: the 16 x 4 x 4 input values and the 4 x NK*NK x 256 weights.
+// Forward (GX = false) and dL/dX (GX = true) contraction on split-layout spectra.
+//   in  [B][KD] spectra: X (KD = Cin) or G (KD = Cout)
+//   wt  weights rearranged as [KDp][NDp][TP], zero-padded (forward: [c][s][tap];
+//       dL/dX: [s][c][tap]); KDp = KD rounded up to 4, NDp = ND rounded up to 64
+//   out [B][ND] spectra: Y (ND = Cout) or gX (ND = Cin)
+// The bins of a spectrum are cut into runs of 4: along a row of the main block
+// (same k, four consecutive l) or down the Nyquist column (four consecutive k,
+// l = P/2).  A wave owns one run, 16 batch rows and 64 outputs (four 16 x 16 D
+// tiles per bin); a workgroup is 4 waves on 4 consecutive runs and the same
+// outputs, so their weight loads coincide in L1.  Inside a run the kernel
+// spectrum factorises: for a row run K(k, l) = sum_b W^(l b) C_b with
+// C_b = sum_a w_ab W^(k a) shared by the 4 bins; for a Nyquist run W^(l b) = (-1)^b
+// and K(k, P/2) = sum_a W^(k a) R_a with R_a = sum_b (-1)^b w_ab.
+// Every load is unconditional: batch rows and channels past the end are clamped
+// to the last valid ones (their weights are zero, their outputs are not stored).
 // ---------------------------------------------------------------------------
-constexpr int kFcBins = 4;     // bins per workgroup
-constexpr int kFcOut = 256;    // outputs per workgroup
-constexpr int kFcThreads = 256;
+constexpr int kCtOut = 64;  // outputs per workgroup
 
-template <int NK, bool GX>
-__global__ __launch_bounds__(kFcThreads) void k_full_contract(const float2 *__restrict__ in,
-                                                              const float *__restrict__ wt,
-                                                              const float2 *__restrict__ twg,
-                                                              float2 *__restrict__ out, int B, int KD, int ND,
-                                                              int P, int Pf, int NB) {
-  constexpr int T = NK * NK;
-  extern __shared__ float smem[];
-  float2 *tw = reinterpret_cast<float2 *>(smem);            // P
-  float2 *sA = tw + ((P + 31) & ~31);                       // [16 b][4 kk][4 bins]
-  float *sW = reinterpret_cast<float *>(sA + 16 * 4 * kFcBins);  // [4 kk][T][256 n]
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int nbg = (NB + kFcBins - 1) / kFcBins;
-  const int bg = blockIdx.x % nbg;
-  const int n0 = (blockIdx.x / nbg) * kFcOut;
-  const int b0 = blockIdx.y * 16;
-  const int bin0 = bg * kFcBins;
-  for (int i = tid; i < P; i += kFcThreads) tw[i] = twg[i];
-  __syncthreads();
-
-  // phases of this workgroup's bins (the same for every lane)
-  float2 u[kFcBins][NK], v[kFcBins][NK];
+template <int NK, bool GX, bool SIDE>
+__device__ __forceinline__ void contract_run(const float2 *__restrict__ in, const float *__restrict__ wt,
+                                             float2 *__restrict__ out, const float2 (&zs)[NK],
+                                             const float2 (&zq)[4][NK], long long pst, long long opst, int B,
+                                             int KD, int KDp, int ND, int NDp, int b0, int n0) {
+  constexpr int TP = tap_pad<NK>();
+  const int lane = threadIdx.x & 63, mrow = lane & 15, kk = lane >> 4;
+  v4f accr[4][4], acci[4][4];  // [bin q][tile t]
 #pragma unroll
-  for (int q = 0; q < kFcBins; ++q) {
-    const int bin = bin0 + q < NB ? bin0 + q : NB - 1;
-    bin_phases<NK>(tw, P, Pf, bin, u[q], v[q]);
-  }
-
-  v4f accr[kFcBins][4], acci[kFcBins][4];
+  for (int q = 0; q < 4; ++q)
 #pragma unroll
-  for (int q = 0; q < kFcBins; ++q)
+    for (int t = 0; t < 4; ++t) accr[q][t] = acci[q][t] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  const int ba = min(b0 + mrow, B - 1);  // A operand row (batch)
+  const float2 *arow = in + (long long)ba * KD * pst;
+  // operands of step (k0, t) are loaded one step ahead: the inputs one k-step ahead,
+  // the weights of the next 16-output tile while the current one runs
+  auto load_a = [&](int k0, float4 (&a)[2]) {
+    const float4 *a4 = reinterpret_cast<const float4 *>(arow + (long long)min(k0 + kk, KD - 1) * pst);
+    a[0] = a4[0], a[1] = a4[1];
+  };
+  auto load_w = [&](int k0, int t, float4 (&w)[TP / 4]) {
+    const float4 *w4 = reinterpret_cast<const float4 *>(wt + ((long long)(k0 + kk) * NDp + n0 + 16 * t + mrow) * TP);
+#pragma unroll
+    for (int i = 0; i < TP / 4; ++i) w[i] = w4[i];
+  };
+  float4 an[2], wn[TP / 4];
+  load_a(0, an);
+  load_w(0, 0, wn);
+  for (int k0 = 0; k0 < KDp; k0 += 4) {
+    const float4 lo = an[0], hi = an[1];
+    if (k0 + 4 < KDp) load_a(k0 + 4, an);
+    const float ar[4] = {lo.x, lo.z, hi.x, hi.z}, ai[4] = {lo.y, lo.w, hi.y, hi.w};
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      accr[q][t] = v4f{0.f, 0.f, 0.f, 0.f};
-      acci[q][t] = v4f{0.f, 0.f, 0.f, 0.f};
-    }
-
-  const int mrow = lane % 16, kk = lane / 16;  // A operand: row b0 + mrow, k = k0 + kk
-  for (int k0 = 0; k0 < KD; k0 += 4) {
-    // stage the inputs: thread -> (b, kk, bin q); out-of-range entries are zero
-    {
-      const int b = tid / 16, kq = (tid / 4) % 4, q = tid % 4;
-      const int gb = b0 + b, gk = k0 + kq, gbin = bin0 + q;
-      float2 val = make_float2(0.f, 0.f);
-      if (gb < B && gk < KD && gbin < NB) val = in[((long long)gb * KD + gk) * NB + gbin];
-      sA[(b * 4 + kq) * kFcBins + q] = val;
-    }
-    // stage the weights [kq][tap][n] for n in [n0, n0 + 256)
-    for (int i = tid; i < 4 * T * kFcOut; i += kFcThreads) {
-      const int n = i % kFcOut, r = i / kFcOut;  // r = kq * T + tap
-      const int kq = r / T, tap = r - kq * T;
-      const int gk = k0 + kq, gn = n0 + n;
-      sW[i] = (gk < KD && gn < ND) ? wt[((long long)gk * T + tap) * ND + gn] : 0.f;
-    }
-    __syncthreads();
-
-    float2 a[kFcBins];
+      float w[TP];
 #pragma unroll
-    for (int q = 0; q < kFcBins; ++q) a[q] = sA[(mrow * 4 + kk) * kFcBins + q];
+      for (int i = 0; i < TP / 4; ++i)
+        w[4 * i] = wn[i].x, w[4 * i + 1] = wn[i].y, w[4 * i + 2] = wn[i].z, w[4 * i + 3] = wn[i].w;
+      if (t < 3)
+        load_w(k0, t + 1, wn);
+      else if (k0 + 4 < KDp)
+        load_w(k0 + 4, 0, wn);
+      // the run-invariant half of the kernel spectrum
+      float2 y[NK];
+      if constexpr (!SIDE) {
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int nl = wave * 64 + t * 16 + mrow;  // B operand column n0 + nl, row k0 + kk
-      float w[T];
+        for (int b = 0; b < NK; ++b) {  // C_b = w_0b + sum_{a>=1} w_ab u_a
+          float cx = w[b], cy = 0.f;
 #pragma unroll
-      for (int tap = 0; tap < T; ++tap) w[tap] = sW[(kk * T + tap) * kFcOut + nl];
+          for (int a = 1; a < NK; ++a) {
+            cx += w[a * NK + b] * zs[a].x;
+            cy += w[a * NK + b] * zs[a].y;
+          }
+          y[b] = make_float2(cx, cy);
+        }
+      } else {
 #pragma unroll
-      for (int q = 0; q < kFcBins; ++q) {
-        const float2 kv = kernel_value<NK>(w, u[q], v[q]);
-        const float br = kv.x, bi = GX ? -kv.y : kv.y;  // dL/dX uses conj(K)
-        accr[q][t] = mfma4(a[q].x, br, accr[q][t]);
-        accr[q][t] = mfma4(-a[q].y, bi, accr[q][t]);
-        acci[q][t] = mfma4(a[q].x, bi, acci[q][t]);
-        acci[q][t] = mfma4(a[q].y, br, acci[q][t]);
+        for (int a = 0; a < NK; ++a) {  // R_a = sum_b (-1)^b w_ab
+          float r = w[a * NK];
+#pragma unroll
+          for (int b = 1; b < NK; ++b) r += (b & 1) ? -w[a * NK + b] : w[a * NK + b];
+          y[a] = make_float2(r, 0.f);
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        // K = y_0 + sum_{i>=1} z_qi y_i  (z_q0 = 1)
+        float kr = y[0].x, ki = y[0].y;
+#pragma unroll
+        for (int i = 1; i < NK; ++i) {
+          if constexpr (!SIDE) {
+            kr += zq[q][i].x * y[i].x - zq[q][i].y * y[i].y;
+            ki += zq[q][i].x * y[i].y + zq[q][i].y * y[i].x;
+          } else {
+            kr += zq[q][i].x * y[i].x;
+            ki += zq[q][i].y * y[i].x;
+          }
+        }
+        // forward: re += Ar Kr - Ai Ki, im += Ar Ki + Ai Kr
+        // dL/dX (conj K): re += Ar Kr + Ai Ki, im += Ai Kr - Ar Ki
+        accr[q][t] = mfma4(ar[q], kr, accr[q][t]);
+        accr[q][t] = mfma4(GX ? ai[q] : -ai[q], ki, accr[q][t]);
+        acci[q][t] = mfma4(GX ? -ar[q] : ar[q], ki, acci[q][t]);
+        acci[q][t] = mfma4(ai[q], kr, acci[q][t]);
       }
     }
-    __syncthreads();
   }
-
-  // D[m][n]: lane holds rows 4 (lane / 16) + j, column lane % 16 of each 16 x 16 tile
+  // D[m][n]: lane holds rows 4 (lane / 16) + j, column lane % 16 of each tile
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    const int gn = n0 + wave * 64 + t * 16 + mrow;
+    const int n = n0 + 16 * t + mrow;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int gb = b0 + 4 * kk + j;
-      if (gb >= B || gn >= ND) continue;
-      float2 *o = out + ((long long)gb * ND + gn) * NB + bin0;
-#pragma unroll
-      for (int q = 0; q < kFcBins; ++q)
-        if (bin0 + q < NB) o[q] = make_float2(accr[q][t][j], acci[q][t][j]);
+      const int b = b0 + 4 * kk + j;
+      if (b >= B || n >= ND) continue;
+      float4 *o = reinterpret_cast<float4 *>(out + ((long long)b * ND + n) * opst);
+      o[0] = make_float4(accr[0][t][j], acci[0][t][j], accr[1][t][j], acci[1][t][j]);
+      o[1] = make_float4(accr[2][t][j], acci[2][t][j], accr[3][t][j], acci[3][t][j]);
     }
   }
 }
 
+template <int NK, bool GX>
+__global__ __launch_bounds__(256) void k_full_contract(SpecLayout in, const float *__restrict__ wt,
+                                                       const float2 *__restrict__ tw, SpecLayout out, int B, int KD,
+                                                       int KDp, int ND, int NDp, int P, int nwg_run, int nsb) {
+  const int H = P / 2;
+  const int nmain = P * H / 4, nrun = nmain + P / 4;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int sb = blk % nsb, rest = blk / nsb;
+  const int g = (rest % nwg_run) * 4 + wave, bt = rest / nwg_run;
+  if (g >= nrun) return;  // no barriers in this kernel
+  if (g < nmain) {
+    const int k = (4 * g) / H, l0 = 4 * g - k * H;
+    float2 u[NK], v[4][NK];
+#pragma unroll
+    for (int a = 0; a < NK; ++a) u[a] = tw[(k * a) % P];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int b = 0; b < NK; ++b) v[q][b] = tw[((l0 + q) * b) % P];
+    contract_run<NK, GX, false>(in.main + 4 * g, wt, out.main + 4 * g, u, v, in.ps, out.ps, B, KD, KDp, ND, NDp,
+                                bt * 16, sb * kCtOut);
+  } else {
+    const int k0 = 4 * (g - nmain);
+    float2 z[NK], u[4][NK];
+#pragma unroll
+    for (int b = 0; b < NK; ++b) z[b] = make_float2((b & 1) ? -1.f : 1.f, 0.f);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int a = 0; a < NK; ++a) u[q][a] = tw[((k0 + q) * a) % P];
+    contract_run<NK, GX, true>(in.side + k0, wt, out.side + k0, z, u, in.sps, out.sps, B, KD, KDp, ND, NDp, bt * 16,
+                               sb * kCtOut);
+  }
+}
+
 // ---------------------------------------------------------------------------
-// dL/dw partial sums over one chunk of bins.
-//   G [B][S][NB], X [B][C][NB] complex; part [chunk][S][C][NK*NK] float
-// gK[s][c] = sum_b G[b][s] conj(X[b][c]) on the matrix cores (M = s, N = c, K-dim = b,
-// 4 batch rows per step), then dL/dw[s][c][a][b] += Re(gK conj(W^(k a) W^(l b))).
-// A workgroup (4 waves) owns a 32 x 32 (s, c) block, each wave a 16 x 16 tile, and
-// walks the chunk's bins 8 at a time; for each group of 8 bins the batch is staged in
-// LDS 16 rows at a time, so the LDS footprint does not depend on B.
+// dL/dw partial sums over one chunk of runs (runs as in the contraction).
+//   G [B][S], X [B][C] split-layout spectra; part [chunk][S][C][NK*NK] float
+// Per bin gK[s][c] = sum_b G[b][s] conj(X[b][c]) on the matrix cores (M = s, N = c,
+// K-dim = b, 4 batch rows per step), then
+//   dL/dw[s][c][a][b] = Re sum_bins gK conj(W^(k a) W^(l b)),
+// done per run: a row run sums E_b = sum_q gK_q conj(W^(l_q b)) and adds
+// Re(E_b conj(W^(k a))); a Nyquist run sums F_a = sum_q gK_q conj(W^(k_q a)) and adds
+// (-1)^b Re(F_a).  A workgroup (4 waves) owns a 32 x 32 (s, c) block, each wave a
+// 16 x 16 tile, and walks its chunk 4 runs (16 bins, one 128-byte line of every
+// spectrum it reads; 2 runs for the larger kernels) at a time, 4 batch rows per step, loading the next step while
+// the current one runs.  Loads are unconditional: batch rows past the end are
+// clamped and masked to zero, channels and runs past the end are clamped and
+// their results dropped.
 // ---------------------------------------------------------------------------
-constexpr int kGwBins = 8;
-constexpr int kGwBatch = 16;
+// Runs per work item: 4 (16 bins, a 128-byte line per spectrum row) while the
+// per-lane dL/dw accumulators are small, 2 for the 4 x 4 and 5 x 5 kernels.
+template <int NK>
+__host__ __device__ constexpr int gw_runs() {
+  return NK <= 3 ? 4 : 2;
+}
+
+// Adds one run's gK (4 bins: d*[q], lane rows j) projected onto the taps to gw.
+template <int NK>
+__device__ __forceinline__ void gw_project_run(float (&gw)[4][NK * NK], const v4f (&dr)[4 * gw_runs<NK>()],
+                                               const v4f (&di)[4 * gw_runs<NK>()], int r, int g, int nmain, int H, int P,
+                                               const float2 *tw) {
+  if (g < nmain) {
+    const int k = (4 * g) / H, l0 = 4 * g - k * H;
+    float2 u[NK], v[4][NK];
+#pragma unroll
+    for (int a = 0; a < NK; ++a) u[a] = tw[(k * a) % P];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int b = 0; b < NK; ++b) v[q][b] = tw[((l0 + q) * b) % P];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int b = 0; b < NK; ++b) {
+        float ex = 0.f, ey = 0.f;  // E_b = sum_q D_q conj(v_qb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          ex += dr[4 * r + q][j] * v[q][b].x + di[4 * r + q][j] * v[q][b].y;
+          ey += di[4 * r + q][j] * v[q][b].x - dr[4 * r + q][j] * v[q][b].y;
+        }
+#pragma unroll
+        for (int a = 0; a < NK; ++a) gw[j][a * NK + b] += ex * u[a].x + ey * u[a].y;
+      }
+  } else {
+    const int k0 = 4 * (g - nmain);
+    float2 u[4][NK];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int a = 0; a < NK; ++a) u[q][a] = tw[((k0 + q) * a) % P];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int a = 0; a < NK; ++a) {
+        float f = 0.f;  // Re F_a = Re sum_q D_q conj(u_qa)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) f += dr[4 * r + q][j] * u[q][a].x + di[4 * r + q][j] * u[q][a].y;
+#pragma unroll
+        for (int b = 0; b < NK; ++b) gw[j][a * NK + b] += (b & 1) ? -f : f;
+      }
+  }
+}
 
 template <int NK>
-__global__ __launch_bounds__(256) void k_full_gw(const float2 *__restrict__ G, const float2 *__restrict__ X,
-                                                 const float2 *__restrict__ twg, float *__restrict__ part, int B,
-                                                 int S, int C, int P, int Pf, int NB, int chunk_bins) {
-  constexpr int T = NK * NK;
+__global__ __launch_bounds__(256) void k_full_gw(SpecLayout G, SpecLayout X, const float2 *__restrict__ twg,
+                                                 float *__restrict__ part, int B, int S, int C, int P,
+                                                 int groups_per_chunk) {
+  constexpr int T = NK * NK, kGwRuns = gw_runs<NK>();
   extern __shared__ float smem[];
   float2 *tw = reinterpret_cast<float2 *>(smem);
-  float2 *sG = tw + ((P + 31) & ~31);          // [16 b][32 s][8 bins]
-  float2 *sX = sG + kGwBatch * 32 * kGwBins;   // [16 b][32 c][8 bins]
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int sblocks = (S + 31) / 32, cblocks = (C + 31) / 32;
-  const int blk = blockIdx.x % (sblocks * cblocks);
-  const int chunk = blockIdx.x / (sblocks * cblocks);
-  const int s0 = (blk / cblocks) * 32, c0 = (blk % cblocks) * 32;
-  const int ws = (wave >> 1) * 16, wc = (wave & 1) * 16;  // wave tile inside the block
-  const int bin_begin = chunk * chunk_bins;
-  const int bin_end = min(NB, bin_begin + chunk_bins);
-  for (int i = tid; i < P; i += 256) tw[i] = twg[i];
+  for (int i = threadIdx.x; i < P; i += 256) tw[i] = twg[i];
+  __syncthreads();
 
-  float gw[4][T];  // rows s0 + ws + 4 (lane / 16) + j, column c0 + wc + lane % 16
+  const int H = P / 2, nmain = P * H / 4, nrun = nmain + P / 4;
+  const int ngroups = (nrun + kGwRuns - 1) / kGwRuns;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int mrow = lane & 15, kq = lane >> 4;
+  const int sblocks = (S + 31) / 32, cblocks = (C + 31) / 32;
+  const int blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int tile = blk % (sblocks * cblocks), chunk = blk / (sblocks * cblocks);
+  const int s0 = (tile / cblocks) * 32 + (wave >> 1) * 16, c0 = (tile % cblocks) * 32 + (wave & 1) * 16;
+  const int sa = min(s0 + mrow, S - 1), cb = min(c0 + mrow, C - 1);  // A row (s), B column (c) of this lane
+  const int gr_begin = chunk * groups_per_chunk, gr_end = min(ngroups, gr_begin + groups_per_chunk);
+
+  float gw[4][T];  // rows s0 + 4 (lane / 16) + j, column c0 + lane % 16
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int t = 0; t < T; ++t) gw[j][t] = 0.f;
-  const int mrow = lane % 16, kq = lane / 16;
 
-  for (int bb = bin_begin; bb < bin_end; bb += kGwBins) {
-    v4f dr[kGwBins], di[kGwBins];
+  // work item: (group of 4 runs, batch row b0 + lane / 16)
+  float4 ng[kGwRuns][2], nx[kGwRuns][2];
+  auto load_item = [&](int grp, int b0) {
+    const long long bc = min(b0 + kq, B - 1);
 #pragma unroll
-    for (int q = 0; q < kGwBins; ++q) dr[q] = di[q] = v4f{0.f, 0.f, 0.f, 0.f};
-    for (int b0 = 0; b0 < B; b0 += kGwBatch) {
-      __syncthreads();
-      // stage G[b0..b0+16][s0..s0+32][bins] and X[b0..b0+16][c0..c0+32][bins]; zero outside
-      for (int i = tid; i < kGwBatch * 32 * kGwBins; i += 256) {
-        const int q = i % kGwBins, r = i / kGwBins;  // r = b * 32 + x
-        const int b = b0 + r / 32, x = r % 32;
-        const int gbin = bb + q;
-        const bool ok = gbin < bin_end && b < B;
-        const int gs = s0 + x, gc = c0 + x;
-        sG[i] = (ok && gs < S) ? G[((long long)b * S + gs) * NB + gbin] : make_float2(0.f, 0.f);
-        sX[i] = (ok && gc < C) ? X[((long long)b * C + gc) * NB + gbin] : make_float2(0.f, 0.f);
+    for (int r = 0; r < kGwRuns; ++r) {
+      const int g = min(grp * kGwRuns + r, nrun - 1);
+      const bool side = g >= nmain;
+      const float4 *ga = reinterpret_cast<const float4 *>(
+          side ? G.side + (bc * S + sa) * G.sps + 4 * (g - nmain) : G.main + (bc * S + sa) * G.ps + 4 * g);
+      const float4 *xa = reinterpret_cast<const float4 *>(
+          side ? X.side + (bc * C + cb) * X.sps + 4 * (g - nmain) : X.main + (bc * C + cb) * X.ps + 4 * g);
+      ng[r][0] = ga[0], ng[r][1] = ga[1], nx[r][0] = xa[0], nx[r][1] = xa[1];
+    }
+  };
+  if (gr_begin < gr_end) load_item(gr_begin, 0);
+  v4f dr[4 * kGwRuns], di[4 * kGwRuns];
+  for (int grp = gr_begin, b0 = 0; grp < gr_end;) {
+    float4 cg[kGwRuns][2], cx[kGwRuns][2];
+#pragma unroll
+    for (int r = 0; r < kGwRuns; ++r)
+      cg[r][0] = ng[r][0], cg[r][1] = ng[r][1], cx[r][0] = nx[r][0], cx[r][1] = nx[r][1];
+    int grp2 = grp, b02 = b0 + 4;
+    if (b02 >= B) b02 = 0, ++grp2;
+    if (grp2 < gr_end) load_item(grp2, b02);
+    if (b0 == 0) {
+#pragma unroll
+      for (int q = 0; q < 4 * kGwRuns; ++q) dr[q] = di[q] = v4f{0.f, 0.f, 0.f, 0.f};
+    }
+    const float m = b0 + kq < B ? 1.f : 0.f;  // batch rows past the end add nothing
+#pragma unroll
+    for (int r = 0; r < kGwRuns; ++r) {
+      const float gr[4] = {m * cg[r][0].x, m * cg[r][0].z, m * cg[r][1].x, m * cg[r][1].z};
+      const float gi[4] = {m * cg[r][0].y, m * cg[r][0].w, m * cg[r][1].y, m * cg[r][1].w};
+      const float xr[4] = {cx[r][0].x, cx[r][0].z, cx[r][1].x, cx[r][1].z};
+      const float xi[4] = {cx[r][0].y, cx[r][0].w, cx[r][1].y, cx[r][1].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        // D = G conj(X):  re = Gr Xr + Gi Xi,  im = Gi Xr - Gr Xi
+        dr[4 * r + q] = mfma4(gr[q], xr[q], dr[4 * r + q]);
+        dr[4 * r + q] = mfma4(gi[q], xi[q], dr[4 * r + q]);
+        di[4 * r + q] = mfma4(gi[q], xr[q], di[4 * r + q]);
+        di[4 * r + q] = mfma4(-gr[q], xi[q], di[4 * r + q]);
       }
-      __syncthreads();
-#pragma unroll
-      for (int q = 0; q < kGwBins; ++q)
-#pragma unroll
-        for (int b4 = 0; b4 < kGwBatch; b4 += 4) {
-          const int b = b4 + kq;
-          const float2 g = sG[(b * 32 + ws + mrow) * kGwBins + q];  // A[m = s][k = b]
-          const float2 x = sX[(b * 32 + wc + mrow) * kGwBins + q];  // B[k = b][n = c]
-          // D = G conj(X):  re = Gr Xr + Gi Xi,  im = Gi Xr - Gr Xi
-          dr[q] = mfma4(g.x, x.x, dr[q]);
-          dr[q] = mfma4(g.y, x.y, dr[q]);
-          di[q] = mfma4(g.y, x.x, di[q]);
-          di[q] = mfma4(-g.x, x.y, di[q]);
-        }
     }
+    if (b02 == 0) {  // the group is complete: project its runs onto the taps
 #pragma unroll
-    for (int q = 0; q < kGwBins; ++q) {
-      const int gbin = bb + q;
-      if (gbin >= bin_end) break;
-      float2 u[NK], v[NK];
-      bin_phases<NK>(tw, P, Pf, gbin, u, v);
-#pragma unroll
-      for (int a = 0; a < NK; ++a)
-#pragma unroll
-        for (int b = 0; b < NK; ++b) {
-          // phase W^(k a) W^(l b); Re(D conj(phase)) = Dr pr + Di pi
-          const float pr = u[a].x * v[b].x - u[a].y * v[b].y;
-          const float pi = u[a].x * v[b].y + u[a].y * v[b].x;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) gw[j][a * NK + b] += dr[q][j] * pr + di[q][j] * pi;
-        }
+      for (int r = 0; r < kGwRuns; ++r) {
+        const int g = grp * kGwRuns + r;
+        if (g < nrun) gw_project_run<NK>(gw, dr, di, r, g, nmain, H, P, tw);
+      }
     }
+    grp = grp2, b0 = b02;
   }
-  // write this chunk's partial sums
+  // this chunk's partial sums
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const int gs = s0 + ws + 4 * kq + j, gc = c0 + wc + mrow;
+    const int gs = s0 + 4 * kq + j, gc = c0 + mrow;
     if (gs >= S || gc >= C) continue;
     float *p = part + (((long long)chunk * S + gs) * C + gc) * T;
 #pragma unroll
@@ -278,16 +372,22 @@ __global__ void k_full_gw_reduce(const float *__restrict__ part, float *__restri
   }
 }
 
-// Weights rearranged for the contraction: forward [c][tap][s], dL/dX [s][tap][c].
-__global__ void k_full_weights(const float *__restrict__ w, float *__restrict__ wf, float *__restrict__ wg, int S,
-                               int C, int T) {
-  const long long n = (long long)S * C * T;
+// Weights rearranged for the contraction, zero-padded: wt[kd][nd][tap] of
+// [KDp][NDp][TP] with w[s][c][tap] at (kd, nd) = (c, s) forward, (s, c) for dL/dX.
+__global__ void k_full_weights(const float *__restrict__ w, float *__restrict__ wt, int S, int C, int T, int TP,
+                               int gx, int KDp, int NDp) {
+  const int KD = gx ? S : C, ND = gx ? C : S;
+  const long long n = (long long)KDp * NDp * TP;
   for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long long)gridDim.x * blockDim.x) {
-    const int tap = (int)(i % T);
-    const long long sc = i / T;
-    const int c = (int)(sc % C), s = (int)(sc / C);
-    if (wf) wf[((long long)c * T + tap) * S + s] = w[i];
-    if (wg) wg[((long long)s * T + tap) * C + c] = w[i];
+    const int tap = (int)(i % TP);
+    const long long r = i / TP;
+    const int nd = (int)(r % NDp), kd = (int)(r / NDp);
+    float v = 0.f;
+    if (kd < KD && nd < ND && tap < T) {
+      const int s_ = gx ? kd : nd, c_ = gx ? nd : kd;
+      v = w[((long long)s_ * C + c_) * T + tap];
+    }
+    wt[i] = v;
   }
 }
 
@@ -308,70 +408,78 @@ static bool dispatch_nk(int nk, F &&f) {
 
 bool full_kernel_size_supported(int nk) { return nk >= 1 && nk <= 5; }
 
-static size_t contract_lds(int P, int nk) {
-  return ((size_t)((P + 31) & ~31) + 16 * 4 * kFcBins) * sizeof(float2) + (size_t)4 * nk * nk * kFcOut * sizeof(float);
+static int round_up(int v, int m) { return (v + m - 1) / m * m; }
+static int tap_pad_rt(int nk) { return (nk * nk + 3) & ~3; }
+
+size_t full_weight_floats(int KD, int ND, int nk) {
+  return (size_t)round_up(KD, 4) * round_up(ND, kCtOut) * tap_pad_rt(nk);
 }
 
-hipError_t launch_full_weights(const float *w, float *wf, float *wg, int S, int C, int nk, hipStream_t s) {
-  const long long n = (long long)S * C * nk * nk;
+hipError_t launch_full_weights(const float *w, float *wt, bool gx, int S, int C, int nk, hipStream_t s) {
+  const int KDp = round_up(gx ? S : C, 4), NDp = round_up(gx ? C : S, kCtOut), TP = tap_pad_rt(nk);
+  const long long n = (long long)KDp * NDp * TP;
   long long g = (n + 255) / 256;
   if (g > 65536) g = 65536;
   timing_before("full_weights", s);
-  hipLaunchKernelGGL(k_full_weights, dim3((unsigned)g), dim3(256), 0, s, w, wf, wg, S, C, nk * nk);
+  hipLaunchKernelGGL(k_full_weights, dim3((unsigned)g), dim3(256), 0, s, w, wt, S, C, nk * nk, TP, gx ? 1 : 0, KDp,
+                     NDp);
   const hipError_t e = hipGetLastError();
   timing_after("full_weights", s);
   return e;
 }
 
-hipError_t launch_full_contract(bool gx, int nk, const float2 *in, const float *wt, const float2 *tw, float2 *out,
+hipError_t launch_full_contract(bool gx, int nk, SpecLayout in, const float *wt, const float2 *tw, SpecLayout out,
                                 int B, int KD, int ND, int P, hipStream_t s) {
-  const int Pf = P / 2 + 1, NB = P * Pf;
-  const long long nbg = (NB + kFcBins - 1) / kFcBins;
-  const long long gx_ = nbg * ((ND + kFcOut - 1) / kFcOut);
-  const int gy = (B + 15) / 16;
-  if (gx_ >= (1LL << 31)) return hipErrorInvalidValue;
+  const int nrun = P * (P / 2) / 4 + P / 4;
+  const int nwg_run = (nrun + 3) / 4, nsb = (ND + kCtOut - 1) / kCtOut, nbt = (B + 15) / 16;
+  const long long blocks = (long long)nwg_run * nsb * nbt;
+  if (blocks >= (1LL << 31) || P % 8 != 0) return hipErrorInvalidValue;
+  const int KDp = round_up(KD, 4), NDp = round_up(ND, kCtOut);
   hipError_t err = hipErrorInvalidValue;
   dispatch_nk(nk, [&](auto nc) {
     constexpr int NK = decltype(nc)::value;
     const char *nm = gx ? "full_contract_gx" : "full_contract_fwd";
     timing_before(nm, s);
     if (gx)
-      hipLaunchKernelGGL((k_full_contract<NK, true>), dim3((unsigned)gx_, gy), dim3(kFcThreads), contract_lds(P, NK),
-                         s, in, wt, tw, out, B, KD, ND, P, Pf, NB);
+      hipLaunchKernelGGL((k_full_contract<NK, true>), dim3((unsigned)blocks), dim3(256), 0, s, in, wt, tw, out, B,
+                         KD, KDp, ND, NDp, P, nwg_run, nsb);
     else
-      hipLaunchKernelGGL((k_full_contract<NK, false>), dim3((unsigned)gx_, gy), dim3(kFcThreads),
-                         contract_lds(P, NK), s, in, wt, tw, out, B, KD, ND, P, Pf, NB);
+      hipLaunchKernelGGL((k_full_contract<NK, false>), dim3((unsigned)blocks), dim3(256), 0, s, in, wt, tw, out, B,
+                         KD, KDp, ND, NDp, P, nwg_run, nsb);
     err = hipGetLastError();
     timing_after(nm, s);
   });
   return err;
 }
 
-int full_gw_chunks(int B, int S, int C, int P) {
-  const int NB = P * (P / 2 + 1);
-  const int blocks = ((S + 31) / 32) * ((C + 31) / 32);
-  int chunks = (2048 + blocks - 1) / blocks;  // about 2048 workgroups
-  const int maxc = (NB + kGwBins - 1) / kGwBins;
-  if (chunks > maxc) chunks = maxc;
-  if (chunks < 1) chunks = 1;
+static int gw_runs_rt(int nk) { return nk <= 3 ? 4 : 2; }
+
+int full_gw_chunks(int B, int S, int C, int P, int nk) {
   (void)B;
+  const int nrun = P * (P / 2) / 4 + P / 4;
+  const int ngroups = (nrun + gw_runs_rt(nk) - 1) / gw_runs_rt(nk);
+  const int tiles = ((S + 31) / 32) * ((C + 31) / 32);
+  int chunks = (2048 + tiles - 1) / tiles;  // about 2048 workgroups
+  if (chunks > ngroups) chunks = ngroups;
+  if (chunks < 1) chunks = 1;
   return chunks;
 }
 
-hipError_t launch_full_gw(int nk, const float2 *G, const float2 *X, const float2 *tw, float *part, float *gw, int B,
-                          int S, int C, int P, hipStream_t s) {
-  const int Pf = P / 2 + 1, NB = P * Pf;
-  const int chunks = full_gw_chunks(B, S, C, P);
-  int chunk_bins = (NB + chunks - 1) / chunks;
-  chunk_bins = (chunk_bins + kGwBins - 1) / kGwBins * kGwBins;
-  const int blocks = ((S + 31) / 32) * ((C + 31) / 32);
-  const size_t lds = ((size_t)((P + 31) & ~31) + 2 * (size_t)kGwBatch * 32 * kGwBins) * sizeof(float2);
+hipError_t launch_full_gw(int nk, SpecLayout G, SpecLayout X, const float2 *tw, float *part, float *gw, int B, int S,
+                          int C, int P, hipStream_t s) {
+  if (P % 8 != 0) return hipErrorInvalidValue;
+  const int nrun = P * (P / 2) / 4 + P / 4;
+  const int ngroups = (nrun + gw_runs_rt(nk) - 1) / gw_runs_rt(nk);
+  const int chunks = full_gw_chunks(B, S, C, P, nk);
+  const int groups_per_chunk = (ngroups + chunks - 1) / chunks;
+  const int tiles = ((S + 31) / 32) * ((C + 31) / 32);
+  const size_t lds = (size_t)P * sizeof(float2);
   hipError_t err = hipErrorInvalidValue;
   dispatch_nk(nk, [&](auto nc) {
     constexpr int NK = decltype(nc)::value;
     timing_before("full_gw", s);
-    hipLaunchKernelGGL((k_full_gw<NK>), dim3((unsigned)(blocks * chunks)), dim3(256), lds, s, G, X, tw, part, B, S, C,
-                       P, Pf, NB, chunk_bins);
+    hipLaunchKernelGGL((k_full_gw<NK>), dim3((unsigned)(tiles * chunks)), dim3(256), lds, s, G, X, tw, part, B, S, C,
+                       P, groups_per_chunk);
     err = hipGetLastError();
     timing_after("full_gw", s);
   });

@@ -6,6 +6,8 @@
 
 #include <cstdint>
 
+#include "fdc.h"
+
 namespace fdc {
 
 // How a logical rows x cols image maps onto a stored image (row stride `cols_stored`).
@@ -47,6 +49,17 @@ inline SpecLayout split_layout(const float2 *p, long long planes, int rows, int 
   float2 *q = const_cast<float2 *>(p);
   return SpecLayout{q, (long long)rows * (L - 1), L - 1, q + planes * rows * (L - 1), rows, 1};
 }
+// Split layout of `planes` P x (P/2+1) Full FDC spectra with padded plane strides
+// (FDC_FULL_MAIN_PLANE / FDC_FULL_SIDE_PLANE bins), so that the same bin of
+// successive planes does not fall on one memory channel.
+inline SpecLayout full_spec_layout(const float2 *p, long long planes, int P) {
+  float2 *q = const_cast<float2 *>(p);
+  const long long ms = FDC_FULL_MAIN_PLANE(P);
+  return SpecLayout{q, ms, P / 2, q + planes * ms, FDC_FULL_SIDE_PLANE(P), 1};
+}
+inline long long full_spec_elems(long long planes, int P) {
+  return planes * ((long long)FDC_FULL_MAIN_PLANE(P) + FDC_FULL_SIDE_PLANE(P));
+}
 
 // Kernel timing hooks (no-ops unless enabled through the ABI).
 void timing_before(const char *name, hipStream_t s);
@@ -68,6 +81,9 @@ hipError_t launch_row_c2r(int n, SpecLayout in, float *y, long long planes, int 
 // data (in place allowed).
 hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long long planes, int L, int ld,
                           long long in_plane_stride, long long out_plane_stride, hipStream_t s);
+// Column DFTs of `planes` split-layout n x (n/2+1) half spectra with the strides of
+// `in` and `out` (in place allowed).
+hipError_t launch_col_fft_split(int n, int dir, SpecLayout in, SpecLayout out, long long planes, hipStream_t s);
 
 // Fused CIC + FDP column kernels (square n x n images pooled to m x m; L = m/2 + 1).
 // T, Xh, U, Tg and V are split-layout spectra (SpecLayout) with L bins per row.
@@ -82,15 +98,18 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
 hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, float2 *V, int B, int C, int S,
                              hipStream_t s);
 
-// Full FDC (full_fdc.hip).  Spectra in the plain layout [planes][P][P/2+1]; tw is the
-// device table W^j = exp(-2 pi i j / P), j < P.
+// Full FDC (full_fdc.hip).  Spectra in the padded split layout full_spec_layout,
+// P a multiple of 8; tw is the device table
+// W^j = exp(-2 pi i j / P), j < P.  Rearranged weights take full_weight_floats(KD, ND, nk)
+// floats: KD = Cin, ND = Cout forward (gx = false); KD = Cout, ND = Cin for dL/dX.
 bool full_kernel_size_supported(int nk);
-int full_gw_chunks(int B, int S, int C, int P);
-hipError_t launch_full_weights(const float *w, float *wf, float *wg, int S, int C, int nk, hipStream_t s);
-hipError_t launch_full_contract(bool gx, int nk, const float2 *in, const float *wt, const float2 *tw, float2 *out,
+size_t full_weight_floats(int KD, int ND, int nk);
+int full_gw_chunks(int B, int S, int C, int P, int nk);
+hipError_t launch_full_weights(const float *w, float *wt, bool gx, int S, int C, int nk, hipStream_t s);
+hipError_t launch_full_contract(bool gx, int nk, SpecLayout in, const float *wt, const float2 *tw, SpecLayout out,
                                 int B, int KD, int ND, int P, hipStream_t s);
-hipError_t launch_full_gw(int nk, const float2 *G, const float2 *X, const float2 *tw, float *part, float *gw, int B,
-                          int S, int C, int P, hipStream_t s);
+hipError_t launch_full_gw(int nk, SpecLayout G, SpecLayout X, const float2 *tw, float *part, float *gw, int B, int S,
+                          int C, int P, hipStream_t s);
 
 // Spectral CIC and FDP.
 hipError_t launch_cic_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, long long P,

@@ -15,20 +15,13 @@
 // Intermediates stay row-major [plane][row][column]; column kernels own CT adjacent
 // columns (numbered across planes) with the column index fastest across lanes, so
 // every global access is a run of up to CT consecutive complex values.
+#include "device.h"
 #include "fft.h"
 #include "internal.h"
 
 #include <string>
 
 namespace fdc {
-
-// Blocks are dispatched round-robin over the 8 XCDs; renumber them so that
-// neighbouring tiles (which share cache lines) run on the same XCD and its L2.
-__device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
-  const int q = nblocks >> 3, rem = nblocks & 7;
-  const int x = bid & 7, i = bid >> 3;
-  return x * q + (x < rem ? x : rem) + i;
-}
 
 // Element offset of logical pixel (r, w) of an image seen through `v`, or -1 when
 // the pixel is not stored (cropped away).  MODE is v.mode, fixed at compile time.
@@ -283,6 +276,33 @@ __device__ __forceinline__ ColPtr split_col(const float2 *base, int planes, int 
   float2 *b = const_cast<float2 *>(base);
   if (l < H) return ColPtr{b + (long long)plane * ROWS * H + l, H};
   return ColPtr{b + (long long)planes * ROWS * H + (long long)plane * ROWS, 1};
+}
+
+// Column DFTs (N, direction DIR) of `planes` split-layout N x (N/2+1) half spectra
+// with any plane strides (SpecLayout), in place or out of place (each workgroup
+// reads its columns whole before writing).
+__device__ __forceinline__ ColPtr layout_col(const SpecLayout &sl, int H, int plane, int l) {
+  if (l < H) return ColPtr{sl.main + (long long)plane * sl.ps + l, sl.rs};
+  return ColPtr{sl.side + (long long)plane * sl.sps, sl.srs};
+}
+
+template <int N, int CT, int DIR>
+__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft_split(SpecLayout in, SpecLayout out, int planes) {
+  using Cfg = FftCfg<N>;
+  constexpr int L = N / 2 + 1, TPS = Cfg::TPS, E = Cfg::E;
+  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
+  stage_twiddles<N>(tw, threadIdx.x, CT * TPS);
+  const int s = threadIdx.x % CT, t = threadIdx.x / CT;
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
+  const ColPtr ic = layout_col(in, L - 1, c.plane, c.l);
+  float2 v[E];
+#pragma unroll
+  for (int m = 0; m < E; ++m) v[m] = ic.p[(t + TPS * m) * ic.stride];  // lanes past the end read a valid column
+  fft_seq<N, DIR>(v, t, lds, s, CT, tw, 1);
+  if (!c.ok) return;
+  const ColPtr oc = layout_col(out, L - 1, c.plane, c.l);
+#pragma unroll
+  for (int m = 0; m < E; ++m) oc.p[(t + TPS * m) * oc.stride] = v[m];
 }
 
 // Forward, first half: column DFT (N) of the pruned row spectra, keep the M rows
@@ -734,6 +754,25 @@ hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long lo
     else
       err = launch(ni.c_str(), k_col_fft<N, CT, +1>, grid, CT * FftCfg<N>::TPS, lds, s, in, out, L, ld, (int)planes,
                    in_plane_stride, out_plane_stride);
+  });
+  return err;
+}
+
+hipError_t launch_col_fft_split(int n, int dir, SpecLayout in, SpecLayout out, long long planes, hipStream_t s) {
+  hipError_t err = hipErrorInvalidValue;
+  dispatch_n(n, [&](auto nc) {
+    constexpr int N = decltype(nc)::value;
+    constexpr int L = N / 2 + 1;
+    constexpr int CT = col_ct_for(col_ct<N>(), L);
+    const size_t lds = (twiddle_lds_elems<N>() + lds_size<kColLds>(N * CT)) * sizeof(float2);
+    const unsigned grid = col_grid(planes, L, CT);
+    if (grid == 0) return;
+    static const std::string nf = "col_fft_fwd_" + std::to_string(N);
+    static const std::string ni = "col_fft_inv_" + std::to_string(N);
+    if (dir < 0)
+      err = launch(nf.c_str(), k_col_fft_split<N, CT, -1>, grid, CT * FftCfg<N>::TPS, lds, s, in, out, (int)planes);
+    else
+      err = launch(ni.c_str(), k_col_fft_split<N, CT, +1>, grid, CT * FftCfg<N>::TPS, lds, s, in, out, (int)planes);
   });
   return err;
 }

@@ -187,6 +187,16 @@ class CicLayer(_LayerPlan):
         return (gx if need_gx else None), (gK if need_gk else None)
 
 
+def full_main_plane(P):
+    """FDC_FULL_MAIN_PLANE(P) of fdc.h: complex elements per main-block plane of a Full FDC spectrum."""
+    return P * (P // 2) + 64
+
+
+def full_side_plane(P):
+    """FDC_FULL_SIDE_PLANE(P) of fdc.h: complex elements per Nyquist-column plane."""
+    return P + 8
+
+
 class FullLayer(_LayerPlan):
     """Full FDC layer: x [B][Cin][P][P], w [Cout][Cin][n][n] -> y [B][Cout][O][O]
     (fdc_full_layer_*).  Workspaces are allocated once per layer object."""
@@ -201,8 +211,19 @@ class FullLayer(_LayerPlan):
         self.bwd_ws = _workspace(self.bwd_ws_bytes, self.device)
 
     def new_saved(self):
-        """Buffer for rfft2(x), [B][Cin][P][P/2+1] complex."""
-        return torch.empty((self.B, self.Cin, self.P, self.P // 2 + 1), dtype=torch.complex64, device=self.device)
+        """Buffer for rfft2(x) (see fdc_full_forward for its layout)."""
+        return torch.empty(self.saved_bytes // 8, dtype=torch.complex64, device=self.device)
+
+    def saved_spectrum(self, saved):
+        """rfft2(x) held in a saved buffer, as a [B][Cin][P][P/2+1] tensor: columns
+        0..P/2-1 come from the main block, column P/2 from the block after it (both
+        with the padded plane strides FDC_FULL_MAIN_PLANE / FDC_FULL_SIDE_PLANE)."""
+        B, C, P = self.B, self.Cin, self.P
+        h = P // 2
+        ms, ss = full_main_plane(P), full_side_plane(P)
+        main = saved[: B * C * ms].view(B, C, ms)[..., : P * h].reshape(B, C, P, h)
+        side = saved[B * C * ms:].view(B, C, ss)[..., :P].reshape(B, C, P, 1)
+        return torch.cat([main, side], dim=-1)
 
     def new_output(self):
         return torch.empty((self.B, self.Cout, self.out, self.out), dtype=torch.float32, device=self.device)
@@ -211,7 +232,7 @@ class FullLayer(_LayerPlan):
         _check(x, torch.float32, (self.B, self.Cin, self.P, self.P), "x")
         _check(w, torch.float32, (self.Cout, self.Cin, self.n, self.n), "w")
         if saved is not None:
-            _check(saved, torch.complex64, (self.B, self.Cin, self.P, self.P // 2 + 1), "saved")
+            _check(saved, torch.complex64, (self.saved_bytes // 8,), "saved")
         y = self.new_output() if y is None else y
         _check(y, torch.float32, (self.B, self.Cout, self.out, self.out), "y")
         call("fdc_full_forward", self._p, _ptr(x), _ptr(w), _ptr(y), _ptr(saved), _ptr(self.fwd_ws),

@@ -8,7 +8,7 @@ import ctypes
 
 import pytest
 
-from paper_2106_12736_amd import _lib
+from paper_2106_12736_amd import _lib, layers
 from paper_2106_12736_amd._lib import FDC_EHIP, FDC_EINVAL, FDC_EUNSUPPORTED, FDC_EWORKSPACE, FDC_OK
 
 
@@ -117,6 +117,7 @@ def test_layer_calls_reject_bad_arguments():
     ((2, 0, 4, 16, 3, 1), FDC_EINVAL),
     ((2, 3, 0, 16, 3, 1), FDC_EINVAL),
     ((2, 3, 4, 2048, 3, 1), FDC_EUNSUPPORTED),  # outside the FFT length set
+    ((2, 3, 4, 4, 3, 1), FDC_EUNSUPPORTED),     # not a multiple of 8
 ])
 def test_full_plan_validation(args, expect):
     """Arguments are checked before the plan touches the device."""
@@ -136,7 +137,7 @@ def test_full_plan_valid_sizes_reach_the_device():
         return
     f, sv, b = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
     assert _lib.status("fdc_layer_workspace_size", p, ctypes.byref(f), ctypes.byref(sv), ctypes.byref(b)) == FDC_OK
-    assert sv.value == 2 * 3 * 16 * 9 * 8
+    assert sv.value == 2 * 3 * (layers.full_main_plane(16) + layers.full_side_plane(16)) * 8
     o = ctypes.c_int()
     assert _lib.status("fdc_layer_output_size", p, ctypes.byref(o)) == FDC_OK
     assert o.value == 14
@@ -185,3 +186,16 @@ def test_destroyed_plan_is_refused():
     assert _lib.status("fdc_fft_workspace_size", ctypes.cast(bogus, ctypes.c_void_p),
                        ctypes.byref(ctypes.c_size_t())) == FDC_EINVAL
     assert _lib.status("fdc_fft_plan_destroy", p) == FDC_OK
+
+
+def test_full_plane_strides_match_header():
+    """The binding's copy of the saved-spectrum plane strides equals the header's macros."""
+    import os
+    import re
+    hdr = open(os.path.join(os.path.dirname(__file__), "..", "include", "fdc.h")).read()
+    m = re.search(r"#define FDC_FULL_MAIN_PLANE\(P\) \(\(int64_t\)\(P\) \* \(\(P\) / 2\) \+ (\d+)\)", hdr)
+    s = re.search(r"#define FDC_FULL_SIDE_PLANE\(P\) \(\(int64_t\)\(P\) \+ (\d+)\)", hdr)
+    assert m and s
+    for P in (8, 224, 512):
+        assert layers.full_main_plane(P) == P * (P // 2) + int(m.group(1))
+        assert layers.full_side_plane(P) == P + int(s.group(1))
