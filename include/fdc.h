@@ -176,19 +176,19 @@ fdc_status fdc_cic_layer_backward(const fdc_layer_plan *plan, const float *gy, c
                                   const fdc_c64 *K, float *gx, fdc_c64 *gK,
                                   void *ws, size_t ws_bytes, hipStream_t stream);
 
-/* Plane strides, in complex elements, of the Full FDC spectrum blocks (the `saved`
- * buffer below): each P x P/2 main plane is followed by 64 unused elements and each
- * P-element Nyquist-column plane by 8, so that one frequency bin of successive planes
- * does not map onto one memory channel. */
-#define FDC_FULL_MAIN_PLANE(P) ((int64_t)(P) * ((P) / 2) + 64)
+/* Strides, in complex elements, of a Full FDC spectrum (the `saved` buffer below).
+ * Columns 0..P/2-1 form the main block: row k of every plane side by side, each
+ * FDC_FULL_ROW(P) elements (P/2 bins and 16 unused).  Column P/2 forms the side
+ * block: FDC_FULL_SIDE_PLANE(P) elements per plane (P bins and 8 unused). */
+#define FDC_FULL_ROW(P) ((int64_t)(P) / 2 + 16)
 #define FDC_FULL_SIDE_PLANE(P) ((int64_t)(P) + 8)
 
 /* Full FDC forward: y = artifact(irfft2(sum_c rfft2(x[b][c]) o K[s][c])) with
  * K[s][c] = rfft2(pad(w[s][c])).  K is generated per bin inside the contraction
- * and never stored.  `saved` (may be NULL) receives rfft2(x), complex: for plane
- * i = b * Cin + c, columns 0..P/2-1 as a row-major P x P/2 array at element
- * i * FDC_FULL_MAIN_PLANE(P), then column P/2 (P elements) at element
- * B * Cin * FDC_FULL_MAIN_PLANE(P) + i * FDC_FULL_SIDE_PLANE(P); the backward pass
+ * and never stored.  `saved` (may be NULL) receives rfft2(x), complex: with
+ * planes i = b * Cin + c (n = B * Cin of them), bin (k, l < P/2) of plane i at element
+ * (k * n + i) * FDC_FULL_ROW(P) + l and bin (k, P/2) at element
+ * P * n * FDC_FULL_ROW(P) + i * FDC_FULL_SIDE_PLANE(P) + k.  The backward pass
  * reads it for dL/dw. */
 fdc_status fdc_full_forward(const fdc_layer_plan *plan, const float *x, const float *w, float *y,
                             void *saved, void *ws, size_t ws_bytes, hipStream_t stream);

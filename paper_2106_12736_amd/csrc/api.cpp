@@ -1,7 +1,7 @@
 // C ABI of libfdc: argument validation, plans, workspace layout and kernel
 // sequencing.  Every entry point validates on the host first and returns
 // before enqueuing anything when an argument is wrong.
-#include "../../include/fdc.h"
+#include "fdc.h"
 #include "internal.h"
 
 #include <cmath>
@@ -72,8 +72,8 @@ Timing &timing() {
   return t;
 }
 void timing_release(Timing &t) {
-  for (auto e : t.start) hipEventDestroy(e);
-  for (auto e : t.stop) hipEventDestroy(e);
+  for (auto e : t.start) (void)hipEventDestroy(e);
+  for (auto e : t.stop) (void)hipEventDestroy(e);
   t.start.clear();
   t.stop.clear();
   t.names.clear();

@@ -16,8 +16,9 @@
 //
 // Spectra use the split layout of a P x (P/2+1) half spectrum: a main block of
 // P x P/2 planes (columns 0..P/2-1) followed by a side block of P-element planes (the
-// Nyquist column l = P/2), so that runs of 4 bins are 32-byte aligned; plane strides
-// are padded (full_spec_layout).
+// Nyquist column l = P/2), so that runs of 4 bins are 32-byte aligned.  In the main
+// block row k of every plane lies side by side (full_spec_layout), so the planes a
+// run's contraction reads are a few MB apart rather than a plane apart.
 //
 // Complex products use four real v_mfma_f32_16x16x4f32 per 4-deep K step:
 //   re += Ar Br - Ai Bi,  im += Ar Bi + Ai Br.
@@ -186,8 +187,8 @@ __global__ __launch_bounds__(256) void k_full_contract(SpecLayout in, const floa
     for (int q = 0; q < 4; ++q)
 #pragma unroll
       for (int b = 0; b < NK; ++b) v[q][b] = tw[((l0 + q) * b) % P];
-    contract_run<NK, GX, false>(in.main + 4 * g, wt, out.main + 4 * g, u, v, in.ps, out.ps, B, KD, KDp, ND, NDp,
-                                bt * 16, sb * kCtOut);
+    contract_run<NK, GX, false>(in.main + k * in.rs + l0, wt, out.main + k * out.rs + l0, u, v, in.ps, out.ps, B, KD,
+                                KDp, ND, NDp, bt * 16, sb * kCtOut);
   } else {
     const int k0 = 4 * (g - nmain);
     float2 z[NK], u[4][NK];
@@ -211,17 +212,16 @@ __global__ __launch_bounds__(256) void k_full_contract(SpecLayout in, const floa
 // done per run: a row run sums E_b = sum_q gK_q conj(W^(l_q b)) and adds
 // Re(E_b conj(W^(k a))); a Nyquist run sums F_a = sum_q gK_q conj(W^(k_q a)) and adds
 // (-1)^b Re(F_a).  A workgroup (4 waves) owns a 32 x 32 (s, c) block, each wave a
-// 16 x 16 tile, and walks its chunk 4 runs (16 bins, one 128-byte line of every
-// spectrum it reads; 2 runs for the larger kernels) at a time, 4 batch rows per step, loading the next step while
+// 16 x 16 tile, and walks its chunk 2 runs (8 bins) at a time, 4 batch rows per step, loading the next step while
 // the current one runs.  Loads are unconditional: batch rows past the end are
 // clamped and masked to zero, channels and runs past the end are clamped and
 // their results dropped.
 // ---------------------------------------------------------------------------
-// Runs per work item: 4 (16 bins, a 128-byte line per spectrum row) while the
-// per-lane dL/dw accumulators are small, 2 for the 4 x 4 and 5 x 5 kernels.
+// Runs per work item: 2 (8 bins), which keeps a wave within 256 registers so that two
+// waves share a SIMD and one's projection overlaps the other's matrix-core work.
 template <int NK>
 __host__ __device__ constexpr int gw_runs() {
-  return NK <= 3 ? 4 : 2;
+  return 2;
 }
 
 // Adds one run's gK (4 bins: d*[q], lane rows j) projected onto the taps to gw.
@@ -272,7 +272,7 @@ __device__ __forceinline__ void gw_project_run(float (&gw)[4][NK * NK], const v4
 }
 
 template <int NK>
-__global__ __launch_bounds__(256) void k_full_gw(SpecLayout G, SpecLayout X, const float2 *__restrict__ twg,
+__global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, const float2 *__restrict__ twg,
                                                  float *__restrict__ part, int B, int S, int C, int P,
                                                  int groups_per_chunk) {
   constexpr int T = NK * NK, kGwRuns = gw_runs<NK>();
@@ -306,10 +306,11 @@ __global__ __launch_bounds__(256) void k_full_gw(SpecLayout G, SpecLayout X, con
     for (int r = 0; r < kGwRuns; ++r) {
       const int g = min(grp * kGwRuns + r, nrun - 1);
       const bool side = g >= nmain;
+      const int k = (4 * g) / H, l0 = 4 * g - k * H;  // row run (k, l0..l0+3) when not on the side
       const float4 *ga = reinterpret_cast<const float4 *>(
-          side ? G.side + (bc * S + sa) * G.sps + 4 * (g - nmain) : G.main + (bc * S + sa) * G.ps + 4 * g);
+          side ? G.side + (bc * S + sa) * G.sps + 4 * (g - nmain) : G.main + (bc * S + sa) * G.ps + k * G.rs + l0);
       const float4 *xa = reinterpret_cast<const float4 *>(
-          side ? X.side + (bc * C + cb) * X.sps + 4 * (g - nmain) : X.main + (bc * C + cb) * X.ps + 4 * g);
+          side ? X.side + (bc * C + cb) * X.sps + 4 * (g - nmain) : X.main + (bc * C + cb) * X.ps + k * X.rs + l0);
       ng[r][0] = ga[0], ng[r][1] = ga[1], nx[r][0] = xa[0], nx[r][1] = xa[1];
     }
   };
@@ -363,13 +364,25 @@ __global__ __launch_bounds__(256) void k_full_gw(SpecLayout G, SpecLayout X, con
   }
 }
 
-// dL/dw = sum over chunks, in chunk order.
-__global__ void k_full_gw_reduce(const float *__restrict__ part, float *__restrict__ gw, long long n, int chunks) {
-  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long long)gridDim.x * blockDim.x) {
-    float acc = 0.f;
-    for (int c = 0; c < chunks; ++c) acc += part[(long long)c * n + i];
-    gw[i] = acc;
+// dL/dw = sum over chunks in a fixed order: a workgroup owns 64 outputs; its four
+// waves sum the chunks congruent to 0, 1, 2, 3 mod 4 (four accumulators each, chunk
+// c into accumulator (c / 4) mod 4), and the 16 partial sums are added in order.
+__global__ __launch_bounds__(256) void k_full_gw_reduce(const float *__restrict__ part, float *__restrict__ gw,
+                                                        long long n, int chunks) {
+  __shared__ float red[4][64];
+  const int o = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const long long i = (long long)blockIdx.x * 64 + o;
+  const long long ii = i < n ? i : n - 1;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  int c = w;
+  for (; c + 12 < chunks; c += 16) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc[u] += part[(long long)(c + 4 * u) * n + ii];
   }
+  for (int u = 0; c < chunks; c += 4, ++u) acc[u] += part[(long long)c * n + ii];
+  red[w][o] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  __syncthreads();
+  if (w == 0 && i < n) gw[i] = (red[0][o] + red[1][o]) + (red[2][o] + red[3][o]);
 }
 
 // Weights rearranged for the contraction, zero-padded: wt[kd][nd][tap] of
@@ -452,14 +465,21 @@ hipError_t launch_full_contract(bool gx, int nk, SpecLayout in, const float *wt,
   return err;
 }
 
-static int gw_runs_rt(int nk) { return nk <= 3 ? 4 : 2; }
+static int gw_runs_rt(int nk) {
+  (void)nk;
+  return 2;
+}
 
+// Bin chunks of the dL/dw pass: about 8192 workgroups, so that the workgroups running
+// at one time on an XCD are the tiles of one or two short chunks and share the spectra
+// they read through L2; at most 512 chunks of partial sums.
 int full_gw_chunks(int B, int S, int C, int P, int nk) {
   (void)B;
   const int nrun = P * (P / 2) / 4 + P / 4;
   const int ngroups = (nrun + gw_runs_rt(nk) - 1) / gw_runs_rt(nk);
   const int tiles = ((S + 31) / 32) * ((C + 31) / 32);
-  int chunks = (2048 + tiles - 1) / tiles;  // about 2048 workgroups
+  int chunks = (8192 + tiles - 1) / tiles;
+  if (chunks > 512) chunks = 512;
   if (chunks > ngroups) chunks = ngroups;
   if (chunks < 1) chunks = 1;
   return chunks;
@@ -485,8 +505,8 @@ hipError_t launch_full_gw(int nk, SpecLayout G, SpecLayout X, const float2 *tw, 
   });
   if (err != hipSuccess) return err;
   const long long n = (long long)S * C * nk * nk;
-  long long g = (n + 255) / 256;
-  if (g > 65536) g = 65536;
+  const long long g = (n + 63) / 64;
+  if (g >= (1LL << 31)) return hipErrorInvalidValue;
   timing_before("full_gw_reduce", s);
   hipLaunchKernelGGL(k_full_gw_reduce, dim3((unsigned)g), dim3(256), 0, s, part, gw, n, chunks);
   err = hipGetLastError();

@@ -36,10 +36,10 @@ bool size_supported(int n);
 struct SpecLayout {
   float2 *main;
   long long ps;
-  int rs;
+  long long rs;
   float2 *side;
   long long sps;
-  int srs;
+  long long srs;
 };
 inline SpecLayout plain_layout(const float2 *p, int rows, int L) {
   float2 *q = const_cast<float2 *>(p);
@@ -49,16 +49,18 @@ inline SpecLayout split_layout(const float2 *p, long long planes, int rows, int 
   float2 *q = const_cast<float2 *>(p);
   return SpecLayout{q, (long long)rows * (L - 1), L - 1, q + planes * rows * (L - 1), rows, 1};
 }
-// Split layout of `planes` P x (P/2+1) Full FDC spectra with padded plane strides
-// (FDC_FULL_MAIN_PLANE / FDC_FULL_SIDE_PLANE bins), so that the same bin of
-// successive planes does not fall on one memory channel.
+// Layout of `planes` P x (P/2+1) Full FDC spectra.  Main block: row k of every plane
+// side by side, plane i's bins l < P/2 of row k at main[(k * planes + i) * R + l] with
+// R = FDC_FULL_ROW(P) (P/2 plus padding), so that one bin of all planes -- what the
+// per-bin channel contractions read -- lies within planes * R elements.  Side block
+// (column P/2): plane i's P bins at side[i * FDC_FULL_SIDE_PLANE(P) + k].
 inline SpecLayout full_spec_layout(const float2 *p, long long planes, int P) {
   float2 *q = const_cast<float2 *>(p);
-  const long long ms = FDC_FULL_MAIN_PLANE(P);
-  return SpecLayout{q, ms, P / 2, q + planes * ms, FDC_FULL_SIDE_PLANE(P), 1};
+  const long long R = FDC_FULL_ROW(P);
+  return SpecLayout{q, R, planes * R, q + (long long)P * planes * R, FDC_FULL_SIDE_PLANE(P), 1};
 }
 inline long long full_spec_elems(long long planes, int P) {
-  return planes * ((long long)FDC_FULL_MAIN_PLANE(P) + FDC_FULL_SIDE_PLANE(P));
+  return planes * ((long long)P * FDC_FULL_ROW(P) + FDC_FULL_SIDE_PLANE(P));
 }
 
 // Kernel timing hooks (no-ops unless enabled through the ABI).

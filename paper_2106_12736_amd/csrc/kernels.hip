@@ -281,9 +281,13 @@ __device__ __forceinline__ ColPtr split_col(const float2 *base, int planes, int 
 // Column DFTs (N, direction DIR) of `planes` split-layout N x (N/2+1) half spectra
 // with any plane strides (SpecLayout), in place or out of place (each workgroup
 // reads its columns whole before writing).
-__device__ __forceinline__ ColPtr layout_col(const SpecLayout &sl, int H, int plane, int l) {
-  if (l < H) return ColPtr{sl.main + (long long)plane * sl.ps + l, sl.rs};
-  return ColPtr{sl.side + (long long)plane * sl.sps, sl.srs};
+struct ColPtr64 {
+  float2 *p;
+  long long stride;
+};
+__device__ __forceinline__ ColPtr64 layout_col(const SpecLayout &sl, int H, int plane, int l) {
+  if (l < H) return ColPtr64{sl.main + (long long)plane * sl.ps + l, sl.rs};
+  return ColPtr64{sl.side + (long long)plane * sl.sps, sl.srs};
 }
 
 template <int N, int CT, int DIR>
@@ -294,13 +298,13 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft_split(SpecLayout
   stage_twiddles<N>(tw, threadIdx.x, CT * TPS);
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
-  const ColPtr ic = layout_col(in, L - 1, c.plane, c.l);
+  const ColPtr64 ic = layout_col(in, L - 1, c.plane, c.l);
   float2 v[E];
 #pragma unroll
   for (int m = 0; m < E; ++m) v[m] = ic.p[(t + TPS * m) * ic.stride];  // lanes past the end read a valid column
   fft_seq<N, DIR>(v, t, lds, s, CT, tw, 1);
   if (!c.ok) return;
-  const ColPtr oc = layout_col(out, L - 1, c.plane, c.l);
+  const ColPtr64 oc = layout_col(out, L - 1, c.plane, c.l);
 #pragma unroll
   for (int m = 0; m < E; ++m) oc.p[(t + TPS * m) * oc.stride] = v[m];
 }

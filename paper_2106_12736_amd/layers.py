@@ -187,9 +187,9 @@ class CicLayer(_LayerPlan):
         return (gx if need_gx else None), (gK if need_gk else None)
 
 
-def full_main_plane(P):
-    """FDC_FULL_MAIN_PLANE(P) of fdc.h: complex elements per main-block plane of a Full FDC spectrum."""
-    return P * (P // 2) + 64
+def full_row(P):
+    """FDC_FULL_ROW(P) of fdc.h: complex elements per plane row in a Full FDC spectrum's main block."""
+    return P // 2 + 16
 
 
 def full_side_plane(P):
@@ -215,14 +215,13 @@ class FullLayer(_LayerPlan):
         return torch.empty(self.saved_bytes // 8, dtype=torch.complex64, device=self.device)
 
     def saved_spectrum(self, saved):
-        """rfft2(x) held in a saved buffer, as a [B][Cin][P][P/2+1] tensor: columns
-        0..P/2-1 come from the main block, column P/2 from the block after it (both
-        with the padded plane strides FDC_FULL_MAIN_PLANE / FDC_FULL_SIDE_PLANE)."""
+        """rfft2(x) held in a saved buffer (layout in fdc_full_forward's header entry),
+        as a [B][Cin][P][P/2+1] tensor."""
         B, C, P = self.B, self.Cin, self.P
-        h = P // 2
-        ms, ss = full_main_plane(P), full_side_plane(P)
-        main = saved[: B * C * ms].view(B, C, ms)[..., : P * h].reshape(B, C, P, h)
-        side = saved[B * C * ms:].view(B, C, ss)[..., :P].reshape(B, C, P, 1)
+        h, R, SS = P // 2, full_row(P), full_side_plane(P)
+        n = B * C
+        main = saved[: P * n * R].view(P, B, C, R)[..., :h].permute(1, 2, 0, 3)
+        side = saved[P * n * R:].view(B, C, SS)[..., :P].reshape(B, C, P, 1)
         return torch.cat([main, side], dim=-1)
 
     def new_output(self):

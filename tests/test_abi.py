@@ -137,7 +137,7 @@ def test_full_plan_valid_sizes_reach_the_device():
         return
     f, sv, b = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
     assert _lib.status("fdc_layer_workspace_size", p, ctypes.byref(f), ctypes.byref(sv), ctypes.byref(b)) == FDC_OK
-    assert sv.value == 2 * 3 * (layers.full_main_plane(16) + layers.full_side_plane(16)) * 8
+    assert sv.value == 2 * 3 * (16 * layers.full_row(16) + layers.full_side_plane(16)) * 8
     o = ctypes.c_int()
     assert _lib.status("fdc_layer_output_size", p, ctypes.byref(o)) == FDC_OK
     assert o.value == 14
@@ -189,13 +189,13 @@ def test_destroyed_plan_is_refused():
 
 
 def test_full_plane_strides_match_header():
-    """The binding's copy of the saved-spectrum plane strides equals the header's macros."""
+    """The binding's copy of the saved-spectrum strides equals the header's macros."""
     import os
     import re
     hdr = open(os.path.join(os.path.dirname(__file__), "..", "include", "fdc.h")).read()
-    m = re.search(r"#define FDC_FULL_MAIN_PLANE\(P\) \(\(int64_t\)\(P\) \* \(\(P\) / 2\) \+ (\d+)\)", hdr)
+    m = re.search(r"#define FDC_FULL_ROW\(P\) \(\(int64_t\)\(P\) / 2 \+ (\d+)\)", hdr)
     s = re.search(r"#define FDC_FULL_SIDE_PLANE\(P\) \(\(int64_t\)\(P\) \+ (\d+)\)", hdr)
     assert m and s
     for P in (8, 224, 512):
-        assert layers.full_main_plane(P) == P * (P // 2) + int(m.group(1))
+        assert layers.full_row(P) == P // 2 + int(m.group(1))
         assert layers.full_side_plane(P) == P + int(s.group(1))
