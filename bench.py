@@ -147,7 +147,7 @@ def measured_traffic(kernel, workload):
 # CPU baseline: the float64 oracle on the host cores
 # ----------------------------------------------------------------------------
 
-def cpu_baseline(wl, data, min_seconds=10.0, max_reps=3):
+def cpu_baseline(wl, data, min_seconds=10.0, max_reps=50):
     import numpy as np
     from threadpoolctl import threadpool_info
 
@@ -266,7 +266,7 @@ class FullFdcRun:
             fdc.full_fdc_backward(g, xs, w, fdc.ARTIFACT_CROP)
             reps += 1
             el = time.perf_counter() - t0
-            if el >= min_seconds or reps >= 3:
+            if el >= min_seconds or reps >= 50:
                 break
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
         return {
