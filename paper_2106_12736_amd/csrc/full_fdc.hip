@@ -79,8 +79,7 @@ __device__ __forceinline__ void contract_run(const float2 *__restrict__ in, cons
 
   const int ba = min(b0 + mrow, B - 1);  // A operand row (batch)
   const float2 *arow = in + (long long)ba * KD * pst;
-  // operands of step (k0, t) are loaded one step ahead: the inputs one k-step ahead,
-  // the weights of the next 16-output tile while the current one runs
+  // the inputs and the weights of all four tiles are loaded one k-step ahead
   auto load_a = [&](int k0, float4 (&a)[2]) {
     const float4 *a4 = reinterpret_cast<const float4 *>(arow + (long long)min(k0 + kk, KD - 1) * pst);
     a[0] = a4[0], a[1] = a4[1];
@@ -90,23 +89,29 @@ __device__ __forceinline__ void contract_run(const float2 *__restrict__ in, cons
 #pragma unroll
     for (int i = 0; i < TP / 4; ++i) w[i] = w4[i];
   };
-  float4 an[2], wn[TP / 4];
+  float4 an[2], wn[4][TP / 4];
   load_a(0, an);
-  load_w(0, 0, wn);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) load_w(0, t, wn[t]);
   for (int k0 = 0; k0 < KDp; k0 += 4) {
     const float4 lo = an[0], hi = an[1];
-    if (k0 + 4 < KDp) load_a(k0 + 4, an);
+    float4 wc[4][TP / 4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int i = 0; i < TP / 4; ++i) wc[t][i] = wn[t][i];
+    if (k0 + 4 < KDp) {
+      load_a(k0 + 4, an);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) load_w(k0 + 4, t, wn[t]);
+    }
     const float ar[4] = {lo.x, lo.z, hi.x, hi.z}, ai[4] = {lo.y, lo.w, hi.y, hi.w};
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       float w[TP];
 #pragma unroll
       for (int i = 0; i < TP / 4; ++i)
-        w[4 * i] = wn[i].x, w[4 * i + 1] = wn[i].y, w[4 * i + 2] = wn[i].z, w[4 * i + 3] = wn[i].w;
-      if (t < 3)
-        load_w(k0, t + 1, wn);
-      else if (k0 + 4 < KDp)
-        load_w(k0 + 4, 0, wn);
+        w[4 * i] = wc[t][i].x, w[4 * i + 1] = wc[t][i].y, w[4 * i + 2] = wc[t][i].z, w[4 * i + 3] = wc[t][i].w;
       // the run-invariant half of the kernel spectrum
       float2 y[NK];
       if constexpr (!SIDE) {
@@ -115,8 +120,8 @@ __device__ __forceinline__ void contract_run(const float2 *__restrict__ in, cons
           float cx = w[b], cy = 0.f;
 #pragma unroll
           for (int a = 1; a < NK; ++a) {
-            cx += w[a * NK + b] * zs[a].x;
-            cy += w[a * NK + b] * zs[a].y;
+            cx = fmaf(w[a * NK + b], zs[a].x, cx);
+            cy = fmaf(w[a * NK + b], zs[a].y, cy);
           }
           y[b] = make_float2(cx, cy);
         }
@@ -136,11 +141,13 @@ __device__ __forceinline__ void contract_run(const float2 *__restrict__ in, cons
 #pragma unroll
         for (int i = 1; i < NK; ++i) {
           if constexpr (!SIDE) {
-            kr += zq[q][i].x * y[i].x - zq[q][i].y * y[i].y;
-            ki += zq[q][i].x * y[i].y + zq[q][i].y * y[i].x;
+            kr = fmaf(zq[q][i].x, y[i].x, kr);
+            kr = fmaf(-zq[q][i].y, y[i].y, kr);
+            ki = fmaf(zq[q][i].x, y[i].y, ki);
+            ki = fmaf(zq[q][i].y, y[i].x, ki);
           } else {
-            kr += zq[q][i].x * y[i].x;
-            ki += zq[q][i].y * y[i].x;
+            kr = fmaf(zq[q][i].x, y[i].x, kr);
+            ki = fmaf(zq[q][i].y, y[i].x, ki);
           }
         }
         // forward: re += Ar Kr - Ai Ki, im += Ar Ki + Ai Kr
@@ -245,11 +252,13 @@ __device__ __forceinline__ void gw_project_run(float (&gw)[4][NK * NK], const v4
         float ex = 0.f, ey = 0.f;  // E_b = sum_q D_q conj(v_qb)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          ex += dr[4 * r + q][j] * v[q][b].x + di[4 * r + q][j] * v[q][b].y;
-          ey += di[4 * r + q][j] * v[q][b].x - dr[4 * r + q][j] * v[q][b].y;
+          ex = fmaf(dr[4 * r + q][j], v[q][b].x, ex);
+          ex = fmaf(di[4 * r + q][j], v[q][b].y, ex);
+          ey = fmaf(di[4 * r + q][j], v[q][b].x, ey);
+          ey = fmaf(-dr[4 * r + q][j], v[q][b].y, ey);
         }
 #pragma unroll
-        for (int a = 0; a < NK; ++a) gw[j][a * NK + b] += ex * u[a].x + ey * u[a].y;
+        for (int a = 0; a < NK; ++a) gw[j][a * NK + b] = fmaf(ey, u[a].y, fmaf(ex, u[a].x, gw[j][a * NK + b]));
       }
   } else {
     const int k0 = 4 * (g - nmain);
@@ -264,7 +273,7 @@ __device__ __forceinline__ void gw_project_run(float (&gw)[4][NK * NK], const v4
       for (int a = 0; a < NK; ++a) {
         float f = 0.f;  // Re F_a = Re sum_q D_q conj(u_qa)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) f += dr[4 * r + q][j] * u[q][a].x + di[4 * r + q][j] * u[q][a].y;
+        for (int q = 0; q < 4; ++q) f = fmaf(di[4 * r + q][j], u[q][a].y, fmaf(dr[4 * r + q][j], u[q][a].x, f));
 #pragma unroll
         for (int b = 0; b < NK; ++b) gw[j][a * NK + b] += (b & 1) ? -f : f;
       }

@@ -339,33 +339,50 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fwd_crop(const float
 // Forward, second half: for every output channel o = c*J + j, the CIC product
 // (Eq. 5) of the pooled spectrum with kernel o at the kept bins, then the inverse
 // column DFT (M).  Xh [B*C][M rows], K [S][N][N/2+1] -> U [B*S][M rows].
-template <int N, int M, int CT>
+// A workgroup takes JW consecutive output channels of one input channel (groups =
+// B * C * J / JW of them): it loads the pooled column once, and the next kernel
+// column while the current one is transformed.
+// Output channels of one input channel handled by one workgroup of the CIC inverse
+// kernel (a divisor of J): the pooled input column is loaded once for all of them.
+constexpr int kCicJW = 4;
+
+template <int N, int M, int CT, int JW>
 __global__ __launch_bounds__(CT *FftCfg<M>::TPS) void k_col_cic_inv(const float2 *__restrict__ Xh,
                                                                    const float2 *__restrict__ K,
                                                                    float2 *__restrict__ U, int C, int J,
-                                                                   int planes) {
+                                                                   int groups) {
   using CM = FftCfg<M>;
   constexpr int L = M / 2 + 1, NF = N / 2 + 1, TPS = CM::TPS, E = CM::E;
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<M>();
   stage_twiddles<M>(tw, threadIdx.x, CT * TPS);
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
-  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
-  const int S = C * J;
-  const int b = c.plane / S;
-  const int o = c.plane - b * S;
-  const ColPtr xc = split_col<M, L>(Xh, planes / J, b * C + o / J, c.l);
-  const float2 *kcol = K + (long long)o * N * NF + c.l;
-  float2 z[E];
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, groups);
+  const int S = C * J, JB = J / JW;
+  const int bc = c.plane / JB;              // b * C + ci
+  const int o0 = (bc % C) * J + (c.plane - bc * JB) * JW;
+  const int b = bc / C;
+  const ColPtr xc = split_col<M, L>(Xh, groups / JB, bc, c.l);
+  float2 x[E], kn[E];
+  auto load_k = [&](int o) {
+    const float2 *kcol = K + (long long)o * N * NF + c.l;
 #pragma unroll
-  for (int m = 0; m < E; ++m) {
-    const int mrow = t + TPS * m;
-    z[m] = cmul(xc.p[mrow * xc.stride], kcol[kept_row<N, M>(mrow) * NF]);  // valid column on every lane
+    for (int m = 0; m < E; ++m) kn[m] = kcol[kept_row<N, M>(t + TPS * m) * NF];  // valid column on every lane
+  };
+#pragma unroll
+  for (int m = 0; m < E; ++m) x[m] = xc.p[(t + TPS * m) * xc.stride];
+  load_k(o0);
+  for (int jj = 0; jj < JW; ++jj) {
+    float2 z[E];
+#pragma unroll
+    for (int m = 0; m < E; ++m) z[m] = cmul(x[m], kn[m]);
+    if (jj + 1 < JW) load_k(o0 + jj + 1);  // the next kernel column loads while this one transforms
+    fft_seq<M, +1>(z, t, lds, s, CT, tw, 1);
+    if (c.ok) {
+      const ColPtr uc = split_col<M, L>(U, groups * JW, b * S + o0 + jj, c.l);  // B * S planes
+#pragma unroll
+      for (int m = 0; m < E; ++m) uc.p[(t + TPS * m) * uc.stride] = z[m];
+    }
   }
-  fft_seq<M, +1>(z, t, lds, s, CT, tw, 1);
-  if (!c.ok) return;
-  const ColPtr uc = split_col<M, L>(U, planes, c.plane, c.l);
-#pragma unroll
-  for (int m = 0; m < E; ++m) uc.p[(t + TPS * m) * uc.stride] = z[m];
 }
 
 // Geometry of the dK kernel: tiles of 8 columns (there are only S * L columns,
@@ -790,13 +807,29 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
     constexpr int CTN = col_ct_for(col_ct<N>(), L), CTM = col_ct_for(col_ct<M>(), L);
     static const std::string n1 = "col_fwd_crop_" + std::to_string(N) + "_" + std::to_string(M);
     static const std::string n2 = "col_cic_inv_" + std::to_string(N) + "_" + std::to_string(M);
-    const unsigned g1 = col_grid((long long)B * C, L, CTN), g2 = col_grid((long long)B * S, L, CTM);
-    if (g1 == 0 || g2 == 0) return;
+    const unsigned g1 = col_grid((long long)B * C, L, CTN);
+    if (g1 == 0) return;
     err = launch(n1.c_str(), k_col_fwd_crop<N, M, CTN>, g1, CTN * FftCfg<N>::TPS, (twiddle_lds_elems<N>() + lds_size<kColLds>(N * CTN)) * sizeof(float2),
                  s, T, Xh, B * C);
     if (err != hipSuccess) return;
-    err = launch(n2.c_str(), k_col_cic_inv<N, M, CTM>, g2, CTM * FftCfg<M>::TPS, (twiddle_lds_elems<M>() + lds_size<kColLds>(M * CTM)) * sizeof(float2),
-                 s, Xh, K, U, C, S / C, B * S);
+    const int J = S / C;
+    const int jw = J % kCicJW == 0 ? kCicJW : (J % 4 == 0 && kCicJW >= 4 ? 4 : (J % 2 == 0 && kCicJW >= 2 ? 2 : 1));
+    const long long groups = (long long)B * C * (J / jw);
+    const unsigned g2 = col_grid(groups, L, CTM);
+    if (g2 == 0) {
+      err = hipErrorInvalidValue;
+      return;
+    }
+    const size_t lds2 = (twiddle_lds_elems<M>() + lds_size<kColLds>(M * CTM)) * sizeof(float2);
+    auto go = [&](auto kern) {
+      err = launch(n2.c_str(), kern, g2, CTM * FftCfg<M>::TPS, lds2, s, Xh, K, U, C, J, (int)groups);
+    };
+    switch (jw) {
+      case 8: go(k_col_cic_inv<N, M, CTM, 8>); break;
+      case 4: go(k_col_cic_inv<N, M, CTM, 4>); break;
+      case 2: go(k_col_cic_inv<N, M, CTM, 2>); break;
+      default: go(k_col_cic_inv<N, M, CTM, 1>);
+    }
   });
   return err;
 }
