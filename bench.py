@@ -9,7 +9,10 @@ grayscale images, five CIC + FDP layers with channel fan-out
 (rfft2 -> CIC -> FDP -> irfft2) and every layer backward (kernel gradients of
 all layers, activation gradients of layers 2..5; the gradient of the input
 image is not part of a training step).  Inputs are resident in HBM before the
-timed region starts.
+timed region starts.  The step runs through the stack executor (fdc_cic_stack_*),
+which performs every layer's transforms but keeps the activations between layers
+in registers; --per-layer times the layer-by-layer calls instead (same results up
+to fp32 rounding).
 
 With --workload full_fdc_<P>_c<C> it times one Full FDC layer instead (16 images of
 P x P, C -> C channels, 3 x 3 weights, crop): forward, then dL/dx and dL/dw; the
@@ -68,6 +71,38 @@ def step_launches(wl, input_grad=False):
         if i > 0 or input_grad:
             out.append((f"col_bwd_gx_{N}_{M}", C64 * (B * S * M * L + S * M * L + B * C * N * L)))
             out.append((f"row_c2r_{N}", C64 * B * C * N * L + F32 * B * C * N * N))
+    return out
+
+
+def fused_step_launches(wl, input_grad=False):
+    """(kernel name, algorithmic bytes) of every launch of one step of the fused stack
+    executor: as step_launches, with each layer boundary's inverse rows and the next
+    layer's forward rows (and the backward's adjoint pair) in one kernel."""
+    out = []
+    n = wl.layers
+    for i in range(n):
+        B, C, S, N, M, L, _ = layer_dims(wl, i)
+        if i == 0:
+            out.append((f"row_r2c_{N}", F32 * B * C * N * N + C64 * B * C * N * L))
+        out.append((f"col_fwd_crop_{N}_{M}", C64 * (B * C * N * L + B * C * M * L)))
+        out.append((f"col_cic_inv_{N}_{M}", C64 * (B * C * M * L + S * M * L + B * S * M * L)))
+        if i + 1 < n:
+            _, _, _, N2, M2, L2, _ = layer_dims(wl, i + 1)
+            out.append((f"row_c2r_r2c_{M}", C64 * B * S * M * L + C64 * B * S * N2 * L2))
+        else:
+            out.append((f"row_c2r_{M}", C64 * B * S * M * L + F32 * B * S * M * M))
+    for i in reversed(range(n)):
+        B, C, S, N, M, L, NF = layer_dims(wl, i)
+        if i == n - 1:
+            out.append((f"row_r2c_{M}", F32 * B * S * M * M + C64 * B * S * M * L))
+        out.append((f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + S * N * NF)))
+        if i > 0 or input_grad:
+            out.append((f"col_bwd_gx_{N}_{M}", C64 * (B * S * M * L + S * M * L + B * C * N * L)))
+            if i > 0:
+                _, _, _, _, Mp, Lp, _ = layer_dims(wl, i - 1)
+                out.append((f"row_c2r_r2c_{N}", C64 * B * C * N * L + C64 * B * C * Mp * Lp))
+            else:
+                out.append((f"row_c2r_{N}", C64 * B * C * N * L + F32 * B * C * N * N))
     return out
 
 
@@ -180,7 +215,8 @@ def cpu_baseline(wl, data, min_seconds=10.0, max_reps=50):
 # ----------------------------------------------------------------------------
 
 class CicStackRun:
-    """The CIC + FDP stack step on preallocated buffers."""
+    """The CIC + FDP stack step on preallocated buffers: the fused stack executor
+    (fdc_cic_stack_*), or the layer-by-layer calls with --per-layer."""
 
     def __init__(self, wl, args, dev):
         import torch
@@ -191,11 +227,17 @@ class CicStackRun:
         self.x = torch.from_numpy(self.data.x).to(dev)
         self.Ks = [torch.from_numpy(k).to(dev) for k in self.data.kernels]
         self.g = torch.from_numpy(self.data.grad).to(dev)
-        self.stack = layers.CicStack(wl.batch, wl.sizes, wl.channels, device=dev)
+        self.per_layer = args.per_layer
+        if self.per_layer:
+            self.stack = layers.CicStack(wl.batch, wl.sizes, wl.channels, device=dev)
+            model = step_launches
+        else:
+            self.stack = layers.CicStackFused(wl.batch, wl.sizes, wl.channels, device=dev)
+            model = fused_step_launches
         self.gin = (torch.empty((wl.batch, wl.channels[0], wl.sizes[0], wl.sizes[0]), dtype=torch.float32,
                                 device=dev) if args.input_grad else None)
         self.input_grad = args.input_grad
-        self.launches = [(name, nbytes, "B") for name, nbytes in step_launches(wl, args.input_grad)]
+        self.launches = [(name, nbytes, "B") for name, nbytes in model(wl, args.input_grad)]
         self.api_bytes = step_api_bytes(wl, args.input_grad)
 
     def step(self):
@@ -203,12 +245,14 @@ class CicStackRun:
         self.stack.backward(self.g, self.Ks, input_grad=self.gin)
 
     def outputs(self):
-        return [self.stack.acts[-1]] + list(self.stack.gks)
+        last = self.stack.acts[-1] if self.per_layer else self.stack.out
+        return [last] + list(self.stack.gks)
 
     def config(self):
         wl = self.wl
         return {"workload": wl.name, "batch": wl.batch, "sizes": list(wl.sizes), "channels": list(wl.channels),
-                "input_grad": bool(self.input_grad)}
+                "input_grad": bool(self.input_grad),
+                "executor": "per_layer" if self.per_layer else "fused_stack"}
 
     def cpu_baseline(self):
         return cpu_baseline(self.wl, self.data)
@@ -290,6 +334,8 @@ def main():
                          "(full_fdc_512_c256, ...) workload")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
     ap.add_argument("--input-grad", action="store_true", help="CIC stack: also compute the input-image gradient")
+    ap.add_argument("--per-layer", action="store_true",
+                    help="CIC stack: run the layer-by-layer calls instead of the fused stack executor")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of HIP graph replays")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the timed region, run one plain streaming copy kernel (dst = src * 1) over "

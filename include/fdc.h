@@ -201,6 +201,38 @@ fdc_status fdc_full_backward(const fdc_layer_plan *plan, const float *gy, const 
                              hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
+/* Stack of CIC + FDP layers executed as one unit                            */
+/* ------------------------------------------------------------------------ */
+/* Layer i (0 <= i < layers) is the layer of fdc_cic_layer_plan_create with B
+ * images, C = channels[i], S = channels[i+1], N = sizes[i], M = sizes[i+1] and
+ * artifact NONE (sizes and channels: host arrays of layers + 1 entries, copied).
+ * The stack runs the same transforms as the layer calls in sequence (results agree
+ * to fp32 rounding), but the activations and activation gradients between layers
+ * are not written to memory: the inverse row transform of one layer and the
+ * forward row transform of the next run in one kernel on the same rows.  Plans
+ * are immutable host objects. */
+typedef struct fdc_stack_plan fdc_stack_plan;
+fdc_status fdc_cic_stack_plan_create(fdc_stack_plan **plan, int B, int layers, const int *sizes,
+                                     const int *channels);
+fdc_status fdc_cic_stack_plan_destroy(fdc_stack_plan *plan);
+/* Workspace bytes of one forward and one backward call. */
+fdc_status fdc_cic_stack_workspace_size(const fdc_stack_plan *plan, size_t *fwd_ws, size_t *bwd_ws);
+/* Bytes of layer `layer`'s saved buffer (as fdc_layer_workspace_size gives for that layer). */
+fdc_status fdc_cic_stack_saved_size(const fdc_stack_plan *plan, int layer, size_t *bytes);
+/* x [B][C_0][N_0][N_0] -> y [B][C_L][N_L][N_L] (L = layers).  K and saved are host
+ * arrays of `layers` device pointers: K[i] layer i's kernels [S][N][N/2+1]; saved[i]
+ * receives layer i's pooled input spectrum (layout of fdc_cic_layer_forward).
+ * `saved` may be NULL when no backward follows. */
+fdc_status fdc_cic_stack_forward(const fdc_stack_plan *plan, const float *x, const fdc_c64 *const *K, float *y,
+                                 void *const *saved, void *ws, size_t ws_bytes, hipStream_t stream);
+/* gy [B][C_L][N_L][N_L] -> gK[i] (host array of `layers` device pointers, each
+ * overwritten as fdc_cic_layer_backward writes it) and gx [B][C_0][N_0][N_0]
+ * (NULL: skipped). */
+fdc_status fdc_cic_stack_backward(const fdc_stack_plan *plan, const float *gy, const void *const *saved,
+                                  const fdc_c64 *const *K, float *gx, fdc_c64 *const *gK, void *ws,
+                                  size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
 /* Kernel timing (measurement support, off by default)                      */
 /* ------------------------------------------------------------------------ */
 /* While enabled, every kernel the library launches (only those named

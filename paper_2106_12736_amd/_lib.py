@@ -49,6 +49,12 @@ _SIGS = {
     "fdc_cic_layer_backward": [_P, _P, _P, _P, _P, _P, _P, _SZ, _P],
     "fdc_full_forward": [_P, _P, _P, _P, _P, _P, _SZ, _P],
     "fdc_full_backward": [_P, _P, _P, _P, _P, _P, _P, _SZ, _P],
+    "fdc_cic_stack_plan_create": [_PP, _I, _I, _P, _P],
+    "fdc_cic_stack_plan_destroy": [_P],
+    "fdc_cic_stack_workspace_size": [_P, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ)],
+    "fdc_cic_stack_saved_size": [_P, _I, ctypes.POINTER(_SZ)],
+    "fdc_cic_stack_forward": [_P, _P, _P, _P, _P, _P, _SZ, _P],
+    "fdc_cic_stack_backward": [_P, _P, _P, _P, _P, _P, _P, _SZ, _P],
     "fdc_kernel_timing_enable": [_I, ctypes.c_char_p],
     "fdc_kernel_timing_disable": [],
     "fdc_kernel_timing_report": [ctypes.c_char_p, _SZ],

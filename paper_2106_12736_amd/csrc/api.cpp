@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <algorithm>
 #include <map>
 #include <mutex>
 #include <new>
@@ -37,6 +38,7 @@ bool even_pos(long long v) { return v > 0 && v % 2 == 0; }
 
 constexpr uint32_t kFftMagic = 0xFDC0FF70u;
 constexpr uint32_t kLayerMagic = 0xFDC01A7Eu;
+constexpr uint32_t kStackMagic = 0xFDC05AC4u;
 
 }  // namespace
 
@@ -418,6 +420,183 @@ fdc_status fdc_cic_layer_backward(const fdc_layer_plan *p, const float *gy, cons
     return check_hip(fdc::launch_row_c2r(N, fdc::split_layout(V, (long long)B * C, N, L), gx, (long long)B * C, N,
                                          L, 1.f, 0.5f, id, (long long)N * N, s),
                      "layer backward dx rows");
+  }
+  return FDC_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Stack of CIC + FDP layers
+// ---------------------------------------------------------------------------
+struct fdc_stack_plan {
+  uint32_t magic;
+  int B, layers;
+  std::vector<int> N, C;  // sizes[0..layers], channels[0..layers]
+  size_t ws_a, ws_b, ws_x;  // complex elements: T / Tg buffer, U / V buffer, Xh when `saved` is NULL
+  std::vector<size_t> saved;
+};
+
+namespace {
+// per-layer geometry: planes and bins of the four spectra of layer i
+struct StackLayer {
+  int N, M, L, C, S;
+};
+StackLayer stack_layer(const fdc_stack_plan *p, int i) {
+  return StackLayer{p->N[i], p->N[i + 1], p->N[i + 1] / 2 + 1, p->C[i], p->C[i + 1]};
+}
+fdc_status check_stack_plan(const fdc_stack_plan *p) {
+  if (p == nullptr || p->magic != kStackMagic) return fail(FDC_EINVAL, "invalid or destroyed stack plan");
+  return FDC_OK;
+}
+}  // namespace
+
+fdc_status fdc_cic_stack_plan_create(fdc_stack_plan **plan, int B, int layers, const int *sizes, const int *channels) {
+  if (plan == nullptr) return fail(FDC_EINVAL, "plan out-pointer is NULL");
+  *plan = nullptr;
+  if (B < 1 || layers < 1) return fail(FDC_EINVAL, "B and layers must be >= 1 (B=%d layers=%d)", B, layers);
+  if (!sizes || !channels) return fail(FDC_EINVAL, "sizes or channels is NULL");
+  for (int i = 0; i < layers; ++i) {
+    const int N = sizes[i], M = sizes[i + 1], C = channels[i], S = channels[i + 1];
+    if (C < 1 || S < 1 || S % C) return fail(FDC_EINVAL, "layer %d: channels %d -> %d (need S mod C == 0)", i, C, S);
+    if (!even_pos(N) || !even_pos(M) || M > N)
+      return fail(FDC_EINVAL, "layer %d: sizes %d -> %d (even, positive, non-increasing)", i, N, M);
+    if (!fdc::cic_pair_supported(N, M))
+      return fail(FDC_EUNSUPPORTED, "layer %d: size %d -> %d not supported", i, N, M);
+  }
+  auto *p = new (std::nothrow) fdc_stack_plan{};
+  if (p == nullptr) return fail(FDC_EINVAL, "out of host memory");
+  p->magic = kStackMagic;
+  p->B = B, p->layers = layers;
+  p->N.assign(sizes, sizes + layers + 1);
+  p->C.assign(channels, channels + layers + 1);
+  for (int i = 0; i < layers; ++i) {
+    const StackLayer g = stack_layer(p, i);
+    const size_t t = (size_t)B * g.C * g.N * g.L, u = (size_t)B * g.S * g.M * g.L, x = (size_t)B * g.C * g.M * g.L;
+    // forward: T (in A) and U (in B); backward: Tg = [B S M L] (in A) and V = [B C N L] (in B)
+    p->ws_a = std::max(p->ws_a, std::max(t, u));
+    p->ws_b = std::max(p->ws_b, std::max(u, t));
+    p->ws_x = std::max(p->ws_x, x);
+    p->saved.push_back(x * sizeof(fdc_c64));
+  }
+  *plan = p;
+  return FDC_OK;
+}
+
+fdc_status fdc_cic_stack_plan_destroy(fdc_stack_plan *plan) {
+  if (plan == nullptr) return FDC_OK;
+  if (plan->magic != kStackMagic) return fail(FDC_EINVAL, "invalid or destroyed stack plan");
+  plan->magic = 0;
+  delete plan;
+  return FDC_OK;
+}
+
+fdc_status fdc_cic_stack_workspace_size(const fdc_stack_plan *p, size_t *fwd_ws, size_t *bwd_ws) {
+  if (fdc_status st = check_stack_plan(p)) return st;
+  if (fwd_ws) *fwd_ws = (p->ws_a + p->ws_b + p->ws_x) * sizeof(fdc_c64);
+  if (bwd_ws) *bwd_ws = (p->ws_a + p->ws_b) * sizeof(fdc_c64);
+  return FDC_OK;
+}
+
+fdc_status fdc_cic_stack_saved_size(const fdc_stack_plan *p, int layer, size_t *bytes) {
+  if (fdc_status st = check_stack_plan(p)) return st;
+  if (layer < 0 || layer >= p->layers) return fail(FDC_EINVAL, "layer %d outside [0, %d)", layer, p->layers);
+  if (bytes == nullptr) return fail(FDC_EINVAL, "bytes is NULL");
+  *bytes = p->saved[layer];
+  return FDC_OK;
+}
+
+fdc_status fdc_cic_stack_forward(const fdc_stack_plan *p, const float *x, const fdc_c64 *const *K, float *y,
+                                 void *const *saved, void *ws, size_t ws_bytes, hipStream_t s) {
+  if (fdc_status st = check_stack_plan(p)) return st;
+  if (!x || !K || !y) return fail(FDC_EINVAL, "NULL tensor");
+  for (int i = 0; i < p->layers; ++i)
+    if (!K[i] || (saved && !saved[i])) return fail(FDC_EINVAL, "layer %d: NULL kernel or saved buffer", i);
+  if (fdc_status st = check_ws(ws, ws_bytes, (p->ws_a + p->ws_b + p->ws_x) * sizeof(fdc_c64))) return st;
+  const int B = p->B;
+  auto *A = reinterpret_cast<float2 *>(ws);
+  auto *U = A + p->ws_a;
+  auto *Xw = U + p->ws_b;
+  for (int i = 0; i < p->layers; ++i) {
+    const StackLayer g = stack_layer(p, i);
+    const long long cin = (long long)B * g.C, cout = (long long)B * g.S;
+    auto *Xh = saved ? reinterpret_cast<float2 *>(saved[i]) : Xw;
+    if (i == 0) {
+      ImgView id{0, 0, g.N, g.N};
+      if (fdc_status st = check_hip(fdc::launch_row_r2c(g.N, x, fdc::split_layout(A, cin, g.N, g.L), cin, g.N, id,
+                                                        (long long)g.N * g.N, g.L, 1.f, 1.f, s),
+                                    "stack forward rows"))
+        return st;
+    }
+    if (fdc_status st = check_hip(fdc::launch_col_fwd_cic(g.N, g.M, A, reinterpret_cast<const float2 *>(K[i]), U, Xh,
+                                                          B, g.C, g.S, s),
+                                  "stack forward columns"))
+      return st;
+    const float inv = 1.f / ((float)g.M * (float)g.M);
+    if (i + 1 < p->layers) {
+      // this layer's inverse rows and the next layer's forward rows on the same rows
+      const StackLayer h = stack_layer(p, i + 1);
+      if (fdc_status st = check_hip(fdc::launch_row_c2r_r2c(g.M, fdc::split_layout(U, cout, g.M, g.L), g.L, inv, 1.f,
+                                                            fdc::split_layout(A, cout, h.N, h.L), h.L, 1.f, 1.f,
+                                                            cout, g.M, s),
+                                    "stack forward boundary rows"))
+        return st;
+    } else {
+      ImgView id{0, 0, g.M, g.M};
+      if (fdc_status st = check_hip(fdc::launch_row_c2r(g.M, fdc::split_layout(U, cout, g.M, g.L), y, cout, g.M, g.L,
+                                                        inv, 1.f, id, (long long)g.M * g.M, s),
+                                    "stack forward inverse rows"))
+        return st;
+    }
+  }
+  return FDC_OK;
+}
+
+fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, const void *const *saved,
+                                  const fdc_c64 *const *K, float *gx, fdc_c64 *const *gK, void *ws, size_t ws_bytes,
+                                  hipStream_t s) {
+  if (fdc_status st = check_stack_plan(p)) return st;
+  if (!gy || !saved || !K || !gK) return fail(FDC_EINVAL, "NULL tensor or array");
+  for (int i = 0; i < p->layers; ++i)
+    if (!saved[i] || !K[i] || !gK[i]) return fail(FDC_EINVAL, "layer %d: NULL saved, kernel or dK", i);
+  if (fdc_status st = check_ws(ws, ws_bytes, (p->ws_a + p->ws_b) * sizeof(fdc_c64))) return st;
+  const int B = p->B;
+  auto *Tg = reinterpret_cast<float2 *>(ws);
+  auto *V = Tg + p->ws_a;
+  for (int i = p->layers - 1; i >= 0; --i) {
+    const StackLayer g = stack_layer(p, i);
+    const long long cin = (long long)B * g.C, cout = (long long)B * g.S;
+    const float inv = 1.f / ((float)g.M * (float)g.M);
+    if (i == p->layers - 1) {
+      ImgView id{0, 0, g.M, g.M};
+      if (fdc_status st = check_hip(fdc::launch_row_r2c(g.M, gy, fdc::split_layout(Tg, cout, g.M, g.L), cout, g.M, id,
+                                                        (long long)g.M * g.M, g.L, inv, 2.f, s),
+                                    "stack backward rows"))
+        return st;
+    }
+    if (fdc_status st = check_hip(fdc::launch_col_bwd_gk(g.N, g.M, Tg, reinterpret_cast<const float2 *>(saved[i]),
+                                                         reinterpret_cast<float2 *>(gK[i]), B, g.C, g.S, s),
+                                  "stack backward dK"))
+      return st;
+    if (i == 0 && !gx) break;
+    if (fdc_status st = check_hip(fdc::launch_col_bwd_gx(g.N, g.M, Tg, reinterpret_cast<const float2 *>(K[i]), V, B,
+                                                         g.C, g.S, s),
+                                  "stack backward dx columns"))
+      return st;
+    if (i > 0) {
+      // this layer's adjoint inverse rows and the previous layer's upstream-gradient rows
+      const StackLayer h = stack_layer(p, i - 1);
+      const float hinv = 1.f / ((float)h.M * (float)h.M);
+      if (fdc_status st = check_hip(fdc::launch_row_c2r_r2c(g.N, fdc::split_layout(V, cin, g.N, g.L), g.L, 1.f, 0.5f,
+                                                            fdc::split_layout(Tg, cin, h.M, h.L), h.L, hinv, 2.f,
+                                                            cin, g.N, s),
+                                    "stack backward boundary rows"))
+        return st;
+    } else {
+      ImgView id{0, 0, g.N, g.N};
+      if (fdc_status st = check_hip(fdc::launch_row_c2r(g.N, fdc::split_layout(V, cin, g.N, g.L), gx, cin, g.N, g.L,
+                                                        1.f, 0.5f, id, (long long)g.N * g.N, s),
+                                    "stack backward dx rows"))
+        return st;
+    }
   }
   return FDC_OK;
 }

@@ -78,6 +78,11 @@ hipError_t launch_row_r2c(int n, const float *x, SpecLayout out, long long plane
                           ImgView in_view, long long in_plane_stride, int L, float alpha, float beta, hipStream_t s);
 hipError_t launch_row_c2r(int n, SpecLayout in, float *y, long long planes, int rows_per_plane, int L, float alpha,
                           float beta, ImgView out_view, long long out_plane_stride, hipStream_t s);
+// Inverse then forward real row transforms of the same rows (a boundary between two
+// stacked layers): launch_row_c2r(in, Lin, a1, b1) followed by launch_row_r2c(out,
+// Lout, a2, b2) with the real rows kept in registers.
+hipError_t launch_row_c2r_r2c(int n, SpecLayout in, int Lin, float a1, float b1, SpecLayout out, int Lout, float a2,
+                              float b2, long long planes, int rows_per_plane, hipStream_t s);
 
 // Column DFTs of length n over the first `L` columns of row-major [planes][n][ld] complex
 // data (in place allowed).

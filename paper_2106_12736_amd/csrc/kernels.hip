@@ -180,6 +180,83 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
   }
 }
 
+// Inverse real row transform followed by the forward real row transform of the same
+// rows, for a boundary between two layers of a stack: in (Lin bins per row, weights
+// a1 at l = 0 and N/2, a1 * b1 elsewhere, real-part semantics as k_row_c2r) ->
+// the two real rows of each pair, kept in registers -> out (Lout bins, weights as
+// k_row_r2c with a2, b2).  The same rows, pairing and arithmetic as k_row_c2r
+// followed by k_row_r2c, without writing the real rows to memory.
+template <int N, int SPW>
+__global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r_r2c(SpecLayout in, int Lin, float a1, float b1,
+                                                                    SpecLayout out, int Lout, float a2, float b2,
+                                                                    long long npairs, int rows_per_plane) {
+  using Cfg = FftCfg<N>;
+  constexpr int TPS = Cfg::TPS, E = Cfg::E;
+  static_assert(TPS <= 64, "a row sequence must fit in one wavefront");
+  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
+  stage_twiddles<N>(tw, threadIdx.x, SPW * TPS);
+  const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
+  long long pair = (long long)xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
+  const bool active = pair < npairs;
+  if (!active) pair = npairs - 1;
+  const long long row0 = 2 * pair;
+  const long long plane = row0 / rows_per_plane;
+  const int r0 = (int)(row0 - plane * rows_per_plane);
+  const float2 *ia = in.main + plane * in.ps + (long long)r0 * in.rs;
+  const float2 *ib = ia + in.rs;
+  const float2 *sa = in.side + plane * in.sps + (long long)r0 * in.srs;
+
+  float2 v[E];
+#pragma unroll
+  for (int m = 0; m < E; ++m) {
+    const int k = t + TPS * m;
+    const bool upper = 2 * k > N;
+    const int kk = upper ? N - k : k;
+    const bool in_main = kk < Lin - 1;
+    const float2 *pa = in_main ? ia + kk : sa;
+    const float2 *pb = in_main ? ib + kk : sa + in.srs;
+    float2 a = *pa, b = *pb;
+    const bool edge = (kk == 0 || 2 * kk == N);
+    const float wgt = kk < Lin ? (edge ? a1 : a1 * b1) : 0.f;
+    a = cscale(a, wgt);
+    b = cscale(b, wgt);
+    if (edge) {
+      a.y = 0.f;
+      b.y = 0.f;
+    }
+    if (upper) {
+      a.y = -a.y;
+      b.y = -b.y;
+    }
+    v[m] = make_float2(a.x - b.y, a.y + b.x);
+  }
+  fft_seq<N, +1, true, true, kRowLds>(v, t, lds, s * N, 1, tw, 1);
+  // v[m] = (row r0, row r0 + 1) at column t + TPS m: the packed input of the forward transform
+  fft_seq<N, -1, true, true, kRowLds>(v, t, lds, s * N, 1, tw, 1);
+  lds_barrier<true>();
+#pragma unroll
+  for (int m = 0; m < E; ++m) lds[lds_phys<kRowLds>(s * N + t + TPS * m)] = v[m];
+  lds_barrier<true>();
+  if (!active) return;
+  float2 *oa = out.main + plane * out.ps + (long long)r0 * out.rs;
+  float2 *ob = oa + out.rs;
+  for (int k = t; k < Lout; k += TPS) {
+    const float2 zk = lds[lds_phys<kRowLds>(s * N + k)];
+    const float2 zn = lds[lds_phys<kRowLds>(s * N + (k == 0 ? 0 : N - k))];
+    const float wgt = 0.5f * bin_weight(k, N, a2, b2);
+    const float2 A = make_float2((zk.x + zn.x) * wgt, (zk.y - zn.y) * wgt);
+    const float2 Bv = make_float2((zk.y + zn.y) * wgt, (zn.x - zk.x) * wgt);
+    if (k < Lout - 1) {
+      oa[k] = A;
+      ob[k] = Bv;
+    } else {
+      float2 *so = out.side + plane * out.sps + (long long)r0 * out.srs;
+      so[0] = A;
+      so[out.srs] = Bv;
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // column transforms
 //
@@ -747,6 +824,22 @@ hipError_t launch_row_c2r(int n, SpecLayout in, float *y, long long planes, int 
         err = launch(nm.c_str(), k_row_c2r<N, SPW, 2>, grid, SPW * FftCfg<N>::TPS, lds, s, in, y, npairs,
                      rows_per_plane, L, alpha, beta, out_view, out_plane_stride);
     }
+  });
+  return err;
+}
+
+hipError_t launch_row_c2r_r2c(int n, SpecLayout in, int Lin, float a1, float b1, SpecLayout out, int Lout, float a2,
+                              float b2, long long planes, int rows_per_plane, hipStream_t s) {
+  hipError_t err = hipErrorInvalidValue;
+  dispatch_n(n, [&](auto nc) {
+    constexpr int N = decltype(nc)::value;
+    constexpr int SPW = row_spw<N>();
+    const long long npairs = planes * rows_per_plane / 2;
+    const unsigned grid = (unsigned)((npairs + SPW - 1) / SPW);
+    const size_t lds = (twiddle_lds_elems<N>() + lds_size<kRowLds>(SPW * N)) * sizeof(float2);
+    static const std::string nm = "row_c2r_r2c_" + std::to_string(N);
+    err = launch(nm.c_str(), k_row_c2r_r2c<N, SPW>, grid, SPW * FftCfg<N>::TPS, lds, s, in, Lin, a1, b1, out, Lout,
+                 a2, b2, npairs, rows_per_plane);
   });
   return err;
 }

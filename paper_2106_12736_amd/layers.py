@@ -283,3 +283,67 @@ class CicStack:
                            gK=self.gks[i])
             g = gx
         return self.gks
+
+
+def _ptr_array(tensors):
+    arr = (ctypes.c_void_p * len(tensors))()
+    for i, t in enumerate(tensors):
+        arr[i] = t.data_ptr() if t is not None else None
+    return arr
+
+
+class CicStackFused:
+    """The same stack as CicStack run through fdc_cic_stack_*: one plan, the
+    activations between layers never written to memory.  Kernel gradients, saved
+    spectra, the last activation and workspaces are preallocated."""
+
+    def __init__(self, batch, sizes, channels, device="cuda"):
+        self.batch, self.sizes, self.channels = batch, tuple(sizes), tuple(channels)
+        self.layers = len(sizes) - 1
+        self.device = torch.device(device)
+        self._sizes = (ctypes.c_int * len(sizes))(*sizes)
+        self._chans = (ctypes.c_int * len(channels))(*channels)
+        self._p = ctypes.c_void_p()
+        call("fdc_cic_stack_plan_create", ctypes.byref(self._p), batch, self.layers, self._sizes, self._chans)
+        f, b = ctypes.c_size_t(), ctypes.c_size_t()
+        call("fdc_cic_stack_workspace_size", self._p, ctypes.byref(f), ctypes.byref(b))
+        self.fwd_ws = _workspace(f.value, self.device)
+        self.bwd_ws = _workspace(b.value, self.device)
+        self.saved = []
+        for i in range(self.layers):
+            n = ctypes.c_size_t()
+            call("fdc_cic_stack_saved_size", self._p, i, ctypes.byref(n))
+            self.saved.append(torch.empty(n.value // 8, dtype=torch.complex64, device=self.device))
+        self.out = torch.empty((batch, channels[-1], sizes[-1], sizes[-1]), dtype=torch.float32, device=self.device)
+        self.gks = [torch.empty((channels[i + 1], sizes[i], sizes[i] // 2 + 1), dtype=torch.complex64,
+                                device=self.device) for i in range(self.layers)]
+        self._saved_arr = _ptr_array(self.saved)
+        self._gk_arr = _ptr_array(self.gks)
+
+    def __del__(self):
+        if getattr(self, "_p", None) and _lib._lib is not None:
+            _lib.lib().fdc_cic_stack_plan_destroy(self._p)
+
+    def _kernels(self, kernels):
+        if len(kernels) != self.layers:
+            raise ValueError(f"{self.layers} kernel tensors expected")
+        for i, K in enumerate(kernels):
+            _check(K, torch.complex64, (self.channels[i + 1], self.sizes[i], self.sizes[i] // 2 + 1), f"K[{i}]")
+        return _ptr_array(kernels)
+
+    def forward(self, x, kernels):
+        _check(x, torch.float32, (self.batch, self.channels[0], self.sizes[0], self.sizes[0]), "x")
+        call("fdc_cic_stack_forward", self._p, _ptr(x), self._kernels(kernels), _ptr(self.out), self._saved_arr,
+             _ptr(self.fwd_ws), self.fwd_ws.numel(), _stream())
+        return self.out
+
+    def backward(self, gy, kernels, input_grad=None):
+        """Kernel gradients of every layer (and the input gradient into `input_grad` if given)."""
+        _check(gy, torch.float32, tuple(self.out.shape), "gy")
+        if input_grad is not None:
+            _check(input_grad, torch.float32, (self.batch, self.channels[0], self.sizes[0], self.sizes[0]),
+                   "input_grad")
+        call("fdc_cic_stack_backward", self._p, _ptr(gy), self._saved_arr, self._kernels(kernels), _ptr(input_grad),
+             self._gk_arr, _ptr(self.bwd_ws), self.bwd_ws.numel(), _stream())
+        return self.gks
+

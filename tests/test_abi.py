@@ -199,3 +199,61 @@ def test_full_plane_strides_match_header():
     for P in (8, 224, 512):
         assert layers.full_row(P) == P // 2 + int(m.group(1))
         assert layers.full_side_plane(P) == P + int(s.group(1))
+
+
+def _stack(B, sizes, chans):
+    p = ctypes.c_void_p()
+    st = _lib.status("fdc_cic_stack_plan_create", ctypes.byref(p), B, len(sizes) - 1,
+                     (ctypes.c_int * len(sizes))(*sizes), (ctypes.c_int * len(chans))(*chans))
+    return st, p
+
+
+@pytest.mark.parametrize("B,sizes,chans,expect", [
+    (8, (64, 32, 16), (1, 4, 8), FDC_OK),
+    (0, (64, 32), (1, 4), FDC_EINVAL),
+    (2, (64,), (1,), FDC_EINVAL),              # no layer
+    (2, (64, 32), (2, 3), FDC_EINVAL),         # S mod C != 0
+    (2, (32, 64), (1, 2), FDC_EINVAL),         # growing size
+    (2, (64, 30), (1, 2), FDC_EUNSUPPORTED),   # a valid FDP size, but not a pooling the fused layer has
+    (2, (2048, 1024), (1, 2), FDC_EUNSUPPORTED),
+])
+def test_stack_plan_validation(B, sizes, chans, expect):
+    st, p = _stack(B, sizes, chans)
+    assert st == expect
+    if st == FDC_OK:
+        assert _lib.status("fdc_cic_stack_plan_destroy", p) == FDC_OK
+
+
+def test_stack_plan_sizes_and_argument_checks():
+    """Saved sizes equal the layer plans'; workspaces cover every layer's spectra;
+    bad arguments are refused before anything is enqueued."""
+    B, sizes, chans = 4, (256, 128, 64), (1, 8, 16)
+    st, p = _stack(B, sizes, chans)
+    assert st == FDC_OK
+    f, b = ctypes.c_size_t(), ctypes.c_size_t()
+    assert _lib.status("fdc_cic_stack_workspace_size", p, ctypes.byref(f), ctypes.byref(b)) == FDC_OK
+    tmax = 0
+    for i in range(2):
+        N, M, C, S = sizes[i], sizes[i + 1], chans[i], chans[i + 1]
+        L = M // 2 + 1
+        tmax = max(tmax, B * C * N * L, B * S * M * L)
+        n = ctypes.c_size_t()
+        assert _lib.status("fdc_cic_stack_saved_size", p, i, ctypes.byref(n)) == FDC_OK
+        lp = ctypes.c_void_p()
+        assert _lib.status("fdc_cic_layer_plan_create", ctypes.byref(lp), B, C, S, N, M, 0, 1) == FDC_OK
+        sv = ctypes.c_size_t()
+        assert _lib.status("fdc_layer_workspace_size", lp, None, ctypes.byref(sv), None) == FDC_OK
+        assert n.value == sv.value
+        assert _lib.status("fdc_layer_plan_destroy", lp) == FDC_OK
+    assert b.value == 2 * tmax * 8 and f.value >= b.value
+    n = ctypes.c_size_t()
+    assert _lib.status("fdc_cic_stack_saved_size", p, 2, ctypes.byref(n)) == FDC_EINVAL
+    d = ctypes.c_void_p(0x1000)
+    arr = (ctypes.c_void_p * 2)(0x1000, 0x1000)
+    null_arr = (ctypes.c_void_p * 2)(0x1000, None)
+    assert _lib.status("fdc_cic_stack_forward", p, d, null_arr, d, None, d, 1 << 40, None) == FDC_EINVAL
+    assert _lib.status("fdc_cic_stack_forward", p, d, arr, d, None, d, 8, None) == FDC_EWORKSPACE
+    assert _lib.status("fdc_cic_stack_backward", p, d, arr, arr, None, null_arr, d, 1 << 40, None) == FDC_EINVAL
+    assert _lib.status("fdc_cic_stack_backward", p, d, arr, arr, None, arr, d, 8, None) == FDC_EWORKSPACE
+    assert _lib.status("fdc_cic_stack_plan_destroy", p) == FDC_OK
+    assert _lib.status("fdc_cic_stack_forward", p, d, arr, d, None, d, 1 << 40, None) == FDC_EINVAL

@@ -1,0 +1,88 @@
+"""GPU tests of the fused stack executor (fdc_cic_stack_*).  It runs the same
+kernels on the same rows as the layer-by-layer calls, with the activations between
+layers kept in registers; the compiler may contract multiply-adds differently inside
+the fused boundary kernel, so the two agree to fp32 rounding (not bit for bit).  Every
+CIC workload runs at full size, including the input-image gradient: against the
+layer-by-layer path at a tight tolerance and against the oracle at the parity bar;
+the fused step also replays identically as a HIP graph."""
+
+import numpy as np
+import pytest
+import torch
+
+from _parity import assert_parity, to_np
+from oracle import fdc
+from paper_2106_12736_amd import inputs, layers
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_both(wl):
+    d = inputs.make_cic_stack(wl)
+    x = torch.from_numpy(d.x).cuda()
+    Ks = [torch.from_numpy(k).cuda() for k in d.kernels]
+    g = torch.from_numpy(d.grad).cuda()
+    ref = layers.CicStack(wl.batch, wl.sizes, wl.channels)
+    gin_ref = torch.empty_like(x)
+    ref.forward(x, Ks)
+    ref.backward(g, Ks, input_grad=gin_ref)
+    fused = layers.CicStackFused(wl.batch, wl.sizes, wl.channels)
+    gin = torch.empty_like(x)
+    fused.forward(x, Ks)
+    fused.backward(g, Ks, input_grad=gin)
+    torch.cuda.synchronize()
+    return d, ref, gin_ref, fused, gin
+
+
+def _close(got, ref, name, rel=1e-6):
+    d = (got - ref).abs()
+    r = (d.norm() / ref.norm()).item()
+    print(f"  {name}: max |d| {d.max().item():.3e}, rel-L2 {r:.3e}", flush=True)
+    assert r <= rel, f"{name}: rel-L2 {r:.3e} against the layer-by-layer path"
+
+
+@pytest.mark.parametrize("wl", inputs.CIC_WORKLOADS, ids=lambda w: w.name)
+def test_fused_stack_matches_layer_calls_and_oracle(wl):
+    print(f"fused stack {wl.name}", flush=True)
+    d, ref, gin_ref, fused, gin = _run_both(wl)
+    _close(fused.out, ref.acts[-1], "y")
+    for i in range(wl.layers):
+        _close(fused.saved[i], ref.saved[i], f"saved[{i}]")
+        _close(fused.gks[i], ref.gks[i], f"dK[{i}]")
+    _close(gin, gin_ref, "gx")
+    x64 = d.x.astype(np.float64)
+    kd = [k.astype(np.complex128) for k in d.kernels]
+    y_ref, saved = fdc.cic_stack_forward(x64, kd, wl.sizes)
+    gks_ref, gx_ref = fdc.cic_stack_backward(d.grad.astype(np.float64), saved, kd, wl.sizes, want_input_grad=True)
+    assert_parity(to_np(fused.out), y_ref, "y")
+    for i in range(wl.layers):
+        assert_parity(to_np(fused.gks[i]), gks_ref[i], f"dK[{i}]")
+    assert_parity(to_np(gin), gx_ref, "gx")
+
+
+def test_fused_stack_graph_replays():
+    wl = inputs.STACK512
+    d = inputs.make_cic_stack(wl)
+    x = torch.from_numpy(d.x).cuda()
+    Ks = [torch.from_numpy(k).cuda() for k in d.kernels]
+    g = torch.from_numpy(d.grad).cuda()
+    st = layers.CicStackFused(wl.batch, wl.sizes, wl.channels)
+
+    def step():
+        st.forward(x, Ks)
+        st.backward(g, Ks)
+
+    step()
+    torch.cuda.synchronize()
+    ref = [st.out.clone()] + [k.clone() for k in st.gks]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for rep in range(3):
+        torch.randn(1 << 20, device="cuda").mul_(2.0).sum().item()
+        for t in [st.out] + st.gks:
+            t.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(zip(ref, [st.out] + st.gks)):
+            assert torch.equal(a, b), f"replay {rep}: output {i}"
