@@ -228,6 +228,36 @@ def cic_spectral_chain(x, kernels, sizes):
 
 
 # ----------------------------------------------------------------------------
+# FDCNN data flow (section 2.5.1): one RFFT before all FDC/FDP layers, one IRFFT after
+# ----------------------------------------------------------------------------
+
+def cic_chain_forward(x, kernels, sizes):
+    """The FDCNN of section 2.5.1: RFFT once, then every FDC (CIC, Eq. 5) and FDP layer
+    on spectra (Algorithm 1's spectral in/out form), then IRFFT once.  No projection
+    between layers.  Returns (y, saved) with saved[i] = layer i's input spectrum."""
+    spec = dft.rfft2(x)
+    saved = []
+    for i, k in enumerate(kernels):
+        saved.append(spec)
+        m = sizes[i + 1]
+        spec = fdp(cic(spec, k), m, m)
+    m = sizes[-1]
+    return dft.irfft2(spec, m, m), saved
+
+
+def cic_chain_backward(gy, saved, kernels, sizes, want_input_grad=False):
+    """Reverse of ``cic_chain_forward``: (list of dL/dK per layer, dL/dx or None)."""
+    g = dft.irfft2_adjoint(gy)
+    gks = [None] * len(kernels)
+    for i in reversed(range(len(kernels))):
+        n = sizes[i]
+        gz = fdp_backward(g, n, n)
+        g, gks[i] = cic_backward(gz, saved[i], kernels[i])
+    gx = dft.rfft2_adjoint(g, sizes[0], sizes[0]) if want_input_grad else None
+    return gks, gx
+
+
+# ----------------------------------------------------------------------------
 # Full FDC (Algorithm 2) with the convolution-over-volume sum of Eq. 2 per bin
 # ----------------------------------------------------------------------------
 

@@ -332,3 +332,62 @@ def test_stack_gradients_finite_difference():
     xp[1, 0, 3, 5] += eps
     xm[1, 0, 3, 5] -= eps
     assert abs((loss(Ks, xp) - loss(Ks, xm)) / (2 * eps) - gx[1, 0, 3, 5]) < 1e-7
+
+
+# ---------------------------------------------------------------------------- FDCNN chain
+def test_chain_single_layer_is_the_layer():
+    x = RNG.standard_normal((2, 1, 16, 16))
+    K = [0.1 * _rand_complex((3, 16, 9))]
+    y, _ = fdc.cic_chain_forward(x, K, (16, 8))
+    ref, _ = fdc.cic_fdp_layer_forward(x, K[0], 8)
+    np.testing.assert_allclose(y, ref, atol=1e-13)
+
+
+def test_chain_of_a_cosine_is_a_cosine():
+    """A single frequency (p, q) inside every pooled band passes every layer as one
+    bin: the output of channel o is (2 / M^2) |V| cos(2 pi (p h + q w) / M + arg V) with
+    V = (N0^2 / 2) times the product of each layer's kernel at that frequency, read at
+    (p mod N_i, q) for the channel o's ancestor in layer i (CIC: channel o of a layer
+    reads input channel o // J)."""
+    sizes, chans = (32, 16, 8), (1, 2, 4)
+    n0, m = sizes[0], sizes[-1]
+    p, q = 3, 2
+    hh, ww = np.meshgrid(np.arange(n0), np.arange(n0), indexing="ij")
+    x = np.cos(2 * np.pi * (p * hh + q * ww) / n0)[None, None]
+    Ks = [_rand_complex((chans[i + 1], sizes[i], sizes[i] // 2 + 1)) for i in range(2)]
+    y, _ = fdc.cic_chain_forward(x, Ks, sizes)
+    hm, wm = np.meshgrid(np.arange(m), np.arange(m), indexing="ij")
+    for o in range(chans[-1]):
+        v = n0 * n0 / 2.0
+        ch = o
+        for i in reversed(range(2)):
+            v = v * Ks[i][ch, p % sizes[i], q]
+            ch = ch // (chans[i + 1] // chans[i])
+        expect = (2.0 / (m * m)) * np.abs(v) * np.cos(2 * np.pi * (p * hm + q * wm) / m + np.angle(v))
+        np.testing.assert_allclose(y[0, o], expect, atol=1e-9 * np.abs(v) / (m * m))
+
+
+def test_chain_backward_is_the_adjoint():
+    sizes, chans = (16, 8, 4), (1, 2, 4)
+    x = RNG.standard_normal((2, 1, 16, 16))
+    Ks = [_rand_complex((chans[i + 1], sizes[i], sizes[i] // 2 + 1)) for i in range(2)]
+    y, saved = fdc.cic_chain_forward(x, Ks, sizes)
+    gy = RNG.standard_normal(y.shape)
+    gks, gx = fdc.cic_chain_backward(gy, saved, Ks, sizes, want_input_grad=True)
+    # linear in x: <y(dx), gy> = <dx, gx>
+    dx = RNG.standard_normal(x.shape)
+    ydx, _ = fdc.cic_chain_forward(dx, Ks, sizes)
+    np.testing.assert_allclose(np.sum(ydx * gy), np.sum(dx * gx), rtol=1e-10)
+    # finite differences in Re and Im of kernel entries of both layers
+    eps = 1e-6
+    for li, (o, k, l) in [(0, (1, 3, 2)), (0, (0, 15, 0)), (1, (3, 1, 1)), (1, (2, 7, 4))]:
+        for comp in (1.0, 1j):
+            Kp = [k_.copy() for k_ in Ks]
+            Km = [k_.copy() for k_ in Ks]
+            Kp[li][o, k, l] += eps * comp
+            Km[li][o, k, l] -= eps * comp
+            yp, _ = fdc.cic_chain_forward(x, Kp, sizes)
+            ym, _ = fdc.cic_chain_forward(x, Km, sizes)
+            fd = np.sum((yp - ym) * gy) / (2 * eps)
+            an = gks[li][o, k, l].real if comp == 1.0 else gks[li][o, k, l].imag
+            np.testing.assert_allclose(an, fd, rtol=1e-6, atol=1e-9)
