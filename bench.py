@@ -106,6 +106,37 @@ def fused_step_launches(wl, input_grad=False):
     return out
 
 
+def chain_step_launches(wl, input_grad=False):
+    """(kernel name, algorithmic bytes) of every launch of one step of the FDCNN chain
+    (one rfft2, every FDC + FDP layer on spectra, one irfft2, and the backward)."""
+    out = []
+    n = wl.layers
+    B = wl.batch
+    N0, C0 = wl.sizes[0], wl.channels[0]
+    NF0 = N0 // 2 + 1
+    ML, CL = wl.sizes[-1], wl.channels[-1]
+    MFL = ML // 2 + 1
+    out.append((f"row_r2c_{N0}", F32 * B * C0 * N0 * N0 + C64 * B * C0 * N0 * NF0))
+    out.append((f"col_fft_fwd_{N0}", 2 * C64 * B * C0 * N0 * NF0))
+    for i in range(n):
+        B, C, S, N, M, L, NF = layer_dims(wl, i)
+        out.append(("cic_fdp_fwd", C64 * (B * C * M * L + S * M * L + B * S * M * L)))
+    out.append((f"col_fft_inv_{ML}", 2 * C64 * B * CL * ML * MFL))
+    out.append((f"row_c2r_{ML}", C64 * B * CL * ML * MFL + F32 * B * CL * ML * ML))
+    out.append((f"row_r2c_{ML}", F32 * B * CL * ML * ML + C64 * B * CL * ML * MFL))
+    out.append((f"col_fft_fwd_{ML}", 2 * C64 * B * CL * ML * MFL))
+    for i in reversed(range(n)):
+        B, C, S, N, M, L, NF = layer_dims(wl, i)
+        if i > 0 or input_grad:
+            # reads gY and K at the kept bins, writes all of gX (zeros at dropped bins)
+            out.append(("cic_fdp_bwd_gx", C64 * (B * S * M * L + S * M * L + B * C * N * NF)))
+        out.append(("cic_fdp_bwd_gk", C64 * (B * S * M * L + B * C * M * L + S * N * NF)))
+    if input_grad:
+        out.append((f"col_fft_inv_{N0}", 2 * C64 * B * C0 * N0 * NF0))
+        out.append((f"row_c2r_{N0}", C64 * B * C0 * N0 * NF0 + F32 * B * C0 * N0 * N0))
+    return out
+
+
 def step_api_bytes(wl, input_grad=False):
     """Bytes of the tensors that cross the layer interface in one step, each counted once:
     forward x, K at the kept bins, y; backward g, K, the saved pooled spectrum, gx, gK at kept bins."""
@@ -182,7 +213,7 @@ def measured_traffic(kernel, workload):
 # CPU baseline: the float64 oracle on the host cores
 # ----------------------------------------------------------------------------
 
-def cpu_baseline(wl, data, min_seconds=10.0, max_reps=50):
+def cpu_baseline(wl, data, min_seconds=10.0, max_reps=50, chain=False):
     import numpy as np
     from threadpoolctl import threadpool_info
 
@@ -192,9 +223,11 @@ def cpu_baseline(wl, data, min_seconds=10.0, max_reps=50):
     kd = [k.astype(np.complex128) for k in data.kernels]
     g = data.grad.astype(np.float64)
     reps, t0 = 0, time.perf_counter()
+    fwd, bwd = (fdc.cic_chain_forward, fdc.cic_chain_backward) if chain else (fdc.cic_stack_forward,
+                                                                              fdc.cic_stack_backward)
     while True:
-        _, saved = fdc.cic_stack_forward(x, kd, wl.sizes)
-        fdc.cic_stack_backward(g, saved, kd, wl.sizes, want_input_grad=False)
+        _, saved = fwd(x, kd, wl.sizes)
+        bwd(g, saved, kd, wl.sizes, want_input_grad=False)
         reps += 1
         el = time.perf_counter() - t0
         if el >= min_seconds or reps >= max_reps:
@@ -228,7 +261,11 @@ class CicStackRun:
         self.Ks = [torch.from_numpy(k).to(dev) for k in self.data.kernels]
         self.g = torch.from_numpy(self.data.grad).to(dev)
         self.per_layer = args.per_layer
-        if self.per_layer:
+        self.executor = "chain" if args.chain else ("per_layer" if args.per_layer else "fused_stack")
+        if args.chain:
+            self.stack = layers.CicChain(wl.batch, wl.sizes, wl.channels, device=dev)
+            model = chain_step_launches
+        elif self.per_layer:
             self.stack = layers.CicStack(wl.batch, wl.sizes, wl.channels, device=dev)
             model = step_launches
         else:
@@ -245,17 +282,17 @@ class CicStackRun:
         self.stack.backward(self.g, self.Ks, input_grad=self.gin)
 
     def outputs(self):
-        last = self.stack.acts[-1] if self.per_layer else self.stack.out
+        last = self.stack.acts[-1] if self.executor == "per_layer" else self.stack.out
         return [last] + list(self.stack.gks)
 
     def config(self):
         wl = self.wl
         return {"workload": wl.name, "batch": wl.batch, "sizes": list(wl.sizes), "channels": list(wl.channels),
                 "input_grad": bool(self.input_grad),
-                "executor": "per_layer" if self.per_layer else "fused_stack"}
+                "executor": self.executor}
 
     def cpu_baseline(self):
-        return cpu_baseline(self.wl, self.data)
+        return cpu_baseline(self.wl, self.data, chain=self.executor == "chain")
 
 
 class FullFdcRun:
@@ -336,6 +373,9 @@ def main():
     ap.add_argument("--input-grad", action="store_true", help="CIC stack: also compute the input-image gradient")
     ap.add_argument("--per-layer", action="store_true",
                     help="CIC stack: run the layer-by-layer calls instead of the fused stack executor")
+    ap.add_argument("--chain", action="store_true",
+                    help="CIC stack: the FDCNN data flow of section 2.5.1 (one rfft2, FDC + FDP layers on spectra, "
+                         "one irfft2); a different function from the per-layer transforms")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of HIP graph replays")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the timed region, run one plain streaming copy kernel (dst = src * 1) over "

@@ -117,6 +117,18 @@ fdc_status fdc_cic_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *
 /* ------------------------------------------------------------------------ */
 /* Frequency Domain Pooling (section 2.4.2)                                 */
 /* ------------------------------------------------------------------------ */
+/* One FDC layer of the FDCNN on spectra (section 2.5.1: the network transforms once,
+ * before its first layer, and inverts once after its last): CIC (Eq. 5) followed by
+ * FDP to M x M, forming only the bins FDP keeps.  X [B][C][N][N/2+1], K [S][N][N/2+1]
+ * -> Y [B][S][M][M/2+1]; S mod C == 0, N and M even, M <= N. */
+fdc_status fdc_cic_fdp_forward(const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *Y, int B, int C, int S, int N, int M,
+                               hipStream_t stream);
+/* gY [B][S][M][M/2+1] -> gX [B][C][N][N/2+1] (NULL: skipped) and gK [S][N][N/2+1]
+ * (NULL: skipped; summed over the batch in order), both with exact zeros at the bins
+ * FDP drops. */
+fdc_status fdc_cic_fdp_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX, fdc_c64 *gK,
+                                int B, int C, int S, int N, int M, hipStream_t stream);
+
 /* FDP crops the RFFT-shifted half spectrum: (H-Mh)/2 rows off the top and the
  * bottom, (W-Mw)/2 columns off the right, then shifts back.  In unshifted
  * order it keeps rows [0, Mh/2) and [H-Mh/2, H) and columns [0, Mw/2]; no

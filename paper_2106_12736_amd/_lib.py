@@ -38,6 +38,8 @@ _SIGS = {
     "fdc_irfft2_backward": [_P, _P, _P, _P, _SZ, _P],
     "fdc_cic_forward": [_P, _P, _P, _I, _I, _I, _I, _I, _P],
     "fdc_cic_backward": [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P],
+    "fdc_cic_fdp_forward": [_P, _P, _P, _I, _I, _I, _I, _I, _P],
+    "fdc_cic_fdp_backward": [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P],
     "fdp_forward": [_P, _P, _I64, _I, _I, _I, _I, _P],
     "fdp_backward": [_P, _P, _I64, _I, _I, _I, _I, _P],
     "fdc_cic_layer_plan_create": [_PP, _I, _I, _I, _I, _I, _I, _I],

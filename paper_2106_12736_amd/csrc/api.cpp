@@ -264,6 +264,43 @@ fdc_status fdc_cic_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *
   return FDC_OK;
 }
 
+static fdc_status check_cic_fdp(int B, int C, int S, int N, int M) {
+  if (B < 1 || C < 1 || S < 1) return fail(FDC_EINVAL, "B, C, S must be >= 1 (B=%d C=%d S=%d)", B, C, S);
+  if (S % C) return fail(FDC_EINVAL, "CIC needs S mod C == 0 (S=%d C=%d)", S, C);
+  if (!even_pos(N) || !even_pos(M) || M > N)
+    return fail(FDC_EINVAL, "N and M must be positive and even with M <= N (N=%d M=%d)", N, M);
+  return FDC_OK;
+}
+
+fdc_status fdc_cic_fdp_forward(const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *Y, int B, int C, int S, int N, int M,
+                               hipStream_t s) {
+  if (fdc_status st = check_cic_fdp(B, C, S, N, M)) return st;
+  if (!X || !K || !Y) return fail(FDC_EINVAL, "NULL tensor");
+  return check_hip(fdc::launch_cic_fdp_fwd(reinterpret_cast<const float2 *>(X), reinterpret_cast<const float2 *>(K),
+                                           reinterpret_cast<float2 *>(Y), B, C, S, N, M, s),
+                   "cic_fdp_forward");
+}
+
+fdc_status fdc_cic_fdp_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX, fdc_c64 *gK,
+                                int B, int C, int S, int N, int M, hipStream_t s) {
+  if (fdc_status st = check_cic_fdp(B, C, S, N, M)) return st;
+  if (!gY || (gX && !K) || (gK && !X)) return fail(FDC_EINVAL, "NULL tensor");
+  if (gX) {
+    if (fdc_status st = check_hip(fdc::launch_cic_fdp_bwd_gx(reinterpret_cast<const float2 *>(gY),
+                                                             reinterpret_cast<const float2 *>(K),
+                                                             reinterpret_cast<float2 *>(gX), B, C, S, N, M, s),
+                                  "cic_fdp_backward gX"))
+      return st;
+  }
+  if (gK) {
+    return check_hip(fdc::launch_cic_fdp_bwd_gk(reinterpret_cast<const float2 *>(gY),
+                                                reinterpret_cast<const float2 *>(X), reinterpret_cast<float2 *>(gK),
+                                                B, C, S, N, M, s),
+                     "cic_fdp_backward gK");
+  }
+  return FDC_OK;
+}
+
 static fdc_status check_fdp(int64_t count, int H, int W, int Mh, int Mw) {
   if (count < 1) return fail(FDC_EINVAL, "count must be >= 1");
   if (!even_pos(H) || !even_pos(W) || !even_pos(Mh) || !even_pos(Mw))

@@ -125,6 +125,14 @@ hipError_t launch_cic_bwd_gx(const float2 *gY, const float2 *K, float2 *gX, int 
                              hipStream_t s);
 hipError_t launch_cic_bwd_gk(const float2 *gY, const float2 *X, float2 *gK, int B, int C, int S, long long P,
                              hipStream_t s);
+// FDC layer of the FDCNN on spectra followed by FDP (only the kept bins are formed), and
+// its backward (gX and gK with exact zeros at the dropped bins).
+hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, int N, int M,
+                              hipStream_t s);
+hipError_t launch_cic_fdp_bwd_gx(const float2 *gY, const float2 *K, float2 *gX, int B, int C, int S, int N, int M,
+                                 hipStream_t s);
+hipError_t launch_cic_fdp_bwd_gk(const float2 *gY, const float2 *X, float2 *gK, int B, int C, int S, int N, int M,
+                                 hipStream_t s);
 hipError_t launch_fdp_gather(const float2 *X, float2 *Y, long long count, int H, int Wf, int Mh, int Mwf,
                              hipStream_t s);
 hipError_t launch_fdp_scatter(const float2 *gY, float2 *gX, long long count, int H, int Wf, int Mh, int Mwf,

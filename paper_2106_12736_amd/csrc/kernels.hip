@@ -962,6 +962,129 @@ hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, fl
   return err;
 }
 
+// e / d and e mod d for 0 <= e < 2^24, d >= 1: a float estimate corrected by one step.
+__device__ __forceinline__ int div_small(int e, int d, float rd, int &rem) {
+  int q = (int)((float)e * rd);
+  int r = e - q * d;
+  if (r < 0) q -= 1, r += d;
+  if (r >= d) q += 1, r -= d;
+  rem = r;
+  return q;
+}
+
+// FDC layer of the FDCNN on spectra (Eq. 5, Algorithm 1) followed by FDP, forming only
+// the bins FDP keeps: Y [B][S][M][M/2+1] from X [B][C][N][N/2+1], K [S][N][N/2+1].
+// Kept rows of the N-point spectrum: k < M/2 and k >= N - M/2 (output row k or
+// k - (N - M)); kept columns l <= M/2.  Grid: y over the output planes, x over the
+// plane's elements in order, so stores are contiguous.
+__global__ __launch_bounds__(256) void k_cic_fdp_fwd(const float2 *__restrict__ X, const float2 *__restrict__ K,
+                                                     float2 *__restrict__ Y, int C, int J, int N, int M,
+                                                     long long planes) {
+  const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1, pe = M * Lm;
+  const float rl = 1.f / (float)Lm;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= pe) return;
+  int l;
+  const int k = div_small(e, Lm, rl, l);
+  const int kr = k < M / 2 ? k : k + (N - M);
+  for (long long pl = blockIdx.y; pl < planes; pl += gridDim.y) {
+    const int o = (int)(pl % S);
+    const long long b = pl / S;
+    Y[pl * pe + e] = cmul(X[((b * C + o / J) * N + kr) * NF + l], K[((long long)o * N + kr) * NF + l]);
+  }
+}
+
+// Backward of k_cic_fdp_fwd: gX [B][C][N][N/2+1] = sum_j gY conj(K) at the kept bins,
+// exact zeros at the bins FDP drops.
+__global__ __launch_bounds__(256) void k_cic_fdp_bwd_gx(const float2 *__restrict__ gY, const float2 *__restrict__ K,
+                                                        float2 *__restrict__ gX, int C, int J, int N, int M,
+                                                        long long planes) {
+  const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1, pe = N * NF;
+  const float rn = 1.f / (float)NF;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= pe) return;
+  int l;
+  const int kr = div_small(e, NF, rn, l);
+  const bool kept = l < Lm && (kr < M / 2 || kr >= N - M / 2);
+  const int k = kr < M / 2 ? kr : kr - (N - M);
+  for (long long pl = blockIdx.y; pl < planes; pl += gridDim.y) {
+    const int c = (int)(pl % C);
+    const long long b = pl / C;
+    float2 acc = make_float2(0.f, 0.f);
+    if (kept) {
+      for (int j = 0; j < J; ++j) {
+        const int o = c * J + j;
+        acc = cfmac(acc, gY[((b * S + o) * M + k) * Lm + l], K[((long long)o * N + kr) * NF + l]);
+      }
+    }
+    gX[pl * pe + e] = acc;
+  }
+}
+
+// dK [S][N][N/2+1] = sum_b gY conj(X) at the kept bins (batch summed in order), exact
+// zeros at the bins FDP drops.
+__global__ __launch_bounds__(256) void k_cic_fdp_bwd_gk(const float2 *__restrict__ gY, const float2 *__restrict__ X,
+                                                        float2 *__restrict__ gK, int B, int C, int J, int N, int M,
+                                                        long long planes) {
+  const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1, pe = N * NF;
+  const float rn = 1.f / (float)NF;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= pe) return;
+  int l;
+  const int kr = div_small(e, NF, rn, l);
+  const bool kept = l < Lm && (kr < M / 2 || kr >= N - M / 2);
+  const int k = kr < M / 2 ? kr : kr - (N - M);
+  for (long long o = blockIdx.y; o < planes; o += gridDim.y) {
+    float2 acc = make_float2(0.f, 0.f);
+    if (kept) {
+      const long long c = o / J;
+      for (int b = 0; b < B; ++b)
+        acc = cfmac(acc, gY[(((long long)b * S + o) * M + k) * Lm + l], X[(((long long)b * C + c) * N + kr) * NF + l]);
+    }
+    gK[o * pe + e] = acc;
+  }
+}
+
+static dim3 plane_grid(long long plane_elems, long long planes) {
+  return dim3((unsigned)((plane_elems + 255) / 256), (unsigned)(planes < 65535 ? planes : 65535));
+}
+
+hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, int N, int M,
+                              hipStream_t s) {
+  if ((long long)N * (N / 2 + 1) >= (1 << 24)) return hipErrorInvalidValue;
+  const long long planes = (long long)B * S;
+  timing_before("cic_fdp_fwd", s);
+  hipLaunchKernelGGL(k_cic_fdp_fwd, plane_grid((long long)M * (M / 2 + 1), planes), dim3(256), 0, s, X, K, Y, C,
+                     S / C, N, M, planes);
+  const hipError_t e = hipGetLastError();
+  timing_after("cic_fdp_fwd", s);
+  return e;
+}
+
+hipError_t launch_cic_fdp_bwd_gx(const float2 *gY, const float2 *K, float2 *gX, int B, int C, int S, int N, int M,
+                                 hipStream_t s) {
+  if ((long long)N * (N / 2 + 1) >= (1 << 24)) return hipErrorInvalidValue;
+  const long long planes = (long long)B * C;
+  timing_before("cic_fdp_bwd_gx", s);
+  hipLaunchKernelGGL(k_cic_fdp_bwd_gx, plane_grid((long long)N * (N / 2 + 1), planes), dim3(256), 0, s, gY, K, gX,
+                     C, S / C, N, M, planes);
+  const hipError_t e = hipGetLastError();
+  timing_after("cic_fdp_bwd_gx", s);
+  return e;
+}
+
+hipError_t launch_cic_fdp_bwd_gk(const float2 *gY, const float2 *X, float2 *gK, int B, int C, int S, int N, int M,
+                                 hipStream_t s) {
+  if ((long long)N * (N / 2 + 1) >= (1 << 24)) return hipErrorInvalidValue;
+  const long long planes = S;
+  timing_before("cic_fdp_bwd_gk", s);
+  hipLaunchKernelGGL(k_cic_fdp_bwd_gk, plane_grid((long long)N * (N / 2 + 1), planes), dim3(256), 0, s, gY, X, gK, B,
+                     C, S / C, N, M, planes);
+  const hipError_t e = hipGetLastError();
+  timing_after("cic_fdp_bwd_gk", s);
+  return e;
+}
+
 hipError_t launch_cic_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, long long P,
                           hipStream_t s) {
   const long long total = (long long)B * S * P;

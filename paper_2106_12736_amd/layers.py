@@ -347,3 +347,75 @@ class CicStackFused:
              self._gk_arr, _ptr(self.bwd_ws), self.bwd_ws.numel(), _stream())
         return self.gks
 
+
+
+def cic_fdp_forward(X, K, M):
+    """FDC layer of the FDCNN on spectra followed by FDP: [B][C][N][N/2+1] -> [B][S][M][M/2+1]."""
+    _check(X, torch.complex64, name="X")
+    _check(K, torch.complex64, name="K")
+    B, C, N, _ = X.shape
+    S = K.shape[0]
+    Y = torch.empty((B, S, M, M // 2 + 1), dtype=torch.complex64, device=X.device)
+    call("fdc_cic_fdp_forward", _ptr(X), _ptr(K), _ptr(Y), B, C, S, N, M, _stream())
+    return Y
+
+
+def cic_fdp_backward(gY, X, K, need_gx=True, need_gk=True):
+    _check(gY, torch.complex64, name="gY")
+    B, S, M, _ = gY.shape
+    C, N = X.shape[1], X.shape[2]
+    gX = torch.empty_like(X) if need_gx else None
+    gK = torch.empty_like(K) if need_gk else None
+    call("fdc_cic_fdp_backward", _ptr(gY), _ptr(X), _ptr(K), _ptr(gX), _ptr(gK), B, C, S, N, M, _stream())
+    return gX, gK
+
+
+class CicChain:
+    """The FDCNN data flow of section 2.5.1 on a CIC + FDP stack: one rfft2 of the
+    input, every FDC (CIC) + FDP layer on spectra (fdc_cic_fdp_*), one irfft2 of the
+    last spectrum.  All buffers are preallocated, so a step allocates nothing."""
+
+    def __init__(self, batch, sizes, channels, device="cuda"):
+        self.batch, self.sizes, self.channels = batch, tuple(sizes), tuple(channels)
+        self.layers = len(sizes) - 1
+        self.device = torch.device(device)
+        B = batch
+        self.plan_in = FftPlan(B * channels[0], sizes[0], sizes[0])
+        self.plan_out = FftPlan(B * channels[-1], sizes[-1], sizes[-1])
+        self.ws = _workspace(max(self.plan_in.ws_bytes, self.plan_out.ws_bytes), self.device)
+        cd = torch.complex64
+        self.specs = [torch.empty((B, channels[i], sizes[i], sizes[i] // 2 + 1), dtype=cd, device=self.device)
+                      for i in range(self.layers + 1)]
+        self.gspecs = [torch.empty_like(t) for t in self.specs]
+        self.out = torch.empty((B, channels[-1], sizes[-1], sizes[-1]), dtype=torch.float32, device=self.device)
+        self.gks = [torch.empty((channels[i + 1], sizes[i], sizes[i] // 2 + 1), dtype=cd, device=self.device)
+                    for i in range(self.layers)]
+
+    def forward(self, x, kernels):
+        _check(x, torch.float32, (self.batch, self.channels[0], self.sizes[0], self.sizes[0]), "x")
+        s = _stream()
+        call("fdc_rfft2", self.plan_in._p, _ptr(x), _ptr(self.specs[0]), None, 0, s)
+        B = self.batch
+        for i, K in enumerate(kernels):
+            _check(K, torch.complex64, (self.channels[i + 1], self.sizes[i], self.sizes[i] // 2 + 1), f"K[{i}]")
+            call("fdc_cic_fdp_forward", _ptr(self.specs[i]), _ptr(K), _ptr(self.specs[i + 1]), B, self.channels[i],
+                 self.channels[i + 1], self.sizes[i], self.sizes[i + 1], s)
+        call("fdc_irfft2", self.plan_out._p, _ptr(self.specs[-1]), _ptr(self.out), _ptr(self.ws), self.ws.numel(), s)
+        return self.out
+
+    def backward(self, gy, kernels, input_grad=None):
+        """Kernel gradients of every layer (and the input gradient into `input_grad` if given)."""
+        _check(gy, torch.float32, tuple(self.out.shape), "gy")
+        s = _stream()
+        B = self.batch
+        call("fdc_irfft2_backward", self.plan_out._p, _ptr(gy), _ptr(self.gspecs[-1]), None, 0, s)
+        for i in reversed(range(self.layers)):
+            need_gx = i > 0 or input_grad is not None
+            call("fdc_cic_fdp_backward", _ptr(self.gspecs[i + 1]), _ptr(self.specs[i]), _ptr(kernels[i]),
+                 _ptr(self.gspecs[i] if need_gx else None), _ptr(self.gks[i]), B, self.channels[i],
+                 self.channels[i + 1], self.sizes[i], self.sizes[i + 1], s)
+        if input_grad is not None:
+            _check(input_grad, torch.float32, (B, self.channels[0], self.sizes[0], self.sizes[0]), "input_grad")
+            call("fdc_rfft2_backward", self.plan_in._p, _ptr(self.gspecs[0]), _ptr(input_grad), _ptr(self.ws),
+                 self.ws.numel(), s)
+        return self.gks

@@ -1,0 +1,92 @@
+"""GPU parity of the FDCNN data flow of section 2.5.1 (one rfft2, every FDC + FDP layer
+on spectra, one irfft2) against the float64 oracle: the fused spectral CIC + FDP op on
+its own, and the whole chain forward and backward on every CIC workload at full size."""
+
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+from _parity import assert_parity, to_np
+from oracle import fdc
+from paper_2106_12736_amd import inputs, layers
+
+pytestmark = pytest.mark.gpu
+
+
+def _rng(*key):
+    return np.random.default_rng(zlib.crc32(repr(key).encode()))
+
+
+def _c64(rng, shape):
+    return (rng.standard_normal(shape) + 1j * rng.standard_normal(shape)).astype(np.complex64)
+
+
+@pytest.mark.parametrize("B,C,S,N,M", [
+    (1, 1, 1, 4, 2), (2, 1, 4, 8, 4), (3, 2, 6, 16, 16), (2, 4, 4, 32, 8), (1, 3, 9, 64, 32), (2, 2, 4, 224, 112),
+])
+def test_cic_fdp_op(B, C, S, N, M):
+    rng = _rng("cic_fdp", B, C, S, N, M)
+    X = _c64(rng, (B, C, N, N // 2 + 1))
+    K = _c64(rng, (S, N, N // 2 + 1))
+    gY = _c64(rng, (B, S, M, M // 2 + 1))
+    Xd, Kd = torch.from_numpy(X).cuda(), torch.from_numpy(K).cuda()
+    Y = layers.cic_fdp_forward(Xd, Kd, M)
+    gX, gK = layers.cic_fdp_backward(torch.from_numpy(gY).cuda(), Xd, Kd)
+    torch.cuda.synchronize()
+    X64, K64, g64 = X.astype(np.complex128), K.astype(np.complex128), gY.astype(np.complex128)
+    assert_parity(to_np(Y), fdc.fdp(fdc.cic(X64, K64), M, M), "Y")
+    gz = fdc.fdp_backward(g64, N, N)
+    gx_ref, gk_ref = fdc.cic_backward(gz, X64, K64)
+    assert_parity(to_np(gX), gx_ref, "gX")
+    assert_parity(to_np(gK), gk_ref, "gK")
+    assert np.all(to_np(gK)[np.abs(gk_ref) == 0] == 0), "dropped bins must be exact zeros"
+
+
+@pytest.mark.parametrize("wl", inputs.CIC_WORKLOADS, ids=lambda w: w.name)
+def test_chain_forward_backward(wl):
+    print(f"chain {wl.name}", flush=True)
+    d = inputs.make_cic_stack(wl)
+    x = torch.from_numpy(d.x).cuda()
+    Ks = [torch.from_numpy(k).cuda() for k in d.kernels]
+    ch = layers.CicChain(wl.batch, wl.sizes, wl.channels)
+    gin = torch.empty_like(x)
+    ch.forward(x, Ks)
+    ch.backward(torch.from_numpy(d.grad).cuda(), Ks, input_grad=gin)
+    torch.cuda.synchronize()
+    kd = [k.astype(np.complex128) for k in d.kernels]
+    y_ref, saved = fdc.cic_chain_forward(d.x.astype(np.float64), kd, wl.sizes)
+    gks_ref, gx_ref = fdc.cic_chain_backward(d.grad.astype(np.float64), saved, kd, wl.sizes, want_input_grad=True)
+    assert_parity(to_np(ch.out), y_ref, "y")
+    for i in range(wl.layers):
+        assert_parity(to_np(ch.gks[i]), gks_ref[i], f"dK[{i}]")
+    assert_parity(to_np(gin), gx_ref, "gx")
+
+
+def test_chain_graph_replays():
+    wl = inputs.STACK512
+    d = inputs.make_cic_stack(wl)
+    x = torch.from_numpy(d.x).cuda()
+    Ks = [torch.from_numpy(k).cuda() for k in d.kernels]
+    g = torch.from_numpy(d.grad).cuda()
+    ch = layers.CicChain(wl.batch, wl.sizes, wl.channels)
+
+    def step():
+        ch.forward(x, Ks)
+        ch.backward(g, Ks)
+
+    step()
+    torch.cuda.synchronize()
+    ref = [ch.out.clone()] + [k.clone() for k in ch.gks]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for rep in range(3):
+        torch.randn(1 << 20, device="cuda").mul_(2.0).sum().item()
+        for t in [ch.out] + ch.gks:
+            t.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(zip(ref, [ch.out] + ch.gks)):
+            assert torch.equal(a, b), f"replay {rep}: output {i}"
