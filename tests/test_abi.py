@@ -257,3 +257,14 @@ def test_stack_plan_sizes_and_argument_checks():
     assert _lib.status("fdc_cic_stack_backward", p, d, arr, arr, None, arr, d, 8, None) == FDC_EWORKSPACE
     assert _lib.status("fdc_cic_stack_plan_destroy", p) == FDC_OK
     assert _lib.status("fdc_cic_stack_forward", p, d, arr, d, None, d, 1 << 40, None) == FDC_EINVAL
+
+
+def test_cic_fdp_validation():
+    d = ctypes.c_void_p(0x1000)
+    assert _lib.status("fdc_cic_fdp_forward", d, d, d, 2, 3, 4, 8, 4, None) == FDC_EINVAL  # S mod C
+    assert _lib.status("fdc_cic_fdp_forward", d, d, d, 2, 1, 4, 8, 16, None) == FDC_EINVAL  # M > N
+    assert _lib.status("fdc_cic_fdp_forward", d, d, d, 2, 1, 4, 8, 3, None) == FDC_EINVAL   # odd M
+    assert _lib.status("fdc_cic_fdp_forward", None, d, d, 2, 1, 4, 8, 4, None) == FDC_EINVAL
+    assert _lib.status("fdc_cic_fdp_backward", d, None, d, None, d, 2, 1, 4, 8, 4, None) == FDC_EINVAL  # gK needs X
+    assert _lib.status("fdc_cic_fdp_backward", d, d, None, d, None, 2, 1, 4, 8, 4, None) == FDC_EINVAL  # gX needs K
+    assert _lib.status("fdc_cic_fdp_backward", d, d, d, None, None, 2, 1, 4, 8, 4, None) == FDC_OK     # nothing asked
