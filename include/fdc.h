@@ -195,6 +195,19 @@ fdc_status fdc_cic_layer_backward(const fdc_layer_plan *plan, const float *gy, c
 #define FDC_FULL_ROW(P) ((int64_t)(P) / 2 + 16)
 #define FDC_FULL_SIDE_PLANE(P) ((int64_t)(P) + 8)
 
+/* The CIC + FDP layer with spatial kernels (section 2.4.1.2, Algorithm 1): w [S][n][n]
+ * fp32, n = the plan's kernel_n (1..8), placed at the top-left of the N x N grid and
+ * transformed on every call at the bins FDP keeps; otherwise fdc_cic_layer_forward /
+ * backward, with the plan's artifact mode.  The backward gives gw [S][n][n] (NULL:
+ * skipped; summed over the batch and bins in a fixed order) and gx (NULL: skipped).
+ * Workspaces: fdc_cic_spatial_workspace_size (they hold the kernel spectra and dK). */
+fdc_status fdc_cic_spatial_workspace_size(const fdc_layer_plan *plan, size_t *fwd_ws, size_t *bwd_ws);
+fdc_status fdc_cic_spatial_layer_forward(const fdc_layer_plan *plan, const float *x, const float *w, float *y,
+                                         void *saved, void *ws, size_t ws_bytes, hipStream_t stream);
+fdc_status fdc_cic_spatial_layer_backward(const fdc_layer_plan *plan, const float *gy, const void *saved,
+                                          const float *w, float *gx, float *gw, void *ws, size_t ws_bytes,
+                                          hipStream_t stream);
+
 /* Full FDC forward: y = artifact(irfft2(sum_c rfft2(x[b][c]) o K[s][c])) with
  * K[s][c] = rfft2(pad(w[s][c])).  K is generated per bin inside the contraction
  * and never stored.  `saved` (may be NULL) receives rfft2(x), complex: with

@@ -228,6 +228,27 @@ def cic_spectral_chain(x, kernels, sizes):
 
 
 # ----------------------------------------------------------------------------
+# CIC with spatial kernels (section 2.4.1.2): n x n kernels transformed on every call
+# ----------------------------------------------------------------------------
+
+def cic_spatial_layer_forward(x, w, m, artifact=ARTIFACT_NONE):
+    """Algorithm 1 with the kernel steps: w [S][n][n] padded to N x N at the top-left
+    and transformed, then the CIC + FDP layer.  Returns (y, x_spec)."""
+    n_img = x.shape[-1]
+    k_spec = kernel_spectrum(w, n_img, n_img)
+    return cic_fdp_layer_forward(x, k_spec, m, artifact, w.shape[-1])
+
+
+def cic_spatial_layer_backward(gy, x_spec, w, m, artifact=ARTIFACT_NONE, want_gx=True):
+    """Reverse of ``cic_spatial_layer_forward``: (gx or None, gw [S][n][n])."""
+    n_img = x_spec.shape[-2]
+    n = w.shape[-1]
+    k_spec = kernel_spectrum(w, n_img, n_img)
+    gx, g_k = cic_fdp_layer_backward(gy, x_spec, k_spec, m, artifact, n, want_gx)
+    return gx, kernel_spectrum_backward(g_k, n)
+
+
+# ----------------------------------------------------------------------------
 # FDCNN data flow (section 2.5.1): one RFFT before all FDC/FDP layers, one IRFFT after
 # ----------------------------------------------------------------------------
 

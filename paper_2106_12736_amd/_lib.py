@@ -49,6 +49,9 @@ _SIGS = {
     "fdc_layer_output_size": [_P, ctypes.POINTER(_I)],
     "fdc_cic_layer_forward": [_P, _P, _P, _P, _P, _P, _SZ, _P],
     "fdc_cic_layer_backward": [_P, _P, _P, _P, _P, _P, _P, _SZ, _P],
+    "fdc_cic_spatial_workspace_size": [_P, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ)],
+    "fdc_cic_spatial_layer_forward": [_P, _P, _P, _P, _P, _P, _SZ, _P],
+    "fdc_cic_spatial_layer_backward": [_P, _P, _P, _P, _P, _P, _P, _SZ, _P],
     "fdc_full_forward": [_P, _P, _P, _P, _P, _P, _SZ, _P],
     "fdc_full_backward": [_P, _P, _P, _P, _P, _P, _P, _SZ, _P],
     "fdc_cic_stack_plan_create": [_PP, _I, _I, _P, _P],

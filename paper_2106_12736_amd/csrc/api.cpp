@@ -36,6 +36,8 @@ fdc_status check_hip(hipError_t e, const char *what) {
 
 bool even_pos(long long v) { return v > 0 && v % 2 == 0; }
 
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
 constexpr uint32_t kFftMagic = 0xFDC0FF70u;
 constexpr uint32_t kLayerMagic = 0xFDC01A7Eu;
 constexpr uint32_t kStackMagic = 0xFDC05AC4u;
@@ -52,6 +54,7 @@ struct fdc_layer_plan {
   uint32_t magic;
   int kind;  // 0: CIC + FDP, 1: Full FDC
   int B, C, S, N, M, artifact, kn, out;
+  int ksz;  // CIC: spatial kernel size for the spatial-kernel calls (0: none given)
   size_t fwd_ws, saved, bwd_ws;
   float2 *tw;  // Full FDC: device table W^j = exp(-2 pi i j / N), j < N (owned by the plan)
 };
@@ -358,6 +361,7 @@ fdc_status fdc_cic_layer_plan_create(fdc_layer_plan **plan, int B, int C, int S,
   p->B = B, p->C = C, p->S = S, p->N = N, p->M = M;
   p->artifact = artifact;
   p->kn = artifact == FDC_ARTIFACT_NONE ? 1 : kernel_n;
+  p->ksz = kernel_n >= 1 && kernel_n <= M ? kernel_n : 0;
   p->out = artifact_out(M, artifact, p->kn);
   // split-layout spectra (fdc::SpecLayout) of L = M/2 + 1 bins per row
   const size_t L = (size_t)M / 2 + 1;
@@ -458,6 +462,82 @@ fdc_status fdc_cic_layer_backward(const fdc_layer_plan *p, const float *gy, cons
                                          L, 1.f, 0.5f, id, (long long)N * N, s),
                      "layer backward dx rows");
   }
+  return FDC_OK;
+}
+
+// ---------------------------------------------------------------------------
+// CIC layer with spatial kernels
+// ---------------------------------------------------------------------------
+namespace {
+struct SpatialWs {
+  size_t k, gk, part, layer, fwd, bwd;  // byte offsets and totals
+};
+SpatialWs spatial_layout(const fdc_layer_plan *p) {
+  SpatialWs w{};
+  const size_t kbytes = align256((size_t)p->S * p->N * (p->N / 2 + 1) * sizeof(fdc_c64));
+  w.k = 0;
+  w.fwd = kbytes + align256(p->fwd_ws);
+  w.gk = kbytes;
+  w.part = w.gk + kbytes;
+  w.layer = w.part + align256((size_t)p->S * fdc::cic_wgrad_blocks(p->M) * p->ksz * p->ksz * sizeof(float));
+  w.bwd = w.layer + align256(p->bwd_ws);
+  return w;
+}
+fdc_status check_spatial_plan(const fdc_layer_plan *p) {
+  if (fdc_status st = check_layer_plan(p, 0)) return st;
+  if (!fdc::spatial_kernel_size_supported(p->ksz))
+    return fail(FDC_EUNSUPPORTED, "spatial kernels need a plan with kernel_n in [1, %d] and <= M (got %d)", 8,
+                p->ksz);
+  return FDC_OK;
+}
+}  // namespace
+
+fdc_status fdc_cic_spatial_workspace_size(const fdc_layer_plan *p, size_t *fwd_ws, size_t *bwd_ws) {
+  if (fdc_status st = check_spatial_plan(p)) return st;
+  const SpatialWs w = spatial_layout(p);
+  if (fwd_ws) *fwd_ws = w.fwd;
+  if (bwd_ws) *bwd_ws = w.bwd;
+  return FDC_OK;
+}
+
+fdc_status fdc_cic_spatial_layer_forward(const fdc_layer_plan *p, const float *x, const float *w, float *y,
+                                         void *saved, void *ws, size_t ws_bytes, hipStream_t s) {
+  if (fdc_status st = check_spatial_plan(p)) return st;
+  if (!x || !w || !y) return fail(FDC_EINVAL, "NULL tensor");
+  const SpatialWs L = spatial_layout(p);
+  if (fdc_status st = check_ws(ws, ws_bytes, L.fwd)) return st;
+  char *base = static_cast<char *>(ws);
+  auto *K = reinterpret_cast<float2 *>(base + L.k);
+  if (fdc_status st = check_hip(fdc::launch_cic_kspec(p->N, w, K, p->S, p->ksz, p->M, s), "spatial kernel spectra"))
+    return st;
+  const size_t layer_off = L.fwd - align256(p->fwd_ws);  // the layer workspace follows the spectra
+  return fdc_cic_layer_forward(p, x, reinterpret_cast<const fdc_c64 *>(K), y, saved, base + layer_off,
+                               align256(p->fwd_ws), s);
+}
+
+fdc_status fdc_cic_spatial_layer_backward(const fdc_layer_plan *p, const float *gy, const void *saved, const float *w,
+                                          float *gx, float *gw, void *ws, size_t ws_bytes, hipStream_t s) {
+  if (fdc_status st = check_spatial_plan(p)) return st;
+  if (!gy) return fail(FDC_EINVAL, "gy is NULL");
+  if (gw && !saved) return fail(FDC_EINVAL, "saved is NULL but gw was requested");
+  if (gx && !w) return fail(FDC_EINVAL, "w is NULL but gx was requested");
+  if (!gx && !gw) return FDC_OK;
+  const SpatialWs L = spatial_layout(p);
+  if (fdc_status st = check_ws(ws, ws_bytes, L.bwd)) return st;
+  char *base = static_cast<char *>(ws);
+  auto *K = reinterpret_cast<float2 *>(base + L.k);
+  auto *gK = reinterpret_cast<float2 *>(base + L.gk);
+  auto *part = reinterpret_cast<float *>(base + L.part);
+  if (gx) {
+    if (fdc_status st = check_hip(fdc::launch_cic_kspec(p->N, w, K, p->S, p->ksz, p->M, s), "spatial kernel spectra"))
+      return st;
+  }
+  if (fdc_status st = fdc_cic_layer_backward(p, gy, saved, reinterpret_cast<const fdc_c64 *>(K), gx,
+                                             gw ? reinterpret_cast<fdc_c64 *>(gK) : nullptr, base + L.layer,
+                                             align256(p->bwd_ws), s))
+    return st;
+  if (gw)
+    return check_hip(fdc::launch_cic_wgrad(p->N, gK, part, gw, p->S, p->ksz, p->M, s), "spatial kernel gradient");
   return FDC_OK;
 }
 
@@ -642,7 +722,6 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, cons
 // Full FDC
 // ---------------------------------------------------------------------------
 namespace {
-size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 struct FullWs {  // byte offsets inside the forward / backward workspaces
   size_t x, y, wf;         // forward: X (when `saved` is NULL), Y, rearranged weights
   size_t g, gx, wg, part;  // backward: G, dL/dX spectrum, rearranged weights, dL/dw partials

@@ -125,6 +125,14 @@ hipError_t launch_cic_bwd_gx(const float2 *gY, const float2 *K, float2 *gX, int 
                              hipStream_t s);
 hipError_t launch_cic_bwd_gk(const float2 *gY, const float2 *X, float2 *gK, int B, int C, int S, long long P,
                              hipStream_t s);
+// Spatial-kernel CIC: kernel spectra of n x n kernels at the kept bins of an n_img -> M
+// layer (into K [S][n_img][n_img/2+1]), and dL/dw from dK (part: S * cic_wgrad_blocks(M)
+// * n * n floats of scratch).
+bool spatial_kernel_size_supported(int n);
+int cic_wgrad_blocks(int M);
+hipError_t launch_cic_kspec(int n_img, const float *w, float2 *K, int S, int n, int M, hipStream_t s);
+hipError_t launch_cic_wgrad(int n_img, const float2 *gK, float *part, float *gw, int S, int n, int M,
+                            hipStream_t s);
 // FDC layer of the FDCNN on spectra followed by FDP (only the kept bins are formed), and
 // its backward (gX and gK with exact zeros at the dropped bins).
 hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, int N, int M,

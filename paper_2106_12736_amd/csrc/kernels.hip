@@ -1085,6 +1085,149 @@ hipError_t launch_cic_fdp_bwd_gk(const float2 *gY, const float2 *X, float2 *gK, 
   return e;
 }
 
+// Kernel spectra of n x n spatial kernels placed at the top-left of the N x N grid
+// (section 2.4.1.2), formed on every call at the bins the FDP of an N -> M layer keeps:
+// K[o](k, l) = sum_a W^(k a) sum_b w[o][a][b] W^(l b), W = exp(-2 pi i / N), into
+// K [S][N][N/2+1] (the other bins are not written).
+template <int N>
+__global__ __launch_bounds__(256) void k_cic_kspec(const float *__restrict__ w, float2 *__restrict__ K, int n, int M,
+                                                   int total) {
+  constexpr int NF = N / 2 + 1;
+  const int L = M / 2 + 1;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= total) return;
+  int l, k;
+  const int r = div_small(e, L, 1.f / (float)L, l);
+  const int o = div_small(r, M, 1.f / (float)M, k);
+  const int kr = k < M / 2 ? k : k + (N - M);
+  const float *wo = w + (long long)o * n * n;
+  float2 acc = make_float2(0.f, 0.f);
+  for (int a = 0; a < n; ++a) {
+    float rx = 0.f, ry = 0.f;  // sum_b w_ab W^(l b)
+    for (int b = 0; b < n; ++b) {
+      const float2 v = twiddle_load<N>((l * b) % N);
+      rx = fmaf(wo[a * n + b], v.x, rx);
+      ry = fmaf(wo[a * n + b], v.y, ry);
+    }
+    const float2 u = twiddle_load<N>((kr * a) % N);
+    acc.x = fmaf(u.x, rx, fmaf(-u.y, ry, acc.x));
+    acc.y = fmaf(u.x, ry, fmaf(u.y, rx, acc.y));
+  }
+  K[((long long)o * N + kr) * NF + l] = acc;
+}
+
+// dL/dw of those kernels from dK [S][N][N/2+1] at the kept bins (the rfft2 adjoint
+// restricted to the n x n support): dL/dw[o][a][b] = Re sum dK(k, l) conj(W^(k a + l b)).
+// Workgroup (rb, o) takes rows rb, rb + RB, ... of the M kept rows; a wave sums one
+// row at a time, E_b = sum_l dK(k, l) conj(W^(l b)) reduced across its lanes, and
+// adds Re(E_b conj(W^(k a))).  Partial sums part [S][RB][n n] are added in order by
+// k_cic_wgrad_reduce.  n <= kSpatialMaxN.
+constexpr int kSpatialMaxN = 8;
+template <int N>
+__global__ __launch_bounds__(256) void k_cic_wgrad_part(const float2 *__restrict__ gK, float *__restrict__ part,
+                                                        int n, int M, int RB) {
+  constexpr int NF = N / 2 + 1;
+  const int L = M / 2 + 1;
+  const int rb = blockIdx.x, o = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float acc[kSpatialMaxN * kSpatialMaxN];
+#pragma unroll
+  for (int i = 0; i < kSpatialMaxN * kSpatialMaxN; ++i) acc[i] = 0.f;
+  for (int k = rb + RB * wave; k < M; k += 4 * RB) {
+    const int kr = k < M / 2 ? k : k + (N - M);
+    const float2 *row = gK + ((long long)o * N + kr) * NF;
+    float ex[kSpatialMaxN], ey[kSpatialMaxN];
+#pragma unroll
+    for (int b = 0; b < kSpatialMaxN; ++b) ex[b] = ey[b] = 0.f;
+    for (int l = lane; l < L; l += 64) {
+      const float2 g = row[l];
+#pragma unroll
+      for (int b = 0; b < kSpatialMaxN; ++b) {
+        if (b < n) {
+          const float2 v = twiddle_load<N>((l * b) % N);  // g conj(v)
+          ex[b] = fmaf(g.x, v.x, fmaf(g.y, v.y, ex[b]));
+          ey[b] = fmaf(g.y, v.x, fmaf(-g.x, v.y, ey[b]));
+        }
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < kSpatialMaxN; ++b) {
+      if (b < n) {
+        for (int off = 32; off > 0; off >>= 1) {
+          ex[b] += __shfl_xor(ex[b], off);
+          ey[b] += __shfl_xor(ey[b], off);
+        }
+      }
+    }
+#pragma unroll
+    for (int a = 0; a < kSpatialMaxN; ++a) {
+      if (a < n) {
+        const float2 u = twiddle_load<N>((kr * a) % N);
+#pragma unroll
+        for (int b = 0; b < kSpatialMaxN; ++b)
+          if (b < n) acc[a * kSpatialMaxN + b] = fmaf(ex[b], u.x, fmaf(ey[b], u.y, acc[a * kSpatialMaxN + b]));
+      }
+    }
+  }
+  // every lane of a wave holds the wave's sums; add the four waves in order
+  __shared__ float red[4][kSpatialMaxN * kSpatialMaxN];
+  if (lane == 0) {
+#pragma unroll
+    for (int i = 0; i < kSpatialMaxN * kSpatialMaxN; ++i) red[wave][i] = acc[i];
+  }
+  __syncthreads();
+  const int t = threadIdx.x;
+  if (t < n * n) {
+    const int a = t / n, b = t - (t / n) * n;
+    const int i = a * kSpatialMaxN + b;
+    part[((long long)o * RB + rb) * n * n + t] = (red[0][i] + red[1][i]) + (red[2][i] + red[3][i]);
+  }
+}
+
+__global__ void k_cic_wgrad_reduce(const float *__restrict__ part, float *__restrict__ gw, int nn, int RB,
+                                   int total) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= total) return;
+  const int o = i / nn, t = i - (i / nn) * nn;
+  float acc = 0.f;
+  for (int rb = 0; rb < RB; ++rb) acc += part[((long long)o * RB + rb) * nn + t];
+  gw[i] = acc;
+}
+
+bool spatial_kernel_size_supported(int n) { return n >= 1 && n <= kSpatialMaxN; }
+
+int cic_wgrad_blocks(int M) { return M >= 256 ? 32 : (M >= 64 ? 16 : 4); }
+
+hipError_t launch_cic_kspec(int n_img, const float *w, float2 *K, int S, int n, int M, hipStream_t s) {
+  hipError_t err = hipErrorInvalidValue;
+  dispatch_n(n_img, [&](auto nc) {
+    constexpr int N = decltype(nc)::value;
+    const long long total = (long long)S * M * (M / 2 + 1);
+    if (total >= (1 << 24)) return;
+    err = launch("cic_kspec", k_cic_kspec<N>, (unsigned)((total + 255) / 256), 256, 0, s, w, K, n, M, (int)total);
+  });
+  return err;
+}
+
+hipError_t launch_cic_wgrad(int n_img, const float2 *gK, float *part, float *gw, int S, int n, int M,
+                            hipStream_t s) {
+  if (!spatial_kernel_size_supported(n)) return hipErrorInvalidValue;
+  const int RB = cic_wgrad_blocks(M);
+  hipError_t err = hipErrorInvalidValue;
+  dispatch_n(n_img, [&](auto nc) {
+    constexpr int N = decltype(nc)::value;
+    if (S > 65535) return;
+    timing_before("cic_wgrad", s);
+    hipLaunchKernelGGL(k_cic_wgrad_part<N>, dim3(RB, S), dim3(256), 0, s, gK, part, n, M, RB);
+    err = hipGetLastError();
+    timing_after("cic_wgrad", s);
+  });
+  if (err != hipSuccess) return err;
+  const int total = S * n * n;
+  return launch("cic_wgrad_reduce", k_cic_wgrad_reduce, (unsigned)((total + 255) / 256), 256, 0, s, part, gw, n * n,
+                RB, total);
+}
+
 hipError_t launch_cic_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, long long P,
                           hipStream_t s) {
   const long long total = (long long)B * S * P;

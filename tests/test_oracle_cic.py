@@ -391,3 +391,26 @@ def test_chain_backward_is_the_adjoint():
             fd = np.sum((yp - ym) * gy) / (2 * eps)
             an = gks[li][o, k, l].real if comp == 1.0 else gks[li][o, k, l].imag
             np.testing.assert_allclose(an, fd, rtol=1e-6, atol=1e-9)
+
+
+# ---------------------------------------------------------------------------- spatial kernels
+@pytest.mark.parametrize("n,artifact", [(3, fdc.ARTIFACT_CROP), (5, fdc.ARTIFACT_CROP), (3, fdc.ARTIFACT_ROLL)])
+def test_spatial_cic_is_depthwise_convolution(n, artifact):
+    """Without pooling the spatial-kernel CIC layer is a depthwise convolution with
+    channel multiplier J and flipped kernels (valid for CROP, circular same-size for
+    ROLL); its weight gradient is the library's autograd gradient of that convolution."""
+    B, C, J, N = 2, 2, 3, 16
+    x = RNG.standard_normal((B, C, N, N))
+    w = RNG.standard_normal((C * J, n, n))
+    y, xs = fdc.cic_spatial_layer_forward(x, w, N, artifact)
+    xt = torch.from_numpy(x)
+    if artifact == fdc.ARTIFACT_ROLL:
+        p = (n - 1) // 2
+        xt = F.pad(xt, (p, n - 1 - p, p, n - 1 - p), mode="circular")
+    wt = torch.from_numpy(w[:, None, ::-1, ::-1].copy()).requires_grad_(True)
+    ref = F.conv2d(xt, wt, groups=C)
+    np.testing.assert_allclose(y, ref.detach().numpy(), atol=1e-10)
+    gy = RNG.standard_normal(y.shape)
+    ref.backward(torch.from_numpy(gy))
+    _, gw = fdc.cic_spatial_layer_backward(gy, xs, w, N, artifact, want_gx=False)
+    np.testing.assert_allclose(gw, wt.grad.numpy()[:, 0, ::-1, ::-1], atol=1e-9)
