@@ -137,6 +137,33 @@ def chain_step_launches(wl, input_grad=False):
     return out
 
 
+def spatial_step_launches(wl, n, input_grad=False):
+    """(kernel name, algorithmic bytes) of every launch of one step of the stack with
+    n x n spatial kernels (layer by layer, ROLL): step_launches plus the kernel-spectrum
+    formation before each layer's product and the weight-gradient projection."""
+    out = []
+    for i in range(wl.layers):
+        B, C, S, N, M, L, _ = layer_dims(wl, i)
+        out.append(("cic_kspec", F32 * S * n * n + C64 * S * M * L))
+        out.append((f"row_r2c_{N}", F32 * B * C * N * N + C64 * B * C * N * L))
+        out.append((f"col_fwd_crop_{N}_{M}", C64 * (B * C * N * L + B * C * M * L)))
+        out.append((f"col_cic_inv_{N}_{M}", C64 * (B * C * M * L + S * M * L + B * S * M * L)))
+        out.append((f"row_c2r_{M}", C64 * B * S * M * L + F32 * B * S * M * M))
+    for i in reversed(range(wl.layers)):
+        B, C, S, N, M, L, NF = layer_dims(wl, i)
+        gx = i > 0 or input_grad
+        if gx:
+            out.append(("cic_kspec", F32 * S * n * n + C64 * S * M * L))
+        out.append((f"row_r2c_{M}", F32 * B * S * M * M + C64 * B * S * M * L))
+        out.append((f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + S * N * NF)))
+        if gx:
+            out.append((f"col_bwd_gx_{N}_{M}", C64 * (B * S * M * L + S * M * L + B * C * N * L)))
+            out.append((f"row_c2r_{N}", C64 * B * C * N * L + F32 * B * C * N * N))
+        out.append(("cic_wgrad", C64 * S * M * L))
+        out.append(("cic_wgrad_reduce", F32 * S * n * n))
+    return out
+
+
 def step_api_bytes(wl, input_grad=False):
     """Bytes of the tensors that cross the layer interface in one step, each counted once:
     forward x, K at the kept bins, y; backward g, K, the saved pooled spectrum, gx, gK at kept bins."""
@@ -243,6 +270,35 @@ def cpu_baseline(wl, data, min_seconds=10.0, max_reps=50, chain=False):
     }
 
 
+def spatial_cpu_baseline(wl, data, min_seconds=10.0, max_reps=50):
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import fdc
+
+    x = data.x.astype(np.float64)
+    ws = [w.astype(np.float64) for w in data.weights]
+    g0 = data.grad.astype(np.float64)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        h, saved = x, []
+        for i in range(wl.layers):
+            h, xs = fdc.cic_spatial_layer_forward(h, ws[i], wl.sizes[i + 1], fdc.ARTIFACT_ROLL)
+            saved.append(xs)
+        g = g0
+        for i in reversed(range(wl.layers)):
+            g, _ = fdc.cic_spatial_layer_backward(g, saved[i], ws[i], wl.sizes[i + 1], fdc.ARTIFACT_ROLL,
+                                                  want_gx=i > 0)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds or reps >= max_reps:
+            break
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": reps * wl.batch / el, "unit": "images/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} full step(s) of the same workload (batch {wl.batch}, all {wl.layers} layers, "
+                      f"fwd+bwd, float64) in {el:.1f} s on {os.cpu_count()} host CPUs visible"}
+
+
 # ----------------------------------------------------------------------------
 # main
 # ----------------------------------------------------------------------------
@@ -262,7 +318,16 @@ class CicStackRun:
         self.g = torch.from_numpy(self.data.grad).to(dev)
         self.per_layer = args.per_layer
         self.executor = "chain" if args.chain else ("per_layer" if args.per_layer else "fused_stack")
-        if args.chain:
+        self.spatial = args.spatial_kernel
+        if self.spatial:
+            self.executor = "per_layer"
+            self.data = inputs.make_cic_spatial(wl, self.spatial)
+            self.x = torch.from_numpy(self.data.x).to(dev)
+            self.Ks = [torch.from_numpy(w).to(dev) for w in self.data.weights]
+            self.g = torch.from_numpy(self.data.grad).to(dev)
+            self.stack = layers.CicSpatialStack(wl.batch, wl.sizes, wl.channels, self.spatial, device=dev)
+            model = lambda w_, ig: spatial_step_launches(w_, self.spatial, ig)  # noqa: E731
+        elif args.chain:
             self.stack = layers.CicChain(wl.batch, wl.sizes, wl.channels, device=dev)
             model = chain_step_launches
         elif self.per_layer:
@@ -283,15 +348,18 @@ class CicStackRun:
 
     def outputs(self):
         last = self.stack.acts[-1] if self.executor == "per_layer" else self.stack.out
-        return [last] + list(self.stack.gks)
+        return [last] + list(self.stack.gws if self.spatial else self.stack.gks)
 
     def config(self):
         wl = self.wl
         return {"workload": wl.name, "batch": wl.batch, "sizes": list(wl.sizes), "channels": list(wl.channels),
                 "input_grad": bool(self.input_grad),
-                "executor": self.executor}
+                "executor": self.executor,
+                "kernels": f"spatial {self.spatial}x{self.spatial}, roll" if self.spatial else "spectral"}
 
     def cpu_baseline(self):
+        if self.spatial:
+            return spatial_cpu_baseline(self.wl, self.data)
         return cpu_baseline(self.wl, self.data, chain=self.executor == "chain")
 
 
@@ -373,6 +441,8 @@ def main():
     ap.add_argument("--input-grad", action="store_true", help="CIC stack: also compute the input-image gradient")
     ap.add_argument("--per-layer", action="store_true",
                     help="CIC stack: run the layer-by-layer calls instead of the fused stack executor")
+    ap.add_argument("--spatial-kernel", type=int, default=0, metavar="n",
+                    help="CIC stack: n x n spatial kernels transformed on every call (ROLL), layer by layer")
     ap.add_argument("--chain", action="store_true",
                     help="CIC stack: the FDCNN data flow of section 2.5.1 (one rfft2, FDC + FDP layers on spectra, "
                          "one irfft2); a different function from the per-layer transforms")

@@ -1085,35 +1085,57 @@ hipError_t launch_cic_fdp_bwd_gk(const float2 *gY, const float2 *X, float2 *gK, 
   return e;
 }
 
+// Largest spatial kernel of the spatial-kernel CIC calls.
+constexpr int kSpatialMaxN = 8;
+
 // Kernel spectra of n x n spatial kernels placed at the top-left of the N x N grid
 // (section 2.4.1.2), formed on every call at the bins the FDP of an N -> M layer keeps:
-// K[o](k, l) = sum_a W^(k a) sum_b w[o][a][b] W^(l b), W = exp(-2 pi i / N), into
-// K [S][N][N/2+1] (the other bins are not written).
+// K[o](k, l) = sum_a W^(k a) R_a(l) with R_a(l) = sum_b w[o][a][b] W^(l b),
+// W = exp(-2 pi i / N), into K [S][N][N/2+1] (the other bins are not written).  A
+// thread owns one column (o, l) of one block of kKspecRows kept rows: it forms R_a(l)
+// once and walks the rows, so each row of K is written by consecutive lanes.
+// Twiddles come from an LDS copy.
+constexpr int kKspecRows = 16;
 template <int N>
 __global__ __launch_bounds__(256) void k_cic_kspec(const float *__restrict__ w, float2 *__restrict__ K, int n, int M,
-                                                   int total) {
+                                                   int ncol_blocks) {
   constexpr int NF = N / 2 + 1;
+  __shared__ float2 tw[N];
+  for (int i = threadIdx.x; i < N; i += 256) tw[i] = twiddle_load<N>(i);
+  __syncthreads();
   const int L = M / 2 + 1;
-  const int e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= total) return;
-  int l, k;
-  const int r = div_small(e, L, 1.f / (float)L, l);
-  const int o = div_small(r, M, 1.f / (float)M, k);
-  const int kr = k < M / 2 ? k : k + (N - M);
+  const int o = blockIdx.x / ncol_blocks;
+  const int l = (blockIdx.x - o * ncol_blocks) * 64 + (threadIdx.x & 63);
+  if (l >= L) return;
   const float *wo = w + (long long)o * n * n;
-  float2 acc = make_float2(0.f, 0.f);
-  for (int a = 0; a < n; ++a) {
-    float rx = 0.f, ry = 0.f;  // sum_b w_ab W^(l b)
-    for (int b = 0; b < n; ++b) {
-      const float2 v = twiddle_load<N>((l * b) % N);
-      rx = fmaf(wo[a * n + b], v.x, rx);
-      ry = fmaf(wo[a * n + b], v.y, ry);
+  float2 R[kSpatialMaxN];
+#pragma unroll
+  for (int a = 0; a < kSpatialMaxN; ++a) {
+    float rx = 0.f, ry = 0.f;
+    if (a < n) {
+      for (int b = 0; b < n; ++b) {
+        const float2 v = tw[(l * b) % N];
+        rx = fmaf(wo[a * n + b], v.x, rx);
+        ry = fmaf(wo[a * n + b], v.y, ry);
+      }
     }
-    const float2 u = twiddle_load<N>((kr * a) % N);
-    acc.x = fmaf(u.x, rx, fmaf(-u.y, ry, acc.x));
-    acc.y = fmaf(u.x, ry, fmaf(u.y, rx, acc.y));
+    R[a] = make_float2(rx, ry);
   }
-  K[((long long)o * N + kr) * NF + l] = acc;
+  float2 *ko = K + (long long)o * N * NF + l;
+  const int k_end = min(M, (int)(blockIdx.y + 1) * kKspecRows);
+  for (int k = blockIdx.y * kKspecRows + (threadIdx.x >> 6); k < k_end; k += 4) {
+    const int kr = k < M / 2 ? k : k + (N - M);
+    float2 acc = make_float2(0.f, 0.f);
+#pragma unroll
+    for (int a = 0; a < kSpatialMaxN; ++a) {
+      if (a < n) {
+        const float2 u = tw[(kr * a) % N];
+        acc.x = fmaf(u.x, R[a].x, fmaf(-u.y, R[a].y, acc.x));
+        acc.y = fmaf(u.x, R[a].y, fmaf(u.y, R[a].x, acc.y));
+      }
+    }
+    ko[(long long)kr * NF] = acc;
+  }
 }
 
 // dL/dw of those kernels from dK [S][N][N/2+1] at the kept bins (the rfft2 adjoint
@@ -1122,11 +1144,13 @@ __global__ __launch_bounds__(256) void k_cic_kspec(const float *__restrict__ w, 
 // row at a time, E_b = sum_l dK(k, l) conj(W^(l b)) reduced across its lanes, and
 // adds Re(E_b conj(W^(k a))).  Partial sums part [S][RB][n n] are added in order by
 // k_cic_wgrad_reduce.  n <= kSpatialMaxN.
-constexpr int kSpatialMaxN = 8;
 template <int N>
 __global__ __launch_bounds__(256) void k_cic_wgrad_part(const float2 *__restrict__ gK, float *__restrict__ part,
                                                         int n, int M, int RB) {
   constexpr int NF = N / 2 + 1;
+  __shared__ float2 tw[N];
+  for (int i = threadIdx.x; i < N; i += 256) tw[i] = twiddle_load<N>(i);
+  __syncthreads();
   const int L = M / 2 + 1;
   const int rb = blockIdx.x, o = blockIdx.y;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -1144,7 +1168,7 @@ __global__ __launch_bounds__(256) void k_cic_wgrad_part(const float2 *__restrict
 #pragma unroll
       for (int b = 0; b < kSpatialMaxN; ++b) {
         if (b < n) {
-          const float2 v = twiddle_load<N>((l * b) % N);  // g conj(v)
+          const float2 v = tw[(l * b) % N];  // g conj(v)
           ex[b] = fmaf(g.x, v.x, fmaf(g.y, v.y, ex[b]));
           ey[b] = fmaf(g.y, v.x, fmaf(-g.x, v.y, ey[b]));
         }
@@ -1162,7 +1186,7 @@ __global__ __launch_bounds__(256) void k_cic_wgrad_part(const float2 *__restrict
 #pragma unroll
     for (int a = 0; a < kSpatialMaxN; ++a) {
       if (a < n) {
-        const float2 u = twiddle_load<N>((kr * a) % N);
+        const float2 u = tw[(kr * a) % N];
 #pragma unroll
         for (int b = 0; b < kSpatialMaxN; ++b)
           if (b < n) acc[a * kSpatialMaxN + b] = fmaf(ex[b], u.x, fmaf(ey[b], u.y, acc[a * kSpatialMaxN + b]));
@@ -1199,12 +1223,18 @@ bool spatial_kernel_size_supported(int n) { return n >= 1 && n <= kSpatialMaxN; 
 int cic_wgrad_blocks(int M) { return M >= 256 ? 32 : (M >= 64 ? 16 : 4); }
 
 hipError_t launch_cic_kspec(int n_img, const float *w, float2 *K, int S, int n, int M, hipStream_t s) {
+  if (!spatial_kernel_size_supported(n)) return hipErrorInvalidValue;
   hipError_t err = hipErrorInvalidValue;
   dispatch_n(n_img, [&](auto nc) {
     constexpr int N = decltype(nc)::value;
-    const long long total = (long long)S * M * (M / 2 + 1);
-    if (total >= (1 << 24)) return;
-    err = launch("cic_kspec", k_cic_kspec<N>, (unsigned)((total + 255) / 256), 256, 0, s, w, K, n, M, (int)total);
+    const int ncb = (M / 2 + 1 + 63) / 64;
+    const long long blocks = (long long)S * ncb;
+    if (blocks >= (1LL << 31)) return;
+    const int rowb = (M + kKspecRows - 1) / kKspecRows;
+    timing_before("cic_kspec", s);
+    hipLaunchKernelGGL(k_cic_kspec<N>, dim3((unsigned)blocks, rowb), dim3(256), 0, s, w, K, n, M, ncb);
+    err = hipGetLastError();
+    timing_after("cic_kspec", s);
   });
   return err;
 }

@@ -190,3 +190,30 @@ def make_full_fdc(wl: FullFdcLayer, batch=None):
     o = wl.size - wl.n + 1
     grad = normal(rng, (b, wl.cout, o, o))
     return FullFdcInputs(x, w, grad)
+
+
+@dataclass
+class CicSpatialInputs:
+    x: np.ndarray            # [B][C0][N0][N0] float32
+    weights: list = field(default_factory=list)   # per layer [S][n][n] float32
+    grad: np.ndarray = None  # [B][S_last][M_last][M_last] float32
+
+
+def make_cic_spatial(wl: CicStack, n, batch=None):
+    """A CIC stack workload with n x n spatial kernels instead of spectra: the same
+    images, He-normal depthwise weights N(0, 2 / n^2) per layer (fan-in n^2: each
+    output channel convolves one input channel), and the upstream gradient."""
+    b = wl.batch if batch is None else batch
+    rng = rng_for(wl.index, salt=100 + n)
+    n0, c0 = wl.sizes[0], wl.channels[0]
+    if wl.image == "uniform":
+        x = uniform_images(rng, b, c0, n0)
+    elif wl.image == "disc":
+        x = disc_images(rng, b, c0, n0)
+    else:
+        x = fundus_images(rng, b, c0, n0)
+    std = np.float32(np.sqrt(2.0 / (n * n)))
+    weights = [rng.standard_normal((wl.channels[i + 1], n, n), dtype=np.float32) * std for i in range(wl.layers)]
+    grad = normal(rng, (b, wl.channels[-1], wl.sizes[-1], wl.sizes[-1]))
+    return CicSpatialInputs(x, weights, grad)
+

@@ -249,6 +249,69 @@ class FullLayer(_LayerPlan):
         return (gx if need_gx else None), (gw if need_gw else None)
 
 
+class CicSpatialLayer(CicLayer):
+    """The CIC + FDP layer with spatial n x n kernels w [S][n][n], transformed on every
+    call (fdc_cic_spatial_layer_*); n is the plan's kernel_n."""
+
+    def __init__(self, B, C, S, N, M, kernel_n, artifact="roll", device="cuda"):
+        super().__init__(B, C, S, N, M, artifact=artifact, kernel_n=kernel_n, device=device)
+        self.n = kernel_n
+        f, b = ctypes.c_size_t(), ctypes.c_size_t()
+        call("fdc_cic_spatial_workspace_size", self._p, ctypes.byref(f), ctypes.byref(b))
+        self.fwd_ws = _workspace(f.value, self.device)
+        self.bwd_ws = _workspace(b.value, self.device)
+
+    def forward(self, x, w, y=None, saved=None):
+        _check(x, torch.float32, (self.B, self.C, self.N, self.N), "x")
+        _check(w, torch.float32, (self.S, self.n, self.n), "w")
+        y = self.new_output() if y is None else y
+        call("fdc_cic_spatial_layer_forward", self._p, _ptr(x), _ptr(w), _ptr(y), _ptr(saved), _ptr(self.fwd_ws),
+             self.fwd_ws.numel(), _stream())
+        return y
+
+    def backward(self, gy, saved, w, need_gx=True, need_gw=True, gx=None, gw=None):
+        _check(gy, torch.float32, (self.B, self.S, self.out, self.out), "gy")
+        if need_gx and gx is None:
+            gx = torch.empty((self.B, self.C, self.N, self.N), dtype=torch.float32, device=self.device)
+        if need_gw and gw is None:
+            gw = torch.empty((self.S, self.n, self.n), dtype=torch.float32, device=self.device)
+        call("fdc_cic_spatial_layer_backward", self._p, _ptr(gy), _ptr(saved), _ptr(w),
+             _ptr(gx if need_gx else None), _ptr(gw if need_gw else None), _ptr(self.bwd_ws), self.bwd_ws.numel(),
+             _stream())
+        return (gx if need_gx else None), (gw if need_gw else None)
+
+
+class CicSpatialStack:
+    """A stack of spatial-kernel CIC + FDP layers (ROLL artifact handling, so sizes
+    stay powers of two) with preallocated activations, saved spectra and gradients."""
+
+    def __init__(self, batch, sizes, channels, kernel_n, device="cuda"):
+        self.layers = [CicSpatialLayer(batch, channels[i], channels[i + 1], sizes[i], sizes[i + 1], kernel_n,
+                                       artifact="roll", device=device) for i in range(len(sizes) - 1)]
+        self.saved = [layer.new_saved() for layer in self.layers]
+        self.acts = [layer.new_output() for layer in self.layers]
+        self.gacts = [None] + [torch.empty((batch, channels[i], sizes[i], sizes[i]), dtype=torch.float32,
+                                           device=device) for i in range(1, len(sizes) - 1)]
+        self.gws = [torch.empty((channels[i + 1], kernel_n, kernel_n), dtype=torch.float32, device=device)
+                    for i in range(len(sizes) - 1)]
+
+    def forward(self, x, weights):
+        h = x
+        for layer, w, y, sv in zip(self.layers, weights, self.acts, self.saved):
+            layer.forward(h, w, y=y, saved=sv)
+            h = y
+        return h
+
+    def backward(self, gy, weights, input_grad=None):
+        g = gy
+        for i in reversed(range(len(self.layers))):
+            gx = self.gacts[i] if i > 0 else input_grad
+            self.layers[i].backward(g, self.saved[i], weights[i], need_gx=gx is not None, need_gw=True, gx=gx,
+                                    gw=self.gws[i])
+            g = gx
+        return self.gws
+
+
 class CicStack:
     """A stack of fused CIC + FDP layers with preallocated activations, saved
     spectra and gradients, so that one forward + backward step allocates nothing."""

@@ -1,0 +1,84 @@
+"""GPU parity of the CIC + FDP layer with spatial n x n kernels (kernel spectra formed
+on every call, section 2.4.1.2) and its weight gradient, against the float64 oracle:
+single layers over sizes, poolings, kernel sizes and artifact modes, and a full-size
+stack in the configuration the benchmark times with --spatial-kernel 3."""
+
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+from _parity import assert_parity, to_np
+from oracle import fdc
+from paper_2106_12736_amd import inputs, layers
+
+pytestmark = pytest.mark.gpu
+
+MODE = {"none": fdc.ARTIFACT_NONE, "crop": fdc.ARTIFACT_CROP, "roll": fdc.ARTIFACT_ROLL}
+
+
+def _rng(*key):
+    return np.random.default_rng(zlib.crc32(repr(key).encode()))
+
+
+CASES = [
+    # N, M, B, C, J, n, artifact
+    (16, 16, 2, 1, 3, 3, "crop"),
+    (16, 8, 2, 2, 2, 3, "roll"),
+    (32, 16, 1, 1, 4, 5, "crop"),
+    (64, 32, 2, 1, 4, 1, "none"),
+    (64, 64, 1, 2, 2, 8, "roll"),
+    (128, 64, 2, 1, 2, 3, "crop"),
+    (224, 224, 1, 1, 2, 3, "roll"),
+    (512, 256, 1, 1, 2, 5, "crop"),
+    (1024, 512, 1, 1, 2, 3, "roll"),
+]
+
+
+@pytest.mark.parametrize("N,M,B,C,J,n,artifact", CASES)
+def test_spatial_layer(N, M, B, C, J, n, artifact):
+    print(f"spatial N={N} M={M} B={B} C={C} J={J} n={n} {artifact}", flush=True)
+    rng = _rng("spatial", N, M, B, C, J, n, artifact)
+    S = C * J
+    x = inputs.normal(rng, (B, C, N, N))
+    w = inputs.normal(rng, (S, n, n)) * np.float32(np.sqrt(2.0 / (n * n)))
+    layer = layers.CicSpatialLayer(B, C, S, N, M, n, artifact=artifact)
+    gy = inputs.normal(rng, (B, S, layer.out, layer.out))
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    saved = layer.new_saved()
+    y = layer.forward(xd, wd, saved=saved)
+    gx, gw = layer.backward(torch.from_numpy(gy).cuda(), saved, wd)
+    torch.cuda.synchronize()
+    y_ref, xs = fdc.cic_spatial_layer_forward(x.astype(np.float64), w.astype(np.float64), M, MODE[artifact])
+    gx_ref, gw_ref = fdc.cic_spatial_layer_backward(gy.astype(np.float64), xs, w.astype(np.float64), M,
+                                                    MODE[artifact])
+    assert_parity(to_np(y), y_ref, "y")
+    assert_parity(to_np(gx), gx_ref, "gx")
+    assert_parity(to_np(gw), gw_ref, "gw")
+
+
+@pytest.mark.parametrize("wl", [inputs.STACK256, inputs.STACK1024], ids=lambda w: w.name)
+def test_spatial_stack(wl):
+    print(f"spatial stack {wl.name}", flush=True)
+    n = 3
+    d = inputs.make_cic_spatial(wl, n)
+    st = layers.CicSpatialStack(wl.batch, wl.sizes, wl.channels, n)
+    x = torch.from_numpy(d.x).cuda()
+    ws = [torch.from_numpy(w).cuda() for w in d.weights]
+    gin = torch.empty_like(x)
+    st.forward(x, ws)
+    st.backward(torch.from_numpy(d.grad).cuda(), ws, input_grad=gin)
+    torch.cuda.synchronize()
+    h = d.x.astype(np.float64)
+    saved = []
+    for i in range(wl.layers):
+        h, xs = fdc.cic_spatial_layer_forward(h, d.weights[i].astype(np.float64), wl.sizes[i + 1], fdc.ARTIFACT_ROLL)
+        saved.append(xs)
+    assert_parity(to_np(st.acts[-1]), h, "y")
+    g = d.grad.astype(np.float64)
+    for i in reversed(range(wl.layers)):
+        g, gw = fdc.cic_spatial_layer_backward(g, saved[i], d.weights[i].astype(np.float64), wl.sizes[i + 1],
+                                               fdc.ARTIFACT_ROLL)
+        assert_parity(to_np(st.gws[i]), gw, f"gw[{i}]")
+    assert_parity(to_np(gin), g, "gx")
