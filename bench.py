@@ -363,6 +363,88 @@ class CicStackRun:
         return cpu_baseline(self.wl, self.data, chain=self.executor == "chain")
 
 
+def full_cic_step_launches(wl):
+    """One step of the Full FDC layer with CIC (spatial kernels, no pooling, crop):
+    forward, dL/dx and dL/dw."""
+    B, C, S, P, n = wl.batch, wl.cin, wl.cout, wl.size, wl.n
+    L = P // 2 + 1
+    O = P - n + 1
+    return [
+        ("cic_kspec", F32 * S * n * n + C64 * S * P * L),
+        (f"row_r2c_{P}", F32 * B * C * P * P + C64 * B * C * P * L),
+        (f"col_fwd_crop_{P}_{P}", C64 * (B * C * P * L + B * C * P * L)),
+        (f"col_cic_inv_{P}_{P}", C64 * (B * C * P * L + S * P * L + B * S * P * L)),
+        (f"row_c2r_{P}", C64 * B * S * P * L + F32 * B * S * O * O),
+        ("cic_kspec", F32 * S * n * n + C64 * S * P * L),
+        (f"row_r2c_{P}", F32 * B * S * O * O + C64 * B * S * P * L),
+        (f"col_bwd_gk_{P}", C64 * (B * S * P * L + B * C * P * L + S * P * L)),
+        (f"col_bwd_gx_{P}_{P}", C64 * (B * S * P * L + S * P * L + B * C * P * L)),
+        (f"row_c2r_{P}", C64 * B * C * P * L + F32 * B * C * P * P),
+        ("cic_wgrad", C64 * S * P * L),
+        ("cic_wgrad_reduce", F32 * S * n * n),
+    ]
+
+
+class FullCicRun:
+    """One Full FDC layer with CIC (the paper's VGG16 Conv Block 4 variant): forward,
+    dL/dx and dL/dw through fdc_cic_spatial_layer_*."""
+
+    def __init__(self, wl, args, dev):
+        import torch
+
+        from paper_2106_12736_amd import inputs, layers
+        self.wl = wl
+        self.data = inputs.make_full_cic(wl)
+        self.x = torch.from_numpy(self.data.x).to(dev)
+        self.w = torch.from_numpy(self.data.w).to(dev)
+        self.g = torch.from_numpy(self.data.grad).to(dev)
+        self.layer = layers.CicSpatialLayer(wl.batch, wl.cin, wl.cout, wl.size, wl.size, wl.n, artifact="crop",
+                                            device=dev)
+        self.saved = self.layer.new_saved()
+        self.y = self.layer.new_output()
+        self.gx = torch.empty_like(self.x)
+        self.gw = torch.empty_like(self.w)
+        self.launches = [(nm, b, "B") for nm, b in full_cic_step_launches(wl)]
+        B, C, S, P, n = wl.batch, wl.cin, wl.cout, wl.size, wl.n
+        O = P - n + 1
+        self.api_bytes = F32 * (2 * B * C * P * P + 2 * B * S * O * O + 3 * S * n * n) + C64 * B * C * P * (P // 2 + 1)
+
+    def step(self):
+        self.layer.forward(self.x, self.w, y=self.y, saved=self.saved)
+        self.layer.backward(self.g, self.saved, self.w, gx=self.gx, gw=self.gw)
+
+    def outputs(self):
+        return [self.y, self.gx, self.gw]
+
+    def config(self):
+        wl = self.wl
+        return {"workload": wl.name, "batch": wl.batch, "size": wl.size, "cin": wl.cin, "cout": wl.cout,
+                "kernel": wl.n, "artifact": "crop", "product": "cic"}
+
+    def cpu_baseline(self, min_seconds=10.0):
+        import numpy as np
+        from threadpoolctl import threadpool_info
+
+        from oracle import fdc
+
+        wl = self.wl
+        x = self.data.x[:1].astype(np.float64)
+        w = self.data.w.astype(np.float64)
+        g = self.data.grad[:1].astype(np.float64)
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            _, xs = fdc.cic_spatial_layer_forward(x, w, wl.size, fdc.ARTIFACT_CROP)
+            fdc.cic_spatial_layer_backward(g, xs, w, wl.size, fdc.ARTIFACT_CROP)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= min_seconds or reps >= 50:
+                break
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        return {"value": reps / el, "unit": "images/s", "cores": threads, "kind": "oracle",
+                "sample": f"{reps} step(s) of one image of the same layer (fwd, dL/dx, dL/dw, float64) in {el:.1f} s; "
+                          f"{os.cpu_count()} host CPUs visible"}
+
+
 class FullFdcRun:
     """One Full FDC layer step (forward, dL/dx, dL/dw) on preallocated buffers."""
 
@@ -462,7 +544,7 @@ def main():
 
     from paper_2106_12736_amd import _lib, inputs
 
-    workloads = {w.name: w for w in inputs.CIC_WORKLOADS + inputs.FULL_FDC_WORKLOADS}
+    workloads = {w.name: w for w in inputs.CIC_WORKLOADS + inputs.FULL_FDC_WORKLOADS + inputs.FULL_CIC_WORKLOADS}
     if args.workload not in workloads:
         sys.exit(f"unknown workload {args.workload}; one of {sorted(workloads)}")
     wl = workloads[args.workload]
@@ -472,7 +554,12 @@ def main():
     torch.cuda.set_device(dev)
     _lib.lib()  # fails loudly if libfdc.so is not built
 
-    run = (FullFdcRun if isinstance(wl, inputs.FullFdcLayer) else CicStackRun)(wl, args, dev)
+    if isinstance(wl, inputs.FullFdcLayer):
+        run = FullFdcRun(wl, args, dev)
+    elif isinstance(wl, inputs.FullCicLayer):
+        run = FullCicRun(wl, args, dev)
+    else:
+        run = CicStackRun(wl, args, dev)
     step = run.step
     stream = torch.cuda.current_stream()
 

@@ -67,6 +67,26 @@ FULL_FDC_WORKLOADS = tuple(
 )
 
 
+@dataclass(frozen=True)
+class FullCicLayer:
+    """A Full FDC layer with CIC as the paper's VGG16 variants use it (the layers of
+    Conv Block 4 at 512 x 512 input, i.e. 64 x 64 activations): B x Cin x P x P ->
+    B x Cout x (P-n+1)^2, n x n spatial kernels, crop, Cout = J * Cin."""
+    name: str
+    index: int
+    batch: int
+    size: int
+    cin: int
+    cout: int
+    n: int = 3
+
+
+FULL_CIC_WORKLOADS = (
+    FullCicLayer("full_cic_64_c256_512", 6, 16, 64, 256, 512),
+    FullCicLayer("full_cic_64_c512_512", 6, 16, 64, 512, 512),
+)
+
+
 def rng_for(index, salt=0):
     return np.random.default_rng(SEED_BASE + index + 1000 * salt)
 
@@ -216,4 +236,22 @@ def make_cic_spatial(wl: CicStack, n, batch=None):
     weights = [rng.standard_normal((wl.channels[i + 1], n, n), dtype=np.float32) * std for i in range(wl.layers)]
     grad = normal(rng, (b, wl.channels[-1], wl.sizes[-1], wl.sizes[-1]))
     return CicSpatialInputs(x, weights, grad)
+
+
+@dataclass
+class FullCicInputs:
+    x: np.ndarray     # [B][Cin][P][P]
+    w: np.ndarray     # [Cout][n][n]
+    grad: np.ndarray  # [B][Cout][P-n+1][P-n+1]
+
+
+def make_full_cic(wl: FullCicLayer, batch=None):
+    """Activations N(0,1), He-normal depthwise weights N(0, 2 / n^2), upstream gradient N(0,1)."""
+    b = wl.batch if batch is None else batch
+    rng = rng_for(wl.index, salt=wl.cin * 1000 + wl.cout)
+    x = normal(rng, (b, wl.cin, wl.size, wl.size))
+    w = rng.standard_normal((wl.cout, wl.n, wl.n), dtype=np.float32) * np.float32(np.sqrt(2.0 / (wl.n * wl.n)))
+    o = wl.size - wl.n + 1
+    grad = normal(rng, (b, wl.cout, o, o))
+    return FullCicInputs(x, w, grad)
 

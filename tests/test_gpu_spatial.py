@@ -82,3 +82,25 @@ def test_spatial_stack(wl):
                                                fdc.ARTIFACT_ROLL)
         assert_parity(to_np(st.gws[i]), gw, f"gw[{i}]")
     assert_parity(to_np(gin), g, "gx")
+
+
+@pytest.mark.parametrize("wl", inputs.FULL_CIC_WORKLOADS, ids=lambda w: w.name)
+def test_full_fdc_with_cic_block4(wl):
+    """The Full FDC layer with CIC at the paper's VGG16 Conv Block 4 shapes (64 x 64,
+    256 -> 512 and 512 -> 512 channels, 3 x 3, crop), 16 images, in the configuration
+    the benchmark times; every output element against the oracle."""
+    print(f"full cic {wl.name}", flush=True)
+    d = inputs.make_full_cic(wl)
+    layer = layers.CicSpatialLayer(wl.batch, wl.cin, wl.cout, wl.size, wl.size, wl.n, artifact="crop")
+    xd, wd = torch.from_numpy(d.x).cuda(), torch.from_numpy(d.w).cuda()
+    saved = layer.new_saved()
+    y = layer.forward(xd, wd, saved=saved)
+    gx, gw = layer.backward(torch.from_numpy(d.grad).cuda(), saved, wd)
+    torch.cuda.synchronize()
+    y_ref, xs = fdc.cic_spatial_layer_forward(d.x.astype(np.float64), d.w.astype(np.float64), wl.size,
+                                              fdc.ARTIFACT_CROP)
+    gx_ref, gw_ref = fdc.cic_spatial_layer_backward(d.grad.astype(np.float64), xs, d.w.astype(np.float64), wl.size,
+                                                    fdc.ARTIFACT_CROP)
+    assert_parity(to_np(y), y_ref, "y")
+    assert_parity(to_np(gx), gx_ref, "gx")
+    assert_parity(to_np(gw), gw_ref, "gw")
