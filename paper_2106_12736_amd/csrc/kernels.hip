@@ -274,6 +274,21 @@ template <int N>
 constexpr int col_ct() {
   return FftCfg<N>::TPS >= 64 ? 8 : (FftCfg<N>::TPS >= 32 ? 16 : 32);
 }
+// Narrower tiles (twice the workgroups) where measurement favoured them: the dX
+// kernel (three transforms per tile), the forward crop at 128 and 256 points and the
+// CIC inverse at 64 points.
+template <int N>
+constexpr int col_ct_gx() {
+  return col_ct<N>() / 2;
+}
+template <int N>
+constexpr int col_ct_crop() {
+  return (N == 128 || N == 256) ? col_ct<N>() / 2 : col_ct<N>();
+}
+template <int M>
+constexpr int col_ct_cic() {
+  return M == 64 ? col_ct<M>() / 2 : col_ct<M>();
+}
 
 // CT for columns [0, L): at most `ct` and a divisor of L - 1 when L - 1 > 0.
 __host__ __device__ constexpr int col_ct_for(int ct, int L) {
@@ -897,7 +912,7 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
   dispatch_nm(n, m, [&](auto nc, auto mc) {
     constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
-    constexpr int CTN = col_ct_for(col_ct<N>(), L), CTM = col_ct_for(col_ct<M>(), L);
+    constexpr int CTN = col_ct_for(col_ct_crop<N>(), L), CTM = col_ct_for(col_ct_cic<M>(), L);
     static const std::string n1 = "col_fwd_crop_" + std::to_string(N) + "_" + std::to_string(M);
     static const std::string n2 = "col_cic_inv_" + std::to_string(N) + "_" + std::to_string(M);
     const unsigned g1 = col_grid((long long)B * C, L, CTN);
@@ -951,7 +966,7 @@ hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, fl
   dispatch_nm(n, m, [&](auto nc, auto mc) {
     constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
-    constexpr int CT = col_ct_for(col_ct<N>(), L);
+    constexpr int CT = col_ct_for(col_ct_gx<N>(), L);
     const size_t lds = (twiddle_lds_elems<N>() + cic_lds_elems<N, M, CT>()) * sizeof(float2);
     const unsigned grid = col_grid((long long)B * C, L, CT);
     if (grid == 0) return;
