@@ -309,14 +309,21 @@ struct ColRef {
 
 // Column `s` of tile w.  Out-of-range lanes of the last tail tile get ok = false
 // and a valid (repeated) column, so their loads stay in bounds.
+// Main tiles run through G consecutive planes (G divides `planes`) at one column
+// position before moving on: kernels number their planes so that such a group
+// reads the same columns of a shared operand, which the group's workgroups -- on
+// one XCD after xcd_remap, at about the same time -- then fetch once into its L2.
 template <int CT>
-__device__ __forceinline__ ColRef column_ref(int w, int s, int L, int planes) {
+__device__ __forceinline__ ColRef column_ref(int w, int s, int L, int planes, int G = 1) {
   const int mpp = (L - 1) / CT, rt = L - mpp * CT;
   const int main_tiles = planes * mpp;
   ColRef r;
   if (w < main_tiles) {
-    r.plane = w / mpp;
-    r.l = (w - r.plane * mpp) * CT + s;
+    const int blk = G * mpp;
+    const int gi = w / blk, rr = w - gi * blk;
+    const int tile = rr / G;
+    r.plane = gi * G + (rr - tile * G);
+    r.l = tile * CT + s;
     r.ok = true;
   } else {
     int q = (w - main_tiles) * CT + s;
@@ -441,18 +448,20 @@ constexpr int kCicJW = 4;
 template <int N, int M, int CT, int JW>
 __global__ __launch_bounds__(CT *FftCfg<M>::TPS) void k_col_cic_inv(const float2 *__restrict__ Xh,
                                                                    const float2 *__restrict__ K,
-                                                                   float2 *__restrict__ U, int C, int J,
+                                                                   float2 *__restrict__ U, int B, int C, int J,
                                                                    int groups) {
   using CM = FftCfg<M>;
   constexpr int L = M / 2 + 1, NF = N / 2 + 1, TPS = CM::TPS, E = CM::E;
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<M>();
   stage_twiddles<M>(tw, threadIdx.x, CT * TPS);
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
-  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, groups);
+  // group index (ci * JB + jb) * B + b: the B images read the same kernel columns
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, groups, B);
   const int S = C * J, JB = J / JW;
-  const int bc = c.plane / JB;              // b * C + ci
-  const int o0 = (bc % C) * J + (c.plane - bc * JB) * JW;
-  const int b = bc / C;
+  const int b = c.plane % B, cj = c.plane / B;
+  const int ci = cj / JB;
+  const int o0 = ci * J + (cj - ci * JB) * JW;
+  const int bc = b * C + ci;
   const ColPtr xc = split_col<M, L>(Xh, groups / JB, bc, c.l);
   float2 x[E], kn[E];
   auto load_k = [&](int o) {
@@ -506,7 +515,8 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
   stage_twiddles<M>(tw, threadIdx.x, NT);
   const int s = threadIdx.x % CT, t = (threadIdx.x / CT) % TPS, g = threadIdx.x / (CT * TPS);
   const int wg = xcd_remap(blockIdx.x, gridDim.x);
-  const ColRef c = column_ref<CT>(wg, s, L, S);
+  // the J output channels of one input channel read the same pooled-input columns
+  const ColRef c = column_ref<CT>(wg, s, L, S, J);
   const int o = c.plane, ci = o / J;
   const int nf = N / 2 + 1;
 
@@ -595,9 +605,11 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
   stage_twiddles<N>(tw, threadIdx.x, CT * TPSN);
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   const int tp = t % TPSM, js = t / TPSM;
-  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
-  const int b = c.plane / C;
-  const int ci = c.plane - b * C;
+  // plane index ci * B + b: the B images read the same kernel columns
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes, planes / C);
+  const int B = planes / C;
+  const int ci = c.plane / B;
+  const int b = c.plane - ci * B;
   const int S = C * J;
 
   float2 acc[CM::E];
@@ -639,7 +651,7 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
   }
   fft_seq<N, +1>(w, t, lds, s, CT, tw, 1);
   if (!c.ok) return;
-  const ColPtr vc = split_col<N, L>(V, planes, c.plane, c.l);
+  const ColPtr vc = split_col<N, L>(V, planes, b * C + ci, c.l);
 #pragma unroll
   for (int m = 0; m < CN::E; ++m) vc.p[(t + TPSN * m) * vc.stride] = w[m];
 }
@@ -930,7 +942,7 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
     }
     const size_t lds2 = (twiddle_lds_elems<M>() + lds_size<kColLds>(M * CTM)) * sizeof(float2);
     auto go = [&](auto kern) {
-      err = launch(n2.c_str(), kern, g2, CTM * FftCfg<M>::TPS, lds2, s, Xh, K, U, C, J, (int)groups);
+      err = launch(n2.c_str(), kern, g2, CTM * FftCfg<M>::TPS, lds2, s, Xh, K, U, B, C, J, (int)groups);
     };
     switch (jw) {
       case 8: go(k_col_cic_inv<N, M, CTM, 8>); break;
