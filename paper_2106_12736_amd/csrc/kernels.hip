@@ -520,14 +520,14 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
   const int o = c.plane, ci = o / J;
   const int nf = N / 2 + 1;
 
-  // zeros of the columns l >= L, grid-stride over [S][N][L, nf)
+  // zeros of the columns l >= L: groups of LW lanes take the S * N rows in turn
   {
-    const int w = nf - L;
-    const long long total = (long long)S * N * w;
-    for (long long i = (long long)wg * NT + threadIdx.x; i < total; i += (long long)gridDim.x * NT) {
-      const long long row = i / w;
-      gK[row * nf + L + (i - row * w)] = make_float2(0.f, 0.f);
-    }
+    static_assert((NT & (NT - 1)) == 0, "NT must be a power of two");
+    constexpr int LW = NT < 64 ? NT : 64;
+    const int lane = threadIdx.x % LW;
+    const long long ngrp = (long long)gridDim.x * (NT / LW);
+    for (long long row = ((long long)wg * NT + threadIdx.x) / LW; row < (long long)S * N; row += ngrp)
+      for (int l = L + lane; l < nf; l += LW) gK[row * nf + l] = make_float2(0.f, 0.f);
   }
 
   float2 acc[E];
@@ -539,13 +539,23 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
     const ColPtr gc = split_col<M, L>(Tg, B * S, (act ? b : 0) * S + o, c.l);
     const ColPtr xc = split_col<M, L>(Xh, B * C, (act ? b : 0) * C + ci, c.l);
     // loads are unconditional (inactive lanes read a valid column); inactive lanes add nothing
-    float2 v[E];
+    float2 v[E], xv[E];
 #pragma unroll
     for (int m = 0; m < E; ++m) v[m] = gc.p[(t + TPS * m) * gc.stride];
+    // the pooled-input column is loaded before the transform so that its loads are
+    // all in flight together (up to 8 values per lane: registers allow it)
+    if constexpr (E <= 8) {
+#pragma unroll
+      for (int m = 0; m < E; ++m) xv[m] = xc.p[(t + TPS * m) * xc.stride];
+    }
     fft_seq<M, -1>(v, t, lds, g * M * CT + s, CT, tw, 1);
+    if constexpr (E > 8) {
+#pragma unroll
+      for (int m = 0; m < E; ++m) xv[m] = xc.p[(t + TPS * m) * xc.stride];
+    }
 #pragma unroll
     for (int m = 0; m < E; ++m) {
-      const float2 sum = cfmac(acc[m], v[m], xc.p[(t + TPS * m) * xc.stride]);
+      const float2 sum = cfmac(acc[m], v[m], xv[m]);
       acc[m] = act ? sum : acc[m];
     }
   }
@@ -622,13 +632,22 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
     const ColPtr gc = split_col<M, L>(Tg, planes * J, b * S + o, c.l);
     const float2 *kcol = K + (long long)o * N * NF + c.l;
     // loads are unconditional (inactive lanes read a valid column); inactive lanes add nothing
-    float2 g[CM::E];
+    float2 g[CM::E], kv[CM::E];
 #pragma unroll
     for (int m = 0; m < CM::E; ++m) g[m] = gc.p[(tp + TPSM * m) * gc.stride];
+    // the kernel column is loaded before the transform (up to 8 values per lane)
+    if constexpr (CM::E <= 8) {
+#pragma unroll
+      for (int m = 0; m < CM::E; ++m) kv[m] = kcol[(long long)kept_row<N, M>(tp + TPSM * m) * NF];
+    }
     fft_seq<M, -1>(g, tp, lds, js * M * CT + s, CT, tw, N / M);
+    if constexpr (CM::E > 8) {
+#pragma unroll
+      for (int m = 0; m < CM::E; ++m) kv[m] = kcol[(long long)kept_row<N, M>(tp + TPSM * m) * NF];
+    }
 #pragma unroll
     for (int m = 0; m < CM::E; ++m) {
-      const float2 sum = cfmac(acc[m], g[m], kcol[(long long)kept_row<N, M>(tp + TPSM * m) * NF]);
+      const float2 sum = cfmac(acc[m], g[m], kv[m]);
       acc[m] = act ? sum : acc[m];
     }
   }
