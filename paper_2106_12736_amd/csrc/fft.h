@@ -304,11 +304,20 @@ __device__ __forceinline__ void lds_barrier() {
   }
 }
 
+// Padded-layout index arithmetic with compile-time offsets.  For a base that is a
+// multiple of 32, i0 >= 0 and a power-of-two stride S (a divisor or a multiple
+// of 32), lds_phys(i0 + r S) = lds_phys(i0) + r S + floor(r S / 32) whenever the
+// run i0, i0 + S, ... stays in one aligned block of max(32, S * count) -- true for
+// the Stockham exchanges below -- so only lds_phys(i0) is computed at run time.
+constexpr bool pad_pow2_fit(int s) { return s > 0 && (s & (s - 1)) == 0; }
+constexpr int pad_offset(int c) { return c + c / 32; }
+
 // Transform one sequence.  Thread t (0 <= t < TPS) holds v[m] = element t + TPS*m
 // on entry and exit.  Element e of the sequence lives in LDS at
 // lds[lds_phys(base + e * es)].  Every thread of the workgroup (of the wave with
 // WAVE) must call this: it contains barriers.  With LEAD_SYNC the first LDS write
-// waits for every thread's earlier use of the LDS.  LAYOUT: lds_phys layout.
+// waits for every thread's earlier use of the LDS.  LAYOUT: lds_phys layout; with
+// kLdsPad, es must be 1 and, when N is a multiple of 32, base a multiple of 32.
 // tw: twiddle table in LDS (stage_twiddles) of length N * tws.
 template <int N, int DIR, bool LEAD_SYNC = true, bool WAVE = false, int LAYOUT = kLdsPlain>
 __device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2 *lds, int base, int es,
@@ -316,6 +325,7 @@ __device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2
   using C = FftCfg<N>;
   constexpr int E = C::E;
   constexpr int TPS = C::TPS;
+  constexpr bool PAD = LAYOUT == kLdsPad && N % 32 == 0;
   static_for<0, C::P>([&](auto pc) {
     constexpr int p = decltype(pc)::value;
     constexpr int R = C::R[p];
@@ -323,18 +333,25 @@ __device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2
     constexpr int NS = stockham_ns<N>(p);
     constexpr int NR = N / R;
     static_assert(BPT * R == E && BPT * TPS == NR, "radix plan does not fit the thread layout");
+    // folded padded addressing of this pass's reads (j + r NR, and j = t + TPS q)
+    // and writes (jo + r NS, jo inside an aligned block of NS R)
+    constexpr bool FOLD_RD = PAD && NR % 32 == 0;
+    constexpr bool FOLD_RQ = FOLD_RD && TPS % 32 == 0;
+    constexpr bool FOLD_WR = PAD && pad_pow2_fit(NS) && pad_pow2_fit(NS * R);
     float2 a[E];
     if constexpr (p == 0) {
 #pragma unroll
       for (int m = 0; m < E; ++m) a[m] = v[m];
     } else {
+      const int rd0 = FOLD_RQ ? lds_phys<LAYOUT>(base + t) : 0;
 #pragma unroll
       for (int q = 0; q < BPT; ++q) {
         const int j = t + TPS * q;
         const int k = j % NS;
+        const int rdq = FOLD_RQ ? rd0 + pad_offset(TPS * q) : (FOLD_RD ? lds_phys<LAYOUT>(base + j) : 0);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-          float2 x = lds[lds_phys<LAYOUT>(base + (j + r * NR) * es)];
+          float2 x = FOLD_RD ? lds[rdq + pad_offset(r * NR)] : lds[lds_phys<LAYOUT>(base + (j + r * NR) * es)];
           if (r > 0) {
             float2 w = tw[r * k * (N / (NS * R)) * tws];
             if (DIR > 0) w.y = -w.y;
@@ -363,8 +380,14 @@ __device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2
       for (int q = 0; q < BPT; ++q) {
         const int j = t + TPS * q;
         const int jo = (j / NS) * NS * R + (j % NS);
+        if constexpr (FOLD_WR) {
+          const int w0 = lds_phys<LAYOUT>(base + jo);
 #pragma unroll
-        for (int r = 0; r < R; ++r) lds[lds_phys<LAYOUT>(base + (jo + r * NS) * es)] = a[q + BPT * r];
+          for (int r = 0; r < R; ++r) lds[w0 + pad_offset(r * NS)] = a[q + BPT * r];
+        } else {
+#pragma unroll
+          for (int r = 0; r < R; ++r) lds[lds_phys<LAYOUT>(base + (jo + r * NS) * es)] = a[q + BPT * r];
+        }
       }
       lds_barrier<WAVE>();
     }

@@ -61,6 +61,21 @@ constexpr int row_spw() {
   return s > 64 ? 64 : s;
 }
 
+// Sequence s's natural-order elements into the padded LDS rows (element e at
+// lds_phys(s N + e)), thread t holding elements t + TPS m.
+template <int N>
+__device__ __forceinline__ void row_to_lds(const float2 (&v)[FftCfg<N>::E], float2 *lds, int s, int t) {
+  constexpr int TPS = FftCfg<N>::TPS, E = FftCfg<N>::E;
+  if constexpr (N % 32 == 0 && TPS % 32 == 0) {
+    const int i0 = lds_phys<kRowLds>(s * N + t);
+#pragma unroll
+    for (int m = 0; m < E; ++m) lds[i0 + pad_offset(TPS * m)] = v[m];
+  } else {
+#pragma unroll
+    for (int m = 0; m < E; ++m) lds[lds_phys<kRowLds>(s * N + t + TPS * m)] = v[m];
+  }
+}
+
 // Real rows are transformed in pairs packed as one complex sequence z = a + i b.
 // A sequence uses TPS <= 64 threads, so a wavefront holds whole sequences and
 // the LDS exchanges need only wave-level ordering.
@@ -75,12 +90,13 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(const float *__
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
   stage_twiddles<N>(tw, threadIdx.x, SPW * TPS);
   const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
-  long long pair = (long long)xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
+  // 32-bit row arithmetic: the launchers keep planes * rows_per_plane below 2^31
+  int pair = xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
   const bool active = pair < npairs;
-  if (!active) pair = npairs - 1;
-  const long long row0 = 2 * pair;
-  const long long plane = row0 / rows_per_plane;
-  const int r0 = (int)(row0 - plane * rows_per_plane);
+  if (!active) pair = (int)npairs - 1;
+  const unsigned row0 = 2u * (unsigned)pair;
+  const long long plane = row0 / (unsigned)rows_per_plane;
+  const int r0 = (int)(row0 - (unsigned)plane * (unsigned)rows_per_plane);
   const float *xp = x + plane * in_plane_stride;
 
   float2 v[E];
@@ -96,8 +112,7 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(const float *__
   }
   fft_seq<N, -1, true, true, kRowLds>(v, t, lds, s * N, 1, tw, 1);
   lds_barrier<true>();
-#pragma unroll
-  for (int m = 0; m < E; ++m) lds[lds_phys<kRowLds>(s * N + t + TPS * m)] = v[m];
+  row_to_lds<N>(v, lds, s, t);
   lds_barrier<true>();
   if (!active) return;
   float2 *oa = out.main + plane * out.ps + (long long)r0 * out.rs;
@@ -120,7 +135,112 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(const float *__
   }
 }
 
-template <int N, int SPW, int MODE>
+// Input of the inverse real row transform of the pair (r0, r0 + 1) for thread t:
+// v[m] = A_k + i B_k at k = t + TPS m, where A and B are the Hermitian extensions of
+// the two rows' half spectra weighted by c_l (a1 at l = 0 and N/2, a1 b1 elsewhere,
+// 0 at l >= Lin), with real-part semantics at l = 0 and N/2.
+// Input-bin modes: LIN = 0 any Lin; LIN = 1 Lin = N/2 + 1; LIN = 2 Lin = N/4 + 1.  The
+// last two know at compile time which elements are zero, main-block bins or the
+// last (side-block) bin, and leave out the common factor a1 b1, which the caller
+// applies after the transform (b1 must be nonzero).
+template <int N, int LIN>
+__device__ __forceinline__ void c2r_gather(float2 (&v)[FftCfg<N>::E], const SpecLayout &in, long long plane, int r0,
+                                           int t, int Lin, float a1, float b1) {
+  using Cfg = FftCfg<N>;
+  constexpr int TPS = Cfg::TPS, E = Cfg::E;
+  const float2 *ia = in.main + plane * in.ps + (long long)r0 * in.rs;
+  const float2 *ib = ia + in.rs;
+  const float2 *sa = in.side + plane * in.sps + (long long)r0 * in.srs;
+  if constexpr (LIN == 0) {
+#pragma unroll
+    for (int m = 0; m < E; ++m) {
+      const int k = t + TPS * m;
+      const bool upper = 2 * k > N;
+      const int kk = upper ? N - k : k;
+      // unconditional loads from valid addresses; bins beyond Lin get weight 0 (the loaded
+      // value is always used, so the load is not sunk into a per-lane branch)
+      const bool in_main = kk < Lin - 1;
+      const float2 *pa = in_main ? ia + kk : sa;
+      const float2 *pb = in_main ? ib + kk : sa + in.srs;
+      float2 a = *pa, b = *pb;
+      const bool edge = (kk == 0 || 2 * kk == N);
+      const float wgt = kk < Lin ? (edge ? a1 : a1 * b1) : 0.f;
+      a = cscale(a, wgt);
+      b = cscale(b, wgt);
+      if (edge) {  // real-part semantics of the inverse at l = 0 and l = n/2
+        a.y = 0.f;
+        b.y = 0.f;
+      }
+      if (upper) {  // Hermitian extension of each real row's half spectrum
+        a.y = -a.y;
+        b.y = -b.y;
+      }
+      v[m] = make_float2(a.x - b.y, a.y + b.x);  // A + i B
+    }
+  } else {
+    static_assert(E % (LIN == 1 ? 2 : 4) == 0, "input-bin mode needs E divisible by 2 (LIN 1) or 4 (LIN 2)");
+    (void)Lin;
+    (void)a1;
+    constexpr int KS = LIN == 1 ? N / 2 : N / 4;  // the side-block bin, Lin - 1
+    const float2 *sb = sa + in.srs;
+    const float e1 = 1.f / b1;  // edge weight a1 relative to the common a1 b1
+    const bool t0 = t == 0;
+    // Lane conditions act through pointer selects and multipliers, never through a
+    // branch around a load (which would make the load wait for its data alone).
+    const float ex = t0 ? e1 : 1.f, ey = t0 ? 0.f : 1.f;
+    static_for<0, E>([&](auto mc) {
+      constexpr int m = decltype(mc)::value;
+      constexpr bool low = m < E / 2;  // k < N/2: bin k; otherwise bin N - k, conjugated
+      // LIN 2: bins above N/4 are dropped, which empties m in (E/4, 3E/4) and, at
+      // m = E/4, every lane but t = 0 (bin N/4)
+      if constexpr (LIN == 2 && m > E / 4 && m < 3 * E / 4) {
+        v[m] = make_float2(0.f, 0.f);
+        return;
+      }
+      float2 a, b;
+      if constexpr (LIN == 2 && m == E / 4) {
+        const float keep = t0 ? 1.f : 0.f;
+        a = cscale(*sa, keep);
+        b = cscale(*sb, keep);
+      } else {
+        // m whose lane t = 0 holds the side bin KS (bin KS - t on the other lanes)
+        constexpr bool side_m = (LIN == 1 && m == E / 2) || (LIN == 2 && m == 3 * E / 4);
+        if constexpr (side_m) {
+          const float2 *pa = t0 ? sa : ia + (KS - t);
+          const float2 *pb = t0 ? sb : ib + (KS - t);
+          a = *pa;
+          b = *pb;
+        } else {
+          const int kk = low ? t + TPS * m : N - t - TPS * m;
+          a = ia[kk];
+          b = ib[kk];
+        }
+        // l = 0 (m = 0, t = 0) and, with LIN 1, l = N/2 (m = E/2, t = 0): weight a1 and
+        // real-part semantics
+        if constexpr (m == 0 || (LIN == 1 && m == E / 2)) {
+          a = make_float2(a.x * ex, a.y * ey);
+          b = make_float2(b.x * ex, b.y * ey);
+        }
+      }
+      if constexpr (!low) {
+        a.y = -a.y;
+        b.y = -b.y;
+      }
+      v[m] = make_float2(a.x - b.y, a.y + b.x);
+    });
+  }
+}
+
+// Input-bin mode of c2r_gather for Lin bins of an N-point row (and weight b1).
+template <int N>
+int c2r_lin_mode(int Lin, float b1) {
+  if (b1 == 0.f) return 0;
+  if (Lin == N / 2 + 1 && FftCfg<N>::E % 2 == 0) return 1;
+  if (Lin == N / 4 + 1 && N % 4 == 0 && FftCfg<N>::E % 4 == 0) return 2;
+  return 0;
+}
+
+template <int N, int SPW, int MODE, int LIN>
 __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(SpecLayout in, float *__restrict__ y,
                                                                 long long npairs, int rows_per_plane, int L,
                                                                 float alpha, float beta, ImgView view,
@@ -131,52 +251,26 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
   stage_twiddles<N>(tw, threadIdx.x, SPW * TPS);
   const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
-  long long pair = (long long)xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
+  // 32-bit row arithmetic: the launchers keep planes * rows_per_plane below 2^31
+  int pair = xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
   const bool active = pair < npairs;
-  if (!active) pair = npairs - 1;
-  const long long row0 = 2 * pair;
-  const long long plane = row0 / rows_per_plane;
-  const int r0 = (int)(row0 - plane * rows_per_plane);
-  const float2 *ia = in.main + plane * in.ps + (long long)r0 * in.rs;
-  const float2 *ib = ia + in.rs;
-  const float2 *sa = in.side + plane * in.sps + (long long)r0 * in.srs;
-
+  if (!active) pair = (int)npairs - 1;
+  const unsigned row0 = 2u * (unsigned)pair;
+  const long long plane = row0 / (unsigned)rows_per_plane;
+  const int r0 = (int)(row0 - (unsigned)plane * (unsigned)rows_per_plane);
   float2 v[E];
-#pragma unroll
-  for (int m = 0; m < E; ++m) {
-    const int k = t + TPS * m;
-    const bool upper = 2 * k > N;
-    const int kk = upper ? N - k : k;
-    // unconditional loads from valid addresses; bins beyond L get weight 0 (the loaded
-    // value is always used, so the load is not sunk into a per-lane branch)
-    const bool in_main = kk < L - 1;
-    const float2 *pa = in_main ? ia + kk : sa;
-    const float2 *pb = in_main ? ib + kk : sa + in.srs;
-    float2 a = *pa, b = *pb;
-    const bool edge = (kk == 0 || 2 * kk == N);
-    const float wgt = kk < L ? (edge ? alpha : alpha * beta) : 0.f;
-    a = cscale(a, wgt);
-    b = cscale(b, wgt);
-    if (edge) {  // real-part semantics of the inverse at l = 0 and l = n/2
-      a.y = 0.f;
-      b.y = 0.f;
-    }
-    if (upper) {  // Hermitian extension of each real row's half spectrum
-      a.y = -a.y;
-      b.y = -b.y;
-    }
-    v[m] = make_float2(a.x - b.y, a.y + b.x);  // A + i B
-  }
+  c2r_gather<N, LIN>(v, in, plane, r0, t, L, alpha, beta);
   fft_seq<N, +1, true, true, kRowLds>(v, t, lds, s * N, 1, tw, 1);
   if (!active) return;
+  const float sc = LIN == 0 ? 1.f : alpha * beta;  // the factor c2r_gather left out
   float *yp = y + plane * out_plane_stride;
 #pragma unroll
   for (int m = 0; m < E; ++m) {
     const int w = t + TPS * m;
     const int oa = view_index<MODE>(view, N, r0, w);
     const int ob = view_index<MODE>(view, N, r0 + 1, w);
-    if (oa >= 0) yp[oa] = v[m].x;
-    if (ob >= 0) yp[ob] = v[m].y;
+    if (oa >= 0) yp[oa] = LIN == 0 ? v[m].x : v[m].x * sc;
+    if (ob >= 0) yp[ob] = LIN == 0 ? v[m].y : v[m].y * sc;
   }
 }
 
@@ -186,7 +280,7 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
 // the two real rows of each pair, kept in registers -> out (Lout bins, weights as
 // k_row_r2c with a2, b2).  The same rows, pairing and arithmetic as k_row_c2r
 // followed by k_row_r2c, without writing the real rows to memory.
-template <int N, int SPW>
+template <int N, int SPW, int LIN>
 __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r_r2c(SpecLayout in, int Lin, float a1, float b1,
                                                                     SpecLayout out, int Lout, float a2, float b2,
                                                                     long long npairs, int rows_per_plane) {
@@ -196,54 +290,29 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r_r2c(SpecLayout 
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
   stage_twiddles<N>(tw, threadIdx.x, SPW * TPS);
   const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
-  long long pair = (long long)xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
+  // 32-bit row arithmetic: the launchers keep planes * rows_per_plane below 2^31
+  int pair = xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
   const bool active = pair < npairs;
-  if (!active) pair = npairs - 1;
-  const long long row0 = 2 * pair;
-  const long long plane = row0 / rows_per_plane;
-  const int r0 = (int)(row0 - plane * rows_per_plane);
-  const float2 *ia = in.main + plane * in.ps + (long long)r0 * in.rs;
-  const float2 *ib = ia + in.rs;
-  const float2 *sa = in.side + plane * in.sps + (long long)r0 * in.srs;
-
+  if (!active) pair = (int)npairs - 1;
+  const unsigned row0 = 2u * (unsigned)pair;
+  const long long plane = row0 / (unsigned)rows_per_plane;
+  const int r0 = (int)(row0 - (unsigned)plane * (unsigned)rows_per_plane);
   float2 v[E];
-#pragma unroll
-  for (int m = 0; m < E; ++m) {
-    const int k = t + TPS * m;
-    const bool upper = 2 * k > N;
-    const int kk = upper ? N - k : k;
-    const bool in_main = kk < Lin - 1;
-    const float2 *pa = in_main ? ia + kk : sa;
-    const float2 *pb = in_main ? ib + kk : sa + in.srs;
-    float2 a = *pa, b = *pb;
-    const bool edge = (kk == 0 || 2 * kk == N);
-    const float wgt = kk < Lin ? (edge ? a1 : a1 * b1) : 0.f;
-    a = cscale(a, wgt);
-    b = cscale(b, wgt);
-    if (edge) {
-      a.y = 0.f;
-      b.y = 0.f;
-    }
-    if (upper) {
-      a.y = -a.y;
-      b.y = -b.y;
-    }
-    v[m] = make_float2(a.x - b.y, a.y + b.x);
-  }
+  c2r_gather<N, LIN>(v, in, plane, r0, t, Lin, a1, b1);
   fft_seq<N, +1, true, true, kRowLds>(v, t, lds, s * N, 1, tw, 1);
   // v[m] = (row r0, row r0 + 1) at column t + TPS m: the packed input of the forward transform
   fft_seq<N, -1, true, true, kRowLds>(v, t, lds, s * N, 1, tw, 1);
   lds_barrier<true>();
-#pragma unroll
-  for (int m = 0; m < E; ++m) lds[lds_phys<kRowLds>(s * N + t + TPS * m)] = v[m];
+  row_to_lds<N>(v, lds, s, t);
   lds_barrier<true>();
   if (!active) return;
+  const float a2s = LIN == 0 ? a2 : a2 * (a1 * b1);  // with the factor c2r_gather left out
   float2 *oa = out.main + plane * out.ps + (long long)r0 * out.rs;
   float2 *ob = oa + out.rs;
   for (int k = t; k < Lout; k += TPS) {
     const float2 zk = lds[lds_phys<kRowLds>(s * N + k)];
     const float2 zn = lds[lds_phys<kRowLds>(s * N + (k == 0 ? 0 : N - k))];
-    const float wgt = 0.5f * bin_weight(k, N, a2, b2);
+    const float wgt = 0.5f * bin_weight(k, N, a2s, b2);
     const float2 A = make_float2((zk.x + zn.x) * wgt, (zk.y - zn.y) * wgt);
     const float2 Bv = make_float2((zk.y + zn.y) * wgt, (zn.x - zk.x) * wgt);
     if (k < Lout - 1) {
@@ -823,6 +892,7 @@ static unsigned grid_stride_blocks(long long total, int block) {
 hipError_t launch_row_r2c(int n, const float *x, SpecLayout out, long long planes, int rows_per_plane,
                           ImgView in_view, long long in_plane_stride, int L, float alpha, float beta, hipStream_t s) {
   hipError_t err = hipErrorInvalidValue;
+  if (planes * rows_per_plane >= (1LL << 31)) return err;
   dispatch_n(n, [&](auto nc) {
     constexpr int N = decltype(nc)::value;
     constexpr int SPW = row_spw<N>();
@@ -850,6 +920,7 @@ hipError_t launch_row_r2c(int n, const float *x, SpecLayout out, long long plane
 hipError_t launch_row_c2r(int n, SpecLayout in, float *y, long long planes, int rows_per_plane, int L, float alpha,
                           float beta, ImgView out_view, long long out_plane_stride, hipStream_t s) {
   hipError_t err = hipErrorInvalidValue;
+  if (planes * rows_per_plane >= (1LL << 31)) return err;
   dispatch_n(n, [&](auto nc) {
     constexpr int N = decltype(nc)::value;
     constexpr int SPW = row_spw<N>();
@@ -857,18 +928,24 @@ hipError_t launch_row_c2r(int n, SpecLayout in, float *y, long long planes, int 
     const unsigned grid = (unsigned)((npairs + SPW - 1) / SPW);
     const size_t lds = (twiddle_lds_elems<N>() + lds_size<kRowLds>(SPW * N)) * sizeof(float2);
     static const std::string nm = "row_c2r_" + std::to_string(N);
+    auto go = [&](auto kern) {
+      err = launch(nm.c_str(), kern, grid, SPW * FftCfg<N>::TPS, lds, s, in, y, npairs, rows_per_plane, L, alpha,
+                   beta, out_view, out_plane_stride);
+    };
     switch (out_view.mode) {
       case 0:
-        err = launch(nm.c_str(), k_row_c2r<N, SPW, 0>, grid, SPW * FftCfg<N>::TPS, lds, s, in, y, npairs,
-                     rows_per_plane, L, alpha, beta, out_view, out_plane_stride);
+        switch (c2r_lin_mode<N>(L, beta)) {
+          case 1:
+            if constexpr (FftCfg<N>::E % 2 == 0) go(k_row_c2r<N, SPW, 0, 1>);
+            break;
+          case 2:
+            if constexpr (FftCfg<N>::E % 4 == 0) go(k_row_c2r<N, SPW, 0, 2>);
+            break;
+          default: go(k_row_c2r<N, SPW, 0, 0>);
+        }
         break;
-      case 1:
-        err = launch(nm.c_str(), k_row_c2r<N, SPW, 1>, grid, SPW * FftCfg<N>::TPS, lds, s, in, y, npairs,
-                     rows_per_plane, L, alpha, beta, out_view, out_plane_stride);
-        break;
-      default:
-        err = launch(nm.c_str(), k_row_c2r<N, SPW, 2>, grid, SPW * FftCfg<N>::TPS, lds, s, in, y, npairs,
-                     rows_per_plane, L, alpha, beta, out_view, out_plane_stride);
+      case 1: go(k_row_c2r<N, SPW, 1, 0>); break;
+      default: go(k_row_c2r<N, SPW, 2, 0>);
     }
   });
   return err;
@@ -877,6 +954,7 @@ hipError_t launch_row_c2r(int n, SpecLayout in, float *y, long long planes, int 
 hipError_t launch_row_c2r_r2c(int n, SpecLayout in, int Lin, float a1, float b1, SpecLayout out, int Lout, float a2,
                               float b2, long long planes, int rows_per_plane, hipStream_t s) {
   hipError_t err = hipErrorInvalidValue;
+  if (planes * rows_per_plane >= (1LL << 31)) return err;
   dispatch_n(n, [&](auto nc) {
     constexpr int N = decltype(nc)::value;
     constexpr int SPW = row_spw<N>();
@@ -884,8 +962,19 @@ hipError_t launch_row_c2r_r2c(int n, SpecLayout in, int Lin, float a1, float b1,
     const unsigned grid = (unsigned)((npairs + SPW - 1) / SPW);
     const size_t lds = (twiddle_lds_elems<N>() + lds_size<kRowLds>(SPW * N)) * sizeof(float2);
     static const std::string nm = "row_c2r_r2c_" + std::to_string(N);
-    err = launch(nm.c_str(), k_row_c2r_r2c<N, SPW>, grid, SPW * FftCfg<N>::TPS, lds, s, in, Lin, a1, b1, out, Lout,
-                 a2, b2, npairs, rows_per_plane);
+    auto go = [&](auto kern) {
+      err = launch(nm.c_str(), kern, grid, SPW * FftCfg<N>::TPS, lds, s, in, Lin, a1, b1, out, Lout, a2, b2, npairs,
+                   rows_per_plane);
+    };
+    switch (c2r_lin_mode<N>(Lin, b1)) {
+      case 1:
+        if constexpr (FftCfg<N>::E % 2 == 0) go(k_row_c2r_r2c<N, SPW, 1>);
+        break;
+      case 2:
+        if constexpr (FftCfg<N>::E % 4 == 0) go(k_row_c2r_r2c<N, SPW, 2>);
+        break;
+      default: go(k_row_c2r_r2c<N, SPW, 0>);
+    }
   });
   return err;
 }
