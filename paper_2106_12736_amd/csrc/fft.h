@@ -238,15 +238,17 @@ struct FftCfg;
 // VGPRs of data) so that kernels stay at 4 or more waves per SIMD; TPS grows
 // with N, which lets the thread layouts of an N- and an M-point transform
 // (M < N) nest inside one workgroup.
-#define FDC_FFT_CFG(N_, TPS_, R0_, R1_, R2_, R3_)                                  \
-  template <>                                                                     \
-  struct FftCfg<N_> {                                                             \
-    static constexpr int N = N_;                                                  \
-    static constexpr int TPS = TPS_;                                              \
-    static constexpr int E = N_ / TPS_;                                           \
-    static constexpr int R[4] = {R0_, R1_, R2_, R3_};                             \
-    static constexpr int P = (R1_ == 1) ? 1 : (R2_ == 1 ? 2 : (R3_ == 1 ? 3 : 4)); \
-  };
+template <int N_, int TPS_, int R0_, int R1_, int R2_, int R3_>
+struct FftPlan {
+  static constexpr int N = N_;
+  static constexpr int TPS = TPS_;
+  static constexpr int E = N_ / TPS_;
+  static constexpr int R[4] = {R0_, R1_, R2_, R3_};
+  static constexpr int P = (R1_ == 1) ? 1 : (R2_ == 1 ? 2 : (R3_ == 1 ? 3 : 4));
+};
+#define FDC_FFT_CFG(N_, TPS_, R0_, R1_, R2_, R3_) \
+  template <>                                     \
+  struct FftCfg<N_> : FftPlan<N_, TPS_, R0_, R1_, R2_, R3_> {};
 //            N   TPS  radices
 FDC_FFT_CFG(2, 1, 2, 1, 1, 1)
 FDC_FFT_CFG(4, 1, 4, 1, 1, 1)
@@ -261,10 +263,15 @@ FDC_FFT_CFG(1024, 64, 16, 8, 8, 1)
 FDC_FFT_CFG(224, 8, 7, 4, 4, 2)
 #undef FDC_FFT_CFG
 
+// Plans of the row transforms (one sequence per TPS <= 64 lanes, LDS exchanges
+// ordered per wave); the same as FftCfg unless specialised.
 template <int N>
+struct RowCfg : FftCfg<N> {};
+
+template <class Cfg>
 constexpr int stockham_ns(int p) {  // product of the radices before pass p
   int ns = 1;
-  for (int i = 0; i < p; ++i) ns *= FftCfg<N>::R[i];
+  for (int i = 0; i < p; ++i) ns *= Cfg::R[i];
   return ns;
 }
 
@@ -319,10 +326,11 @@ constexpr int pad_offset(int c) { return c + c / 32; }
 // waits for every thread's earlier use of the LDS.  LAYOUT: lds_phys layout; with
 // kLdsPad, es must be 1 and, when N is a multiple of 32, base a multiple of 32.
 // tw: twiddle table in LDS (stage_twiddles) of length N * tws.
-template <int N, int DIR, bool LEAD_SYNC = true, bool WAVE = false, int LAYOUT = kLdsPlain>
-__device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2 *lds, int base, int es,
-                                        const float2 *tw, int tws) {
-  using C = FftCfg<N>;
+template <int N, int DIR, bool LEAD_SYNC = true, bool WAVE = false, int LAYOUT = kLdsPlain, class Cfg = FftCfg<N>>
+__device__ __forceinline__ void fft_seq(float2 (&v)[Cfg::E], int t, float2 *lds, int base, int es, const float2 *tw,
+                                        int tws) {
+  using C = Cfg;
+  static_assert(C::N == N, "plan length");
   constexpr int E = C::E;
   constexpr int TPS = C::TPS;
   constexpr bool PAD = LAYOUT == kLdsPad && N % 32 == 0;
@@ -330,7 +338,7 @@ __device__ __forceinline__ void fft_seq(float2 (&v)[FftCfg<N>::E], int t, float2
     constexpr int p = decltype(pc)::value;
     constexpr int R = C::R[p];
     constexpr int BPT = E / R;       // butterflies per thread in this pass
-    constexpr int NS = stockham_ns<N>(p);
+    constexpr int NS = stockham_ns<C>(p);
     constexpr int NR = N / R;
     static_assert(BPT * R == E && BPT * TPS == NR, "radix plan does not fit the thread layout");
     // folded padded addressing of this pass's reads (j + r NR, and j = t + TPS q)

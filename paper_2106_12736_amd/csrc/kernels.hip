@@ -57,15 +57,15 @@ constexpr int kColLds = kLdsPlain;
 // Row pairs per workgroup: 256 threads, at most 64 pairs.
 template <int N>
 constexpr int row_spw() {
-  constexpr int s = 256 / FftCfg<N>::TPS;
+  constexpr int s = 256 / RowCfg<N>::TPS;
   return s > 64 ? 64 : s;
 }
 
 // Sequence s's natural-order elements into the padded LDS rows (element e at
 // lds_phys(s N + e)), thread t holding elements t + TPS m.
 template <int N>
-__device__ __forceinline__ void row_to_lds(const float2 (&v)[FftCfg<N>::E], float2 *lds, int s, int t) {
-  constexpr int TPS = FftCfg<N>::TPS, E = FftCfg<N>::E;
+__device__ __forceinline__ void row_to_lds(const float2 (&v)[RowCfg<N>::E], float2 *lds, int s, int t) {
+  constexpr int TPS = RowCfg<N>::TPS, E = RowCfg<N>::E;
   if constexpr (N % 32 == 0 && TPS % 32 == 0) {
     const int i0 = lds_phys<kRowLds>(s * N + t);
 #pragma unroll
@@ -80,11 +80,11 @@ __device__ __forceinline__ void row_to_lds(const float2 (&v)[FftCfg<N>::E], floa
 // A sequence uses TPS <= 64 threads, so a wavefront holds whole sequences and
 // the LDS exchanges need only wave-level ordering.
 template <int N, int SPW, int MODE>
-__global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(const float *__restrict__ x, SpecLayout out,
+__global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_r2c(const float *__restrict__ x, SpecLayout out,
                                                                 long long npairs, int rows_per_plane, ImgView view,
                                                                 long long in_plane_stride, int L, float alpha,
                                                                 float beta) {
-  using Cfg = FftCfg<N>;
+  using Cfg = RowCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   static_assert(TPS <= 64, "a row sequence must fit in one wavefront");
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
@@ -110,7 +110,7 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(const float *__
     const float xa = xp[ia < 0 ? 0 : ia], xb = xp[ib < 0 ? 0 : ib];
     v[m] = make_float2(ia >= 0 ? xa : 0.f, ib >= 0 ? xb : 0.f);
   }
-  fft_seq<N, -1, true, true, kRowLds>(v, t, lds, s * N, 1, tw, 1);
+  fft_seq<N, -1, true, true, kRowLds, RowCfg<N>>(v, t, lds, s * N, 1, tw, 1);
   lds_barrier<true>();
   row_to_lds<N>(v, lds, s, t);
   lds_barrier<true>();
@@ -144,9 +144,9 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_r2c(const float *__
 // last (side-block) bin, and leave out the common factor a1 b1, which the caller
 // applies after the transform (b1 must be nonzero).
 template <int N, int LIN>
-__device__ __forceinline__ void c2r_gather(float2 (&v)[FftCfg<N>::E], const SpecLayout &in, long long plane, int r0,
+__device__ __forceinline__ void c2r_gather(float2 (&v)[RowCfg<N>::E], const SpecLayout &in, long long plane, int r0,
                                            int t, int Lin, float a1, float b1) {
-  using Cfg = FftCfg<N>;
+  using Cfg = RowCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   const float2 *ia = in.main + plane * in.ps + (long long)r0 * in.rs;
   const float2 *ib = ia + in.rs;
@@ -235,17 +235,17 @@ __device__ __forceinline__ void c2r_gather(float2 (&v)[FftCfg<N>::E], const Spec
 template <int N>
 int c2r_lin_mode(int Lin, float b1) {
   if (b1 == 0.f) return 0;
-  if (Lin == N / 2 + 1 && FftCfg<N>::E % 2 == 0) return 1;
-  if (Lin == N / 4 + 1 && N % 4 == 0 && FftCfg<N>::E % 4 == 0) return 2;
+  if (Lin == N / 2 + 1 && RowCfg<N>::E % 2 == 0) return 1;
+  if (Lin == N / 4 + 1 && N % 4 == 0 && RowCfg<N>::E % 4 == 0) return 2;
   return 0;
 }
 
 template <int N, int SPW, int MODE, int LIN>
-__global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(SpecLayout in, float *__restrict__ y,
+__global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r(SpecLayout in, float *__restrict__ y,
                                                                 long long npairs, int rows_per_plane, int L,
                                                                 float alpha, float beta, ImgView view,
                                                                 long long out_plane_stride) {
-  using Cfg = FftCfg<N>;
+  using Cfg = RowCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   static_assert(TPS <= 64, "a row sequence must fit in one wavefront");
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
@@ -260,7 +260,7 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
   const int r0 = (int)(row0 - (unsigned)plane * (unsigned)rows_per_plane);
   float2 v[E];
   c2r_gather<N, LIN>(v, in, plane, r0, t, L, alpha, beta);
-  fft_seq<N, +1, true, true, kRowLds>(v, t, lds, s * N, 1, tw, 1);
+  fft_seq<N, +1, true, true, kRowLds, RowCfg<N>>(v, t, lds, s * N, 1, tw, 1);
   if (!active) return;
   const float sc = LIN == 0 ? 1.f : alpha * beta;  // the factor c2r_gather left out
   float *yp = y + plane * out_plane_stride;
@@ -281,10 +281,10 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
 // k_row_r2c with a2, b2).  The same rows, pairing and arithmetic as k_row_c2r
 // followed by k_row_r2c, without writing the real rows to memory.
 template <int N, int SPW, int LIN>
-__global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r_r2c(SpecLayout in, int Lin, float a1, float b1,
+__global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r_r2c(SpecLayout in, int Lin, float a1, float b1,
                                                                     SpecLayout out, int Lout, float a2, float b2,
                                                                     long long npairs, int rows_per_plane) {
-  using Cfg = FftCfg<N>;
+  using Cfg = RowCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   static_assert(TPS <= 64, "a row sequence must fit in one wavefront");
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
@@ -299,9 +299,9 @@ __global__ __launch_bounds__(SPW *FftCfg<N>::TPS) void k_row_c2r_r2c(SpecLayout 
   const int r0 = (int)(row0 - (unsigned)plane * (unsigned)rows_per_plane);
   float2 v[E];
   c2r_gather<N, LIN>(v, in, plane, r0, t, Lin, a1, b1);
-  fft_seq<N, +1, true, true, kRowLds>(v, t, lds, s * N, 1, tw, 1);
+  fft_seq<N, +1, true, true, kRowLds, RowCfg<N>>(v, t, lds, s * N, 1, tw, 1);
   // v[m] = (row r0, row r0 + 1) at column t + TPS m: the packed input of the forward transform
-  fft_seq<N, -1, true, true, kRowLds>(v, t, lds, s * N, 1, tw, 1);
+  fft_seq<N, -1, true, true, kRowLds, RowCfg<N>>(v, t, lds, s * N, 1, tw, 1);
   lds_barrier<true>();
   row_to_lds<N>(v, lds, s, t);
   lds_barrier<true>();
@@ -902,15 +902,15 @@ hipError_t launch_row_r2c(int n, const float *x, SpecLayout out, long long plane
     static const std::string nm = "row_r2c_" + std::to_string(N);
     switch (in_view.mode) {
       case 0:
-        err = launch(nm.c_str(), k_row_r2c<N, SPW, 0>, grid, SPW * FftCfg<N>::TPS, lds, s, x, out, npairs,
+        err = launch(nm.c_str(), k_row_r2c<N, SPW, 0>, grid, SPW * RowCfg<N>::TPS, lds, s, x, out, npairs,
                      rows_per_plane, in_view, in_plane_stride, L, alpha, beta);
         break;
       case 1:
-        err = launch(nm.c_str(), k_row_r2c<N, SPW, 1>, grid, SPW * FftCfg<N>::TPS, lds, s, x, out, npairs,
+        err = launch(nm.c_str(), k_row_r2c<N, SPW, 1>, grid, SPW * RowCfg<N>::TPS, lds, s, x, out, npairs,
                      rows_per_plane, in_view, in_plane_stride, L, alpha, beta);
         break;
       default:
-        err = launch(nm.c_str(), k_row_r2c<N, SPW, 2>, grid, SPW * FftCfg<N>::TPS, lds, s, x, out, npairs,
+        err = launch(nm.c_str(), k_row_r2c<N, SPW, 2>, grid, SPW * RowCfg<N>::TPS, lds, s, x, out, npairs,
                      rows_per_plane, in_view, in_plane_stride, L, alpha, beta);
     }
   });
@@ -929,17 +929,17 @@ hipError_t launch_row_c2r(int n, SpecLayout in, float *y, long long planes, int 
     const size_t lds = (twiddle_lds_elems<N>() + lds_size<kRowLds>(SPW * N)) * sizeof(float2);
     static const std::string nm = "row_c2r_" + std::to_string(N);
     auto go = [&](auto kern) {
-      err = launch(nm.c_str(), kern, grid, SPW * FftCfg<N>::TPS, lds, s, in, y, npairs, rows_per_plane, L, alpha,
+      err = launch(nm.c_str(), kern, grid, SPW * RowCfg<N>::TPS, lds, s, in, y, npairs, rows_per_plane, L, alpha,
                    beta, out_view, out_plane_stride);
     };
     switch (out_view.mode) {
       case 0:
         switch (c2r_lin_mode<N>(L, beta)) {
           case 1:
-            if constexpr (FftCfg<N>::E % 2 == 0) go(k_row_c2r<N, SPW, 0, 1>);
+            if constexpr (RowCfg<N>::E % 2 == 0) go(k_row_c2r<N, SPW, 0, 1>);
             break;
           case 2:
-            if constexpr (FftCfg<N>::E % 4 == 0) go(k_row_c2r<N, SPW, 0, 2>);
+            if constexpr (RowCfg<N>::E % 4 == 0) go(k_row_c2r<N, SPW, 0, 2>);
             break;
           default: go(k_row_c2r<N, SPW, 0, 0>);
         }
@@ -963,15 +963,15 @@ hipError_t launch_row_c2r_r2c(int n, SpecLayout in, int Lin, float a1, float b1,
     const size_t lds = (twiddle_lds_elems<N>() + lds_size<kRowLds>(SPW * N)) * sizeof(float2);
     static const std::string nm = "row_c2r_r2c_" + std::to_string(N);
     auto go = [&](auto kern) {
-      err = launch(nm.c_str(), kern, grid, SPW * FftCfg<N>::TPS, lds, s, in, Lin, a1, b1, out, Lout, a2, b2, npairs,
+      err = launch(nm.c_str(), kern, grid, SPW * RowCfg<N>::TPS, lds, s, in, Lin, a1, b1, out, Lout, a2, b2, npairs,
                    rows_per_plane);
     };
     switch (c2r_lin_mode<N>(Lin, b1)) {
       case 1:
-        if constexpr (FftCfg<N>::E % 2 == 0) go(k_row_c2r_r2c<N, SPW, 1>);
+        if constexpr (RowCfg<N>::E % 2 == 0) go(k_row_c2r_r2c<N, SPW, 1>);
         break;
       case 2:
-        if constexpr (FftCfg<N>::E % 4 == 0) go(k_row_c2r_r2c<N, SPW, 2>);
+        if constexpr (RowCfg<N>::E % 4 == 0) go(k_row_c2r_r2c<N, SPW, 2>);
         break;
       default: go(k_row_c2r_r2c<N, SPW, 0>);
     }
