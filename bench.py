@@ -54,8 +54,21 @@ def layer_dims(wl, i):
     return wl.batch, C, S, N, M, M // 2 + 1, N // 2 + 1
 
 
-def step_launches(wl, input_grad=False):
-    """(kernel name, algorithmic bytes) of every launch of one step, in launch order."""
+def gk_launches(B, C, S, N, M, L, NF, ranges=1):
+    """dK of one layer: one launch that reads the upstream and saved spectra and writes
+    all of gK (zeros where FDP drops), or, with the batch cut into R ranges, the range
+    sums written by that launch and added in order by a second one."""
+    if ranges <= 1:
+        return [(f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + S * N * NF))]
+    R = ranges
+    return [(f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + R * S * M * L)),
+            ("gk_reduce", C64 * (R * S * M * L + S * N * NF))]
+
+
+def step_launches(wl, input_grad=False, ranges=None):
+    """(kernel name, algorithmic bytes) of every launch of one step, in launch order;
+    ranges[i]: dK batch ranges of layer i (fdc_cic_layer_dk_ranges, default 1)."""
+    ranges = ranges or [1] * wl.layers
     out = []
     for i in range(wl.layers):
         B, C, S, N, M, L, _ = layer_dims(wl, i)
@@ -66,18 +79,18 @@ def step_launches(wl, input_grad=False):
     for i in reversed(range(wl.layers)):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
         out.append((f"row_r2c_{M}", F32 * B * S * M * M + C64 * B * S * M * L))
-        # reads the upstream spectrum and the saved spectrum, writes all of gK (zeros where FDP drops)
-        out.append((f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + S * N * NF)))
+        out += gk_launches(B, C, S, N, M, L, NF, ranges[i])
         if i > 0 or input_grad:
             out.append((f"col_bwd_gx_{N}_{M}", C64 * (B * S * M * L + S * M * L + B * C * N * L)))
             out.append((f"row_c2r_{N}", C64 * B * C * N * L + F32 * B * C * N * N))
     return out
 
 
-def fused_step_launches(wl, input_grad=False):
+def fused_step_launches(wl, input_grad=False, ranges=None):
     """(kernel name, algorithmic bytes) of every launch of one step of the fused stack
     executor: as step_launches, with each layer boundary's inverse rows and the next
     layer's forward rows (and the backward's adjoint pair) in one kernel."""
+    ranges = ranges or [1] * wl.layers
     out = []
     n = wl.layers
     for i in range(n):
@@ -95,7 +108,7 @@ def fused_step_launches(wl, input_grad=False):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
         if i == n - 1:
             out.append((f"row_r2c_{M}", F32 * B * S * M * M + C64 * B * S * M * L))
-        out.append((f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + S * N * NF)))
+        out += gk_launches(B, C, S, N, M, L, NF, ranges[i])
         if i > 0 or input_grad:
             out.append((f"col_bwd_gx_{N}_{M}", C64 * (B * S * M * L + S * M * L + B * C * N * L)))
             if i > 0:
@@ -137,10 +150,11 @@ def chain_step_launches(wl, input_grad=False):
     return out
 
 
-def spatial_step_launches(wl, n, input_grad=False):
+def spatial_step_launches(wl, n, input_grad=False, ranges=None):
     """(kernel name, algorithmic bytes) of every launch of one step of the stack with
     n x n spatial kernels (layer by layer, ROLL): step_launches plus the kernel-spectrum
     formation before each layer's product and the weight-gradient projection."""
+    ranges = ranges or [1] * wl.layers
     out = []
     for i in range(wl.layers):
         B, C, S, N, M, L, _ = layer_dims(wl, i)
@@ -155,7 +169,7 @@ def spatial_step_launches(wl, n, input_grad=False):
         if gx:
             out.append(("cic_kspec", F32 * S * n * n + C64 * S * M * L))
         out.append((f"row_r2c_{M}", F32 * B * S * M * M + C64 * B * S * M * L))
-        out.append((f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + S * N * NF)))
+        out += gk_launches(B, C, S, N, M, L, NF, ranges[i])
         if gx:
             out.append((f"col_bwd_gx_{N}_{M}", C64 * (B * S * M * L + S * M * L + B * C * N * L)))
             out.append((f"row_c2r_{N}", C64 * B * C * N * L + F32 * B * C * N * N))
@@ -326,16 +340,16 @@ class CicStackRun:
             self.Ks = [torch.from_numpy(w).to(dev) for w in self.data.weights]
             self.g = torch.from_numpy(self.data.grad).to(dev)
             self.stack = layers.CicSpatialStack(wl.batch, wl.sizes, wl.channels, self.spatial, device=dev)
-            model = lambda w_, ig: spatial_step_launches(w_, self.spatial, ig)  # noqa: E731
+            model = lambda w_, ig: spatial_step_launches(w_, self.spatial, ig, self.stack.dk_ranges())  # noqa: E731
         elif args.chain:
             self.stack = layers.CicChain(wl.batch, wl.sizes, wl.channels, device=dev)
             model = chain_step_launches
         elif self.per_layer:
             self.stack = layers.CicStack(wl.batch, wl.sizes, wl.channels, device=dev)
-            model = step_launches
+            model = lambda w_, ig: step_launches(w_, ig, self.stack.dk_ranges())  # noqa: E731
         else:
             self.stack = layers.CicStackFused(wl.batch, wl.sizes, wl.channels, device=dev)
-            model = fused_step_launches
+            model = lambda w_, ig: fused_step_launches(w_, ig, self.stack.dk_ranges())  # noqa: E731
         self.gin = (torch.empty((wl.batch, wl.channels[0], wl.sizes[0], wl.sizes[0]), dtype=torch.float32,
                                 device=dev) if args.input_grad else None)
         self.input_grad = args.input_grad
@@ -363,7 +377,7 @@ class CicStackRun:
         return cpu_baseline(self.wl, self.data, chain=self.executor == "chain")
 
 
-def full_cic_step_launches(wl):
+def full_cic_step_launches(wl, ranges=1):
     """One step of the Full FDC layer with CIC (spatial kernels, no pooling, crop):
     forward, dL/dx and dL/dw."""
     B, C, S, P, n = wl.batch, wl.cin, wl.cout, wl.size, wl.n
@@ -377,7 +391,7 @@ def full_cic_step_launches(wl):
         (f"row_c2r_{P}", C64 * B * S * P * L + F32 * B * S * O * O),
         ("cic_kspec", F32 * S * n * n + C64 * S * P * L),
         (f"row_r2c_{P}", F32 * B * S * O * O + C64 * B * S * P * L),
-        (f"col_bwd_gk_{P}", C64 * (B * S * P * L + B * C * P * L + S * P * L)),
+        *gk_launches(B, C, S, P, P, L, L, ranges),
         (f"col_bwd_gx_{P}_{P}", C64 * (B * S * P * L + S * P * L + B * C * P * L)),
         (f"row_c2r_{P}", C64 * B * C * P * L + F32 * B * C * P * P),
         ("cic_wgrad", C64 * S * P * L),
@@ -404,7 +418,7 @@ class FullCicRun:
         self.y = self.layer.new_output()
         self.gx = torch.empty_like(self.x)
         self.gw = torch.empty_like(self.w)
-        self.launches = [(nm, b, "B") for nm, b in full_cic_step_launches(wl)]
+        self.launches = [(nm, b, "B") for nm, b in full_cic_step_launches(wl, self.layer.dk_ranges())]
         B, C, S, P, n = wl.batch, wl.cin, wl.cout, wl.size, wl.n
         O = P - n + 1
         self.api_bytes = F32 * (2 * B * C * P * P + 2 * B * S * O * O + 3 * S * n * n) + C64 * B * C * P * (P // 2 + 1)
@@ -529,6 +543,9 @@ def main():
                     help="CIC stack: the FDCNN data flow of section 2.5.1 (one rfft2, FDC + FDP layers on spectra, "
                          "one irfft2); a different function from the per-layer transforms")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of HIP graph replays")
+    ap.add_argument("--flush-mib", type=int, default=512, metavar="MIB",
+                    help="buffer written between the individually timed steps of the step-time "
+                         "distribution (evicts the last-level cache; 0: no flush)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the timed region, run one plain streaming copy kernel (dst = src * 1) over "
                          "MIB MiB, a known-size reference for the HBM traffic counters of a profiler run")
@@ -619,6 +636,33 @@ def main():
     # timed region 1: K steps (graph replays unless --eager)
     ms_per_step, wall_ms = timed(graph.replay if graph is not None else step)
 
+    # timed region 1b: the same steps bracketed one by one, for the distribution (p10,
+    # median, p90); back to back, and with a --flush-mib buffer written between steps
+    # (outside the brackets) so that every step starts with its data in HBM, not in the
+    # 256 MB last-level cache
+    def distribution(fn, flush):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(evs):
+            if flush is not None:
+                flush.fill_(float(i & 7))
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        ts = sorted(a.elapsed_time(b) for a, b in evs)
+        q = lambda f: ts[min(len(ts) - 1, int(round(f * (len(ts) - 1))))]
+        return {"p10": q(0.1), "median": q(0.5), "p90": q(0.9)}
+
+    stepfn = graph.replay if graph is not None else step
+    dist = {"back_to_back": distribution(stepfn, None)}
+    if args.flush_mib > 0:
+        flush = torch.empty(args.flush_mib * (1 << 20) // 4, dtype=torch.float32, device=dev)
+        dist["flushed"] = distribution(stepfn, flush)
+        dist["flushed"]["flush_mib"] = args.flush_mib
+        del flush
+
     # timed region 2: K eager steps, the dominant kernel's launches bracketed by HIP events
     # on the stream they run on (events cannot be placed inside a replayed graph)
     _lib.call("fdc_kernel_timing_enable", args.steps * dom_launches_per_step, dominant.encode())
@@ -663,6 +707,7 @@ def main():
         "step_api_bytes": run.api_bytes,
         "step_effective_gbps": run.api_bytes / (ms_per_step * 1e-3) / 1e9,
         "step_kernel_ms": {k: round(v[0], 5) for k, v in sorted(per_name.items(), key=lambda kv: -kv[1][0])},
+        "step_ms_dist": dist,
         "wall_ms_per_step": wall_ms,
         "eager_ms_per_step": eager_ms_per_step,
     }

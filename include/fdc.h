@@ -274,6 +274,17 @@ fdc_status fdc_kernel_timing_report(char *buf, size_t buf_bytes);
  * FDC_EINVAL when the text (with its terminating NUL) exceeds buf_bytes. */
 fdc_status fdc_kernel_timing_launches(char *buf, size_t buf_bytes);
 
+/* How a backward call forms dK (measurement support: which kernels it launches).
+ * *ranges = 1: one dK launch ("col_bwd_gk_<M>") writes all of gK.  *ranges = R > 1:
+ * the dK launch sums each of R contiguous image ranges into scratch inside the
+ * backward workspace (R [S][M][M/2+1] arrays), and a second launch ("gk_reduce")
+ * adds the ranges in range order and writes gK, so results stay repeatable.  R
+ * depends only on the plan: larger batches are cut into ranges so that enough
+ * workgroups run at once.  Layer plans of the spectral-kernel CIC layer (the
+ * plan's layer for the stack call); FDC_EINVAL for other plans or layers. */
+fdc_status fdc_cic_layer_dk_ranges(const fdc_layer_plan *plan, int *ranges);
+fdc_status fdc_cic_stack_dk_ranges(const fdc_stack_plan *plan, int layer, int *ranges);
+
 #ifdef __cplusplus
 }
 #endif

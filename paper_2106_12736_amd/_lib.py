@@ -64,6 +64,8 @@ _SIGS = {
     "fdc_kernel_timing_disable": [],
     "fdc_kernel_timing_report": [ctypes.c_char_p, _SZ],
     "fdc_kernel_timing_launches": [ctypes.c_char_p, _SZ],
+    "fdc_cic_layer_dk_ranges": [_P, ctypes.POINTER(_I)],
+    "fdc_cic_stack_dk_ranges": [_P, _I, ctypes.POINTER(_I)],
 }
 _RESTYPES = {"fdc_status_string": ctypes.c_char_p, "fdc_last_error": ctypes.c_char_p, "fdc_version": _I}
 

@@ -449,8 +449,10 @@ fdc_status fdc_cic_layer_backward(const fdc_layer_plan *p, const float *gy, cons
     return st;
   if (gK) {
     auto *gk = reinterpret_cast<float2 *>(gK);
+    // the dX buffer V (written only after dK) holds dK's batch-range sums
     if (fdc_status st = check_hip(fdc::launch_col_bwd_gk(N, M, Tg, reinterpret_cast<const float2 *>(saved), gk, B,
-                                                         C, S, s), "layer backward dK"))
+                                                         C, S, V, (long long)B * C * N * L, s),
+                                  "layer backward dK"))
       return st;
   }
   if (gx) {
@@ -689,8 +691,10 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, cons
                                     "stack backward rows"))
         return st;
     }
+    // V is free until the dX columns below: dK's batch-range sums go there
     if (fdc_status st = check_hip(fdc::launch_col_bwd_gk(g.N, g.M, Tg, reinterpret_cast<const float2 *>(saved[i]),
-                                                         reinterpret_cast<float2 *>(gK[i]), B, g.C, g.S, s),
+                                                         reinterpret_cast<float2 *>(gK[i]), B, g.C, g.S, V,
+                                                         (long long)p->ws_b, s),
                                   "stack backward dK"))
       return st;
     if (i == 0 && !gx) break;
@@ -916,6 +920,24 @@ fdc_status fdc_kernel_timing_report(char *buf, size_t buf_bytes) {
   }
   if (out.size() + 1 > buf_bytes) return fail(FDC_EINVAL, "report needs %zu bytes", out.size() + 1);
   memcpy(buf, out.c_str(), out.size() + 1);
+  return FDC_OK;
+}
+
+fdc_status fdc_cic_layer_dk_ranges(const fdc_layer_plan *p, int *ranges) {
+  if (fdc_status st = check_layer_plan(p, 0)) return st;
+  if (ranges == nullptr) return fail(FDC_EINVAL, "ranges is NULL");
+  // the same scratch as fdc_cic_layer_backward: the dX buffer
+  *ranges = fdc::gk_batch_ranges(p->N, p->M, p->B, p->S, (long long)p->B * p->C * p->N * (p->M / 2 + 1));
+  return FDC_OK;
+}
+
+fdc_status fdc_cic_stack_dk_ranges(const fdc_stack_plan *p, int layer, int *ranges) {
+  if (fdc_status st = check_stack_plan(p)) return st;
+  if (layer < 0 || layer >= p->layers) return fail(FDC_EINVAL, "layer %d outside [0, %d)", layer, p->layers);
+  if (ranges == nullptr) return fail(FDC_EINVAL, "ranges is NULL");
+  const StackLayer g = stack_layer(p, layer);
+  // the same scratch as fdc_cic_stack_backward: the dX buffer
+  *ranges = fdc::gk_batch_ranges(g.N, g.M, p->B, g.S, (long long)p->ws_b);
   return FDC_OK;
 }
 

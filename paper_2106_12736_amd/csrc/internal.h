@@ -100,8 +100,11 @@ hipError_t launch_col_fft_split(int n, int dir, SpecLayout in, SpecLayout out, l
 bool cic_pair_supported(int n, int m);
 hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, float2 *U, float2 *Xh, int B,
                               int C, int S, hipStream_t s);
+// dK: with scratch `part` (part_elems complex values; may be NULL) the batch is cut
+// into gk_batch_ranges(...) ranges whose sums are added in order by a second kernel.
+int gk_batch_ranges(int n, int m, int B, int S, long long part_elems);
 hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, float2 *gK, int B, int C,
-                             int S, hipStream_t s);
+                             int S, float2 *part, long long part_elems, hipStream_t s);
 hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, float2 *V, int B, int C, int S,
                              hipStream_t s);
 

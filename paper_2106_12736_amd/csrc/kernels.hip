@@ -19,6 +19,7 @@
 #include "fft.h"
 #include "internal.h"
 
+#include <algorithm>
 #include <string>
 
 namespace fdc {
@@ -559,6 +560,8 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS) void k_col_cic_inv(const float2
 // so narrow tiles keep the grid at hundreds of workgroups) and BP batch groups
 // per workgroup, up to 512 threads and at most 8 groups.
 constexpr int kGkCT = 8;
+// Workgroups the dK launch aims for before it cuts the batch into ranges.
+constexpr long long kGkTargetWgs = 512;
 template <int M>
 constexpr int gk_bp() {
   constexpr int bp = 512 / (kGkCT * FftCfg<M>::TPS);
@@ -567,30 +570,38 @@ constexpr int gk_bp() {
 
 // Backward, dL/dK: for the kernel-gradient columns (o, l), column DFT (M) of each
 // upstream-gradient column Tg[b][o] and dK += G conj(Xh[b][o/J]).
-// Group g of the BP groups sums b = g, g + BP, ...; the BP partial sums are then
-// added in group order, so the result does not depend on scheduling.
-// Writes all of gK [S][N][N/2+1]: the kept bins, and exact zeros at the rows and
-// columns FDP drops (rows of the tile's own columns; the columns l >= L of every
-// row are shared out over the whole grid).
+// The batch is cut into BG contiguous ranges, one per workgroup of a tile (grid =
+// tiles * BG, range index slowest); inside a workgroup, group g of the BP wave
+// groups sums b = lo + g, lo + g + BP, ... of its range, and the BP partial sums
+// are added in group order, so the result does not depend on scheduling.
+// BG = 1: writes all of gK [S][N][N/2+1], the kept bins and exact zeros at the
+// rows and columns FDP drops (rows of the tile's own columns; the columns l >= L
+// of every row are shared out over the whole grid).
+// BG > 1: writes range r's sums at the kept bins to part [BG][S][M][M/2+1];
+// k_gk_reduce then adds the ranges in order and writes gK.
 template <int M, int CT, int BP>
 __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const float2 *__restrict__ Tg,
                                                                       const float2 *__restrict__ Xh,
-                                                                      float2 *__restrict__ gK, int B, int C,
-                                                                      int J, int N, int S) {
+                                                                      float2 *__restrict__ gK,
+                                                                      float2 *__restrict__ part, int B, int C,
+                                                                      int J, int N, int S, int BG) {
   using CM = FftCfg<M>;
   constexpr int L = M / 2 + 1, TPS = CM::TPS, E = CM::E;
   constexpr int NT = CT * TPS * BP;
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<M>();
   stage_twiddles<M>(tw, threadIdx.x, NT);
   const int s = threadIdx.x % CT, t = (threadIdx.x / CT) % TPS, g = threadIdx.x / (CT * TPS);
-  const int wg = xcd_remap(blockIdx.x, gridDim.x);
+  const int lin = xcd_remap(blockIdx.x, gridDim.x);
+  const int tiles = gridDim.x / BG;
+  const int range = lin / tiles, wg = lin - range * tiles;
+  const int b_lo = range * B / BG, b_hi = (range + 1) * B / BG;
   // the J output channels of one input channel read the same pooled-input columns
   const ColRef c = column_ref<CT>(wg, s, L, S, J);
   const int o = c.plane, ci = o / J;
   const int nf = N / 2 + 1;
 
   // zeros of the columns l >= L: groups of LW lanes take the S * N rows in turn
-  {
+  if (BG == 1) {
     static_assert((NT & (NT - 1)) == 0, "NT must be a power of two");
     constexpr int LW = NT < 64 ? NT : 64;
     const int lane = threadIdx.x % LW;
@@ -602,9 +613,9 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
   float2 acc[E];
 #pragma unroll
   for (int m = 0; m < E; ++m) acc[m] = make_float2(0.f, 0.f);
-  for (int b0 = 0; b0 < B; b0 += BP) {
+  for (int b0 = b_lo; b0 < b_hi; b0 += BP) {
     const int b = b0 + g;
-    const bool act = c.ok && b < B;
+    const bool act = c.ok && b < b_hi;
     const ColPtr gc = split_col<M, L>(Tg, B * S, (act ? b : 0) * S + o, c.l);
     const ColPtr xc = split_col<M, L>(Xh, B * C, (act ? b : 0) * C + ci, c.l);
     // loads are unconditional (inactive lanes read a valid column); inactive lanes add nothing
@@ -643,6 +654,12 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
     }
   }
   if (!c.ok) return;
+  if (BG > 1) {
+    float2 *pcol = part + ((long long)range * S + o) * M * L + c.l;
+#pragma unroll
+    for (int m = 0; m < E; ++m) pcol[(long long)(t + TPS * m) * L] = acc[m];
+    return;
+  }
   float2 *kcol = gK + (long long)o * N * nf + c.l;
 #pragma unroll
   for (int m = 0; m < E; ++m) {
@@ -652,6 +669,26 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
   }
   // dropped rows [M/2, N - M/2) of this column; N - M is a multiple of TPS
   for (int k = M / 2 + t; k < N - M / 2; k += TPS) kcol[(long long)k * nf] = make_float2(0.f, 0.f);
+}
+
+// gK [S][N][N/2+1] from the BG range sums part [BG][S][M][M/2+1]: at the kept bins
+// the ranges added in order, zeros elsewhere.  A workgroup takes whole rows.
+__global__ __launch_bounds__(256) void k_gk_reduce(const float2 *__restrict__ part, float2 *__restrict__ gK, int BG,
+                                                   int S, int M, int N) {
+  const int L = M / 2 + 1, nf = N / 2 + 1;
+  const long long range_stride = (long long)S * M * L;
+  for (long long r = blockIdx.x; r < (long long)S * N; r += gridDim.x) {
+    const int o = (int)(r / N), krow = (int)(r - (long long)o * N);
+    const int mrow = krow < M / 2 ? krow : (krow >= N - M / 2 ? krow - (N - M) : -1);
+    float2 *dst = gK + r * nf;
+    const float2 *src = part + ((long long)o * M + (mrow < 0 ? 0 : mrow)) * L;
+    for (int l = threadIdx.x; l < nf; l += blockDim.x) {
+      float2 v = make_float2(0.f, 0.f);
+      if (mrow >= 0 && l < L)
+        for (int q = 0; q < BG; ++q) v = cadd(v, src[q * range_stride + l]);
+      dst[l] = v;
+    }
+  }
 }
 
 template <int N, int M>
@@ -1062,20 +1099,47 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
   return err;
 }
 
+int gk_batch_ranges(int n, int m, int B, int S, long long part_elems) {
+  int bg = 1;
+  dispatch_n(m, [&](auto mc) {
+    constexpr int M = decltype(mc)::value;
+    constexpr int L = M / 2 + 1;
+    constexpr int CT = col_ct_for(kGkCT, L), BP = gk_bp<M>();
+    const long long tiles = col_tile_count(S, L, CT);
+    // enough workgroups to fill the chip (kGkTargetWgs), at least BP batch entries per
+    // range, and range sums (written and read once more) of at most a quarter of Tg
+    // (at 8 images, two ranges measured slower than one)
+    long long want = (kGkTargetWgs + tiles - 1) / tiles;
+    want = std::min<long long>(want, std::max(1, B / 8));
+    want = std::min<long long>(want, std::max(1, B / BP));
+    const long long per = (long long)S * M * L;
+    want = std::min<long long>(want, per > 0 ? part_elems / per : 1);
+    if (tiles * want >= (1LL << 31)) want = 1;
+    bg = (int)std::max<long long>(1, want);
+  });
+  (void)n;
+  return bg;
+}
+
 hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, float2 *gK, int B, int C, int S,
-                             hipStream_t s) {
+                             float2 *part, long long part_elems, hipStream_t s) {
   hipError_t err = hipErrorInvalidValue;
   if (!cic_pair_supported(n, m)) return err;
+  const int BG = part ? gk_batch_ranges(n, m, B, S, part_elems) : 1;
   dispatch_n(m, [&](auto mc) {
     constexpr int M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
     constexpr int CT = col_ct_for(kGkCT, L), BP = gk_bp<M>();
     const size_t lds = (twiddle_lds_elems<M>() + lds_size<kColLds>(BP * M * CT)) * sizeof(float2);
-    const unsigned grid = col_grid(S, L, CT);
-    if (grid == 0) return;
+    const unsigned tiles = col_grid(S, L, CT);
+    if (tiles == 0) return;
     static const std::string nm = "col_bwd_gk_" + std::to_string(M);
-    err = launch(nm.c_str(), k_col_bwd_gk<M, CT, BP>, grid, CT * FftCfg<M>::TPS * BP, lds, s, Tg, Xh, gK, B, C,
-                 S / C, n, S);
+    err = launch(nm.c_str(), k_col_bwd_gk<M, CT, BP>, tiles * (unsigned)BG, CT * FftCfg<M>::TPS * BP, lds, s, Tg,
+                 Xh, gK, part, B, C, S / C, n, S, BG);
+    if (err != hipSuccess || BG == 1) return;
+    const long long rows = (long long)S * n;
+    const unsigned grid = (unsigned)std::min<long long>(rows, 8192);
+    err = launch("gk_reduce", k_gk_reduce, grid, 256, 0, s, (const float2 *)part, gK, BG, S, M, n);
   });
   return err;
 }

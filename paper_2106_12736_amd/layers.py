@@ -156,6 +156,12 @@ class CicLayer(_LayerPlan):
         """Buffer for the pooled input spectrum (see fdc_cic_layer_forward for its layout)."""
         return torch.empty(self.saved_bytes // 8, dtype=torch.complex64, device=self.device)
 
+    def dk_ranges(self):
+        """Image ranges the backward's dK step sums separately (fdc_cic_layer_dk_ranges)."""
+        r = ctypes.c_int()
+        call("fdc_cic_layer_dk_ranges", self._p, ctypes.byref(r))
+        return r.value
+
     def saved_spectrum(self, saved):
         """The M x (M/2+1) kept bins held in a saved buffer, as a [B][C][M][M/2+1] tensor:
         columns 0..M/2-1 come from the main block, column M/2 from the block after it."""
@@ -302,6 +308,9 @@ class CicSpatialStack:
             h = y
         return h
 
+    def dk_ranges(self):
+        return [layer.dk_ranges() for layer in self.layers]
+
     def backward(self, gy, weights, input_grad=None):
         g = gy
         for i in reversed(range(len(self.layers))):
@@ -332,6 +341,9 @@ class CicStack:
             layer.forward(h, K, y=y, saved=sv)
             h = y
         return h
+
+    def dk_ranges(self):
+        return [layer.dk_ranges() for layer in self.layers]
 
     def backward(self, gy, kernels, input_grad=None):
         """Gradients of every kernel (and of the input if `input_grad` is a tensor to fill)."""
@@ -386,6 +398,15 @@ class CicStackFused:
     def __del__(self):
         if getattr(self, "_p", None) and _lib._lib is not None:
             _lib.lib().fdc_cic_stack_plan_destroy(self._p)
+
+    def dk_ranges(self):
+        """Image ranges each layer's dK step sums separately (fdc_cic_stack_dk_ranges)."""
+        out = []
+        for i in range(self.layers):
+            r = ctypes.c_int()
+            call("fdc_cic_stack_dk_ranges", self._p, i, ctypes.byref(r))
+            out.append(r.value)
+        return out
 
     def _kernels(self, kernels):
         if len(kernels) != self.layers:

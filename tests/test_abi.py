@@ -268,3 +268,25 @@ def test_cic_fdp_validation():
     assert _lib.status("fdc_cic_fdp_backward", d, None, d, None, d, 2, 1, 4, 8, 4, None) == FDC_EINVAL  # gK needs X
     assert _lib.status("fdc_cic_fdp_backward", d, d, None, d, None, 2, 1, 4, 8, 4, None) == FDC_EINVAL  # gX needs K
     assert _lib.status("fdc_cic_fdp_backward", d, d, d, None, None, 2, 1, 4, 8, 4, None) == FDC_OK     # nothing asked
+
+
+def test_dk_ranges_queries():
+    """The dK batch-range count is a host-side function of the plan: one range at 8
+    images, several at 32 (the 512 stack); bad plans, layers and NULL outputs are
+    refused."""
+    r = ctypes.c_int()
+    lp = ctypes.c_void_p()
+    assert _lib.status("fdc_cic_layer_plan_create", ctypes.byref(lp), 8, 1, 8, 1024, 512, 0, 1) == FDC_OK
+    assert _lib.status("fdc_cic_layer_dk_ranges", lp, ctypes.byref(r)) == FDC_OK and r.value == 1
+    assert _lib.status("fdc_cic_layer_dk_ranges", lp, None) == FDC_EINVAL
+    assert _lib.status("fdc_layer_plan_destroy", lp) == FDC_OK
+    st, sp = _stack(32, (512, 256, 128, 64, 32), (1, 8, 16, 32, 64))
+    assert st == FDC_OK
+    got = []
+    for i in range(4):
+        assert _lib.status("fdc_cic_stack_dk_ranges", sp, i, ctypes.byref(r)) == FDC_OK
+        got.append(r.value)
+    assert all(1 < g <= 32 // 8 for g in got), got
+    assert _lib.status("fdc_cic_stack_dk_ranges", sp, 4, ctypes.byref(r)) == FDC_EINVAL
+    assert _lib.status("fdc_cic_stack_plan_destroy", sp) == FDC_OK
+    assert _lib.status("fdc_cic_stack_dk_ranges", sp, 0, ctypes.byref(r)) == FDC_EINVAL  # destroyed
