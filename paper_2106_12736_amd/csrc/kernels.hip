@@ -1174,11 +1174,11 @@ __device__ __forceinline__ int div_small(int e, int d, float rd, int &rem) {
 // FDC layer of the FDCNN on spectra (Eq. 5, Algorithm 1) followed by FDP, forming only
 // the bins FDP keeps: Y [B][S][M][M/2+1] from X [B][C][N][N/2+1], K [S][N][N/2+1].
 // Kept rows of the N-point spectrum: k < M/2 and k >= N - M/2 (output row k or
-// k - (N - M)); kept columns l <= M/2.  Grid: y over the output planes, x over the
-// plane's elements in order, so stores are contiguous.
+// k - (N - M)); kept columns l <= M/2.  Grid: x over an output plane's elements in
+// order (contiguous stores), y over the output channels; a thread loads its kernel
+// bin once and forms that bin for every image.
 __global__ __launch_bounds__(256) void k_cic_fdp_fwd(const float2 *__restrict__ X, const float2 *__restrict__ K,
-                                                     float2 *__restrict__ Y, int C, int J, int N, int M,
-                                                     long long planes) {
+                                                     float2 *__restrict__ Y, int B, int C, int J, int N, int M) {
   const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1, pe = M * Lm;
   const float rl = 1.f / (float)Lm;
   const int e = blockIdx.x * 256 + threadIdx.x;
@@ -1186,18 +1186,20 @@ __global__ __launch_bounds__(256) void k_cic_fdp_fwd(const float2 *__restrict__ 
   int l;
   const int k = div_small(e, Lm, rl, l);
   const int kr = k < M / 2 ? k : k + (N - M);
-  for (long long pl = blockIdx.y; pl < planes; pl += gridDim.y) {
-    const int o = (int)(pl % S);
-    const long long b = pl / S;
-    Y[pl * pe + e] = cmul(X[((b * C + o / J) * N + kr) * NF + l], K[((long long)o * N + kr) * NF + l]);
+  for (int o = blockIdx.y; o < S; o += gridDim.y) {
+    const float2 kv = K[((long long)o * N + kr) * NF + l];
+    const float2 *xp = X + ((long long)(o / J) * N + kr) * NF + l;
+    float2 *yp = Y + (long long)o * pe + e;
+#pragma unroll 4
+    for (int b = 0; b < B; ++b) yp[(long long)b * S * pe] = cmul(xp[(long long)b * C * N * NF], kv);
   }
 }
 
 // Backward of k_cic_fdp_fwd: gX [B][C][N][N/2+1] = sum_j gY conj(K) at the kept bins,
-// exact zeros at the bins FDP drops.
+// exact zeros at the bins FDP drops.  Grid: x over a plane's elements, y over the
+// input channels; a thread forms its bin for every image.
 __global__ __launch_bounds__(256) void k_cic_fdp_bwd_gx(const float2 *__restrict__ gY, const float2 *__restrict__ K,
-                                                        float2 *__restrict__ gX, int C, int J, int N, int M,
-                                                        long long planes) {
+                                                        float2 *__restrict__ gX, int B, int C, int J, int N, int M) {
   const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1, pe = N * NF;
   const float rn = 1.f / (float)NF;
   const int e = blockIdx.x * 256 + threadIdx.x;
@@ -1206,17 +1208,23 @@ __global__ __launch_bounds__(256) void k_cic_fdp_bwd_gx(const float2 *__restrict
   const int kr = div_small(e, NF, rn, l);
   const bool kept = l < Lm && (kr < M / 2 || kr >= N - M / 2);
   const int k = kr < M / 2 ? kr : kr - (N - M);
-  for (long long pl = blockIdx.y; pl < planes; pl += gridDim.y) {
-    const int c = (int)(pl % C);
-    const long long b = pl / C;
-    float2 acc = make_float2(0.f, 0.f);
-    if (kept) {
-      for (int j = 0; j < J; ++j) {
-        const int o = c * J + j;
-        acc = cfmac(acc, gY[((b * S + o) * M + k) * Lm + l], K[((long long)o * N + kr) * NF + l]);
-      }
+  const long long mpe = (long long)M * Lm;
+  for (int c = blockIdx.y; c < C; c += gridDim.y) {
+    float2 *gp = gX + (long long)c * pe + e;
+    if (!kept) {
+#pragma unroll 4
+      for (int b = 0; b < B; ++b) gp[(long long)b * C * pe] = make_float2(0.f, 0.f);
+      continue;
     }
-    gX[pl * pe + e] = acc;
+    const float2 *kp = K + ((long long)c * J * N + kr) * NF + l;  // K[cJ + j] at j * N * NF
+    const float2 *yp = gY + (long long)c * J * mpe + (long long)k * Lm + l;  // gY[b][cJ + j]
+#pragma unroll 2
+    for (int b = 0; b < B; ++b) {
+      float2 acc = make_float2(0.f, 0.f);
+      for (int j = 0; j < J; ++j)
+        acc = cfmac(acc, yp[((long long)b * S + j) * mpe], kp[(long long)j * N * NF]);
+      gp[(long long)b * C * pe] = acc;
+    }
   }
 }
 
@@ -1237,6 +1245,7 @@ __global__ __launch_bounds__(256) void k_cic_fdp_bwd_gk(const float2 *__restrict
     float2 acc = make_float2(0.f, 0.f);
     if (kept) {
       const long long c = o / J;
+#pragma unroll 4
       for (int b = 0; b < B; ++b)
         acc = cfmac(acc, gY[(((long long)b * S + o) * M + k) * Lm + l], X[(((long long)b * C + c) * N + kr) * NF + l]);
     }
@@ -1251,10 +1260,9 @@ static dim3 plane_grid(long long plane_elems, long long planes) {
 hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, int N, int M,
                               hipStream_t s) {
   if ((long long)N * (N / 2 + 1) >= (1 << 24)) return hipErrorInvalidValue;
-  const long long planes = (long long)B * S;
   timing_before("cic_fdp_fwd", s);
-  hipLaunchKernelGGL(k_cic_fdp_fwd, plane_grid((long long)M * (M / 2 + 1), planes), dim3(256), 0, s, X, K, Y, C,
-                     S / C, N, M, planes);
+  hipLaunchKernelGGL(k_cic_fdp_fwd, plane_grid((long long)M * (M / 2 + 1), S), dim3(256), 0, s, X, K, Y, B, C, S / C,
+                     N, M);
   const hipError_t e = hipGetLastError();
   timing_after("cic_fdp_fwd", s);
   return e;
@@ -1263,10 +1271,9 @@ hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B
 hipError_t launch_cic_fdp_bwd_gx(const float2 *gY, const float2 *K, float2 *gX, int B, int C, int S, int N, int M,
                                  hipStream_t s) {
   if ((long long)N * (N / 2 + 1) >= (1 << 24)) return hipErrorInvalidValue;
-  const long long planes = (long long)B * C;
   timing_before("cic_fdp_bwd_gx", s);
-  hipLaunchKernelGGL(k_cic_fdp_bwd_gx, plane_grid((long long)N * (N / 2 + 1), planes), dim3(256), 0, s, gY, K, gX,
-                     C, S / C, N, M, planes);
+  hipLaunchKernelGGL(k_cic_fdp_bwd_gx, plane_grid((long long)N * (N / 2 + 1), C), dim3(256), 0, s, gY, K, gX, B, C,
+                     S / C, N, M);
   const hipError_t e = hipGetLastError();
   timing_after("cic_fdp_bwd_gx", s);
   return e;
