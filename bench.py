@@ -89,7 +89,8 @@ def step_launches(wl, input_grad=False, ranges=None):
 def fused_step_launches(wl, input_grad=False, ranges=None):
     """(kernel name, algorithmic bytes) of every launch of one step of the fused stack
     executor: as step_launches, with each layer boundary's inverse rows and the next
-    layer's forward rows (and the backward's adjoint pair) in one kernel."""
+    layer's forward rows (and the backward's adjoint pair) in one kernel, and a
+    layer's dK and dX columns in one launch when dK uses one batch range."""
     ranges = ranges or [1] * wl.layers
     out = []
     n = wl.layers
@@ -108,9 +109,17 @@ def fused_step_launches(wl, input_grad=False, ranges=None):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
         if i == n - 1:
             out.append((f"row_r2c_{M}", F32 * B * S * M * M + C64 * B * S * M * L))
-        out += gk_launches(B, C, S, N, M, L, NF, ranges[i])
-        if i > 0 or input_grad:
-            out.append((f"col_bwd_gx_{N}_{M}", C64 * (B * S * M * L + S * M * L + B * C * N * L)))
+        dx = i > 0 or input_grad
+        gx_bytes = C64 * (B * S * M * L + S * M * L + B * C * N * L)
+        if dx and ranges[i] <= 1:
+            # dK and dX columns in one launch: the bytes of both
+            (_, gk_bytes), = gk_launches(B, C, S, N, M, L, NF, 1)
+            out.append((f"col_bwd_dk_dx_{N}_{M}", gk_bytes + gx_bytes))
+        else:
+            out += gk_launches(B, C, S, N, M, L, NF, ranges[i])
+            if dx:
+                out.append((f"col_bwd_gx_{N}_{M}", gx_bytes))
+        if dx:
             if i > 0:
                 _, _, _, _, Mp, Lp, _ = layer_dims(wl, i - 1)
                 out.append((f"row_c2r_r2c_{N}", C64 * B * C * N * L + C64 * B * C * Mp * Lp))

@@ -691,17 +691,28 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, cons
                                     "stack backward rows"))
         return st;
     }
-    // V is free until the dX columns below: dK's batch-range sums go there
-    if (fdc_status st = check_hip(fdc::launch_col_bwd_gk(g.N, g.M, Tg, reinterpret_cast<const float2 *>(saved[i]),
-                                                         reinterpret_cast<float2 *>(gK[i]), B, g.C, g.S, V,
-                                                         (long long)p->ws_b, s),
-                                  "stack backward dK"))
-      return st;
-    if (i == 0 && !gx) break;
-    if (fdc_status st = check_hip(fdc::launch_col_bwd_gx(g.N, g.M, Tg, reinterpret_cast<const float2 *>(K[i]), V, B,
-                                                         g.C, g.S, s),
-                                  "stack backward dx columns"))
-      return st;
+    const bool need_dx = i > 0 || gx;
+    if (need_dx && fdc::gk_batch_ranges(g.N, g.M, B, g.S, (long long)p->ws_b) == 1 &&
+        fdc::col_bwd_dk_dx_supported(g.N, g.M)) {
+      // dK and dX columns side by side in one launch
+      if (fdc_status st = check_hip(fdc::launch_col_bwd_dk_dx(g.N, g.M, Tg, reinterpret_cast<const float2 *>(saved[i]),
+                                                              reinterpret_cast<const float2 *>(K[i]),
+                                                              reinterpret_cast<float2 *>(gK[i]), V, B, g.C, g.S, s),
+                                    "stack backward dK and dx columns"))
+        return st;
+    } else {
+      // V is free until the dX columns below: dK's batch-range sums go there
+      if (fdc_status st = check_hip(fdc::launch_col_bwd_gk(g.N, g.M, Tg, reinterpret_cast<const float2 *>(saved[i]),
+                                                           reinterpret_cast<float2 *>(gK[i]), B, g.C, g.S, V,
+                                                           (long long)p->ws_b, s),
+                                    "stack backward dK"))
+        return st;
+      if (!need_dx) break;
+      if (fdc_status st = check_hip(fdc::launch_col_bwd_gx(g.N, g.M, Tg, reinterpret_cast<const float2 *>(K[i]), V,
+                                                           B, g.C, g.S, s),
+                                    "stack backward dx columns"))
+        return st;
+    }
     if (i > 0) {
       // this layer's adjoint inverse rows and the previous layer's upstream-gradient rows
       const StackLayer h = stack_layer(p, i - 1);

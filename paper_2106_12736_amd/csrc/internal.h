@@ -107,6 +107,11 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
                              int S, float2 *part, long long part_elems, hipStream_t s);
 hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, float2 *V, int B, int C, int S,
                              hipStream_t s);
+// dK (one batch range) and dX of one layer in a single launch, where the dX tiles pack
+// the dK workgroup (col_bwd_dk_dx_supported).
+bool col_bwd_dk_dx_supported(int n, int m);
+hipError_t launch_col_bwd_dk_dx(int n, int m, const float2 *Tg, const float2 *Xh, const float2 *K, float2 *gK,
+                                float2 *V, int B, int C, int S, hipStream_t s);
 
 // Full FDC (full_fdc.hip).  Spectra in the padded split layout full_spec_layout,
 // P a multiple of 8; tw is the device table

@@ -579,20 +579,18 @@ constexpr int gk_bp() {
 // of every row are shared out over the whole grid).
 // BG > 1: writes range r's sums at the kept bins to part [BG][S][M][M/2+1];
 // k_gk_reduce then adds the ranges in order and writes gK.
+// One workgroup of the dK launch: workgroup `lin` (after the XCD remap) of `nwg`,
+// thread `tid`; tw: the twiddle table of an (M * tws)-point transform in LDS.
 template <int M, int CT, int BP>
-__global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const float2 *__restrict__ Tg,
-                                                                      const float2 *__restrict__ Xh,
-                                                                      float2 *__restrict__ gK,
-                                                                      float2 *__restrict__ part, int B, int C,
-                                                                      int J, int N, int S, int BG) {
+__device__ __forceinline__ void col_bwd_gk_tile(int lin, int nwg, int tid, const float2 *tw, int tws, float2 *lds,
+                                                const float2 *__restrict__ Tg, const float2 *__restrict__ Xh,
+                                                float2 *__restrict__ gK, float2 *__restrict__ part, int B, int C,
+                                                int J, int N, int S, int BG) {
   using CM = FftCfg<M>;
   constexpr int L = M / 2 + 1, TPS = CM::TPS, E = CM::E;
   constexpr int NT = CT * TPS * BP;
-  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<M>();
-  stage_twiddles<M>(tw, threadIdx.x, NT);
-  const int s = threadIdx.x % CT, t = (threadIdx.x / CT) % TPS, g = threadIdx.x / (CT * TPS);
-  const int lin = xcd_remap(blockIdx.x, gridDim.x);
-  const int tiles = gridDim.x / BG;
+  const int s = tid % CT, t = (tid / CT) % TPS, g = tid / (CT * TPS);
+  const int tiles = nwg / BG;
   const int range = lin / tiles, wg = lin - range * tiles;
   const int b_lo = range * B / BG, b_hi = (range + 1) * B / BG;
   // the J output channels of one input channel read the same pooled-input columns
@@ -604,9 +602,9 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
   if (BG == 1) {
     static_assert((NT & (NT - 1)) == 0, "NT must be a power of two");
     constexpr int LW = NT < 64 ? NT : 64;
-    const int lane = threadIdx.x % LW;
-    const long long ngrp = (long long)gridDim.x * (NT / LW);
-    for (long long row = ((long long)wg * NT + threadIdx.x) / LW; row < (long long)S * N; row += ngrp)
+    const int lane = tid % LW;
+    const long long ngrp = (long long)nwg * (NT / LW);
+    for (long long row = ((long long)wg * NT + tid) / LW; row < (long long)S * N; row += ngrp)
       for (int l = L + lane; l < nf; l += LW) gK[row * nf + l] = make_float2(0.f, 0.f);
   }
 
@@ -628,7 +626,7 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
 #pragma unroll
       for (int m = 0; m < E; ++m) xv[m] = xc.p[(t + TPS * m) * xc.stride];
     }
-    fft_seq<M, -1>(v, t, lds, g * M * CT + s, CT, tw, 1);
+    fft_seq<M, -1>(v, t, lds, g * M * CT + s, CT, tw, tws);
     if constexpr (E > 8) {
 #pragma unroll
       for (int m = 0; m < E; ++m) xv[m] = xc.p[(t + TPS * m) * xc.stride];
@@ -671,6 +669,18 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
   for (int k = M / 2 + t; k < N - M / 2; k += TPS) kcol[(long long)k * nf] = make_float2(0.f, 0.f);
 }
 
+template <int M, int CT, int BP>
+__global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const float2 *__restrict__ Tg,
+                                                                      const float2 *__restrict__ Xh,
+                                                                      float2 *__restrict__ gK,
+                                                                      float2 *__restrict__ part, int B, int C,
+                                                                      int J, int N, int S, int BG) {
+  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<M>();
+  stage_twiddles<M>(tw, threadIdx.x, CT * FftCfg<M>::TPS * BP);
+  col_bwd_gk_tile<M, CT, BP>(xcd_remap(blockIdx.x, gridDim.x), gridDim.x, threadIdx.x, tw, 1, lds, Tg, Xh, gK, part,
+                             B, C, J, N, S, BG);
+}
+
 // gK [S][N][N/2+1] from the BG range sums part [BG][S][M][M/2+1]: at the kept bins
 // the ranges added in order, zeros elsewhere.  A workgroup takes whole rows.
 __global__ __launch_bounds__(256) void k_gk_reduce(const float2 *__restrict__ part, float2 *__restrict__ gK, int BG,
@@ -707,22 +717,23 @@ constexpr int cic_lds_elems() {
 // bins, FDP adjoint (zero rows at the dropped frequencies), inverse column DFT (N).
 // The thread layout of the N-point transform holds JP = TPS_N / TPS_M groups of
 // the M-point layout, which take the J products in turns.
+// One tile of the dX launch: tile `lin` (after the XCD remap), thread `tid`; tw: the
+// N-point twiddle table in LDS.  With valid = false the tile runs (every barrier is
+// reached) but stores nothing.
 template <int N, int M, int CT>
-__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 *__restrict__ Tg,
-                                                                  const float2 *__restrict__ K,
-                                                                  float2 *__restrict__ V, int C, int J,
-                                                                  int planes) {
+__device__ __forceinline__ void col_bwd_gx_tile(int lin, bool valid, int tid, const float2 *tw, float2 *lds,
+                                                const float2 *__restrict__ Tg, const float2 *__restrict__ K,
+                                                float2 *__restrict__ V, int C, int J, int planes) {
   using CN = FftCfg<N>;
   using CM = FftCfg<M>;
   constexpr int L = M / 2 + 1, NF = N / 2 + 1;
   constexpr int TPSN = CN::TPS, TPSM = CM::TPS, JP = cic_jp<N, M>();
   static_assert(JP * TPSM == TPSN, "thread layouts of the two transforms must nest");
-  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
-  stage_twiddles<N>(tw, threadIdx.x, CT * TPSN);
-  const int s = threadIdx.x % CT, t = threadIdx.x / CT;
+  const int s = tid % CT, t = tid / CT;
   const int tp = t % TPSM, js = t / TPSM;
   // plane index ci * B + b: the B images read the same kernel columns
-  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes, planes / C);
+  ColRef c = column_ref<CT>(lin, s, L, planes, planes / C);
+  c.ok = c.ok && valid;
   const int B = planes / C;
   const int ci = c.plane / B;
   const int b = c.plane - ci * B;
@@ -779,6 +790,43 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
   const ColPtr vc = split_col<N, L>(V, planes, b * C + ci, c.l);
 #pragma unroll
   for (int m = 0; m < CN::E; ++m) vc.p[(t + TPSN * m) * vc.stride] = w[m];
+}
+
+template <int N, int M, int CT>
+__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 *__restrict__ Tg,
+                                                                  const float2 *__restrict__ K,
+                                                                  float2 *__restrict__ V, int C, int J,
+                                                                  int planes) {
+  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
+  stage_twiddles<N>(tw, threadIdx.x, CT * FftCfg<N>::TPS);
+  col_bwd_gx_tile<N, M, CT>(xcd_remap(blockIdx.x, gridDim.x), true, threadIdx.x, tw, lds, Tg, K, V, C, J, planes);
+}
+
+// dK and dX of one layer in one launch (they are independent; both read Tg): the
+// first nk workgroups (nk_used of them real, nk a multiple of 8 so the XCD numbering
+// of the rest stays aligned) run dK tiles of CTK columns; the others each run PACK
+// dX tiles of CTX columns side by side, PACK = dK threads / dX threads.
+template <int N, int M, int CTK, int BP, int CTX>
+__global__ __launch_bounds__(CTK *FftCfg<M>::TPS *BP) void k_col_bwd_dk_dx(
+    const float2 *__restrict__ Tg, const float2 *__restrict__ Xh, const float2 *__restrict__ K,
+    float2 *__restrict__ gK, float2 *__restrict__ V, int B, int C, int J, int S, int nk, int nk_used, int nx_tiles) {
+  constexpr int NT = CTK * FftCfg<M>::TPS * BP, NX = CTX * FftCfg<N>::TPS, PACK = NT / NX;
+  static_assert(PACK >= 1 && PACK * NX == NT, "dX tiles must pack the dK workgroup exactly");
+  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
+  stage_twiddles<N>(tw, threadIdx.x, NT);
+  const int bid = blockIdx.x;
+  if (bid < nk) {
+    if (bid >= nk_used) return;  // padding: no barrier follows
+    col_bwd_gk_tile<M, CTK, BP>(xcd_remap(bid, nk_used), nk_used, threadIdx.x, tw, N / M, lds, Tg, Xh, gK,
+                                nullptr, B, C, J, N, S, 1);
+    return;
+  }
+  const int xb = bid - nk, nxb = gridDim.x - nk;
+  const int sub = threadIdx.x / NX;
+  const int tile = xcd_remap(xb, nxb) * PACK + sub;
+  const bool valid = tile < nx_tiles;
+  col_bwd_gx_tile<N, M, CTX>(valid ? tile : nx_tiles - 1, valid, threadIdx.x - sub * NX, tw,
+                             lds + sub * cic_lds_elems<N, M, CTX>(), Tg, K, V, C, J, B * C);
 }
 
 // ---------------------------------------------------------------------------
@@ -1142,6 +1190,42 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
     err = launch("gk_reduce", k_gk_reduce, grid, 256, 0, s, (const float2 *)part, gK, BG, S, M, n);
   });
   return err;
+}
+
+hipError_t launch_col_bwd_dk_dx(int n, int m, const float2 *Tg, const float2 *Xh, const float2 *K, float2 *gK,
+                                float2 *V, int B, int C, int S, hipStream_t s) {
+  hipError_t err = hipErrorInvalidValue;
+  if (!cic_pair_supported(n, m)) return err;
+  dispatch_nm(n, m, [&](auto nc, auto mc) {
+    constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
+    constexpr int L = M / 2 + 1;
+    constexpr int CTK = col_ct_for(kGkCT, L), BP = gk_bp<M>(), CTX = col_ct_for(col_ct_gx<N>(), L);
+    constexpr int NT = CTK * FftCfg<M>::TPS * BP, NX = CTX * FftCfg<N>::TPS;
+    if constexpr (NX <= NT && NT % NX == 0) {
+      constexpr int PACK = NT / NX;
+      const unsigned nk_used = col_grid(S, L, CTK), nx_tiles = col_grid((long long)B * C, L, CTX);
+      if (nk_used == 0 || nx_tiles == 0) return;
+      const unsigned nk = (nk_used + 7) & ~7u, nxb = (nx_tiles + PACK - 1) / PACK;
+      const long long gk_lds = lds_size<kColLds>(BP * M * CTK), gx_lds = (long long)PACK * cic_lds_elems<N, M, CTX>();
+      const size_t lds = (twiddle_lds_elems<N>() + (gk_lds > gx_lds ? gk_lds : gx_lds)) * sizeof(float2);
+      static const std::string nm = "col_bwd_dk_dx_" + std::to_string(N) + "_" + std::to_string(M);
+      err = launch(nm.c_str(), k_col_bwd_dk_dx<N, M, CTK, BP, CTX>, nk + nxb, NT, lds, s, Tg, Xh, K, gK, V, B, C,
+                   S / C, S, (int)nk, (int)nk_used, (int)nx_tiles);
+    }
+  });
+  return err;
+}
+
+bool col_bwd_dk_dx_supported(int n, int m) {
+  bool ok = false;
+  dispatch_nm(n, m, [&](auto nc, auto mc) {
+    constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
+    constexpr int L = M / 2 + 1;
+    constexpr int CTK = col_ct_for(kGkCT, L), BP = gk_bp<M>(), CTX = col_ct_for(col_ct_gx<N>(), L);
+    constexpr int NT = CTK * FftCfg<M>::TPS * BP, NX = CTX * FftCfg<N>::TPS;
+    ok = NX <= NT && NT % NX == 0;
+  });
+  return ok;
 }
 
 hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, float2 *V, int B, int C, int S,
