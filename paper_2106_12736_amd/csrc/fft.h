@@ -267,6 +267,10 @@ FDC_FFT_CFG(224, 8, 7, 4, 4, 2)
 // ordered per wave); the same as FftCfg unless specialised.
 template <int N>
 struct RowCfg : FftCfg<N> {};
+// Plans of the column transforms (a sequence spread over the waves of a workgroup);
+// the same as FftCfg unless specialised.
+template <int N>
+struct ColCfg : FftCfg<N> {};
 
 template <class Cfg>
 constexpr int stockham_ns(int p) {  // product of the radices before pass p

@@ -342,7 +342,7 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r_r2c(SpecLayout 
 // ---------------------------------------------------------------------------
 template <int N>
 constexpr int col_ct() {
-  return FftCfg<N>::TPS >= 64 ? 8 : (FftCfg<N>::TPS >= 32 ? 16 : 32);
+  return ColCfg<N>::TPS >= 64 ? 8 : (ColCfg<N>::TPS >= 32 ? 16 : 32);
 }
 // Narrower tiles (twice the workgroups) where measurement favoured them: the dX
 // kernel (three transforms per tile), the forward crop at 128 and 256 points and the
@@ -407,10 +407,10 @@ __device__ __forceinline__ ColRef column_ref(int w, int s, int L, int planes, in
 }
 
 template <int N, int CT, int DIR>
-__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft(const float2 *in, float2 *out, int L, int ld,
+__global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fft(const float2 *in, float2 *out, int L, int ld,
                                                                int planes, long long in_plane_stride,
                                                                long long out_plane_stride) {
-  using Cfg = FftCfg<N>;
+  using Cfg = ColCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
   stage_twiddles<N>(tw, threadIdx.x, CT * TPS);
@@ -420,7 +420,7 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft(const float2 *in
   float2 v[E];
 #pragma unroll
   for (int m = 0; m < E; ++m) v[m] = ip[(long long)(t + TPS * m) * ld];  // lanes past the end read a valid column
-  fft_seq<N, DIR>(v, t, lds, s, CT, tw, 1);
+  fft_seq<N, DIR, true, false, kLdsPlain, ColCfg<N>>(v, t, lds, s, CT, tw, 1);
   if (!c.ok) return;
   float2 *op = out + c.plane * out_plane_stride + c.l;
 #pragma unroll
@@ -460,8 +460,8 @@ __device__ __forceinline__ ColPtr64 layout_col(const SpecLayout &sl, int H, int 
 }
 
 template <int N, int CT, int DIR>
-__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft_split(SpecLayout in, SpecLayout out, int planes) {
-  using Cfg = FftCfg<N>;
+__global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fft_split(SpecLayout in, SpecLayout out, int planes) {
+  using Cfg = ColCfg<N>;
   constexpr int L = N / 2 + 1, TPS = Cfg::TPS, E = Cfg::E;
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
   stage_twiddles<N>(tw, threadIdx.x, CT * TPS);
@@ -471,7 +471,7 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft_split(SpecLayout
   float2 v[E];
 #pragma unroll
   for (int m = 0; m < E; ++m) v[m] = ic.p[(t + TPS * m) * ic.stride];  // lanes past the end read a valid column
-  fft_seq<N, DIR>(v, t, lds, s, CT, tw, 1);
+  fft_seq<N, DIR, true, false, kLdsPlain, ColCfg<N>>(v, t, lds, s, CT, tw, 1);
   if (!c.ok) return;
   const ColPtr64 oc = layout_col(out, L - 1, c.plane, c.l);
 #pragma unroll
@@ -482,9 +482,9 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fft_split(SpecLayout
 // FDP keeps.  T [planes][N rows] -> Xh [planes][M rows], both split layout with
 // L = M/2 + 1 bins per row (Xh is the pooled input spectrum the backward reads).
 template <int N, int M, int CT>
-__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fwd_crop(const float2 *__restrict__ T,
+__global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fwd_crop(const float2 *__restrict__ T,
                                                                     float2 *__restrict__ Xh, int planes) {
-  using CN = FftCfg<N>;
+  using CN = ColCfg<N>;
   constexpr int L = M / 2 + 1, TPS = CN::TPS, E = CN::E;
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
   stage_twiddles<N>(tw, threadIdx.x, CT * TPS);
@@ -494,7 +494,7 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fwd_crop(const float
   float2 v[E];
 #pragma unroll
   for (int m = 0; m < E; ++m) v[m] = tc.p[(t + TPS * m) * tc.stride];  // lanes past the end read a valid column
-  fft_seq<N, -1>(v, t, lds, s, CT, tw, 1);
+  fft_seq<N, -1, true, false, kLdsPlain, ColCfg<N>>(v, t, lds, s, CT, tw, 1);
   if (!c.ok) return;
   const ColPtr xc = split_col<M, L>(Xh, planes, c.plane, c.l);
 #pragma unroll
@@ -516,11 +516,11 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_fwd_crop(const float
 constexpr int kCicJW = 4;
 
 template <int N, int M, int CT, int JW>
-__global__ __launch_bounds__(CT *FftCfg<M>::TPS) void k_col_cic_inv(const float2 *__restrict__ Xh,
+__global__ __launch_bounds__(CT *ColCfg<M>::TPS) void k_col_cic_inv(const float2 *__restrict__ Xh,
                                                                    const float2 *__restrict__ K,
                                                                    float2 *__restrict__ U, int B, int C, int J,
                                                                    int groups) {
-  using CM = FftCfg<M>;
+  using CM = ColCfg<M>;
   constexpr int L = M / 2 + 1, NF = N / 2 + 1, TPS = CM::TPS, E = CM::E;
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<M>();
   stage_twiddles<M>(tw, threadIdx.x, CT * TPS);
@@ -547,7 +547,7 @@ __global__ __launch_bounds__(CT *FftCfg<M>::TPS) void k_col_cic_inv(const float2
 #pragma unroll
     for (int m = 0; m < E; ++m) z[m] = cmul(x[m], kn[m]);
     if (jj + 1 < JW) load_k(o0 + jj + 1);  // the next kernel column loads while this one transforms
-    fft_seq<M, +1>(z, t, lds, s, CT, tw, 1);
+    fft_seq<M, +1, true, false, kLdsPlain, ColCfg<M>>(z, t, lds, s, CT, tw, 1);
     if (c.ok) {
       const ColPtr uc = split_col<M, L>(U, groups * JW, b * S + o0 + jj, c.l);  // B * S planes
 #pragma unroll
@@ -564,7 +564,7 @@ constexpr int kGkCT = 8;
 constexpr long long kGkTargetWgs = 512;
 template <int M>
 constexpr int gk_bp() {
-  constexpr int bp = 512 / (kGkCT * FftCfg<M>::TPS);
+  constexpr int bp = 512 / (kGkCT * ColCfg<M>::TPS);
   return bp < 1 ? 1 : (bp > 8 ? 8 : bp);
 }
 
@@ -586,7 +586,7 @@ __device__ __forceinline__ void col_bwd_gk_tile(int lin, int nwg, int tid, const
                                                 const float2 *__restrict__ Tg, const float2 *__restrict__ Xh,
                                                 float2 *__restrict__ gK, float2 *__restrict__ part, int B, int C,
                                                 int J, int N, int S, int BG) {
-  using CM = FftCfg<M>;
+  using CM = ColCfg<M>;
   constexpr int L = M / 2 + 1, TPS = CM::TPS, E = CM::E;
   constexpr int NT = CT * TPS * BP;
   const int s = tid % CT, t = (tid / CT) % TPS, g = tid / (CT * TPS);
@@ -626,7 +626,7 @@ __device__ __forceinline__ void col_bwd_gk_tile(int lin, int nwg, int tid, const
 #pragma unroll
       for (int m = 0; m < E; ++m) xv[m] = xc.p[(t + TPS * m) * xc.stride];
     }
-    fft_seq<M, -1>(v, t, lds, g * M * CT + s, CT, tw, tws);
+    fft_seq<M, -1, true, false, kLdsPlain, ColCfg<M>>(v, t, lds, g * M * CT + s, CT, tw, tws);
     if constexpr (E > 8) {
 #pragma unroll
       for (int m = 0; m < E; ++m) xv[m] = xc.p[(t + TPS * m) * xc.stride];
@@ -670,13 +670,13 @@ __device__ __forceinline__ void col_bwd_gk_tile(int lin, int nwg, int tid, const
 }
 
 template <int M, int CT, int BP>
-__global__ __launch_bounds__(CT *FftCfg<M>::TPS *BP) void k_col_bwd_gk(const float2 *__restrict__ Tg,
+__global__ __launch_bounds__(CT *ColCfg<M>::TPS *BP) void k_col_bwd_gk(const float2 *__restrict__ Tg,
                                                                       const float2 *__restrict__ Xh,
                                                                       float2 *__restrict__ gK,
                                                                       float2 *__restrict__ part, int B, int C,
                                                                       int J, int N, int S, int BG) {
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<M>();
-  stage_twiddles<M>(tw, threadIdx.x, CT * FftCfg<M>::TPS * BP);
+  stage_twiddles<M>(tw, threadIdx.x, CT * ColCfg<M>::TPS * BP);
   col_bwd_gk_tile<M, CT, BP>(xcd_remap(blockIdx.x, gridDim.x), gridDim.x, threadIdx.x, tw, 1, lds, Tg, Xh, gK, part,
                              B, C, J, N, S, BG);
 }
@@ -703,7 +703,7 @@ __global__ __launch_bounds__(256) void k_gk_reduce(const float2 *__restrict__ pa
 
 template <int N, int M>
 constexpr int cic_jp() {
-  return FftCfg<N>::TPS / FftCfg<M>::TPS;
+  return ColCfg<N>::TPS / ColCfg<M>::TPS;
 }
 
 template <int N, int M, int CT>
@@ -724,8 +724,8 @@ template <int N, int M, int CT>
 __device__ __forceinline__ void col_bwd_gx_tile(int lin, bool valid, int tid, const float2 *tw, float2 *lds,
                                                 const float2 *__restrict__ Tg, const float2 *__restrict__ K,
                                                 float2 *__restrict__ V, int C, int J, int planes) {
-  using CN = FftCfg<N>;
-  using CM = FftCfg<M>;
+  using CN = ColCfg<N>;
+  using CM = ColCfg<M>;
   constexpr int L = M / 2 + 1, NF = N / 2 + 1;
   constexpr int TPSN = CN::TPS, TPSM = CM::TPS, JP = cic_jp<N, M>();
   static_assert(JP * TPSM == TPSN, "thread layouts of the two transforms must nest");
@@ -757,7 +757,7 @@ __device__ __forceinline__ void col_bwd_gx_tile(int lin, bool valid, int tid, co
 #pragma unroll
       for (int m = 0; m < CM::E; ++m) kv[m] = kcol[(long long)kept_row<N, M>(tp + TPSM * m) * NF];
     }
-    fft_seq<M, -1>(g, tp, lds, js * M * CT + s, CT, tw, N / M);
+    fft_seq<M, -1, true, false, kLdsPlain, ColCfg<M>>(g, tp, lds, js * M * CT + s, CT, tw, N / M);
     if constexpr (CM::E > 8) {
 #pragma unroll
       for (int m = 0; m < CM::E; ++m) kv[m] = kcol[(long long)kept_row<N, M>(tp + TPSM * m) * NF];
@@ -785,7 +785,7 @@ __device__ __forceinline__ void col_bwd_gx_tile(int lin, bool valid, int tid, co
     }
     w[m] = sum;
   }
-  fft_seq<N, +1>(w, t, lds, s, CT, tw, 1);
+  fft_seq<N, +1, true, false, kLdsPlain, ColCfg<N>>(w, t, lds, s, CT, tw, 1);
   if (!c.ok) return;
   const ColPtr vc = split_col<N, L>(V, planes, b * C + ci, c.l);
 #pragma unroll
@@ -793,12 +793,12 @@ __device__ __forceinline__ void col_bwd_gx_tile(int lin, bool valid, int tid, co
 }
 
 template <int N, int M, int CT>
-__global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 *__restrict__ Tg,
+__global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_bwd_gx(const float2 *__restrict__ Tg,
                                                                   const float2 *__restrict__ K,
                                                                   float2 *__restrict__ V, int C, int J,
                                                                   int planes) {
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
-  stage_twiddles<N>(tw, threadIdx.x, CT * FftCfg<N>::TPS);
+  stage_twiddles<N>(tw, threadIdx.x, CT * ColCfg<N>::TPS);
   col_bwd_gx_tile<N, M, CT>(xcd_remap(blockIdx.x, gridDim.x), true, threadIdx.x, tw, lds, Tg, K, V, C, J, planes);
 }
 
@@ -807,10 +807,10 @@ __global__ __launch_bounds__(CT *FftCfg<N>::TPS) void k_col_bwd_gx(const float2 
 // of the rest stays aligned) run dK tiles of CTK columns; the others each run PACK
 // dX tiles of CTX columns side by side, PACK = dK threads / dX threads.
 template <int N, int M, int CTK, int BP, int CTX>
-__global__ __launch_bounds__(CTK *FftCfg<M>::TPS *BP) void k_col_bwd_dk_dx(
+__global__ __launch_bounds__(CTK *ColCfg<M>::TPS *BP) void k_col_bwd_dk_dx(
     const float2 *__restrict__ Tg, const float2 *__restrict__ Xh, const float2 *__restrict__ K,
     float2 *__restrict__ gK, float2 *__restrict__ V, int B, int C, int J, int S, int nk, int nk_used, int nx_tiles) {
-  constexpr int NT = CTK * FftCfg<M>::TPS * BP, NX = CTX * FftCfg<N>::TPS, PACK = NT / NX;
+  constexpr int NT = CTK * ColCfg<M>::TPS * BP, NX = CTX * ColCfg<N>::TPS, PACK = NT / NX;
   static_assert(PACK >= 1 && PACK * NX == NT, "dX tiles must pack the dK workgroup exactly");
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
   stage_twiddles<N>(tw, threadIdx.x, NT);
@@ -1083,10 +1083,10 @@ hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long lo
     static const std::string nf = "col_fft_fwd_" + std::to_string(N);
     static const std::string ni = "col_fft_inv_" + std::to_string(N);
     if (dir < 0)
-      err = launch(nf.c_str(), k_col_fft<N, CT, -1>, grid, CT * FftCfg<N>::TPS, lds, s, in, out, L, ld, (int)planes,
+      err = launch(nf.c_str(), k_col_fft<N, CT, -1>, grid, CT * ColCfg<N>::TPS, lds, s, in, out, L, ld, (int)planes,
                    in_plane_stride, out_plane_stride);
     else
-      err = launch(ni.c_str(), k_col_fft<N, CT, +1>, grid, CT * FftCfg<N>::TPS, lds, s, in, out, L, ld, (int)planes,
+      err = launch(ni.c_str(), k_col_fft<N, CT, +1>, grid, CT * ColCfg<N>::TPS, lds, s, in, out, L, ld, (int)planes,
                    in_plane_stride, out_plane_stride);
   });
   return err;
@@ -1104,9 +1104,9 @@ hipError_t launch_col_fft_split(int n, int dir, SpecLayout in, SpecLayout out, l
     static const std::string nf = "col_fft_fwd_" + std::to_string(N);
     static const std::string ni = "col_fft_inv_" + std::to_string(N);
     if (dir < 0)
-      err = launch(nf.c_str(), k_col_fft_split<N, CT, -1>, grid, CT * FftCfg<N>::TPS, lds, s, in, out, (int)planes);
+      err = launch(nf.c_str(), k_col_fft_split<N, CT, -1>, grid, CT * ColCfg<N>::TPS, lds, s, in, out, (int)planes);
     else
-      err = launch(ni.c_str(), k_col_fft_split<N, CT, +1>, grid, CT * FftCfg<N>::TPS, lds, s, in, out, (int)planes);
+      err = launch(ni.c_str(), k_col_fft_split<N, CT, +1>, grid, CT * ColCfg<N>::TPS, lds, s, in, out, (int)planes);
   });
   return err;
 }
@@ -1122,7 +1122,7 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
     static const std::string n2 = "col_cic_inv_" + std::to_string(N) + "_" + std::to_string(M);
     const unsigned g1 = col_grid((long long)B * C, L, CTN);
     if (g1 == 0) return;
-    err = launch(n1.c_str(), k_col_fwd_crop<N, M, CTN>, g1, CTN * FftCfg<N>::TPS, (twiddle_lds_elems<N>() + lds_size<kColLds>(N * CTN)) * sizeof(float2),
+    err = launch(n1.c_str(), k_col_fwd_crop<N, M, CTN>, g1, CTN * ColCfg<N>::TPS, (twiddle_lds_elems<N>() + lds_size<kColLds>(N * CTN)) * sizeof(float2),
                  s, T, Xh, B * C);
     if (err != hipSuccess) return;
     const int J = S / C;
@@ -1135,7 +1135,7 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
     }
     const size_t lds2 = (twiddle_lds_elems<M>() + lds_size<kColLds>(M * CTM)) * sizeof(float2);
     auto go = [&](auto kern) {
-      err = launch(n2.c_str(), kern, g2, CTM * FftCfg<M>::TPS, lds2, s, Xh, K, U, B, C, J, (int)groups);
+      err = launch(n2.c_str(), kern, g2, CTM * ColCfg<M>::TPS, lds2, s, Xh, K, U, B, C, J, (int)groups);
     };
     switch (jw) {
       case 8: go(k_col_cic_inv<N, M, CTM, 8>); break;
@@ -1182,7 +1182,7 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
     const unsigned tiles = col_grid(S, L, CT);
     if (tiles == 0) return;
     static const std::string nm = "col_bwd_gk_" + std::to_string(M);
-    err = launch(nm.c_str(), k_col_bwd_gk<M, CT, BP>, tiles * (unsigned)BG, CT * FftCfg<M>::TPS * BP, lds, s, Tg,
+    err = launch(nm.c_str(), k_col_bwd_gk<M, CT, BP>, tiles * (unsigned)BG, CT * ColCfg<M>::TPS * BP, lds, s, Tg,
                  Xh, gK, part, B, C, S / C, n, S, BG);
     if (err != hipSuccess || BG == 1) return;
     const long long rows = (long long)S * n;
@@ -1200,7 +1200,7 @@ hipError_t launch_col_bwd_dk_dx(int n, int m, const float2 *Tg, const float2 *Xh
     constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
     constexpr int CTK = col_ct_for(kGkCT, L), BP = gk_bp<M>(), CTX = col_ct_for(col_ct_gx<N>(), L);
-    constexpr int NT = CTK * FftCfg<M>::TPS * BP, NX = CTX * FftCfg<N>::TPS;
+    constexpr int NT = CTK * ColCfg<M>::TPS * BP, NX = CTX * ColCfg<N>::TPS;
     if constexpr (NX <= NT && NT % NX == 0) {
       constexpr int PACK = NT / NX;
       const unsigned nk_used = col_grid(S, L, CTK), nx_tiles = col_grid((long long)B * C, L, CTX);
@@ -1222,7 +1222,7 @@ bool col_bwd_dk_dx_supported(int n, int m) {
     constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
     constexpr int CTK = col_ct_for(kGkCT, L), BP = gk_bp<M>(), CTX = col_ct_for(col_ct_gx<N>(), L);
-    constexpr int NT = CTK * FftCfg<M>::TPS * BP, NX = CTX * FftCfg<N>::TPS;
+    constexpr int NT = CTK * ColCfg<M>::TPS * BP, NX = CTX * ColCfg<N>::TPS;
     ok = NX <= NT && NT % NX == 0;
   });
   return ok;
@@ -1239,7 +1239,7 @@ hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, fl
     const unsigned grid = col_grid((long long)B * C, L, CT);
     if (grid == 0) return;
     static const std::string nm = "col_bwd_gx_" + std::to_string(N) + "_" + std::to_string(M);
-    err = launch(nm.c_str(), k_col_bwd_gx<N, M, CT>, grid, CT * FftCfg<N>::TPS, lds, s, Tg, K, V, C, S / C,
+    err = launch(nm.c_str(), k_col_bwd_gx<N, M, CT>, grid, CT * ColCfg<N>::TPS, lds, s, Tg, K, V, C, S / C,
                  B * C);
   });
   return err;
