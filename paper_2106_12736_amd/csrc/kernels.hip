@@ -8,10 +8,14 @@
 // Layer backward:
 //   k_row_r2c     upstream gradient -> (c_l/m^2) weighted half spectrum
 //   k_col_bwd_gk  column DFT (m), dL/dK = sum_b G conj(Xhat); the batch is split over
-//                 wave groups of one workgroup and summed in a fixed order
+//                 wave groups of one workgroup (and, for large batches, over image
+//                 ranges added by k_gk_reduce) and summed in a fixed order
 //   k_col_bwd_gx  column DFTs (m) of the J gradients, sum_j G conj(K), zero-padded
 //                 inverse column DFT (n)
+//   k_col_bwd_dk_dx  the two above in one launch (stack executor)
 //   k_row_c2r     adjoint row transform (n)
+// Stack executor: k_row_c2r_r2c runs a layer's inverse rows and the next layer's
+// forward rows (backward: the adjoint pair) on the same rows in one kernel.
 // Intermediates stay row-major [plane][row][column]; column kernels own CT adjacent
 // columns (numbered across planes) with the column index fastest across lanes, so
 // every global access is a run of up to CT consecutive complex values.
