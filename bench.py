@@ -54,6 +54,16 @@ def layer_dims(wl, i):
     return wl.batch, C, S, N, M, M // 2 + 1, N // 2 + 1
 
 
+def fwd_col_launches(B, C, S, N, M, L):
+    """The forward's column work of one layer: the column DFT with the FDP crop (writes
+    the saved spectrum) and the CIC product with the inverse column DFT, in one kernel
+    when an input channel has 1, 2 or 4 output channels, else in two."""
+    if S // C in (1, 2, 4):
+        return [(f"col_fwd_cic_{N}_{M}", C64 * (B * C * N * L + B * C * M * L + S * M * L + B * S * M * L))]
+    return [(f"col_fwd_crop_{N}_{M}", C64 * (B * C * N * L + B * C * M * L)),
+            (f"col_cic_inv_{N}_{M}", C64 * (B * C * M * L + S * M * L + B * S * M * L))]
+
+
 def gk_launches(B, C, S, N, M, L, NF, ranges=1):
     """dK of one layer: one launch that reads the upstream and saved spectra and writes
     all of gK (zeros where FDP drops), or, with the batch cut into R ranges, the range
@@ -73,8 +83,7 @@ def step_launches(wl, input_grad=False, ranges=None):
     for i in range(wl.layers):
         B, C, S, N, M, L, _ = layer_dims(wl, i)
         out.append((f"row_r2c_{N}", F32 * B * C * N * N + C64 * B * C * N * L))
-        out.append((f"col_fwd_crop_{N}_{M}", C64 * (B * C * N * L + B * C * M * L)))
-        out.append((f"col_cic_inv_{N}_{M}", C64 * (B * C * M * L + S * M * L + B * S * M * L)))
+        out += fwd_col_launches(B, C, S, N, M, L)
         out.append((f"row_c2r_{M}", C64 * B * S * M * L + F32 * B * S * M * M))
     for i in reversed(range(wl.layers)):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
@@ -98,8 +107,7 @@ def fused_step_launches(wl, input_grad=False, ranges=None):
         B, C, S, N, M, L, _ = layer_dims(wl, i)
         if i == 0:
             out.append((f"row_r2c_{N}", F32 * B * C * N * N + C64 * B * C * N * L))
-        out.append((f"col_fwd_crop_{N}_{M}", C64 * (B * C * N * L + B * C * M * L)))
-        out.append((f"col_cic_inv_{N}_{M}", C64 * (B * C * M * L + S * M * L + B * S * M * L)))
+        out += fwd_col_launches(B, C, S, N, M, L)
         if i + 1 < n:
             _, _, _, N2, M2, L2, _ = layer_dims(wl, i + 1)
             out.append((f"row_c2r_r2c_{M}", C64 * B * S * M * L + C64 * B * S * N2 * L2))
@@ -169,8 +177,7 @@ def spatial_step_launches(wl, n, input_grad=False, ranges=None):
         B, C, S, N, M, L, _ = layer_dims(wl, i)
         out.append(("cic_kspec", F32 * S * n * n + C64 * S * M * L))
         out.append((f"row_r2c_{N}", F32 * B * C * N * N + C64 * B * C * N * L))
-        out.append((f"col_fwd_crop_{N}_{M}", C64 * (B * C * N * L + B * C * M * L)))
-        out.append((f"col_cic_inv_{N}_{M}", C64 * (B * C * M * L + S * M * L + B * S * M * L)))
+        out += fwd_col_launches(B, C, S, N, M, L)
         out.append((f"row_c2r_{M}", C64 * B * S * M * L + F32 * B * S * M * M))
     for i in reversed(range(wl.layers)):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
@@ -395,8 +402,7 @@ def full_cic_step_launches(wl, ranges=1):
     return [
         ("cic_kspec", F32 * S * n * n + C64 * S * P * L),
         (f"row_r2c_{P}", F32 * B * C * P * P + C64 * B * C * P * L),
-        (f"col_fwd_crop_{P}_{P}", C64 * (B * C * P * L + B * C * P * L)),
-        (f"col_cic_inv_{P}_{P}", C64 * (B * C * P * L + S * P * L + B * S * P * L)),
+        *fwd_col_launches(B, C, S, P, P, L),
         (f"row_c2r_{P}", C64 * B * S * P * L + F32 * B * S * O * O),
         ("cic_kspec", F32 * S * n * n + C64 * S * P * L),
         (f"row_r2c_{P}", F32 * B * S * O * O + C64 * B * S * P * L),

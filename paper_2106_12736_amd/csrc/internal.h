@@ -98,6 +98,8 @@ hipError_t launch_col_fft_split(int n, int dir, SpecLayout in, SpecLayout out, l
 //   bwd_gk: Tg [B*S][m rows], Xh -> gK [S][n][n/2+1]: every bin (zeros where FDP drops)
 //   bwd_gx: Tg, K -> V [B*C][n rows]
 bool cic_pair_supported(int n, int m);
+// Whether the forward's two column kernels run as one (k_col_fwd_cic) for J = S / C.
+bool fwd_cic_fused(int J);
 hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, float2 *U, float2 *Xh, int B,
                               int C, int S, hipStream_t s);
 // dK: with scratch `part` (part_elems complex values; may be NULL) the batch is cut

@@ -560,6 +560,73 @@ __global__ __launch_bounds__(CT *ColCfg<M>::TPS) void k_col_cic_inv(const float2
   }
 }
 
+// Forward, both halves in one kernel for layers whose output channels per input
+// channel all fit one workgroup (JW = J): column DFT (N) of T, the kept rows to Xh and
+// to an LDS tile, then the CIC product (Eq. 5) and inverse column DFT (M) for each of
+// the J output channels.  The N-point thread layout holds JP = TPS_N / TPS_M groups
+// of the M-point layout, which take the output channels in turns.  Planes and tile
+// order as k_col_cic_inv (JB = 1): the B images of one input channel in a row.
+template <int N, int M, int CT, int JW>
+__global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fwd_cic(const float2 *__restrict__ T,
+                                                                   const float2 *__restrict__ K,
+                                                                   float2 *__restrict__ U, float2 *__restrict__ Xh,
+                                                                   int B, int C) {
+  using CN = ColCfg<N>;
+  using CM = ColCfg<M>;
+  constexpr int L = M / 2 + 1, NF = N / 2 + 1, TPSN = CN::TPS, TPSM = CM::TPS, EN = CN::E, EM = CM::E;
+  constexpr int JP = TPSN / TPSM;
+  static_assert(JP * TPSM == TPSN, "thread layouts of the two transforms must nest");
+  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
+  stage_twiddles<N>(tw, threadIdx.x, CT * TPSN);
+  const int s = threadIdx.x % CT, t = threadIdx.x / CT;
+  const int tp = t % TPSM, js = t / TPSM;
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, B * C, B);
+  const int b = c.plane % B, ci = c.plane / B;
+  const int bc = b * C + ci, S = C * JW;
+  const ColPtr tc = split_col<N, L>(T, B * C, bc, c.l);
+  float2 v[EN];
+#pragma unroll
+  for (int m = 0; m < EN; ++m) v[m] = tc.p[(t + TPSN * m) * tc.stride];  // lanes past the end read a valid column
+  fft_seq<N, -1, true, false, kLdsPlain, CN>(v, t, lds, s, CT, tw, 1);
+  const ColPtr xc = split_col<M, L>(Xh, B * C, bc, c.l);
+  __syncthreads();  // every lane is done with the transform's LDS
+#pragma unroll
+  for (int m = 0; m < EN; ++m) {
+    const int k = t + TPSN * m;
+    if (k < M / 2 || k >= N - M / 2) {
+      const int mrow = k < M / 2 ? k : k - (N - M);
+      if (c.ok) xc.p[mrow * xc.stride] = v[m];
+      lds[s + mrow * CT] = v[m];
+    }
+  }
+  __syncthreads();
+  float2 x[EM];
+#pragma unroll
+  for (int m = 0; m < EM; ++m) x[m] = lds[s + (tp + TPSM * m) * CT];
+  for (int j0 = 0; j0 < JW; j0 += JP) {
+    const int jj = j0 + js;
+    const bool act = c.ok && jj < JW;
+    const int o = ci * JW + (jj < JW ? jj : 0);
+    const float2 *kcol = K + (long long)o * N * NF + c.l;
+    float2 z[EM];
+#pragma unroll
+    for (int m = 0; m < EM; ++m) z[m] = cmul(x[m], kcol[kept_row<N, M>(tp + TPSM * m) * NF]);
+    // the first exchange write waits for every lane's reads of the tile above
+    fft_seq<M, +1, true, false, kLdsPlain, CM>(z, tp, lds, js * M * CT + s, CT, tw, N / M);
+    if (act) {
+      const ColPtr uc = split_col<M, L>(U, B * S, b * S + o, c.l);
+#pragma unroll
+      for (int m = 0; m < EM; ++m) uc.p[(tp + TPSM * m) * uc.stride] = z[m];
+    }
+  }
+}
+
+template <int N, int M, int CT>
+constexpr int fwd_cic_lds_elems() {
+  constexpr int a = N * CT, b = (ColCfg<N>::TPS / ColCfg<M>::TPS) * M * CT;
+  return lds_size<kColLds>(a > b ? a : b);
+}
+
 // Geometry of the dK kernel: tiles of 8 columns (there are only S * L columns,
 // so narrow tiles keep the grid at hundreds of workgroups) and BP batch groups
 // per workgroup, up to 512 threads and at most 8 groups.
@@ -1115,6 +1182,8 @@ hipError_t launch_col_fft_split(int n, int dir, SpecLayout in, SpecLayout out, l
   return err;
 }
 
+bool fwd_cic_fused(int J) { return J == 1 || J == 2 || J == 4; }
+
 hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, float2 *U, float2 *Xh, int B,
                               int C, int S, hipStream_t s) {
   hipError_t err = hipErrorInvalidValue;
@@ -1124,12 +1193,26 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
     constexpr int CTN = col_ct_for(col_ct_crop<N>(), L), CTM = col_ct_for(col_ct_cic<M>(), L);
     static const std::string n1 = "col_fwd_crop_" + std::to_string(N) + "_" + std::to_string(M);
     static const std::string n2 = "col_cic_inv_" + std::to_string(N) + "_" + std::to_string(M);
+    static const std::string n3 = "col_fwd_cic_" + std::to_string(N) + "_" + std::to_string(M);
+    const int J = S / C;
+    if (fwd_cic_fused(J)) {
+      // both halves in one kernel: J output channels per workgroup
+      const unsigned g = col_grid((long long)B * C, L, CTN);
+      if (g == 0) return;
+      const size_t lds = (twiddle_lds_elems<N>() + fwd_cic_lds_elems<N, M, CTN>()) * sizeof(float2);
+      auto go = [&](auto kern) { err = launch(n3.c_str(), kern, g, CTN * ColCfg<N>::TPS, lds, s, T, K, U, Xh, B, C); };
+      switch (J) {
+        case 4: go(k_col_fwd_cic<N, M, CTN, 4>); break;
+        case 2: go(k_col_fwd_cic<N, M, CTN, 2>); break;
+        default: go(k_col_fwd_cic<N, M, CTN, 1>);
+      }
+      return;
+    }
     const unsigned g1 = col_grid((long long)B * C, L, CTN);
     if (g1 == 0) return;
     err = launch(n1.c_str(), k_col_fwd_crop<N, M, CTN>, g1, CTN * ColCfg<N>::TPS, (twiddle_lds_elems<N>() + lds_size<kColLds>(N * CTN)) * sizeof(float2),
                  s, T, Xh, B * C);
     if (err != hipSuccess) return;
-    const int J = S / C;
     const int jw = J % kCicJW == 0 ? kCicJW : (J % 4 == 0 && kCicJW >= 4 ? 4 : (J % 2 == 0 && kCicJW >= 2 ? 2 : 1));
     const long long groups = (long long)B * C * (J / jw);
     const unsigned g2 = col_grid(groups, L, CTM);
