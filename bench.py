@@ -119,8 +119,8 @@ def fused_step_launches(wl, input_grad=False, ranges=None):
             out.append((f"row_r2c_{M}", F32 * B * S * M * M + C64 * B * S * M * L))
         dx = i > 0 or input_grad
         gx_bytes = C64 * (B * S * M * L + S * M * L + B * C * N * L)
-        if dx and ranges[i] <= 1:
-            # dK and dX columns in one launch: the bytes of both
+        if dx and ranges[i] <= 1 and N <= 256:
+            # dK and dX columns in one launch (layers of at most 256 points): the bytes of both
             (_, gk_bytes), = gk_launches(B, C, S, N, M, L, NF, 1)
             out.append((f"col_bwd_dk_dx_{N}_{M}", gk_bytes + gx_bytes))
         else:
