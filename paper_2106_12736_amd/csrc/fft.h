@@ -268,9 +268,14 @@ FDC_FFT_CFG(224, 8, 7, 4, 4, 2)
 template <int N>
 struct RowCfg : FftCfg<N> {};
 // Plans of the column transforms (a sequence spread over the waves of a workgroup);
-// the same as FftCfg unless specialised.
+// the same as FftCfg unless specialised.  128 points: 16 threads of 8 elements in
+// three passes instead of 8 threads of 16 in two, which halves the registers of the
+// column kernels' data (the dK kernel went from 159 to 110 VGPRs, two workgroups per
+// CU instead of one, and a layer's dK + dX from 37 to 24 us).
 template <int N>
 struct ColCfg : FftCfg<N> {};
+template <>
+struct ColCfg<128> : FftPlan<128, 16, 8, 8, 2, 1> {};
 
 template <class Cfg>
 constexpr int stockham_ns(int p) {  // product of the radices before pass p
