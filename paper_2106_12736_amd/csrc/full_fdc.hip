@@ -280,13 +280,23 @@ __device__ __forceinline__ void gw_project_run(float (&gw)[4][NK * NK], const v4
   }
 }
 
+// LDS staging of one step (4 batch rows, kGwRuns runs of 4 bins) for a 32 x 32
+// (s, c) block: G rows [4][32][kGwStage] and X rows [4][32][kGwStage] complex, each
+// (b, s) row holding the step's 4 * kGwRuns bins plus one of padding.  Every element
+// is loaded from memory once per workgroup (the four waves read each operand row
+// twice: waves 0/1 share s rows, 0/2 share c rows).
+constexpr int kGwStage = 4 * 2 + 1;
+constexpr int kGwStageElems = 2 * 4 * 32 * kGwStage;
+
 template <int NK>
 __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, const float2 *__restrict__ twg,
                                                  float *__restrict__ part, int B, int S, int C, int P,
                                                  int groups_per_chunk) {
   constexpr int T = NK * NK, kGwRuns = gw_runs<NK>();
+  static_assert(4 * kGwRuns + 1 == kGwStage, "stage row holds the step's bins and one pad");
   extern __shared__ float smem[];
   float2 *tw = reinterpret_cast<float2 *>(smem);
+  float2 *stage = tw + ((P + 31) & ~31);  // two buffers of kGwStageElems
   for (int i = threadIdx.x; i < P; i += 256) tw[i] = twg[i];
   __syncthreads();
 
@@ -297,9 +307,13 @@ __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, 
   const int sblocks = (S + 31) / 32, cblocks = (C + 31) / 32;
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
   const int tile = blk % (sblocks * cblocks), chunk = blk / (sblocks * cblocks);
-  const int s0 = (tile / cblocks) * 32 + (wave >> 1) * 16, c0 = (tile % cblocks) * 32 + (wave & 1) * 16;
-  const int sa = min(s0 + mrow, S - 1), cb = min(c0 + mrow, C - 1);  // A row (s), B column (c) of this lane
+  const int sbase = (tile / cblocks) * 32, cbase = (tile % cblocks) * 32;
+  const int s0 = sbase + (wave >> 1) * 16, c0 = cbase + (wave & 1) * 16;
   const int gr_begin = chunk * groups_per_chunk, gr_end = min(ngroups, gr_begin + groups_per_chunk);
+  // cooperative loads: thread = (batch row lb, block row lr, run lrun)
+  const int lrun = threadIdx.x & 1, lr = (threadIdx.x >> 1) & 31, lb = threadIdx.x >> 6;
+  static_assert(kGwRuns == 2, "cooperative load mapping assumes two runs per step");
+  const int gs = min(sbase + lr, S - 1), gc = min(cbase + lr, C - 1);
 
   float gw[4][T];  // rows s0 + 4 (lane / 16) + j, column c0 + lane % 16
 #pragma unroll
@@ -307,67 +321,83 @@ __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, 
 #pragma unroll
     for (int t = 0; t < T; ++t) gw[j][t] = 0.f;
 
-  // work item: (group of 4 runs, batch row b0 + lane / 16)
-  float4 ng[kGwRuns][2], nx[kGwRuns][2];
-  auto load_item = [&](int grp, int b0) {
-    const long long bc = min(b0 + kq, B - 1);
-#pragma unroll
-    for (int r = 0; r < kGwRuns; ++r) {
-      const int g = min(grp * kGwRuns + r, nrun - 1);
-      const bool side = g >= nmain;
-      const int k = (4 * g) / H, l0 = 4 * g - k * H;  // row run (k, l0..l0+3) when not on the side
-      const float4 *ga = reinterpret_cast<const float4 *>(
-          side ? G.side + (bc * S + sa) * G.sps + 4 * (g - nmain) : G.main + (bc * S + sa) * G.ps + k * G.rs + l0);
-      const float4 *xa = reinterpret_cast<const float4 *>(
-          side ? X.side + (bc * C + cb) * X.sps + 4 * (g - nmain) : X.main + (bc * C + cb) * X.ps + k * X.rs + l0);
-      ng[r][0] = ga[0], ng[r][1] = ga[1], nx[r][0] = xa[0], nx[r][1] = xa[1];
-    }
+  // This thread's share of a step: 4 bins of G (r[0], r[1]) and of X (r[2], r[3]) for
+  // batch row b0 + lb, block row lr, run lrun.  Two register sets hold the loads of the
+  // next two steps, so that the loads of step t + 2 are in flight while step t computes.
+  int lgrp = gr_begin, lb0 = 0;  // load cursor
+  // (past the chunk's last step the run index is clamped and the load is not used: an
+  // unconditional load keeps the wait counts exact, so step t waits for its own loads only)
+  auto load_next = [&](float4(&r)[4]) {
+    const long long bc = min(lb0 + lb, B - 1);
+    const int g = min(lgrp * kGwRuns + lrun, nrun - 1);
+    const bool side = g >= nmain;
+    const int k = (4 * g) / H, l0 = 4 * g - k * H;  // row run (k, l0..l0+3) when not on the side
+    const float4 *ga = reinterpret_cast<const float4 *>(
+        side ? G.side + (bc * S + gs) * G.sps + 4 * (g - nmain) : G.main + (bc * S + gs) * G.ps + k * G.rs + l0);
+    const float4 *xa = reinterpret_cast<const float4 *>(
+        side ? X.side + (bc * C + gc) * X.sps + 4 * (g - nmain) : X.main + (bc * C + gc) * X.ps + k * X.rs + l0);
+    r[0] = ga[0], r[1] = ga[1], r[2] = xa[0], r[3] = xa[1];
+    lb0 += 4;
+    if (lb0 >= B) lb0 = 0, ++lgrp;
   };
-  if (gr_begin < gr_end) load_item(gr_begin, 0);
+  float4 ra[4], rb[4];
+  load_next(ra);
+  load_next(rb);
   v4f dr[4 * kGwRuns], di[4 * kGwRuns];
-  for (int grp = gr_begin, b0 = 0; grp < gr_end;) {
-    float4 cg[kGwRuns][2], cx[kGwRuns][2];
-#pragma unroll
-    for (int r = 0; r < kGwRuns; ++r)
-      cg[r][0] = ng[r][0], cg[r][1] = ng[r][1], cx[r][0] = nx[r][0], cx[r][1] = nx[r][1];
-    int grp2 = grp, b02 = b0 + 4;
-    if (b02 >= B) b02 = 0, ++grp2;
-    if (grp2 < gr_end) load_item(grp2, b02);
+  int grp = gr_begin, b0 = 0;  // compute cursor
+  // one step: registers r (loaded two steps ago) into LDS buffer buf, then the products
+  auto step = [&](float4(&r)[4], int buf) {
+    // (the barrier below also ends every wave's reads of this buffer two steps ago)
+    {
+      float2 *sg = stage + buf * kGwStageElems + (lb * 32 + lr) * kGwStage + 4 * lrun;
+      float2 *sx = sg + 4 * 32 * kGwStage;
+      sg[0] = make_float2(r[0].x, r[0].y), sg[1] = make_float2(r[0].z, r[0].w);
+      sg[2] = make_float2(r[1].x, r[1].y), sg[3] = make_float2(r[1].z, r[1].w);
+      sx[0] = make_float2(r[2].x, r[2].y), sx[1] = make_float2(r[2].z, r[2].w);
+      sx[2] = make_float2(r[3].x, r[3].y), sx[3] = make_float2(r[3].z, r[3].w);
+    }
+    __syncthreads();
+    load_next(r);
     if (b0 == 0) {
 #pragma unroll
       for (int q = 0; q < 4 * kGwRuns; ++q) dr[q] = di[q] = v4f{0.f, 0.f, 0.f, 0.f};
     }
     const float m = b0 + kq < B ? 1.f : 0.f;  // batch rows past the end add nothing
+    const float2 *ag = stage + buf * kGwStageElems + (kq * 32 + (s0 - sbase) + mrow) * kGwStage;
+    const float2 *ax = stage + buf * kGwStageElems + 4 * 32 * kGwStage + (kq * 32 + (c0 - cbase) + mrow) * kGwStage;
 #pragma unroll
-    for (int r = 0; r < kGwRuns; ++r) {
-      const float gr[4] = {m * cg[r][0].x, m * cg[r][0].z, m * cg[r][1].x, m * cg[r][1].z};
-      const float gi[4] = {m * cg[r][0].y, m * cg[r][0].w, m * cg[r][1].y, m * cg[r][1].w};
-      const float xr[4] = {cx[r][0].x, cx[r][0].z, cx[r][1].x, cx[r][1].z};
-      const float xi[4] = {cx[r][0].y, cx[r][0].w, cx[r][1].y, cx[r][1].w};
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        // D = G conj(X):  re = Gr Xr + Gi Xi,  im = Gi Xr - Gr Xi
-        dr[4 * r + q] = mfma4(gr[q], xr[q], dr[4 * r + q]);
-        dr[4 * r + q] = mfma4(gi[q], xi[q], dr[4 * r + q]);
-        di[4 * r + q] = mfma4(gi[q], xr[q], di[4 * r + q]);
-        di[4 * r + q] = mfma4(-gr[q], xi[q], di[4 * r + q]);
-      }
+    for (int q = 0; q < 4 * kGwRuns; ++q) {
+      const float2 g2 = ag[q], x2 = ax[q];
+      const float gr = m * g2.x, gi = m * g2.y;
+      // D = G conj(X):  re = Gr Xr + Gi Xi,  im = Gi Xr - Gr Xi
+      dr[q] = mfma4(gr, x2.x, dr[q]);
+      dr[q] = mfma4(gi, x2.y, dr[q]);
+      di[q] = mfma4(gi, x2.x, di[q]);
+      di[q] = mfma4(-gr, x2.y, di[q]);
     }
-    if (b02 == 0) {  // the group is complete: project its runs onto the taps
+    b0 += 4;
+    if (b0 >= B) {  // the group is complete: project its runs onto the taps
 #pragma unroll
       for (int r = 0; r < kGwRuns; ++r) {
         const int g = grp * kGwRuns + r;
         if (g < nrun) gw_project_run<NK>(gw, dr, di, r, g, nmain, H, P, tw);
       }
+      b0 = 0, ++grp;
     }
-    grp = grp2, b0 = b02;
+  };
+  const int nsteps = max(0, gr_end - gr_begin) * ((B + 3) / 4);
+  int t = 0;
+  for (; t + 1 < nsteps; t += 2) {  // one path round the loop keeps the wait counts exact
+    step(ra, 0);
+    step(rb, 1);
   }
+  if (t < nsteps) step(ra, 0);
   // this chunk's partial sums
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const int gs = s0 + 4 * kq + j, gc = c0 + mrow;
-    if (gs >= S || gc >= C) continue;
-    float *p = part + (((long long)chunk * S + gs) * C + gc) * T;
+    const int os = s0 + 4 * kq + j, oc = c0 + mrow;
+    if (os >= S || oc >= C) continue;
+    float *p = part + (((long long)chunk * S + os) * C + oc) * T;
 #pragma unroll
     for (int t = 0; t < T; ++t) p[t] = gw[j][t];
   }
@@ -502,7 +532,7 @@ hipError_t launch_full_gw(int nk, SpecLayout G, SpecLayout X, const float2 *tw, 
   const int chunks = full_gw_chunks(B, S, C, P, nk);
   const int groups_per_chunk = (ngroups + chunks - 1) / chunks;
   const int tiles = ((S + 31) / 32) * ((C + 31) / 32);
-  const size_t lds = (size_t)P * sizeof(float2);
+  const size_t lds = ((size_t)((P + 31) & ~31) + 2 * kGwStageElems) * sizeof(float2);
   hipError_t err = hipErrorInvalidValue;
   dispatch_nk(nk, [&](auto nc) {
     constexpr int NK = decltype(nc)::value;
