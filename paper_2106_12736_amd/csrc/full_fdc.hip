@@ -225,27 +225,26 @@ __global__ __launch_bounds__(256) void k_full_contract(SpecLayout in, const floa
 // batch rows past the end are clamped and masked to zero, channels and runs past the
 // end are clamped and their results dropped.
 // ---------------------------------------------------------------------------
-// Runs per work item: 2 (8 bins), which keeps a wave within 256 registers so that two
-// waves share a SIMD and one's projection overlaps the other's matrix-core work.
+// Twiddles W^i for i < n P in LDS: every phase index the projection forms (k a,
+// (l + q) b with k < P, l + q < P/2, a, b < n) is then a plain table index.
 template <int NK>
-__host__ __device__ constexpr int gw_runs() {
-  return 2;
+__host__ __device__ constexpr int gw_tw_elems(int P) {
+  return (NK * P + 31) & ~31;
 }
 
-// Adds one run's gK (4 bins: d*[q], lane rows j) projected onto the taps to gw.
+// Adds one run's gK (4 bins: dr/di[q], lane rows j) projected onto the taps to gw.
+// Row run (k, l0..l0+3); Nyquist run (k0..k0+3, P/2) when side.
 template <int NK>
-__device__ __forceinline__ void gw_project_run(float (&gw)[4][NK * NK], const v4f (&dr)[4 * gw_runs<NK>()],
-                                               const v4f (&di)[4 * gw_runs<NK>()], int r, int g, int nmain, int H, int P,
-                                               const float2 *tw) {
-  if (g < nmain) {
-    const int k = (4 * g) / H, l0 = 4 * g - k * H;
+__device__ __forceinline__ void gw_project_run(float (&gw)[4][NK * NK], const v4f (&dr)[4], const v4f (&di)[4],
+                                               bool side, int k, int l0, const float2 *tw) {
+  if (!side) {
     float2 u[NK], v[4][NK];
 #pragma unroll
-    for (int a = 0; a < NK; ++a) u[a] = tw[(k * a) % P];
+    for (int a = 0; a < NK; ++a) u[a] = tw[k * a];
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int b = 0; b < NK; ++b) v[q][b] = tw[((l0 + q) * b) % P];
+      for (int b = 0; b < NK; ++b) v[q][b] = tw[(l0 + q) * b];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -253,56 +252,76 @@ __device__ __forceinline__ void gw_project_run(float (&gw)[4][NK * NK], const v4
         float ex = 0.f, ey = 0.f;  // E_b = sum_q D_q conj(v_qb)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          ex = fmaf(dr[4 * r + q][j], v[q][b].x, ex);
-          ex = fmaf(di[4 * r + q][j], v[q][b].y, ex);
-          ey = fmaf(di[4 * r + q][j], v[q][b].x, ey);
-          ey = fmaf(-dr[4 * r + q][j], v[q][b].y, ey);
+          ex = fmaf(dr[q][j], v[q][b].x, ex);
+          ex = fmaf(di[q][j], v[q][b].y, ex);
+          ey = fmaf(di[q][j], v[q][b].x, ey);
+          ey = fmaf(-dr[q][j], v[q][b].y, ey);
         }
 #pragma unroll
         for (int a = 0; a < NK; ++a) gw[j][a * NK + b] = fmaf(ey, u[a].y, fmaf(ex, u[a].x, gw[j][a * NK + b]));
       }
   } else {
-    const int k0 = 4 * (g - nmain);
     float2 u[4][NK];
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int a = 0; a < NK; ++a) u[q][a] = tw[((k0 + q) * a) % P];
+      for (int a = 0; a < NK; ++a) u[q][a] = tw[(k + q) * a];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int a = 0; a < NK; ++a) {
         float f = 0.f;  // Re F_a = Re sum_q D_q conj(u_qa)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) f = fmaf(di[4 * r + q][j], u[q][a].y, fmaf(dr[4 * r + q][j], u[q][a].x, f));
+        for (int q = 0; q < 4; ++q) f = fmaf(di[q][j], u[q][a].y, fmaf(dr[q][j], u[q][a].x, f));
 #pragma unroll
         for (int b = 0; b < NK; ++b) gw[j][a * NK + b] += (b & 1) ? -f : f;
       }
   }
 }
 
-// LDS staging of one step (4 batch rows, kGwRuns runs of 4 bins) for a 32 x 32
-// (s, c) block: G rows [4][32][kGwStage] and X rows [4][32][kGwStage] complex, each
-// (b, s) row holding the step's 4 * kGwRuns bins plus one of padding.  Every element
-// is loaded from memory once per workgroup (the four waves read each operand row
-// twice: waves 0/1 share s rows, 0/2 share c rows).
-constexpr int kGwStage = 4 * 2 + 1;
-constexpr int kGwStageElems = 2 * 4 * 32 * kGwStage;
+// Position of a run of 4 bins, advanced one run at a time (no divisions on the way).
+struct GwRun {
+  int g, k, l0;  // run index; row k and first column l0 (row runs) or first row k (Nyquist runs)
+  __device__ void start(int g0, int nmain, int H) {
+    g = g0;
+    if (g < nmain) {
+      k = (4 * g) / H, l0 = 4 * g - k * H;
+    } else {
+      k = 4 * (g - nmain), l0 = 0;
+    }
+  }
+  __device__ void next(int nmain, int H) {
+    ++g;
+    if (g == nmain) {
+      k = 0, l0 = 0;
+    } else if (g > nmain) {
+      k += 4;
+    } else if ((l0 += 4) == H) {
+      l0 = 0, ++k;
+    }
+  }
+};
+
+// LDS staging of one step (4 batch rows, one run of 4 bins) for a 32 x 32 (s, c)
+// block: G rows [4][32][5] and X rows [4][32][5] complex, each (b, s) row holding the
+// run's 4 bins and one of padding.  Every element is loaded from memory once per
+// workgroup (the four waves read each operand row twice: waves 0/1 share s rows, 0/2
+// share c rows).
+constexpr int kGwStageRow = 5;
+constexpr int kGwStageElems = 2 * 4 * 32 * kGwStageRow;
 
 template <int NK>
 __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, const float2 *__restrict__ twg,
                                                  float *__restrict__ part, int B, int S, int C, int P,
-                                                 int groups_per_chunk) {
-  constexpr int T = NK * NK, kGwRuns = gw_runs<NK>();
-  static_assert(4 * kGwRuns + 1 == kGwStage, "stage row holds the step's bins and one pad");
+                                                 int runs_per_chunk) {
+  constexpr int T = NK * NK, SR = kGwStageRow, SE = kGwStageElems;
   extern __shared__ float smem[];
   float2 *tw = reinterpret_cast<float2 *>(smem);
-  float2 *stage = tw + ((P + 31) & ~31);  // two buffers of kGwStageElems
-  for (int i = threadIdx.x; i < P; i += 256) tw[i] = twg[i];
+  float2 *stage = tw + gw_tw_elems<NK>(P);  // two buffers of SE
+  for (int i = threadIdx.x; i < NK * P; i += 256) tw[i] = twg[i % P];
   __syncthreads();
 
   const int H = P / 2, nmain = P * H / 4, nrun = nmain + P / 4;
-  const int ngroups = (nrun + kGwRuns - 1) / kGwRuns;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int mrow = lane & 15, kq = lane >> 4;
   const int sblocks = (S + 31) / 32, cblocks = (C + 31) / 32;
@@ -310,11 +329,18 @@ __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, 
   const int tile = blk % (sblocks * cblocks), chunk = blk / (sblocks * cblocks);
   const int sbase = (tile / cblocks) * 32, cbase = (tile % cblocks) * 32;
   const int s0 = sbase + (wave >> 1) * 16, c0 = cbase + (wave & 1) * 16;
-  const int gr_begin = chunk * groups_per_chunk, gr_end = min(ngroups, gr_begin + groups_per_chunk);
-  // cooperative loads: thread = (batch row lb, block row lr, run lrun)
-  const int lrun = threadIdx.x & 1, lr = (threadIdx.x >> 1) & 31, lb = threadIdx.x >> 6;
-  static_assert(kGwRuns == 2, "cooperative load mapping assumes two runs per step");
-  const int gs = min(sbase + lr, S - 1), gc = min(cbase + lr, C - 1);
+  const int r_begin = chunk * runs_per_chunk, r_end = min(nrun, r_begin + runs_per_chunk);
+
+  // Cooperative loads: wave lb takes batch row b0 + lb of the step; lane (lr, unit)
+  // loads the run's 4 bins of G row sbase + lr (unit 0) or X row cbase + lr (unit 1).
+  // Per-lane bases and batch strides of both blocks, so that a step's address is one
+  // multiply-add.
+  const int lb = wave, unit = lane & 1, lr = lane >> 1;
+  const SpecLayout &L = unit ? X : G;
+  const long long row = unit ? min(cbase + lr, C - 1) : min(sbase + lr, S - 1);
+  const long long nch = unit ? C : S;
+  const float2 *mbase = L.main + row * L.ps, *sbase_p = L.side + row * L.sps;
+  const long long mbst = nch * L.ps, sbst = nch * L.sps, mrs = L.rs;
 
   float gw[4][T];  // rows s0 + 4 (lane / 16) + j, column c0 + lane % 16
 #pragma unroll
@@ -322,71 +348,67 @@ __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, 
 #pragma unroll
     for (int t = 0; t < T; ++t) gw[j][t] = 0.f;
 
-  // This thread's share of a step: 4 bins of G (r[0], r[1]) and of X (r[2], r[3]) for
-  // batch row b0 + lb, block row lr, run lrun.  Two register sets hold the loads of the
-  // next two steps, so that the loads of step t + 2 are in flight while step t computes.
-  int lgrp = gr_begin, lb0 = 0;  // load cursor
-  // (past the chunk's last step the run index is clamped and the load is not used: an
-  // unconditional load keeps the wait counts exact, so step t waits for its own loads only)
-  auto load_next = [&](float4(&r)[4]) {
+  // Two register sets hold the loads of the next two steps, so that the loads of step
+  // t + 2 are in flight while step t computes.  Past the chunk's last step the run is
+  // clamped and the load is not used: an unconditional load keeps the wait counts
+  // exact, so step t waits for its own loads only.
+  GwRun lrun;
+  lrun.start(r_begin, nmain, H);
+  int lb0 = 0;  // load cursor: run lrun, batch rows lb0..lb0+3
+  auto load_next = [&](float4(&r)[2]) {
     const long long bc = min(lb0 + lb, B - 1);
-    const int g = min(lgrp * kGwRuns + lrun, nrun - 1);
-    const bool side = g >= nmain;
-    const int k = (4 * g) / H, l0 = 4 * g - k * H;  // row run (k, l0..l0+3) when not on the side
-    const float4 *ga = reinterpret_cast<const float4 *>(
-        side ? G.side + (bc * S + gs) * G.sps + 4 * (g - nmain) : G.main + (bc * S + gs) * G.ps + k * G.rs + l0);
-    const float4 *xa = reinterpret_cast<const float4 *>(
-        side ? X.side + (bc * C + gc) * X.sps + 4 * (g - nmain) : X.main + (bc * C + gc) * X.ps + k * X.rs + l0);
-    r[0] = ga[0], r[1] = ga[1], r[2] = xa[0], r[3] = xa[1];
+    const bool side = lrun.g >= nmain;
+    const int gk = min(lrun.k, side ? P - 4 : P - 1);  // in range past the last run
+    const float2 *a = side ? sbase_p + bc * sbst + gk : mbase + bc * mbst + gk * mrs + lrun.l0;
+    const float4 *a4 = reinterpret_cast<const float4 *>(a);
+    r[0] = a4[0], r[1] = a4[1];
     lb0 += 4;
-    if (lb0 >= B) lb0 = 0, ++lgrp;
+    if (lb0 >= B) lb0 = 0, lrun.next(nmain, H);
   };
-  float4 ra[4], rb[4];
+  float4 ra[2], rb[2];
   load_next(ra);
   load_next(rb);
-  v4f dr[4 * kGwRuns], di[4 * kGwRuns];
-  int grp = gr_begin, b0 = 0;  // compute cursor
+  v4f dr[4], di[4];
+  GwRun crun;
+  crun.start(r_begin, nmain, H);
+  int b0 = 0;  // compute cursor
   // one step: registers r (loaded two steps ago) into LDS buffer buf, then the products
-  auto step = [&](float4(&r)[4], int buf) {
+  auto step = [&](float4(&r)[2], int buf) {
     // (the barrier below also ends every wave's reads of this buffer two steps ago)
     {
-      float2 *sg = stage + buf * kGwStageElems + (lb * 32 + lr) * kGwStage + 4 * lrun;
-      float2 *sx = sg + 4 * 32 * kGwStage;
-      sg[0] = make_float2(r[0].x, r[0].y), sg[1] = make_float2(r[0].z, r[0].w);
-      sg[2] = make_float2(r[1].x, r[1].y), sg[3] = make_float2(r[1].z, r[1].w);
-      sx[0] = make_float2(r[2].x, r[2].y), sx[1] = make_float2(r[2].z, r[2].w);
-      sx[2] = make_float2(r[3].x, r[3].y), sx[3] = make_float2(r[3].z, r[3].w);
+      float2 *d = stage + buf * SE + unit * (4 * 32 * SR) + (lb * 32 + lr) * SR;
+      if (b0 + lb < B) {
+        d[0] = make_float2(r[0].x, r[0].y), d[1] = make_float2(r[0].z, r[0].w);
+        d[2] = make_float2(r[1].x, r[1].y), d[3] = make_float2(r[1].z, r[1].w);
+      } else {  // batch rows past the end add nothing
+        d[0] = d[1] = d[2] = d[3] = make_float2(0.f, 0.f);
+      }
     }
     __syncthreads();
     load_next(r);
     if (b0 == 0) {
 #pragma unroll
-      for (int q = 0; q < 4 * kGwRuns; ++q) dr[q] = di[q] = v4f{0.f, 0.f, 0.f, 0.f};
+      for (int q = 0; q < 4; ++q) dr[q] = di[q] = v4f{0.f, 0.f, 0.f, 0.f};
     }
-    const float m = b0 + kq < B ? 1.f : 0.f;  // batch rows past the end add nothing
-    const float2 *ag = stage + buf * kGwStageElems + (kq * 32 + (s0 - sbase) + mrow) * kGwStage;
-    const float2 *ax = stage + buf * kGwStageElems + 4 * 32 * kGwStage + (kq * 32 + (c0 - cbase) + mrow) * kGwStage;
+    const float2 *ag = stage + buf * SE + (kq * 32 + (s0 - sbase) + mrow) * SR;
+    const float2 *ax = stage + buf * SE + 4 * 32 * SR + (kq * 32 + (c0 - cbase) + mrow) * SR;
 #pragma unroll
-    for (int q = 0; q < 4 * kGwRuns; ++q) {
+    for (int q = 0; q < 4; ++q) {
       const float2 g2 = ag[q], x2 = ax[q];
-      const float gr = m * g2.x, gi = m * g2.y;
       // D = G conj(X):  re = Gr Xr + Gi Xi,  im = Gi Xr - Gr Xi
-      dr[q] = mfma4(gr, x2.x, dr[q]);
-      dr[q] = mfma4(gi, x2.y, dr[q]);
-      di[q] = mfma4(gi, x2.x, di[q]);
-      di[q] = mfma4(-gr, x2.y, di[q]);
+      dr[q] = mfma4(g2.x, x2.x, dr[q]);
+      dr[q] = mfma4(g2.y, x2.y, dr[q]);
+      di[q] = mfma4(g2.y, x2.x, di[q]);
+      di[q] = mfma4(-g2.x, x2.y, di[q]);
     }
     b0 += 4;
-    if (b0 >= B) {  // the group is complete: project its runs onto the taps
-#pragma unroll
-      for (int r = 0; r < kGwRuns; ++r) {
-        const int g = grp * kGwRuns + r;
-        if (g < nrun) gw_project_run<NK>(gw, dr, di, r, g, nmain, H, P, tw);
-      }
-      b0 = 0, ++grp;
+    if (b0 >= B) {  // the run is complete: project it onto the taps
+      gw_project_run<NK>(gw, dr, di, crun.g >= nmain, crun.k, crun.l0, tw);
+      b0 = 0;
+      crun.next(nmain, H);
     }
   };
-  const int nsteps = max(0, gr_end - gr_begin) * ((B + 3) / 4);
+  const int nsteps = max(0, r_end - r_begin) * ((B + 3) / 4);
   int t = 0;
   for (; t + 1 < nsteps; t += 2) {  // one path round the loop keeps the wait counts exact
     step(ra, 0);
@@ -505,22 +527,16 @@ hipError_t launch_full_contract(bool gx, int nk, SpecLayout in, const float *wt,
   return err;
 }
 
-static int gw_runs_rt(int nk) {
-  (void)nk;
-  return 2;
-}
-
 // Bin chunks of the dL/dw pass: about 8192 workgroups, so that the workgroups running
 // at one time on an XCD are the tiles of one or two short chunks and share the spectra
 // they read through L2; at most 512 chunks of partial sums.
 int full_gw_chunks(int B, int S, int C, int P, int nk) {
-  (void)B;
+  (void)B, (void)nk;
   const int nrun = P * (P / 2) / 4 + P / 4;
-  const int ngroups = (nrun + gw_runs_rt(nk) - 1) / gw_runs_rt(nk);
   const int tiles = ((S + 31) / 32) * ((C + 31) / 32);
   int chunks = (8192 + tiles - 1) / tiles;
   if (chunks > 512) chunks = 512;
-  if (chunks > ngroups) chunks = ngroups;
+  if (chunks > nrun) chunks = nrun;
   if (chunks < 1) chunks = 1;
   return chunks;
 }
@@ -529,17 +545,17 @@ hipError_t launch_full_gw(int nk, SpecLayout G, SpecLayout X, const float2 *tw, 
                           int C, int P, hipStream_t s) {
   if (P % 8 != 0) return hipErrorInvalidValue;
   const int nrun = P * (P / 2) / 4 + P / 4;
-  const int ngroups = (nrun + gw_runs_rt(nk) - 1) / gw_runs_rt(nk);
   const int chunks = full_gw_chunks(B, S, C, P, nk);
-  const int groups_per_chunk = (ngroups + chunks - 1) / chunks;
+  const int runs_per_chunk = (nrun + chunks - 1) / chunks;
   const int tiles = ((S + 31) / 32) * ((C + 31) / 32);
-  const size_t lds = ((size_t)((P + 31) & ~31) + 2 * kGwStageElems) * sizeof(float2);
   hipError_t err = hipErrorInvalidValue;
   dispatch_nk(nk, [&](auto nc) {
     constexpr int NK = decltype(nc)::value;
+    const size_t lds = ((size_t)gw_tw_elems<NK>(P) + 2 * kGwStageElems) * sizeof(float2);
+    if (lds > 65536) return;  // (P <= 1024, n <= 5 stays within 60 KB)
     timing_before("full_gw", s);
     hipLaunchKernelGGL((k_full_gw<NK>), dim3((unsigned)(tiles * chunks)), dim3(256), lds, s, G, X, tw, part, B, S, C,
-                       P, groups_per_chunk);
+                       P, runs_per_chunk);
     err = hipGetLastError();
     timing_after("full_gw", s);
   });
