@@ -233,46 +233,59 @@ __host__ __device__ constexpr int gw_tw_elems(int P) {
 }
 
 // Adds one run's gK (4 bins: dr/di[q], lane rows j) projected onto the taps to gw.
-// Row run (k, l0..l0+3); Nyquist run (k0..k0+3, P/2) when side.
-template <int NK>
-__device__ __forceinline__ void gw_project_run(float (&gw)[4][NK * NK], const v4f (&dr)[4], const v4f (&di)[4],
-                                               bool side, int k, int l0, const float2 *tw) {
-  if (!side) {
+// Row run (k, l0..l0+3); Nyquist run (k0..k0+3, P/2) when SIDE.  The phases of tap
+// row / column 0 are exactly 1, so their products are plain sums.
+template <int NK, bool SIDE>
+__device__ __forceinline__ void gw_project_run(float (&gw)[4][NK * NK], const v4f (&dr)[4], const v4f (&di)[4], int k,
+                                               int l0, const float2 *tw) {
+  if constexpr (!SIDE) {
     float2 u[NK], v[4][NK];
 #pragma unroll
-    for (int a = 0; a < NK; ++a) u[a] = tw[k * a];
+    for (int a = 1; a < NK; ++a) u[a] = tw[k * a];
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int b = 0; b < NK; ++b) v[q][b] = tw[(l0 + q) * b];
+      for (int b = 1; b < NK; ++b) v[q][b] = tw[(l0 + q) * b];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int b = 0; b < NK; ++b) {
-        float ex = 0.f, ey = 0.f;  // E_b = sum_q D_q conj(v_qb)
+        float ex, ey;  // E_b = sum_q D_q conj(v_qb)
+        if (b == 0) {
+          ex = (dr[0][j] + dr[1][j]) + (dr[2][j] + dr[3][j]);
+          ey = (di[0][j] + di[1][j]) + (di[2][j] + di[3][j]);
+        } else {
+          ex = ey = 0.f;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          ex = fmaf(dr[q][j], v[q][b].x, ex);
-          ex = fmaf(di[q][j], v[q][b].y, ex);
-          ey = fmaf(di[q][j], v[q][b].x, ey);
-          ey = fmaf(-dr[q][j], v[q][b].y, ey);
+          for (int q = 0; q < 4; ++q) {
+            ex = fmaf(dr[q][j], v[q][b].x, ex);
+            ex = fmaf(di[q][j], v[q][b].y, ex);
+            ey = fmaf(di[q][j], v[q][b].x, ey);
+            ey = fmaf(-dr[q][j], v[q][b].y, ey);
+          }
         }
+        gw[j][b] += ex;
 #pragma unroll
-        for (int a = 0; a < NK; ++a) gw[j][a * NK + b] = fmaf(ey, u[a].y, fmaf(ex, u[a].x, gw[j][a * NK + b]));
+        for (int a = 1; a < NK; ++a) gw[j][a * NK + b] = fmaf(ey, u[a].y, fmaf(ex, u[a].x, gw[j][a * NK + b]));
       }
   } else {
     float2 u[4][NK];
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int a = 0; a < NK; ++a) u[q][a] = tw[(k + q) * a];
+      for (int a = 1; a < NK; ++a) u[q][a] = tw[(k + q) * a];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int a = 0; a < NK; ++a) {
-        float f = 0.f;  // Re F_a = Re sum_q D_q conj(u_qa)
+        float f;  // Re F_a = Re sum_q D_q conj(u_qa)
+        if (a == 0) {
+          f = (dr[0][j] + dr[1][j]) + (dr[2][j] + dr[3][j]);
+        } else {
+          f = 0.f;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) f = fmaf(di[q][j], u[q][a].y, fmaf(dr[q][j], u[q][a].x, f));
+          for (int q = 0; q < 4; ++q) f = fmaf(di[q][j], u[q][a].y, fmaf(dr[q][j], u[q][a].x, f));
+        }
 #pragma unroll
         for (int b = 0; b < NK; ++b) gw[j][a * NK + b] += (b & 1) ? -f : f;
       }
@@ -403,7 +416,10 @@ __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, 
     }
     b0 += 4;
     if (b0 >= B) {  // the run is complete: project it onto the taps
-      gw_project_run<NK>(gw, dr, di, crun.g >= nmain, crun.k, crun.l0, tw);
+      if (crun.g >= nmain)
+        gw_project_run<NK, true>(gw, dr, di, crun.k, crun.l0, tw);
+      else
+        gw_project_run<NK, false>(gw, dr, di, crun.k, crun.l0, tw);
       b0 = 0;
       crun.next(nmain, H);
     }
