@@ -219,10 +219,10 @@ __global__ __launch_bounds__(256) void k_full_contract(SpecLayout in, const floa
 // done per run: a row run sums E_b = sum_q gK_q conj(W^(l_q b)) and adds
 // Re(E_b conj(W^(k a))); a Nyquist run sums F_a = sum_q gK_q conj(W^(k_q a)) and adds
 // (-1)^b Re(F_a).  A workgroup (4 waves) owns a 32 x 32 (s, c) block, each wave a
-// 16 x 16 tile, and walks its chunk 2 runs (8 bins) at a time, 4 batch rows per step.
+// 16 x 16 tile, and walks its chunk one run (4 bins) at a time, 4 batch rows per step.
 // A step's G and X rows are loaded once per workgroup and staged in LDS, and the
 // loads of step t + 2 are in flight while step t computes.  Loads are unconditional:
-// batch rows past the end are clamped and masked to zero, channels and runs past the
+// batch rows past the end are clamped and staged as zeros, channels and runs past the
 // end are clamped and their results dropped.
 // ---------------------------------------------------------------------------
 // Twiddles W^i for i < n P in LDS: every phase index the projection forms (k a,
