@@ -167,6 +167,22 @@ def chain_step_launches(wl, input_grad=False):
     return out
 
 
+def classifier_step_launches(wl, classes, n_params):
+    """One training step of the FDCNN classifier: the chain forward, the head forward
+    (ReLU + fully connected layer, then the loss), the head backward, the chain backward
+    (no input gradient), and the Adam update of every parameter (plus its step count)."""
+    chain = chain_step_launches(wl, False)
+    n_fwd = 2 + wl.layers + 2  # rfft2 (rows, columns), the layers, irfft2 (columns, rows)
+    B, F = wl.batch, wl.channels[-1] * wl.sizes[-1] ** 2
+    chunks = -(-F // 1024)
+    head = [
+        ("head_fwd", F32 * (B * F + classes * F + B * chunks * classes)),
+        ("head_loss", F32 * (B * chunks * classes + classes + 2 * B * classes)),
+        ("head_bwd", F32 * (2 * B * F + 2 * classes * F + B * classes)),
+    ]
+    return chain[:n_fwd] + head + chain[n_fwd:] + [("adam", 7 * F32 * n_params), ("adam_count", 8)]
+
+
 def spatial_step_launches(wl, n, input_grad=False, ranges=None):
     """(kernel name, algorithmic bytes) of every launch of one step of the stack with
     n x n spatial kernels (layer by layer, ROLL): step_launches plus the kernel-spectrum
@@ -333,6 +349,37 @@ def spatial_cpu_baseline(wl, data, min_seconds=10.0, max_reps=50):
 # main
 # ----------------------------------------------------------------------------
 
+def classifier_cpu_baseline(wl, data, W, bias, labels, min_seconds=10.0, max_reps=50):
+    """The oracle's training step of the classifier (chain, head, Adam) on the same
+    inputs, repeated to about min_seconds."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import classifier
+
+    x = data.x.astype(np.float64)
+    kd = [k.astype(np.complex128) for k in data.kernels]
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        _, _, gks, gW, gb = classifier.classifier_gradients(x, kd, W, bias, labels, wl.sizes)
+        flat_p = np.concatenate([np.concatenate([k.view(np.float64).ravel() for k in kd]), W.ravel(), bias])
+        flat_g = np.concatenate([np.concatenate([g.view(np.float64).ravel() for g in gks]), gW.ravel(), gb])
+        classifier.adam_step(flat_p, flat_g, 0 * flat_p, 0 * flat_p, 1, 1e-5, 0.9, 0.999, 1e-8, 1e-6)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds or reps >= max_reps:
+            break
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {
+        "value": reps * wl.batch / el,
+        "unit": "images/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{reps} full training step(s) of the same workload (batch {wl.batch}, chain of {wl.layers} "
+                  f"layers, head, Adam, float64) in {el:.1f} s on {os.cpu_count()} host CPUs visible",
+    }
+
+
 class CicStackRun:
     """The CIC + FDP stack step on preallocated buffers: the fused stack executor
     (fdc_cic_stack_*), or the layer-by-layer calls with --per-layer."""
@@ -348,6 +395,7 @@ class CicStackRun:
         self.g = torch.from_numpy(self.data.grad).to(dev)
         self.per_layer = args.per_layer
         self.executor = "chain" if args.chain else ("per_layer" if args.per_layer else "fused_stack")
+        self.clf = None
         self.spatial = args.spatial_kernel
         if self.spatial:
             self.executor = "per_layer"
@@ -357,6 +405,20 @@ class CicStackRun:
             self.g = torch.from_numpy(self.data.grad).to(dev)
             self.stack = layers.CicSpatialStack(wl.batch, wl.sizes, wl.channels, self.spatial, device=dev)
             model = lambda w_, ig: spatial_step_launches(w_, self.spatial, ig, self.stack.dk_ranges())  # noqa: E731
+        elif args.classifier:
+            import numpy as np
+            self.executor = "classifier"
+            classes = 2
+            self.clf = layers.FdcnnClassifier(wl.batch, wl.sizes, wl.channels, classes=classes, device=dev)
+            self.stack = self.clf.chain
+            F = self.clf.features
+            rng = np.random.default_rng(20210700 + wl.index)
+            self.W = (rng.standard_normal((classes, F)) * np.sqrt(2.0 / F)).astype(np.float32)
+            self.bias = np.zeros(classes, np.float32)
+            self.labels = (np.arange(wl.batch) % classes).astype(np.int32)
+            self.clf.load(self.Ks, torch.from_numpy(self.W).to(dev), torch.from_numpy(self.bias).to(dev))
+            self.labels_d = torch.from_numpy(self.labels).to(dev)
+            model = lambda w_, ig: classifier_step_launches(w_, classes, self.clf.n_params)  # noqa: E731
         elif args.chain:
             self.stack = layers.CicChain(wl.batch, wl.sizes, wl.channels, device=dev)
             model = chain_step_launches
@@ -373,23 +435,43 @@ class CicStackRun:
         self.api_bytes = step_api_bytes(wl, args.input_grad)
 
     def step(self):
+        if self.clf is not None:
+            self.clf.train_step(self.x, self.labels_d)
+            return
         self.stack.forward(self.x, self.Ks)
         self.stack.backward(self.g, self.Ks, input_grad=self.gin)
 
     def outputs(self):
+        if self.clf is not None:
+            return [self.clf.loss, self.clf.logits, self.clf.params, self.clf.m, self.clf.v, self.clf.step_count]
         last = self.stack.acts[-1] if self.executor == "per_layer" else self.stack.out
         return [last] + list(self.stack.gws if self.spatial else self.stack.gks)
 
+    def save_state(self):
+        """Training state a step changes (classifier only), for the graph replay check."""
+        return self.clf.state() if self.clf is not None else None
+
+    def restore_state(self, st):
+        if st is not None:
+            self.clf.set_state(st)
+
     def config(self):
         wl = self.wl
-        return {"workload": wl.name, "batch": wl.batch, "sizes": list(wl.sizes), "channels": list(wl.channels),
-                "input_grad": bool(self.input_grad),
-                "executor": self.executor,
-                "kernels": f"spatial {self.spatial}x{self.spatial}, roll" if self.spatial else "spectral"}
+        cfg = {"workload": wl.name, "batch": wl.batch, "sizes": list(wl.sizes), "channels": list(wl.channels),
+               "input_grad": bool(self.input_grad),
+               "executor": self.executor,
+               "kernels": f"spatial {self.spatial}x{self.spatial}, roll" if self.spatial else "spectral"}
+        if self.clf is not None:
+            cfg["head"] = (f"relu, fully connected {self.clf.features} -> {self.clf.classes}, softmax cross-entropy; "
+                           f"adam lr {self.clf.lr:g}, weight decay {self.clf.weight_decay:g}")
+        return cfg
 
     def cpu_baseline(self):
         if self.spatial:
             return spatial_cpu_baseline(self.wl, self.data)
+        if self.clf is not None:
+            return classifier_cpu_baseline(self.wl, self.data, self.W.astype("float64"), self.bias.astype("float64"),
+                                           self.labels)
         return cpu_baseline(self.wl, self.data, chain=self.executor == "chain")
 
 
@@ -557,6 +639,9 @@ def main():
     ap.add_argument("--chain", action="store_true",
                     help="CIC stack: the FDCNN data flow of section 2.5.1 (one rfft2, FDC + FDP layers on spectra, "
                          "one irfft2); a different function from the per-layer transforms")
+    ap.add_argument("--classifier", action="store_true",
+                    help="CIC stack: one training step of the FDCNN classifier (the chain of --chain, a ReLU, a "
+                         "fully connected layer to 2 classes, softmax cross-entropy, Adam)")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of HIP graph replays")
     ap.add_argument("--flush-mib", type=int, default=512, metavar="MIB",
                     help="buffer written between the individually timed steps of the step-time "
@@ -624,12 +709,15 @@ def main():
     # captured launches reuse them); a replay must reproduce the eager step exactly
     graph = None
     if not args.eager:
+        state = run.save_state() if hasattr(run, "save_state") else None
         step()
         torch.cuda.synchronize()
         ref = [t.clone() for t in run.outputs()]
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
             step()
+        if state is not None:  # a training step changes its own state: replay from the same one
+            run.restore_state(state)
         graph.replay()
         torch.cuda.synchronize()
         if not all(torch.equal(a, b) for a, b in zip(ref, run.outputs())):

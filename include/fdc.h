@@ -258,6 +258,39 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *plan, const float *gy, c
                                   size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
+/* FDCNN classifier head and optimiser                                      */
+/* ------------------------------------------------------------------------ */
+/* The FDCNN of section 2.5.1 (Fig. 3) applies a ReLU to the spatial output of its final
+ * inverse transform and feeds it to fully connected layers; section 3.1 trains it with
+ * the cross-entropy loss and Adam with weight decay.  The head here is ReLU, one fully
+ * connected layer to `classes` outputs (1..16) and the softmax cross-entropy averaged
+ * over the batch.
+ *   y [B][F] fp32 (the chain output, F = C * M * M), W [classes][F], bias [classes],
+ *   labels [B] int32 in [0, classes) (device memory), logits [B][classes], loss [1].
+ * Every sum runs in a fixed order.  B * classes <= 15872.  An out-of-range label is
+ * not detected on the host: it gives a NaN loss and NaN gradients. */
+fdc_status fdc_head_workspace_size(int B, int64_t F, int classes, size_t *bytes);
+/* logits = relu(y) W^T + bias; loss = mean_b (logsumexp(logits[b]) - logits[b][labels[b]]).
+ * ws: fdc_head_workspace_size bytes of scratch (partial logits). */
+fdc_status fdc_head_forward(const float *y, const float *W, const float *bias, const int32_t *labels, float *logits,
+                            float *loss, int B, int64_t F, int classes, void *ws, size_t ws_bytes,
+                            hipStream_t stream);
+/* From the forward's logits: dlogits = (softmax(logits) - onehot(labels)) / B;
+ * gW = dlogits^T relu(y), gbias = sum_b dlogits, gy = [y > 0] (dlogits W) (gy NULL:
+ * skipped).  All outputs are overwritten. */
+fdc_status fdc_head_backward(const float *y, const float *W, const float *logits, const int32_t *labels, float *gy,
+                             float *gW, float *gbias, int B, int64_t F, int classes, hipStream_t stream);
+/* One Adam step (Kingma and Ba, with weight decay added to the gradient as PyTorch's
+ * Adam does) over n floats, in place on p, m and v (m, v start at zero).  A complex
+ * parameter is updated as its (re, im) float pairs.  step_count is a device int32
+ * holding the steps taken so far (start it at 0); the call updates with t = count + 1
+ * and then stores t, so a captured graph advances on every replay.
+ *   g' = g + wd p;  m = b1 m + (1 - b1) g';  v = b2 v + (1 - b2) g'^2;
+ *   p -= lr / (1 - b1^t) * m / (sqrt(v) / sqrt(1 - b2^t) + eps). */
+fdc_status fdc_adam_step(float *p, const float *g, float *m, float *v, int64_t n, int32_t *step_count, float lr,
+                         float beta1, float beta2, float eps, float weight_decay, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
 /* Kernel timing (measurement support, off by default)                      */
 /* ------------------------------------------------------------------------ */
 /* While enabled, every kernel the library launches (only those named

@@ -19,10 +19,12 @@ The oracle is plain, slow and written to be checked by eye against the paper:
 * ``conv``  -- brute-force spatial convolutions (Eq. 1, Eq. 2 and the circular
                convolution the convolution theorem refers to), used to pin the
                oracle against a computation that involves no transform at all.
+* ``classifier`` -- the FDCNN head of section 2.5.1 (ReLU, a fully connected
+               layer, softmax cross-entropy) and the Adam step of section 3.1.
 
 Every function works in float64 (complex128 for spectra).  Pins: see the
 ``-m "not gpu"`` tests in ``tests/test_oracle_*.py``.  No oracle function is
 "parity unpinned".
 """
 
-from . import conv, dft, fdc  # noqa: F401
+from . import classifier, conv, dft, fdc  # noqa: F401

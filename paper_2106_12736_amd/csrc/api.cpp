@@ -877,6 +877,55 @@ fdc_status fdc_full_backward(const fdc_layer_plan *p, const float *gy, const voi
 }
 
 // ---------------------------------------------------------------------------
+// FDCNN classifier head and Adam
+// ---------------------------------------------------------------------------
+static fdc_status check_head(int B, int64_t F, int classes) {
+  if (B < 1 || F < 1) return fail(FDC_EINVAL, "B and F must be positive (got %d, %lld)", B, (long long)F);
+  if (classes < 1 || classes > fdc::kHeadMaxClasses)
+    return fail(FDC_EUNSUPPORTED, "classes must be in [1, %d] (got %d)", fdc::kHeadMaxClasses, classes);
+  if ((long long)B * classes > fdc::kHeadMaxPairs)
+    return fail(FDC_EUNSUPPORTED, "B * classes = %lld exceeds the head's LDS (%d)", (long long)B * classes,
+                fdc::kHeadMaxPairs);
+  if ((long long)B * F >= (1LL << 40)) return fail(FDC_EUNSUPPORTED, "B * F too large");
+  return FDC_OK;
+}
+
+fdc_status fdc_head_workspace_size(int B, int64_t F, int classes, size_t *bytes) {
+  if (fdc_status st = check_head(B, F, classes)) return st;
+  if (!bytes) return fail(FDC_EINVAL, "bytes is NULL");
+  *bytes = (size_t)fdc::head_chunks(F) * B * classes * sizeof(float);
+  return FDC_OK;
+}
+
+fdc_status fdc_head_forward(const float *y, const float *W, const float *bias, const int32_t *labels, float *logits,
+                            float *loss, int B, int64_t F, int classes, void *ws, size_t ws_bytes, hipStream_t s) {
+  size_t need = 0;
+  if (fdc_status st = fdc_head_workspace_size(B, F, classes, &need)) return st;
+  if (!y || !W || !bias || !labels || !logits || !loss) return fail(FDC_EINVAL, "NULL tensor");
+  if (!ws || ws_bytes < need) return fail(FDC_EWORKSPACE, "head workspace: need %zu bytes, got %zu", need, ws_bytes);
+  return check_hip(fdc::launch_head_forward(y, W, bias, labels, logits, loss, static_cast<float *>(ws), B, F, classes,
+                                            s),
+                   "head forward");
+}
+
+fdc_status fdc_head_backward(const float *y, const float *W, const float *logits, const int32_t *labels, float *gy,
+                             float *gW, float *gbias, int B, int64_t F, int classes, hipStream_t s) {
+  if (fdc_status st = check_head(B, F, classes)) return st;
+  if (!y || !W || !logits || !labels || !gW || !gbias) return fail(FDC_EINVAL, "NULL tensor");
+  return check_hip(fdc::launch_head_backward(y, W, logits, labels, gy, gW, gbias, B, F, classes, s), "head backward");
+}
+
+fdc_status fdc_adam_step(float *p, const float *g, float *m, float *v, int64_t n, int32_t *step_count, float lr,
+                         float beta1, float beta2, float eps, float weight_decay, hipStream_t s) {
+  if (n < 0) return fail(FDC_EINVAL, "n must be >= 0 (got %lld)", (long long)n);
+  if (n > 0 && (!p || !g || !m || !v)) return fail(FDC_EINVAL, "NULL tensor");
+  if (!step_count) return fail(FDC_EINVAL, "step_count is NULL");
+  if (!(beta1 >= 0.f && beta1 < 1.f && beta2 >= 0.f && beta2 < 1.f))
+    return fail(FDC_EINVAL, "betas must be in [0, 1) (got %g, %g)", (double)beta1, (double)beta2);
+  return check_hip(fdc::launch_adam(p, g, m, v, n, step_count, lr, beta1, beta2, eps, weight_decay, s), "adam");
+}
+
+// ---------------------------------------------------------------------------
 // kernel timing
 // ---------------------------------------------------------------------------
 fdc_status fdc_kernel_timing_enable(int max_launches, const char *only_kernel) {

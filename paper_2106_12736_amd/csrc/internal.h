@@ -156,4 +156,16 @@ hipError_t launch_fdp_gather(const float2 *X, float2 *Y, long long count, int H,
 hipError_t launch_fdp_scatter(const float2 *gY, float2 *gX, long long count, int H, int Wf, int Mh, int Mwf,
                               hipStream_t s);
 
+// FDCNN classifier head and Adam (head.hip).  At most kHeadMaxClasses classes; the
+// forward takes head_chunks(F) * B * classes floats of scratch (partial logits).
+constexpr int kHeadMaxClasses = 16;
+constexpr int kHeadMaxPairs = 15872;  // B * classes: the logits in LDS next to a 1 KB reduction buffer
+long long head_chunks(long long F);
+hipError_t launch_head_forward(const float *y, const float *W, const float *bias, const int *labels, float *logits,
+                               float *loss, float *part, int B, long long F, int classes, hipStream_t s);
+hipError_t launch_head_backward(const float *y, const float *W, const float *logits, const int *labels, float *gy,
+                                float *gW, float *gbias, int B, long long F, int classes, hipStream_t s);
+hipError_t launch_adam(float *p, const float *g, float *m, float *v, long long n, int *count, float lr, float beta1,
+                       float beta2, float eps, float wd, hipStream_t s);
+
 }  // namespace fdc

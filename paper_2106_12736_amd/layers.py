@@ -503,3 +503,95 @@ class CicChain:
             call("fdc_rfft2_backward", self.plan_in._p, _ptr(self.gspecs[0]), _ptr(input_grad), _ptr(self.ws),
                  self.ws.numel(), s)
         return self.gks
+
+
+class FdcnnClassifier:
+    """The FDCNN of section 2.5.1 (Fig. 3) as a classifier, trained as section 3.1
+    describes: the spectral chain (CicChain: one rfft2, every FDC + FDP layer on
+    spectra, one irfft2), a ReLU, one fully connected layer to `classes` outputs
+    (fdc_head_*), the mean softmax cross-entropy, and Adam with weight decay
+    (fdc_adam_step; the paper's learning rate 1e-5 and weight decay 1e-6 by default).
+
+    All parameters (each layer's kernel spectra, then W [classes][F], then bias) live in
+    one flat fp32 buffer, their gradients and the Adam moments in three more, so that
+    one launch updates them all; `kernels`, `W` and `bias` are views of it.  The step
+    count lives on the device, so a captured step advances on every replay."""
+
+    def __init__(self, batch, sizes, channels, classes=2, lr=1e-5, weight_decay=1e-6, betas=(0.9, 0.999),
+                 eps=1e-8, device="cuda"):
+        self.chain = CicChain(batch, sizes, channels, device=device)
+        self.batch, self.classes = batch, classes
+        self.lr, self.weight_decay, self.betas, self.eps = lr, weight_decay, betas, eps
+        dev = self.chain.device
+        kshapes = [(channels[i + 1], sizes[i], sizes[i] // 2 + 1) for i in range(len(sizes) - 1)]
+        self.features = channels[-1] * sizes[-1] * sizes[-1]
+        F = self.features
+        sizes_f = [2 * s[0] * s[1] * s[2] for s in kshapes] + [classes * F, classes]
+        offs = [0]
+        for n in sizes_f:
+            offs.append(offs[-1] + n)
+        self.n_params = offs[-1]
+        self.params = torch.zeros(self.n_params, dtype=torch.float32, device=dev)
+        self.grads = torch.zeros_like(self.params)
+        self.m = torch.zeros_like(self.params)
+        self.v = torch.zeros_like(self.params)
+        self.step_count = torch.zeros(1, dtype=torch.int32, device=dev)
+
+        def views(buf):
+            ks = [buf[offs[i]:offs[i + 1]].view(torch.complex64).view(s) for i, s in enumerate(kshapes)]
+            n = len(kshapes)
+            return ks, buf[offs[n]:offs[n + 1]].view(classes, F), buf[offs[n + 1]:offs[n + 2]]
+
+        self.kernels, self.W, self.bias = views(self.params)
+        gks, self.gW, self.gbias = views(self.grads)
+        self.chain.gks = gks  # the chain's backward writes dL/dK straight into the gradient buffer
+        self.logits = torch.empty((batch, classes), dtype=torch.float32, device=dev)
+        self.loss = torch.empty(1, dtype=torch.float32, device=dev)
+        self.gy = torch.empty_like(self.chain.out)
+        n = ctypes.c_size_t()
+        call("fdc_head_workspace_size", batch, F, classes, ctypes.byref(n))
+        self.head_ws = _workspace(n.value, dev)
+
+    def load(self, kernels, W, bias):
+        """Copy initial parameters in and clear the optimiser state."""
+        for dst, src in zip(self.kernels, kernels):
+            dst.copy_(src)
+        self.W.copy_(W)
+        self.bias.copy_(bias)
+        self.m.zero_()
+        self.v.zero_()
+        self.step_count.zero_()
+
+    def forward(self, x, labels):
+        """Chain, ReLU, fully connected layer and loss; returns (logits, loss)."""
+        _check(labels, torch.int32, (self.batch,), "labels")
+        y = self.chain.forward(x, self.kernels)
+        call("fdc_head_forward", _ptr(y), _ptr(self.W), _ptr(self.bias), _ptr(labels), _ptr(self.logits),
+             _ptr(self.loss), self.batch, self.features, self.classes, _ptr(self.head_ws), self.head_ws.numel(),
+             _stream())
+        return self.logits, self.loss
+
+    def backward(self, labels):
+        """Gradients of the last forward's loss into `grads` (dL/dK, dL/dW, dL/dbias)."""
+        call("fdc_head_backward", _ptr(self.chain.out), _ptr(self.W), _ptr(self.logits), _ptr(labels),
+             _ptr(self.gy), _ptr(self.gW), _ptr(self.gbias), self.batch, self.features, self.classes, _stream())
+        self.chain.backward(self.gy, self.kernels)
+
+    def optimizer_step(self):
+        b1, b2 = self.betas
+        call("fdc_adam_step", _ptr(self.params), _ptr(self.grads), _ptr(self.m), _ptr(self.v), self.n_params,
+             _ptr(self.step_count), self.lr, b1, b2, self.eps, self.weight_decay, _stream())
+
+    def train_step(self, x, labels):
+        self.forward(x, labels)
+        self.backward(labels)
+        self.optimizer_step()
+        return self.loss
+
+    def state(self):
+        """A copy of the training state (parameters, moments, step count)."""
+        return [t.clone() for t in (self.params, self.m, self.v, self.step_count)]
+
+    def set_state(self, st):
+        for dst, src in zip((self.params, self.m, self.v, self.step_count), st):
+            dst.copy_(src)

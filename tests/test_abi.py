@@ -290,3 +290,35 @@ def test_dk_ranges_queries():
     assert _lib.status("fdc_cic_stack_dk_ranges", sp, 4, ctypes.byref(r)) == FDC_EINVAL
     assert _lib.status("fdc_cic_stack_plan_destroy", sp) == FDC_OK
     assert _lib.status("fdc_cic_stack_dk_ranges", sp, 0, ctypes.byref(r)) == FDC_EINVAL  # destroyed
+
+
+def test_head_and_adam_validation():
+    """The classifier head and Adam refuse bad sizes and NULL arguments on the host,
+    before any launch; the head workspace is one float per (chunk of 1024 features,
+    image, class)."""
+    n = ctypes.c_size_t()
+    assert _lib.status("fdc_head_workspace_size", 8, 131072, 2, ctypes.byref(n)) == FDC_OK
+    assert n.value == 128 * 8 * 2 * 4
+    assert _lib.status("fdc_head_workspace_size", 3, 1025, 5, ctypes.byref(n)) == FDC_OK and n.value == 2 * 3 * 5 * 4
+    assert _lib.status("fdc_head_workspace_size", 0, 10, 2, ctypes.byref(n)) == FDC_EINVAL
+    assert _lib.status("fdc_head_workspace_size", 2, 0, 2, ctypes.byref(n)) == FDC_EINVAL
+    assert _lib.status("fdc_head_workspace_size", 2, 10, 0, ctypes.byref(n)) == FDC_EUNSUPPORTED
+    assert _lib.status("fdc_head_workspace_size", 2, 10, 17, ctypes.byref(n)) == FDC_EUNSUPPORTED
+    assert _lib.status("fdc_head_workspace_size", 4096, 10, 16, ctypes.byref(n)) == FDC_EUNSUPPORTED  # LDS
+    assert _lib.status("fdc_head_workspace_size", 2, 10, 2, None) == FDC_EINVAL
+    fake = ctypes.c_void_p(0x1000)
+    # NULL tensors and a short workspace
+    assert _lib.status("fdc_head_forward", None, fake, fake, fake, fake, fake, 2, 10, 2, fake, 16, None) == FDC_EINVAL
+    assert _lib.status("fdc_head_forward", fake, fake, fake, fake, fake, fake, 2, 10, 2, fake, 15,
+                       None) == FDC_EWORKSPACE
+    assert _lib.status("fdc_head_backward", fake, fake, fake, fake, None, None, fake, 2, 10, 2,
+                       None) == FDC_EINVAL
+    f = ctypes.c_float
+    assert _lib.status("fdc_adam_step", fake, fake, fake, fake, -1, fake, f(1e-3), f(0.9), f(0.999), f(1e-8), f(0.0),
+                       None) == FDC_EINVAL
+    assert _lib.status("fdc_adam_step", fake, fake, fake, fake, 10, None, f(1e-3), f(0.9), f(0.999), f(1e-8), f(0.0),
+                       None) == FDC_EINVAL
+    assert _lib.status("fdc_adam_step", None, fake, fake, fake, 10, fake, f(1e-3), f(0.9), f(0.999), f(1e-8), f(0.0),
+                       None) == FDC_EINVAL
+    assert _lib.status("fdc_adam_step", fake, fake, fake, fake, 10, fake, f(1e-3), f(1.0), f(0.999), f(1e-8), f(0.0),
+                       None) == FDC_EINVAL
