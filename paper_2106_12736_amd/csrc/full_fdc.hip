@@ -323,7 +323,9 @@ struct GwRun {
 constexpr int kGwStageRow = 5;
 constexpr int kGwStageElems = 2 * 4 * 32 * kGwStageRow;
 
-template <int NK>
+// EVEN: the batch takes an even number of 4-row steps (B rounded up to 4 is a multiple
+// of 8), which allows the run-by-run loop.
+template <int NK, bool EVEN>
 __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, const float2 *__restrict__ twg,
                                                  float *__restrict__ part, int B, int S, int C, int P,
                                                  int runs_per_chunk) {
@@ -385,8 +387,9 @@ __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, 
   GwRun crun;
   crun.start(r_begin, nmain, H);
   int b0 = 0;  // compute cursor
-  // one step: registers r (loaded two steps ago) into LDS buffer buf, then the products
-  auto step = [&](float4(&r)[2], int buf) {
+  // Stage the registers r (loaded two steps ago) into LDS buffer buf, then this step's
+  // products (4 batch rows of the run crun).
+  auto stage_and_multiply = [&](float4(&r)[2], int buf) __attribute__((always_inline)) {
     // (the barrier below also ends every wave's reads of this buffer two steps ago)
     {
       float2 *d = stage + buf * SE + unit * (4 * 32 * SR) + (lb * 32 + lr) * SR;
@@ -399,10 +402,6 @@ __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, 
     }
     __syncthreads();
     load_next(r);
-    if (b0 == 0) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) dr[q] = di[q] = v4f{0.f, 0.f, 0.f, 0.f};
-    }
     const float2 *ag = stage + buf * SE + (kq * 32 + (s0 - sbase) + mrow) * SR;
     const float2 *ax = stage + buf * SE + 4 * 32 * SR + (kq * 32 + (c0 - cbase) + mrow) * SR;
 #pragma unroll
@@ -415,22 +414,46 @@ __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, 
       di[q] = mfma4(-g2.x, x2.y, di[q]);
     }
     b0 += 4;
-    if (b0 >= B) {  // the run is complete: project it onto the taps
-      if (crun.g >= nmain)
-        gw_project_run<NK, true>(gw, dr, di, crun.k, crun.l0, tw);
-      else
-        gw_project_run<NK, false>(gw, dr, di, crun.k, crun.l0, tw);
-      b0 = 0;
-      crun.next(nmain, H);
-    }
   };
-  const int nsteps = max(0, r_end - r_begin) * ((B + 3) / 4);
-  int t = 0;
-  for (; t + 1 < nsteps; t += 2) {  // one path round the loop keeps the wait counts exact
-    step(ra, 0);
-    step(rb, 1);
+  auto clear_sums = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) dr[q] = di[q] = v4f{0.f, 0.f, 0.f, 0.f};
+  };
+  auto finish_run = [&]() __attribute__((always_inline)) {  // project the run onto the taps
+    if (crun.g >= nmain)
+      gw_project_run<NK, true>(gw, dr, di, crun.k, crun.l0, tw);
+    else
+      gw_project_run<NK, false>(gw, dr, di, crun.k, crun.l0, tw);
+    b0 = 0;
+    crun.next(nmain, H);
+  };
+  const int spr = (B + 3) / 4;  // steps per run
+  if constexpr (EVEN) {
+    // An even step count per run (the launcher checks): a run is whole pairs of steps,
+    // so the register sets alternate inside it, and the sums are cleared before and
+    // projected after it, with no branch on them inside the step loop.
+    for (int g = r_begin; g < r_end; ++g) {
+      clear_sums();
+      for (int t = 0; t < spr; t += 2) {  // one path round the loop keeps the wait counts exact
+        stage_and_multiply(ra, 0);
+        stage_and_multiply(rb, 1);
+      }
+      finish_run();
+    }
+  } else {
+    auto step = [&](float4(&r)[2], int buf) __attribute__((always_inline)) {
+      if (b0 == 0) clear_sums();
+      stage_and_multiply(r, buf);
+      if (b0 >= B) finish_run();
+    };
+    const int nsteps = max(0, r_end - r_begin) * spr;
+    int t = 0;
+    for (; t + 1 < nsteps; t += 2) {  // one path round the loop keeps the wait counts exact
+      step(ra, 0);
+      step(rb, 1);
+    }
+    if (t < nsteps) step(ra, 0);
   }
-  if (t < nsteps) step(ra, 0);
   // this chunk's partial sums
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -570,8 +593,12 @@ hipError_t launch_full_gw(int nk, SpecLayout G, SpecLayout X, const float2 *tw, 
     const size_t lds = ((size_t)gw_tw_elems<NK>(P) + 2 * kGwStageElems) * sizeof(float2);
     if (lds > 65536) return;  // (P <= 1024, n <= 5 stays within 60 KB)
     timing_before("full_gw", s);
-    hipLaunchKernelGGL((k_full_gw<NK>), dim3((unsigned)(tiles * chunks)), dim3(256), lds, s, G, X, tw, part, B, S, C,
-                       P, runs_per_chunk);
+    if (((B + 3) / 4) % 2 == 0)
+      hipLaunchKernelGGL((k_full_gw<NK, true>), dim3((unsigned)(tiles * chunks)), dim3(256), lds, s, G, X, tw, part, B,
+                         S, C, P, runs_per_chunk);
+    else
+      hipLaunchKernelGGL((k_full_gw<NK, false>), dim3((unsigned)(tiles * chunks)), dim3(256), lds, s, G, X, tw, part,
+                         B, S, C, P, runs_per_chunk);
     err = hipGetLastError();
     timing_after("full_gw", s);
   });
