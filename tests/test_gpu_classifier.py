@@ -98,8 +98,10 @@ def _classifier_setup(wl, classes=2, lr=1e-5):
     return d, clf, W, bias, labels
 
 
-@pytest.mark.parametrize("wl", [inputs.LAYER64, inputs.STACK256], ids=lambda w: w.name)
+@pytest.mark.parametrize("wl", inputs.CIC_WORKLOADS, ids=lambda w: w.name)
 def test_classifier_step(wl):
+    """One training step at full size on every CIC workload (cic_stack_1024 is the one
+    bench.py --classifier times): loss, logits, every gradient, and the Adam update."""
     print(f"classifier {wl.name}", flush=True)
     d, clf, W, bias, labels = _classifier_setup(wl, lr=1e-2)
     x = torch.from_numpy(d.x).cuda()
