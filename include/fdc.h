@@ -33,6 +33,17 @@
  * Sizes.     Transform lengths must be in the supported set: a power of two
  *            from 2 to 1024, or 224 (= 7 * 32, the 224 x 224 image size of the
  *            Full FDC workloads).  Other lengths return FDC_EUNSUPPORTED.
+ *            The kernels index the rows of a batch with 32-bit integers: a
+ *            plan whose images times rows (or times stored bins) reach 2^31
+ *            is refused with FDC_EUNSUPPORTED when it is created, so a call
+ *            on a valid plan never fails part-way through its launches.
+ * Plans.     Plan handles are checked against the library's registry of live
+ *            plans before they are read: a destroyed or never-created handle,
+ *            or a plan of another kind, returns FDC_EINVAL.  Destroying NULL is
+ *            a no-op; destroying a handle twice returns FDC_EINVAL.  (A new
+ *            plan may be created at the address of a destroyed one, after
+ *            which the old handle names the new plan.)  Plans are immutable
+ *            after creation and may be used from several host threads.
  * Errors.    Calls return an fdc_status.  fdc_last_error() gives a
  *            thread-local text for the last non-OK status of this thread.
  *            No C++ exception crosses this interface.
@@ -53,7 +64,8 @@ typedef struct { float re, im; } fdc_c64;
 typedef enum {
   FDC_OK = 0,
   FDC_EINVAL = 1,          /* bad argument: NULL pointer, size <= 0, odd size, S mod C != 0, M > N ... */
-  FDC_EUNSUPPORTED = 2,    /* valid but not implemented: transform length outside the supported set */
+  FDC_EUNSUPPORTED = 2,    /* valid but not implemented: transform length outside the supported set,
+                              sizes beyond the kernels' 32-bit indexing */
   FDC_EWORKSPACE = 3,      /* workspace pointer NULL or smaller than the queried size */
   FDC_EHIP = 4             /* a HIP runtime call or kernel launch failed (text in fdc_last_error) */
 } fdc_status;

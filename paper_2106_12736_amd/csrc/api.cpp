@@ -13,6 +13,7 @@
 #include <mutex>
 #include <new>
 #include <string>
+#include <unordered_set>
 #include <vector>
 
 namespace {
@@ -41,6 +42,34 @@ size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 constexpr uint32_t kFftMagic = 0xFDC0FF70u;
 constexpr uint32_t kLayerMagic = 0xFDC01A7Eu;
 constexpr uint32_t kStackMagic = 0xFDC05AC4u;
+
+// Registry of live plan handles.  A handle is dereferenced only after it is found
+// here, so a destroyed or never-created handle is refused without reading freed
+// memory; the magic word then tells the three plan types apart.
+std::mutex g_plans_mu;
+std::unordered_set<const void *> &live_plans() {
+  static std::unordered_set<const void *> s;
+  return s;
+}
+bool plan_register(const void *p) {
+  std::lock_guard<std::mutex> g(g_plans_mu);
+  try {
+    live_plans().insert(p);
+  } catch (...) {
+    return false;
+  }
+  return true;
+}
+bool plan_live(const void *p) {
+  if (p == nullptr) return false;
+  std::lock_guard<std::mutex> g(g_plans_mu);
+  return live_plans().count(p) != 0;
+}
+// Removes p; false when p was not a live plan.
+bool plan_unregister(const void *p) {
+  std::lock_guard<std::mutex> g(g_plans_mu);
+  return live_plans().erase(p) != 0;
+}
 
 }  // namespace
 
@@ -95,7 +124,7 @@ void timing_before(const char *name, hipStream_t s) {
   if (t.used >= t.max) return;
   if (!t.only.empty() && t.only != name) return;
   t.names[t.used] = name;
-  hipEventRecord(t.start[t.used], s);
+  (void)hipEventRecord(t.start[t.used], s);
 }
 void timing_after(const char *name, hipStream_t s) {
   Timing &t = timing();
@@ -103,7 +132,7 @@ void timing_after(const char *name, hipStream_t s) {
   std::lock_guard<std::mutex> g(t.mu);
   if (t.used >= t.max) return;
   if (!t.only.empty() && t.only != name) return;
-  hipEventRecord(t.stop[t.used], s);
+  (void)hipEventRecord(t.stop[t.used], s);
   ++t.used;
 }
 }  // namespace fdc
@@ -131,7 +160,7 @@ int fdc_version(void) { return 100; }
 // 2-D real FFT plans
 // ---------------------------------------------------------------------------
 static fdc_status check_fft_plan(const fdc_fft_plan *p) {
-  if (p == nullptr || p->magic != kFftMagic) return fail(FDC_EINVAL, "invalid or destroyed fft plan");
+  if (!plan_live(p) || p->magic != kFftMagic) return fail(FDC_EINVAL, "invalid or destroyed fft plan");
   return FDC_OK;
 }
 
@@ -146,16 +175,23 @@ fdc_status fdc_fft_plan_create(fdc_fft_plan **plan, int64_t count, int h, int w)
   if (!even_pos(h) || !even_pos(w)) return fail(FDC_EINVAL, "h and w must be positive and even (%d x %d)", h, w);
   if (!fdc::size_supported(h) || !fdc::size_supported(w))
     return fail(FDC_EUNSUPPORTED, "transform size %d x %d not supported", h, w);
+  if (!fdc::index_fits(count, h) || !fdc::index_fits(count, w / 2 + 1))
+    return fail(FDC_EUNSUPPORTED, "count %lld of %d x %d images exceeds the kernels' 32-bit row indexing",
+                (long long)count, h, w);
   auto *p = new (std::nothrow) fdc_fft_plan{kFftMagic, count, h, w};
   if (p == nullptr) return fail(FDC_EINVAL, "out of host memory");
+  if (!plan_register(p)) {
+    delete p;
+    return fail(FDC_EINVAL, "out of host memory");
+  }
   *plan = p;
   return FDC_OK;
 }
 
 fdc_status fdc_fft_plan_destroy(fdc_fft_plan *plan) {
   if (plan == nullptr) return FDC_OK;
-  if (plan->magic != kFftMagic) return fail(FDC_EINVAL, "invalid or destroyed fft plan");
-  plan->magic = 0;
+  if (!plan_live(plan) || plan->magic != kFftMagic) return fail(FDC_EINVAL, "invalid or destroyed fft plan");
+  plan_unregister(plan);
   delete plan;
   return FDC_OK;
 }
@@ -272,6 +308,8 @@ static fdc_status check_cic_fdp(int B, int C, int S, int N, int M) {
   if (S % C) return fail(FDC_EINVAL, "CIC needs S mod C == 0 (S=%d C=%d)", S, C);
   if (!even_pos(N) || !even_pos(M) || M > N)
     return fail(FDC_EINVAL, "N and M must be positive and even with M <= N (N=%d M=%d)", N, M);
+  if (!fdc::cic_fdp_size_supported(N))
+    return fail(FDC_EUNSUPPORTED, "spectrum of %d x %d bins exceeds the kernels' bin indexing", N, N / 2 + 1);
   return FDC_OK;
 }
 
@@ -332,8 +370,13 @@ fdc_status fdp_backward(const fdc_c64 *gY, fdc_c64 *gX, int64_t count, int H, in
 // ---------------------------------------------------------------------------
 // layer plans
 // ---------------------------------------------------------------------------
+static fdc_status check_any_layer_plan(const fdc_layer_plan *p) {
+  if (!plan_live(p) || p->magic != kLayerMagic) return fail(FDC_EINVAL, "invalid or destroyed layer plan");
+  return FDC_OK;
+}
+
 static fdc_status check_layer_plan(const fdc_layer_plan *p, int kind) {
-  if (p == nullptr || p->magic != kLayerMagic) return fail(FDC_EINVAL, "invalid or destroyed layer plan");
+  if (fdc_status st = check_any_layer_plan(p)) return st;
   if (p->kind != kind) return fail(FDC_EINVAL, "layer plan is of the other layer kind");
   return FDC_OK;
 }
@@ -354,6 +397,8 @@ fdc_status fdc_cic_layer_plan_create(fdc_layer_plan **plan, int B, int C, int S,
   if (!fdc::cic_pair_supported(N, M))
     return fail(FDC_EUNSUPPORTED, "layer size %d -> %d not supported (N in the supported set, M in {N, N/2, N/4})",
                 N, M);
+  if (!fdc::index_fits((long long)B * C, N) || !fdc::index_fits((long long)B * S, M))
+    return fail(FDC_EUNSUPPORTED, "B * C * N or B * S * M rows exceed the kernels' 32-bit row indexing");
   auto *p = new (std::nothrow) fdc_layer_plan{};
   if (p == nullptr) return fail(FDC_EINVAL, "out of host memory");
   p->magic = kLayerMagic;
@@ -369,21 +414,25 @@ fdc_status fdc_cic_layer_plan_create(fdc_layer_plan **plan, int B, int C, int S,
   p->fwd_ws = ((size_t)B * C * N * L + (size_t)B * S * M * L + (size_t)B * C * M * L) * c64;  // T, U, Xh
   p->saved = (size_t)B * C * M * L * c64;                             // pooled input spectrum
   p->bwd_ws = ((size_t)B * S * M * L + (size_t)B * C * N * L) * c64;  // Tg, V
+  if (!plan_register(p)) {
+    delete p;
+    return fail(FDC_EINVAL, "out of host memory");
+  }
   *plan = p;
   return FDC_OK;
 }
 
 fdc_status fdc_layer_plan_destroy(fdc_layer_plan *plan) {
   if (plan == nullptr) return FDC_OK;
-  if (plan->magic != kLayerMagic) return fail(FDC_EINVAL, "invalid or destroyed layer plan");
-  plan->magic = 0;
-  if (plan->tw != nullptr) hipFree(plan->tw);
+  if (fdc_status st = check_any_layer_plan(plan)) return st;
+  plan_unregister(plan);
+  if (plan->tw != nullptr) (void)hipFree(plan->tw);
   delete plan;
   return FDC_OK;
 }
 
 fdc_status fdc_layer_workspace_size(const fdc_layer_plan *p, size_t *fwd_ws, size_t *saved, size_t *bwd_ws) {
-  if (p == nullptr || p->magic != kLayerMagic) return fail(FDC_EINVAL, "invalid or destroyed layer plan");
+  if (fdc_status st = check_any_layer_plan(p)) return st;
   if (fwd_ws) *fwd_ws = p->fwd_ws;
   if (saved) *saved = p->saved;
   if (bwd_ws) *bwd_ws = p->bwd_ws;
@@ -391,7 +440,7 @@ fdc_status fdc_layer_workspace_size(const fdc_layer_plan *p, size_t *fwd_ws, siz
 }
 
 fdc_status fdc_layer_output_size(const fdc_layer_plan *p, int *out_size) {
-  if (p == nullptr || p->magic != kLayerMagic) return fail(FDC_EINVAL, "invalid or destroyed layer plan");
+  if (fdc_status st = check_any_layer_plan(p)) return st;
   if (out_size == nullptr) return fail(FDC_EINVAL, "out_size is NULL");
   *out_size = p->out;
   return FDC_OK;
@@ -490,6 +539,8 @@ fdc_status check_spatial_plan(const fdc_layer_plan *p) {
   if (!fdc::spatial_kernel_size_supported(p->ksz))
     return fail(FDC_EUNSUPPORTED, "spatial kernels need a plan with kernel_n in [1, %d] and <= M (got %d)", 8,
                 p->ksz);
+  if (!fdc::spatial_channels_supported(p->S))
+    return fail(FDC_EUNSUPPORTED, "spatial kernels: too many output channels (%d)", p->S);
   return FDC_OK;
 }
 }  // namespace
@@ -563,7 +614,7 @@ StackLayer stack_layer(const fdc_stack_plan *p, int i) {
   return StackLayer{p->N[i], p->N[i + 1], p->N[i + 1] / 2 + 1, p->C[i], p->C[i + 1]};
 }
 fdc_status check_stack_plan(const fdc_stack_plan *p) {
-  if (p == nullptr || p->magic != kStackMagic) return fail(FDC_EINVAL, "invalid or destroyed stack plan");
+  if (!plan_live(p) || p->magic != kStackMagic) return fail(FDC_EINVAL, "invalid or destroyed stack plan");
   return FDC_OK;
 }
 }  // namespace
@@ -580,6 +631,9 @@ fdc_status fdc_cic_stack_plan_create(fdc_stack_plan **plan, int B, int layers, c
       return fail(FDC_EINVAL, "layer %d: sizes %d -> %d (even, positive, non-increasing)", i, N, M);
     if (!fdc::cic_pair_supported(N, M))
       return fail(FDC_EUNSUPPORTED, "layer %d: size %d -> %d not supported", i, N, M);
+    if (!fdc::index_fits((long long)B * C, N) || !fdc::index_fits((long long)B * S, M))
+      return fail(FDC_EUNSUPPORTED, "layer %d: B * C * N or B * S * M rows exceed the kernels' 32-bit row indexing",
+                  i);
   }
   auto *p = new (std::nothrow) fdc_stack_plan{};
   if (p == nullptr) return fail(FDC_EINVAL, "out of host memory");
@@ -596,14 +650,18 @@ fdc_status fdc_cic_stack_plan_create(fdc_stack_plan **plan, int B, int layers, c
     p->ws_x = std::max(p->ws_x, x);
     p->saved.push_back(x * sizeof(fdc_c64));
   }
+  if (!plan_register(p)) {
+    delete p;
+    return fail(FDC_EINVAL, "out of host memory");
+  }
   *plan = p;
   return FDC_OK;
 }
 
 fdc_status fdc_cic_stack_plan_destroy(fdc_stack_plan *plan) {
   if (plan == nullptr) return FDC_OK;
-  if (plan->magic != kStackMagic) return fail(FDC_EINVAL, "invalid or destroyed stack plan");
-  plan->magic = 0;
+  if (fdc_status st = check_stack_plan(plan)) return st;
+  plan_unregister(plan);
   delete plan;
   return FDC_OK;
 }
@@ -771,6 +829,10 @@ fdc_status fdc_full_layer_plan_create(fdc_layer_plan **plan, int B, int Cin, int
     return fail(FDC_EUNSUPPORTED, "image size %d not supported (Full FDC needs a multiple of 8 in the FFT set)", P);
   if (!fdc::full_kernel_size_supported(kernel_n))
     return fail(FDC_EUNSUPPORTED, "Full FDC supports kernel_n 1..5 (got %d)", kernel_n);
+  if (!fdc::index_fits((long long)B * Cin, P) || !fdc::index_fits((long long)B * Cout, P) ||
+      !fdc::full_launch_fits(B, Cin, Cout, P, kernel_n))
+    return fail(FDC_EUNSUPPORTED, "B = %d, %d -> %d channels at %d^2 exceed the kernels' grid or row indexing", B,
+                Cin, Cout, P);
   auto *p = new (std::nothrow) fdc_layer_plan{};
   if (p == nullptr) return fail(FDC_EINVAL, "out of host memory");
   p->magic = kLayerMagic;
@@ -791,9 +853,14 @@ fdc_status fdc_full_layer_plan_create(fdc_layer_plan **plan, int B, int Cin, int
     return fail(FDC_EHIP, "hipMalloc of the %d-entry twiddle table failed", P);
   }
   if (hipMemcpy(p->tw, tw.data(), P * sizeof(float2), hipMemcpyHostToDevice) != hipSuccess) {
-    hipFree(p->tw);
+    (void)hipFree(p->tw);
     delete p;
     return fail(FDC_EHIP, "copy of the twiddle table failed");
+  }
+  if (!plan_register(p)) {
+    (void)hipFree(p->tw);
+    delete p;
+    return fail(FDC_EINVAL, "out of host memory");
   }
   *plan = p;
   return FDC_OK;
@@ -886,7 +953,7 @@ static fdc_status check_head(int B, int64_t F, int classes) {
   if ((long long)B * classes > fdc::kHeadMaxPairs)
     return fail(FDC_EUNSUPPORTED, "B * classes = %lld exceeds the head's LDS (%d)", (long long)B * classes,
                 fdc::kHeadMaxPairs);
-  if ((long long)B * F >= (1LL << 40)) return fail(FDC_EUNSUPPORTED, "B * F too large");
+  if ((long long)B * F >= (1LL << 40) || F >= (1LL << 38)) return fail(FDC_EUNSUPPORTED, "B * F or F too large");
   return FDC_OK;
 }
 

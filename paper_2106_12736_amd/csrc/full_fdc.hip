@@ -522,6 +522,21 @@ static bool dispatch_nk(int nk, F &&f) {
 
 bool full_kernel_size_supported(int nk) { return nk >= 1 && nk <= 5; }
 
+bool full_launch_fits(int B, int Cin, int Cout, int P, int nk) {
+  if (P % 8 != 0 || B < 1 || B > 65535 * 16) return false;
+  const long long nrun = (long long)P * (P / 2) / 4 + P / 4;
+  const long long nwg_run = (nrun + 3) / 4, nbt = (B + 15) / 16;
+  const long long lim = 1LL << 31;
+  // the two contractions
+  if (nwg_run * ((Cout + kCtOut - 1) / kCtOut) * nbt >= lim) return false;
+  if (nwg_run * ((Cin + kCtOut - 1) / kCtOut) * nbt >= lim) return false;
+  // dL/dw: tiles of 32 x 32 (s, c) times bin chunks, and the fixed-order reduction
+  const long long tiles = (long long)((Cout + 31) / 32) * ((Cin + 31) / 32);
+  if (tiles * full_gw_chunks(B, Cout, Cin, P, nk) >= lim) return false;
+  if (((long long)Cout * Cin * nk * nk + 63) / 64 >= lim) return false;
+  return true;
+}
+
 static int round_up(int v, int m) { return (v + m - 1) / m * m; }
 static int tap_pad_rt(int nk) { return (nk * nk + 3) & ~3; }
 

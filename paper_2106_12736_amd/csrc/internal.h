@@ -25,6 +25,14 @@ struct ImgView {
 
 bool size_supported(int n);
 
+// The kernels index rows (and columns) of a batch of images with 32-bit integers.
+// The C ABI checks these limits on the host, at plan creation or at the top of a
+// call without a plan, so that a call that fails enqueues nothing.
+// index_fits(planes, n): planes * n < 2^31.
+inline bool index_fits(long long planes, long long n) {
+  return planes > 0 && n > 0 && planes <= ((1LL << 31) - 1) / n;
+}
+
 // Storage of a half spectrum of `planes` images with `rows` rows and L stored bins
 // per row.  Bins l < L-1 of row r of plane p are at main[p*ps + r*rs + l]; the last
 // bin, l = L-1, is at side[p*sps + r*srs].
@@ -122,6 +130,9 @@ hipError_t launch_col_bwd_dk_dx(int n, int m, const float2 *Tg, const float2 *Xh
 bool full_kernel_size_supported(int nk);
 size_t full_weight_floats(int KD, int ND, int nk);
 int full_gw_chunks(int B, int S, int C, int P, int nk);
+// Whether every Full FDC launch of a layer (both contractions, dL/dw and its reduction)
+// fits its grid limits.
+bool full_launch_fits(int B, int Cin, int Cout, int P, int nk);
 hipError_t launch_full_weights(const float *w, float *wt, bool gx, int S, int C, int nk, hipStream_t s);
 hipError_t launch_full_contract(bool gx, int nk, SpecLayout in, const float *wt, const float2 *tw, SpecLayout out,
                                 int B, int KD, int ND, int P, hipStream_t s);
@@ -139,12 +150,16 @@ hipError_t launch_cic_bwd_gk(const float2 *gY, const float2 *X, float2 *gK, int 
 // layer (into K [S][n_img][n_img/2+1]), and dL/dw from dK (part: S * cic_wgrad_blocks(M)
 // * n * n floats of scratch).
 bool spatial_kernel_size_supported(int n);
+// Output channels the spatial-kernel weight-gradient launch accepts.
+bool spatial_channels_supported(int S);
 int cic_wgrad_blocks(int M);
 hipError_t launch_cic_kspec(int n_img, const float *w, float2 *K, int S, int n, int M, hipStream_t s);
 hipError_t launch_cic_wgrad(int n_img, const float2 *gK, float *part, float *gw, int S, int n, int M,
                             hipStream_t s);
 // FDC layer of the FDCNN on spectra followed by FDP (only the kept bins are formed), and
 // its backward (gX and gK with exact zeros at the dropped bins).
+// Largest spectrum the spectral FDC + FDP kernels index: N (N/2 + 1) bins below 2^24.
+bool cic_fdp_size_supported(int N);
 hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, int N, int M,
                               hipStream_t s);
 hipError_t launch_cic_fdp_bwd_gx(const float2 *gY, const float2 *K, float2 *gX, int B, int C, int S, int N, int M,

@@ -1600,6 +1600,10 @@ __global__ void k_cic_wgrad_reduce(const float *__restrict__ part, float *__rest
 
 bool spatial_kernel_size_supported(int n) { return n >= 1 && n <= kSpatialMaxN; }
 
+bool spatial_channels_supported(int S) { return S >= 1 && S <= 65535; }
+
+bool cic_fdp_size_supported(int N) { return (long long)N * (N / 2 + 1) < (1 << 24); }
+
 int cic_wgrad_blocks(int M) { return M >= 256 ? 32 : (M >= 64 ? 16 : 4); }
 
 hipError_t launch_cic_kspec(int n_img, const float *w, float2 *K, int S, int n, int M, hipStream_t s) {

@@ -6,6 +6,7 @@ computation runs in libfdc's HIP kernels.  Tensors must be contiguous CUDA
 """
 
 import ctypes
+import weakref
 
 import torch
 
@@ -38,6 +39,18 @@ def _workspace(nbytes, device):
     return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
 
 
+def _own(obj, destroy):
+    """Destroy obj's plan handle `obj._p` with the C function `destroy` when obj is
+    collected or at interpreter exit; the function object is bound now, so the call
+    does not depend on module state during shutdown."""
+    weakref.finalize(obj, getattr(_lib.lib(), destroy), ctypes.c_void_p(obj._p.value))
+
+
+def _check_saved(saved, nbytes, name="saved"):
+    """A saved-spectrum buffer: contiguous complex64 of exactly nbytes bytes."""
+    _check(saved, torch.complex64, (nbytes // 8,), name)
+
+
 class FftPlan:
     """Batched 2-D real FFT of `count` h x w images (fdc_rfft2 and friends)."""
 
@@ -45,13 +58,10 @@ class FftPlan:
         self.count, self.h, self.w = count, h, w
         self._p = ctypes.c_void_p()
         call("fdc_fft_plan_create", ctypes.byref(self._p), count, h, w)
+        _own(self, "fdc_fft_plan_destroy")
         n = ctypes.c_size_t()
         call("fdc_fft_workspace_size", self._p, ctypes.byref(n))
         self.ws_bytes = n.value
-
-    def __del__(self):
-        if getattr(self, "_p", None) and _lib._lib is not None:
-            _lib.lib().fdc_fft_plan_destroy(self._p)
 
     def _spec_shape(self, lead):
         return lead + (self.h, self.w // 2 + 1)
@@ -131,10 +141,6 @@ class _LayerPlan:
         self.fwd_ws_bytes, self.saved_bytes, self.bwd_ws_bytes = f.value, s.value, b.value
         self.out = o.value
 
-    def __del__(self):
-        if getattr(self, "_p", None) and _lib._lib is not None:
-            _lib.lib().fdc_layer_plan_destroy(self._p)
-
 
 class CicLayer(_LayerPlan):
     """Fused CIC + FDP layer: x [B][C][N][N] -> y [B][S][O][O] (fdc_cic_layer_*).
@@ -147,6 +153,7 @@ class CicLayer(_LayerPlan):
         self.B, self.C, self.S, self.N, self.M = B, C, S, N, M
         self._p = ctypes.c_void_p()
         call("fdc_cic_layer_plan_create", ctypes.byref(self._p), B, C, S, N, M, _ARTIFACTS[artifact], kernel_n)
+        _own(self, "fdc_layer_plan_destroy")
         self._sizes()
         self.device = torch.device(device)
         self.fwd_ws = _workspace(self.fwd_ws_bytes, self.device)
@@ -178,6 +185,9 @@ class CicLayer(_LayerPlan):
         _check(x, torch.float32, (self.B, self.C, self.N, self.N), "x")
         _check(K, torch.complex64, (self.S, self.N, self.N // 2 + 1), "K")
         y = self.new_output() if y is None else y
+        _check(y, torch.float32, (self.B, self.S, self.out, self.out), "y")
+        if saved is not None:
+            _check_saved(saved, self.saved_bytes)
         call("fdc_cic_layer_forward", self._p, _ptr(x), _ptr(K), _ptr(y), _ptr(saved), _ptr(self.fwd_ws),
              self.fwd_ws.numel(), _stream())
         return y
@@ -188,6 +198,12 @@ class CicLayer(_LayerPlan):
             gx = torch.empty((self.B, self.C, self.N, self.N), dtype=torch.float32, device=self.device)
         if need_gk and gK is None:
             gK = torch.empty((self.S, self.N, self.N // 2 + 1), dtype=torch.complex64, device=self.device)
+        if need_gx:
+            _check(gx, torch.float32, (self.B, self.C, self.N, self.N), "gx")
+            _check(K, torch.complex64, (self.S, self.N, self.N // 2 + 1), "K")
+        if need_gk:
+            _check(gK, torch.complex64, (self.S, self.N, self.N // 2 + 1), "gK")
+            _check_saved(saved, self.saved_bytes)
         call("fdc_cic_layer_backward", self._p, _ptr(gy), _ptr(saved), _ptr(K), _ptr(gx if need_gx else None),
              _ptr(gK if need_gk else None), _ptr(self.bwd_ws), self.bwd_ws.numel(), _stream())
         return (gx if need_gx else None), (gK if need_gk else None)
@@ -211,6 +227,7 @@ class FullLayer(_LayerPlan):
         self.B, self.Cin, self.Cout, self.P, self.n = B, Cin, Cout, P, kernel_n
         self._p = ctypes.c_void_p()
         call("fdc_full_layer_plan_create", ctypes.byref(self._p), B, Cin, Cout, P, kernel_n, _ARTIFACTS[artifact])
+        _own(self, "fdc_layer_plan_destroy")
         self._sizes()
         self.device = torch.device(device)
         self.fwd_ws = _workspace(self.fwd_ws_bytes, self.device)
@@ -250,6 +267,12 @@ class FullLayer(_LayerPlan):
             gx = torch.empty((self.B, self.Cin, self.P, self.P), dtype=torch.float32, device=self.device)
         if need_gw and gw is None:
             gw = torch.empty((self.Cout, self.Cin, self.n, self.n), dtype=torch.float32, device=self.device)
+        if need_gx:
+            _check(gx, torch.float32, (self.B, self.Cin, self.P, self.P), "gx")
+            _check(w, torch.float32, (self.Cout, self.Cin, self.n, self.n), "w")
+        if need_gw:
+            _check(gw, torch.float32, (self.Cout, self.Cin, self.n, self.n), "gw")
+            _check_saved(saved, self.saved_bytes)
         call("fdc_full_backward", self._p, _ptr(gy), _ptr(saved), _ptr(w), _ptr(gx if need_gx else None),
              _ptr(gw if need_gw else None), _ptr(self.bwd_ws), self.bwd_ws.numel(), _stream())
         return (gx if need_gx else None), (gw if need_gw else None)
@@ -271,6 +294,9 @@ class CicSpatialLayer(CicLayer):
         _check(x, torch.float32, (self.B, self.C, self.N, self.N), "x")
         _check(w, torch.float32, (self.S, self.n, self.n), "w")
         y = self.new_output() if y is None else y
+        _check(y, torch.float32, (self.B, self.S, self.out, self.out), "y")
+        if saved is not None:
+            _check_saved(saved, self.saved_bytes)
         call("fdc_cic_spatial_layer_forward", self._p, _ptr(x), _ptr(w), _ptr(y), _ptr(saved), _ptr(self.fwd_ws),
              self.fwd_ws.numel(), _stream())
         return y
@@ -281,6 +307,12 @@ class CicSpatialLayer(CicLayer):
             gx = torch.empty((self.B, self.C, self.N, self.N), dtype=torch.float32, device=self.device)
         if need_gw and gw is None:
             gw = torch.empty((self.S, self.n, self.n), dtype=torch.float32, device=self.device)
+        if need_gx:
+            _check(gx, torch.float32, (self.B, self.C, self.N, self.N), "gx")
+            _check(w, torch.float32, (self.S, self.n, self.n), "w")
+        if need_gw:
+            _check(gw, torch.float32, (self.S, self.n, self.n), "gw")
+            _check_saved(saved, self.saved_bytes)
         call("fdc_cic_spatial_layer_backward", self._p, _ptr(gy), _ptr(saved), _ptr(w),
              _ptr(gx if need_gx else None), _ptr(gw if need_gw else None), _ptr(self.bwd_ws), self.bwd_ws.numel(),
              _stream())
@@ -380,6 +412,7 @@ class CicStackFused:
         self._chans = (ctypes.c_int * len(channels))(*channels)
         self._p = ctypes.c_void_p()
         call("fdc_cic_stack_plan_create", ctypes.byref(self._p), batch, self.layers, self._sizes, self._chans)
+        _own(self, "fdc_cic_stack_plan_destroy")
         f, b = ctypes.c_size_t(), ctypes.c_size_t()
         call("fdc_cic_stack_workspace_size", self._p, ctypes.byref(f), ctypes.byref(b))
         self.fwd_ws = _workspace(f.value, self.device)
@@ -394,10 +427,6 @@ class CicStackFused:
                                 device=self.device) for i in range(self.layers)]
         self._saved_arr = _ptr_array(self.saved)
         self._gk_arr = _ptr_array(self.gks)
-
-    def __del__(self):
-        if getattr(self, "_p", None) and _lib._lib is not None:
-            _lib.lib().fdc_cic_stack_plan_destroy(self._p)
 
     def dk_ranges(self):
         """Image ranges each layer's dK step sums separately (fdc_cic_stack_dk_ranges)."""

@@ -179,13 +179,61 @@ def test_timing_api_arguments():
 
 
 def test_destroyed_plan_is_refused():
+    """Handles are looked up in the library's registry of live plans before they are
+    read: a destroyed handle, a never-created one and a plan of another type are all
+    refused with FDC_EINVAL, without touching freed memory."""
     st, p = _fft_plan(1, 8, 8)
     assert st == FDC_OK
-    # destroy through a copy of the handle, then use a fresh invalid handle object
+    n = ctypes.c_size_t()
     bogus = ctypes.create_string_buffer(64)
-    assert _lib.status("fdc_fft_workspace_size", ctypes.cast(bogus, ctypes.c_void_p),
-                       ctypes.byref(ctypes.c_size_t())) == FDC_EINVAL
+    assert _lib.status("fdc_fft_workspace_size", ctypes.cast(bogus, ctypes.c_void_p), ctypes.byref(n)) == FDC_EINVAL
+    # an fft plan is not a layer or stack plan
+    assert _lib.status("fdc_layer_workspace_size", p, None, None, None) == FDC_EINVAL
+    assert _lib.status("fdc_cic_stack_workspace_size", p, None, None) == FDC_EINVAL
     assert _lib.status("fdc_fft_plan_destroy", p) == FDC_OK
+    assert _lib.status("fdc_fft_workspace_size", p, ctypes.byref(n)) == FDC_EINVAL
+    assert _lib.status("fdc_rfft2", p, ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1000), None, 0, None) == FDC_EINVAL
+    assert _lib.status("fdc_fft_plan_destroy", p) == FDC_EINVAL  # a second destroy
+    assert _lib.status("fdc_fft_plan_destroy", None) == FDC_OK
+
+
+def test_destroyed_layer_and_stack_plans_are_refused():
+    lp = ctypes.c_void_p()
+    assert _lib.status("fdc_cic_layer_plan_create", ctypes.byref(lp), 2, 1, 4, 64, 32, 0, 1) == FDC_OK
+    assert _lib.status("fdc_layer_plan_destroy", lp) == FDC_OK
+    d = ctypes.c_void_p(0x1000)
+    assert _lib.status("fdc_layer_output_size", lp, ctypes.byref(ctypes.c_int())) == FDC_EINVAL
+    assert _lib.status("fdc_cic_layer_forward", lp, d, d, d, None, d, 1 << 30, None) == FDC_EINVAL
+    assert _lib.status("fdc_layer_plan_destroy", lp) == FDC_EINVAL
+    st, sp = _stack(2, (64, 32), (1, 4))
+    assert st == FDC_OK
+    assert _lib.status("fdc_layer_workspace_size", sp, None, None, None) == FDC_EINVAL  # not a layer plan
+    assert _lib.status("fdc_cic_stack_plan_destroy", sp) == FDC_OK
+    assert _lib.status("fdc_cic_stack_plan_destroy", sp) == FDC_EINVAL
+
+
+def test_oversize_counts_fail_before_any_launch():
+    """Sizes beyond the kernels' 32-bit row and grid indexing are refused with
+    FDC_EUNSUPPORTED when the plan is made (or at the top of a call without a plan),
+    so no later call can enqueue part of its work and then fail.  On a machine
+    without a GPU any launch would return FDC_EHIP instead, so these statuses also
+    show that nothing was launched."""
+    p = ctypes.c_void_p()
+    assert _lib.status("fdc_fft_plan_create", ctypes.byref(p), 1 << 30, 2, 2) == FDC_EUNSUPPORTED
+    assert _lib.status("fdc_fft_plan_create", ctypes.byref(p), (1 << 31) // 1024, 1024, 16) == FDC_EUNSUPPORTED
+    st, q = _fft_plan((1 << 30) - 1, 2, 2)  # the largest count of 2 x 2 images
+    assert st == FDC_OK
+    assert _lib.status("fdc_fft_plan_destroy", q) == FDC_OK
+    assert _lib.status("fdc_cic_layer_plan_create", ctypes.byref(p), 1 << 21, 1, 1, 1024, 512, 0, 1) == FDC_EUNSUPPORTED
+    assert _lib.status("fdc_cic_layer_plan_create", ctypes.byref(p), 1 << 16, 1, 1024, 64, 32, 0, 1) == FDC_EUNSUPPORTED
+    st, _ = _stack(1 << 21, (1024, 512), (1, 1))
+    assert st == FDC_EUNSUPPORTED
+    assert _lib.status("fdc_full_layer_plan_create", ctypes.byref(p), 16, 1 << 20, 64, 512, 3, 1) == FDC_EUNSUPPORTED
+    d = ctypes.c_void_p(0x1000)
+    assert _lib.status("fdc_cic_fdp_forward", d, d, d, 1, 1, 1, 8192, 4096, None) == FDC_EUNSUPPORTED
+    assert _lib.status("fdc_cic_fdp_backward", d, d, d, d, d, 1, 1, 1, 8192, 4096, None) == FDC_EUNSUPPORTED
+    n = ctypes.c_size_t()
+    assert _lib.status("fdc_head_workspace_size", 1, 1 << 38, 2, ctypes.byref(n)) == FDC_EUNSUPPORTED
 
 
 def test_full_plane_strides_match_header():

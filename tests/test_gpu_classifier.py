@@ -64,6 +64,29 @@ def test_head_forward_backward(B, F, classes):
     assert np.all(to_np(gy)[y <= 0] == 0), "the ReLU blocks the gradient where y <= 0"
 
 
+@pytest.mark.parametrize("B,F,classes", [(3, 7, 5), (5, 9000, 16), (16, 4096, 16), (8, 131072, 2)])
+def test_head_backward_from_oracle_logits(B, F, classes):
+    """The head backward on its own: the GPU takes the oracle's logits (rounded to fp32),
+    so its gradients are checked against the oracle independently of the GPU forward."""
+    print(f"head backward B={B} F={F} classes={classes}", flush=True)
+    rng = _rng("head-bwd", B, F, classes)
+    y = rng.standard_normal((B, F)).astype(np.float32)
+    W = (rng.standard_normal((classes, F)) / np.sqrt(F)).astype(np.float32)
+    bias = rng.standard_normal(classes).astype(np.float32)
+    labels = rng.integers(0, classes, B).astype(np.int32)
+    ref_logits, _ = classifier.head_forward(y.astype(np.float64), W, bias, labels)
+    logits32 = ref_logits.astype(np.float32)
+    yd, Wd, ld, lg = (torch.from_numpy(a).cuda() for a in (y, W, labels, logits32))
+    gy, gW = torch.empty_like(yd), torch.empty_like(Wd)
+    gb = torch.empty(classes, dtype=torch.float32, device="cuda")
+    call("fdc_head_backward", _p(yd), _p(Wd), _p(lg), _p(ld), _p(gy), _p(gW), _p(gb), B, F, classes, _stream())
+    torch.cuda.synchronize()
+    rgy, rgW, rgb = classifier.head_backward(y.astype(np.float64), W, logits32.astype(np.float64), labels)
+    assert_parity(to_np(gy), rgy, "gy")
+    assert_parity(to_np(gW), rgW, "gW")
+    assert_parity(to_np(gb), rgb, "gbias")
+
+
 @pytest.mark.parametrize("n", [1, 1000, 262147, (1 << 24) + 5])
 def test_adam_step(n):
     print(f"adam n={n}", flush=True)
