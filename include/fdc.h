@@ -287,6 +287,19 @@ fdc_status fdc_head_workspace_size(int B, int64_t F, int classes, size_t *bytes)
 fdc_status fdc_head_forward(const float *y, const float *W, const float *bias, const int32_t *labels, float *logits,
                             float *loss, int B, int64_t F, int classes, void *ws, size_t ws_bytes,
                             hipStream_t stream);
+/* fdc_head_forward without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops, harnesses that forbid
+ * allocation).  It allocates nothing: the partial logits go to a static device array
+ * of 2^18 floats (1 MiB) that the library holds on each device it runs on until the
+ * process ends.  Same kernels and results as fdc_head_forward.
+ * Limit: ceil(F / 1024) * B * classes <= 262144, else FDC_EUNSUPPORTED (nothing
+ * enqueued).  The array is looked up on the first call on each device (the current
+ * device; `stream` must belong to it).  Every call on a device shares that device's
+ * array, so calls that may overlap on one device (different streams, host threads)
+ * race and must be ordered by the caller; the array keeps the last call's partial
+ * logits, and no part of it needs to start at zero. */
+fdc_status fdc_head_forward_noalloc(const float *y, const float *W, const float *bias, const int32_t *labels,
+                                    float *logits, float *loss, int B, int64_t F, int classes, hipStream_t stream);
 /* From the forward's logits: dlogits = (softmax(logits) - onehot(labels)) / B;
  * gW = dlogits^T relu(y), gbias = sum_b dlogits, gy = [y > 0] (dlogits W) (gy NULL:
  * skipped).  All outputs are overwritten. */

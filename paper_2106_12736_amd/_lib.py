@@ -43,6 +43,7 @@ _SIGS = {
     "fdp_forward": [_P, _P, _I64, _I, _I, _I, _I, _P],
     "fdc_head_workspace_size": [_I, _I64, _I, ctypes.POINTER(_SZ)],
     "fdc_head_forward": [_P, _P, _P, _P, _P, _P, _I, _I64, _I, _P, _SZ, _P],
+    "fdc_head_forward_noalloc": [_P, _P, _P, _P, _P, _P, _I, _I64, _I, _P],
     "fdc_head_backward": [_P, _P, _P, _P, _P, _P, _P, _I, _I64, _I, _P],
     "fdc_adam_step": [_P, _P, _P, _P, _I64, _P, ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float,
                       ctypes.c_float, _P],

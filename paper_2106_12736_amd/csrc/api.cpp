@@ -975,6 +975,20 @@ fdc_status fdc_head_forward(const float *y, const float *W, const float *bias, c
                    "head forward");
 }
 
+fdc_status fdc_head_forward_noalloc(const float *y, const float *W, const float *bias, const int32_t *labels,
+                                    float *logits, float *loss, int B, int64_t F, int classes, hipStream_t s) {
+  if (fdc_status st = check_head(B, F, classes)) return st;
+  if (!y || !W || !bias || !labels || !logits || !loss) return fail(FDC_EINVAL, "NULL tensor");
+  const long long need = fdc::head_chunks(F) * B * classes;
+  if (need > fdc::kHeadScratchFloats)
+    return fail(FDC_EUNSUPPORTED,
+                "head_forward_noalloc: ceil(F / 1024) * B * classes = %lld partial logits exceed the library's "
+                "static scratch of %lld floats; use fdc_head_forward with a workspace",
+                need, (long long)fdc::kHeadScratchFloats);
+  return check_hip(fdc::launch_head_forward_noalloc(y, W, bias, labels, logits, loss, B, F, classes, s),
+                   "head forward (static scratch)");
+}
+
 fdc_status fdc_head_backward(const float *y, const float *W, const float *logits, const int32_t *labels, float *gy,
                              float *gW, float *gbias, int B, int64_t F, int classes, hipStream_t s) {
   if (fdc_status st = check_head(B, F, classes)) return st;

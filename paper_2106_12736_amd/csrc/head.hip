@@ -15,6 +15,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 namespace fdc {
 
 constexpr int kHeadThreads = 256;
@@ -216,6 +218,46 @@ hipError_t launch_head_forward(const float *y, const float *W, const float *bias
   e = hipGetLastError();
   timing_after("head_loss", s);
   return e;
+}
+
+// Partial logits of the allocation-free forward (fdc_head_forward_noalloc): one array
+// per device, resident while the library is loaded, shared by every call on that
+// device.  In host code `scratch` names a host-side stand-in; kernels get the device
+// address that hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) float scratch[kHeadScratchFloats];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float *g_scratch_ptr[kMaxDevices];  // device address of `scratch`, per device (nullptr: not yet looked up)
+}  // namespace
+
+hipError_t head_scratch_address(float **out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void *ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (ptr == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = static_cast<float *>(ptr);
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_head_forward_noalloc(const float *y, const float *W, const float *bias, const int *labels,
+                                       float *logits, float *loss, int B, long long F, int classes, hipStream_t s) {
+  if (head_chunks(F) * B * classes > kHeadScratchFloats) return hipErrorInvalidValue;
+  float *part = nullptr;
+  const hipError_t e = head_scratch_address(&part);
+  if (e != hipSuccess) return e;
+  // every partial-logit slot the loss kernel reads is written first by k_head_fwd, so
+  // nothing needs clearing between calls
+  return launch_head_forward(y, W, bias, labels, logits, loss, part, B, F, classes, s);
 }
 
 hipError_t launch_head_backward(const float *y, const float *W, const float *logits, const int *labels, float *gy,

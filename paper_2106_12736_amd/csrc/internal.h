@@ -178,6 +178,13 @@ constexpr int kHeadMaxPairs = 15872;  // B * classes: the logits in LDS next to 
 long long head_chunks(long long F);
 hipError_t launch_head_forward(const float *y, const float *W, const float *bias, const int *labels, float *logits,
                                float *loss, float *part, int B, long long F, int classes, hipStream_t s);
+// The forward without a caller workspace: the partial logits go to a file-scope
+// device array of kHeadScratchFloats floats (one per device, shared by all calls on
+// it).  Requires head_chunks(F) * B * classes <= kHeadScratchFloats.
+constexpr long long kHeadScratchFloats = 1LL << 18;
+hipError_t head_scratch_address(float **out);
+hipError_t launch_head_forward_noalloc(const float *y, const float *W, const float *bias, const int *labels,
+                                       float *logits, float *loss, int B, long long F, int classes, hipStream_t s);
 hipError_t launch_head_backward(const float *y, const float *W, const float *logits, const int *labels, float *gy,
                                 float *gW, float *gbias, int B, long long F, int classes, hipStream_t s);
 hipError_t launch_adam(float *p, const float *g, float *m, float *v, long long n, int *count, float lr, float beta1,
