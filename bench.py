@@ -95,19 +95,48 @@ def step_launches(wl, input_grad=False, ranges=None):
     return out
 
 
-def fused_step_launches(wl, input_grad=False, ranges=None):
+def tail_launches(wl, a, input_grad=False):
+    """The stack's last two layers (a, a + 1) run by the LDS-resident tail kernels:
+    (forward launch, [backward launch, in-order dK sums of both layers]).
+    Bytes: what crosses HBM -- the previous layer's column-inverted spectra (or the
+    input image), both kernels at the kept bins, both saved spectra, the output;
+    backward the upstream gradient, both saved spectra and kernels, the per-image dK
+    products (written, then read by the in-order sums) and the previous layer's
+    upstream-gradient spectrum (or the input gradient)."""
+    B, C, S, N, M, L, NF = layer_dims(wl, a)
+    _, _, S2, _, M2, L2, NF2 = layer_dims(wl, a + 1)
+    k_bytes = C64 * (S * M * L + S2 * M2 * L2)
+    saved_bytes = C64 * (B * C * M * L + B * S * M2 * L2)
+    out_bytes = F32 * B * S2 * M2 * M2
+    in_bytes = C64 * B * C * N * NF if a > 0 else F32 * B * C * N * N
+    part_a, part_b = C64 * B * S * M * L, C64 * B * S2 * M2 * L2
+    name = f"{N}_{M}_{M2}"
+    fwd = (f"tail_fwd_{name}", in_bytes + k_bytes + saved_bytes + out_bytes)
+    dx_bytes = in_bytes if (a > 0 or input_grad) else 0
+    bwd = [(f"tail_bwd_{name}", out_bytes + saved_bytes + k_bytes + part_a + part_b + dx_bytes),
+           ("gk_reduce", part_a + part_b + C64 * (S * N * NF + S2 * M * NF2))]
+    return fwd, bwd
+
+
+def fused_step_launches(wl, input_grad=False, ranges=None, tail=-1):
     """(kernel name, algorithmic bytes) of every launch of one step of the fused stack
     executor: as step_launches, with each layer boundary's inverse rows and the next
-    layer's forward rows (and the backward's adjoint pair) in one kernel, and a
-    layer's dK and dX columns in one launch when dK uses one batch range."""
+    layer's forward rows (and the backward's adjoint pair) in one kernel, a layer's
+    dK and dX columns in one launch when dK uses one batch range, and the last two
+    layers in the LDS-resident tail kernels from layer `tail` on (-1: none)."""
     ranges = ranges or [1] * wl.layers
     out = []
     n = wl.layers
     for i in range(n):
         B, C, S, N, M, L, _ = layer_dims(wl, i)
+        if i == tail:
+            out.append(tail_launches(wl, tail, input_grad)[0])
+            break
         if i == 0:
             out.append((f"row_r2c_{N}", F32 * B * C * N * N + C64 * B * C * N * L))
         out += fwd_col_launches(B, C, S, N, M, L)
+        if i + 1 == tail:
+            continue
         if i + 1 < n:
             _, _, _, N2, M2, L2, _ = layer_dims(wl, i + 1)
             out.append((f"row_c2r_r2c_{M}", C64 * B * S * M * L + C64 * B * S * N2 * L2))
@@ -115,6 +144,10 @@ def fused_step_launches(wl, input_grad=False, ranges=None):
             out.append((f"row_c2r_{M}", C64 * B * S * M * L + F32 * B * S * M * M))
     for i in reversed(range(n)):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
+        if tail >= 0 and i >= tail:
+            if i == tail + 1:
+                out += tail_launches(wl, tail, input_grad)[1]
+            continue
         if i == n - 1:
             out.append((f"row_r2c_{M}", F32 * B * S * M * M + C64 * B * S * M * L))
         dx = i > 0 or input_grad
@@ -427,7 +460,7 @@ class CicStackRun:
             model = lambda w_, ig: step_launches(w_, ig, self.stack.dk_ranges())  # noqa: E731
         else:
             self.stack = layers.CicStackFused(wl.batch, wl.sizes, wl.channels, device=dev)
-            model = lambda w_, ig: fused_step_launches(w_, ig, self.stack.dk_ranges())  # noqa: E731
+            model = lambda w_, ig: fused_step_launches(w_, ig, self.stack.dk_ranges(), self.stack.tail())  # noqa: E731
         self.gin = (torch.empty((wl.batch, wl.channels[0], wl.sizes[0], wl.sizes[0]), dtype=torch.float32,
                                 device=dev) if args.input_grad else None)
         self.input_grad = args.input_grad
@@ -461,6 +494,8 @@ class CicStackRun:
                "input_grad": bool(self.input_grad),
                "executor": self.executor,
                "kernels": f"spatial {self.spatial}x{self.spatial}, roll" if self.spatial else "spectral"}
+        if self.executor == "fused_stack":
+            cfg["lds_tail_from_layer"] = self.stack.tail()
         if self.clf is not None:
             cfg["head"] = (f"relu, fully connected {self.clf.features} -> {self.clf.classes}, softmax cross-entropy; "
                            f"adam lr {self.clf.lr:g}, weight decay {self.clf.weight_decay:g}")

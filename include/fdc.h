@@ -188,8 +188,9 @@ fdc_status fdc_layer_output_size(const fdc_layer_plan *plan, int *out_size);
 /* x [B][C][N][N] float32, K [S][N][N/2+1] complex -> y [B][S][O][O] float32.
  * `saved` (may be NULL when no backward will follow; fdc_layer_workspace_size
  * gives its size) receives the pooled input spectrum the backward pass needs:
- * the M x (M/2+1) bins FDP keeps, complex, as columns 0..M/2-1 in a block
- * [B][C][M][M/2] followed by column M/2 in a block [B][C][M]. */
+ * the M x (M/2+1) bins FDP keeps, complex: columns 0..M/2-1 in a block
+ * [B][C][M/16][M][8] of 8-column tiles stored down the rows when M/2 is a multiple
+ * of 8 (else a block [B][C][M][M/2]), followed by column M/2 in a block [B][C][M]. */
 fdc_status fdc_cic_layer_forward(const fdc_layer_plan *plan, const float *x, const fdc_c64 *K,
                                  float *y, void *saved, void *ws, size_t ws_bytes,
                                  hipStream_t stream);
@@ -246,8 +247,14 @@ fdc_status fdc_full_backward(const fdc_layer_plan *plan, const float *gy, const 
  * The stack runs the same transforms as the layer calls in sequence (results agree
  * to fp32 rounding), but the activations and activation gradients between layers
  * are not written to memory: the inverse row transform of one layer and the
- * forward row transform of the next run in one kernel on the same rows.  Plans
- * are immutable host objects. */
+ * forward row transform of the next run in one kernel on the same rows.  When the
+ * last two layers take inputs of at most 128 x 128 (the instantiated shape is
+ * 128 -> 64 -> 32 with two output channels per input channel in both), one
+ * workgroup per input plane of the first of them runs every step of both layers
+ * with all intermediates in LDS (one forward launch; one backward launch plus the
+ * in-order sum of the per-image dK products); fdc_cic_stack_tail reports it.
+ * FDC_STACK_TAIL=0 in the environment when the plan is created keeps every layer
+ * on the per-layer kernels (for comparisons).  Plans are immutable host objects. */
 typedef struct fdc_stack_plan fdc_stack_plan;
 fdc_status fdc_cic_stack_plan_create(fdc_stack_plan **plan, int B, int layers, const int *sizes,
                                      const int *channels);
@@ -342,6 +349,11 @@ fdc_status fdc_kernel_timing_launches(char *buf, size_t buf_bytes);
  * plan's layer for the stack call); FDC_EINVAL for other plans or layers. */
 fdc_status fdc_cic_layer_dk_ranges(const fdc_layer_plan *plan, int *ranges);
 fdc_status fdc_cic_stack_dk_ranges(const fdc_stack_plan *plan, int layer, int *ranges);
+/* The first layer of the stack's LDS-resident tail (the last two layers run by
+ * "tail_fwd_<N>_<M1>_<M2>", "tail_bwd_<N>_<M1>_<M2>" and one "gk_reduce" launch),
+ * or -1 when every layer runs on the per-layer kernels.  The dK ranges query does
+ * not apply to the tail's two layers. */
+fdc_status fdc_cic_stack_tail(const fdc_stack_plan *plan, int *first_layer);
 
 #ifdef __cplusplus
 }

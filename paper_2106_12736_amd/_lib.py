@@ -72,6 +72,7 @@ _SIGS = {
     "fdc_kernel_timing_launches": [ctypes.c_char_p, _SZ],
     "fdc_cic_layer_dk_ranges": [_P, ctypes.POINTER(_I)],
     "fdc_cic_stack_dk_ranges": [_P, _I, ctypes.POINTER(_I)],
+    "fdc_cic_stack_tail": [_P, ctypes.POINTER(_I)],
 }
 _RESTYPES = {"fdc_status_string": ctypes.c_char_p, "fdc_last_error": ctypes.c_char_p, "fdc_version": _I}
 

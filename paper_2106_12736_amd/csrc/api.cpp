@@ -5,6 +5,7 @@
 #include "internal.h"
 
 #include <cmath>
+#include <cstdlib>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -397,8 +398,10 @@ fdc_status fdc_cic_layer_plan_create(fdc_layer_plan **plan, int B, int C, int S,
   if (!fdc::cic_pair_supported(N, M))
     return fail(FDC_EUNSUPPORTED, "layer size %d -> %d not supported (N in the supported set, M in {N, N/2, N/4})",
                 N, M);
-  if (!fdc::index_fits((long long)B * C, N) || !fdc::index_fits((long long)B * S, M))
-    return fail(FDC_EUNSUPPORTED, "B * C * N or B * S * M rows exceed the kernels' 32-bit row indexing");
+  if (!fdc::index_fits((long long)B * C, N) || !fdc::index_fits((long long)B * S, M) ||
+      !fdc::index_fits((long long)S * N, N / 2 + 1))
+    return fail(FDC_EUNSUPPORTED, "B * C * N or B * S * M rows, or the S * N * (N/2+1) bins of gK, exceed the "
+                "kernels' 32-bit indexing");
   auto *p = new (std::nothrow) fdc_layer_plan{};
   if (p == nullptr) return fail(FDC_EINVAL, "out of host memory");
   p->magic = kLayerMagic;
@@ -465,7 +468,7 @@ fdc_status fdc_cic_layer_forward(const fdc_layer_plan *p, const float *x, const 
   // the pooled input spectrum goes to `saved` when the caller keeps it, else to the workspace
   auto *Xh = saved != nullptr ? reinterpret_cast<float2 *>(saved) : U + (size_t)B * S * M * L;
   ImgView id{0, 0, N, N};
-  if (fdc_status st = check_hip(fdc::launch_row_r2c(N, x, fdc::split_layout(T, (long long)B * C, N, L),
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(N, x, fdc::tiled_layout(T, (long long)B * C, N, L),
                                                     (long long)B * C, N, id, (long long)N * N, L, 1.f, 1.f, s),
                                 "layer forward rows"))
     return st;
@@ -473,7 +476,7 @@ fdc_status fdc_cic_layer_forward(const fdc_layer_plan *p, const float *x, const 
                                                         S, s),
                                 "layer forward columns"))
     return st;
-  return check_hip(fdc::launch_row_c2r(M, fdc::split_layout(U, (long long)B * S, M, L), y, (long long)B * S, M, L,
+  return check_hip(fdc::launch_row_c2r(M, fdc::tiled_layout(U, (long long)B * S, M, L), y, (long long)B * S, M, L,
                                        1.f / ((float)M * (float)M), 1.f, artifact_view(p),
                                        (long long)p->out * p->out, s),
                    "layer forward inverse rows");
@@ -490,7 +493,7 @@ fdc_status fdc_cic_layer_backward(const fdc_layer_plan *p, const float *gy, cons
   const int B = p->B, C = p->C, S = p->S, N = p->N, M = p->M, L = M / 2 + 1;
   auto *Tg = reinterpret_cast<float2 *>(ws);
   auto *V = Tg + (size_t)B * S * M * L;
-  if (fdc_status st = check_hip(fdc::launch_row_r2c(M, gy, fdc::split_layout(Tg, (long long)B * S, M, L),
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(M, gy, fdc::tiled_layout(Tg, (long long)B * S, M, L),
                                                     (long long)B * S, M, artifact_view(p),
                                                     (long long)p->out * p->out, L, 1.f / ((float)M * (float)M),
                                                     2.f, s),
@@ -509,7 +512,7 @@ fdc_status fdc_cic_layer_backward(const fdc_layer_plan *p, const float *gy, cons
                                                          s), "layer backward dx columns"))
       return st;
     ImgView id{0, 0, N, N};
-    return check_hip(fdc::launch_row_c2r(N, fdc::split_layout(V, (long long)B * C, N, L), gx, (long long)B * C, N,
+    return check_hip(fdc::launch_row_c2r(N, fdc::tiled_layout(V, (long long)B * C, N, L), gx, (long long)B * C, N,
                                          L, 1.f, 0.5f, id, (long long)N * N, s),
                      "layer backward dx rows");
   }
@@ -603,6 +606,7 @@ struct fdc_stack_plan {
   std::vector<int> N, C;  // sizes[0..layers], channels[0..layers]
   size_t ws_a, ws_b, ws_x;  // complex elements: T / Tg buffer, U / V buffer, Xh when `saved` is NULL
   std::vector<size_t> saved;
+  int tail;  // first of the two last layers run by the LDS-resident tail kernels, or -1
 };
 
 namespace {
@@ -616,6 +620,16 @@ StackLayer stack_layer(const fdc_stack_plan *p, int i) {
 fdc_status check_stack_plan(const fdc_stack_plan *p) {
   if (!plan_live(p) || p->magic != kStackMagic) return fail(FDC_EINVAL, "invalid or destroyed stack plan");
   return FDC_OK;
+}
+// The layer where the stack's LDS-resident tail starts (the last two layers, when
+// their sizes and fan-outs are an instantiated tail), or -1.  FDC_STACK_TAIL=0 in the
+// environment at plan creation keeps every layer on the per-layer kernels.
+int stack_tail(int layers, const int *N, const int *C) {
+  const char *env = std::getenv("FDC_STACK_TAIL");
+  if (env != nullptr && env[0] == '0') return -1;
+  if (layers < 2) return -1;
+  const int a = layers - 2;
+  return fdc::tail_supported(N[a], N[a + 1], N[a + 2], C[a + 1] / C[a], C[a + 2] / C[a + 1]) ? a : -1;
 }
 }  // namespace
 
@@ -631,9 +645,10 @@ fdc_status fdc_cic_stack_plan_create(fdc_stack_plan **plan, int B, int layers, c
       return fail(FDC_EINVAL, "layer %d: sizes %d -> %d (even, positive, non-increasing)", i, N, M);
     if (!fdc::cic_pair_supported(N, M))
       return fail(FDC_EUNSUPPORTED, "layer %d: size %d -> %d not supported", i, N, M);
-    if (!fdc::index_fits((long long)B * C, N) || !fdc::index_fits((long long)B * S, M))
-      return fail(FDC_EUNSUPPORTED, "layer %d: B * C * N or B * S * M rows exceed the kernels' 32-bit row indexing",
-                  i);
+    if (!fdc::index_fits((long long)B * C, N) || !fdc::index_fits((long long)B * S, M) ||
+        !fdc::index_fits((long long)S * N, N / 2 + 1))
+      return fail(FDC_EUNSUPPORTED, "layer %d: B * C * N or B * S * M rows, or the bins of gK, exceed the kernels' "
+                  "32-bit indexing", i);
   }
   auto *p = new (std::nothrow) fdc_stack_plan{};
   if (p == nullptr) return fail(FDC_EINVAL, "out of host memory");
@@ -649,6 +664,16 @@ fdc_status fdc_cic_stack_plan_create(fdc_stack_plan **plan, int B, int layers, c
     p->ws_b = std::max(p->ws_b, std::max(u, t));
     p->ws_x = std::max(p->ws_x, x);
     p->saved.push_back(x * sizeof(fdc_c64));
+  }
+  p->tail = stack_tail(layers, sizes, channels);
+  if (p->tail >= 0) {
+    // the tail keeps both layers' pooled spectra (in Xw when `saved` is NULL) and
+    // writes both layers' per-image dK products to the U / V buffer
+    const StackLayer ga = stack_layer(p, p->tail), gb = stack_layer(p, p->tail + 1);
+    const size_t xa = (size_t)B * ga.C * ga.M * ga.L, xb = (size_t)B * gb.C * gb.M * gb.L;
+    const size_t pa = (size_t)B * ga.S * ga.M * ga.L, pb = (size_t)B * gb.S * gb.M * gb.L;
+    p->ws_x = std::max(p->ws_x, xa + xb);
+    p->ws_b = std::max(p->ws_b, pa + pb);
   }
   if (!plan_register(p)) {
     delete p;
@@ -696,9 +721,28 @@ fdc_status fdc_cic_stack_forward(const fdc_stack_plan *p, const float *x, const 
     const StackLayer g = stack_layer(p, i);
     const long long cin = (long long)B * g.C, cout = (long long)B * g.S;
     auto *Xh = saved ? reinterpret_cast<float2 *>(saved[i]) : Xw;
+    if (i == p->tail) {
+      // the last two layers in one launch, from the previous layer's column-inverted
+      // spectra in U (or from x when the tail is the whole stack)
+      const StackLayer h = stack_layer(p, i + 1);
+      auto *Xh2 = saved ? reinterpret_cast<float2 *>(saved[i + 1]) : Xw + (size_t)cin * g.M * g.L;
+      fdc::SpecLayout in{};
+      float a_in = 1.f;
+      if (i > 0) {
+        const StackLayer f = stack_layer(p, i - 1);
+        in = fdc::tiled_layout(U, (long long)B * f.S, f.M, f.L);
+        a_in = 1.f / ((float)f.M * (float)f.M);
+      }
+      return check_hip(fdc::launch_tail_fwd(g.N, g.M, h.M, g.S / g.C, h.S / h.C, in, i == 0 ? x : nullptr, a_in,
+                                            reinterpret_cast<const float2 *>(K[i]),
+                                            reinterpret_cast<const float2 *>(K[i + 1]),
+                                            fdc::tiled_layout(Xh, cin, g.M, g.L),
+                                            fdc::tiled_layout(Xh2, cout, h.M, h.L), y, B, g.C, s),
+                       "stack forward tail");
+    }
     if (i == 0) {
       ImgView id{0, 0, g.N, g.N};
-      if (fdc_status st = check_hip(fdc::launch_row_r2c(g.N, x, fdc::split_layout(A, cin, g.N, g.L), cin, g.N, id,
+      if (fdc_status st = check_hip(fdc::launch_row_r2c(g.N, x, fdc::tiled_layout(A, cin, g.N, g.L), cin, g.N, id,
                                                         (long long)g.N * g.N, g.L, 1.f, 1.f, s),
                                     "stack forward rows"))
         return st;
@@ -708,17 +752,18 @@ fdc_status fdc_cic_stack_forward(const fdc_stack_plan *p, const float *x, const 
                                   "stack forward columns"))
       return st;
     const float inv = 1.f / ((float)g.M * (float)g.M);
+    if (i + 1 == p->tail) continue;  // the tail starts from this layer's column-inverted spectra
     if (i + 1 < p->layers) {
       // this layer's inverse rows and the next layer's forward rows on the same rows
       const StackLayer h = stack_layer(p, i + 1);
-      if (fdc_status st = check_hip(fdc::launch_row_c2r_r2c(g.M, fdc::split_layout(U, cout, g.M, g.L), g.L, inv, 1.f,
-                                                            fdc::split_layout(A, cout, h.N, h.L), h.L, 1.f, 1.f,
+      if (fdc_status st = check_hip(fdc::launch_row_c2r_r2c(g.M, fdc::tiled_layout(U, cout, g.M, g.L), g.L, inv, 1.f,
+                                                            fdc::tiled_layout(A, cout, h.N, h.L), h.L, 1.f, 1.f,
                                                             cout, g.M, s),
                                     "stack forward boundary rows"))
         return st;
     } else {
       ImgView id{0, 0, g.M, g.M};
-      if (fdc_status st = check_hip(fdc::launch_row_c2r(g.M, fdc::split_layout(U, cout, g.M, g.L), y, cout, g.M, g.L,
+      if (fdc_status st = check_hip(fdc::launch_row_c2r(g.M, fdc::tiled_layout(U, cout, g.M, g.L), y, cout, g.M, g.L,
                                                         inv, 1.f, id, (long long)g.M * g.M, s),
                                     "stack forward inverse rows"))
         return st;
@@ -739,12 +784,42 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, cons
   auto *Tg = reinterpret_cast<float2 *>(ws);
   auto *V = Tg + p->ws_a;
   for (int i = p->layers - 1; i >= 0; --i) {
+    if (p->tail >= 0 && i == p->tail + 1) {
+      // the last two layers in one launch: their dK products per image go to V and are
+      // summed over the images in order; the output is the previous layer's
+      // upstream-gradient row spectrum in Tg (or the input gradient)
+      const int a = p->tail;
+      const StackLayer ga = stack_layer(p, a), gb = stack_layer(p, a + 1);
+      auto *part_a = V, *part_b = V + (size_t)B * ga.S * ga.M * ga.L;
+      const int out_mode = a > 0 ? 0 : (gx ? 1 : 2);
+      fdc::SpecLayout tg{};
+      if (a > 0) {
+        const StackLayer f = stack_layer(p, a - 1);
+        tg = fdc::tiled_layout(Tg, (long long)B * ga.C, f.M, f.L);
+      }
+      const float a_out = 1.f / ((float)ga.N * (float)ga.N);
+      if (fdc_status st = check_hip(
+              fdc::launch_tail_bwd(ga.N, ga.M, gb.M, ga.S / ga.C, gb.S / gb.C, gy,
+                                   fdc::tiled_layout(static_cast<const float2 *>(saved[a]), (long long)B * ga.C, ga.M, ga.L),
+                                   fdc::tiled_layout(static_cast<const float2 *>(saved[a + 1]), (long long)B * gb.C, gb.M, gb.L),
+                                   reinterpret_cast<const float2 *>(K[a]), reinterpret_cast<const float2 *>(K[a + 1]),
+                                   part_a, part_b, out_mode, tg, a_out, gx, B, ga.C, s),
+              "stack backward tail"))
+        return st;
+      if (fdc_status st = check_hip(fdc::launch_gk_reduce2(part_a, reinterpret_cast<float2 *>(gK[a]), ga.S, ga.M,
+                                                           ga.N, part_b, reinterpret_cast<float2 *>(gK[a + 1]), gb.S,
+                                                           gb.M, gb.N, B, s),
+                                    "stack backward tail dK sums"))
+        return st;
+      i = a;  // continue with layer a - 1
+      continue;
+    }
     const StackLayer g = stack_layer(p, i);
     const long long cin = (long long)B * g.C, cout = (long long)B * g.S;
     const float inv = 1.f / ((float)g.M * (float)g.M);
     if (i == p->layers - 1) {
       ImgView id{0, 0, g.M, g.M};
-      if (fdc_status st = check_hip(fdc::launch_row_r2c(g.M, gy, fdc::split_layout(Tg, cout, g.M, g.L), cout, g.M, id,
+      if (fdc_status st = check_hip(fdc::launch_row_r2c(g.M, gy, fdc::tiled_layout(Tg, cout, g.M, g.L), cout, g.M, id,
                                                         (long long)g.M * g.M, g.L, inv, 2.f, s),
                                     "stack backward rows"))
         return st;
@@ -775,14 +850,14 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, cons
       // this layer's adjoint inverse rows and the previous layer's upstream-gradient rows
       const StackLayer h = stack_layer(p, i - 1);
       const float hinv = 1.f / ((float)h.M * (float)h.M);
-      if (fdc_status st = check_hip(fdc::launch_row_c2r_r2c(g.N, fdc::split_layout(V, cin, g.N, g.L), g.L, 1.f, 0.5f,
-                                                            fdc::split_layout(Tg, cin, h.M, h.L), h.L, hinv, 2.f,
+      if (fdc_status st = check_hip(fdc::launch_row_c2r_r2c(g.N, fdc::tiled_layout(V, cin, g.N, g.L), g.L, 1.f, 0.5f,
+                                                            fdc::tiled_layout(Tg, cin, h.M, h.L), h.L, hinv, 2.f,
                                                             cin, g.N, s),
                                     "stack backward boundary rows"))
         return st;
     } else {
       ImgView id{0, 0, g.N, g.N};
-      if (fdc_status st = check_hip(fdc::launch_row_c2r(g.N, fdc::split_layout(V, cin, g.N, g.L), gx, cin, g.N, g.L,
+      if (fdc_status st = check_hip(fdc::launch_row_c2r(g.N, fdc::tiled_layout(V, cin, g.N, g.L), gx, cin, g.N, g.L,
                                                         1.f, 0.5f, id, (long long)g.N * g.N, s),
                                     "stack backward dx rows"))
         return st;
@@ -1069,6 +1144,13 @@ fdc_status fdc_cic_layer_dk_ranges(const fdc_layer_plan *p, int *ranges) {
   if (ranges == nullptr) return fail(FDC_EINVAL, "ranges is NULL");
   // the same scratch as fdc_cic_layer_backward: the dX buffer
   *ranges = fdc::gk_batch_ranges(p->N, p->M, p->B, p->S, (long long)p->B * p->C * p->N * (p->M / 2 + 1));
+  return FDC_OK;
+}
+
+fdc_status fdc_cic_stack_tail(const fdc_stack_plan *p, int *first_layer) {
+  if (fdc_status st = check_stack_plan(p)) return st;
+  if (first_layer == nullptr) return fail(FDC_EINVAL, "first_layer is NULL");
+  *first_layer = p->tail;
   return FDC_OK;
 }
 

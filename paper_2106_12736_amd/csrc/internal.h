@@ -34,28 +34,47 @@ inline bool index_fits(long long planes, long long n) {
 }
 
 // Storage of a half spectrum of `planes` images with `rows` rows and L stored bins
-// per row.  Bins l < L-1 of row r of plane p are at main[p*ps + r*rs + l]; the last
-// bin, l = L-1, is at side[p*sps + r*srs].
+// per row.  Bins l < L-1 of row r of plane p are at
+// main[p*ps + r*rs + (l/8)*ts + l%8] (the 8-bin tiles of a row are ts apart; ts = 8
+// is row-major); the last bin, l = L-1, is at side[p*sps + r*srs].
 //   plain: the row-major [planes][rows][L] array (side = main + L - 1).
-//   split: a main block [planes][rows][L-1] followed by the last column as a
-//          [planes][rows] block.  With L - 1 = n/2 a power of two every main row
-//          starts on an aligned boundary, and the odd last column is contiguous
-//          along the rows, so column tiles read whole aligned runs everywhere.
+//   split: a row-major main block [planes][rows][L-1] followed by the last column
+//          as a [planes][rows] block.  With L - 1 = n/2 a power of two every main
+//          row starts on an aligned boundary, and the odd last column is contiguous
+//          along the rows.
+//   tiled: the split layout with the main block of each plane stored as column
+//          tiles [planes][(L-1)/8][rows][8]: a column transform's tile of 8
+//          columns is one contiguous run down the rows (64-byte row pieces read
+//          from a row-major block run at half the HBM rate), and two adjacent rows
+//          of a tile share a 128-byte line, as a row transform's pair of rows
+//          reads them.  Used for every intermediate of the CIC layer path.
 struct SpecLayout {
   float2 *main;
   long long ps;
   long long rs;
+  long long ts;
   float2 *side;
   long long sps;
   long long srs;
 };
+// Offset of bin l (< L-1) inside its row of the main block.
+__host__ __device__ __forceinline__ long long bin_off(const SpecLayout &s, int l) {
+  return (long long)(l >> 3) * s.ts + (l & 7);
+}
 inline SpecLayout plain_layout(const float2 *p, int rows, int L) {
   float2 *q = const_cast<float2 *>(p);
-  return SpecLayout{q, (long long)rows * L, L, q + (L - 1), (long long)rows * L, L};
+  return SpecLayout{q, (long long)rows * L, L, 8, q + (L - 1), (long long)rows * L, L};
 }
 inline SpecLayout split_layout(const float2 *p, long long planes, int rows, int L) {
   float2 *q = const_cast<float2 *>(p);
-  return SpecLayout{q, (long long)rows * (L - 1), L - 1, q + planes * rows * (L - 1), rows, 1};
+  return SpecLayout{q, (long long)rows * (L - 1), L - 1, 8, q + planes * rows * (L - 1), rows, 1};
+}
+// Tiles of 8 bins when L - 1 is a multiple of 8; narrower rows are one tile (the
+// split layout).
+inline SpecLayout tiled_layout(const float2 *p, long long planes, int rows, int L) {
+  if ((L - 1) % 8 != 0) return split_layout(p, planes, rows, L);
+  float2 *q = const_cast<float2 *>(p);
+  return SpecLayout{q, (long long)rows * (L - 1), 8, (long long)rows * 8, q + planes * rows * (L - 1), rows, 1};
 }
 // Layout of `planes` P x (P/2+1) Full FDC spectra.  Main block: row k of every plane
 // side by side, plane i's bins l < P/2 of row k at main[(k * planes + i) * R + l] with
@@ -65,7 +84,7 @@ inline SpecLayout split_layout(const float2 *p, long long planes, int rows, int 
 inline SpecLayout full_spec_layout(const float2 *p, long long planes, int P) {
   float2 *q = const_cast<float2 *>(p);
   const long long R = FDC_FULL_ROW(P);
-  return SpecLayout{q, R, planes * R, q + (long long)P * planes * R, FDC_FULL_SIDE_PLANE(P), 1};
+  return SpecLayout{q, R, planes * R, 8, q + (long long)P * planes * R, FDC_FULL_SIDE_PLANE(P), 1};
 }
 inline long long full_spec_elems(long long planes, int P) {
   return planes * ((long long)P * FDC_FULL_ROW(P) + FDC_FULL_SIDE_PLANE(P));
@@ -117,11 +136,33 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
                              int S, float2 *part, long long part_elems, hipStream_t s);
 hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, float2 *V, int B, int C, int S,
                              hipStream_t s);
+// gK [S][N][N/2+1] from BG partial sums part [BG][S][M][M/2+1] (plain layout): at the
+// kept bins the partial sums added in order, exact zeros elsewhere; one launch for
+// one reduction (part1 NULL) or two.
+hipError_t launch_gk_reduce2(const float2 *part0, float2 *gK0, int S0, int M0, int N0, const float2 *part1,
+                             float2 *gK1, int S1, int M1, int N1, int BG, hipStream_t s);
 // dK (one batch range) and dX of one layer in a single launch, where the dX tiles pack
 // the dK workgroup (col_bwd_dk_dx_supported).
 bool col_bwd_dk_dx_supported(int n, int m);
 hipError_t launch_col_bwd_dk_dx(int n, int m, const float2 *Tg, const float2 *Xh, const float2 *K, float2 *gK,
                                 float2 *V, int B, int C, int S, hipStream_t s);
+
+// The last two layers of a stack with all intermediates in LDS (tail.hip): layer a
+// (na -> ma, fan-out ja) and layer b (ma -> mb, fan-out jb), one workgroup per input
+// plane (b, c) of layer a, B * C workgroups.
+//   fwd: in = previous layer's column-inverted spectra (split [B C][na][na/2+1]) with
+//        inverse weight a_in, or x = input images [B][C][na][na] (x non-NULL);
+//        saved_a split [B C][ma][ma/2+1], saved_b split [B C ja][mb][mb/2+1]; y.
+//   bwd: part_a plain [B][C ja][ma][ma/2+1], part_b plain [B][C ja jb][mb][mb/2+1]
+//        (per-image dK products; launch_gk_reduce sums them); out_mode 0: Tg split
+//        [B C][na][na/2+1] with weights (c_l a_out); 1: gx [B][C][na][na]; 2: none.
+bool tail_supported(int na, int ma, int mb, int ja, int jb);
+hipError_t launch_tail_fwd(int na, int ma, int mb, int ja, int jb, SpecLayout in, const float *x, float a_in,
+                           const float2 *Ka, const float2 *Kb, SpecLayout saved_a, SpecLayout saved_b, float *y,
+                           int B, int C, hipStream_t s);
+hipError_t launch_tail_bwd(int na, int ma, int mb, int ja, int jb, const float *gy, SpecLayout saved_a,
+                           SpecLayout saved_b, const float2 *Ka, const float2 *Kb, float2 *part_a, float2 *part_b,
+                           int out_mode, SpecLayout Tg, float a_out, float *gx, int B, int C, hipStream_t s);
 
 // Full FDC (full_fdc.hip).  Spectra in the padded split layout full_spec_layout,
 // P a multiple of 8; tw is the device table

@@ -130,8 +130,9 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_r2c(const float *__
     const float2 A = make_float2((zk.x + zn.x) * wgt, (zk.y - zn.y) * wgt);
     const float2 Bv = make_float2((zk.y + zn.y) * wgt, (zn.x - zk.x) * wgt);
     if (k < L - 1) {
-      oa[k] = A;
-      ob[k] = Bv;
+      const long long o = bin_off(out, k);
+      oa[o] = A;
+      ob[o] = Bv;
     } else {
       float2 *sa = out.side + plane * out.sps + (long long)r0 * out.srs;
       sa[0] = A;
@@ -165,8 +166,9 @@ __device__ __forceinline__ void c2r_gather(float2 (&v)[RowCfg<N>::E], const Spec
       // unconditional loads from valid addresses; bins beyond Lin get weight 0 (the loaded
       // value is always used, so the load is not sunk into a per-lane branch)
       const bool in_main = kk < Lin - 1;
-      const float2 *pa = in_main ? ia + kk : sa;
-      const float2 *pb = in_main ? ib + kk : sa + in.srs;
+      const long long o = bin_off(in, kk);
+      const float2 *pa = in_main ? ia + o : sa;
+      const float2 *pb = in_main ? ib + o : sa + in.srs;
       float2 a = *pa, b = *pb;
       const bool edge = (kk == 0 || 2 * kk == N);
       const float wgt = kk < Lin ? (edge ? a1 : a1 * b1) : 0.f;
@@ -211,14 +213,16 @@ __device__ __forceinline__ void c2r_gather(float2 (&v)[RowCfg<N>::E], const Spec
         // m whose lane t = 0 holds the side bin KS (bin KS - t on the other lanes)
         constexpr bool side_m = (LIN == 1 && m == E / 2) || (LIN == 2 && m == 3 * E / 4);
         if constexpr (side_m) {
-          const float2 *pa = t0 ? sa : ia + (KS - t);
-          const float2 *pb = t0 ? sb : ib + (KS - t);
+          const long long o = bin_off(in, KS - t);
+          const float2 *pa = t0 ? sa : ia + o;
+          const float2 *pb = t0 ? sb : ib + o;
           a = *pa;
           b = *pb;
         } else {
           const int kk = low ? t + TPS * m : N - t - TPS * m;
-          a = ia[kk];
-          b = ib[kk];
+          const long long o = bin_off(in, kk);
+          a = ia[o];
+          b = ib[o];
         }
         // l = 0 (m = 0, t = 0) and, with LIN 1, l = N/2 (m = E/2, t = 0): weight a1 and
         // real-part semantics
@@ -321,8 +325,9 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r_r2c(SpecLayout 
     const float2 A = make_float2((zk.x + zn.x) * wgt, (zk.y - zn.y) * wgt);
     const float2 Bv = make_float2((zk.y + zn.y) * wgt, (zn.x - zk.x) * wgt);
     if (k < Lout - 1) {
-      oa[k] = A;
-      ob[k] = Bv;
+      const long long o = bin_off(out, k);
+      oa[o] = A;
+      ob[o] = Bv;
     } else {
       float2 *so = out.side + plane * out.sps + (long long)r0 * out.srs;
       so[0] = A;
@@ -437,17 +442,24 @@ __device__ __forceinline__ int kept_row(int mrow) {
   return mrow < M / 2 ? mrow : mrow + (N - M);
 }
 
-// Column (plane, l) of a split-layout spectrum (see SpecLayout) of `planes`
-// images with ROWS rows and L bins per row: row r is at p[r * stride].
+// Column (plane, l) of a tiled spectrum (tiled_layout) of `planes` images with ROWS
+// rows and L bins per row: row r is at p[r * stride].  Bins l < L-1 sit in tiles of
+// 8 columns stored down the rows (stride 8); narrower rows (L - 1 < 8) are
+// row-major; the last bin is in the side block (stride 1).
 struct ColPtr {
   float2 *p;
   int stride;
 };
 template <int ROWS, int L>
-__device__ __forceinline__ ColPtr split_col(const float2 *base, int planes, int plane, int l) {
+__device__ __forceinline__ ColPtr tiled_col(const float2 *base, int planes, int plane, int l) {
   constexpr int H = L - 1;
   float2 *b = const_cast<float2 *>(base);
-  if (l < H) return ColPtr{b + (long long)plane * ROWS * H + l, H};
+  if (l < H) {
+    if constexpr (H % 8 == 0)
+      return ColPtr{b + (long long)plane * ROWS * H + (long long)(l >> 3) * ROWS * 8 + (l & 7), 8};
+    else
+      return ColPtr{b + (long long)plane * ROWS * H + l, H};
+  }
   return ColPtr{b + (long long)planes * ROWS * H + (long long)plane * ROWS, 1};
 }
 
@@ -459,7 +471,7 @@ struct ColPtr64 {
   long long stride;
 };
 __device__ __forceinline__ ColPtr64 layout_col(const SpecLayout &sl, int H, int plane, int l) {
-  if (l < H) return ColPtr64{sl.main + (long long)plane * sl.ps + l, sl.rs};
+  if (l < H) return ColPtr64{sl.main + (long long)plane * sl.ps + bin_off(sl, l), sl.rs};
   return ColPtr64{sl.side + (long long)plane * sl.sps, sl.srs};
 }
 
@@ -494,13 +506,13 @@ __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fwd_crop(const float
   stage_twiddles<N>(tw, threadIdx.x, CT * TPS);
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
-  const ColPtr tc = split_col<N, L>(T, planes, c.plane, c.l);
+  const ColPtr tc = tiled_col<N, L>(T, planes, c.plane, c.l);
   float2 v[E];
 #pragma unroll
   for (int m = 0; m < E; ++m) v[m] = tc.p[(t + TPS * m) * tc.stride];  // lanes past the end read a valid column
   fft_seq<N, -1, true, false, kLdsPlain, ColCfg<N>>(v, t, lds, s, CT, tw, 1);
   if (!c.ok) return;
-  const ColPtr xc = split_col<M, L>(Xh, planes, c.plane, c.l);
+  const ColPtr xc = tiled_col<M, L>(Xh, planes, c.plane, c.l);
 #pragma unroll
   for (int m = 0; m < E; ++m) {
     const int k = t + TPS * m;
@@ -536,7 +548,7 @@ __global__ __launch_bounds__(CT *ColCfg<M>::TPS) void k_col_cic_inv(const float2
   const int ci = cj / JB;
   const int o0 = ci * J + (cj - ci * JB) * JW;
   const int bc = b * C + ci;
-  const ColPtr xc = split_col<M, L>(Xh, groups / JB, bc, c.l);
+  const ColPtr xc = tiled_col<M, L>(Xh, groups / JB, bc, c.l);
   float2 x[E], kn[E];
   auto load_k = [&](int o) {
     const float2 *kcol = K + (long long)o * N * NF + c.l;
@@ -553,7 +565,7 @@ __global__ __launch_bounds__(CT *ColCfg<M>::TPS) void k_col_cic_inv(const float2
     if (jj + 1 < JW) load_k(o0 + jj + 1);  // the next kernel column loads while this one transforms
     fft_seq<M, +1, true, false, kLdsPlain, ColCfg<M>>(z, t, lds, s, CT, tw, 1);
     if (c.ok) {
-      const ColPtr uc = split_col<M, L>(U, groups * JW, b * S + o0 + jj, c.l);  // B * S planes
+      const ColPtr uc = tiled_col<M, L>(U, groups * JW, b * S + o0 + jj, c.l);  // B * S planes
 #pragma unroll
       for (int m = 0; m < E; ++m) uc.p[(t + TPS * m) * uc.stride] = z[m];
     }
@@ -583,12 +595,12 @@ __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fwd_cic(const float2
   const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, B * C, B);
   const int b = c.plane % B, ci = c.plane / B;
   const int bc = b * C + ci, S = C * JW;
-  const ColPtr tc = split_col<N, L>(T, B * C, bc, c.l);
+  const ColPtr tc = tiled_col<N, L>(T, B * C, bc, c.l);
   float2 v[EN];
 #pragma unroll
   for (int m = 0; m < EN; ++m) v[m] = tc.p[(t + TPSN * m) * tc.stride];  // lanes past the end read a valid column
   fft_seq<N, -1, true, false, kLdsPlain, CN>(v, t, lds, s, CT, tw, 1);
-  const ColPtr xc = split_col<M, L>(Xh, B * C, bc, c.l);
+  const ColPtr xc = tiled_col<M, L>(Xh, B * C, bc, c.l);
   __syncthreads();  // every lane is done with the transform's LDS
 #pragma unroll
   for (int m = 0; m < EN; ++m) {
@@ -614,7 +626,7 @@ __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fwd_cic(const float2
     // the first exchange write waits for every lane's reads of the tile above
     fft_seq<M, +1, true, false, kLdsPlain, CM>(z, tp, lds, js * M * CT + s, CT, tw, N / M);
     if (act) {
-      const ColPtr uc = split_col<M, L>(U, B * S, b * S + o, c.l);
+      const ColPtr uc = tiled_col<M, L>(U, B * S, b * S + o, c.l);
 #pragma unroll
       for (int m = 0; m < EM; ++m) uc.p[(tp + TPSM * m) * uc.stride] = z[m];
     }
@@ -685,8 +697,8 @@ __device__ __forceinline__ void col_bwd_gk_tile(int lin, int nwg, int tid, const
   for (int b0 = b_lo; b0 < b_hi; b0 += BP) {
     const int b = b0 + g;
     const bool act = c.ok && b < b_hi;
-    const ColPtr gc = split_col<M, L>(Tg, B * S, (act ? b : 0) * S + o, c.l);
-    const ColPtr xc = split_col<M, L>(Xh, B * C, (act ? b : 0) * C + ci, c.l);
+    const ColPtr gc = tiled_col<M, L>(Tg, B * S, (act ? b : 0) * S + o, c.l);
+    const ColPtr xc = tiled_col<M, L>(Xh, B * C, (act ? b : 0) * C + ci, c.l);
     // loads are unconditional (inactive lanes read a valid column); inactive lanes add nothing
     float2 v[E], xv[E];
 #pragma unroll
@@ -752,24 +764,54 @@ __global__ __launch_bounds__(CT *ColCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
                              B, C, J, N, S, BG);
 }
 
-// gK [S][N][N/2+1] from the BG range sums part [BG][S][M][M/2+1]: at the kept bins
-// the ranges added in order, zeros elsewhere.  A workgroup takes whole rows.
-__global__ __launch_bounds__(256) void k_gk_reduce(const float2 *__restrict__ part, float2 *__restrict__ gK, int BG,
-                                                   int S, int M, int N) {
-  const int L = M / 2 + 1, nf = N / 2 + 1;
-  const long long range_stride = (long long)S * M * L;
-  for (long long r = blockIdx.x; r < (long long)S * N; r += gridDim.x) {
-    const int o = (int)(r / N), krow = (int)(r - (long long)o * N);
-    const int mrow = krow < M / 2 ? krow : (krow >= N - M / 2 ? krow - (N - M) : -1);
-    float2 *dst = gK + r * nf;
-    const float2 *src = part + ((long long)o * M + (mrow < 0 ? 0 : mrow)) * L;
-    for (int l = threadIdx.x; l < nf; l += blockDim.x) {
+// gK [S][N][N/2+1] from BG partial sums part [BG][S][M][M/2+1] (plain layout), for
+// one or two reductions (grid.y selects the GkSum): a wavefront per gK row, its
+// lanes along the row; the partial sums added in order at the kept bins, exact
+// zeros elsewhere.
+struct GkSum {
+  const float2 *part;
+  float2 *gK;
+  int BG, S, M, N;
+};
+
+__global__ __launch_bounds__(256) void k_gk_reduce(GkSum d0, GkSum d1) {
+  const GkSum d = blockIdx.y == 0 ? d0 : d1;
+  const int L = d.M / 2 + 1, nf = d.N / 2 + 1, lane = threadIdx.x & 63;
+  const long long rows = (long long)d.S * d.N;
+  const long long range_stride = (long long)d.S * d.M * L;
+  for (long long r = (long long)blockIdx.x * 4 + (threadIdx.x >> 6); r < rows; r += (long long)gridDim.x * 4) {
+    const int o = (int)(r / d.N), krow = (int)(r - (long long)o * d.N);
+    const int mrow = krow < d.M / 2 ? krow : (krow >= d.N - d.M / 2 ? krow - (d.N - d.M) : -1);
+    float2 *dst = d.gK + r * nf;
+    const float2 *src = d.part + ((long long)o * d.M + (mrow < 0 ? 0 : mrow)) * L;
+    for (int l = lane; l < nf; l += 64) {
       float2 v = make_float2(0.f, 0.f);
-      if (mrow >= 0 && l < L)
-        for (int q = 0; q < BG; ++q) v = cadd(v, src[q * range_stride + l]);
+      if (mrow >= 0 && l < L) {
+        int q = 0;
+        for (; q + 8 <= d.BG; q += 8) {  // eight loads in flight, then added in order
+          float2 a[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) a[i] = src[(q + i) * range_stride + l];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) v = cadd(v, a[i]);
+        }
+        for (; q < d.BG; ++q) v = cadd(v, src[q * range_stride + l]);
+      }
       dst[l] = v;
     }
   }
+}
+
+static hipError_t gk_reduce(const GkSum &d0, const GkSum *d1, hipStream_t s) {
+  long long rows = (long long)d0.S * d0.N;
+  if (d1) rows = std::max(rows, (long long)d1->S * d1->N);
+  const unsigned gx = (unsigned)std::min<long long>((rows + 3) / 4, 4096);
+  const char *nm = "gk_reduce";
+  timing_before(nm, s);
+  hipLaunchKernelGGL(k_gk_reduce, dim3(gx, d1 ? 2 : 1), dim3(256), 0, s, d0, d1 ? *d1 : d0);
+  const hipError_t e = hipGetLastError();
+  timing_after(nm, s);
+  return e;
 }
 
 template <int N, int M>
@@ -817,7 +859,7 @@ __device__ __forceinline__ void col_bwd_gx_tile(int lin, bool valid, int tid, co
     const int j = j0 + js;
     const bool act = c.ok && j < J;
     const int o = ci * J + (act ? j : 0);
-    const ColPtr gc = split_col<M, L>(Tg, planes * J, b * S + o, c.l);
+    const ColPtr gc = tiled_col<M, L>(Tg, planes * J, b * S + o, c.l);
     const float2 *kcol = K + (long long)o * N * NF + c.l;
     // loads are unconditional (inactive lanes read a valid column); inactive lanes add nothing
     float2 g[CM::E], kv[CM::E];
@@ -858,7 +900,7 @@ __device__ __forceinline__ void col_bwd_gx_tile(int lin, bool valid, int tid, co
   }
   fft_seq<N, +1, true, false, kLdsPlain, ColCfg<N>>(w, t, lds, s, CT, tw, 1);
   if (!c.ok) return;
-  const ColPtr vc = split_col<N, L>(V, planes, b * C + ci, c.l);
+  const ColPtr vc = tiled_col<N, L>(V, planes, b * C + ci, c.l);
 #pragma unroll
   for (int m = 0; m < CN::E; ++m) vc.p[(t + TPSN * m) * vc.stride] = w[m];
 }
@@ -1272,11 +1314,15 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
     err = launch(nm.c_str(), k_col_bwd_gk<M, CT, BP>, tiles * (unsigned)BG, CT * ColCfg<M>::TPS * BP, lds, s, Tg,
                  Xh, gK, part, B, C, S / C, n, S, BG);
     if (err != hipSuccess || BG == 1) return;
-    const long long rows = (long long)S * n;
-    const unsigned grid = (unsigned)std::min<long long>(rows, 8192);
-    err = launch("gk_reduce", k_gk_reduce, grid, 256, 0, s, (const float2 *)part, gK, BG, S, M, n);
+    err = gk_reduce(GkSum{part, gK, BG, S, M, n}, nullptr, s);
   });
   return err;
+}
+
+hipError_t launch_gk_reduce2(const float2 *part0, float2 *gK0, int S0, int M0, int N0, const float2 *part1,
+                             float2 *gK1, int S1, int M1, int N1, int BG, hipStream_t s) {
+  const GkSum d1{part1, gK1, BG, S1, M1, N1};
+  return gk_reduce(GkSum{part0, gK0, BG, S0, M0, N0}, part1 ? &d1 : nullptr, s);
 }
 
 hipError_t launch_col_bwd_dk_dx(int n, int m, const float2 *Tg, const float2 *Xh, const float2 *K, float2 *gK,

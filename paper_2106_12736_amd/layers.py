@@ -171,10 +171,14 @@ class CicLayer(_LayerPlan):
 
     def saved_spectrum(self, saved):
         """The M x (M/2+1) kept bins held in a saved buffer, as a [B][C][M][M/2+1] tensor:
-        columns 0..M/2-1 come from the main block, column M/2 from the block after it."""
+        columns 0..M/2-1 come from the main block (8-column tiles [M/16][M][8] per
+        image and channel when M/2 is a multiple of 8), column M/2 from the block after it."""
         B, C, M = self.B, self.C, self.M
         h = M // 2
-        main = saved[: B * C * M * h].view(B, C, M, h)
+        if h % 8 == 0:
+            main = saved[: B * C * M * h].view(B, C, h // 8, M, 8).permute(0, 1, 3, 2, 4).reshape(B, C, M, h)
+        else:
+            main = saved[: B * C * M * h].view(B, C, M, h)
         side = saved[B * C * M * h:].view(B, C, M, 1)
         return torch.cat([main, side], dim=-1)
 
@@ -427,6 +431,12 @@ class CicStackFused:
                                 device=self.device) for i in range(self.layers)]
         self._saved_arr = _ptr_array(self.saved)
         self._gk_arr = _ptr_array(self.gks)
+
+    def tail(self):
+        """First layer of the LDS-resident tail (fdc_cic_stack_tail), or -1."""
+        r = ctypes.c_int()
+        call("fdc_cic_stack_tail", self._p, ctypes.byref(r))
+        return r.value
 
     def dk_ranges(self):
         """Image ranges each layer's dK step sums separately (fdc_cic_stack_dk_ranges)."""

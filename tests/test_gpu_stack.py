@@ -86,3 +86,71 @@ def test_fused_stack_graph_replays():
         torch.cuda.synchronize()
         for i, (a, b) in enumerate(zip(ref, [st.out] + st.gks)):
             assert torch.equal(a, b), f"replay {rep}: output {i}"
+
+
+def _fused(wl, x, Ks, g, input_grad, tail_env=None):
+    import os
+    old = os.environ.get("FDC_STACK_TAIL")
+    if tail_env is not None:
+        os.environ["FDC_STACK_TAIL"] = tail_env
+    try:
+        st = layers.CicStackFused(wl.batch, wl.sizes, wl.channels)
+    finally:
+        if tail_env is not None:
+            if old is None:
+                del os.environ["FDC_STACK_TAIL"]
+            else:
+                os.environ["FDC_STACK_TAIL"] = old
+    gin = torch.empty_like(x) if input_grad else None
+    st.forward(x, Ks)
+    st.backward(g, Ks, input_grad=gin)
+    torch.cuda.synchronize()
+    return st, gin
+
+
+@pytest.mark.parametrize("wl", inputs.CIC_WORKLOADS[1:], ids=lambda w: w.name)
+def test_stack_tail_matches_per_layer_kernels(wl):
+    """The LDS-resident tail (the last two layers in one launch each way) against the
+    same stack with every layer on the per-layer kernels."""
+    print(f"stack tail {wl.name}", flush=True)
+    d = inputs.make_cic_stack(wl)
+    x = torch.from_numpy(d.x).cuda()
+    Ks = [torch.from_numpy(k).cuda() for k in d.kernels]
+    g = torch.from_numpy(d.grad).cuda()
+    on, gin_on = _fused(wl, x, Ks, g, True)
+    off, gin_off = _fused(wl, x, Ks, g, True, tail_env="0")
+    assert on.tail() == wl.layers - 2 and off.tail() == -1
+    _close(on.out, off.out, "y")
+    for i in range(wl.layers):
+        _close(on.saved[i], off.saved[i], f"saved[{i}]")
+        _close(on.gks[i], off.gks[i], f"dK[{i}]")
+    _close(gin_on, gin_off, "gx")
+    # exact zeros at the bins FDP drops
+    for i in range(wl.layers):
+        N, M = wl.sizes[i], wl.sizes[i + 1]
+        gk = to_np(on.gks[i])
+        assert np.all(gk[:, M // 2:N - M // 2, :] == 0) and np.all(gk[:, :, M // 2 + 1:] == 0)
+
+
+@pytest.mark.parametrize("input_grad", [True, False])
+def test_stack_that_is_only_a_tail(input_grad):
+    """A two-layer stack 128 -> 64 -> 32 is all tail: the forward starts from the input
+    images and the backward ends in the input gradient (or in nothing)."""
+    wl = inputs.CicStack("tail_only_128", 77, 3, (128, 64, 32), (2, 4, 8), "disc")
+    print(f"tail-only stack, input grad {input_grad}", flush=True)
+    d = inputs.make_cic_stack(wl)
+    x = torch.from_numpy(d.x).cuda()
+    Ks = [torch.from_numpy(k).cuda() for k in d.kernels]
+    g = torch.from_numpy(d.grad).cuda()
+    st, gin = _fused(wl, x, Ks, g, input_grad)
+    assert st.tail() == 0
+    x64 = d.x.astype(np.float64)
+    kd = [k.astype(np.complex128) for k in d.kernels]
+    y_ref, saved = fdc.cic_stack_forward(x64, kd, wl.sizes)
+    gks_ref, gx_ref = fdc.cic_stack_backward(d.grad.astype(np.float64), saved, kd, wl.sizes,
+                                             want_input_grad=input_grad)
+    assert_parity(to_np(st.out), y_ref, "y")
+    for i in range(wl.layers):
+        assert_parity(to_np(st.gks[i]), gks_ref[i], f"dK[{i}]")
+    if input_grad:
+        assert_parity(to_np(gin), gx_ref, "gx")
