@@ -103,6 +103,31 @@ __device__ __forceinline__ void stage_twiddles(float2 *tw, int tid, int nthreads
   __syncthreads();
 }
 
+// The same staging in two halves, so that a kernel can issue its own global loads
+// between them and wait for both together: fetch() loads this thread's share of the
+// table into registers, commit() writes it to LDS and synchronises the workgroup
+// (every thread of the workgroup must call it).
+template <int N, int NT>
+struct TwiddleStage {
+  static constexpr int PER = (N + NT - 1) / NT;
+  float2 v[PER];
+  __device__ __forceinline__ void fetch(int tid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int j = tid + i * NT;
+      v[i] = twiddle_load<N>(j < N ? j : 0);
+    }
+  }
+  __device__ __forceinline__ void commit(float2 *tw, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int j = tid + i * NT;
+      if (j < N) tw[j] = v[i];
+    }
+    __syncthreads();
+  }
+};
+
 // ---------------------------------------------------------------------------
 // compile-time loops
 // ---------------------------------------------------------------------------

@@ -93,7 +93,8 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_r2c(const float *__
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   static_assert(TPS <= 64, "a row sequence must fit in one wavefront");
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
-  stage_twiddles<N>(tw, threadIdx.x, SPW * TPS);
+  TwiddleStage<N, SPW * TPS> tws;
+  tws.fetch(threadIdx.x);
   const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
   // 32-bit row arithmetic: the launchers keep planes * rows_per_plane below 2^31
   int pair = xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
@@ -115,6 +116,7 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_r2c(const float *__
     const float xa = xp[ia < 0 ? 0 : ia], xb = xp[ib < 0 ? 0 : ib];
     v[m] = make_float2(ia >= 0 ? xa : 0.f, ib >= 0 ? xb : 0.f);
   }
+  tws.commit(tw, threadIdx.x);  // the twiddle table and the rows load together
   fft_seq<N, -1, true, true, kRowLds, RowCfg<N>>(v, t, lds, s * N, 1, tw, 1);
   lds_barrier<true>();
   row_to_lds<N>(v, lds, s, t);
@@ -258,7 +260,8 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   static_assert(TPS <= 64, "a row sequence must fit in one wavefront");
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
-  stage_twiddles<N>(tw, threadIdx.x, SPW * TPS);
+  TwiddleStage<N, SPW * TPS> tws;
+  tws.fetch(threadIdx.x);
   const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
   // 32-bit row arithmetic: the launchers keep planes * rows_per_plane below 2^31
   int pair = xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
@@ -269,6 +272,7 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
   const int r0 = (int)(row0 - (unsigned)plane * (unsigned)rows_per_plane);
   float2 v[E];
   c2r_gather<N, LIN>(v, in, plane, r0, t, L, alpha, beta);
+  tws.commit(tw, threadIdx.x);  // the twiddle table and the rows load together
   fft_seq<N, +1, true, true, kRowLds, RowCfg<N>>(v, t, lds, s * N, 1, tw, 1);
   if (!active) return;
   const float sc = LIN == 0 ? 1.f : alpha * beta;  // the factor c2r_gather left out
@@ -297,7 +301,8 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r_r2c(SpecLayout 
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   static_assert(TPS <= 64, "a row sequence must fit in one wavefront");
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
-  stage_twiddles<N>(tw, threadIdx.x, SPW * TPS);
+  TwiddleStage<N, SPW * TPS> tws;
+  tws.fetch(threadIdx.x);
   const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
   // 32-bit row arithmetic: the launchers keep planes * rows_per_plane below 2^31
   int pair = xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
@@ -308,6 +313,7 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r_r2c(SpecLayout 
   const int r0 = (int)(row0 - (unsigned)plane * (unsigned)rows_per_plane);
   float2 v[E];
   c2r_gather<N, LIN>(v, in, plane, r0, t, Lin, a1, b1);
+  tws.commit(tw, threadIdx.x);  // the twiddle table and the rows load together
   fft_seq<N, +1, true, true, kRowLds, RowCfg<N>>(v, t, lds, s * N, 1, tw, 1);
   // v[m] = (row r0, row r0 + 1) at column t + TPS m: the packed input of the forward transform
   fft_seq<N, -1, true, true, kRowLds, RowCfg<N>>(v, t, lds, s * N, 1, tw, 1);
@@ -503,13 +509,15 @@ __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fwd_crop(const float
   using CN = ColCfg<N>;
   constexpr int L = M / 2 + 1, TPS = CN::TPS, E = CN::E;
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
-  stage_twiddles<N>(tw, threadIdx.x, CT * TPS);
+  TwiddleStage<N, CT * TPS> tws;
+  tws.fetch(threadIdx.x);
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
   const ColPtr tc = tiled_col<N, L>(T, planes, c.plane, c.l);
   float2 v[E];
 #pragma unroll
   for (int m = 0; m < E; ++m) v[m] = tc.p[(t + TPS * m) * tc.stride];  // lanes past the end read a valid column
+  tws.commit(tw, threadIdx.x);
   fft_seq<N, -1, true, false, kLdsPlain, ColCfg<N>>(v, t, lds, s, CT, tw, 1);
   if (!c.ok) return;
   const ColPtr xc = tiled_col<M, L>(Xh, planes, c.plane, c.l);
@@ -539,7 +547,8 @@ __global__ __launch_bounds__(CT *ColCfg<M>::TPS) void k_col_cic_inv(const float2
   using CM = ColCfg<M>;
   constexpr int L = M / 2 + 1, NF = N / 2 + 1, TPS = CM::TPS, E = CM::E;
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<M>();
-  stage_twiddles<M>(tw, threadIdx.x, CT * TPS);
+  TwiddleStage<M, CT * TPS> tws;
+  tws.fetch(threadIdx.x);
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   // group index (ci * JB + jb) * B + b: the B images read the same kernel columns
   const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, groups, B);
@@ -558,6 +567,7 @@ __global__ __launch_bounds__(CT *ColCfg<M>::TPS) void k_col_cic_inv(const float2
 #pragma unroll
   for (int m = 0; m < E; ++m) x[m] = xc.p[(t + TPS * m) * xc.stride];
   load_k(o0);
+  tws.commit(tw, threadIdx.x);
   for (int jj = 0; jj < JW; ++jj) {
     float2 z[E];
 #pragma unroll
@@ -589,7 +599,8 @@ __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fwd_cic(const float2
   constexpr int JP = TPSN / TPSM;
   static_assert(JP * TPSM == TPSN, "thread layouts of the two transforms must nest");
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
-  stage_twiddles<N>(tw, threadIdx.x, CT * TPSN);
+  TwiddleStage<N, CT * TPSN> tws;
+  tws.fetch(threadIdx.x);
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   const int tp = t % TPSM, js = t / TPSM;
   const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, B * C, B);
@@ -599,6 +610,7 @@ __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fwd_cic(const float2
   float2 v[EN];
 #pragma unroll
   for (int m = 0; m < EN; ++m) v[m] = tc.p[(t + TPSN * m) * tc.stride];  // lanes past the end read a valid column
+  tws.commit(tw, threadIdx.x);
   fft_seq<N, -1, true, false, kLdsPlain, CN>(v, t, lds, s, CT, tw, 1);
   const ColPtr xc = tiled_col<M, L>(Xh, B * C, bc, c.l);
   __syncthreads();  // every lane is done with the transform's LDS

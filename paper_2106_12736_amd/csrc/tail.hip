@@ -586,7 +586,7 @@ __global__ __launch_bounds__(NT) void k_tail_bwd(const float *__restrict__ gy, S
 // host side
 // ----------------------------------------------------------------------------
 #ifndef FDC_TAIL_THREADS
-#define FDC_TAIL_THREADS 512
+#define FDC_TAIL_THREADS 1024
 #endif
 constexpr int kTailThreads = FDC_TAIL_THREADS;
 
