@@ -169,6 +169,18 @@ def fused_step_launches(wl, input_grad=False, ranges=None, tail=-1):
     return out
 
 
+def fft2_launches(n, planes, inverse):
+    """(kernel name, algorithmic bytes) of one n x n rfft2 (or irfft2, inverse=True) of
+    `planes` planes: one launch for square planes up to 64 x 64, else rows then columns."""
+    nf = n // 2 + 1
+    real, spec = F32 * planes * n * n, C64 * planes * n * nf
+    if n in (16, 32, 64):
+        return [(f"fft2_small_{'inv' if inverse else 'fwd'}_{n}", real + spec)]
+    if inverse:
+        return [(f"col_fft_inv_{n}", 2 * spec), (f"row_c2r_{n}", spec + real)]
+    return [(f"row_r2c_{n}", real + spec), (f"col_fft_fwd_{n}", 2 * spec)]
+
+
 def chain_step_launches(wl, input_grad=False):
     """(kernel name, algorithmic bytes) of every launch of one step of the FDCNN chain
     (one rfft2, every FDC + FDP layer on spectra, one irfft2, and the backward)."""
@@ -179,15 +191,12 @@ def chain_step_launches(wl, input_grad=False):
     NF0 = N0 // 2 + 1
     ML, CL = wl.sizes[-1], wl.channels[-1]
     MFL = ML // 2 + 1
-    out.append((f"row_r2c_{N0}", F32 * B * C0 * N0 * N0 + C64 * B * C0 * N0 * NF0))
-    out.append((f"col_fft_fwd_{N0}", 2 * C64 * B * C0 * N0 * NF0))
+    out += fft2_launches(N0, B * C0, inverse=False)
     for i in range(n):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
         out.append(("cic_fdp_fwd", C64 * (B * C * M * L + S * M * L + B * S * M * L)))
-    out.append((f"col_fft_inv_{ML}", 2 * C64 * B * CL * ML * MFL))
-    out.append((f"row_c2r_{ML}", C64 * B * CL * ML * MFL + F32 * B * CL * ML * ML))
-    out.append((f"row_r2c_{ML}", F32 * B * CL * ML * ML + C64 * B * CL * ML * MFL))
-    out.append((f"col_fft_fwd_{ML}", 2 * C64 * B * CL * ML * MFL))
+    out += fft2_launches(ML, B * CL, inverse=True)
+    out += fft2_launches(ML, B * CL, inverse=False)  # the irfft2 adjoint has the forward's launches
     for i in reversed(range(n)):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
         if i > 0 or input_grad:
@@ -195,8 +204,7 @@ def chain_step_launches(wl, input_grad=False):
             out.append(("cic_fdp_bwd_gx", C64 * (B * S * M * L + S * M * L + B * C * N * NF)))
         out.append(("cic_fdp_bwd_gk", C64 * (B * S * M * L + B * C * M * L + S * N * NF)))
     if input_grad:
-        out.append((f"col_fft_inv_{N0}", 2 * C64 * B * C0 * N0 * NF0))
-        out.append((f"row_c2r_{N0}", C64 * B * C0 * N0 * NF0 + F32 * B * C0 * N0 * N0))
+        out += fft2_launches(N0, B * C0, inverse=True)
     return out
 
 
@@ -205,7 +213,9 @@ def classifier_step_launches(wl, classes, n_params):
     (ReLU + fully connected layer, then the loss), the head backward, the chain backward
     (no input gradient), and the Adam update of every parameter (plus its step count)."""
     chain = chain_step_launches(wl, False)
-    n_fwd = 2 + wl.layers + 2  # rfft2 (rows, columns), the layers, irfft2 (columns, rows)
+    # rfft2, the layers, irfft2
+    n_fwd = (len(fft2_launches(wl.sizes[0], 1, False)) + wl.layers +
+             len(fft2_launches(wl.sizes[-1], 1, True)))
     B, F = wl.batch, wl.channels[-1] * wl.sizes[-1] ** 2
     chunks = -(-F // 1024)
     head = [

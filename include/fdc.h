@@ -132,12 +132,13 @@ fdc_status fdc_cic_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *
 /* One FDC layer of the FDCNN on spectra (section 2.5.1: the network transforms once,
  * before its first layer, and inverts once after its last): CIC (Eq. 5) followed by
  * FDP to M x M, forming only the bins FDP keeps.  X [B][C][N][N/2+1], K [S][N][N/2+1]
- * -> Y [B][S][M][M/2+1]; S mod C == 0, N and M even, M <= N. */
+ * -> Y [B][S][M][M/2+1]; S mod C == 0, N and M even, M <= N.  Y must be 16-byte
+ * aligned (torch allocations are): each thread stores two bins at once. */
 fdc_status fdc_cic_fdp_forward(const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *Y, int B, int C, int S, int N, int M,
                                hipStream_t stream);
 /* gY [B][S][M][M/2+1] -> gX [B][C][N][N/2+1] (NULL: skipped) and gK [S][N][N/2+1]
  * (NULL: skipped; summed over the batch in order), both with exact zeros at the bins
- * FDP drops. */
+ * FDP drops.  gX must be 16-byte aligned. */
 fdc_status fdc_cic_fdp_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX, fdc_c64 *gK,
                                 int B, int C, int S, int N, int M, hipStream_t stream);
 

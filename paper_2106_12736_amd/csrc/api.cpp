@@ -39,6 +39,7 @@ fdc_status check_hip(hipError_t e, const char *what) {
 bool even_pos(long long v) { return v > 0 && v % 2 == 0; }
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 constexpr uint32_t kFftMagic = 0xFDC0FF70u;
 constexpr uint32_t kLayerMagic = 0xFDC01A7Eu;
@@ -217,6 +218,8 @@ fdc_status fdc_rfft2(const fdc_fft_plan *p, const float *x, fdc_c64 *X, void *, 
   const int h = p->h, w = p->w, wf = w / 2 + 1;
   ImgView id{0, 0, h, w};
   auto *out = reinterpret_cast<float2 *>(X);
+  if (fdc::fft2_small_supported(h, w))
+    return check_hip(fdc::launch_fft2_small(h, false, x, out, nullptr, nullptr, p->count, 1.f, 1.f, s), "rfft2");
   if (fdc_status st = check_hip(fdc::launch_row_r2c(w, x, fdc::plain_layout(out, h, wf), p->count, h, id,
                                                     (long long)h * w, wf, 1.f, 1.f, s), "rfft2 rows"))
     return st;
@@ -230,6 +233,9 @@ static fdc_status inverse_like(const fdc_fft_plan *p, const fdc_c64 *X, float *x
   if (!x || !X) return fail(FDC_EINVAL, "NULL tensor");
   if (fdc_status st = check_ws(ws, ws_bytes, fft_spec_bytes(p))) return st;
   const int h = p->h, w = p->w, wf = w / 2 + 1;
+  if (fdc::fft2_small_supported(h, w))
+    return check_hip(fdc::launch_fft2_small(h, true, nullptr, nullptr, x, reinterpret_cast<const float2 *>(X),
+                                            p->count, alpha, beta, s), what);
   auto *tmp = reinterpret_cast<float2 *>(ws);
   if (fdc_status st = check_hip(fdc::launch_col_fft(h, +1, reinterpret_cast<const float2 *>(X), tmp, p->count, wf,
                                                     wf, (long long)h * wf, (long long)h * wf, s), what))
@@ -257,6 +263,9 @@ fdc_status fdc_irfft2_backward(const fdc_fft_plan *p, const float *gx, fdc_c64 *
   const int h = p->h, w = p->w, wf = w / 2 + 1;
   ImgView id{0, 0, h, w};
   auto *out = reinterpret_cast<float2 *>(gX);
+  if (fdc::fft2_small_supported(h, w))
+    return check_hip(fdc::launch_fft2_small(h, false, gx, out, nullptr, nullptr, p->count,
+                                            1.f / ((float)h * (float)w), 2.f, s), "irfft2_backward");
   if (fdc_status st = check_hip(fdc::launch_row_r2c(w, gx, fdc::plain_layout(out, h, wf), p->count, h, id,
                                                     (long long)h * w, wf, 1.f / ((float)h * (float)w), 2.f, s),
                                 "irfft2_backward rows"))
@@ -318,6 +327,7 @@ fdc_status fdc_cic_fdp_forward(const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *Y, i
                                hipStream_t s) {
   if (fdc_status st = check_cic_fdp(B, C, S, N, M)) return st;
   if (!X || !K || !Y) return fail(FDC_EINVAL, "NULL tensor");
+  if (!aligned16(Y)) return fail(FDC_EINVAL, "Y must be 16-byte aligned");
   return check_hip(fdc::launch_cic_fdp_fwd(reinterpret_cast<const float2 *>(X), reinterpret_cast<const float2 *>(K),
                                            reinterpret_cast<float2 *>(Y), B, C, S, N, M, s),
                    "cic_fdp_forward");
@@ -327,6 +337,7 @@ fdc_status fdc_cic_fdp_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c
                                 int B, int C, int S, int N, int M, hipStream_t s) {
   if (fdc_status st = check_cic_fdp(B, C, S, N, M)) return st;
   if (!gY || (gX && !K) || (gK && !X)) return fail(FDC_EINVAL, "NULL tensor");
+  if (gX && !aligned16(gX)) return fail(FDC_EINVAL, "gX must be 16-byte aligned");
   if (gX) {
     if (fdc_status st = check_hip(fdc::launch_cic_fdp_bwd_gx(reinterpret_cast<const float2 *>(gY),
                                                              reinterpret_cast<const float2 *>(K),

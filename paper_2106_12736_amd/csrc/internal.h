@@ -157,6 +157,12 @@ hipError_t launch_col_bwd_dk_dx(int n, int m, const float2 *Tg, const float2 *Xh
 //        (per-image dK products; launch_gk_reduce sums them); out_mode 0: Tg split
 //        [B C][na][na/2+1] with weights (c_l a_out); 1: gx [B][C][na][na]; 2: none.
 bool tail_supported(int na, int ma, int mb, int ja, int jb);
+// Whole 2-D transforms of small square planes in one launch (tail.hip): forward
+// x [count][n][n] -> X [count][n][n/2+1] with row weights (alpha, beta), or inverse
+// Xi -> xo with c-weights (alpha, beta) and real-part semantics.
+bool fft2_small_supported(int h, int w);
+hipError_t launch_fft2_small(int n, bool inverse, const float *x, float2 *X, float *xo, const float2 *Xi,
+                             long long count, float alpha, float beta, hipStream_t s);
 hipError_t launch_tail_fwd(int na, int ma, int mb, int ja, int jb, SpecLayout in, const float *x, float a_in,
                            const float2 *Ka, const float2 *Kb, SpecLayout saved_a, SpecLayout saved_b, float *y,
                            int B, int C, hipStream_t s);

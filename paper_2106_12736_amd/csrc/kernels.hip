@@ -777,50 +777,58 @@ __global__ __launch_bounds__(CT *ColCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
 }
 
 // gK [S][N][N/2+1] from BG partial sums part [BG][S][M][M/2+1] (plain layout), for
-// one or two reductions (grid.y selects the GkSum): a wavefront per gK row, its
-// lanes along the row; the partial sums added in order at the kept bins, exact
-// zeros elsewhere.
+// one or two reductions (grid.y selects the GkSum): a thread per gK element, its BG
+// partial sums loaded together (16 at a time) and added in order at the kept bins,
+// exact zeros elsewhere.  Consecutive threads take consecutive bins of a row.
 struct GkSum {
   const float2 *part;
   float2 *gK;
   int BG, S, M, N;
 };
 
-__global__ __launch_bounds__(256) void k_gk_reduce(GkSum d0, GkSum d1) {
+constexpr int kGkReduceThreads = 256;
+
+__global__ __launch_bounds__(kGkReduceThreads) void k_gk_reduce(GkSum d0, GkSum d1) {
   const GkSum d = blockIdx.y == 0 ? d0 : d1;
-  const int L = d.M / 2 + 1, nf = d.N / 2 + 1, lane = threadIdx.x & 63;
-  const long long rows = (long long)d.S * d.N;
+  const int L = d.M / 2 + 1, nf = d.N / 2 + 1;
+  // 32-bit element arithmetic: the launchers keep S * N * (N/2+1) below 2^31
+  const unsigned total = (unsigned)(d.S * d.N * nf);
   const long long range_stride = (long long)d.S * d.M * L;
-  for (long long r = (long long)blockIdx.x * 4 + (threadIdx.x >> 6); r < rows; r += (long long)gridDim.x * 4) {
-    const int o = (int)(r / d.N), krow = (int)(r - (long long)o * d.N);
+  for (unsigned i = blockIdx.x * kGkReduceThreads + threadIdx.x; i < total; i += gridDim.x * kGkReduceThreads) {
+    const int r = (int)(i / (unsigned)nf), l = (int)i - r * nf;
+    const int o = r / d.N, krow = r - o * d.N;
     const int mrow = krow < d.M / 2 ? krow : (krow >= d.N - d.M / 2 ? krow - (d.N - d.M) : -1);
-    float2 *dst = d.gK + r * nf;
-    const float2 *src = d.part + ((long long)o * d.M + (mrow < 0 ? 0 : mrow)) * L;
-    for (int l = lane; l < nf; l += 64) {
-      float2 v = make_float2(0.f, 0.f);
-      if (mrow >= 0 && l < L) {
-        int q = 0;
-        for (; q + 8 <= d.BG; q += 8) {  // eight loads in flight, then added in order
-          float2 a[8];
+    float2 v = make_float2(0.f, 0.f);
+    if (mrow >= 0 && l < L) {
+      const float2 *src = d.part + ((long long)o * d.M + mrow) * L + l;
+      int q = 0;
+      for (; q + 16 <= d.BG; q += 16) {
+        float2 a[16];
 #pragma unroll
-          for (int i = 0; i < 8; ++i) a[i] = src[(q + i) * range_stride + l];
+        for (int u = 0; u < 16; ++u) a[u] = src[(q + u) * range_stride];
 #pragma unroll
-          for (int i = 0; i < 8; ++i) v = cadd(v, a[i]);
-        }
-        for (; q < d.BG; ++q) v = cadd(v, src[q * range_stride + l]);
+        for (int u = 0; u < 16; ++u) v = cadd(v, a[u]);
       }
-      dst[l] = v;
+      for (; q + 4 <= d.BG; q += 4) {
+        float2 a[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) a[u] = src[(q + u) * range_stride];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v = cadd(v, a[u]);
+      }
+      for (; q < d.BG; ++q) v = cadd(v, src[q * range_stride]);
     }
+    d.gK[i] = v;
   }
 }
 
 static hipError_t gk_reduce(const GkSum &d0, const GkSum *d1, hipStream_t s) {
-  long long rows = (long long)d0.S * d0.N;
-  if (d1) rows = std::max(rows, (long long)d1->S * d1->N);
-  const unsigned gx = (unsigned)std::min<long long>((rows + 3) / 4, 4096);
+  long long total = (long long)d0.S * d0.N * (d0.N / 2 + 1);
+  if (d1) total = std::max(total, (long long)d1->S * d1->N * (d1->N / 2 + 1));
+  const unsigned gx = (unsigned)std::min<long long>((total + kGkReduceThreads - 1) / kGkReduceThreads, 1 << 16);
   const char *nm = "gk_reduce";
   timing_before(nm, s);
-  hipLaunchKernelGGL(k_gk_reduce, dim3(gx, d1 ? 2 : 1), dim3(256), 0, s, d0, d1 ? *d1 : d0);
+  hipLaunchKernelGGL(k_gk_reduce, dim3(gx, d1 ? 2 : 1), dim3(kGkReduceThreads), 0, s, d0, d1 ? *d1 : d0);
   const hipError_t e = hipGetLastError();
   timing_after(nm, s);
   return e;
@@ -1403,59 +1411,117 @@ __device__ __forceinline__ int div_small(int e, int d, float rd, int &rem) {
   return q;
 }
 
+// k_cic_fdp_fwd and k_cic_fdp_bwd_gx give each thread two consecutive bins (e0,
+// e0 + 1), e0 even, of the plane they write: a plane holds an even number of bins (its
+// row count is even), so the pair is one 16-byte store (the launchers check that the
+// output is 16-byte aligned); the pair may straddle two rows, and inputs are read bin
+// by bin.  (Two bins per lane also for the loads, as 8-byte-aligned 16-byte loads, is
+// slower on gfx950; so is this layout for k_cic_fdp_bwd_gk, whose main stream is its
+// loads.)
+struct BinPair {
+  int k[2], l[2];  // row and column of the two bins in a plane of rows x cols
+  __device__ BinPair(int e0, int cols, float rcols) {
+    k[0] = div_small(e0, cols, rcols, l[0]);
+    k[1] = k[0], l[1] = l[0] + 1;
+    if (l[1] == cols) k[1] += 1, l[1] = 0;
+  }
+};
+
+__device__ __forceinline__ float4 pack2(float2 a, float2 b) { return make_float4(a.x, a.y, b.x, b.y); }
+
+// images whose loads a thread has in flight at once
+constexpr int kChainImages = 8;
+
 // FDC layer of the FDCNN on spectra (Eq. 5, Algorithm 1) followed by FDP, forming only
 // the bins FDP keeps: Y [B][S][M][M/2+1] from X [B][C][N][N/2+1], K [S][N][N/2+1].
 // Kept rows of the N-point spectrum: k < M/2 and k >= N - M/2 (output row k or
-// k - (N - M)); kept columns l <= M/2.  Grid: x over an output plane's elements in
-// order (contiguous stores), y over the output channels; a thread loads its kernel
-// bin once and forms that bin for every image.
+// k - (N - M)); kept columns l <= M/2.  Grid: x over an output plane's bin pairs in
+// order (contiguous stores), y over the output channels; a thread loads its two kernel
+// bins once and forms them for every image.
 __global__ __launch_bounds__(256) void k_cic_fdp_fwd(const float2 *__restrict__ X, const float2 *__restrict__ K,
                                                      float2 *__restrict__ Y, int B, int C, int J, int N, int M) {
   const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1, pe = M * Lm;
-  const float rl = 1.f / (float)Lm;
-  const int e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= pe) return;
-  int l;
-  const int k = div_small(e, Lm, rl, l);
-  const int kr = k < M / 2 ? k : k + (N - M);
+  const int e0 = 2 * (blockIdx.x * 256 + threadIdx.x);
+  if (e0 >= pe) return;
+  const BinPair q(e0, Lm, 1.f / (float)Lm);
+  int off[2];  // bin offsets in an N-plane
+#pragma unroll
+  for (int h = 0; h < 2; ++h) off[h] = (q.k[h] < M / 2 ? q.k[h] : q.k[h] + (N - M)) * NF + q.l[h];
+  const long long xs = (long long)C * N * NF, ys = (long long)S * (pe / 2);  // image strides (float2, float4)
   for (int o = blockIdx.y; o < S; o += gridDim.y) {
-    const float2 kv = K[((long long)o * N + kr) * NF + l];
-    const float2 *xp = X + ((long long)(o / J) * N + kr) * NF + l;
-    float2 *yp = Y + (long long)o * pe + e;
-#pragma unroll 4
-    for (int b = 0; b < B; ++b) yp[(long long)b * S * pe] = cmul(xp[(long long)b * C * N * NF], kv);
+    const float2 *ko = K + (long long)o * N * NF;
+    const float2 kv0 = ko[off[0]], kv1 = ko[off[1]];
+    const float2 *xo = X + (long long)(o / J) * N * NF;
+    float4 *yo = reinterpret_cast<float4 *>(Y + (long long)o * pe + e0);
+    int b = 0;
+    for (; b + kChainImages <= B; b += kChainImages) {
+      float2 a0[kChainImages], a1[kChainImages];
+#pragma unroll
+      for (int u = 0; u < kChainImages; ++u) {
+        a0[u] = xo[(b + u) * xs + off[0]];
+        a1[u] = xo[(b + u) * xs + off[1]];
+      }
+#pragma unroll
+      for (int u = 0; u < kChainImages; ++u) yo[(b + u) * ys] = pack2(cmul(a0[u], kv0), cmul(a1[u], kv1));
+    }
+    for (; b < B; ++b) yo[b * ys] = pack2(cmul(xo[b * xs + off[0]], kv0), cmul(xo[b * xs + off[1]], kv1));
   }
 }
 
-// Backward of k_cic_fdp_fwd: gX [B][C][N][N/2+1] = sum_j gY conj(K) at the kept bins,
-// exact zeros at the bins FDP drops.  Grid: x over a plane's elements, y over the
-// input channels; a thread forms its bin for every image.
+// Backward of k_cic_fdp_fwd: gX [B][C][N][N/2+1] = sum_j gY conj(K) at the kept bins
+// (j in order), exact zeros at the bins FDP drops.  Grid: x over a plane's bin pairs,
+// y over the input channels; a thread forms its two bins for every image, four images
+// at a time.
 __global__ __launch_bounds__(256) void k_cic_fdp_bwd_gx(const float2 *__restrict__ gY, const float2 *__restrict__ K,
                                                         float2 *__restrict__ gX, int B, int C, int J, int N, int M) {
+  constexpr int BI = 4;
   const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1, pe = N * NF;
-  const float rn = 1.f / (float)NF;
-  const int e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= pe) return;
-  int l;
-  const int kr = div_small(e, NF, rn, l);
-  const bool kept = l < Lm && (kr < M / 2 || kr >= N - M / 2);
-  const int k = kr < M / 2 ? kr : kr - (N - M);
-  const long long mpe = (long long)M * Lm;
+  const int e0 = 2 * (blockIdx.x * 256 + threadIdx.x);
+  if (e0 >= pe) return;
+  const BinPair q(e0, NF, 1.f / (float)NF);
+  bool kept[2];
+  int koff[2], yoff[2];  // bin offsets in an N-plane (K) and in an M-plane (gY)
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int kr = q.k[h], l = q.l[h];
+    kept[h] = l < Lm && (kr < M / 2 || kr >= N - M / 2);
+    const int k = kr < M / 2 ? kr : kr - (N - M);
+    koff[h] = kept[h] ? kr * NF + l : 0;  // a dropped bin reads bin 0 and is not used
+    yoff[h] = kept[h] ? k * Lm + l : 0;
+  }
+  const long long mpe = (long long)M * Lm, ys = (long long)S * mpe, xs = (long long)C * (pe / 2);
+  const long long kps = (long long)N * NF;
   for (int c = blockIdx.y; c < C; c += gridDim.y) {
-    float2 *gp = gX + (long long)c * pe + e;
-    if (!kept) {
-#pragma unroll 4
-      for (int b = 0; b < B; ++b) gp[(long long)b * C * pe] = make_float2(0.f, 0.f);
+    float4 *gp = reinterpret_cast<float4 *>(gX + (long long)c * pe + e0);
+    if (!kept[0] && !kept[1]) {
+      for (int b = 0; b < B; ++b) gp[b * xs] = make_float4(0.f, 0.f, 0.f, 0.f);
       continue;
     }
-    const float2 *kp = K + ((long long)c * J * N + kr) * NF + l;  // K[cJ + j] at j * N * NF
-    const float2 *yp = gY + (long long)c * J * mpe + (long long)k * Lm + l;  // gY[b][cJ + j]
-#pragma unroll 2
-    for (int b = 0; b < B; ++b) {
-      float2 acc = make_float2(0.f, 0.f);
-      for (int j = 0; j < J; ++j)
-        acc = cfmac(acc, yp[((long long)b * S + j) * mpe], kp[(long long)j * N * NF]);
-      gp[(long long)b * C * pe] = acc;
+    const float2 *kp = K + (long long)c * J * kps;   // K[cJ + j] at j * N * NF
+    const float2 *yp = gY + (long long)c * J * mpe;  // gY[b][cJ + j] at b * S * mpe + j * mpe
+    for (int b0 = 0; b0 < B; b0 += BI) {
+      float2 a0[BI], a1[BI];
+#pragma unroll
+      for (int u = 0; u < BI; ++u) a0[u] = a1[u] = make_float2(0.f, 0.f);
+      for (int j = 0; j < J; ++j) {
+        const float2 k0 = kp[j * kps + koff[0]], k1 = kp[j * kps + koff[1]];
+        float2 g0[BI], g1[BI];
+#pragma unroll
+        for (int u = 0; u < BI; ++u) {
+          const long long bo = (long long)min(b0 + u, B - 1) * ys + j * mpe;  // images past the end: not stored
+          g0[u] = yp[bo + yoff[0]];
+          g1[u] = yp[bo + yoff[1]];
+        }
+#pragma unroll
+        for (int u = 0; u < BI; ++u) {
+          a0[u] = cfmac(a0[u], g0[u], k0);
+          a1[u] = cfmac(a1[u], g1[u], k1);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < BI; ++u)
+        if (b0 + u < B)
+          gp[(b0 + u) * xs] = pack2(kept[0] ? a0[u] : make_float2(0.f, 0.f), kept[1] ? a1[u] : make_float2(0.f, 0.f));
     }
   }
 }
@@ -1493,7 +1559,7 @@ hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B
                               hipStream_t s) {
   if ((long long)N * (N / 2 + 1) >= (1 << 24)) return hipErrorInvalidValue;
   timing_before("cic_fdp_fwd", s);
-  hipLaunchKernelGGL(k_cic_fdp_fwd, plane_grid((long long)M * (M / 2 + 1), S), dim3(256), 0, s, X, K, Y, B, C, S / C,
+  hipLaunchKernelGGL(k_cic_fdp_fwd, plane_grid((long long)M * (M / 2 + 1) / 2, S), dim3(256), 0, s, X, K, Y, B, C, S / C,
                      N, M);
   const hipError_t e = hipGetLastError();
   timing_after("cic_fdp_fwd", s);
@@ -1504,7 +1570,7 @@ hipError_t launch_cic_fdp_bwd_gx(const float2 *gY, const float2 *K, float2 *gX, 
                                  hipStream_t s) {
   if ((long long)N * (N / 2 + 1) >= (1 << 24)) return hipErrorInvalidValue;
   timing_before("cic_fdp_bwd_gx", s);
-  hipLaunchKernelGGL(k_cic_fdp_bwd_gx, plane_grid((long long)N * (N / 2 + 1), C), dim3(256), 0, s, gY, K, gX, B, C,
+  hipLaunchKernelGGL(k_cic_fdp_bwd_gx, plane_grid((long long)N * (N / 2 + 1) / 2, C), dim3(256), 0, s, gY, K, gX, B, C,
                      S / C, N, M);
   const hipError_t e = hipGetLastError();
   timing_after("cic_fdp_bwd_gx", s);

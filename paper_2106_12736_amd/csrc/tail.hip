@@ -583,6 +583,107 @@ __global__ __launch_bounds__(NT) void k_tail_bwd(const float *__restrict__ gy, S
 }
 
 // ----------------------------------------------------------------------------
+// Whole 2-D transforms of small square planes (N <= 64), P planes per workgroup:
+// the row pass and the column pass of section 2.4.1.1 meet in LDS, so a transform
+// is one launch.  Spectra use the plain layout [planes][N][N/2+1].
+//   forward: X = rows (weights a2 at l = 0 and N/2, a2 b2 elsewhere) then columns;
+//   inverse: columns, then rows with the c-weights a1 (l = 0, N/2) and a1 b1 and
+//            real-part semantics, the layout and weights of the row kernels.
+// ----------------------------------------------------------------------------
+template <int N, int P>
+struct Small2d {
+  static constexpr int L = N / 2 + 1, ld = plane_ld(L), NT = 256;
+  static constexpr int TW = twiddle_lds_elems<N>(), PL = TW, SCR = PL + P * N * ld;
+  static constexpr int END = SCR + row_scratch<N, NT>(P * N / 2);
+};
+
+template <int N, int P>
+__global__ __launch_bounds__(256) void k_fft2_small_fwd(const float *__restrict__ x, float2 *__restrict__ X,
+                                                        long long count, float a2, float b2) {
+  using G = Small2d<N, P>;
+  constexpr int L = G::L, ld = G::ld, NT = G::NT, TPS = Plan<N>::TPS, E = Plan<N>::E;
+  float2 *tw = t_lds, *pl = t_lds + G::PL, *scr = t_lds + G::SCR;
+  stage_twiddles<N>(tw, threadIdx.x, NT);
+  const long long q0 = (long long)xcd_remap(blockIdx.x, gridDim.x) * P;
+  const int np = (int)(count - q0 < P ? count - q0 : P);
+  {  // rows: pairs of real rows packed as one complex sequence -> planes [N][ld]
+    constexpr int SEQ = NT / TPS, H = N / 2;
+    const RowLanes<N> ln;
+    for (int r0 = 0; r0 + ln.first < np * H; r0 += SEQ) {
+      const int it = r0 + ln.first + ln.s;
+      const bool act = it < np * H;
+      const int q = act ? it / H : 0, r = 2 * (act ? it % H : 0);
+      const float *xr = x + ((q0 + q) * N + r) * N;
+      float2 v[E];
+#pragma unroll
+      for (int m = 0; m < E; ++m) v[m] = make_float2(xr[ln.t + TPS * m], xr[N + ln.t + TPS * m]);
+      fft_seq<N, -1, true, true, kLdsPad, Plan<N>>(v, ln.t, scr, (ln.first + ln.s) * N, 1, tw, 1);
+      float2 *dst = pl + (q * N + r) * ld;
+      r2c_out<N, L>(v, scr, ln.first + ln.s, ln.t, a2, b2, [&](int rr, int k, float2 val) {
+        if (act) dst[rr * ld + k] = val;
+      });
+    }
+  }
+  __syncthreads();
+  col_pass<N, -1, NT>(
+      np, L, tw, 1,
+      [&](float2 (&v)[E], int q, int l, int t, bool) {
+#pragma unroll
+        for (int m = 0; m < E; ++m) v[m] = pl[(q * N + t + TPS * m) * ld + l];
+      },
+      [&](int q) { return pl + q * N * ld; },
+      [&](const float2 (&v)[E], int q, int l, int t, bool act) {
+        if (!act) return;
+        float2 *o = X + (q0 + q) * N * L + l;
+#pragma unroll
+        for (int m = 0; m < E; ++m) o[(t + TPS * m) * L] = v[m];
+      });
+}
+
+template <int N, int P>
+__global__ __launch_bounds__(256) void k_fft2_small_inv(const float2 *__restrict__ X, float *__restrict__ x,
+                                                        long long count, float a1, float b1) {
+  using G = Small2d<N, P>;
+  constexpr int L = G::L, ld = G::ld, NT = G::NT, TPS = Plan<N>::TPS, E = Plan<N>::E;
+  float2 *tw = t_lds, *pl = t_lds + G::PL, *scr = t_lds + G::SCR;
+  stage_twiddles<N>(tw, threadIdx.x, NT);
+  const long long q0 = (long long)xcd_remap(blockIdx.x, gridDim.x) * P;
+  const int np = (int)(count - q0 < P ? count - q0 : P);
+  col_pass<N, +1, NT>(
+      np, L, tw, 1,
+      [&](float2 (&v)[E], int q, int l, int t, bool act) {
+        const float2 *c = X + (q0 + q) * N * L + (act ? l : 0);  // idle lanes read a valid column
+#pragma unroll
+        for (int m = 0; m < E; ++m) v[m] = c[(t + TPS * m) * L];
+      },
+      [&](int q) { return pl + q * N * ld; },
+      [&](const float2 (&v)[E], int q, int l, int t, bool act) {
+        if (!act) return;
+#pragma unroll
+        for (int m = 0; m < E; ++m) pl[(q * N + t + TPS * m) * ld + l] = v[m];
+      });
+  __syncthreads();
+  {  // rows: inverse of pairs of rows packed as one complex sequence -> real rows
+    constexpr int SEQ = NT / TPS, H = N / 2;
+    const RowLanes<N> ln;
+    for (int r0 = 0; r0 + ln.first < np * H; r0 += SEQ) {
+      const int it = r0 + ln.first + ln.s;
+      const bool act = it < np * H;
+      const int q = act ? it / H : 0, r = 2 * (act ? it % H : 0);
+      const float2 *src = pl + (q * N + r) * ld;
+      float2 v[E];
+      c2r_in<N, L>(v, [&](int rr, int k) { return src[rr * ld + k]; }, ln.t, a1, b1);
+      fft_seq<N, +1, true, true, kLdsPad, Plan<N>>(v, ln.t, scr, (ln.first + ln.s) * N, 1, tw, 1);
+      if (act) {
+        float *xr = x + ((q0 + q) * N + r) * N;
+#pragma unroll
+        for (int m = 0; m < E; ++m) xr[ln.t + TPS * m] = v[m].x, xr[N + ln.t + TPS * m] = v[m].y;
+      }
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------
 // host side
 // ----------------------------------------------------------------------------
 #ifndef FDC_TAIL_THREADS
@@ -688,6 +789,59 @@ hipError_t launch_tail_bwd(int na, int ma, int mb, int ja, int jb, const float *
       case 1: go(std::integral_constant<int, 1>{}); break;
       default: go(std::integral_constant<int, 2>{});
     }
+  });
+  return err;
+}
+
+// Small square 2-D transforms: N in {16, 32, 64}; P planes per workgroup, chosen so
+// that a launch has at least about 512 workgroups when the batch allows it.
+template <class F>
+static bool dispatch_small2d(int n, long long count, F &&f) {
+  auto with_p = [&](auto nc) {
+    if (count >= 2048)
+      f(nc, std::integral_constant<int, 4>{});
+    else if (count >= 1024)
+      f(nc, std::integral_constant<int, 2>{});
+    else
+      f(nc, std::integral_constant<int, 1>{});
+  };
+  switch (n) {
+    case 16: with_p(std::integral_constant<int, 16>{}); return true;
+    case 32: with_p(std::integral_constant<int, 32>{}); return true;
+    case 64: with_p(std::integral_constant<int, 64>{}); return true;
+    default: return false;
+  }
+}
+
+bool fft2_small_supported(int h, int w) { return h == w && (h == 16 || h == 32 || h == 64); }
+
+template <auto Kern, class... Args>
+static hipError_t small2d_launch(const char *name, unsigned grid, size_t lds, hipStream_t s, Args... args) {
+  hipError_t e = allow_lds<Kern>(lds);
+  if (e != hipSuccess) return e;
+  const auto kern = Kern;
+  timing_before(name, s);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, s, args...);
+  e = hipGetLastError();
+  timing_after(name, s);
+  return e;
+}
+
+hipError_t launch_fft2_small(int n, bool inverse, const float *x, float2 *X, float *xo, const float2 *Xi,
+                             long long count, float alpha, float beta, hipStream_t s) {
+  hipError_t err = hipErrorInvalidValue;
+  dispatch_small2d(n, count, [&](auto nc, auto pc) {
+    constexpr int N = decltype(nc)::value, P = decltype(pc)::value;
+    constexpr size_t lds = (size_t)Small2d<N, P>::END * sizeof(float2);
+    static_assert(lds <= 160 * 1024, "small 2-D transform: LDS");
+    const long long grid = (count + P - 1) / P;
+    if (count < 1 || grid >= (1LL << 31)) return;
+    static const std::string fw = "fft2_small_fwd_" + std::to_string(N);
+    static const std::string iv = "fft2_small_inv_" + std::to_string(N);
+    if (inverse)
+      err = small2d_launch<k_fft2_small_inv<N, P>>(iv.c_str(), (unsigned)grid, lds, s, Xi, xo, count, alpha, beta);
+    else
+      err = small2d_launch<k_fft2_small_fwd<N, P>>(fw.c_str(), (unsigned)grid, lds, s, x, X, count, alpha, beta);
   });
   return err;
 }

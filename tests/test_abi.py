@@ -316,6 +316,9 @@ def test_cic_fdp_validation():
     assert _lib.status("fdc_cic_fdp_backward", d, None, d, None, d, 2, 1, 4, 8, 4, None) == FDC_EINVAL  # gK needs X
     assert _lib.status("fdc_cic_fdp_backward", d, d, None, d, None, 2, 1, 4, 8, 4, None) == FDC_EINVAL  # gX needs K
     assert _lib.status("fdc_cic_fdp_backward", d, d, d, None, None, 2, 1, 4, 8, 4, None) == FDC_OK     # nothing asked
+    m = ctypes.c_void_p(0x1008)  # 8- but not 16-byte aligned output
+    assert _lib.status("fdc_cic_fdp_forward", d, d, m, 2, 1, 4, 8, 4, None) == FDC_EINVAL
+    assert _lib.status("fdc_cic_fdp_backward", d, d, d, m, None, 2, 1, 4, 8, 4, None) == FDC_EINVAL
 
 
 def test_dk_ranges_queries():

@@ -25,6 +25,8 @@ def _c64(rng, shape):
 
 @pytest.mark.parametrize("B,C,S,N,M", [
     (1, 1, 1, 4, 2), (2, 1, 4, 8, 4), (3, 2, 6, 16, 16), (2, 4, 4, 32, 8), (1, 3, 9, 64, 32), (2, 2, 4, 224, 112),
+    # batches past one group of in-flight images, with a ragged rest; odd row lengths
+    (11, 2, 4, 16, 8), (9, 1, 8, 32, 16), (17, 3, 3, 8, 8),
 ])
 def test_cic_fdp_op(B, C, S, N, M):
     rng = _rng("cic_fdp", B, C, S, N, M)

@@ -49,6 +49,23 @@ def test_fft_plan_forward_inverse_and_adjoints(h, w):
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("n,count", [(16, 2051), (32, 1029), (32, 1), (64, 2050), (64, 1027)])
+def test_fft_small_planes_many_per_workgroup(n, count):
+    # square planes up to 64 x 64 take one launch per transform with 1, 2 or 4 planes per
+    # workgroup (by batch size); ragged counts leave a partly filled last workgroup
+    print(f"fft small {n} x {count}", flush=True)
+    rng = _rng("fft_small", n, count)
+    plan = layers.FftPlan(count, n, n)
+    x = rng.standard_normal((count, n, n)).astype(np.float32)
+    Y = _crand(rng, (count, n, n // 2 + 1))
+    x64, Y128 = x.astype(np.float64), Y.astype(np.complex128)
+    assert_parity(to_np(plan.rfft2(_gpu(x))), dft.rfft2(x64), "rfft2")
+    assert_parity(to_np(plan.irfft2(_gpu(Y))), dft.irfft2(Y128, n, n), "irfft2")
+    assert_parity(to_np(plan.rfft2_backward(_gpu(Y))), dft.rfft2_adjoint(Y128, n, n), "rfft2_backward")
+    assert_parity(to_np(plan.irfft2_backward(_gpu(x))), dft.irfft2_adjoint(x64), "irfft2_backward")
+    torch.cuda.synchronize()
+
+
 def test_fft_structured_inputs():
     # impulse, constant and a single cosine through the 1024 x 1024 plan
     h = w = 1024
