@@ -124,13 +124,16 @@ def fused_step_launches(wl, input_grad=False, ranges=None, tail=-1):
     layer's forward rows (and the backward's adjoint pair) in one kernel, a layer's
     dK and dX columns in one launch when dK uses one batch range, and the last two
     layers in the LDS-resident tail kernels from layer `tail` on (-1: none)."""
-    ranges = ranges or [1] * wl.layers
+    return fused_fwd_launches(wl, tail) + fused_bwd_launches(wl, input_grad, ranges, tail)
+
+
+def fused_fwd_launches(wl, tail=-1):
     out = []
     n = wl.layers
     for i in range(n):
         B, C, S, N, M, L, _ = layer_dims(wl, i)
         if i == tail:
-            out.append(tail_launches(wl, tail, input_grad)[0])
+            out.append(tail_launches(wl, tail, False)[0])
             break
         if i == 0:
             out.append((f"row_r2c_{N}", F32 * B * C * N * N + C64 * B * C * N * L))
@@ -142,6 +145,13 @@ def fused_step_launches(wl, input_grad=False, ranges=None, tail=-1):
             out.append((f"row_c2r_r2c_{M}", C64 * B * S * M * L + C64 * B * S * N2 * L2))
         else:
             out.append((f"row_c2r_{M}", C64 * B * S * M * L + F32 * B * S * M * M))
+    return out
+
+
+def fused_bwd_launches(wl, input_grad=False, ranges=None, tail=-1):
+    ranges = ranges or [1] * wl.layers
+    out = []
+    n = wl.layers
     for i in reversed(range(n)):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
         if tail >= 0 and i >= tail:
@@ -251,6 +261,24 @@ def spatial_step_launches(wl, n, input_grad=False, ranges=None):
         out.append(("cic_wgrad", C64 * S * M * L))
         out.append(("cic_wgrad_reduce", F32 * S * n * n))
     return out
+
+
+def spatial_fused_step_launches(wl, n, input_grad=False, ranges=None, tail=-1):
+    """(kernel name, algorithmic bytes) of every launch of one step of the stack with
+    n x n spatial kernels through the stack executor (fdc_cic_spatial_stack_*): every
+    layer's kernel spectra in one launch before the forward and before the backward,
+    the fused executor's launches, and every layer's dL/dw in one launch plus the sum
+    of its partials."""
+    kspec = wgrad = reduce_ = 0
+    for i in range(wl.layers):
+        B, C, S, N, M, L, _ = layer_dims(wl, i)
+        rb = 32 if M >= 256 else (16 if M >= 64 else 4)
+        kspec += F32 * S * n * n + C64 * S * M * L
+        wgrad += C64 * S * M * L + F32 * S * rb * n * n
+        reduce_ += F32 * S * rb * n * n + F32 * S * n * n
+    return ([("cic_kspec_stack", kspec)] + fused_fwd_launches(wl, tail) + [("cic_kspec_stack", kspec)] +
+            fused_bwd_launches(wl, input_grad, ranges, tail) +
+            [("cic_wgrad_stack", wgrad), ("cic_wgrad_stack_reduce", reduce_)])
 
 
 def step_api_bytes(wl, input_grad=False):
@@ -441,13 +469,18 @@ class CicStackRun:
         self.clf = None
         self.spatial = args.spatial_kernel
         if self.spatial:
-            self.executor = "per_layer"
             self.data = inputs.make_cic_spatial(wl, self.spatial)
             self.x = torch.from_numpy(self.data.x).to(dev)
             self.Ks = [torch.from_numpy(w).to(dev) for w in self.data.weights]
             self.g = torch.from_numpy(self.data.grad).to(dev)
-            self.stack = layers.CicSpatialStack(wl.batch, wl.sizes, wl.channels, self.spatial, device=dev)
-            model = lambda w_, ig: spatial_step_launches(w_, self.spatial, ig, self.stack.dk_ranges())  # noqa: E731
+            if self.per_layer:
+                self.stack = layers.CicSpatialStack(wl.batch, wl.sizes, wl.channels, self.spatial, device=dev)
+                model = lambda w_, ig: spatial_step_launches(w_, self.spatial, ig, self.stack.dk_ranges())  # noqa: E731
+            else:
+                self.executor = "fused_stack"
+                self.stack = layers.CicSpatialStackFused(wl.batch, wl.sizes, wl.channels, self.spatial, device=dev)
+                model = lambda w_, ig: spatial_fused_step_launches(  # noqa: E731
+                    w_, self.spatial, ig, self.stack.dk_ranges(), self.stack.tail())
         elif args.classifier:
             import numpy as np
             self.executor = "classifier"
@@ -680,7 +713,8 @@ def main():
     ap.add_argument("--per-layer", action="store_true",
                     help="CIC stack: run the layer-by-layer calls instead of the fused stack executor")
     ap.add_argument("--spatial-kernel", type=int, default=0, metavar="n",
-                    help="CIC stack: n x n spatial kernels transformed on every call (ROLL), layer by layer")
+                    help="CIC stack: n x n spatial kernels transformed on every call (ROLL), through the stack "
+                         "executor (with --per-layer: layer by layer)")
     ap.add_argument("--chain", action="store_true",
                     help="CIC stack: the FDCNN data flow of section 2.5.1 (one rfft2, FDC + FDP layers on spectra, "
                          "one irfft2); a different function from the per-layer transforms")

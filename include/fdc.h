@@ -277,6 +277,27 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *plan, const float *gy, c
                                   const fdc_c64 *const *K, float *gx, fdc_c64 *const *gK, void *ws,
                                   size_t ws_bytes, hipStream_t stream);
 
+/* The same stack with n x n spatial kernels (section 2.4.1.2) and ROLL artifact
+ * handling in every layer: the result of fdc_cic_spatial_layer_forward / backward
+ * with artifact ROLL and kernel_n = n, layer after layer (to fp32 rounding).  w is a
+ * host array of `layers` device pointers, w[i] [S_i][n][n] fp32 (S_i = channels[i+1]);
+ * n in [1, 8] and n <= every layer's output size.  Each call forms every layer's
+ * kernel spectra at the kept bins in one launch, with the ROLL shift s = (n-1)/2 of
+ * the layer's M x M output folded in as the phase exp(+2 pi i s (k + l) / M) of output
+ * bin (k, l), then runs the stack executor on them (saved buffers as
+ * fdc_cic_stack_forward).  The backward gives gw[i] [S_i][n][n] (host array of device
+ * pointers, all required; each summed over the batch and bins in a fixed order) and
+ * gx (NULL: skipped); dK of every layer goes through the workspace and is projected
+ * onto the taps in one launch.  Workspaces: fdc_cic_spatial_stack_workspace_size. */
+fdc_status fdc_cic_spatial_stack_workspace_size(const fdc_stack_plan *plan, int kernel_n, size_t *fwd_ws,
+                                                size_t *bwd_ws);
+fdc_status fdc_cic_spatial_stack_forward(const fdc_stack_plan *plan, int kernel_n, const float *x,
+                                         const float *const *w, float *y, void *const *saved, void *ws,
+                                         size_t ws_bytes, hipStream_t stream);
+fdc_status fdc_cic_spatial_stack_backward(const fdc_stack_plan *plan, int kernel_n, const float *gy,
+                                          const void *const *saved, const float *const *w, float *gx,
+                                          float *const *gw, void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* ------------------------------------------------------------------------ */
 /* FDCNN classifier head and optimiser                                      */
 /* ------------------------------------------------------------------------ */

@@ -66,6 +66,9 @@ _SIGS = {
     "fdc_cic_stack_saved_size": [_P, _I, ctypes.POINTER(_SZ)],
     "fdc_cic_stack_forward": [_P, _P, _P, _P, _P, _P, _SZ, _P],
     "fdc_cic_stack_backward": [_P, _P, _P, _P, _P, _P, _P, _SZ, _P],
+    "fdc_cic_spatial_stack_workspace_size": [_P, _I, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ)],
+    "fdc_cic_spatial_stack_forward": [_P, _I, _P, _P, _P, _P, _P, _SZ, _P],
+    "fdc_cic_spatial_stack_backward": [_P, _I, _P, _P, _P, _P, _P, _P, _SZ, _P],
     "fdc_kernel_timing_enable": [_I, ctypes.c_char_p],
     "fdc_kernel_timing_disable": [],
     "fdc_kernel_timing_report": [ctypes.c_char_p, _SZ],

@@ -1175,6 +1175,121 @@ fdc_status fdc_cic_stack_dk_ranges(const fdc_stack_plan *p, int layer, int *rang
   return FDC_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Stack with spatial kernels: the kernel spectra of every layer (with the ROLL shift
+// folded in as a phase) in one launch, the stack executor on them, and dL/dw of every
+// layer from the executor's dK in one launch (plus the in-order sum of its partials).
+// ---------------------------------------------------------------------------
+namespace {
+struct SpatialStackWs {
+  std::vector<size_t> k, gk, part;  // byte offsets per layer
+  size_t stack_fwd, stack_bwd, fwd, bwd;
+};
+SpatialStackWs spatial_stack_layout(const fdc_stack_plan *p, int n) {
+  SpatialStackWs w;
+  size_t off = 0;
+  for (int i = 0; i < p->layers; ++i) {
+    const StackLayer g = stack_layer(p, i);
+    w.k.push_back(off);
+    off += align256((size_t)g.S * g.N * (g.N / 2 + 1) * sizeof(fdc_c64));
+  }
+  w.stack_fwd = off;
+  w.fwd = off + align256((p->ws_a + p->ws_b + p->ws_x) * sizeof(fdc_c64));
+  for (int i = 0; i < p->layers; ++i) {
+    const StackLayer g = stack_layer(p, i);
+    w.gk.push_back(off);
+    off += align256((size_t)g.S * g.N * (g.N / 2 + 1) * sizeof(fdc_c64));
+  }
+  for (int i = 0; i < p->layers; ++i) {
+    const StackLayer g = stack_layer(p, i);
+    w.part.push_back(off);
+    off += align256((size_t)g.S * fdc::cic_wgrad_stack_blocks(g.M) * n * n * sizeof(float));
+  }
+  w.stack_bwd = off;
+  w.bwd = off + align256((p->ws_a + p->ws_b) * sizeof(fdc_c64));
+  return w;
+}
+fdc_status check_spatial_stack(const fdc_stack_plan *p, int n) {
+  if (fdc_status st = check_stack_plan(p)) return st;
+  if (!fdc::spatial_kernel_size_supported(n)) return fail(FDC_EUNSUPPORTED, "kernel_n must be in [1, 8] (got %d)", n);
+  for (int i = 0; i < p->layers; ++i)
+    if (n > p->N[i + 1]) return fail(FDC_EINVAL, "kernel_n %d larger than layer %d's output %d", n, i, p->N[i + 1]);
+  return FDC_OK;
+}
+// kernel spectra of every layer into the workspace (batches of fdc::kSpatialBatch layers)
+fdc_status spatial_stack_kspec(const fdc_stack_plan *p, int n, const float *const *w, char *base,
+                               const SpatialStackWs &L, std::vector<const fdc_c64 *> &K, hipStream_t s) {
+  K.assign(p->layers, nullptr);
+  for (int i0 = 0; i0 < p->layers; i0 += fdc::kSpatialBatch) {
+    fdc::SpatialBatch sb{};
+    for (int i = i0; i < p->layers && i < i0 + fdc::kSpatialBatch; ++i) {
+      const StackLayer g = stack_layer(p, i);
+      auto *Ki = reinterpret_cast<float2 *>(base + L.k[i]);
+      K[i] = reinterpret_cast<const fdc_c64 *>(Ki);
+      fdc::SpatialLayer &d = sb.layer[sb.count++];
+      d.w = w[i], d.K = Ki, d.N = g.N, d.M = g.M, d.S = g.S, d.n = n, d.roll = (n - 1) / 2;
+    }
+    if (fdc_status st = check_hip(fdc::launch_cic_kspec_stack(sb, s), "spatial stack kernel spectra")) return st;
+  }
+  return FDC_OK;
+}
+}  // namespace
+
+fdc_status fdc_cic_spatial_stack_workspace_size(const fdc_stack_plan *p, int kernel_n, size_t *fwd_ws,
+                                                size_t *bwd_ws) {
+  if (fdc_status st = check_spatial_stack(p, kernel_n)) return st;
+  const SpatialStackWs L = spatial_stack_layout(p, kernel_n);
+  if (fwd_ws) *fwd_ws = L.fwd;
+  if (bwd_ws) *bwd_ws = L.bwd;
+  return FDC_OK;
+}
+
+fdc_status fdc_cic_spatial_stack_forward(const fdc_stack_plan *p, int kernel_n, const float *x, const float *const *w,
+                                         float *y, void *const *saved, void *ws, size_t ws_bytes, hipStream_t s) {
+  if (fdc_status st = check_spatial_stack(p, kernel_n)) return st;
+  if (!x || !w || !y) return fail(FDC_EINVAL, "NULL tensor or array");
+  for (int i = 0; i < p->layers; ++i)
+    if (!w[i] || (saved && !saved[i])) return fail(FDC_EINVAL, "layer %d: NULL weights or saved buffer", i);
+  const SpatialStackWs L = spatial_stack_layout(p, kernel_n);
+  if (fdc_status st = check_ws(ws, ws_bytes, L.fwd)) return st;
+  char *base = static_cast<char *>(ws);
+  std::vector<const fdc_c64 *> K;
+  if (fdc_status st = spatial_stack_kspec(p, kernel_n, w, base, L, K, s)) return st;
+  return fdc_cic_stack_forward(p, x, K.data(), y, saved, base + L.stack_fwd, L.fwd - L.stack_fwd, s);
+}
+
+fdc_status fdc_cic_spatial_stack_backward(const fdc_stack_plan *p, int kernel_n, const float *gy,
+                                          const void *const *saved, const float *const *w, float *gx,
+                                          float *const *gw, void *ws, size_t ws_bytes, hipStream_t s) {
+  if (fdc_status st = check_spatial_stack(p, kernel_n)) return st;
+  if (!gy || !saved || !w || !gw) return fail(FDC_EINVAL, "NULL tensor or array");
+  for (int i = 0; i < p->layers; ++i)
+    if (!saved[i] || !w[i] || !gw[i]) return fail(FDC_EINVAL, "layer %d: NULL saved, weights or dL/dw", i);
+  const SpatialStackWs L = spatial_stack_layout(p, kernel_n);
+  if (fdc_status st = check_ws(ws, ws_bytes, L.bwd)) return st;
+  char *base = static_cast<char *>(ws);
+  std::vector<const fdc_c64 *> K;
+  if (fdc_status st = spatial_stack_kspec(p, kernel_n, w, base, L, K, s)) return st;
+  std::vector<fdc_c64 *> gK(p->layers);
+  for (int i = 0; i < p->layers; ++i) gK[i] = reinterpret_cast<fdc_c64 *>(base + L.gk[i]);
+  if (fdc_status st = fdc_cic_stack_backward(p, gy, saved, K.data(), gx, gK.data(), base + L.stack_bwd,
+                                             L.bwd - L.stack_bwd, s))
+    return st;
+  for (int i0 = 0; i0 < p->layers; i0 += fdc::kSpatialBatch) {
+    fdc::SpatialBatch sb{};
+    for (int i = i0; i < p->layers && i < i0 + fdc::kSpatialBatch; ++i) {
+      const StackLayer g = stack_layer(p, i);
+      fdc::SpatialLayer &d = sb.layer[sb.count++];
+      d.gK = reinterpret_cast<const float2 *>(gK[i]);
+      d.part = reinterpret_cast<float *>(base + L.part[i]);
+      d.gw = gw[i];
+      d.N = g.N, d.M = g.M, d.S = g.S, d.n = kernel_n, d.roll = (kernel_n - 1) / 2;
+    }
+    if (fdc_status st = check_hip(fdc::launch_cic_wgrad_stack(sb, s), "spatial stack kernel gradients")) return st;
+  }
+  return FDC_OK;
+}
+
 fdc_status fdc_kernel_timing_launches(char *buf, size_t buf_bytes) {
   if (buf == nullptr || buf_bytes == 0) return fail(FDC_EINVAL, "buffer is NULL or empty");
   Timing &t = timing();

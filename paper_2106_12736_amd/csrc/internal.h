@@ -200,6 +200,26 @@ bool spatial_kernel_size_supported(int n);
 // Output channels the spatial-kernel weight-gradient launch accepts.
 bool spatial_channels_supported(int S);
 int cic_wgrad_blocks(int M);
+// One layer of a batched spatial-kernel call (k_cic_kspec_stack, k_cic_wgrad_stack):
+// the caller fills w, K (kspec) or gK, part, gw (wgrad), N, M, S, n and roll (the ROLL
+// shift s, 0 for none); the launchers fill the grid fields.
+struct SpatialLayer {
+  const float *w;
+  float2 *K;
+  const float2 *gK;
+  float *part, *gw;
+  int N, M, S, n, roll;
+  int ncb, rowb, block0, elem0;
+};
+constexpr int kSpatialBatch = 8;
+struct SpatialBatch {
+  SpatialLayer layer[kSpatialBatch];
+  int count;
+};
+// partial sums per output channel of launch_cic_wgrad_stack for an M-point layer
+int cic_wgrad_stack_blocks(int M);
+hipError_t launch_cic_kspec_stack(SpatialBatch sb, hipStream_t s);
+hipError_t launch_cic_wgrad_stack(SpatialBatch sb, hipStream_t s);
 hipError_t launch_cic_kspec(int n_img, const float *w, float2 *K, int S, int n, int M, hipStream_t s);
 hipError_t launch_cic_wgrad(int n_img, const float2 *gK, float *part, float *gw, int S, int n, int M,
                             hipStream_t s);

@@ -1722,6 +1722,263 @@ __global__ void k_cic_wgrad_reduce(const float *__restrict__ part, float *__rest
   gw[i] = acc;
 }
 
+// ---------------------------------------------------------------------------
+// The same two steps for every layer of a stack in one launch each (the spatial-kernel
+// stack): layer sizes are runtime values, each workgroup stages its layer's twiddle
+// table.  ROLL artifact handling (out[i][j] = y[(i + s) mod M][(j + s) mod M]) of a
+// layer's M x M output is a phase at each output bin, exp(+2 pi i s (k' + l) / M) with
+// k' the output row, so it is folded into the kernel spectra here (and its conjugate
+// into dK before the projection); the stack executor then runs without artifact
+// handling.
+// ---------------------------------------------------------------------------
+__device__ const float2 *twiddle_table(int n) {
+  switch (n) {
+#define FDC_TW(V) \
+  case V:         \
+    return reinterpret_cast<const float2 *>(g_twiddle<V>.v);
+    FDC_TW(2) FDC_TW(4) FDC_TW(8) FDC_TW(16) FDC_TW(32) FDC_TW(64) FDC_TW(128) FDC_TW(256) FDC_TW(512) FDC_TW(1024)
+    FDC_TW(224)
+#undef FDC_TW
+    default:
+      return nullptr;
+  }
+}
+
+constexpr int kSpatialTwMax = 1024;
+// rows of one workgroup of k_cic_kspec_stack
+constexpr int kKspecStackRows = 64;
+
+__device__ __forceinline__ const SpatialLayer &spatial_layer_of(const SpatialBatch &sb, int blk) {
+  int i = 0;
+  while (i + 1 < sb.count && blk >= sb.layer[i + 1].block0) ++i;
+  return sb.layer[i];
+}
+
+// a + b mod n for 0 <= a, b < n
+__device__ __forceinline__ int add_mod(int a, int b, int n) {
+  const int t = a + b;
+  return t >= n ? t - n : t;
+}
+
+// Table index of exp(+2 pi i s (k + l) / M) = conj(W_N^(s (k + l) N / M)) for output
+// bin (k < M, l <= M/2), 0 <= s <= 3 (n <= 8)
+__device__ __forceinline__ int roll_index(int s, int k, int l, int M, int N) {
+  const int t = add_mod(k, l < M ? l : l - M, M);
+  int u = 0;
+  for (int r = 0; r < s; ++r) u = add_mod(u, t, M);
+  return u * (N / M);
+}
+
+template <int NK>
+__global__ __launch_bounds__(256) void k_cic_kspec_stack(SpatialBatch sb) {
+  __shared__ float2 tw[kSpatialTwMax];
+  const SpatialLayer &d = spatial_layer_of(sb, blockIdx.x);
+  const int N = d.N, M = d.M, NF = N / 2 + 1, L = M / 2 + 1;
+  const float2 *tab = twiddle_table(N);
+  for (int i = threadIdx.x; i < N; i += 256) tw[i] = tab[i];
+  __syncthreads();
+  const int local = blockIdx.x - d.block0;
+  const int rb = local % d.rowb, rest = local / d.rowb;
+  const int cb = rest % d.ncb, o = rest / d.ncb;
+  const int l = cb * 64 + (threadIdx.x & 63);
+  if (l >= L) return;
+  const float *wo = d.w + (long long)o * NK * NK;
+  float2 R[NK];  // R_a(l) = sum_b w[o][a][b] W^(l b)
+#pragma unroll
+  for (int a = 0; a < NK; ++a) {
+    float rx = 0.f, ry = 0.f;
+    int idx = 0;  // l b mod N
+#pragma unroll
+    for (int b = 0; b < NK; ++b) {
+      const float2 v = tw[idx];
+      rx = fmaf(wo[a * NK + b], v.x, rx);
+      ry = fmaf(wo[a * NK + b], v.y, ry);
+      idx = add_mod(idx, l, N);
+    }
+    R[a] = make_float2(rx, ry);
+  }
+  float2 *ko = d.K + (long long)o * N * NF + l;
+  const int k_end = min(M, (rb + 1) * kKspecStackRows);
+  for (int k = rb * kKspecStackRows + (threadIdx.x >> 6); k < k_end; k += 4) {
+    const int kr = k < M / 2 ? k : k + (N - M);
+    float2 acc = make_float2(0.f, 0.f);
+    int idx = 0;  // kr a mod N
+#pragma unroll
+    for (int a = 0; a < NK; ++a) {
+      const float2 u = tw[idx];
+      acc.x = fmaf(u.x, R[a].x, fmaf(-u.y, R[a].y, acc.x));
+      acc.y = fmaf(u.x, R[a].y, fmaf(u.y, R[a].x, acc.y));
+      idx = add_mod(idx, kr, N);
+    }
+    if (d.roll) acc = cmul(acc, cconj(tw[roll_index(d.roll, k, l, M, N)]));
+    ko[(long long)kr * NF] = acc;
+  }
+}
+
+// Rows of one workgroup of k_cic_wgrad_stack (a quarter per wave).
+constexpr int kWgradStackRows = 64;
+
+// Partial sums of dL/dw for every layer of the batch.  dL/dw[o][a][b] =
+// Re sum_l conj(W^(l b)) F_a(l) with F_a(l) = sum_k dK(k, l) conj(W^(k a)) (k the
+// N-grid row of a kept row): a lane owns one column l and sums F_a(l) down the
+// workgroup's rows (a wave reads a row segment of 64 bins with one load), projects it
+// onto the taps at the end, and the workgroup adds its 256 lanes in a fixed order.
+// Workgroup (layer, o, column block cb, row block rb) writes
+// part[(o * ncb * rowb + cb * rowb + rb) * NK^2 + tap] of its layer.
+template <int NK>
+__global__ __launch_bounds__(256) void k_cic_wgrad_stack(SpatialBatch sb) {
+  constexpr int T = NK * NK;
+  __shared__ float2 tw[kSpatialTwMax];
+  __shared__ float red[4][T];
+  const SpatialLayer &d = spatial_layer_of(sb, blockIdx.x);
+  const int N = d.N, M = d.M, NF = N / 2 + 1, L = M / 2 + 1;
+  const float2 *tab = twiddle_table(N);
+  for (int i = threadIdx.x; i < N; i += 256) tw[i] = tab[i];
+  __syncthreads();
+  const int local = blockIdx.x - d.block0;
+  const int rb = local % d.rowb, rest = local / d.rowb;
+  const int cb = rest % d.ncb, o = rest / d.ncb;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l = cb * 64 + lane;
+  const bool on = l < L;
+  const float2 *col = d.gK + (long long)o * N * NF + (on ? l : 0);
+  float2 F[NK];
+#pragma unroll
+  for (int a = 0; a < NK; ++a) F[a] = make_float2(0.f, 0.f);
+  const int k_end = min(M, (rb + 1) * kWgradStackRows);
+  constexpr int U = 4;  // rows whose loads are in flight together
+  for (int k0 = rb * kWgradStackRows + wave; k0 < k_end; k0 += 4 * U) {
+    float2 g[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = k0 + 4 * u;
+      const int kr = k < M / 2 ? k : k + (N - M);
+      g[u] = (on && k < k_end) ? col[(long long)kr * NF] : make_float2(0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = k0 + 4 * u;
+      if (k >= k_end) break;
+      const int kr = k < M / 2 ? k : k + (N - M);
+      float2 gv = g[u];
+      if (d.roll) gv = cmul(gv, tw[roll_index(d.roll, k, on ? l : 0, M, N)]);  // dK = dK' conj(phase)
+      int idx = 0;  // kr a mod N
+#pragma unroll
+      for (int a = 0; a < NK; ++a) {
+        F[a] = cfmac(F[a], gv, tw[idx]);
+        idx = add_mod(idx, kr, N);
+      }
+    }
+  }
+  // project onto the taps: Re(F_a conj(W^(l b)))
+  float acc[T];
+  {
+    int idx = 0;  // l b mod N
+#pragma unroll
+    for (int b = 0; b < NK; ++b) {
+      const float2 v = tw[idx];
+#pragma unroll
+      for (int a = 0; a < NK; ++a) acc[a * NK + b] = fmaf(F[a].x, v.x, F[a].y * v.y);
+      idx = add_mod(idx, on ? l : 0, N);
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < T; ++t)
+    for (int off = 32; off > 0; off >>= 1) acc[t] += __shfl_xor(acc[t], off);
+  if (lane == 0) {
+#pragma unroll
+    for (int t = 0; t < T; ++t) red[wave][t] = acc[t];
+  }
+  __syncthreads();
+  if (threadIdx.x < T) {
+    const int t = threadIdx.x;
+    d.part[((long long)o * d.ncb * d.rowb + cb * d.rowb + rb) * T + t] =
+        (red[0][t] + red[1][t]) + (red[2][t] + red[3][t]);
+  }
+}
+
+// gw of every layer of the batch from its partial sums (nb = ncb * rowb per output
+// channel), added in order (eight partials' loads in flight at a time).
+__global__ __launch_bounds__(256) void k_cic_wgrad_stack_reduce(SpatialBatch sb, int total) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= total) return;
+  int li = 0;
+  while (li + 1 < sb.count && i >= sb.layer[li + 1].elem0) ++li;
+  const SpatialLayer &d = sb.layer[li];
+  const int nn = d.n * d.n, e = i - d.elem0, nb = d.ncb * d.rowb;
+  const int o = e / nn, t = e - (e / nn) * nn;
+  const float *src = d.part + (long long)o * nb * nn + t;
+  float acc = 0.f;
+  int q = 0;
+  for (; q + 8 <= nb; q += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = src[(q + u) * nn];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc += v[u];
+  }
+  for (; q < nb; ++q) acc += src[q * nn];
+  d.gw[e] = acc;
+}
+
+template <class F>
+static bool dispatch_spatial_n(int n, F &&f) {
+  switch (n) {
+#define FDC_CASE(V)                      \
+  case V:                                \
+    f(std::integral_constant<int, V>{}); \
+    return true;
+    FDC_CASE(1) FDC_CASE(2) FDC_CASE(3) FDC_CASE(4) FDC_CASE(5) FDC_CASE(6) FDC_CASE(7) FDC_CASE(8)
+#undef FDC_CASE
+    default:
+      return false;
+  }
+}
+
+int cic_wgrad_stack_blocks(int M) { return ((M / 2 + 1 + 63) / 64) * ((M + kWgradStackRows - 1) / kWgradStackRows); }
+
+hipError_t launch_cic_kspec_stack(SpatialBatch sb, hipStream_t s) {
+  int blocks = 0;
+  for (int i = 0; i < sb.count; ++i) {
+    SpatialLayer &d = sb.layer[i];
+    if (d.n != sb.layer[0].n || d.N > kSpatialTwMax || d.N % d.M) return hipErrorInvalidValue;
+    d.ncb = (d.M / 2 + 1 + 63) / 64;
+    d.rowb = (d.M + kKspecStackRows - 1) / kKspecStackRows;
+    d.block0 = blocks;
+    const long long nb = (long long)d.S * d.ncb * d.rowb;
+    if (blocks + nb >= (1LL << 31)) return hipErrorInvalidValue;
+    blocks += (int)nb;
+  }
+  hipError_t err = hipErrorInvalidValue;
+  dispatch_spatial_n(sb.layer[0].n, [&](auto nc) {
+    err = launch("cic_kspec_stack", k_cic_kspec_stack<decltype(nc)::value>, (unsigned)blocks, 256, 0, s, sb);
+  });
+  return err;
+}
+
+hipError_t launch_cic_wgrad_stack(SpatialBatch sb, hipStream_t s) {
+  int blocks = 0, elems = 0;
+  for (int i = 0; i < sb.count; ++i) {
+    SpatialLayer &d = sb.layer[i];
+    if (d.n != sb.layer[0].n || d.N > kSpatialTwMax || d.N % d.M) return hipErrorInvalidValue;
+    d.ncb = (d.M / 2 + 1 + 63) / 64;
+    d.rowb = (d.M + kWgradStackRows - 1) / kWgradStackRows;
+    d.block0 = blocks;
+    d.elem0 = elems;
+    const long long nb = (long long)d.S * d.ncb * d.rowb, ne = (long long)d.S * d.n * d.n;
+    if (blocks + nb >= (1LL << 31) || elems + ne >= (1LL << 31)) return hipErrorInvalidValue;
+    blocks += (int)nb;
+    elems += (int)ne;
+  }
+  hipError_t e = hipErrorInvalidValue;
+  dispatch_spatial_n(sb.layer[0].n, [&](auto nc) {
+    e = launch("cic_wgrad_stack", k_cic_wgrad_stack<decltype(nc)::value>, (unsigned)blocks, 256, 0, s, sb);
+  });
+  if (e != hipSuccess) return e;
+  return launch("cic_wgrad_stack_reduce", k_cic_wgrad_stack_reduce, (unsigned)((elems + 255) / 256), 256, 0, s, sb,
+                elems);
+}
+
 bool spatial_kernel_size_supported(int n) { return n >= 1 && n <= kSpatialMaxN; }
 
 bool spatial_channels_supported(int S) { return S >= 1 && S <= 65535; }

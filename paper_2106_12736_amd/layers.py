@@ -471,6 +471,49 @@ class CicStackFused:
         return self.gks
 
 
+class CicSpatialStackFused(CicStackFused):
+    """The stack of CicSpatialStack (n x n spatial kernels, ROLL in every layer) run
+    through fdc_cic_spatial_stack_*: every layer's kernel spectra in one launch, the
+    stack executor, every layer's dL/dw in one launch."""
+
+    def __init__(self, batch, sizes, channels, kernel_n, device="cuda"):
+        super().__init__(batch, sizes, channels, device=device)
+        self.kernel_n = kernel_n
+        f, b = ctypes.c_size_t(), ctypes.c_size_t()
+        call("fdc_cic_spatial_stack_workspace_size", self._p, kernel_n, ctypes.byref(f), ctypes.byref(b))
+        self.fwd_ws = _workspace(f.value, self.device)
+        self.bwd_ws = _workspace(b.value, self.device)
+        self.gks = None
+        self.gws = [torch.empty((channels[i + 1], kernel_n, kernel_n), dtype=torch.float32, device=self.device)
+                    for i in range(self.layers)]
+        self._gw_arr = _ptr_array(self.gws)
+
+    def _weights(self, weights):
+        if len(weights) != self.layers:
+            raise ValueError(f"{self.layers} weight tensors expected")
+        n = self.kernel_n
+        for i, w in enumerate(weights):
+            _check(w, torch.float32, (self.channels[i + 1], n, n), f"w[{i}]")
+        return _ptr_array(weights)
+
+    def forward(self, x, weights):
+        _check(x, torch.float32, (self.batch, self.channels[0], self.sizes[0], self.sizes[0]), "x")
+        call("fdc_cic_spatial_stack_forward", self._p, self.kernel_n, _ptr(x), self._weights(weights), _ptr(self.out),
+             self._saved_arr, _ptr(self.fwd_ws), self.fwd_ws.numel(), _stream())
+        return self.out
+
+    def backward(self, gy, weights, input_grad=None):
+        """dL/dw of every layer (and the input gradient into `input_grad` if given)."""
+        _check(gy, torch.float32, tuple(self.out.shape), "gy")
+        if input_grad is not None:
+            _check(input_grad, torch.float32, (self.batch, self.channels[0], self.sizes[0], self.sizes[0]),
+                   "input_grad")
+        call("fdc_cic_spatial_stack_backward", self._p, self.kernel_n, _ptr(gy), self._saved_arr,
+             self._weights(weights), _ptr(input_grad), self._gw_arr, _ptr(self.bwd_ws), self.bwd_ws.numel(),
+             _stream())
+        return self.gws
+
+
 
 def cic_fdp_forward(X, K, M):
     """FDC layer of the FDCNN on spectra followed by FDP: [B][C][N][N/2+1] -> [B][S][M][M/2+1]."""

@@ -84,6 +84,61 @@ def test_spatial_stack(wl):
     assert_parity(to_np(gin), g, "gx")
 
 
+def _oracle_roll_stack(x, weights, sizes, grad):
+    """The spatial stack layer after layer with ROLL (the oracle's layer functions)."""
+    h, saved = x.astype(np.float64), []
+    for i, w in enumerate(weights):
+        h, xs = fdc.cic_spatial_layer_forward(h, w.astype(np.float64), sizes[i + 1], fdc.ARTIFACT_ROLL)
+        saved.append(xs)
+    g, gws = grad.astype(np.float64), [None] * len(weights)
+    for i in reversed(range(len(weights))):
+        g, gws[i] = fdc.cic_spatial_layer_backward(g, saved[i], weights[i].astype(np.float64), sizes[i + 1],
+                                                   fdc.ARTIFACT_ROLL)
+    return h, gws, g
+
+
+FUSED_SPATIAL = [
+    # workload (or batch, sizes, channels), n: ROLL shifts 0 .. 3
+    (inputs.LAYER64, 5), (inputs.STACK256, 3), (inputs.STACK512, 2), (inputs.STACK1024, 3),
+    ((3, (64, 32, 16), (2, 4, 8)), 4), ((2, (32, 16), (1, 3)), 7), ((2, (16, 16, 8), (1, 2, 2)), 1),
+]
+
+
+@pytest.mark.parametrize("case,n", FUSED_SPATIAL, ids=lambda v: getattr(v, "name", str(v)))
+def test_spatial_stack_fused(case, n):
+    """fdc_cic_spatial_stack_*: every layer's kernel spectra with the ROLL phase in one
+    launch, the stack executor, every dL/dw in one launch; against the oracle's layers."""
+    if isinstance(case, inputs.CicStack):
+        d = inputs.make_cic_spatial(case, n)
+        B, sizes, chans = case.batch, case.sizes, case.channels
+        x, weights, grad = d.x, d.weights, d.grad
+    else:
+        B, sizes, chans = case
+        rng = _rng("spatial_fused", B, sizes, chans, n)
+        x = inputs.normal(rng, (B, chans[0], sizes[0], sizes[0]))
+        weights = [inputs.normal(rng, (chans[i + 1], n, n)) * np.float32(np.sqrt(2.0 / (n * n)))
+                   for i in range(len(sizes) - 1)]
+        grad = inputs.normal(rng, (B, chans[-1], sizes[-1], sizes[-1]))
+    print(f"spatial stack fused {sizes} {chans} B={B} n={n}", flush=True)
+    st = layers.CicSpatialStackFused(B, sizes, chans, n)
+    xd = torch.from_numpy(x).cuda()
+    ws = [torch.from_numpy(w).cuda() for w in weights]
+    gin = torch.empty_like(xd)
+    y = st.forward(xd, ws).clone()
+    gws = [g.clone() for g in st.backward(torch.from_numpy(grad).cuda(), ws, input_grad=gin)]
+    torch.cuda.synchronize()
+    y_ref, gw_ref, gx_ref = _oracle_roll_stack(x, weights, sizes, grad)
+    assert_parity(to_np(y), y_ref, "y")
+    for i in range(len(weights)):
+        assert_parity(to_np(gws[i]), gw_ref[i], f"gw[{i}]")
+    assert_parity(to_np(gin), gx_ref, "gx")
+    # a second call on the same buffers gives identical results (fixed summation order)
+    st.forward(xd, ws)
+    again = st.backward(torch.from_numpy(grad).cuda(), ws, input_grad=gin)
+    torch.cuda.synchronize()
+    assert all(torch.equal(a, b) for a, b in zip(gws, again))
+
+
 @pytest.mark.parametrize("wl", inputs.FULL_CIC_WORKLOADS, ids=lambda w: w.name)
 def test_full_fdc_with_cic_block4(wl):
     """The Full FDC layer with CIC at the paper's VGG16 Conv Block 4 shapes (64 x 64,
