@@ -152,8 +152,19 @@ def test_full_layer_workload_sampled(wl):
         # dL/dx slice gx[b][cs] needs every output channel of image b
         gx_ref, _ = fdc.full_fdc_backward(g64[b:b + 1], xs_b[:, cs], w64[:, cs], crop)
         assert_parity(to_np(gx[b, cs]), gx_ref[0], f"gx[{b}]")
-    # dL/dw slice gw[ss][cs] needs every image of the batch
-    xs_c = dft.rfft2(x64[:, cs])
-    _, gw_ref = fdc.full_fdc_backward(g64[:, ss], xs_c, w64[ss][:, cs], crop, want_gx=False)
-    assert_parity(to_np(gw[ss][:, cs]), gw_ref, "gw")
+    # dL/dw slice gw[ss2][cs2] needs every image of the batch; the pairs straddle the
+    # 16- and 32-channel tile borders of the dL/dw kernel and reach both ends
+    ss2 = sorted({0, 15, 16, 31, 32, Cout // 2 + 1, Cout - 33, Cout - 1})
+    cs2 = sorted({0, 16, 31, 32, Cin // 3, Cin - 1})
+    xs_c = dft.rfft2(x64[:, cs2])
+    _, gw_ref = fdc.full_fdc_backward(g64[:, ss2], xs_c, w64[ss2][:, cs2], crop, want_gx=False)
+    assert_parity(to_np(gw[ss2][:, cs2]), gw_ref, "gw")
     assert torch.isfinite(y).all() and torch.isfinite(gx).all() and torch.isfinite(gw).all()
+    # every element at once: the layer is linear in w and in x, so <gw, w> = <gy, y> = <gx, x>
+    # (Euler's identity for linear maps; float64 sums of the GPU's own tensors)
+    yy = float((to_np(y).astype(np.float64) * g64).sum())
+    ww = float((to_np(gw).astype(np.float64) * w64).sum())
+    xx = float((to_np(gx).astype(np.float64) * x64).sum())
+    scale = float(np.sqrt((to_np(y).astype(np.float64) ** 2).sum() * (g64 ** 2).sum()))
+    assert abs(ww - yy) <= 1e-4 * scale, ("<gw, w> != <gy, y>", ww, yy, scale)
+    assert abs(xx - yy) <= 1e-4 * scale, ("<gx, x> != <gy, y>", xx, yy, scale)
