@@ -545,6 +545,8 @@ __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fwd_crop(const float
 // Output channels of one input channel handled by one workgroup of the CIC inverse
 // kernel (a divisor of J): the pooled input column is loaded once for all of them.
 constexpr int kCicJW = 4;
+// CIC inverse grids below this many workgroups switch to 8-column tiles.
+constexpr unsigned kCicNarrowGrid = 256;
 
 template <int N, int M, int CT, int JW>
 __global__ __launch_bounds__(CT *ColCfg<M>::TPS) void k_col_cic_inv(const float2 *__restrict__ Xh,
@@ -1293,6 +1295,16 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
     auto go = [&](auto kern) {
       err = launch(n2.c_str(), kern, g2, CTM * ColCfg<M>::TPS, lds2, s, Xh, K, U, B, C, J, (int)groups);
     };
+    // Few planes (a small batch at the first layer): 8-column tiles, up to four times the
+    // workgroups, when the default tiles would leave most compute units idle.
+    constexpr int CTS = 8;
+    if (CTS < CTM && jw == kCicJW && g2 < kCicNarrowGrid) {
+      const unsigned g3 = col_grid(groups, L, CTS);
+      const size_t lds3 = (twiddle_lds_elems<M>() + lds_size<kColLds>(M * CTS)) * sizeof(float2);
+      err = launch(n2.c_str(), k_col_cic_inv<N, M, CTS, kCicJW>, g3, CTS * ColCfg<M>::TPS, lds3, s, Xh, K, U, B, C, J,
+                   (int)groups);
+      return;
+    }
     switch (jw) {
       case 8: go(k_col_cic_inv<N, M, CTM, 8>); break;
       case 4: go(k_col_cic_inv<N, M, CTM, 4>); break;
