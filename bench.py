@@ -191,9 +191,11 @@ def fft2_launches(n, planes, inverse):
     return [(f"row_r2c_{n}", real + spec), (f"col_fft_fwd_{n}", 2 * spec)]
 
 
-def chain_step_launches(wl, input_grad=False):
+def chain_step_launches(wl, input_grad=False, hermitian=False):
     """(kernel name, algorithmic bytes) of every launch of one step of the FDCNN chain
-    (one rfft2, every FDC + FDP layer on spectra, one irfft2, and the backward)."""
+    (one rfft2, every FDC + FDP layer on spectra, one irfft2, and the backward); with
+    hermitian=True also Pi_H after every layer but the last, and before their backward
+    (two columns of every plane read and written)."""
     out = []
     n = wl.layers
     B = wl.batch
@@ -202,13 +204,20 @@ def chain_step_launches(wl, input_grad=False):
     ML, CL = wl.sizes[-1], wl.channels[-1]
     MFL = ML // 2 + 1
     out += fft2_launches(N0, B * C0, inverse=False)
+    def pi_h(i):
+        B_, _, S_, _, M_, _, _ = layer_dims(wl, i)
+        return ("hermitian_columns", 2 * C64 * B_ * S_ * 2 * M_)
     for i in range(n):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
         out.append(("cic_fdp_fwd", C64 * (B * C * M * L + S * M * L + B * S * M * L)))
+        if hermitian and i + 1 < n:
+            out.append(pi_h(i))
     out += fft2_launches(ML, B * CL, inverse=True)
     out += fft2_launches(ML, B * CL, inverse=False)  # the irfft2 adjoint has the forward's launches
     for i in reversed(range(n)):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
+        if hermitian and i + 1 < n:
+            out.append(pi_h(i))
         if i > 0 or input_grad:
             # reads gY and K at the kept bins, writes all of gX (zeros at dropped bins)
             out.append(("cic_fdp_bwd_gx", C64 * (B * S * M * L + S * M * L + B * C * N * NF)))
@@ -495,9 +504,10 @@ class CicStackRun:
             self.clf.load(self.Ks, torch.from_numpy(self.W).to(dev), torch.from_numpy(self.bias).to(dev))
             self.labels_d = torch.from_numpy(self.labels).to(dev)
             model = lambda w_, ig: classifier_step_launches(w_, classes, self.clf.n_params)  # noqa: E731
-        elif args.chain:
-            self.stack = layers.CicChain(wl.batch, wl.sizes, wl.channels, device=dev)
-            model = chain_step_launches
+        elif args.chain or args.folded:
+            self.executor = "folded_chain" if args.folded else "chain"
+            self.stack = layers.CicChain(wl.batch, wl.sizes, wl.channels, device=dev, hermitian=args.folded)
+            model = lambda w_, ig: chain_step_launches(w_, ig, hermitian=args.folded)  # noqa: E731
         elif self.per_layer:
             self.stack = layers.CicStack(wl.batch, wl.sizes, wl.channels, device=dev)
             model = lambda w_, ig: step_launches(w_, ig, self.stack.dk_ranges())  # noqa: E731
@@ -718,6 +728,9 @@ def main():
     ap.add_argument("--chain", action="store_true",
                     help="CIC stack: the FDCNN data flow of section 2.5.1 (one rfft2, FDC + FDP layers on spectra, "
                          "one irfft2); a different function from the per-layer transforms")
+    ap.add_argument("--folded", action="store_true",
+                    help="CIC stack: the per-layer stack's function (the default workload) computed as the chain of "
+                         "--chain with Pi_H between layers, since irfft2 followed by rfft2 is Pi_H")
     ap.add_argument("--classifier", action="store_true",
                     help="CIC stack: one training step of the FDCNN classifier (the chain of --chain, a ReLU, a "
                          "fully connected layer to 2 classes, softmax cross-entropy, Adam)")

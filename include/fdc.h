@@ -142,6 +142,15 @@ fdc_status fdc_cic_fdp_forward(const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *Y, i
 fdc_status fdc_cic_fdp_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX, fdc_c64 *gK,
                                 int B, int C, int S, int N, int M, hipStream_t stream);
 
+/* Pi_H in place: Y [count][H][W/2+1] -> rfft2(irfft2(Y)) (section 2.4.1.1, the inverse
+ * with real-part semantics).  Columns 0 and W/2 become (Y[k][l] + conj(Y[-k mod H][l]))/2;
+ * every other bin is unchanged.  H, W even.  The map is a real-linear orthogonal
+ * projection, so it is also its own adjoint (apply it to a gradient to back-propagate).
+ * Between two layers of a CIC + FDP stack (artifact NONE) the irfft2 of one layer and
+ * the rfft2 of the next reduce to this projection: the FDCNN chain of
+ * fdc_cic_fdp_forward with Pi_H after every layer but the last computes the stack. */
+fdc_status fdc_hermitian_project(fdc_c64 *Y, int64_t count, int H, int W, hipStream_t stream);
+
 /* FDP crops the RFFT-shifted half spectrum: (H-Mh)/2 rows off the top and the
  * bottom, (W-Mw)/2 columns off the right, then shifts back.  In unshifted
  * order it keeps rows [0, Mh/2) and [H-Mh/2, H) and columns [0, Mw/2]; no

@@ -354,6 +354,15 @@ fdc_status fdc_cic_fdp_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c
   return FDC_OK;
 }
 
+fdc_status fdc_hermitian_project(fdc_c64 *Y, int64_t count, int H, int W, hipStream_t s) {
+  if (count < 1 || !even_pos(H) || !even_pos(W))
+    return fail(FDC_EINVAL, "count >= 1 and even H, W required (count=%lld H=%d W=%d)", (long long)count, H, W);
+  if (!Y) return fail(FDC_EINVAL, "Y is NULL");
+  if (count > (1LL << 40) / H) return fail(FDC_EUNSUPPORTED, "too many planes (%lld)", (long long)count);
+  return check_hip(fdc::launch_hermitian_columns(reinterpret_cast<float2 *>(Y), count, H, W / 2 + 1, s),
+                   "hermitian_project");
+}
+
 static fdc_status check_fdp(int64_t count, int H, int W, int Mh, int Mw) {
   if (count < 1) return fail(FDC_EINVAL, "count must be >= 1");
   if (!even_pos(H) || !even_pos(W) || !even_pos(Mh) || !even_pos(Mw))

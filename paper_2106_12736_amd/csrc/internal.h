@@ -219,6 +219,8 @@ struct SpatialBatch {
 // partial sums per output channel of launch_cic_wgrad_stack for an M-point layer
 int cic_wgrad_stack_blocks(int M);
 hipError_t launch_cic_kspec_stack(SpatialBatch sb, hipStream_t s);
+// Pi_H of half spectra [count][H][Wf] in place (columns 0 and Wf-1 only).
+hipError_t launch_hermitian_columns(float2 *Y, long long count, int H, int Wf, hipStream_t s);
 hipError_t launch_cic_wgrad_stack(SpatialBatch sb, hipStream_t s);
 hipError_t launch_cic_kspec(int n_img, const float *w, float2 *K, int S, int n, int M, hipStream_t s);
 hipError_t launch_cic_wgrad(int n_img, const float2 *gK, float *part, float *gw, int S, int n, int M,

@@ -1570,6 +1570,35 @@ __global__ __launch_bounds__(256) void k_cic_fdp_bwd_gk(const float2 *__restrict
   }
 }
 
+// Pi_H in place (the round trip rfft2(irfft2(Y)) of section 2.4.1.1 with the real-part
+// semantics of the inverse): half spectra Y [count][H][Wf], H even; columns 0 and Wf-1
+// become (Y[k][l] + conj(Y[-k mod H][l])) / 2, the others are unchanged.  A thread
+// owns one row pair (k, H - k) of one of the two columns, so the update is in place.
+__global__ __launch_bounds__(256) void k_hermitian_columns(float2 *__restrict__ Y, long long count, int H, int Wf) {
+  const int pairs = H / 2 + 1;
+  const long long total = count * 2 * pairs;
+  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < total; i += (long long)gridDim.x * 256) {
+    const int k = (int)(i % pairs);
+    const long long rest = i / pairs;
+    const int l = (rest & 1) ? Wf - 1 : 0;
+    float2 *col = Y + (rest >> 1) * H * (long long)Wf + l;
+    if (k == 0 || 2 * k == H) {
+      col[(long long)k * Wf].y = 0.f;
+    } else {
+      const float2 a = col[(long long)k * Wf], b = col[(long long)(H - k) * Wf];
+      const float2 p = make_float2(0.5f * (a.x + b.x), 0.5f * (a.y - b.y));
+      col[(long long)k * Wf] = p;
+      col[(long long)(H - k) * Wf] = cconj(p);
+    }
+  }
+}
+
+hipError_t launch_hermitian_columns(float2 *Y, long long count, int H, int Wf, hipStream_t s) {
+  const long long total = count * 2 * (H / 2 + 1);
+  return launch("hermitian_columns", k_hermitian_columns, grid_stride_blocks(total, 256), 256, 0, s, Y, count, H,
+                Wf);
+}
+
 static dim3 plane_grid(long long plane_elems, long long planes) {
   return dim3((unsigned)((plane_elems + 255) / 256), (unsigned)(planes < 65535 ? planes : 65535));
 }

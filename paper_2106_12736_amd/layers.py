@@ -515,6 +515,15 @@ class CicSpatialStackFused(CicStackFused):
 
 
 
+def hermitian_project(Y):
+    """Pi_H in place on half spectra [..][H][W/2+1] (fdc_hermitian_project); returns Y."""
+    if Y.dtype != torch.complex64 or not Y.is_cuda or not Y.is_contiguous() or Y.dim() < 2:
+        raise ValueError("Y must be a contiguous complex64 CUDA tensor [..][H][W/2+1]")
+    H, Wf = Y.shape[-2], Y.shape[-1]
+    call("fdc_hermitian_project", _ptr(Y), Y.numel() // (H * Wf), H, 2 * (Wf - 1), _stream())
+    return Y
+
+
 def cic_fdp_forward(X, K, M):
     """FDC layer of the FDCNN on spectra followed by FDP: [B][C][N][N/2+1] -> [B][S][M][M/2+1]."""
     _check(X, torch.complex64, name="X")
@@ -539,9 +548,15 @@ def cic_fdp_backward(gY, X, K, need_gx=True, need_gk=True):
 class CicChain:
     """The FDCNN data flow of section 2.5.1 on a CIC + FDP stack: one rfft2 of the
     input, every FDC (CIC) + FDP layer on spectra (fdc_cic_fdp_*), one irfft2 of the
-    last spectrum.  All buffers are preallocated, so a step allocates nothing."""
+    last spectrum.  All buffers are preallocated, so a step allocates nothing.
 
-    def __init__(self, batch, sizes, channels, device="cuda"):
+    With hermitian=True, Pi_H (fdc_hermitian_project) follows every layer but the last,
+    and its adjoint (itself) precedes their backward: the irfft2 of one layer and the
+    rfft2 of the next reduce to Pi_H, so this computes the per-layer stack of
+    CicStack / CicStackFused (artifact NONE) with one transform at each end."""
+
+    def __init__(self, batch, sizes, channels, device="cuda", hermitian=False):
+        self.hermitian = bool(hermitian)
         self.batch, self.sizes, self.channels = batch, tuple(sizes), tuple(channels)
         self.layers = len(sizes) - 1
         self.device = torch.device(device)
@@ -566,6 +581,9 @@ class CicChain:
             _check(K, torch.complex64, (self.channels[i + 1], self.sizes[i], self.sizes[i] // 2 + 1), f"K[{i}]")
             call("fdc_cic_fdp_forward", _ptr(self.specs[i]), _ptr(K), _ptr(self.specs[i + 1]), B, self.channels[i],
                  self.channels[i + 1], self.sizes[i], self.sizes[i + 1], s)
+            if self.hermitian and i + 1 < self.layers:
+                m = self.sizes[i + 1]
+                call("fdc_hermitian_project", _ptr(self.specs[i + 1]), B * self.channels[i + 1], m, m, s)
         call("fdc_irfft2", self.plan_out._p, _ptr(self.specs[-1]), _ptr(self.out), _ptr(self.ws), self.ws.numel(), s)
         return self.out
 
@@ -577,6 +595,9 @@ class CicChain:
         call("fdc_irfft2_backward", self.plan_out._p, _ptr(gy), _ptr(self.gspecs[-1]), None, 0, s)
         for i in reversed(range(self.layers)):
             need_gx = i > 0 or input_grad is not None
+            if self.hermitian and i + 1 < self.layers:
+                m = self.sizes[i + 1]
+                call("fdc_hermitian_project", _ptr(self.gspecs[i + 1]), B * self.channels[i + 1], m, m, s)
             call("fdc_cic_fdp_backward", _ptr(self.gspecs[i + 1]), _ptr(self.specs[i]), _ptr(kernels[i]),
                  _ptr(self.gspecs[i] if need_gx else None), _ptr(self.gks[i]), B, self.channels[i],
                  self.channels[i + 1], self.sizes[i], self.sizes[i + 1], s)

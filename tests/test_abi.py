@@ -307,6 +307,14 @@ def test_stack_plan_sizes_and_argument_checks():
     assert _lib.status("fdc_cic_stack_forward", p, d, arr, d, None, d, 1 << 40, None) == FDC_EINVAL
 
 
+def test_hermitian_project_validation():
+    d = ctypes.c_void_p(0x1000)
+    assert _lib.status("fdc_hermitian_project", d, 0, 8, 8, None) == FDC_EINVAL   # no planes
+    assert _lib.status("fdc_hermitian_project", d, 2, 7, 8, None) == FDC_EINVAL   # odd H
+    assert _lib.status("fdc_hermitian_project", d, 2, 8, 5, None) == FDC_EINVAL   # odd W
+    assert _lib.status("fdc_hermitian_project", None, 2, 8, 8, None) == FDC_EINVAL
+
+
 def test_cic_fdp_validation():
     d = ctypes.c_void_p(0x1000)
     assert _lib.status("fdc_cic_fdp_forward", d, d, d, 2, 3, 4, 8, 4, None) == FDC_EINVAL  # S mod C

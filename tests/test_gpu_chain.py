@@ -66,6 +66,37 @@ def test_chain_forward_backward(wl):
     assert_parity(to_np(gin), gx_ref, "gx")
 
 
+@pytest.mark.parametrize("wl", inputs.CIC_WORKLOADS, ids=lambda w: w.name)
+def test_chain_with_projection_is_the_stack(wl):
+    """The chain with Pi_H after every layer but the last computes the per-layer stack
+    (rfft2 -> CIC -> FDP -> irfft2 for every layer): against the oracle's layer-by-layer
+    stack, and against the GPU's stack executor on the same inputs."""
+    print(f"chain + Pi_H {wl.name}", flush=True)
+    d = inputs.make_cic_stack(wl)
+    x = torch.from_numpy(d.x).cuda()
+    Ks = [torch.from_numpy(k).cuda() for k in d.kernels]
+    g = torch.from_numpy(d.grad).cuda()
+    ch = layers.CicChain(wl.batch, wl.sizes, wl.channels, hermitian=True)
+    gin = torch.empty_like(x)
+    ch.forward(x, Ks)
+    ch.backward(g, Ks, input_grad=gin)
+    st = layers.CicStackFused(wl.batch, wl.sizes, wl.channels)
+    gin_st = torch.empty_like(x)
+    st.forward(x, Ks)
+    st.backward(g, Ks, input_grad=gin_st)
+    torch.cuda.synchronize()
+    kd = [k.astype(np.complex128) for k in d.kernels]
+    y_ref, saved = fdc.cic_stack_forward(d.x.astype(np.float64), kd, wl.sizes)
+    gks_ref, gx_ref = fdc.cic_stack_backward(d.grad.astype(np.float64), saved, kd, wl.sizes, want_input_grad=True)
+    assert_parity(to_np(ch.out), y_ref, "y")
+    assert_parity(to_np(st.out), y_ref, "y (stack executor)")
+    for i in range(wl.layers):
+        assert_parity(to_np(ch.gks[i]), gks_ref[i], f"dK[{i}]")
+        assert_parity(to_np(st.gks[i]), gks_ref[i], f"dK[{i}] (stack executor)")
+    assert_parity(to_np(gin), gx_ref, "gx")
+    assert_parity(to_np(gin_st), gx_ref, "gx (stack executor)")
+
+
 def test_chain_graph_replays():
     wl = inputs.STACK512
     d = inputs.make_cic_stack(wl)

@@ -66,6 +66,26 @@ def test_fft_small_planes_many_per_workgroup(n, count):
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("count,H,W", [(1, 2, 2), (3, 8, 8), (2, 16, 32), (5, 64, 32), (4, 224, 224), (2, 1024, 1024)])
+def test_hermitian_project(count, H, W):
+    rng = _rng("pi_h", count, H, W)
+    Y = _crand(rng, (count, H, W // 2 + 1))
+    got = to_np(layers.hermitian_project(_gpu(Y)))
+    ref = dft.hermitian_projection(Y.astype(np.complex128))
+    assert_parity(got, ref, "Pi_H")
+    # untouched columns are bit-exact copies, and the projected columns are Hermitian exactly
+    assert np.array_equal(got[..., 1:-1], Y[..., 1:-1])
+    neg = (-np.arange(H)) % H
+    for l in (0, W // 2):
+        assert np.array_equal(got[..., :, l], np.conj(got[..., neg, l]))
+    # Pi_H(irfft2's input) leaves irfft2 unchanged, and rfft2 of a real image is a fixed point
+    plan = layers.FftPlan(count, H, W)
+    assert_parity(to_np(plan.irfft2(_gpu(got))), dft.irfft2(Y.astype(np.complex128), H, W), "irfft2(Pi_H Y)")
+    X = to_np(plan.rfft2(_gpu(rng.standard_normal((count, H, W)).astype(np.float32))))
+    assert_parity(to_np(layers.hermitian_project(_gpu(X))), X.astype(np.complex128), "Pi_H(rfft2 x)")
+    torch.cuda.synchronize()
+
+
 def test_fft_structured_inputs():
     # impulse, constant and a single cosine through the 1024 x 1024 plan
     h = w = 1024
