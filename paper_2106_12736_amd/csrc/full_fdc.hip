@@ -321,7 +321,11 @@ struct GwRun {
 // workgroup (the four waves read each operand row twice: waves 0/1 share s rows, 0/2
 // share c rows).
 constexpr int kGwStageRow = 5;
-constexpr int kGwStageElems = 2 * 4 * 32 * kGwStageRow;
+// X rows start 8 elements (16 banks of 4 bytes) after the G rows: the staging writes of
+// a 16-lane group (8 rows of G and the same 8 rows of X) then fall on distinct banks
+// (with the two blocks a multiple of 32 banks apart every write was a 2-way conflict)
+constexpr int kGwStageUnit = 4 * 32 * kGwStageRow + 8;
+constexpr int kGwStageElems = 2 * kGwStageUnit;
 
 // EVEN: the batch takes an even number of 4-row steps (B rounded up to 4 is a multiple
 // of 8), which allows the run-by-run loop.
@@ -392,7 +396,7 @@ __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, 
   auto stage_and_multiply = [&](float4(&r)[2], int buf) __attribute__((always_inline)) {
     // (the barrier below also ends every wave's reads of this buffer two steps ago)
     {
-      float2 *d = stage + buf * SE + unit * (4 * 32 * SR) + (lb * 32 + lr) * SR;
+      float2 *d = stage + buf * SE + unit * kGwStageUnit + (lb * 32 + lr) * SR;
       if (b0 + lb < B) {
         d[0] = make_float2(r[0].x, r[0].y), d[1] = make_float2(r[0].z, r[0].w);
         d[2] = make_float2(r[1].x, r[1].y), d[3] = make_float2(r[1].z, r[1].w);
@@ -403,7 +407,7 @@ __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, 
     __syncthreads();
     load_next(r);
     const float2 *ag = stage + buf * SE + (kq * 32 + (s0 - sbase) + mrow) * SR;
-    const float2 *ax = stage + buf * SE + 4 * 32 * SR + (kq * 32 + (c0 - cbase) + mrow) * SR;
+    const float2 *ax = stage + buf * SE + kGwStageUnit + (kq * 32 + (c0 - cbase) + mrow) * SR;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const float2 g2 = ag[q], x2 = ax[q];
