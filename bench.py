@@ -191,6 +191,16 @@ def fft2_launches(n, planes, inverse):
     return [(f"row_r2c_{n}", real + spec), (f"col_fft_fwd_{n}", 2 * spec)]
 
 
+def pooled_rfft2_launches(n, m, planes):
+    """(kernel name, algorithmic bytes) of fdc_rfft2_pooled: n x n planes to the bins an
+    FDP to m x m keeps (m/2+1 columns of every row, then m rows of those columns)."""
+    if n in (16, 32, 64) or m == n:
+        return fft2_launches(n, planes, inverse=False)
+    L = m // 2 + 1
+    real = F32 * planes * n * n
+    return [(f"row_r2c_{n}", real + C64 * planes * n * L), (f"col_fft_fwd_{n}", C64 * planes * (n + m) * L)]
+
+
 def chain_step_launches(wl, input_grad=False, hermitian=False):
     """(kernel name, algorithmic bytes) of every launch of one step of the FDCNN chain
     (one rfft2, every FDC + FDP layer on spectra, one irfft2, and the backward); with
@@ -203,7 +213,7 @@ def chain_step_launches(wl, input_grad=False, hermitian=False):
     NF0 = N0 // 2 + 1
     ML, CL = wl.sizes[-1], wl.channels[-1]
     MFL = ML // 2 + 1
-    out += fft2_launches(N0, B * C0, inverse=False)
+    out += pooled_rfft2_launches(N0, wl.sizes[1], B * C0)
     def pi_h(i):
         B_, _, S_, _, M_, _, _ = layer_dims(wl, i)
         return ("hermitian_columns", 2 * C64 * B_ * S_ * 2 * M_)
@@ -741,6 +751,8 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the timed region, run one plain streaming copy kernel (dst = src * 1) over "
                          "MIB MiB, a known-size reference for the HBM traffic counters of a profiler run")
+    ap.add_argument("--launch-table", action="store_true",
+                    help="print every launch of the instrumented step (work, duration, rate) to stderr")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -792,6 +804,11 @@ def main():
     for (name, amount, unit), (_, ms) in zip(launches, recs):
         t, a, n, _ = per_name.get(name, (0.0, 0, 0, unit))
         per_name[name] = (t + float(ms), a + amount, n + 1, unit)
+    if args.launch_table:
+        for i, ((name, amount, unit), (_, ms)) in enumerate(zip(launches, recs)):
+            rate = amount / (float(ms) * 1e-3) / (1e12 if unit == "flop" else 1e9)
+            print(f"launch {i:3d} {name:32s} {amount:14.0f} {unit:6s} {float(ms) * 1e3:9.2f} us "
+                  f"{rate:9.1f} {'TFLOP/s' if unit == 'flop' else 'GB/s'}", file=sys.stderr)
     dominant = max(per_name, key=lambda k: per_name[k][0])
     dom_amount_per_step, dom_launches_per_step, dom_unit = per_name[dominant][1:]
 

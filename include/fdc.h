@@ -112,6 +112,17 @@ fdc_status fdc_rfft2_backward(const fdc_fft_plan *plan, const fdc_c64 *gX, float
 /* Adjoint of fdc_irfft2: gX[k][l] = (c_l / (h w)) * rfft2(gx)[k][l]. */
 fdc_status fdc_irfft2_backward(const fdc_fft_plan *plan, const float *gx, fdc_c64 *gX,
                                void *ws, size_t ws_bytes, hipStream_t stream);
+/* fdc_rfft2 restricted to the bins that Frequency Domain Pooling to mh x mw keeps
+ * (section 2.4.2): X[i][k][l] for l <= mw/2 and k < mh/2 or k >= h - mh/2, each with
+ * the value fdc_rfft2 gives it.  The other bins of X are undefined on return (left as
+ * they were or written).  mh and mw even, 2 <= mh <= h, 2 <= mw <= w (FDC_EINVAL
+ * otherwise); mh = h, mw = w is fdc_rfft2.  The first FDC + FDP layer of an FDCNN
+ * (section 2.5.1) reads only these bins of its input spectrum (fdc_cic_fdp_forward and
+ * fdc_cic_fdp_backward with N = h = w, M = mh = mw), so its input transform needs no
+ * others: the row pass forms mw/2 + 1 bins of every row, the column pass transforms
+ * those columns and stores the mh kept rows.  No workspace. */
+fdc_status fdc_rfft2_pooled(const fdc_fft_plan *plan, const float *x, fdc_c64 *X, int mh,
+                            int mw, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Channel Independent Convolution on spectra (Eq. 5, Algorithm 1)          */

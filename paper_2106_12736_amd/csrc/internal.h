@@ -114,7 +114,8 @@ hipError_t launch_row_c2r_r2c(int n, SpecLayout in, int Lin, float a1, float b1,
 // Column DFTs of length n over the first `L` columns of row-major [planes][n][ld] complex
 // data (in place allowed).
 hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long long planes, int L, int ld,
-                          long long in_plane_stride, long long out_plane_stride, hipStream_t s);
+                          long long in_plane_stride, long long out_plane_stride, hipStream_t s,
+                          int keep = 0);  // keep > 0: store only the rows an FDP to keep rows keeps
 // Column DFTs of `planes` split-layout n x (n/2+1) half spectra with the strides of
 // `in` and `out` (in place allowed).
 hipError_t launch_col_fft_split(int n, int dir, SpecLayout in, SpecLayout out, long long planes, hipStream_t s);

@@ -431,7 +431,7 @@ __device__ __forceinline__ ColRef column_ref(int w, int s, int L, int planes, in
 template <int N, int CT, int DIR>
 __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fft(const float2 *in, float2 *out, int L, int ld,
                                                                int planes, long long in_plane_stride,
-                                                               long long out_plane_stride) {
+                                                               long long out_plane_stride, int keep) {
   using Cfg = ColCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
@@ -446,7 +446,10 @@ __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fft(const float2 *in
   if (!c.ok) return;
   float2 *op = out + c.plane * out_plane_stride + c.l;
 #pragma unroll
-  for (int m = 0; m < E; ++m) op[(long long)(t + TPS * m) * ld] = v[m];
+  for (int m = 0; m < E; ++m) {
+    const int k = t + TPS * m;  // only the rows an FDP to `keep` rows keeps (keep = N: all)
+    if (k < keep / 2 || k >= N - keep / 2) op[(long long)k * ld] = v[m];
+  }
 }
 
 // Row of the n-point spectrum that pooled row `mrow` (of m) comes from.
@@ -1214,7 +1217,7 @@ static unsigned col_grid(long long planes, int L, int ct) {
 }
 
 hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long long planes, int L, int ld,
-                          long long in_plane_stride, long long out_plane_stride, hipStream_t s) {
+                          long long in_plane_stride, long long out_plane_stride, hipStream_t s, int keep) {
   hipError_t err = hipErrorInvalidValue;
   dispatch_n(n, [&](auto nc) {
     constexpr int N = decltype(nc)::value;
@@ -1226,10 +1229,10 @@ hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long lo
     static const std::string ni = "col_fft_inv_" + std::to_string(N);
     if (dir < 0)
       err = launch(nf.c_str(), k_col_fft<N, CT, -1>, grid, CT * ColCfg<N>::TPS, lds, s, in, out, L, ld, (int)planes,
-                   in_plane_stride, out_plane_stride);
+                   in_plane_stride, out_plane_stride, keep > 0 ? keep : N);
     else
       err = launch(ni.c_str(), k_col_fft<N, CT, +1>, grid, CT * ColCfg<N>::TPS, lds, s, in, out, L, ld, (int)planes,
-                   in_plane_stride, out_plane_stride);
+                   in_plane_stride, out_plane_stride, keep > 0 ? keep : N);
   });
   return err;
 }

@@ -75,6 +75,16 @@ class FftPlan:
         out = torch.empty(self._spec_shape(tuple(x.shape[:-2])), dtype=torch.complex64, device=x.device)
         return self._run("fdc_rfft2", x, out, None)
 
+    def rfft2_pooled(self, x, mh, mw, out=None):
+        """fdc_rfft2_pooled into `out` (a new tensor if None): the bins an FDP to
+        mh x mw keeps; the others are undefined."""
+        _check(x, torch.float32, name="x")
+        if out is None:
+            out = torch.empty(self._spec_shape(tuple(x.shape[:-2])), dtype=torch.complex64, device=x.device)
+        _check(out, torch.complex64, self._spec_shape(tuple(x.shape[:-2])), "out")
+        call("fdc_rfft2_pooled", self._p, _ptr(x), _ptr(out), mh, mw, _stream())
+        return out
+
     def irfft2(self, X):
         _check(X, torch.complex64, name="X")
         out = torch.empty(tuple(X.shape[:-2]) + (self.h, self.w), dtype=torch.float32, device=X.device)
@@ -550,6 +560,9 @@ class CicChain:
     input, every FDC (CIC) + FDP layer on spectra (fdc_cic_fdp_*), one irfft2 of the
     last spectrum.  All buffers are preallocated, so a step allocates nothing.
 
+    The input transform forms only the bins the first FDP keeps (fdc_rfft2_pooled): the
+    first layer reads no others, forward or backward.
+
     With hermitian=True, Pi_H (fdc_hermitian_project) follows every layer but the last,
     and its adjoint (itself) precedes their backward: the irfft2 of one layer and the
     rfft2 of the next reduce to Pi_H, so this computes the per-layer stack of
@@ -575,7 +588,10 @@ class CicChain:
     def forward(self, x, kernels):
         _check(x, torch.float32, (self.batch, self.channels[0], self.sizes[0], self.sizes[0]), "x")
         s = _stream()
-        call("fdc_rfft2", self.plan_in._p, _ptr(x), _ptr(self.specs[0]), None, 0, s)
+        # the first FDP keeps only some bins of the input spectrum, and the first layer
+        # (forward and backward) reads no others
+        m = self.sizes[1]
+        call("fdc_rfft2_pooled", self.plan_in._p, _ptr(x), _ptr(self.specs[0]), m, m, s)
         B = self.batch
         for i, K in enumerate(kernels):
             _check(K, torch.complex64, (self.channels[i + 1], self.sizes[i], self.sizes[i] // 2 + 1), f"K[{i}]")

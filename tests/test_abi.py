@@ -60,6 +60,10 @@ def test_fft_calls_reject_bad_arguments_before_launch():
     assert _lib.status("fdc_irfft2", p, dummy, dummy, dummy, 10, None) == FDC_EWORKSPACE
     assert _lib.status("fdc_rfft2_backward", p, dummy, None, dummy, 1 << 20, None) == FDC_EINVAL
     assert _lib.status("fdc_rfft2", None, dummy, dummy, None, 0, None) == FDC_EINVAL
+    for mh, mw in ((0, 16), (16, 0), (15, 16), (16, 17), (66, 16), (16, 66), (-2, 16)):
+        assert _lib.status("fdc_rfft2_pooled", p, dummy, dummy, mh, mw, None) == FDC_EINVAL, (mh, mw)
+    assert _lib.status("fdc_rfft2_pooled", p, None, dummy, 16, 16, None) == FDC_EINVAL
+    assert _lib.status("fdc_rfft2_pooled", None, dummy, dummy, 16, 16, None) == FDC_EINVAL
     _lib.status("fdc_fft_plan_destroy", p)
 
 

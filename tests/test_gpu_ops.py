@@ -66,6 +66,34 @@ def test_fft_small_planes_many_per_workgroup(n, count):
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("count,h,w,mh,mw", [
+    (3, 1024, 1024, 512, 512),  # the first layer of the 1024 stack
+    (5, 512, 512, 256, 256), (2, 256, 256, 128, 128), (4, 128, 128, 64, 64),
+    (3, 224, 224, 112, 112),    # radix-7 lengths
+    (2, 128, 64, 32, 48),       # non-square, different kept heights and widths
+    (2, 256, 256, 2, 2),        # one kept row at each end, two kept columns
+    (2, 128, 128, 128, 64),     # every row kept
+    (2, 256, 128, 64, 128),     # every column kept
+    (3, 512, 512, 512, 512),    # everything kept: fdc_rfft2
+    (7, 32, 32, 16, 16),        # one-launch size: every bin formed
+    (1, 8, 16, 4, 8),
+])
+def test_rfft2_pooled(count, h, w, mh, mw):
+    print(f"rfft2_pooled {count} x {h}x{w} -> {mh}x{mw}", flush=True)
+    rng = _rng("rfft2_pooled", count, h, w, mh, mw)
+    plan = layers.FftPlan(count, h, w)
+    x = rng.standard_normal((count, h, w)).astype(np.float32)
+    nan = float("nan")
+    out = torch.full((count, h, w // 2 + 1), complex(nan, nan), dtype=torch.complex64, device="cuda")
+    got = to_np(plan.rfft2_pooled(_gpu(x), mh, mw, out=out))
+    ref = dft.rfft2(x.astype(np.float64))
+    rows = np.r_[0:mh // 2, h - mh // 2:h]
+    cols = np.arange(mw // 2 + 1)
+    # the kept bins only: the others are undefined (left as they were, or row-pass values)
+    assert_parity(got[:, rows][:, :, cols], ref[:, rows][:, :, cols], "kept bins")
+    torch.cuda.synchronize()
+
+
 @pytest.mark.parametrize("count,H,W", [(1, 2, 2), (3, 8, 8), (2, 16, 32), (5, 64, 32), (4, 224, 224), (2, 1024, 1024)])
 def test_hermitian_project(count, H, W):
     rng = _rng("pi_h", count, H, W)
