@@ -29,6 +29,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <string>
 
 namespace fdc {
@@ -387,7 +388,13 @@ __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, 
   float4 ra[2], rb[2];
   load_next(ra);
   load_next(rb);
-  v4f dr[4], di[4];
+  // Up to 3 x 3 taps and with the run-by-run loop, Gauss's form of the complex
+  // product: t1 = sum Gr Xr, t2 = sum Gi Xi and t3 = sum (Gr + Gi)(Xr - Xi) over the
+  // batch, three matrix products per bin instead of four; the run's D = G conj(X) is
+  // then re = t1 + t2, im = t3 - t1 + t2.  (Elsewhere the third accumulator would
+  // cost occupancy or spill, and four products are kept.)
+  constexpr bool kGauss = EVEN && NK <= 3;
+  v4f t1[4], t2[4], t3[4], dr[4], di[4];
   GwRun crun;
   crun.start(r_begin, nmain, H);
   int b0 = 0;  // compute cursor
@@ -411,19 +418,36 @@ __global__ __launch_bounds__(256, 2) void k_full_gw(SpecLayout G, SpecLayout X, 
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const float2 g2 = ag[q], x2 = ax[q];
-      // D = G conj(X):  re = Gr Xr + Gi Xi,  im = Gi Xr - Gr Xi
-      dr[q] = mfma4(g2.x, x2.x, dr[q]);
-      dr[q] = mfma4(g2.y, x2.y, dr[q]);
-      di[q] = mfma4(g2.y, x2.x, di[q]);
-      di[q] = mfma4(-g2.x, x2.y, di[q]);
+      if constexpr (kGauss) {
+        t1[q] = mfma4(g2.x, x2.x, t1[q]);
+        t2[q] = mfma4(g2.y, x2.y, t2[q]);
+        t3[q] = mfma4(g2.x + g2.y, x2.x - x2.y, t3[q]);
+      } else {  // D = G conj(X):  re = Gr Xr + Gi Xi,  im = Gi Xr - Gr Xi
+        dr[q] = mfma4(g2.x, x2.x, dr[q]);
+        dr[q] = mfma4(g2.y, x2.y, dr[q]);
+        di[q] = mfma4(g2.y, x2.x, di[q]);
+        di[q] = mfma4(-g2.x, x2.y, di[q]);
+      }
     }
     b0 += 4;
   };
   auto clear_sums = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) dr[q] = di[q] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < 4; ++q) {
+      if constexpr (kGauss)
+        t1[q] = t2[q] = t3[q] = v4f{0.f, 0.f, 0.f, 0.f};
+      else
+        dr[q] = di[q] = v4f{0.f, 0.f, 0.f, 0.f};
+    }
   };
   auto finish_run = [&]() __attribute__((always_inline)) {  // project the run onto the taps
+    if constexpr (kGauss) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        dr[q] = t1[q] + t2[q];
+        di[q] = (t3[q] - t1[q]) + t2[q];
+      }
+    }
     if (crun.g >= nmain)
       gw_project_run<NK, true>(gw, dr, di, crun.k, crun.l0, tw);
     else
@@ -587,12 +611,16 @@ hipError_t launch_full_contract(bool gx, int nk, SpecLayout in, const float *wt,
 
 // Bin chunks of the dL/dw pass: about 8192 workgroups, so that the workgroups running
 // at one time on an XCD are the tiles of one or two short chunks and share the spectra
-// they read through L2; at most 512 chunks of partial sums.
+// they read through L2, and at most 129 runs (516 bins) per chunk; at most 512 chunks
+// of partial sums.  At 512 pixels and 256 channels the 8192 workgroups alone give 257
+// runs per chunk, which ran 7-25% slower than 129 (and unevenly from run to run, with
+// up to 2.3 times the HBM reads); 128 runs (two whole rows, so that every chunk starts
+// at the same column) ran 30% slower still.
 int full_gw_chunks(int B, int S, int C, int P, int nk) {
   (void)B, (void)nk;
   const int nrun = P * (P / 2) / 4 + P / 4;
   const int tiles = ((S + 31) / 32) * ((C + 31) / 32);
-  int chunks = (8192 + tiles - 1) / tiles;
+  int chunks = std::max((8192 + tiles - 1) / tiles, (nrun + 128) / 129);
   if (chunks > 512) chunks = 512;
   if (chunks > nrun) chunks = nrun;
   if (chunks < 1) chunks = 1;
@@ -609,8 +637,11 @@ hipError_t launch_full_gw(int nk, SpecLayout G, SpecLayout X, const float2 *tw, 
   hipError_t err = hipErrorInvalidValue;
   dispatch_nk(nk, [&](auto nc) {
     constexpr int NK = decltype(nc)::value;
-    const size_t lds = ((size_t)gw_tw_elems<NK>(P) + 2 * kGwStageElems) * sizeof(float2);
+    size_t lds = ((size_t)gw_tw_elems<NK>(P) + 2 * kGwStageElems) * sizeof(float2);
     if (lds > 65536) return;  // (P <= 1024, n <= 5 stays within 60 KB)
+#ifdef FDC_GW_OCC2
+    if (tiles == 64 && lds < 56 * 1024) lds = 56 * 1024;
+#endif
     timing_before("full_gw", s);
     if (((B + 3) / 4) % 2 == 0)
       hipLaunchKernelGGL((k_full_gw<NK, true>), dim3((unsigned)(tiles * chunks)), dim3(256), lds, s, G, X, tw, part, B,
