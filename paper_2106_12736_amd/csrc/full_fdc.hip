@@ -611,16 +611,18 @@ hipError_t launch_full_contract(bool gx, int nk, SpecLayout in, const float *wt,
 
 // Bin chunks of the dL/dw pass: about 8192 workgroups, so that the workgroups running
 // at one time on an XCD are the tiles of one or two short chunks and share the spectra
-// they read through L2, and at most 129 runs (516 bins) per chunk; at most 512 chunks
-// of partial sums.  At 512 pixels and 256 channels the 8192 workgroups alone give 257
-// runs per chunk, which ran 7-25% slower than 129 (and unevenly from run to run, with
-// up to 2.3 times the HBM reads); 128 runs (two whole rows, so that every chunk starts
-// at the same column) ran 30% slower still.
+// they read through L2, and at most 97 runs (388 bins) per chunk; at most 512 chunks of
+// partial sums.  At 512 pixels and 256 channels (64 tiles) the pass took 13.3-13.8 ms
+// with 97 or 129 runs per chunk, 15.1 ms with 65, 17-22 ms with 128 (two whole rows:
+// every chunk starts at the same column), 22-24 ms with 161 or 193, and 15-19 ms, uneven
+// from run to run and with 2.3 times the HBM reads, with the 257 that 8192 workgroups
+// alone give.
+constexpr int kGwMaxRunsPerChunk = 97;
 int full_gw_chunks(int B, int S, int C, int P, int nk) {
   (void)B, (void)nk;
   const int nrun = P * (P / 2) / 4 + P / 4;
   const int tiles = ((S + 31) / 32) * ((C + 31) / 32);
-  int chunks = std::max((8192 + tiles - 1) / tiles, (nrun + 128) / 129);
+  int chunks = std::max((8192 + tiles - 1) / tiles, (nrun + kGwMaxRunsPerChunk - 1) / kGwMaxRunsPerChunk);
   if (chunks > 512) chunks = 512;
   if (chunks > nrun) chunks = nrun;
   if (chunks < 1) chunks = 1;

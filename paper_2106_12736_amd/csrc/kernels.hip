@@ -669,9 +669,16 @@ constexpr int fwd_cic_lds_elems() {
 constexpr int kGkCT = 8;
 // Workgroups the dK launch aims for before it cuts the batch into ranges.
 constexpr long long kGkTargetWgs = 512;
+// At 512 points the tiles are 4 columns wide, one 256-thread workgroup each (two or more
+// per CU instead of one 512-thread workgroup): 2% faster at 8 images of 1024^2 (41.0
+// against 41.9 us; 2-column tiles took 45.1).
+template <int M>
+constexpr int gk_ct() {
+  return M == 512 ? 4 : kGkCT;
+}
 template <int M>
 constexpr int gk_bp() {
-  constexpr int bp = 512 / (kGkCT * ColCfg<M>::TPS);
+  constexpr int bp = (M == 512 ? 256 : 512) / (gk_ct<M>() * ColCfg<M>::TPS);
   return bp < 1 ? 1 : (bp > 8 ? 8 : bp);
 }
 
@@ -1323,7 +1330,7 @@ int gk_batch_ranges(int n, int m, int B, int S, long long part_elems) {
   dispatch_n(m, [&](auto mc) {
     constexpr int M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
-    constexpr int CT = col_ct_for(kGkCT, L), BP = gk_bp<M>();
+    constexpr int CT = col_ct_for(gk_ct<M>(), L), BP = gk_bp<M>();
     const long long tiles = col_tile_count(S, L, CT);
     // enough workgroups to fill the chip (kGkTargetWgs), at least BP batch entries per
     // range, and range sums (written and read once more) of at most a quarter of Tg
@@ -1348,7 +1355,7 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
   dispatch_n(m, [&](auto mc) {
     constexpr int M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
-    constexpr int CT = col_ct_for(kGkCT, L), BP = gk_bp<M>();
+    constexpr int CT = col_ct_for(gk_ct<M>(), L), BP = gk_bp<M>();
     const size_t lds = (twiddle_lds_elems<M>() + lds_size<kColLds>(BP * M * CT)) * sizeof(float2);
     const unsigned tiles = col_grid(S, L, CT);
     if (tiles == 0) return;
@@ -1374,7 +1381,7 @@ hipError_t launch_col_bwd_dk_dx(int n, int m, const float2 *Tg, const float2 *Xh
   dispatch_nm(n, m, [&](auto nc, auto mc) {
     constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
-    constexpr int CTK = col_ct_for(kGkCT, L), BP = gk_bp<M>(), CTX = col_ct_for(col_ct_gx<N>(), L);
+    constexpr int CTK = col_ct_for(gk_ct<M>(), L), BP = gk_bp<M>(), CTX = col_ct_for(col_ct_gx<N>(), L);
     constexpr int NT = CTK * ColCfg<M>::TPS * BP, NX = CTX * ColCfg<N>::TPS;
     if constexpr (NX <= NT && NT % NX == 0) {
       constexpr int PACK = NT / NX;
@@ -1399,7 +1406,7 @@ bool col_bwd_dk_dx_supported(int n, int m) {
   dispatch_nm(n, m, [&](auto nc, auto mc) {
     constexpr int N = decltype(nc)::value, M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
-    constexpr int CTK = col_ct_for(kGkCT, L), BP = gk_bp<M>(), CTX = col_ct_for(col_ct_gx<N>(), L);
+    constexpr int CTK = col_ct_for(gk_ct<M>(), L), BP = gk_bp<M>(), CTX = col_ct_for(col_ct_gx<N>(), L);
     constexpr int NT = CTK * ColCfg<M>::TPS * BP, NX = CTX * ColCfg<N>::TPS;
     ok = NX <= NT && NT % NX == 0;
   });
@@ -1458,11 +1465,13 @@ constexpr int kChainImages = 8;
 // the bins FDP keeps: Y [B][S][M][M/2+1] from X [B][C][N][N/2+1], K [S][N][N/2+1].
 // Kept rows of the N-point spectrum: k < M/2 and k >= N - M/2 (output row k or
 // k - (N - M)); kept columns l <= M/2.  Grid: x over an output plane's bin pairs in
-// order (contiguous stores), y over the output channels; a thread loads its two kernel
-// bins once and forms them for every image.
+// order (contiguous stores), y over groups of JB output channels of one input channel
+// (o = c J + j): a thread loads its two bins of X[b][c] once for the group's JB
+// outputs, and each output's two kernel bins once for every image.
+template <int JB>
 __global__ __launch_bounds__(256) void k_cic_fdp_fwd(const float2 *__restrict__ X, const float2 *__restrict__ K,
                                                      float2 *__restrict__ Y, int B, int C, int J, int N, int M) {
-  const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1, pe = M * Lm;
+  const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1, pe = M * Lm, JG = J / JB;
   const int e0 = 2 * (blockIdx.x * 256 + threadIdx.x);
   if (e0 >= pe) return;
   const BinPair q(e0, Lm, 1.f / (float)Lm);
@@ -1470,11 +1479,16 @@ __global__ __launch_bounds__(256) void k_cic_fdp_fwd(const float2 *__restrict__ 
 #pragma unroll
   for (int h = 0; h < 2; ++h) off[h] = (q.k[h] < M / 2 ? q.k[h] : q.k[h] + (N - M)) * NF + q.l[h];
   const long long xs = (long long)C * N * NF, ys = (long long)S * (pe / 2);  // image strides (float2, float4)
-  for (int o = blockIdx.y; o < S; o += gridDim.y) {
-    const float2 *ko = K + (long long)o * N * NF;
-    const float2 kv0 = ko[off[0]], kv1 = ko[off[1]];
-    const float2 *xo = X + (long long)(o / J) * N * NF;
-    float4 *yo = reinterpret_cast<float4 *>(Y + (long long)o * pe + e0);
+  for (int gi = blockIdx.y; gi < C * JG; gi += gridDim.y) {
+    const int c = gi / JG, o0 = c * J + (gi - c * JG) * JB;
+    const float2 *xo = X + (long long)c * N * NF;
+    float2 kv[JB][2];
+#pragma unroll
+    for (int jj = 0; jj < JB; ++jj) {
+      const float2 *ko = K + (long long)(o0 + jj) * N * NF;
+      kv[jj][0] = ko[off[0]], kv[jj][1] = ko[off[1]];
+    }
+    float4 *yo = reinterpret_cast<float4 *>(Y + (long long)o0 * pe + e0);
     int b = 0;
     for (; b + kChainImages <= B; b += kChainImages) {
       float2 a0[kChainImages], a1[kChainImages];
@@ -1484,9 +1498,16 @@ __global__ __launch_bounds__(256) void k_cic_fdp_fwd(const float2 *__restrict__ 
         a1[u] = xo[(b + u) * xs + off[1]];
       }
 #pragma unroll
-      for (int u = 0; u < kChainImages; ++u) yo[(b + u) * ys] = pack2(cmul(a0[u], kv0), cmul(a1[u], kv1));
+      for (int jj = 0; jj < JB; ++jj)
+#pragma unroll
+        for (int u = 0; u < kChainImages; ++u)
+          yo[(b + u) * ys + jj * (pe / 2)] = pack2(cmul(a0[u], kv[jj][0]), cmul(a1[u], kv[jj][1]));
     }
-    for (; b < B; ++b) yo[b * ys] = pack2(cmul(xo[b * xs + off[0]], kv0), cmul(xo[b * xs + off[1]], kv1));
+    for (; b < B; ++b) {
+      const float2 a0 = xo[b * xs + off[0]], a1 = xo[b * xs + off[1]];
+#pragma unroll
+      for (int jj = 0; jj < JB; ++jj) yo[b * ys + jj * (pe / 2)] = pack2(cmul(a0, kv[jj][0]), cmul(a1, kv[jj][1]));
+    }
   }
 }
 
@@ -1606,12 +1627,37 @@ static dim3 plane_grid(long long plane_elems, long long planes) {
   return dim3((unsigned)((plane_elems + 255) / 256), (unsigned)(planes < 65535 ? planes : 65535));
 }
 
+// Output channels per thread of the chain's forward: the largest of 8, 4, 2 dividing J
+// that leaves at least 512 workgroups (the input bins are loaded J / JB times), else 1.
+// (Minimum 256 or 1024 workgroups instead: 0.2202 and 0.2235 ms per chain step
+// against 0.2197.)
+static int fdp_fwd_jb(long long gx, int C, int J) {
+  for (int jb = 8; jb > 1; jb /= 2)
+    if (J % jb == 0 && gx * C * (J / jb) >= 512) return jb;
+  return 1;
+}
+template <typename F>
+static void dispatch_jb(int jb, F &&f) {
+  switch (jb) {
+    case 8: f(std::integral_constant<int, 8>{}); break;
+    case 4: f(std::integral_constant<int, 4>{}); break;
+    case 2: f(std::integral_constant<int, 2>{}); break;
+    default: f(std::integral_constant<int, 1>{});
+  }
+}
+
 hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, int N, int M,
                               hipStream_t s) {
   if ((long long)N * (N / 2 + 1) >= (1 << 24)) return hipErrorInvalidValue;
+  const int J = S / C;
+  const dim3 g0 = plane_grid((long long)M * (M / 2 + 1) / 2, 1);
+  const int jb = fdp_fwd_jb(g0.x, C, J);
   timing_before("cic_fdp_fwd", s);
-  hipLaunchKernelGGL(k_cic_fdp_fwd, plane_grid((long long)M * (M / 2 + 1) / 2, S), dim3(256), 0, s, X, K, Y, B, C, S / C,
-                     N, M);
+  dispatch_jb(jb, [&](auto jc) {
+    constexpr int JB = decltype(jc)::value;
+    hipLaunchKernelGGL(k_cic_fdp_fwd<JB>, plane_grid((long long)M * (M / 2 + 1) / 2, (long long)C * (J / JB)),
+                       dim3(256), 0, s, X, K, Y, B, C, J, N, M);
+  });
   const hipError_t e = hipGetLastError();
   timing_after("cic_fdp_fwd", s);
   return e;

@@ -11,7 +11,7 @@ import pytest
 import torch
 
 from _parity import assert_parity, to_np
-from oracle import classifier
+from oracle import classifier, fdc
 from paper_2106_12736_amd import inputs, layers
 from paper_2106_12736_amd._lib import call
 
@@ -121,6 +121,28 @@ def _classifier_setup(wl, classes=2, lr=1e-5):
     return d, clf, W, bias, labels
 
 
+# Chain outputs within this fraction of the largest |output| of zero: the ReLU's
+# decision there is within the fp32 error of the chain (rel-L2 about 1e-7 at 1024^2).
+RELU_AMBIGUOUS = 1e-5
+
+
+def _reference_gradients(d, kd, W, bias, labels, wl, out_gpu):
+    """classifier.classifier_gradients, with the ReLU decision (y > 0, a per-element
+    choice) taken from the GPU's fp32 chain output where the float64 output is within
+    the fp32 error of zero, and checked against the float64 decision everywhere else."""
+    y, saved = fdc.cic_chain_forward(d.x.astype(np.float64), kd, wl.sizes)
+    amb = np.abs(y) <= RELU_AMBIGUOUS * np.abs(y).max()
+    assert amb.sum() <= 1e-3 * amb.size, int(amb.sum())
+    assert np.array_equal((out_gpu > 0)[~amb], (y > 0)[~amb]), "ReLU decisions differ away from zero"
+    y_dec = np.where(amb, out_gpu.astype(np.float64), y)  # same decisions as the GPU, |change| <= the threshold
+    B = y.shape[0]
+    logits, loss = classifier.head_forward(y_dec.reshape(B, -1), W.astype(np.float64), bias.astype(np.float64),
+                                           labels)
+    gy, gW, gbias = classifier.head_backward(y_dec.reshape(B, -1), W.astype(np.float64), logits, labels)
+    gks, _ = fdc.cic_chain_backward(gy.reshape(y.shape), saved, kd, wl.sizes)
+    return loss, logits, gks, gW, gbias
+
+
 @pytest.mark.parametrize("wl", inputs.CIC_WORKLOADS, ids=lambda w: w.name)
 def test_classifier_step(wl):
     """One training step at full size on every CIC workload (cic_stack_1024 is the one
@@ -141,8 +163,7 @@ def test_classifier_step(wl):
     torch.cuda.synchronize()
 
     kd = [k.astype(np.complex128) for k in d.kernels]
-    r_loss, r_logits, r_gks, r_gW, r_gb = classifier.classifier_gradients(
-        d.x.astype(np.float64), kd, W.astype(np.float64), bias.astype(np.float64), labels, wl.sizes)
+    r_loss, r_logits, r_gks, r_gW, r_gb = _reference_gradients(d, kd, W, bias, labels, wl, to_np(clf.chain.out))
     assert_parity(logits, r_logits, "logits")
     assert abs(loss - r_loss) <= 1e-5 * max(1.0, abs(r_loss)), (loss, r_loss)
     for i, (g, r) in enumerate(zip(gks, r_gks)):
