@@ -341,6 +341,9 @@ static fdc_status check_cic_fdp(int B, int C, int S, int N, int M) {
     return fail(FDC_EINVAL, "N and M must be positive and even with M <= N (N=%d M=%d)", N, M);
   if (!fdc::cic_fdp_size_supported(N))
     return fail(FDC_EUNSUPPORTED, "spectrum of %d x %d bins exceeds the kernels' bin indexing", N, N / 2 + 1);
+  // the dK grid (256-bin blocks of an N-plane times S channels) is one-dimensional
+  if ((((long long)N * (N / 2 + 1) + 255) / 256) * S >= (1LL << 31))
+    return fail(FDC_EUNSUPPORTED, "S = %d channels of %d x %d bins exceed the kernels' grid", S, N, N / 2 + 1);
   return FDC_OK;
 }
 

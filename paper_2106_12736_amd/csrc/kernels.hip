@@ -1465,21 +1465,25 @@ constexpr int kChainImages = 8;
 // the bins FDP keeps: Y [B][S][M][M/2+1] from X [B][C][N][N/2+1], K [S][N][N/2+1].
 // Kept rows of the N-point spectrum: k < M/2 and k >= N - M/2 (output row k or
 // k - (N - M)); kept columns l <= M/2.  Grid: x over an output plane's bin pairs in
-// order (contiguous stores), y over groups of JB output channels of one input channel
+// order (contiguous stores) times groups of JB output channels of one input channel
 // (o = c J + j): a thread loads its two bins of X[b][c] once for the group's JB
 // outputs, and each output's two kernel bins once for every image.
 template <int JB>
 __global__ __launch_bounds__(256) void k_cic_fdp_fwd(const float2 *__restrict__ X, const float2 *__restrict__ K,
                                                      float2 *__restrict__ Y, int B, int C, int J, int N, int M) {
   const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1, pe = M * Lm, JG = J / JB;
-  const int e0 = 2 * (blockIdx.x * 256 + threadIdx.x);
+  // one group of one block of bin pairs per workgroup, the groups of a block consecutive
+  // after the XCD remap, so that the J / JB groups reading the same input bins run
+  // together on one XCD and share them through its L2
+  const int lin = xcd_remap(blockIdx.x, gridDim.x), gi = lin % (C * JG);
+  const int e0 = 2 * ((lin / (C * JG)) * 256 + threadIdx.x);
   if (e0 >= pe) return;
   const BinPair q(e0, Lm, 1.f / (float)Lm);
   int off[2];  // bin offsets in an N-plane
 #pragma unroll
   for (int h = 0; h < 2; ++h) off[h] = (q.k[h] < M / 2 ? q.k[h] : q.k[h] + (N - M)) * NF + q.l[h];
   const long long xs = (long long)C * N * NF, ys = (long long)S * (pe / 2);  // image strides (float2, float4)
-  for (int gi = blockIdx.y; gi < C * JG; gi += gridDim.y) {
+  {
     const int c = gi / JG, o0 = c * J + (gi - c * JG) * JB;
     const float2 *xo = X + (long long)c * N * NF;
     float2 kv[JB][2];
@@ -1570,7 +1574,10 @@ __global__ __launch_bounds__(256) void k_cic_fdp_bwd_gx(const float2 *__restrict
 }
 
 // dK [S][N][N/2+1] = sum_b gY conj(X) at the kept bins (batch summed in order), exact
-// zeros at the bins FDP drops.
+// zeros at the bins FDP drops.  Grid: x over the bins of a plane, y over the output
+// channels, so that each channel's planes are streamed in order.  (The J channels of
+// one input channel side by side on one XCD, sharing its bins through L2, or one
+// thread for several of them: 76-79 -> 97-101 and 83-97 us at 1024^2.)
 __global__ __launch_bounds__(256) void k_cic_fdp_bwd_gk(const float2 *__restrict__ gY, const float2 *__restrict__ X,
                                                         float2 *__restrict__ gK, int B, int C, int J, int N, int M,
                                                         long long planes) {
@@ -1651,12 +1658,13 @@ hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B
   if ((long long)N * (N / 2 + 1) >= (1 << 24)) return hipErrorInvalidValue;
   const int J = S / C;
   const dim3 g0 = plane_grid((long long)M * (M / 2 + 1) / 2, 1);
+  if ((long long)g0.x * S >= (1LL << 31)) return hipErrorInvalidValue;
   const int jb = fdp_fwd_jb(g0.x, C, J);
   timing_before("cic_fdp_fwd", s);
   dispatch_jb(jb, [&](auto jc) {
     constexpr int JB = decltype(jc)::value;
-    hipLaunchKernelGGL(k_cic_fdp_fwd<JB>, plane_grid((long long)M * (M / 2 + 1) / 2, (long long)C * (J / JB)),
-                       dim3(256), 0, s, X, K, Y, B, C, J, N, M);
+    hipLaunchKernelGGL(k_cic_fdp_fwd<JB>, dim3((unsigned)(g0.x * (long long)C * (J / JB))), dim3(256), 0, s, X, K, Y,
+                       B, C, J, N, M);
   });
   const hipError_t e = hipGetLastError();
   timing_after("cic_fdp_fwd", s);

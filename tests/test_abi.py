@@ -331,6 +331,10 @@ def test_cic_fdp_validation():
     m = ctypes.c_void_p(0x1008)  # 8- but not 16-byte aligned output
     assert _lib.status("fdc_cic_fdp_forward", d, d, m, 2, 1, 4, 8, 4, None) == FDC_EINVAL
     assert _lib.status("fdc_cic_fdp_backward", d, d, d, m, None, 2, 1, 4, 8, 4, None) == FDC_EINVAL
+    # the dK grid: 2052 blocks of a 1024 x 513 plane times S channels must stay below 2^31
+    big = 1 << 20
+    assert _lib.status("fdc_cic_fdp_forward", d, d, d, 1, big, big, 1024, 512, None) == FDC_EUNSUPPORTED
+    assert _lib.status("fdc_cic_fdp_backward", d, d, d, None, d, 1, big, big, 1024, 512, None) == FDC_EUNSUPPORTED
 
 
 def test_dk_ranges_queries():
