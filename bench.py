@@ -228,10 +228,12 @@ def chain_step_launches(wl, input_grad=False, hermitian=False):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
         if hermitian and i + 1 < n:
             out.append(pi_h(i))
+        # dX and dK in one launch: gY, and X at the kept bins, read; all of gK written (zeros
+        # at dropped bins); with dX also K at the kept bins read and all of gX written
+        nb = C64 * (B * S * M * L + B * C * M * L + S * N * NF)
         if i > 0 or input_grad:
-            # reads gY and K at the kept bins, writes all of gX (zeros at dropped bins)
-            out.append(("cic_fdp_bwd_gx", C64 * (B * S * M * L + S * M * L + B * C * N * NF)))
-        out.append(("cic_fdp_bwd_gk", C64 * (B * S * M * L + B * C * M * L + S * N * NF)))
+            nb += C64 * (S * M * L + B * C * N * NF)
+        out.append(("cic_fdp_bwd", nb))
     if input_grad:
         out += fft2_launches(N0, B * C0, inverse=True)
     return out

@@ -341,8 +341,10 @@ static fdc_status check_cic_fdp(int B, int C, int S, int N, int M) {
     return fail(FDC_EINVAL, "N and M must be positive and even with M <= N (N=%d M=%d)", N, M);
   if (!fdc::cic_fdp_size_supported(N))
     return fail(FDC_EUNSUPPORTED, "spectrum of %d x %d bins exceeds the kernels' bin indexing", N, N / 2 + 1);
-  // the dK grid (256-bin blocks of an N-plane times S channels) is one-dimensional
-  if ((((long long)N * (N / 2 + 1) + 255) / 256) * S >= (1LL << 31))
+  // the backward's one-dimensional grid: 256-bin blocks of an N-plane times S channels
+  // (dK) and 256-pair blocks times C channels (dX)
+  const long long pe = (long long)N * (N / 2 + 1);
+  if (((pe + 255) / 256) * S + ((pe / 2 + 255) / 256) * C >= (1LL << 31))
     return fail(FDC_EUNSUPPORTED, "S = %d channels of %d x %d bins exceed the kernels' grid", S, N, N / 2 + 1);
   return FDC_OK;
 }
@@ -362,20 +364,10 @@ fdc_status fdc_cic_fdp_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c
   if (fdc_status st = check_cic_fdp(B, C, S, N, M)) return st;
   if (!gY || (gX && !K) || (gK && !X)) return fail(FDC_EINVAL, "NULL tensor");
   if (gX && !aligned16(gX)) return fail(FDC_EINVAL, "gX must be 16-byte aligned");
-  if (gX) {
-    if (fdc_status st = check_hip(fdc::launch_cic_fdp_bwd_gx(reinterpret_cast<const float2 *>(gY),
-                                                             reinterpret_cast<const float2 *>(K),
-                                                             reinterpret_cast<float2 *>(gX), B, C, S, N, M, s),
-                                  "cic_fdp_backward gX"))
-      return st;
-  }
-  if (gK) {
-    return check_hip(fdc::launch_cic_fdp_bwd_gk(reinterpret_cast<const float2 *>(gY),
-                                                reinterpret_cast<const float2 *>(X), reinterpret_cast<float2 *>(gK),
-                                                B, C, S, N, M, s),
-                     "cic_fdp_backward gK");
-  }
-  return FDC_OK;
+  return check_hip(fdc::launch_cic_fdp_bwd(reinterpret_cast<const float2 *>(gY), reinterpret_cast<const float2 *>(K),
+                                           reinterpret_cast<float2 *>(gX), reinterpret_cast<const float2 *>(X),
+                                           reinterpret_cast<float2 *>(gK), B, C, S, N, M, s),
+                   "cic_fdp_backward");
 }
 
 fdc_status fdc_hermitian_project(fdc_c64 *Y, int64_t count, int H, int W, hipStream_t s) {

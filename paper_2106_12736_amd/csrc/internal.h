@@ -232,10 +232,9 @@ hipError_t launch_cic_wgrad(int n_img, const float2 *gK, float *part, float *gw,
 bool cic_fdp_size_supported(int N);
 hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, int N, int M,
                               hipStream_t s);
-hipError_t launch_cic_fdp_bwd_gx(const float2 *gY, const float2 *K, float2 *gX, int B, int C, int S, int N, int M,
-                                 hipStream_t s);
-hipError_t launch_cic_fdp_bwd_gk(const float2 *gY, const float2 *X, float2 *gK, int B, int C, int S, int N, int M,
-                                 hipStream_t s);
+// gX (NULL: skipped; needs K) and gK (NULL: skipped; needs X) in one launch.
+hipError_t launch_cic_fdp_bwd(const float2 *gY, const float2 *K, float2 *gX, const float2 *X, float2 *gK, int B,
+                              int C, int S, int N, int M, hipStream_t s);
 hipError_t launch_fdp_gather(const float2 *X, float2 *Y, long long count, int H, int Wf, int Mh, int Mwf,
                              hipStream_t s);
 hipError_t launch_fdp_scatter(const float2 *gY, float2 *gX, long long count, int H, int Wf, int Mh, int Mwf,

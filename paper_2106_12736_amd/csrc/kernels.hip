@@ -1440,12 +1440,12 @@ __device__ __forceinline__ int div_small(int e, int d, float rd, int &rem) {
   return q;
 }
 
-// k_cic_fdp_fwd and k_cic_fdp_bwd_gx give each thread two consecutive bins (e0,
+// k_cic_fdp_fwd and the dX blocks of k_cic_fdp_bwd give each thread two consecutive bins (e0,
 // e0 + 1), e0 even, of the plane they write: a plane holds an even number of bins (its
 // row count is even), so the pair is one 16-byte store (the launchers check that the
 // output is 16-byte aligned); the pair may straddle two rows, and inputs are read bin
 // by bin.  (Two bins per lane also for the loads, as 8-byte-aligned 16-byte loads, is
-// slower on gfx950; so is this layout for k_cic_fdp_bwd_gk, whose main stream is its
+// slower on gfx950; so is this layout for the dK blocks, whose main stream is their
 // loads.)
 struct BinPair {
   int k[2], l[2];  // row and column of the two bins in a plane of rows x cols
@@ -1515,15 +1515,19 @@ __global__ __launch_bounds__(256) void k_cic_fdp_fwd(const float2 *__restrict__ 
   }
 }
 
-// Backward of k_cic_fdp_fwd: gX [B][C][N][N/2+1] = sum_j gY conj(K) at the kept bins
-// (j in order), exact zeros at the bins FDP drops.  Grid: x over a plane's bin pairs,
-// y over the input channels; a thread forms its two bins for every image, four images
-// at a time.
-__global__ __launch_bounds__(256) void k_cic_fdp_bwd_gx(const float2 *__restrict__ gY, const float2 *__restrict__ K,
-                                                        float2 *__restrict__ gX, int B, int C, int J, int N, int M) {
+// Backward of k_cic_fdp_fwd, dX and dK of one layer in one launch (both read gY; on
+// the small layers of a chain neither fills the chip alone).
+//
+// dX block (bx, by): gX [B][C][N][N/2+1] = sum_j gY conj(K) at the kept bins (j in
+// order), exact zeros at the bins FDP drops.  bx runs over a plane's bin pairs, by (step
+// ny) over the input channels; a thread forms its two bins for every image, four
+// images at a time.
+__device__ __forceinline__ void fdp_bwd_gx_block(const float2 *__restrict__ gY, const float2 *__restrict__ K,
+                                                 float2 *__restrict__ gX, int B, int C, int J, int N, int M, int bx,
+                                                 int by, int ny) {
   constexpr int BI = 4;
   const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1, pe = N * NF;
-  const int e0 = 2 * (blockIdx.x * 256 + threadIdx.x);
+  const int e0 = 2 * (bx * 256 + threadIdx.x);
   if (e0 >= pe) return;
   const BinPair q(e0, NF, 1.f / (float)NF);
   bool kept[2];
@@ -1538,7 +1542,7 @@ __global__ __launch_bounds__(256) void k_cic_fdp_bwd_gx(const float2 *__restrict
   }
   const long long mpe = (long long)M * Lm, ys = (long long)S * mpe, xs = (long long)C * (pe / 2);
   const long long kps = (long long)N * NF;
-  for (int c = blockIdx.y; c < C; c += gridDim.y) {
+  for (int c = by; c < C; c += ny) {
     float4 *gp = reinterpret_cast<float4 *>(gX + (long long)c * pe + e0);
     if (!kept[0] && !kept[1]) {
       for (int b = 0; b < B; ++b) gp[b * xs] = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -1573,23 +1577,24 @@ __global__ __launch_bounds__(256) void k_cic_fdp_bwd_gx(const float2 *__restrict
   }
 }
 
-// dK [S][N][N/2+1] = sum_b gY conj(X) at the kept bins (batch summed in order), exact
-// zeros at the bins FDP drops.  Grid: x over the bins of a plane, y over the output
-// channels, so that each channel's planes are streamed in order.  (The J channels of
-// one input channel side by side on one XCD, sharing its bins through L2, or one
-// thread for several of them: 76-79 -> 97-101 and 83-97 us at 1024^2.)
-__global__ __launch_bounds__(256) void k_cic_fdp_bwd_gk(const float2 *__restrict__ gY, const float2 *__restrict__ X,
-                                                        float2 *__restrict__ gK, int B, int C, int J, int N, int M,
-                                                        long long planes) {
+// dK block (bx, by): dK [S][N][N/2+1] = sum_b gY conj(X) at the kept bins (batch summed
+// in order), exact zeros at the bins FDP drops.  bx runs over the bins of a plane, by
+// (step ny) over the output channels, so that each channel's planes are streamed in
+// order.  (The J channels of one input channel side by side on one XCD, sharing its
+// bins through L2, or one thread for several of them: 76-79 -> 97-101 and 83-97 us at
+// 1024^2.)
+__device__ __forceinline__ void fdp_bwd_gk_block(const float2 *__restrict__ gY, const float2 *__restrict__ X,
+                                                 float2 *__restrict__ gK, int B, int C, int J, int N, int M, int bx,
+                                                 int by, int ny) {
   const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1, pe = N * NF;
   const float rn = 1.f / (float)NF;
-  const int e = blockIdx.x * 256 + threadIdx.x;
+  const int e = bx * 256 + threadIdx.x;
   if (e >= pe) return;
   int l;
   const int kr = div_small(e, NF, rn, l);
   const bool kept = l < Lm && (kr < M / 2 || kr >= N - M / 2);
   const int k = kr < M / 2 ? kr : kr - (N - M);
-  for (long long o = blockIdx.y; o < planes; o += gridDim.y) {
+  for (long long o = by; o < S; o += ny) {
     float2 acc = make_float2(0.f, 0.f);
     if (kept) {
       const long long c = o / J;
@@ -1598,6 +1603,20 @@ __global__ __launch_bounds__(256) void k_cic_fdp_bwd_gk(const float2 *__restrict
         acc = cfmac(acc, gY[(((long long)b * S + o) * M + k) * Lm + l], X[(((long long)b * C + c) * N + kr) * NF + l]);
     }
     gK[o * pe + e] = acc;
+  }
+}
+
+// Workgroups [0, xbx * xby) run dX blocks, the rest dK blocks (kbx * kby of them).
+__global__ __launch_bounds__(256) void k_cic_fdp_bwd(const float2 *__restrict__ gY, const float2 *__restrict__ K,
+                                                     float2 *__restrict__ gX, const float2 *__restrict__ X,
+                                                     float2 *__restrict__ gK, int B, int C, int J, int N, int M,
+                                                     int xbx, int xby, int kbx, int kby) {
+  const int id = blockIdx.x, nx = xbx * xby;
+  if (id < nx) {
+    fdp_bwd_gx_block(gY, K, gX, B, C, J, N, M, id % xbx, id / xbx, xby);
+  } else {
+    const int i = id - nx;
+    fdp_bwd_gk_block(gY, X, gK, B, C, J, N, M, i % kbx, i / kbx, kby);
   }
 }
 
@@ -1671,26 +1690,20 @@ hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B
   return e;
 }
 
-hipError_t launch_cic_fdp_bwd_gx(const float2 *gY, const float2 *K, float2 *gX, int B, int C, int S, int N, int M,
-                                 hipStream_t s) {
-  if ((long long)N * (N / 2 + 1) >= (1 << 24)) return hipErrorInvalidValue;
-  timing_before("cic_fdp_bwd_gx", s);
-  hipLaunchKernelGGL(k_cic_fdp_bwd_gx, plane_grid((long long)N * (N / 2 + 1) / 2, C), dim3(256), 0, s, gY, K, gX, B, C,
-                     S / C, N, M);
+hipError_t launch_cic_fdp_bwd(const float2 *gY, const float2 *K, float2 *gX, const float2 *X, float2 *gK, int B,
+                              int C, int S, int N, int M, hipStream_t s) {
+  const long long pe = (long long)N * (N / 2 + 1);
+  if (pe >= (1 << 24)) return hipErrorInvalidValue;
+  const long long xbx = gX ? (pe / 2 + 255) / 256 : 0, xby = gX ? C : 0;
+  const long long kbx = gK ? (pe + 255) / 256 : 0, kby = gK ? S : 0;
+  const long long total = xbx * xby + kbx * kby;
+  if (total == 0) return hipSuccess;
+  if (total >= (1LL << 31)) return hipErrorInvalidValue;
+  timing_before("cic_fdp_bwd", s);
+  hipLaunchKernelGGL(k_cic_fdp_bwd, dim3((unsigned)total), dim3(256), 0, s, gY, K, gX, X, gK, B, C, S / C, N, M,
+                     (int)xbx, (int)xby, (int)(kbx > 0 ? kbx : 1), (int)(kby > 0 ? kby : 1));
   const hipError_t e = hipGetLastError();
-  timing_after("cic_fdp_bwd_gx", s);
-  return e;
-}
-
-hipError_t launch_cic_fdp_bwd_gk(const float2 *gY, const float2 *X, float2 *gK, int B, int C, int S, int N, int M,
-                                 hipStream_t s) {
-  if ((long long)N * (N / 2 + 1) >= (1 << 24)) return hipErrorInvalidValue;
-  const long long planes = S;
-  timing_before("cic_fdp_bwd_gk", s);
-  hipLaunchKernelGGL(k_cic_fdp_bwd_gk, plane_grid((long long)N * (N / 2 + 1), planes), dim3(256), 0, s, gY, X, gK, B,
-                     C, S / C, N, M, planes);
-  const hipError_t e = hipGetLastError();
-  timing_after("cic_fdp_bwd_gk", s);
+  timing_after("cic_fdp_bwd", s);
   return e;
 }
 
