@@ -221,6 +221,30 @@ __global__ __launch_bounds__(NT) void k_tail_fwd(SpecLayout in, const float *__r
   float2 *TA = t_lds + G::fTA, *XA = t_lds + G::fXA, *UA = t_lds + G::fUA, *TB = t_lds + G::fTB,
          *XB = t_lds + G::fXB, *UB = t_lds + G::fUB;
 
+  // The kernel bins of stages C and F, loaded now (when each stage is one round of its
+  // column pass, so that this thread's item is known): their loads complete with
+  // stage A's, instead of each stage waiting for its own.
+  constexpr bool PC = JA * LA <= NT / Plan<MA>::TPS, PF = JA * JB * LB <= NT / Plan<MB>::TPS;
+  float2 kpa[Plan<MA>::E], kpb[Plan<MB>::E];
+  if constexpr (PC) {
+    const ColLanes<MA> ln;
+    const int it = ln.first + ln.s;
+    const bool act = it < JA * LA;
+    const int j = act ? it / LA : 0, lc = act ? it - (it / LA) * LA : 0;
+    const float2 *kc = Ka + (long long)(c * JA + j) * NA * NFA + lc;
+#pragma unroll
+    for (int m = 0; m < Plan<MA>::E; ++m) kpa[m] = kc[(long long)kept<NA, MA>(ln.t + Plan<MA>::TPS * m) * NFA];
+  }
+  if constexpr (PF) {
+    const ColLanes<MB> ln;
+    const int it = ln.first + ln.s;
+    const bool act = it < JA * JB * LB;
+    const int q = act ? it / LB : 0, lc = act ? it - (it / LB) * LB : 0;
+    const float2 *kc = Kb + (long long)((c * JA) * JB + q) * MA * NFB + lc;
+#pragma unroll
+    for (int m = 0; m < Plan<MB>::E; ++m) kpb[m] = kc[(long long)kept<MA, MB>(ln.t + Plan<MB>::TPS * m) * NFB];
+  }
+
   // A: layer a's input rows -> TA [NA][LA]
   {
     float2 *scr = UA;  // UA, TB are not in use yet
@@ -280,7 +304,7 @@ __global__ __launch_bounds__(NT) void k_tail_fwd(SpecLayout in, const float *__r
 #pragma unroll
         for (int m = 0; m < Plan<MA>::E; ++m) {
           const int mrow = t + Plan<MA>::TPS * m;
-          v[m] = cmul(XA[mrow * ldA + l], kc[(long long)kept<NA, MA>(mrow) * NFA]);
+          v[m] = cmul(XA[mrow * ldA + l], PC ? kpa[m] : kc[(long long)kept<NA, MA>(mrow) * NFA]);
         }
       },
       [&](int j) { return UA + j * MA * ldA; },
@@ -343,7 +367,7 @@ __global__ __launch_bounds__(NT) void k_tail_fwd(SpecLayout in, const float *__r
 #pragma unroll
         for (int m = 0; m < Plan<MB>::E; ++m) {
           const int mrow = t + Plan<MB>::TPS * m;
-          v[m] = cmul(XB[j * MB * ldB + mrow * ldB + l], kc[(long long)kept<MA, MB>(mrow) * NFB]);
+          v[m] = cmul(XB[j * MB * ldB + mrow * ldB + l], PF ? kpb[m] : kc[(long long)kept<MA, MB>(mrow) * NFB]);
         }
       },
       [&](int q) { return UB + q * MB * ldB; },
@@ -404,6 +428,27 @@ __global__ __launch_bounds__(NT) void k_tail_bwd(const float *__restrict__ gy, S
   const int c = wg / B, b = wg - (wg / B) * B;
   const int Sa = C * JA, Sb = Sa * JB;
   float2 *GB = t_lds + G::bGB, *VB = t_lds + G::bVB, *GA = t_lds + G::bGA, *VA = t_lds + G::bVA;
+
+  // The saved-spectrum and kernel bins of stage S5, loaded now (when the stage is one
+  // round of its column pass, so that this thread's item is known): their loads complete
+  // with stage S1's, instead of the stage waiting for them after its transform.  (The
+  // same for stage S2 as well takes 128 VGPRs and spills: no faster.)
+  constexpr bool P5 = JA * LA <= NT / Plan<MA>::TPS;
+  float2 xp5[Plan<MA>::E], kp5[Plan<MA>::E];
+  if constexpr (P5) {
+    const ColLanes<MA> ln;
+    const int it = ln.first + ln.s;
+    const bool act = it < JA * LA;
+    const int j = act ? it / LA : 0, lc = act ? it - (it / LA) * LA : 0;
+    const long long xplane = (long long)b * C + c;
+    const float2 *kc = Ka + (long long)(c * JA + j) * NA * NFA + lc;
+#pragma unroll
+    for (int m = 0; m < Plan<MA>::E; ++m) {
+      const int row = ln.t + Plan<MA>::TPS * m;
+      xp5[m] = *spec_at(saved_a, xplane, row, lc, LA);
+      kp5[m] = kc[(long long)kept<NA, MA>(row) * NFA];
+    }
+  }
 
   // S1: rows of the JA JB upstream gradients: (c_l / MB^2) rfft -> GB[q] [MB][LB]
   {
@@ -515,8 +560,8 @@ __global__ __launch_bounds__(NT) void k_tail_bwd(const float *__restrict__ gy, S
 #pragma unroll
         for (int m = 0; m < Plan<MA>::E; ++m) {
           const int row = t + Plan<MA>::TPS * m;
-          const float2 xv = *spec_at(saved_a, xplane, row, lc, LA);
-          const float2 kv = kc[(long long)kept<NA, MA>(row) * NFA];
+          const float2 xv = P5 ? xp5[m] : *spec_at(saved_a, xplane, row, lc, LA);
+          const float2 kv = P5 ? kp5[m] : kc[(long long)kept<NA, MA>(row) * NFA];
           if (act) {
             pp[(long long)row * LA] = cmulc(v[m], xv);
             GA[j * MA * ldA + row * ldA + l] = cmulc(v[m], kv);
