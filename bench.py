@@ -204,8 +204,8 @@ def pooled_rfft2_launches(n, m, planes):
 def chain_step_launches(wl, input_grad=False, hermitian=False):
     """(kernel name, algorithmic bytes) of every launch of one step of the FDCNN chain
     (one rfft2, every FDC + FDP layer on spectra, one irfft2, and the backward); with
-    hermitian=True also Pi_H after every layer but the last, and before their backward
-    (two columns of every plane read and written)."""
+    hermitian=True the layers' launches also apply Pi_H, with the same launches and
+    bytes."""
     out = []
     n = wl.layers
     B = wl.batch
@@ -214,22 +214,17 @@ def chain_step_launches(wl, input_grad=False, hermitian=False):
     ML, CL = wl.sizes[-1], wl.channels[-1]
     MFL = ML // 2 + 1
     out += pooled_rfft2_launches(N0, wl.sizes[1], B * C0)
-    def pi_h(i):
-        B_, _, S_, _, M_, _, _ = layer_dims(wl, i)
-        return ("hermitian_columns", 2 * C64 * B_ * S_ * 2 * M_)
     for i in range(n):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
+        # (with hermitian=True, Pi_H of the output is part of the same launch)
         out.append(("cic_fdp_fwd", C64 * (B * C * M * L + S * M * L + B * S * M * L)))
-        if hermitian and i + 1 < n:
-            out.append(pi_h(i))
     out += fft2_launches(ML, B * CL, inverse=True)
     out += fft2_launches(ML, B * CL, inverse=False)  # the irfft2 adjoint has the forward's launches
     for i in reversed(range(n)):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
-        if hermitian and i + 1 < n:
-            out.append(pi_h(i))
-        # dX and dK in one launch: gY, and X at the kept bins, read; all of gK written (zeros
-        # at dropped bins); with dX also K at the kept bins read and all of gX written
+        # dX and dK in one launch (with hermitian=True and i > 0, Pi_H of dX in it too):
+        # gY, and X at the kept bins, read; all of gK written (zeros at dropped bins); with
+        # dX also K at the kept bins read and all of gX written
         nb = C64 * (B * S * M * L + B * C * M * L + S * N * NF)
         if i > 0 or input_grad:
             nb += C64 * (S * M * L + B * C * N * NF)

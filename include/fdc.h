@@ -161,6 +161,16 @@ fdc_status fdc_cic_fdp_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c
  * the rfft2 of the next reduce to this projection: the FDCNN chain of
  * fdc_cic_fdp_forward with Pi_H after every layer but the last computes the stack. */
 fdc_status fdc_hermitian_project(fdc_c64 *Y, int64_t count, int H, int W, hipStream_t stream);
+/* The chain of the previous two entries in one call each: fdc_cic_fdp_forward with Y
+ * written as Pi_H(Y), and fdc_cic_fdp_backward with gX written as Pi_H(gX) (gK as
+ * fdc_cic_fdp_backward writes it).  The results equal the separate calls followed by
+ * fdc_hermitian_project (same arithmetic, bit for bit).  Between two layers of a
+ * CIC + FDP stack (artifact NONE) the forward of every layer but the last and the
+ * backward of every layer but the first take these forms. */
+fdc_status fdc_cic_fdp_forward_projected(const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *Y, int B, int C, int S,
+                                         int N, int M, hipStream_t stream);
+fdc_status fdc_cic_fdp_backward_projected(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX,
+                                          fdc_c64 *gK, int B, int C, int S, int N, int M, hipStream_t stream);
 
 /* FDP crops the RFFT-shifted half spectrum: (H-Mh)/2 rows off the top and the
  * bottom, (W-Mw)/2 columns off the right, then shifts back.  In unshifted

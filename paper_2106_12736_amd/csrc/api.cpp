@@ -342,32 +342,56 @@ static fdc_status check_cic_fdp(int B, int C, int S, int N, int M) {
   if (!fdc::cic_fdp_size_supported(N))
     return fail(FDC_EUNSUPPORTED, "spectrum of %d x %d bins exceeds the kernels' bin indexing", N, N / 2 + 1);
   // the backward's one-dimensional grid: 256-bin blocks of an N-plane times S channels
-  // (dK) and 256-pair blocks times C channels (dX)
+  // (dK), 256-pair blocks times C channels (dX) and, projected, a thread per bin of
+  // dX's columns 0 and N/2; the projected forward adds a thread per bin of Y's columns
+  // 0 and M/2 to its grid, which is smaller than the backward's
   const long long pe = (long long)N * (N / 2 + 1);
-  if (((pe + 255) / 256) * S + ((pe / 2 + 255) / 256) * C >= (1LL << 31))
-    return fail(FDC_EUNSUPPORTED, "S = %d channels of %d x %d bins exceed the kernels' grid", S, N, N / 2 + 1);
+  if (((pe + 255) / 256) * S + ((pe / 2 + 255) / 256) * C + ((long long)B * C * N * 2 + 255) / 256 +
+          ((long long)B * S * M * 2 + 255) / 256 >= (1LL << 31))
+    return fail(FDC_EUNSUPPORTED, "B = %d, S = %d channels of %d x %d bins exceed the kernels' grid", B, S, N,
+                N / 2 + 1);
   return FDC_OK;
 }
 
-fdc_status fdc_cic_fdp_forward(const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *Y, int B, int C, int S, int N, int M,
-                               hipStream_t s) {
+static fdc_status cic_fdp_forward(const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *Y, int B, int C, int S, int N, int M,
+                                  bool project, hipStream_t s) {
   if (fdc_status st = check_cic_fdp(B, C, S, N, M)) return st;
   if (!X || !K || !Y) return fail(FDC_EINVAL, "NULL tensor");
   if (!aligned16(Y)) return fail(FDC_EINVAL, "Y must be 16-byte aligned");
   return check_hip(fdc::launch_cic_fdp_fwd(reinterpret_cast<const float2 *>(X), reinterpret_cast<const float2 *>(K),
-                                           reinterpret_cast<float2 *>(Y), B, C, S, N, M, s),
+                                           reinterpret_cast<float2 *>(Y), B, C, S, N, M, project, s),
                    "cic_fdp_forward");
 }
 
-fdc_status fdc_cic_fdp_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX, fdc_c64 *gK,
-                                int B, int C, int S, int N, int M, hipStream_t s) {
+fdc_status fdc_cic_fdp_forward(const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *Y, int B, int C, int S, int N, int M,
+                               hipStream_t s) {
+  return cic_fdp_forward(X, K, Y, B, C, S, N, M, false, s);
+}
+
+fdc_status fdc_cic_fdp_forward_projected(const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *Y, int B, int C, int S, int N,
+                                         int M, hipStream_t s) {
+  return cic_fdp_forward(X, K, Y, B, C, S, N, M, true, s);
+}
+
+static fdc_status cic_fdp_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX, fdc_c64 *gK,
+                                   int B, int C, int S, int N, int M, bool project, hipStream_t s) {
   if (fdc_status st = check_cic_fdp(B, C, S, N, M)) return st;
   if (!gY || (gX && !K) || (gK && !X)) return fail(FDC_EINVAL, "NULL tensor");
   if (gX && !aligned16(gX)) return fail(FDC_EINVAL, "gX must be 16-byte aligned");
   return check_hip(fdc::launch_cic_fdp_bwd(reinterpret_cast<const float2 *>(gY), reinterpret_cast<const float2 *>(K),
                                            reinterpret_cast<float2 *>(gX), reinterpret_cast<const float2 *>(X),
-                                           reinterpret_cast<float2 *>(gK), B, C, S, N, M, s),
+                                           reinterpret_cast<float2 *>(gK), B, C, S, N, M, project, s),
                    "cic_fdp_backward");
+}
+
+fdc_status fdc_cic_fdp_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX, fdc_c64 *gK,
+                                int B, int C, int S, int N, int M, hipStream_t s) {
+  return cic_fdp_backward(gY, X, K, gX, gK, B, C, S, N, M, false, s);
+}
+
+fdc_status fdc_cic_fdp_backward_projected(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX,
+                                          fdc_c64 *gK, int B, int C, int S, int N, int M, hipStream_t s) {
+  return cic_fdp_backward(gY, X, K, gX, gK, B, C, S, N, M, true, s);
 }
 
 fdc_status fdc_hermitian_project(fdc_c64 *Y, int64_t count, int H, int W, hipStream_t s) {

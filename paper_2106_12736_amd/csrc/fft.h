@@ -32,6 +32,14 @@ __device__ __forceinline__ float2 cmul(float2 a, float2 b) {
 __device__ __forceinline__ float2 cmulc(float2 a, float2 b) {
   return make_float2(a.x * b.x + a.y * b.y, a.y * b.x - a.x * b.y);
 }
+// cmul and cfmac with the fused multiply-adds written out, so that every call site rounds
+// alike (the compiler may fuse the plain forms differently in different code paths)
+__device__ __forceinline__ float2 cmul_f(float2 a, float2 b) {
+  return make_float2(fmaf(a.x, b.x, -(a.y * b.y)), fmaf(a.x, b.y, a.y * b.x));
+}
+__device__ __forceinline__ float2 cfmac_f(float2 a, float2 b, float2 c) {
+  return make_float2(fmaf(b.y, c.y, fmaf(b.x, c.x, a.x)), fmaf(-b.x, c.y, fmaf(b.y, c.x, a.y)));
+}
 __device__ __forceinline__ float2 cscale(float2 a, float s) { return make_float2(a.x * s, a.y * s); }
 __device__ __forceinline__ float2 cconj(float2 a) { return make_float2(a.x, -a.y); }
 // a + b * conj(c)

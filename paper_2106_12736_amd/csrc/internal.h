@@ -230,11 +230,13 @@ hipError_t launch_cic_wgrad(int n_img, const float2 *gK, float *part, float *gw,
 // its backward (gX and gK with exact zeros at the dropped bins).
 // Largest spectrum the spectral FDC + FDP kernels index: N (N/2 + 1) bins below 2^24.
 bool cic_fdp_size_supported(int N);
+// project: Y written as Pi_H(Y).
 hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, int N, int M,
-                              hipStream_t s);
-// gX (NULL: skipped; needs K) and gK (NULL: skipped; needs X) in one launch.
+                              bool project, hipStream_t s);
+// gX (NULL: skipped; needs K) and gK (NULL: skipped; needs X) in one launch; project:
+// gX written as Pi_H(gX).
 hipError_t launch_cic_fdp_bwd(const float2 *gY, const float2 *K, float2 *gX, const float2 *X, float2 *gK, int B,
-                              int C, int S, int N, int M, hipStream_t s);
+                              int C, int S, int N, int M, bool project, hipStream_t s);
 hipError_t launch_fdp_gather(const float2 *X, float2 *Y, long long count, int H, int Wf, int Mh, int Mwf,
                              hipStream_t s);
 hipError_t launch_fdp_scatter(const float2 *gY, float2 *gX, long long count, int H, int Wf, int Mh, int Mwf,

@@ -1468,20 +1468,61 @@ constexpr int kChainImages = 8;
 // order (contiguous stores) times groups of JB output channels of one input channel
 // (o = c J + j): a thread loads its two bins of X[b][c] once for the group's JB
 // outputs, and each output's two kernel bins once for every image.
-template <int JB>
+// Pi_H of one bin of column 0 or the last column from its value y and the value yp of
+// row -k of the same column: (y + conj(yp)) / 2, the real part alone where row -k is
+// row k (k = 0 and H/2); the arithmetic of k_hermitian_columns.
+__device__ __forceinline__ float2 hermitian_bin(float2 y, float2 yp, bool self) {
+  return self ? make_float2(y.x, 0.f) : make_float2(0.5f * (y.x + yp.x), 0.5f * (y.y - yp.y));
+}
+
+// PROJ: Y is written as Pi_H(Y) (columns 0 and M/2 Hermitian-projected along the rows),
+// which equals k_cic_fdp_fwd followed by k_hermitian_columns on Y: the main workgroups
+// (the first nmain) store every bin but those of the two columns, and the workgroups
+// after them form those columns, a thread per bin (b, o, row, column), from the bin and
+// its partner in row -k.  The products use cmul_f, so both paths round alike.
+template <int JB, bool PROJ>
 __global__ __launch_bounds__(256) void k_cic_fdp_fwd(const float2 *__restrict__ X, const float2 *__restrict__ K,
-                                                     float2 *__restrict__ Y, int B, int C, int J, int N, int M) {
+                                                     float2 *__restrict__ Y, int B, int C, int J, int N, int M,
+                                                     int nmain) {
   const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1, pe = M * Lm, JG = J / JB;
+  if constexpr (PROJ) {
+    if ((int)blockIdx.x >= nmain) {
+      const long long id = (long long)(blockIdx.x - nmain) * 256 + threadIdx.x;
+      if (id >= (long long)B * S * M * 2) return;
+      const int l = (id & 1) ? Lm - 1 : 0;
+      const long long r = id >> 1;
+      const int k = (int)(r % M);
+      const long long bo = r / M;  // b * S + o
+      const int o = (int)(bo % S), b = (int)(bo / S), c = o / J, kp = (M - k) % M;
+      const float2 *xo = X + ((long long)b * C + c) * N * NF + l, *ko = K + (long long)o * N * NF + l;
+      const int kr = k < M / 2 ? k : k + (N - M), krp = kp < M / 2 ? kp : kp + (N - M);
+      const float2 y = cmul_f(xo[(long long)kr * NF], ko[(long long)kr * NF]);
+      const float2 yp = cmul_f(xo[(long long)krp * NF], ko[(long long)krp * NF]);
+      Y[(bo * M + k) * Lm + l] = hermitian_bin(y, yp, k == 0 || 2 * k == M);
+      return;
+    }
+  }
   // one group of one block of bin pairs per workgroup, the groups of a block consecutive
   // after the XCD remap, so that the J / JB groups reading the same input bins run
   // together on one XCD and share them through its L2
-  const int lin = xcd_remap(blockIdx.x, gridDim.x), gi = lin % (C * JG);
+  const int lin = xcd_remap(blockIdx.x, nmain), gi = lin % (C * JG);
   const int e0 = 2 * ((lin / (C * JG)) * 256 + threadIdx.x);
   if (e0 >= pe) return;
   const BinPair q(e0, Lm, 1.f / (float)Lm);
   int off[2];  // bin offsets in an N-plane
 #pragma unroll
   for (int h = 0; h < 2; ++h) off[h] = (q.k[h] < M / 2 ? q.k[h] : q.k[h] + (N - M)) * NF + q.l[h];
+  // bins the edge workgroups store (PROJ)
+  const bool skip0 = PROJ && (q.l[0] == 0 || q.l[0] == Lm - 1), skip1 = PROJ && (q.l[1] == 0 || q.l[1] == Lm - 1);
+  auto store = [&](float4 *dst, float2 v0, float2 v1) {
+    if (!skip0 && !skip1) {
+      *dst = pack2(v0, v1);
+    } else {
+      float2 *d2 = reinterpret_cast<float2 *>(dst);
+      if (!skip0) d2[0] = v0;
+      if (!skip1) d2[1] = v1;
+    }
+  };
   const long long xs = (long long)C * N * NF, ys = (long long)S * (pe / 2);  // image strides (float2, float4)
   {
     const int c = gi / JG, o0 = c * J + (gi - c * JG) * JB;
@@ -1505,12 +1546,12 @@ __global__ __launch_bounds__(256) void k_cic_fdp_fwd(const float2 *__restrict__ 
       for (int jj = 0; jj < JB; ++jj)
 #pragma unroll
         for (int u = 0; u < kChainImages; ++u)
-          yo[(b + u) * ys + jj * (pe / 2)] = pack2(cmul(a0[u], kv[jj][0]), cmul(a1[u], kv[jj][1]));
+          store(yo + (b + u) * ys + jj * (pe / 2), cmul_f(a0[u], kv[jj][0]), cmul_f(a1[u], kv[jj][1]));
     }
     for (; b < B; ++b) {
       const float2 a0 = xo[b * xs + off[0]], a1 = xo[b * xs + off[1]];
 #pragma unroll
-      for (int jj = 0; jj < JB; ++jj) yo[b * ys + jj * (pe / 2)] = pack2(cmul(a0, kv[jj][0]), cmul(a1, kv[jj][1]));
+      for (int jj = 0; jj < JB; ++jj) store(yo + b * ys + jj * (pe / 2), cmul_f(a0, kv[jj][0]), cmul_f(a1, kv[jj][1]));
     }
   }
 }
@@ -1522,6 +1563,8 @@ __global__ __launch_bounds__(256) void k_cic_fdp_fwd(const float2 *__restrict__ 
 // order), exact zeros at the bins FDP drops.  bx runs over a plane's bin pairs, by (step
 // ny) over the input channels; a thread forms its two bins for every image, four
 // images at a time.
+// PROJ: the bins of columns 0 and N/2 are left to fdp_bwd_gx_edge.
+template <bool PROJ>
 __device__ __forceinline__ void fdp_bwd_gx_block(const float2 *__restrict__ gY, const float2 *__restrict__ K,
                                                  float2 *__restrict__ gX, int B, int C, int J, int N, int M, int bx,
                                                  int by, int ny) {
@@ -1542,10 +1585,20 @@ __device__ __forceinline__ void fdp_bwd_gx_block(const float2 *__restrict__ gY, 
   }
   const long long mpe = (long long)M * Lm, ys = (long long)S * mpe, xs = (long long)C * (pe / 2);
   const long long kps = (long long)N * NF;
+  const bool skip0 = PROJ && (q.l[0] == 0 || q.l[0] == NF - 1), skip1 = PROJ && (q.l[1] == 0 || q.l[1] == NF - 1);
+  auto store = [&](float4 *dst, float2 v0, float2 v1) {
+    if (!skip0 && !skip1) {
+      *dst = pack2(v0, v1);
+    } else {
+      float2 *d2 = reinterpret_cast<float2 *>(dst);
+      if (!skip0) d2[0] = v0;
+      if (!skip1) d2[1] = v1;
+    }
+  };
   for (int c = by; c < C; c += ny) {
     float4 *gp = reinterpret_cast<float4 *>(gX + (long long)c * pe + e0);
     if (!kept[0] && !kept[1]) {
-      for (int b = 0; b < B; ++b) gp[b * xs] = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int b = 0; b < B; ++b) store(gp + b * xs, make_float2(0.f, 0.f), make_float2(0.f, 0.f));
       continue;
     }
     const float2 *kp = K + (long long)c * J * kps;   // K[cJ + j] at j * N * NF
@@ -1565,16 +1618,43 @@ __device__ __forceinline__ void fdp_bwd_gx_block(const float2 *__restrict__ gY, 
         }
 #pragma unroll
         for (int u = 0; u < BI; ++u) {
-          a0[u] = cfmac(a0[u], g0[u], k0);
-          a1[u] = cfmac(a1[u], g1[u], k1);
+          a0[u] = cfmac_f(a0[u], g0[u], k0);
+          a1[u] = cfmac_f(a1[u], g1[u], k1);
         }
       }
 #pragma unroll
       for (int u = 0; u < BI; ++u)
         if (b0 + u < B)
-          gp[(b0 + u) * xs] = pack2(kept[0] ? a0[u] : make_float2(0.f, 0.f), kept[1] ? a1[u] : make_float2(0.f, 0.f));
+          store(gp + (b0 + u) * xs, kept[0] ? a0[u] : make_float2(0.f, 0.f), kept[1] ? a1[u] : make_float2(0.f, 0.f));
     }
   }
+}
+
+// Pi_H of dX at columns 0 and N/2, thread id over (b, c, row, column): the bin and its
+// partner in row -k formed as fdp_bwd_gx_block forms them (zero at bins FDP drops; Pi_H
+// acts on the whole N-plane, so the dropped row M/2 receives half of row N - M/2).
+__device__ __forceinline__ void fdp_bwd_gx_edge(const float2 *__restrict__ gY, const float2 *__restrict__ K,
+                                                float2 *__restrict__ gX, int B, int C, int J, int N, int M,
+                                                long long id) {
+  const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1;
+  if (id >= (long long)B * C * N * 2) return;
+  const int l = (id & 1) ? NF - 1 : 0;
+  const long long r = id >> 1;
+  const int kr = (int)(r % N);
+  const long long bc = r / N;  // b * C + c
+  const int c = (int)(bc % C), b = (int)(bc / C), krp = (N - kr) % N;
+  const long long mpe = (long long)M * Lm, kps = (long long)N * NF;
+  auto dsum = [&](int row) {  // sum_j gY conj(K) at (row, l), zero where FDP drops it
+    float2 a = make_float2(0.f, 0.f);
+    if (l < Lm && (row < M / 2 || row >= N - M / 2)) {
+      const int k = row < M / 2 ? row : row - (N - M);
+      const float2 *yp = gY + ((long long)b * S + (long long)c * J) * mpe + (long long)k * Lm + l;
+      const float2 *kp = K + (long long)c * J * kps + (long long)row * NF + l;
+      for (int j = 0; j < J; ++j) a = cfmac_f(a, yp[j * mpe], kp[j * kps]);
+    }
+    return a;
+  };
+  gX[(bc * N + kr) * NF + l] = hermitian_bin(dsum(kr), dsum(krp), kr == 0 || 2 * kr == N);
 }
 
 // dK block (bx, by): dK [S][N][N/2+1] = sum_b gY conj(X) at the kept bins (batch summed
@@ -1606,17 +1686,21 @@ __device__ __forceinline__ void fdp_bwd_gk_block(const float2 *__restrict__ gY, 
   }
 }
 
-// Workgroups [0, xbx * xby) run dX blocks, the rest dK blocks (kbx * kby of them).
+// Workgroups [0, xbx * xby) run dX blocks, the next kbx * kby dK blocks, and with PROJ
+// the rest the Pi_H bins of dX (fdp_bwd_gx_edge).
+template <bool PROJ>
 __global__ __launch_bounds__(256) void k_cic_fdp_bwd(const float2 *__restrict__ gY, const float2 *__restrict__ K,
                                                      float2 *__restrict__ gX, const float2 *__restrict__ X,
                                                      float2 *__restrict__ gK, int B, int C, int J, int N, int M,
-                                                     int xbx, int xby, int kbx, int kby) {
+                                                     int xbx, int xby, int kbx, int kby, int nk) {
   const int id = blockIdx.x, nx = xbx * xby;
   if (id < nx) {
-    fdp_bwd_gx_block(gY, K, gX, B, C, J, N, M, id % xbx, id / xbx, xby);
-  } else {
+    fdp_bwd_gx_block<PROJ>(gY, K, gX, B, C, J, N, M, id % xbx, id / xbx, xby);
+  } else if (!PROJ || id < nx + nk) {
     const int i = id - nx;
     fdp_bwd_gk_block(gY, X, gK, B, C, J, N, M, i % kbx, i / kbx, kby);
+  } else {
+    fdp_bwd_gx_edge(gY, K, gX, B, C, J, N, M, (long long)(id - nx - nk) * 256 + threadIdx.x);
   }
 }
 
@@ -1673,7 +1757,7 @@ static void dispatch_jb(int jb, F &&f) {
 }
 
 hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, int N, int M,
-                              hipStream_t s) {
+                              bool project, hipStream_t s) {
   if ((long long)N * (N / 2 + 1) >= (1 << 24)) return hipErrorInvalidValue;
   const int J = S / C;
   const dim3 g0 = plane_grid((long long)M * (M / 2 + 1) / 2, 1);
@@ -1682,8 +1766,15 @@ hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B
   timing_before("cic_fdp_fwd", s);
   dispatch_jb(jb, [&](auto jc) {
     constexpr int JB = decltype(jc)::value;
-    hipLaunchKernelGGL(k_cic_fdp_fwd<JB>, dim3((unsigned)(g0.x * (long long)C * (J / JB))), dim3(256), 0, s, X, K, Y,
-                       B, C, J, N, M);
+    const long long nmain = g0.x * (long long)C * (J / JB);
+    if (project) {
+      const long long nedge = ((long long)B * S * M * 2 + 255) / 256;
+      hipLaunchKernelGGL((k_cic_fdp_fwd<JB, true>), dim3((unsigned)(nmain + nedge)), dim3(256), 0, s, X, K, Y, B, C,
+                         J, N, M, (int)nmain);
+    } else {
+      hipLaunchKernelGGL((k_cic_fdp_fwd<JB, false>), dim3((unsigned)nmain), dim3(256), 0, s, X, K, Y, B, C, J, N, M,
+                         (int)nmain);
+    }
   });
   const hipError_t e = hipGetLastError();
   timing_after("cic_fdp_fwd", s);
@@ -1691,17 +1782,23 @@ hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B
 }
 
 hipError_t launch_cic_fdp_bwd(const float2 *gY, const float2 *K, float2 *gX, const float2 *X, float2 *gK, int B,
-                              int C, int S, int N, int M, hipStream_t s) {
+                              int C, int S, int N, int M, bool project, hipStream_t s) {
   const long long pe = (long long)N * (N / 2 + 1);
   if (pe >= (1 << 24)) return hipErrorInvalidValue;
   const long long xbx = gX ? (pe / 2 + 255) / 256 : 0, xby = gX ? C : 0;
   const long long kbx = gK ? (pe + 255) / 256 : 0, kby = gK ? S : 0;
-  const long long total = xbx * xby + kbx * kby;
+  const long long nedge = (gX && project) ? ((long long)B * C * N * 2 + 255) / 256 : 0;
+  const long long total = xbx * xby + kbx * kby + nedge;
   if (total == 0) return hipSuccess;
   if (total >= (1LL << 31)) return hipErrorInvalidValue;
   timing_before("cic_fdp_bwd", s);
-  hipLaunchKernelGGL(k_cic_fdp_bwd, dim3((unsigned)total), dim3(256), 0, s, gY, K, gX, X, gK, B, C, S / C, N, M,
-                     (int)xbx, (int)xby, (int)(kbx > 0 ? kbx : 1), (int)(kby > 0 ? kby : 1));
+  const int kbx1 = (int)(kbx > 0 ? kbx : 1), kby1 = (int)(kby > 0 ? kby : 1), nk = (int)(kbx * kby);
+  if (project && gX)
+    hipLaunchKernelGGL(k_cic_fdp_bwd<true>, dim3((unsigned)total), dim3(256), 0, s, gY, K, gX, X, gK, B, C, S / C, N,
+                       M, (int)xbx, (int)xby, kbx1, kby1, nk);
+  else
+    hipLaunchKernelGGL(k_cic_fdp_bwd<false>, dim3((unsigned)total), dim3(256), 0, s, gY, K, gX, X, gK, B, C, S / C, N,
+                       M, (int)xbx, (int)xby, kbx1, kby1, nk);
   const hipError_t e = hipGetLastError();
   timing_after("cic_fdp_bwd", s);
   return e;

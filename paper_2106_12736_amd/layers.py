@@ -534,24 +534,28 @@ def hermitian_project(Y):
     return Y
 
 
-def cic_fdp_forward(X, K, M):
-    """FDC layer of the FDCNN on spectra followed by FDP: [B][C][N][N/2+1] -> [B][S][M][M/2+1]."""
+def cic_fdp_forward(X, K, M, project=False):
+    """FDC layer of the FDCNN on spectra followed by FDP: [B][C][N][N/2+1] -> [B][S][M][M/2+1]
+    (with project=True, Pi_H of the result: fdc_cic_fdp_forward_projected)."""
     _check(X, torch.complex64, name="X")
     _check(K, torch.complex64, name="K")
     B, C, N, _ = X.shape
     S = K.shape[0]
     Y = torch.empty((B, S, M, M // 2 + 1), dtype=torch.complex64, device=X.device)
-    call("fdc_cic_fdp_forward", _ptr(X), _ptr(K), _ptr(Y), B, C, S, N, M, _stream())
+    fn = "fdc_cic_fdp_forward_projected" if project else "fdc_cic_fdp_forward"
+    call(fn, _ptr(X), _ptr(K), _ptr(Y), B, C, S, N, M, _stream())
     return Y
 
 
-def cic_fdp_backward(gY, X, K, need_gx=True, need_gk=True):
+def cic_fdp_backward(gY, X, K, need_gx=True, need_gk=True, project=False):
+    """Its backward (with project=True, Pi_H of gX: fdc_cic_fdp_backward_projected)."""
     _check(gY, torch.complex64, name="gY")
     B, S, M, _ = gY.shape
     C, N = X.shape[1], X.shape[2]
     gX = torch.empty_like(X) if need_gx else None
     gK = torch.empty_like(K) if need_gk else None
-    call("fdc_cic_fdp_backward", _ptr(gY), _ptr(X), _ptr(K), _ptr(gX), _ptr(gK), B, C, S, N, M, _stream())
+    fn = "fdc_cic_fdp_backward_projected" if project else "fdc_cic_fdp_backward"
+    call(fn, _ptr(gY), _ptr(X), _ptr(K), _ptr(gX), _ptr(gK), B, C, S, N, M, _stream())
     return gX, gK
 
 
@@ -563,8 +567,9 @@ class CicChain:
     The input transform forms only the bins the first FDP keeps (fdc_rfft2_pooled): the
     first layer reads no others, forward or backward.
 
-    With hermitian=True, Pi_H (fdc_hermitian_project) follows every layer but the last,
-    and its adjoint (itself) precedes their backward: the irfft2 of one layer and the
+    With hermitian=True, Pi_H follows every layer but the last (the projected form of
+    fdc_cic_fdp_forward), and its adjoint (itself) precedes their backward (the projected
+    form of the next layer's fdc_cic_fdp_backward): the irfft2 of one layer and the
     rfft2 of the next reduce to Pi_H, so this computes the per-layer stack of
     CicStack / CicStackFused (artifact NONE) with one transform at each end."""
 
@@ -595,11 +600,10 @@ class CicChain:
         B = self.batch
         for i, K in enumerate(kernels):
             _check(K, torch.complex64, (self.channels[i + 1], self.sizes[i], self.sizes[i] // 2 + 1), f"K[{i}]")
-            call("fdc_cic_fdp_forward", _ptr(self.specs[i]), _ptr(K), _ptr(self.specs[i + 1]), B, self.channels[i],
+            # Pi_H on every layer's output but the last, in the layer's own launch
+            fn = "fdc_cic_fdp_forward_projected" if self.hermitian and i + 1 < self.layers else "fdc_cic_fdp_forward"
+            call(fn, _ptr(self.specs[i]), _ptr(K), _ptr(self.specs[i + 1]), B, self.channels[i],
                  self.channels[i + 1], self.sizes[i], self.sizes[i + 1], s)
-            if self.hermitian and i + 1 < self.layers:
-                m = self.sizes[i + 1]
-                call("fdc_hermitian_project", _ptr(self.specs[i + 1]), B * self.channels[i + 1], m, m, s)
         call("fdc_irfft2", self.plan_out._p, _ptr(self.specs[-1]), _ptr(self.out), _ptr(self.ws), self.ws.numel(), s)
         return self.out
 
@@ -611,10 +615,10 @@ class CicChain:
         call("fdc_irfft2_backward", self.plan_out._p, _ptr(gy), _ptr(self.gspecs[-1]), None, 0, s)
         for i in reversed(range(self.layers)):
             need_gx = i > 0 or input_grad is not None
-            if self.hermitian and i + 1 < self.layers:
-                m = self.sizes[i + 1]
-                call("fdc_hermitian_project", _ptr(self.gspecs[i + 1]), B * self.channels[i + 1], m, m, s)
-            call("fdc_cic_fdp_backward", _ptr(self.gspecs[i + 1]), _ptr(self.specs[i]), _ptr(kernels[i]),
+            # Pi_H (its own adjoint) on the input gradient of every layer but the first,
+            # in the layer's own launch
+            fn = "fdc_cic_fdp_backward_projected" if self.hermitian and i > 0 else "fdc_cic_fdp_backward"
+            call(fn, _ptr(self.gspecs[i + 1]), _ptr(self.specs[i]), _ptr(kernels[i]),
                  _ptr(self.gspecs[i] if need_gx else None), _ptr(self.gks[i]), B, self.channels[i],
                  self.channels[i + 1], self.sizes[i], self.sizes[i + 1], s)
         if input_grad is not None:

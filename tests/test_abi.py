@@ -322,6 +322,9 @@ def test_hermitian_project_validation():
 def test_cic_fdp_validation():
     d = ctypes.c_void_p(0x1000)
     assert _lib.status("fdc_cic_fdp_forward", d, d, d, 2, 3, 4, 8, 4, None) == FDC_EINVAL  # S mod C
+    assert _lib.status("fdc_cic_fdp_forward_projected", d, d, d, 2, 3, 4, 8, 4, None) == FDC_EINVAL
+    assert _lib.status("fdc_cic_fdp_backward_projected", d, d, d, d, d, 2, 1, 4, 8, 3, None) == FDC_EINVAL
+    assert _lib.status("fdc_cic_fdp_backward_projected", d, d, d, None, None, 2, 1, 4, 8, 4, None) == FDC_OK
     assert _lib.status("fdc_cic_fdp_forward", d, d, d, 2, 1, 4, 8, 16, None) == FDC_EINVAL  # M > N
     assert _lib.status("fdc_cic_fdp_forward", d, d, d, 2, 1, 4, 8, 3, None) == FDC_EINVAL   # odd M
     assert _lib.status("fdc_cic_fdp_forward", None, d, d, 2, 1, 4, 8, 4, None) == FDC_EINVAL

@@ -9,7 +9,7 @@ import pytest
 import torch
 
 from _parity import assert_parity, to_np
-from oracle import fdc
+from oracle import dft, fdc
 from paper_2106_12736_amd import inputs, layers
 
 pytestmark = pytest.mark.gpu
@@ -44,6 +44,34 @@ def test_cic_fdp_op(B, C, S, N, M):
     assert_parity(to_np(gX), gx_ref, "gX")
     assert_parity(to_np(gK), gk_ref, "gK")
     assert np.all(to_np(gK)[np.abs(gk_ref) == 0] == 0), "dropped bins must be exact zeros"
+
+
+@pytest.mark.parametrize("B,C,S,N,M", [
+    (1, 1, 1, 4, 2), (2, 1, 4, 8, 4), (3, 2, 6, 16, 16), (2, 4, 4, 32, 8), (1, 3, 9, 64, 32), (2, 2, 4, 224, 112),
+    (11, 2, 4, 16, 8), (9, 1, 8, 32, 16), (17, 3, 3, 8, 8), (8, 1, 8, 1024, 512),
+])
+def test_cic_fdp_projected_op(B, C, S, N, M):
+    """The projected forms equal the plain calls followed by Pi_H, bit for bit (same
+    arithmetic), and the oracle's Pi_H of the oracle's layer; columns 0 and N/2 of dX
+    include the unpooled case (M = N, both columns kept)."""
+    print(f"cic_fdp projected B={B} C={C} S={S} N={N} M={M}", flush=True)
+    rng = _rng("cic_fdp_proj", B, C, S, N, M)
+    X = _c64(rng, (B, C, N, N // 2 + 1))
+    K = _c64(rng, (S, N, N // 2 + 1))
+    gY = _c64(rng, (B, S, M, M // 2 + 1))
+    Xd, Kd, gYd = (torch.from_numpy(a).cuda() for a in (X, K, gY))
+    Y = layers.cic_fdp_forward(Xd, Kd, M)
+    Yp = layers.cic_fdp_forward(Xd, Kd, M, project=True)
+    gX, gK = layers.cic_fdp_backward(gYd, Xd, Kd)
+    gXp, gKp = layers.cic_fdp_backward(gYd, Xd, Kd, project=True)
+    layers.hermitian_project(Y)
+    layers.hermitian_project(gX)
+    torch.cuda.synchronize()
+    assert torch.equal(Yp, Y) and torch.equal(gXp, gX) and torch.equal(gKp, gK)
+    X64, K64, g64 = X.astype(np.complex128), K.astype(np.complex128), gY.astype(np.complex128)
+    assert_parity(to_np(Yp), dft.hermitian_projection(fdc.fdp(fdc.cic(X64, K64), M, M)), "Pi_H Y")
+    gx_ref, _ = fdc.cic_backward(fdc.fdp_backward(g64, N, N), X64, K64)
+    assert_parity(to_np(gXp), dft.hermitian_projection(gx_ref), "Pi_H gX")
 
 
 @pytest.mark.parametrize("wl", inputs.CIC_WORKLOADS, ids=lambda w: w.name)
