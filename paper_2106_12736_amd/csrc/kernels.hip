@@ -25,6 +25,7 @@
 
 #include <algorithm>
 #include <string>
+#include <type_traits>
 
 namespace fdc {
 
@@ -66,6 +67,31 @@ constexpr int row_spw() {
   return s > 64 ? 64 : s;
 }
 
+// Sequence (row pair) index of this thread in its workgroup.  With one sequence per
+// wavefront it is read from the first lane, so that the compiler sees it as uniform
+// and keeps the row addresses derived from it in scalar registers.
+template <int TPS>
+__device__ __forceinline__ int row_seq() {
+  const int s = (int)threadIdx.x / TPS;
+  if constexpr (TPS == 64) return __builtin_amdgcn_readfirstlane(s);
+  else return s;
+}
+
+// Element i of p addressed by a 32-bit byte offset (i * sizeof(T) < 2^32): on a base
+// uniform across the wavefront the access is one instruction with a scalar base and a
+// 32-bit lane offset, instead of 64-bit address arithmetic per lane.
+template <class T>
+__device__ __forceinline__ T &at32(T *p, unsigned i) {
+  using B = typename std::conditional<std::is_const<T>::value, const char, char>::type;
+  return *reinterpret_cast<T *>(reinterpret_cast<B *>(p) + i * (unsigned)sizeof(T));
+}
+
+// Offset of bin l (< L-1) in its row of the main block, 32-bit: a row's bins lie within
+// one plane, (L-1) * rows complex values.
+__device__ __forceinline__ unsigned bin_off32(const SpecLayout &sl, int l) {
+  return (unsigned)(l >> 3) * (unsigned)sl.ts + (unsigned)(l & 7);
+}
+
 // Sequence s's natural-order elements into the padded LDS rows (element e at
 // lds_phys(s N + e)), thread t holding elements t + TPS m.
 template <int N>
@@ -95,7 +121,7 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_r2c(const float *__
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
   TwiddleStage<N, SPW * TPS> tws;
   tws.fetch(threadIdx.x);
-  const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
+  const int t = threadIdx.x % TPS, s = row_seq<TPS>();
   // 32-bit row arithmetic: the launchers keep planes * rows_per_plane below 2^31
   int pair = xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
   const bool active = pair < npairs;
@@ -113,7 +139,7 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_r2c(const float *__
     const int ib = view_index<MODE>(view, N, r0 + 1, w);
     // unconditional loads (a cropped-away pixel reads element 0), zeroed afterwards: a load
     // under a lane condition would be issued in its own branch and wait for its data alone
-    const float xa = xp[ia < 0 ? 0 : ia], xb = xp[ib < 0 ? 0 : ib];
+    const float xa = at32(xp, (unsigned)(ia < 0 ? 0 : ia)), xb = at32(xp, (unsigned)(ib < 0 ? 0 : ib));
     v[m] = make_float2(ia >= 0 ? xa : 0.f, ib >= 0 ? xb : 0.f);
   }
   tws.commit(tw, threadIdx.x);  // the twiddle table and the rows load together
@@ -132,9 +158,9 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_r2c(const float *__
     const float2 A = make_float2((zk.x + zn.x) * wgt, (zk.y - zn.y) * wgt);
     const float2 Bv = make_float2((zk.y + zn.y) * wgt, (zn.x - zk.x) * wgt);
     if (k < L - 1) {
-      const long long o = bin_off(out, k);
-      oa[o] = A;
-      ob[o] = Bv;
+      const unsigned o = bin_off32(out, k);
+      at32(oa, o) = A;
+      at32(ob, o) = Bv;
     } else {
       float2 *sa = out.side + plane * out.sps + (long long)r0 * out.srs;
       sa[0] = A;
@@ -168,7 +194,7 @@ __device__ __forceinline__ void c2r_gather(float2 (&v)[RowCfg<N>::E], const Spec
       // unconditional loads from valid addresses; bins beyond Lin get weight 0 (the loaded
       // value is always used, so the load is not sunk into a per-lane branch)
       const bool in_main = kk < Lin - 1;
-      const long long o = bin_off(in, kk);
+      const unsigned o = bin_off32(in, kk);
       const float2 *pa = in_main ? ia + o : sa;
       const float2 *pb = in_main ? ib + o : sa + in.srs;
       float2 a = *pa, b = *pb;
@@ -215,16 +241,16 @@ __device__ __forceinline__ void c2r_gather(float2 (&v)[RowCfg<N>::E], const Spec
         // m whose lane t = 0 holds the side bin KS (bin KS - t on the other lanes)
         constexpr bool side_m = (LIN == 1 && m == E / 2) || (LIN == 2 && m == 3 * E / 4);
         if constexpr (side_m) {
-          const long long o = bin_off(in, KS - t);
+          const unsigned o = bin_off32(in, KS - t);
           const float2 *pa = t0 ? sa : ia + o;
           const float2 *pb = t0 ? sb : ib + o;
           a = *pa;
           b = *pb;
         } else {
           const int kk = low ? t + TPS * m : N - t - TPS * m;
-          const long long o = bin_off(in, kk);
-          a = ia[o];
-          b = ib[o];
+          const unsigned o = bin_off32(in, kk);
+          a = at32(ia, o);
+          b = at32(ib, o);
         }
         // l = 0 (m = 0, t = 0) and, with LIN 1, l = N/2 (m = E/2, t = 0): weight a1 and
         // real-part semantics
@@ -262,7 +288,7 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
   TwiddleStage<N, SPW * TPS> tws;
   tws.fetch(threadIdx.x);
-  const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
+  const int t = threadIdx.x % TPS, s = row_seq<TPS>();
   // 32-bit row arithmetic: the launchers keep planes * rows_per_plane below 2^31
   int pair = xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
   const bool active = pair < npairs;
@@ -282,8 +308,8 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
     const int w = t + TPS * m;
     const int oa = view_index<MODE>(view, N, r0, w);
     const int ob = view_index<MODE>(view, N, r0 + 1, w);
-    if (oa >= 0) yp[oa] = LIN == 0 ? v[m].x : v[m].x * sc;
-    if (ob >= 0) yp[ob] = LIN == 0 ? v[m].y : v[m].y * sc;
+    if (oa >= 0) at32(yp, (unsigned)oa) = LIN == 0 ? v[m].x : v[m].x * sc;
+    if (ob >= 0) at32(yp, (unsigned)ob) = LIN == 0 ? v[m].y : v[m].y * sc;
   }
 }
 
@@ -303,7 +329,7 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r_r2c(SpecLayout 
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
   TwiddleStage<N, SPW * TPS> tws;
   tws.fetch(threadIdx.x);
-  const int t = threadIdx.x % TPS, s = threadIdx.x / TPS;
+  const int t = threadIdx.x % TPS, s = row_seq<TPS>();
   // 32-bit row arithmetic: the launchers keep planes * rows_per_plane below 2^31
   int pair = xcd_remap(blockIdx.x, gridDim.x) * SPW + s;
   const bool active = pair < npairs;
@@ -331,9 +357,9 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r_r2c(SpecLayout 
     const float2 A = make_float2((zk.x + zn.x) * wgt, (zk.y - zn.y) * wgt);
     const float2 Bv = make_float2((zk.y + zn.y) * wgt, (zn.x - zk.x) * wgt);
     if (k < Lout - 1) {
-      const long long o = bin_off(out, k);
-      oa[o] = A;
-      ob[o] = Bv;
+      const unsigned o = bin_off32(out, k);
+      at32(oa, o) = A;
+      at32(ob, o) = Bv;
     } else {
       float2 *so = out.side + plane * out.sps + (long long)r0 * out.srs;
       so[0] = A;
