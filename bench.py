@@ -57,8 +57,10 @@ def layer_dims(wl, i):
 def fwd_col_launches(B, C, S, N, M, L):
     """The forward's column work of one layer: the column DFT with the FDP crop (writes
     the saved spectrum) and the CIC product with the inverse column DFT, in one kernel
-    when an input channel has 1, 2 or 4 output channels, else in two."""
-    if S // C in (1, 2, 4):
+    when an input channel has 1, 2 or 4 output channels (or 8, at N <= 256), else in two.
+    At 8 the kernel's two channel groups each read the input columns; the model counts
+    them once (algorithmic bytes)."""
+    if S // C in (1, 2, 4) or (S // C == 8 and N <= 256):
         return [(f"col_fwd_cic_{N}_{M}", C64 * (B * C * N * L + B * C * M * L + S * M * L + B * S * M * L))]
     return [(f"col_fwd_crop_{N}_{M}", C64 * (B * C * N * L + B * C * M * L)),
             (f"col_cic_inv_{N}_{M}", C64 * (B * C * M * L + S * M * L + B * S * M * L))]

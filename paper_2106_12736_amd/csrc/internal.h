@@ -122,12 +122,14 @@ hipError_t launch_col_fft_split(int n, int dir, SpecLayout in, SpecLayout out, l
 
 // Fused CIC + FDP column kernels (square n x n images pooled to m x m; L = m/2 + 1).
 // T, Xh, U, Tg and V are split-layout spectra (SpecLayout) with L bins per row.
-//   fwd:   T [B*C][n rows] -> Xh [B*C][m rows] (written, then read) -> U [B*S][m rows]
+//   fwd:   T [B*C][n rows] -> Xh [B*C][m rows] and U [B*S][m rows] (one kernel, or two
+//          with Xh written and read back)
 //   bwd_gk: Tg [B*S][m rows], Xh -> gK [S][n][n/2+1]: every bin (zeros where FDP drops)
 //   bwd_gx: Tg, K -> V [B*C][n rows]
 bool cic_pair_supported(int n, int m);
-// Whether the forward's two column kernels run as one (k_col_fwd_cic) for J = S / C.
-bool fwd_cic_fused(int J);
+// Output channels per workgroup when the forward's two column kernels run as one
+// (k_col_fwd_cic) for J = S / C and n-point columns, else 0.
+int fwd_cic_jw(int J, int n);
 hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, float2 *U, float2 *Xh, int B,
                               int C, int S, hipStream_t s);
 // dK: with scratch `part` (part_elems complex values; may be NULL) the batch is cut

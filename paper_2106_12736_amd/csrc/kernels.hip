@@ -620,17 +620,19 @@ __global__ __launch_bounds__(CT *ColCfg<M>::TPS) void k_col_cic_inv(const float2
   }
 }
 
-// Forward, both halves in one kernel for layers whose output channels per input
-// channel all fit one workgroup (JW = J): column DFT (N) of T, the kept rows to Xh and
-// to an LDS tile, then the CIC product (Eq. 5) and inverse column DFT (M) for each of
-// the J output channels.  The N-point thread layout holds JP = TPS_N / TPS_M groups
-// of the M-point layout, which take the output channels in turns.  Planes and tile
-// order as k_col_cic_inv (JB = 1): the B images of one input channel in a row.
+// Forward, both halves in one kernel: column DFT (N) of T, the kept rows to Xh and to
+// an LDS tile, then the CIC product (Eq. 5) and inverse column DFT (M) for JW output
+// channels.  The J = JW * JB output channels of an input channel are split over JB
+// workgroup groups, each of which transforms the input column itself (group 0 stores
+// Xh).  The N-point thread layout holds JP = TPS_N / TPS_M groups of the M-point
+// layout, which take the output channels in turns.  Planes and tile order as
+// k_col_cic_inv: group index (ci * JB + jb) * B + b, the B images of one input
+// channel and channel group in a row.
 template <int N, int M, int CT, int JW>
 __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fwd_cic(const float2 *__restrict__ T,
                                                                    const float2 *__restrict__ K,
                                                                    float2 *__restrict__ U, float2 *__restrict__ Xh,
-                                                                   int B, int C) {
+                                                                   int B, int C, int JB) {
   using CN = ColCfg<N>;
   using CM = ColCfg<M>;
   constexpr int L = M / 2 + 1, NF = N / 2 + 1, TPSN = CN::TPS, TPSM = CM::TPS, EN = CN::E, EM = CM::E;
@@ -641,9 +643,10 @@ __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fwd_cic(const float2
   tws.fetch(threadIdx.x);
   const int s = threadIdx.x % CT, t = threadIdx.x / CT;
   const int tp = t % TPSM, js = t / TPSM;
-  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, B * C, B);
-  const int b = c.plane % B, ci = c.plane / B;
-  const int bc = b * C + ci, S = C * JW;
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, B * C * JB, B);
+  const int b = c.plane % B, cj = c.plane / B;
+  const int ci = cj / JB, jb = cj - ci * JB;
+  const int bc = b * C + ci, J = JW * JB, S = C * J;
   const ColPtr tc = tiled_col<N, L>(T, B * C, bc, c.l);
   float2 v[EN];
 #pragma unroll
@@ -657,7 +660,7 @@ __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fwd_cic(const float2
     const int k = t + TPSN * m;
     if (k < M / 2 || k >= N - M / 2) {
       const int mrow = k < M / 2 ? k : k - (N - M);
-      if (c.ok) xc.p[mrow * xc.stride] = v[m];
+      if (c.ok && jb == 0) xc.p[mrow * xc.stride] = v[m];
       lds[s + mrow * CT] = v[m];
     }
   }
@@ -668,7 +671,7 @@ __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fwd_cic(const float2
   for (int j0 = 0; j0 < JW; j0 += JP) {
     const int jj = j0 + js;
     const bool act = c.ok && jj < JW;
-    const int o = ci * JW + (jj < JW ? jj : 0);
+    const int o = ci * J + jb * JW + (jj < JW ? jj : 0);
     const float2 *kcol = K + (long long)o * N * NF + c.l;
     float2 z[EM];
 #pragma unroll
@@ -1289,7 +1292,13 @@ hipError_t launch_col_fft_split(int n, int dir, SpecLayout in, SpecLayout out, l
   return err;
 }
 
-bool fwd_cic_fused(int J) { return J == 1 || J == 2 || J == 4; }
+// Output channels per workgroup of the fused forward column kernel for J output
+// channels per input channel and n-point columns (0: not fused, the crop and CIC
+// inverse kernels run instead).  J = 8 at n <= 256 is split into two groups of four,
+// each of which transforms the input column itself: at 256 points that costs less than
+// storing the pooled spectrum and reading it back (the 256^2 stack 0.0797 -> 0.0771 ms);
+// at 512 and 1024 points it measured slower (0.3051 -> 0.3087 ms) or the same.
+int fwd_cic_jw(int J, int n) { return (J == 1 || J == 2 || J == 4) ? J : ((J == 8 && n <= 256) ? 4 : 0); }
 
 hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, float2 *U, float2 *Xh, int B,
                               int C, int S, hipStream_t s) {
@@ -1301,14 +1310,17 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
     static const std::string n1 = "col_fwd_crop_" + std::to_string(N) + "_" + std::to_string(M);
     static const std::string n2 = "col_cic_inv_" + std::to_string(N) + "_" + std::to_string(M);
     static const std::string n3 = "col_fwd_cic_" + std::to_string(N) + "_" + std::to_string(M);
-    const int J = S / C;
-    if (fwd_cic_fused(J)) {
-      // both halves in one kernel: J output channels per workgroup
-      const unsigned g = col_grid((long long)B * C, L, CTN);
+    const int J = S / C, jwf = fwd_cic_jw(J, N);
+    if (jwf > 0) {
+      // both halves in one kernel: jwf output channels per workgroup
+      const int jb = J / jwf;
+      const unsigned g = col_grid((long long)B * C * jb, L, CTN);
       if (g == 0) return;
       const size_t lds = (twiddle_lds_elems<N>() + fwd_cic_lds_elems<N, M, CTN>()) * sizeof(float2);
-      auto go = [&](auto kern) { err = launch(n3.c_str(), kern, g, CTN * ColCfg<N>::TPS, lds, s, T, K, U, Xh, B, C); };
-      switch (J) {
+      auto go = [&](auto kern) {
+        err = launch(n3.c_str(), kern, g, CTN * ColCfg<N>::TPS, lds, s, T, K, U, Xh, B, C, jb);
+      };
+      switch (jwf) {
         case 4: go(k_col_fwd_cic<N, M, CTN, 4>); break;
         case 2: go(k_col_fwd_cic<N, M, CTN, 2>); break;
         default: go(k_col_fwd_cic<N, M, CTN, 1>);
