@@ -198,25 +198,30 @@ __host__ __device__ constexpr int row_scratch(int items) {
 // ----------------------------------------------------------------------------
 // forward
 // ----------------------------------------------------------------------------
-// One workgroup per input plane (b, c) of layer a; workgroup w after the XCD remap
-// takes c = w / B, b = w % B (the B images of one channel read the same kernels).
+// One workgroup per input plane (b, c) of layer a and group of JL of its JA output
+// channels (JL = JA, or fewer when the input planes alone would leave compute units
+// idle: each group then repeats stages A and B, and group 0 stores saved_a); workgroup
+// w after the XCD remap takes b = w % B, then the group, then c (the B images of one
+// channel group read the same kernels).
 //   FIRST = false: in = previous layer's column-inverted spectra, split layout
 //                  [B * C][NA rows][NA/2+1], inverse row weights a_in (= 1 / NA^2).
 //   FIRST = true:  x = input images [B][C][NA][NA].
 //   saved_a: split [B * C][MA][LA]; saved_b: split [B * S_a][MB][LB];
 //   Ka [S_a][NA][NA/2+1], Kb [S_b][MA][MA/2+1]; y [B][S_b][MB][MB].
-template <int NA, int MA, int MB, int JA, int JB, int NT, bool FIRST>
+template <int NA, int MA, int MB, int JA, int JB, int NT, bool FIRST, int JL>
 __global__ __launch_bounds__(NT) void k_tail_fwd(SpecLayout in, const float *__restrict__ x, float a_in,
                                                  const float2 *__restrict__ Ka, const float2 *__restrict__ Kb,
                                                  SpecLayout saved_a, SpecLayout saved_b, float *__restrict__ y, int B,
                                                  int C) {
-  using G = TailGeom<NA, MA, MB, JA, JB>;
+  static_assert(JA % JL == 0, "channel groups of equal size");
+  using G = TailGeom<NA, MA, MB, JL, JB>;
   constexpr int LA = G::LA, LB = G::LB, ldA = G::ldA, ldB = G::ldB;
-  constexpr int NFA = NA / 2 + 1, NFB = MA / 2 + 1;
+  constexpr int NFA = NA / 2 + 1, NFB = MA / 2 + 1, JG = JA / JL;
   float2 *tw = t_lds;
   stage_twiddles<NA>(tw, threadIdx.x, NT);
   const int wg = xcd_remap(blockIdx.x, gridDim.x);
-  const int c = wg / B, b = wg - (wg / B) * B;
+  const int b = wg % B, cg = wg / B;
+  const int c = cg / JG, j0 = (cg - c * JG) * JL;  // this group's first layer-a output of channel c
   const int Sa = C * JA, Sb = Sa * JB;
   float2 *TA = t_lds + G::fTA, *XA = t_lds + G::fXA, *UA = t_lds + G::fUA, *TB = t_lds + G::fTB,
          *XB = t_lds + G::fXB, *UB = t_lds + G::fUB;
@@ -224,30 +229,30 @@ __global__ __launch_bounds__(NT) void k_tail_fwd(SpecLayout in, const float *__r
   // The kernel bins of stages C and F, loaded now (when each stage is one round of its
   // column pass, so that this thread's item is known): their loads complete with
   // stage A's, instead of each stage waiting for its own.
-  constexpr bool PC = JA * LA <= NT / Plan<MA>::TPS, PF = JA * JB * LB <= NT / Plan<MB>::TPS;
+  constexpr bool PC = JL * LA <= NT / Plan<MA>::TPS, PF = JL * JB * LB <= NT / Plan<MB>::TPS;
   float2 kpa[Plan<MA>::E], kpb[Plan<MB>::E];
   if constexpr (PC) {
     const ColLanes<MA> ln;
     const int it = ln.first + ln.s;
-    const bool act = it < JA * LA;
+    const bool act = it < JL * LA;
     const int j = act ? it / LA : 0, lc = act ? it - (it / LA) * LA : 0;
-    const float2 *kc = Ka + (long long)(c * JA + j) * NA * NFA + lc;
+    const float2 *kc = Ka + (long long)(c * JA + j0 + j) * NA * NFA + lc;
 #pragma unroll
     for (int m = 0; m < Plan<MA>::E; ++m) kpa[m] = kc[(long long)kept<NA, MA>(ln.t + Plan<MA>::TPS * m) * NFA];
   }
   if constexpr (PF) {
     const ColLanes<MB> ln;
     const int it = ln.first + ln.s;
-    const bool act = it < JA * JB * LB;
+    const bool act = it < JL * JB * LB;
     const int q = act ? it / LB : 0, lc = act ? it - (it / LB) * LB : 0;
-    const float2 *kc = Kb + (long long)((c * JA) * JB + q) * MA * NFB + lc;
+    const float2 *kc = Kb + (long long)((c * JA + j0) * JB + q) * MA * NFB + lc;
 #pragma unroll
     for (int m = 0; m < Plan<MB>::E; ++m) kpb[m] = kc[(long long)kept<MA, MB>(ln.t + Plan<MB>::TPS * m) * NFB];
   }
 
   // A: layer a's input rows -> TA [NA][LA]
   {
-    float2 *scr = UA;  // UA, TB are not in use yet
+    float2 *scr = UA;  // UA and the planes after it are not in use yet (tail_fwd_lds covers the scratch)
     constexpr int TPS = Plan<NA>::TPS, SEQ = NT / TPS;
     const RowLanes<NA> ln;
     const long long plane = (long long)b * C + c;
@@ -289,18 +294,18 @@ __global__ __launch_bounds__(NT) void k_tail_fwd(SpecLayout in, const float *__r
             if (k < MA / 2 || k >= NA - MA / 2) {
               const int mrow = k < MA / 2 ? k : k - (NA - MA);
               XA[mrow * ldA + l] = v[m];
-              *spec_at(saved_a, plane, mrow, l, LA) = v[m];
+              if (JG == 1 || j0 == 0) *spec_at(saved_a, plane, mrow, l, LA) = v[m];
             }
           }
         });
   }
   __syncthreads();
-  // C: CIC product with K_a[c JA + j] (Eq. 5) and inverse column DFT (MA) -> UA[j]
+  // C: CIC product with K_a[c JA + j0 + j] (Eq. 5) and inverse column DFT (MA) -> UA[j]
   col_pass<MA, +1, NT>(
-      JA, LA, tw, NA / MA,
+      JL, LA, tw, NA / MA,
       [&](float2 (&v)[Plan<MA>::E], int j, int l, int t, bool act) {
         const int lc = act ? l : 0;
-        const float2 *kc = Ka + (long long)(c * JA + j) * NA * NFA + lc;
+        const float2 *kc = Ka + (long long)(c * JA + j0 + j) * NA * NFA + lc;
 #pragma unroll
         for (int m = 0; m < Plan<MA>::E; ++m) {
           const int mrow = t + Plan<MA>::TPS * m;
@@ -320,9 +325,9 @@ __global__ __launch_bounds__(NT) void k_tail_fwd(SpecLayout in, const float *__r
     constexpr int TPS = Plan<MA>::TPS, SEQ = NT / TPS, P = MA / 2;
     const RowLanes<MA> ln;
     const float inv = 1.f / ((float)MA * (float)MA);
-    for (int r0 = 0; r0 + ln.first < JA * P; r0 += SEQ) {
+    for (int r0 = 0; r0 + ln.first < JL * P; r0 += SEQ) {
       const int it = r0 + ln.first + ln.s;
-      const bool act = it < JA * P;
+      const bool act = it < JL * P;
       const int j = act ? it / P : 0, r = 2 * (act ? it % P : 0);
       const float2 *u = UA + j * MA * ldA + r * ldA;
       float2 v[Plan<MA>::E];
@@ -338,7 +343,7 @@ __global__ __launch_bounds__(NT) void k_tail_fwd(SpecLayout in, const float *__r
   __syncthreads();
   // E: column DFT (MA) of TB[j], keep MB rows -> XB[j] and saved_b
   col_pass<MA, -1, NT>(
-      JA, LB, tw, NA / MA,
+      JL, LB, tw, NA / MA,
       [&](float2 (&v)[Plan<MA>::E], int j, int l, int t, bool) {
 #pragma unroll
         for (int m = 0; m < Plan<MA>::E; ++m) v[m] = TB[j * MA * ldB + (t + Plan<MA>::TPS * m) * ldB + l];
@@ -346,7 +351,7 @@ __global__ __launch_bounds__(NT) void k_tail_fwd(SpecLayout in, const float *__r
       [&](int j) { return TB + j * MA * ldB; },
       [&](const float2 (&v)[Plan<MA>::E], int j, int l, int t, bool act) {
         if (!act) return;
-        const long long plane = (long long)b * Sa + c * JA + j;
+        const long long plane = (long long)b * Sa + c * JA + j0 + j;
 #pragma unroll
         for (int m = 0; m < Plan<MA>::E; ++m) {
           const int k = t + Plan<MA>::TPS * m;
@@ -358,12 +363,12 @@ __global__ __launch_bounds__(NT) void k_tail_fwd(SpecLayout in, const float *__r
         }
       });
   __syncthreads();
-  // F: CIC product with K_b[(c JA + j) JB + i] and inverse column DFT (MB) -> UB[j JB + i]
+  // F: CIC product with K_b[(c JA + j0 + j) JB + i] and inverse column DFT (MB) -> UB[j JB + i]
   col_pass<MB, +1, NT>(
-      JA * JB, LB, tw, NA / MB,
+      JL * JB, LB, tw, NA / MB,
       [&](float2 (&v)[Plan<MB>::E], int q, int l, int t, bool act) {
         const int j = q / JB, lc = act ? l : 0;
-        const float2 *kc = Kb + (long long)((c * JA) * JB + q) * MA * NFB + lc;
+        const float2 *kc = Kb + (long long)((c * JA + j0) * JB + q) * MA * NFB + lc;
 #pragma unroll
         for (int m = 0; m < Plan<MB>::E; ++m) {
           const int mrow = t + Plan<MB>::TPS * m;
@@ -377,22 +382,22 @@ __global__ __launch_bounds__(NT) void k_tail_fwd(SpecLayout in, const float *__r
         for (int m = 0; m < Plan<MB>::E; ++m) UB[q * MB * ldB + (t + Plan<MB>::TPS * m) * ldB + l] = v[m];
       });
   __syncthreads();
-  // G: inverse rows of UB[q] (1/MB^2) -> y [b][(c JA JB) + q]
+  // G: inverse rows of UB[q] (1/MB^2) -> y [b][(c JA + j0) JB + q]
   {
     float2 *scr = TA;
     constexpr int TPS = Plan<MB>::TPS, SEQ = NT / TPS, P = MB / 2;
     const RowLanes<MB> ln;
     const float inv = 1.f / ((float)MB * (float)MB);
-    for (int r0 = 0; r0 + ln.first < JA * JB * P; r0 += SEQ) {
+    for (int r0 = 0; r0 + ln.first < JL * JB * P; r0 += SEQ) {
       const int it = r0 + ln.first + ln.s;
-      const bool act = it < JA * JB * P;
+      const bool act = it < JL * JB * P;
       const int q = act ? it / P : 0, r = 2 * (act ? it % P : 0);
       const float2 *u = UB + q * MB * ldB + r * ldB;
       float2 v[Plan<MB>::E];
       c2r_in<MB, LB>(v, [&](int rr, int k) { return u[rr * ldB + k]; }, ln.t, inv, 1.f);
       fft_seq<MB, +1, true, true, kLdsPad, Plan<MB>>(v, ln.t, scr, (ln.first + ln.s) * MB, 1, tw, NA / MB);
       if (act) {
-        float *yr = y + ((long long)b * Sb + c * JA * JB + q) * MB * MB + (long long)r * MB;
+        float *yr = y + ((long long)b * Sb + (c * JA + j0) * JB + q) * MB * MB + (long long)r * MB;
 #pragma unroll
         for (int m = 0; m < Plan<MB>::E; ++m) {
           yr[ln.t + TPS * m] = v[m].x;
@@ -736,16 +741,22 @@ __global__ __launch_bounds__(256) void k_fft2_small_inv(const float2 *__restrict
 #endif
 constexpr int kTailThreads = FDC_TAIL_THREADS;
 
-template <int NA, int MA, int MB, int JA, int JB>
+// LDS of the forward with JL layer-a output channels per workgroup.
+template <int NA, int MA, int MB, int JL, int JB>
 constexpr size_t tail_fwd_lds() {
-  using G = TailGeom<NA, MA, MB, JA, JB>;
+  using G = TailGeom<NA, MA, MB, JL, JB>;
   constexpr int T = kTailThreads;
-  // row scratch aliases: A in UA.., D and G in TA
-  static_assert(G::fUA + row_scratch<NA, T>(NA / 2) <= G::fEnd, "tail forward: row scratch A");
-  static_assert(G::fTA + row_scratch<MA, T>(JA * MA / 2) <= G::fXA, "tail forward: row scratch D");
-  static_assert(G::fTA + row_scratch<MB, T>(JA * JB * MB / 2) <= G::fXA, "tail forward: row scratch G");
-  return (size_t)G::fEnd * sizeof(float2);
+  // row scratch aliases: A from UA on (past the planes when they are smaller), D and G in TA
+  constexpr int endA = G::fUA + row_scratch<NA, T>(NA / 2);
+  static_assert(G::fTA + row_scratch<MA, T>(JL * MA / 2) <= G::fXA, "tail forward: row scratch D");
+  static_assert(G::fTA + row_scratch<MB, T>(JL * JB * MB / 2) <= G::fXA, "tail forward: row scratch G");
+  return (size_t)(endA > G::fEnd ? endA : G::fEnd) * sizeof(float2);
 }
+
+// Input planes below which the forward tail splits each plane's layer-a output channels
+// over two workgroups, so that the launch covers the compute units (at 256^2, 16 images
+// of 8 channels: 128 planes).
+constexpr long long kTailSplitPlanes = 256;
 
 template <int NA, int MA, int MB, int JA, int JB>
 constexpr size_t tail_bwd_lds() {
@@ -799,16 +810,27 @@ hipError_t launch_tail_fwd(int na, int ma, int mb, int ja, int jb, SpecLayout in
   dispatch_tail(na, ma, mb, ja, jb, [&](auto nac, auto mac, auto mbc, auto jac, auto jbc) {
     constexpr int NA = decltype(nac)::value, MA = decltype(mac)::value, MB = decltype(mbc)::value;
     constexpr int JA = decltype(jac)::value, JB = decltype(jbc)::value;
-    constexpr size_t lds = tail_fwd_lds<NA, MA, MB, JA, JB>();
     static const std::string nm =
         "tail_fwd_" + std::to_string(NA) + "_" + std::to_string(MA) + "_" + std::to_string(MB);
-    const unsigned grid = (unsigned)((long long)B * C);
-    if (x != nullptr)
-      err = tail_launch<k_tail_fwd<NA, MA, MB, JA, JB, kTailThreads, true>>(nm.c_str(), grid, lds, s, in, x, a_in,
-                                                                             Ka, Kb, saved_a, saved_b, y, B, C);
-    else
-      err = tail_launch<k_tail_fwd<NA, MA, MB, JA, JB, kTailThreads, false>>(nm.c_str(), grid, lds, s, in, x, a_in,
-                                                                              Ka, Kb, saved_a, saved_b, y, B, C);
+    const long long planes = (long long)B * C;
+    auto go = [&](auto jlc) {
+      constexpr int JL = decltype(jlc)::value;
+      constexpr size_t lds = tail_fwd_lds<NA, MA, MB, JL, JB>();
+      const unsigned grid = (unsigned)(planes * (JA / JL));
+      if (x != nullptr)
+        err = tail_launch<k_tail_fwd<NA, MA, MB, JA, JB, kTailThreads, true, JL>>(
+            nm.c_str(), grid, lds, s, in, x, a_in, Ka, Kb, saved_a, saved_b, y, B, C);
+      else
+        err = tail_launch<k_tail_fwd<NA, MA, MB, JA, JB, kTailThreads, false, JL>>(
+            nm.c_str(), grid, lds, s, in, x, a_in, Ka, Kb, saved_a, saved_b, y, B, C);
+    };
+    if constexpr (JA % 2 == 0) {
+      if (planes < kTailSplitPlanes) {
+        go(std::integral_constant<int, JA / 2>{});
+        return;
+      }
+    }
+    go(std::integral_constant<int, JA>{});
   });
   return err;
 }
