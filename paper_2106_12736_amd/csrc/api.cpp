@@ -119,23 +119,17 @@ void timing_release(Timing &t) {
 }  // namespace
 
 namespace fdc {
-void timing_before(const char *name, hipStream_t s) {
+bool timing_slot(const char *name, hipEvent_t *start, hipEvent_t *stop) {
   Timing &t = timing();
-  if (!t.enabled) return;
+  if (!t.enabled) return false;
   std::lock_guard<std::mutex> g(t.mu);
-  if (t.used >= t.max) return;
-  if (!t.only.empty() && t.only != name) return;
+  if (t.used >= t.max) return false;
+  if (!t.only.empty() && t.only != name) return false;
   t.names[t.used] = name;
-  (void)hipEventRecord(t.start[t.used], s);
-}
-void timing_after(const char *name, hipStream_t s) {
-  Timing &t = timing();
-  if (!t.enabled) return;
-  std::lock_guard<std::mutex> g(t.mu);
-  if (t.used >= t.max) return;
-  if (!t.only.empty() && t.only != name) return;
-  (void)hipEventRecord(t.stop[t.used], s);
+  *start = t.start[t.used];
+  *stop = t.stop[t.used];
   ++t.used;
+  return true;
 }
 }  // namespace fdc
 

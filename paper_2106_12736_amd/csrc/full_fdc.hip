@@ -577,12 +577,8 @@ hipError_t launch_full_weights(const float *w, float *wt, bool gx, int S, int C,
   const long long n = (long long)KDp * NDp * TP;
   long long g = (n + 255) / 256;
   if (g > 65536) g = 65536;
-  timing_before("full_weights", s);
-  hipLaunchKernelGGL(k_full_weights, dim3((unsigned)g), dim3(256), 0, s, w, wt, S, C, nk * nk, TP, gx ? 1 : 0, KDp,
-                     NDp);
-  const hipError_t e = hipGetLastError();
-  timing_after("full_weights", s);
-  return e;
+  return timed_launch("full_weights", k_full_weights, dim3((unsigned)g), dim3(256), 0, s, w, wt, S, C, nk * nk, TP,
+                      gx ? 1 : 0, KDp, NDp);
 }
 
 hipError_t launch_full_contract(bool gx, int nk, SpecLayout in, const float *wt, const float2 *tw, SpecLayout out,
@@ -596,15 +592,12 @@ hipError_t launch_full_contract(bool gx, int nk, SpecLayout in, const float *wt,
   dispatch_nk(nk, [&](auto nc) {
     constexpr int NK = decltype(nc)::value;
     const char *nm = gx ? "full_contract_gx" : "full_contract_fwd";
-    timing_before(nm, s);
     if (gx)
-      hipLaunchKernelGGL((k_full_contract<NK, true>), dim3((unsigned)blocks), dim3(256), 0, s, in, wt, tw, out, B,
+      err = timed_launch(nm, k_full_contract<NK, true>, dim3((unsigned)blocks), dim3(256), 0, s, in, wt, tw, out, B,
                          KD, KDp, ND, NDp, P, nwg_run, nsb);
     else
-      hipLaunchKernelGGL((k_full_contract<NK, false>), dim3((unsigned)blocks), dim3(256), 0, s, in, wt, tw, out, B,
+      err = timed_launch(nm, k_full_contract<NK, false>, dim3((unsigned)blocks), dim3(256), 0, s, in, wt, tw, out, B,
                          KD, KDp, ND, NDp, P, nwg_run, nsb);
-    err = hipGetLastError();
-    timing_after(nm, s);
   });
   return err;
 }
@@ -639,30 +632,20 @@ hipError_t launch_full_gw(int nk, SpecLayout G, SpecLayout X, const float2 *tw, 
   hipError_t err = hipErrorInvalidValue;
   dispatch_nk(nk, [&](auto nc) {
     constexpr int NK = decltype(nc)::value;
-    size_t lds = ((size_t)gw_tw_elems<NK>(P) + 2 * kGwStageElems) * sizeof(float2);
+    const size_t lds = ((size_t)gw_tw_elems<NK>(P) + 2 * kGwStageElems) * sizeof(float2);
     if (lds > 65536) return;  // (P <= 1024, n <= 5 stays within 60 KB)
-#ifdef FDC_GW_OCC2
-    if (tiles == 64 && lds < 56 * 1024) lds = 56 * 1024;
-#endif
-    timing_before("full_gw", s);
     if (((B + 3) / 4) % 2 == 0)
-      hipLaunchKernelGGL((k_full_gw<NK, true>), dim3((unsigned)(tiles * chunks)), dim3(256), lds, s, G, X, tw, part, B,
-                         S, C, P, runs_per_chunk);
+      err = timed_launch("full_gw", k_full_gw<NK, true>, dim3((unsigned)(tiles * chunks)), dim3(256), lds, s, G, X, tw,
+                         part, B, S, C, P, runs_per_chunk);
     else
-      hipLaunchKernelGGL((k_full_gw<NK, false>), dim3((unsigned)(tiles * chunks)), dim3(256), lds, s, G, X, tw, part,
-                         B, S, C, P, runs_per_chunk);
-    err = hipGetLastError();
-    timing_after("full_gw", s);
+      err = timed_launch("full_gw", k_full_gw<NK, false>, dim3((unsigned)(tiles * chunks)), dim3(256), lds, s, G, X,
+                         tw, part, B, S, C, P, runs_per_chunk);
   });
   if (err != hipSuccess) return err;
   const long long n = (long long)S * C * nk * nk;
   const long long g = (n + 63) / 64;
   if (g >= (1LL << 31)) return hipErrorInvalidValue;
-  timing_before("full_gw_reduce", s);
-  hipLaunchKernelGGL(k_full_gw_reduce, dim3((unsigned)g), dim3(256), 0, s, part, gw, n, chunks);
-  err = hipGetLastError();
-  timing_after("full_gw_reduce", s);
-  return err;
+  return timed_launch("full_gw_reduce", k_full_gw_reduce, dim3((unsigned)g), dim3(256), 0, s, part, gw, n, chunks);
 }
 
 }  // namespace fdc

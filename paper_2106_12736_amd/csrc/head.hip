@@ -206,18 +206,11 @@ hipError_t launch_head_forward(const float *y, const float *W, const float *bias
                                float *loss, float *part, int B, long long F, int classes, hipStream_t s) {
   const long long chunks = head_chunks(F);
   if (chunks >= (1LL << 31) || B > 65535) return hipErrorInvalidValue;
-  timing_before("head_fwd", s);
-  hipLaunchKernelGGL(k_head_fwd, dim3((unsigned)chunks, (unsigned)B), dim3(kHeadThreads), 0, s, y, W, part, F,
-                     classes, (int)chunks);
-  hipError_t e = hipGetLastError();
-  timing_after("head_fwd", s);
+  const hipError_t e = timed_launch("head_fwd", k_head_fwd, dim3((unsigned)chunks, (unsigned)B), dim3(kHeadThreads), 0,
+                                    s, y, W, part, F, classes, (int)chunks);
   if (e != hipSuccess) return e;
-  timing_before("head_loss", s);
-  hipLaunchKernelGGL(k_head_loss, dim3(1), dim3(kHeadThreads), (size_t)B * classes * sizeof(float), s, part, bias,
-                     labels, logits, loss, B, classes, (int)chunks);
-  e = hipGetLastError();
-  timing_after("head_loss", s);
-  return e;
+  return timed_launch("head_loss", k_head_loss, dim3(1), dim3(kHeadThreads), (size_t)B * classes * sizeof(float), s,
+                      part, bias, labels, logits, loss, B, classes, (int)chunks);
 }
 
 // Partial logits of the allocation-free forward (fdc_head_forward_noalloc): one array
@@ -265,12 +258,8 @@ hipError_t launch_head_backward(const float *y, const float *W, const float *log
   const long long blocks = (F + kHeadThreads - 1) / kHeadThreads;
   if (blocks >= (1LL << 31)) return hipErrorInvalidValue;
   const size_t lds = (size_t)B * classes * sizeof(float);
-  timing_before("head_bwd", s);
-  hipLaunchKernelGGL(k_head_bwd, dim3((unsigned)blocks), dim3(kHeadThreads), lds, s, y, W, logits, labels, gy, gW,
-                     gbias, F, B, classes);
-  const hipError_t e = hipGetLastError();
-  timing_after("head_bwd", s);
-  return e;
+  return timed_launch("head_bwd", k_head_bwd, dim3((unsigned)blocks), dim3(kHeadThreads), lds, s, y, W, logits, labels,
+                      gy, gW, gbias, F, B, classes);
 }
 
 hipError_t launch_adam(float *p, const float *g, float *m, float *v, long long n, int *count, float lr, float beta1,
@@ -281,22 +270,15 @@ hipError_t launch_adam(float *p, const float *g, float *m, float *v, long long n
   if (blocks > 65536) blocks = 65536;
   hipError_t e = hipSuccess;
   if (blocks > 0) {
-    timing_before("adam", s);
     if (vec)
-      hipLaunchKernelGGL(k_adam<true>, dim3((unsigned)blocks), dim3(256), 0, s, p, g, m, v, n, count, lr, beta1,
-                         beta2, eps, wd);
+      e = timed_launch("adam", k_adam<true>, dim3((unsigned)blocks), dim3(256), 0, s, p, g, m, v, n, count, lr, beta1,
+                       beta2, eps, wd);
     else
-      hipLaunchKernelGGL(k_adam<false>, dim3((unsigned)blocks), dim3(256), 0, s, p, g, m, v, n, count, lr, beta1,
-                         beta2, eps, wd);
-    e = hipGetLastError();
-    timing_after("adam", s);
+      e = timed_launch("adam", k_adam<false>, dim3((unsigned)blocks), dim3(256), 0, s, p, g, m, v, n, count, lr, beta1,
+                       beta2, eps, wd);
     if (e != hipSuccess) return e;
   }
-  timing_before("adam_count", s);
-  hipLaunchKernelGGL(k_adam_count, dim3(1), dim3(64), 0, s, count);
-  e = hipGetLastError();
-  timing_after("adam_count", s);
-  return e;
+  return timed_launch("adam_count", k_adam_count, dim3(1), dim3(64), 0, s, count);
 }
 
 }  // namespace fdc

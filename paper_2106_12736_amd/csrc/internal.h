@@ -2,6 +2,7 @@
 // (kernels.hip, full_fdc.hip).  Not installed; not part of the ABI.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -90,9 +91,23 @@ inline long long full_spec_elems(long long planes, int P) {
   return planes * ((long long)P * FDC_FULL_ROW(P) + FDC_FULL_SIDE_PLANE(P));
 }
 
-// Kernel timing hooks (no-ops unless enabled through the ABI).
-void timing_before(const char *name, hipStream_t s);
-void timing_after(const char *name, hipStream_t s);
+// Kernel timing (enabled through the ABI): the start and stop events of the next slot
+// when launches of `name` are being timed, else false.
+bool timing_slot(const char *name, hipEvent_t *start, hipEvent_t *stop);
+
+// Launch kern; while its launches are timed, through hipExtLaunchKernelGGL with a slot's
+// events, which the dispatch itself records at the kernel's start and end (so the
+// interval is the kernel's execution, without event records of their own around it).
+template <class Kern, class... Args>
+inline hipError_t timed_launch(const char *name, Kern kern, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                               Args... args) {
+  hipEvent_t e0, e1;
+  if (timing_slot(name, &e0, &e1))
+    hipExtLaunchKernelGGL(kern, grid, block, (std::uint32_t)lds, s, e0, e1, 0u, args...);
+  else
+    hipLaunchKernelGGL(kern, grid, block, lds, s, args...);
+  return hipGetLastError();
+}
 
 // Row transforms of real rows of length n (n in the supported set), processed in pairs.
 // rows_per_plane must be even.  Output/input bins beyond L are not written / read as zero;

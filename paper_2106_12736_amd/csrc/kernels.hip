@@ -875,11 +875,7 @@ static hipError_t gk_reduce(const GkSum &d0, const GkSum *d1, hipStream_t s) {
   if (d1) total = std::max(total, (long long)d1->S * d1->N * (d1->N / 2 + 1));
   const unsigned gx = (unsigned)std::min<long long>((total + kGkReduceThreads - 1) / kGkReduceThreads, 1 << 16);
   const char *nm = "gk_reduce";
-  timing_before(nm, s);
-  hipLaunchKernelGGL(k_gk_reduce, dim3(gx, d1 ? 2 : 1), dim3(kGkReduceThreads), 0, s, d0, d1 ? *d1 : d0);
-  const hipError_t e = hipGetLastError();
-  timing_after(nm, s);
-  return e;
+  return timed_launch(nm, k_gk_reduce, dim3(gx, d1 ? 2 : 1), dim3(kGkReduceThreads), 0, s, d0, d1 ? *d1 : d0);
 }
 
 template <int N, int M>
@@ -1142,11 +1138,7 @@ template <class Kern, class... Args>
 static hipError_t launch(const char *name, Kern kern, unsigned grid, unsigned block, size_t lds, hipStream_t s,
                          Args... args) {
   if (grid == 0) return hipSuccess;
-  timing_before(name, s);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(block), lds, s, args...);
-  const hipError_t e = hipGetLastError();
-  timing_after(name, s);
-  return e;
+  return timed_launch(name, kern, dim3(grid), dim3(block), lds, s, args...);
 }
 
 static unsigned grid_stride_blocks(long long total, int block) {
@@ -1801,21 +1793,19 @@ hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B
   const dim3 g0 = plane_grid((long long)M * (M / 2 + 1) / 2, 1);
   if ((long long)g0.x * S >= (1LL << 31)) return hipErrorInvalidValue;
   const int jb = fdp_fwd_jb(g0.x, C, J);
-  timing_before("cic_fdp_fwd", s);
+  hipError_t e = hipSuccess;
   dispatch_jb(jb, [&](auto jc) {
     constexpr int JB = decltype(jc)::value;
     const long long nmain = g0.x * (long long)C * (J / JB);
     if (project) {
       const long long nedge = ((long long)B * S * M * 2 + 255) / 256;
-      hipLaunchKernelGGL((k_cic_fdp_fwd<JB, true>), dim3((unsigned)(nmain + nedge)), dim3(256), 0, s, X, K, Y, B, C,
-                         J, N, M, (int)nmain);
+      e = timed_launch("cic_fdp_fwd", k_cic_fdp_fwd<JB, true>, dim3((unsigned)(nmain + nedge)), dim3(256), 0, s, X,
+                       K, Y, B, C, J, N, M, (int)nmain);
     } else {
-      hipLaunchKernelGGL((k_cic_fdp_fwd<JB, false>), dim3((unsigned)nmain), dim3(256), 0, s, X, K, Y, B, C, J, N, M,
-                         (int)nmain);
+      e = timed_launch("cic_fdp_fwd", k_cic_fdp_fwd<JB, false>, dim3((unsigned)nmain), dim3(256), 0, s, X, K, Y, B,
+                       C, J, N, M, (int)nmain);
     }
   });
-  const hipError_t e = hipGetLastError();
-  timing_after("cic_fdp_fwd", s);
   return e;
 }
 
@@ -1829,17 +1819,12 @@ hipError_t launch_cic_fdp_bwd(const float2 *gY, const float2 *K, float2 *gX, con
   const long long total = xbx * xby + kbx * kby + nedge;
   if (total == 0) return hipSuccess;
   if (total >= (1LL << 31)) return hipErrorInvalidValue;
-  timing_before("cic_fdp_bwd", s);
   const int kbx1 = (int)(kbx > 0 ? kbx : 1), kby1 = (int)(kby > 0 ? kby : 1), nk = (int)(kbx * kby);
   if (project && gX)
-    hipLaunchKernelGGL(k_cic_fdp_bwd<true>, dim3((unsigned)total), dim3(256), 0, s, gY, K, gX, X, gK, B, C, S / C, N,
-                       M, (int)xbx, (int)xby, kbx1, kby1, nk);
-  else
-    hipLaunchKernelGGL(k_cic_fdp_bwd<false>, dim3((unsigned)total), dim3(256), 0, s, gY, K, gX, X, gK, B, C, S / C, N,
-                       M, (int)xbx, (int)xby, kbx1, kby1, nk);
-  const hipError_t e = hipGetLastError();
-  timing_after("cic_fdp_bwd", s);
-  return e;
+    return timed_launch("cic_fdp_bwd", k_cic_fdp_bwd<true>, dim3((unsigned)total), dim3(256), 0, s, gY, K, gX, X, gK,
+                        B, C, S / C, N, M, (int)xbx, (int)xby, kbx1, kby1, nk);
+  return timed_launch("cic_fdp_bwd", k_cic_fdp_bwd<false>, dim3((unsigned)total), dim3(256), 0, s, gY, K, gX, X, gK, B,
+                      C, S / C, N, M, (int)xbx, (int)xby, kbx1, kby1, nk);
 }
 
 // Largest spatial kernel of the spatial-kernel CIC calls.
@@ -2249,10 +2234,7 @@ hipError_t launch_cic_kspec(int n_img, const float *w, float2 *K, int S, int n, 
     const long long blocks = (long long)S * ncb;
     if (blocks >= (1LL << 31)) return;
     const int rowb = (M + kKspecRows - 1) / kKspecRows;
-    timing_before("cic_kspec", s);
-    hipLaunchKernelGGL(k_cic_kspec<N>, dim3((unsigned)blocks, rowb), dim3(256), 0, s, w, K, n, M, ncb);
-    err = hipGetLastError();
-    timing_after("cic_kspec", s);
+    err = timed_launch("cic_kspec", k_cic_kspec<N>, dim3((unsigned)blocks, rowb), dim3(256), 0, s, w, K, n, M, ncb);
   });
   return err;
 }
@@ -2265,10 +2247,7 @@ hipError_t launch_cic_wgrad(int n_img, const float2 *gK, float *part, float *gw,
   dispatch_n(n_img, [&](auto nc) {
     constexpr int N = decltype(nc)::value;
     if (S > 65535) return;
-    timing_before("cic_wgrad", s);
-    hipLaunchKernelGGL(k_cic_wgrad_part<N>, dim3(RB, S), dim3(256), 0, s, gK, part, n, M, RB);
-    err = hipGetLastError();
-    timing_after("cic_wgrad", s);
+    err = timed_launch("cic_wgrad", k_cic_wgrad_part<N>, dim3(RB, S), dim3(256), 0, s, gK, part, n, M, RB);
   });
   if (err != hipSuccess) return err;
   const int total = S * n * n;

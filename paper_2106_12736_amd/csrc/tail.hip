@@ -796,11 +796,7 @@ static hipError_t tail_launch(const char *name, unsigned grid, size_t lds, hipSt
   hipError_t e = allow_lds<Kern>(lds);
   if (e != hipSuccess) return e;
   const auto kern = Kern;
-  timing_before(name, s);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(kTailThreads), lds, s, args...);
-  e = hipGetLastError();
-  timing_after(name, s);
-  return e;
+  return timed_launch(name, kern, dim3(grid), dim3(kTailThreads), lds, s, args...);
 }
 
 hipError_t launch_tail_fwd(int na, int ma, int mb, int ja, int jb, SpecLayout in, const float *x, float a_in,
@@ -887,11 +883,7 @@ static hipError_t small2d_launch(const char *name, unsigned grid, size_t lds, hi
   hipError_t e = allow_lds<Kern>(lds);
   if (e != hipSuccess) return e;
   const auto kern = Kern;
-  timing_before(name, s);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, s, args...);
-  e = hipGetLastError();
-  timing_after(name, s);
-  return e;
+  return timed_launch(name, kern, dim3(grid), dim3(256), lds, s, args...);
 }
 
 hipError_t launch_fft2_small(int n, bool inverse, const float *x, float2 *X, float *xo, const float2 *Xi,
