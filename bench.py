@@ -66,12 +66,13 @@ def fwd_col_launches(B, C, S, N, M, L):
             (f"col_cic_inv_{N}_{M}", C64 * (B * C * M * L + S * M * L + B * S * M * L))]
 
 
-def gk_launches(B, C, S, N, M, L, NF, ranges=1):
+def gk_launches(B, C, S, N, M, L, NF, ranges=1, zeros=True):
     """dK of one layer: one launch that reads the upstream and saved spectra and writes
-    all of gK (zeros where FDP drops), or, with the batch cut into R ranges, the range
+    all of gK (zeros where FDP drops; with zeros=False only the kept bins, the zeros
+    coming from the launch before), or, with the batch cut into R ranges, the range
     sums written by that launch and added in order by a second one."""
     if ranges <= 1:
-        return [(f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + S * N * NF))]
+        return [(f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + (S * N * NF if zeros else S * M * L)))]
     R = ranges
     return [(f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + R * S * M * L)),
             ("gk_reduce", C64 * (R * S * M * L + S * N * NF))]
@@ -154,6 +155,14 @@ def fused_bwd_launches(wl, input_grad=False, ranges=None, tail=-1):
     ranges = ranges or [1] * wl.layers
     out = []
     n = wl.layers
+
+    def merged(i):  # dK and dX of layer i in one launch
+        N = wl.sizes[i]
+        return (i > 0 or input_grad) and ranges[i] <= 1 and N <= 256
+
+    def zeros_early(i):  # layer i's gK zeros written by layer i + 1's boundary rows
+        return i + 1 < n and not (tail >= 0 and i + 1 >= tail) and not merged(i) and ranges[i] <= 1
+
     for i in reversed(range(n)):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
         if tail >= 0 and i >= tail:
@@ -164,18 +173,19 @@ def fused_bwd_launches(wl, input_grad=False, ranges=None, tail=-1):
             out.append((f"row_r2c_{M}", F32 * B * S * M * M + C64 * B * S * M * L))
         dx = i > 0 or input_grad
         gx_bytes = C64 * (B * S * M * L + S * M * L + B * C * N * L)
-        if dx and ranges[i] <= 1 and N <= 256:
+        if merged(i):
             # dK and dX columns in one launch (layers of at most 256 points): the bytes of both
             (_, gk_bytes), = gk_launches(B, C, S, N, M, L, NF, 1)
             out.append((f"col_bwd_dk_dx_{N}_{M}", gk_bytes + gx_bytes))
         else:
-            out += gk_launches(B, C, S, N, M, L, NF, ranges[i])
+            out += gk_launches(B, C, S, N, M, L, NF, ranges[i], zeros=not zeros_early(i))
             if dx:
                 out.append((f"col_bwd_gx_{N}_{M}", gx_bytes))
         if dx:
             if i > 0:
-                _, _, _, _, Mp, Lp, _ = layer_dims(wl, i - 1)
-                out.append((f"row_c2r_r2c_{N}", C64 * B * C * N * L + C64 * B * C * Mp * Lp))
+                _, _, Sp, Np, Mp, Lp, NFp = layer_dims(wl, i - 1)
+                zero_bytes = C64 * (Sp * Np * NFp - Sp * Mp * Lp) if zeros_early(i - 1) else 0
+                out.append((f"row_c2r_r2c_{N}", C64 * B * C * N * L + C64 * B * C * Mp * Lp + zero_bytes))
             else:
                 out.append((f"row_c2r_{N}", C64 * B * C * N * L + F32 * B * C * N * N))
     return out

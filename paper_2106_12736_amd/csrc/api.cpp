@@ -837,6 +837,19 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, cons
   const int B = p->B;
   auto *Tg = reinterpret_cast<float2 *>(ws);
   auto *V = Tg + p->ws_a;
+  // Layer i's dK and dX in one launch (k_col_bwd_dk_dx), else dK alone.
+  auto dk_merged = [&](int i) {
+    const StackLayer g = stack_layer(p, i);
+    return (i > 0 || gx) && fdc::gk_batch_ranges(g.N, g.M, B, g.S, (long long)p->ws_b) == 1 &&
+           fdc::col_bwd_dk_dx_supported(g.N, g.M);
+  };
+  // Layer i's gK zeros written by the boundary row launch of layer i + 1 (which runs
+  // just before layer i's dK): for a dK launch of one batch range below the tail.
+  auto zeros_early = [&](int i) {
+    if (i + 1 >= p->layers || (p->tail >= 0 && i + 1 >= p->tail)) return false;
+    const StackLayer g = stack_layer(p, i);
+    return !dk_merged(i) && fdc::gk_batch_ranges(g.N, g.M, B, g.S, (long long)p->ws_b) == 1;
+  };
   for (int i = p->layers - 1; i >= 0; --i) {
     if (p->tail >= 0 && i == p->tail + 1) {
       // the last two layers in one launch: their dK products per image go to V and are
@@ -879,8 +892,7 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, cons
         return st;
     }
     const bool need_dx = i > 0 || gx;
-    if (need_dx && fdc::gk_batch_ranges(g.N, g.M, B, g.S, (long long)p->ws_b) == 1 &&
-        fdc::col_bwd_dk_dx_supported(g.N, g.M)) {
+    if (dk_merged(i)) {
       // dK and dX columns side by side in one launch
       if (fdc_status st = check_hip(fdc::launch_col_bwd_dk_dx(g.N, g.M, Tg, reinterpret_cast<const float2 *>(saved[i]),
                                                               reinterpret_cast<const float2 *>(K[i]),
@@ -891,7 +903,7 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, cons
       // V is free until the dX columns below: dK's batch-range sums go there
       if (fdc_status st = check_hip(fdc::launch_col_bwd_gk(g.N, g.M, Tg, reinterpret_cast<const float2 *>(saved[i]),
                                                            reinterpret_cast<float2 *>(gK[i]), B, g.C, g.S, V,
-                                                           (long long)p->ws_b, s),
+                                                           (long long)p->ws_b, s, !zeros_early(i)),
                                     "stack backward dK"))
         return st;
       if (!need_dx) break;
@@ -904,9 +916,12 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, cons
       // this layer's adjoint inverse rows and the previous layer's upstream-gradient rows
       const StackLayer h = stack_layer(p, i - 1);
       const float hinv = 1.f / ((float)h.M * (float)h.M);
+      // with layer i - 1's gK zeros, when its dK launch leaves them to this one
+      const fdc::ZeroBins zb = zeros_early(i - 1) ? fdc::ZeroBins{reinterpret_cast<float2 *>(gK[i - 1]), h.S, h.N, h.M}
+                                                  : fdc::ZeroBins{nullptr, 0, 0, 0};
       if (fdc_status st = check_hip(fdc::launch_row_c2r_r2c(g.N, fdc::tiled_layout(V, cin, g.N, g.L), g.L, 1.f, 0.5f,
                                                             fdc::tiled_layout(Tg, cin, h.M, h.L), h.L, hinv, 2.f,
-                                                            cin, g.N, s),
+                                                            cin, g.N, s, zb),
                                     "stack backward boundary rows"))
         return st;
     } else {

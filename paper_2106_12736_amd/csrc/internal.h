@@ -109,6 +109,13 @@ inline hipError_t timed_launch(const char *name, Kern kern, dim3 grid, dim3 bloc
   return hipGetLastError();
 }
 
+// The bins of a kernel gradient gK [S][N][N/2+1] that an FDP N -> M drops (rows
+// M/2 <= k < N - M/2, and the columns l > M/2 of the other rows): p == NULL for none.
+struct ZeroBins {
+  float2 *p;
+  int S, N, M;
+};
+
 // Row transforms of real rows of length n (n in the supported set), processed in pairs.
 // rows_per_plane must be even.  Output/input bins beyond L are not written / read as zero;
 // the L stored bins are laid out as `spec` says.
@@ -122,9 +129,11 @@ hipError_t launch_row_c2r(int n, SpecLayout in, float *y, long long planes, int 
                           float beta, ImgView out_view, long long out_plane_stride, hipStream_t s);
 // Inverse then forward real row transforms of the same rows (a boundary between two
 // stacked layers): launch_row_c2r(in, Lin, a1, b1) followed by launch_row_r2c(out,
-// Lout, a2, b2) with the real rows kept in registers.
+// Lout, a2, b2) with the real rows kept in registers.  The same launch also writes the
+// zeros of `zeros` (a kernel gradient the next dK launch then leaves to it).
 hipError_t launch_row_c2r_r2c(int n, SpecLayout in, int Lin, float a1, float b1, SpecLayout out, int Lout, float a2,
-                              float b2, long long planes, int rows_per_plane, hipStream_t s);
+                              float b2, long long planes, int rows_per_plane, hipStream_t s,
+                              ZeroBins zeros = ZeroBins{nullptr, 0, 0, 0});
 
 // Column DFTs of length n over the first `L` columns of row-major [planes][n][ld] complex
 // data (in place allowed).
@@ -149,9 +158,11 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
                               int C, int S, hipStream_t s);
 // dK: with scratch `part` (part_elems complex values; may be NULL) the batch is cut
 // into gk_batch_ranges(...) ranges whose sums are added in order by a second kernel.
+// zeros = false: with one range the dropped bins of gK are left as they are (an earlier
+// launch of the same call wrote their zeros).
 int gk_batch_ranges(int n, int m, int B, int S, long long part_elems);
 hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, float2 *gK, int B, int C,
-                             int S, float2 *part, long long part_elems, hipStream_t s);
+                             int S, float2 *part, long long part_elems, hipStream_t s, bool zeros = true);
 hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, float2 *V, int B, int C, int S,
                              hipStream_t s);
 // gK [S][N][N/2+1] from BG partial sums part [BG][S][M][M/2+1] (plain layout): at the

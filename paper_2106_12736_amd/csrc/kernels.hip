@@ -313,6 +313,30 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
   }
 }
 
+// Zeros of z.p at the bins the FDP drops, in jobs of one wavefront: jobs [0, S * CA)
+// are 512-value chunks of the S contiguous dropped-row blocks ((N - M) (N/2+1) values
+// each, CA chunks per block), jobs [S * CA, S * CA + S * M) the dropped columns of one
+// kept row.  Wavefront w of nw takes jobs w, w + nw, ...; w is wave-uniform, so the job
+// arithmetic is scalar and each store instruction writes 64 consecutive values.
+__device__ __forceinline__ void zero_dropped_bins(const ZeroBins &z, unsigned w, unsigned nw, int lane) {
+  const int nf = z.N / 2 + 1, L = z.M / 2 + 1;
+  const unsigned ra = (unsigned)(z.N - z.M) * (unsigned)nf, ca = (ra + 511) / 512;
+  const unsigned ja = (unsigned)z.S * ca, jobs = ja + (unsigned)z.S * (unsigned)z.M;
+  const float2 zero = make_float2(0.f, 0.f);
+  for (unsigned j = w; j < jobs; j += nw) {
+    if (j < ja) {
+      const unsigned o = j / ca, c0 = (j - o * ca) * 512;
+      float2 *blk = z.p + ((long long)o * z.N + z.M / 2) * nf;
+      for (unsigned e = c0 + lane; e < c0 + 512 && e < ra; e += 64) blk[e] = zero;
+    } else {
+      const unsigned r = j - ja, o = r / (unsigned)z.M;
+      const int kr = (int)(r - o * (unsigned)z.M), k = kr < z.M / 2 ? kr : kr + (z.N - z.M);
+      float2 *row = z.p + ((long long)o * z.N + k) * nf;
+      for (int l = L + lane; l < nf; l += 64) row[l] = zero;
+    }
+  }
+}
+
 // Inverse real row transform followed by the forward real row transform of the same
 // rows, for a boundary between two layers of a stack: in (Lin bins per row, weights
 // a1 at l = 0 and N/2, a1 * b1 elsewhere, real-part semantics as k_row_c2r) ->
@@ -322,7 +346,8 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r(SpecLayout in, 
 template <int N, int SPW, int LIN>
 __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r_r2c(SpecLayout in, int Lin, float a1, float b1,
                                                                     SpecLayout out, int Lout, float a2, float b2,
-                                                                    long long npairs, int rows_per_plane) {
+                                                                    long long npairs, int rows_per_plane,
+                                                                    ZeroBins zeros) {
   using Cfg = RowCfg<N>;
   constexpr int TPS = Cfg::TPS, E = Cfg::E;
   static_assert(TPS <= 64, "a row sequence must fit in one wavefront");
@@ -346,25 +371,32 @@ __global__ __launch_bounds__(SPW *RowCfg<N>::TPS) void k_row_c2r_r2c(SpecLayout 
   lds_barrier<true>();
   row_to_lds<N>(v, lds, s, t);
   lds_barrier<true>();
-  if (!active) return;
-  const float a2s = LIN == 0 ? a2 : a2 * (a1 * b1);  // with the factor c2r_gather left out
-  float2 *oa = out.main + plane * out.ps + (long long)r0 * out.rs;
-  float2 *ob = oa + out.rs;
-  for (int k = t; k < Lout; k += TPS) {
-    const float2 zk = lds[lds_phys<kRowLds>(s * N + k)];
-    const float2 zn = lds[lds_phys<kRowLds>(s * N + (k == 0 ? 0 : N - k))];
-    const float wgt = 0.5f * bin_weight(k, N, a2s, b2);
-    const float2 A = make_float2((zk.x + zn.x) * wgt, (zk.y - zn.y) * wgt);
-    const float2 Bv = make_float2((zk.y + zn.y) * wgt, (zn.x - zk.x) * wgt);
-    if (k < Lout - 1) {
-      const unsigned o = bin_off32(out, k);
-      at32(oa, o) = A;
-      at32(ob, o) = Bv;
-    } else {
-      float2 *so = out.side + plane * out.sps + (long long)r0 * out.srs;
-      so[0] = A;
-      so[out.srs] = Bv;
+  if (active) {
+    const float a2s = LIN == 0 ? a2 : a2 * (a1 * b1);  // with the factor c2r_gather left out
+    float2 *oa = out.main + plane * out.ps + (long long)r0 * out.rs;
+    float2 *ob = oa + out.rs;
+    for (int k = t; k < Lout; k += TPS) {
+      const float2 zk = lds[lds_phys<kRowLds>(s * N + k)];
+      const float2 zn = lds[lds_phys<kRowLds>(s * N + (k == 0 ? 0 : N - k))];
+      const float wgt = 0.5f * bin_weight(k, N, a2s, b2);
+      const float2 A = make_float2((zk.x + zn.x) * wgt, (zk.y - zn.y) * wgt);
+      const float2 Bv = make_float2((zk.y + zn.y) * wgt, (zn.x - zk.x) * wgt);
+      if (k < Lout - 1) {
+        const unsigned o = bin_off32(out, k);
+        at32(oa, o) = A;
+        at32(ob, o) = Bv;
+      } else {
+        float2 *so = out.side + plane * out.sps + (long long)r0 * out.srs;
+        so[0] = A;
+        so[out.srs] = Bv;
+      }
     }
+  }
+  // the zeros of a kernel gradient, in wavefront jobs (the rows above are this launch's own work)
+  if (zeros.p != nullptr) {
+    const unsigned wpb = (SPW * RowCfg<N>::TPS) / 64;
+    zero_dropped_bins(zeros, blockIdx.x * wpb + __builtin_amdgcn_readfirstlane(threadIdx.x / 64), gridDim.x * wpb,
+                      threadIdx.x % 64);
   }
 }
 
@@ -719,7 +751,8 @@ constexpr int gk_bp() {
 // are added in group order, so the result does not depend on scheduling.
 // BG = 1: writes all of gK [S][N][N/2+1], the kept bins and exact zeros at the
 // rows and columns FDP drops (rows of the tile's own columns; the columns l >= L
-// of every row are shared out over the whole grid).
+// of every row are shared out over the whole grid); with zeros = false the kept bins
+// only (the zeros come from an earlier launch).
 // BG > 1: writes range r's sums at the kept bins to part [BG][S][M][M/2+1];
 // k_gk_reduce then adds the ranges in order and writes gK.
 // One workgroup of the dK launch: workgroup `lin` (after the XCD remap) of `nwg`,
@@ -728,7 +761,7 @@ template <int M, int CT, int BP>
 __device__ __forceinline__ void col_bwd_gk_tile(int lin, int nwg, int tid, const float2 *tw, int tws, float2 *lds,
                                                 const float2 *__restrict__ Tg, const float2 *__restrict__ Xh,
                                                 float2 *__restrict__ gK, float2 *__restrict__ part, int B, int C,
-                                                int J, int N, int S, int BG) {
+                                                int J, int N, int S, int BG, bool zeros) {
   using CM = ColCfg<M>;
   constexpr int L = M / 2 + 1, TPS = CM::TPS, E = CM::E;
   constexpr int NT = CT * TPS * BP;
@@ -742,7 +775,7 @@ __device__ __forceinline__ void col_bwd_gk_tile(int lin, int nwg, int tid, const
   const int nf = N / 2 + 1;
 
   // zeros of the columns l >= L: groups of LW lanes take the S * N rows in turn
-  if (BG == 1) {
+  if (BG == 1 && zeros) {
     static_assert((NT & (NT - 1)) == 0, "NT must be a power of two");
     constexpr int LW = NT < 64 ? NT : 64;
     const int lane = tid % LW;
@@ -809,7 +842,8 @@ __device__ __forceinline__ void col_bwd_gk_tile(int lin, int nwg, int tid, const
     kcol[(long long)krow * nf] = acc[m];
   }
   // dropped rows [M/2, N - M/2) of this column; N - M is a multiple of TPS
-  for (int k = M / 2 + t; k < N - M / 2; k += TPS) kcol[(long long)k * nf] = make_float2(0.f, 0.f);
+  if (zeros)
+    for (int k = M / 2 + t; k < N - M / 2; k += TPS) kcol[(long long)k * nf] = make_float2(0.f, 0.f);
 }
 
 template <int M, int CT, int BP>
@@ -817,11 +851,11 @@ __global__ __launch_bounds__(CT *ColCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
                                                                       const float2 *__restrict__ Xh,
                                                                       float2 *__restrict__ gK,
                                                                       float2 *__restrict__ part, int B, int C,
-                                                                      int J, int N, int S, int BG) {
+                                                                      int J, int N, int S, int BG, int zeros) {
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<M>();
   stage_twiddles<M>(tw, threadIdx.x, CT * ColCfg<M>::TPS * BP);
   col_bwd_gk_tile<M, CT, BP>(xcd_remap(blockIdx.x, gridDim.x), gridDim.x, threadIdx.x, tw, 1, lds, Tg, Xh, gK, part,
-                             B, C, J, N, S, BG);
+                             B, C, J, N, S, BG, zeros != 0);
 }
 
 // gK [S][N][N/2+1] from BG partial sums part [BG][S][M][M/2+1] (plain layout), for
@@ -995,7 +1029,7 @@ __global__ __launch_bounds__(CTK *ColCfg<M>::TPS *BP) void k_col_bwd_dk_dx(
   if (bid < nk) {
     if (bid >= nk_used) return;  // padding: no barrier follows
     col_bwd_gk_tile<M, CTK, BP>(xcd_remap(bid, nk_used), nk_used, threadIdx.x, tw, N / M, lds, Tg, Xh, gK,
-                                nullptr, B, C, J, N, S, 1);
+                                nullptr, B, C, J, N, S, 1, true);
     return;
   }
   const int xb = bid - nk, nxb = gridDim.x - nk;
@@ -1210,7 +1244,7 @@ hipError_t launch_row_c2r(int n, SpecLayout in, float *y, long long planes, int 
 }
 
 hipError_t launch_row_c2r_r2c(int n, SpecLayout in, int Lin, float a1, float b1, SpecLayout out, int Lout, float a2,
-                              float b2, long long planes, int rows_per_plane, hipStream_t s) {
+                              float b2, long long planes, int rows_per_plane, hipStream_t s, ZeroBins zeros) {
   hipError_t err = hipErrorInvalidValue;
   if (planes * rows_per_plane >= (1LL << 31)) return err;
   dispatch_n(n, [&](auto nc) {
@@ -1222,7 +1256,7 @@ hipError_t launch_row_c2r_r2c(int n, SpecLayout in, int Lin, float a1, float b1,
     static const std::string nm = "row_c2r_r2c_" + std::to_string(N);
     auto go = [&](auto kern) {
       err = launch(nm.c_str(), kern, grid, SPW * RowCfg<N>::TPS, lds, s, in, Lin, a1, b1, out, Lout, a2, b2, npairs,
-                   rows_per_plane);
+                   rows_per_plane, zeros);
     };
     switch (c2r_lin_mode<N>(Lin, b1)) {
       case 1:
@@ -1378,7 +1412,7 @@ int gk_batch_ranges(int n, int m, int B, int S, long long part_elems) {
 }
 
 hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, float2 *gK, int B, int C, int S,
-                             float2 *part, long long part_elems, hipStream_t s) {
+                             float2 *part, long long part_elems, hipStream_t s, bool zeros) {
   hipError_t err = hipErrorInvalidValue;
   if (!cic_pair_supported(n, m)) return err;
   const int BG = part ? gk_batch_ranges(n, m, B, S, part_elems) : 1;
@@ -1391,7 +1425,7 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
     if (tiles == 0) return;
     static const std::string nm = "col_bwd_gk_" + std::to_string(M);
     err = launch(nm.c_str(), k_col_bwd_gk<M, CT, BP>, tiles * (unsigned)BG, CT * ColCfg<M>::TPS * BP, lds, s, Tg,
-                 Xh, gK, part, B, C, S / C, n, S, BG);
+                 Xh, gK, part, B, C, S / C, n, S, BG, zeros ? 1 : 0);
     if (err != hipSuccess || BG == 1) return;
     err = gk_reduce(GkSum{part, gK, BG, S, M, n}, nullptr, s);
   });
