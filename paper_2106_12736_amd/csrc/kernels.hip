@@ -418,15 +418,16 @@ constexpr int col_ct() {
   return ColCfg<N>::TPS >= 64 ? 8 : (ColCfg<N>::TPS >= 32 ? 16 : 32);
 }
 // Narrower tiles (twice the workgroups) where measurement favoured them: the dX
-// kernel (three transforms per tile), the forward crop at 128 and 256 points and the
-// CIC inverse at 64 points.
+// kernel (three transforms per tile), the forward crop at 128, 256 and 1024 points (at
+// 1024 points 8 images of one channel give 257 workgroups of eight waves; with 4-column
+// tiles 10.3 -> 9.0 us) and the CIC inverse at 64 points.
 template <int N>
 constexpr int col_ct_gx() {
   return col_ct<N>() / 2;
 }
 template <int N>
 constexpr int col_ct_crop() {
-  return (N == 128 || N == 256) ? col_ct<N>() / 2 : col_ct<N>();
+  return (N == 128 || N == 256 || N == 1024) ? col_ct<N>() / 2 : col_ct<N>();
 }
 template <int M>
 constexpr int col_ct_cic() {
@@ -737,11 +738,22 @@ template <int M>
 constexpr int gk_ct() {
   return M == 512 ? 4 : kGkCT;
 }
-template <int M>
-constexpr int gk_bp() {
-  constexpr int bp = (M == 512 ? 256 : 512) / (gk_ct<M>() * ColCfg<M>::TPS);
+// batch groups per workgroup for CT-column tiles
+template <int M, int CT>
+constexpr int gk_bp_ct() {
+  constexpr int bp = (M == 512 ? 256 : 512) / (CT * ColCfg<M>::TPS);
   return bp < 1 ? 1 : (bp > 8 ? 8 : bp);
 }
+template <int M>
+constexpr int gk_bp() {
+  return gk_bp_ct<M, gk_ct<M>()>();
+}
+// The standalone dK launch at 128 points takes 4-column tiles (eight batch groups) when
+// the grid of 8-column tiles, with its batch ranges, would be below this many
+// workgroups: at 256^2, 16 images and 8 output channels give 130, and the launch ran
+// 9.1 -> 7.0 us with 4 columns.  On the larger grids (32 images at 512^2) and in the
+// merged dK/dX launch the 8-column tiles measured faster.
+constexpr long long kGkNarrowWgs = 256;
 
 // Backward, dL/dK: for the kernel-gradient columns (o, l), column DFT (M) of each
 // upstream-gradient column Tg[b][o] and dK += G conj(Xh[b][o/J]).
@@ -1389,23 +1401,42 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
   return err;
 }
 
+// Batch ranges of the dK launch at M points with CT-column tiles.
+template <int M, int CT>
+static int gk_ranges_ct(int B, int S, long long part_elems) {
+  constexpr int L = M / 2 + 1, BP = gk_bp_ct<M, CT>();
+  const long long tiles = col_tile_count(S, L, CT);
+  // enough workgroups to fill the chip (kGkTargetWgs), at least BP batch entries per
+  // range, and range sums (written and read once more) of at most a quarter of Tg
+  // (at 8 images, two ranges measured slower than one)
+  long long want = (kGkTargetWgs + tiles - 1) / tiles;
+  want = std::min<long long>(want, std::max(1, B / 8));
+  want = std::min<long long>(want, std::max(1, B / BP));
+  const long long per = (long long)S * M * L;
+  want = std::min<long long>(want, per > 0 ? part_elems / per : 1);
+  if (tiles * want >= (1LL << 31)) want = 1;
+  return (int)std::max<long long>(1, want);
+}
+
+// Whether the standalone dK launch at M points takes 4-column tiles (kGkNarrowWgs).
+template <int M>
+static bool gk_narrow(int B, int S, long long part_elems) {
+  if constexpr (M != 128) {
+    return false;
+  } else {
+    constexpr int L = M / 2 + 1, CT = col_ct_for(gk_ct<M>(), L);
+    return col_tile_count(S, L, CT) * gk_ranges_ct<M, CT>(B, S, part_elems) < kGkNarrowWgs;
+  }
+}
+
 int gk_batch_ranges(int n, int m, int B, int S, long long part_elems) {
   int bg = 1;
   dispatch_n(m, [&](auto mc) {
     constexpr int M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
-    constexpr int CT = col_ct_for(gk_ct<M>(), L), BP = gk_bp<M>();
-    const long long tiles = col_tile_count(S, L, CT);
-    // enough workgroups to fill the chip (kGkTargetWgs), at least BP batch entries per
-    // range, and range sums (written and read once more) of at most a quarter of Tg
-    // (at 8 images, two ranges measured slower than one)
-    long long want = (kGkTargetWgs + tiles - 1) / tiles;
-    want = std::min<long long>(want, std::max(1, B / 8));
-    want = std::min<long long>(want, std::max(1, B / BP));
-    const long long per = (long long)S * M * L;
-    want = std::min<long long>(want, per > 0 ? part_elems / per : 1);
-    if (tiles * want >= (1LL << 31)) want = 1;
-    bg = (int)std::max<long long>(1, want);
+    constexpr int CT = col_ct_for(gk_ct<M>(), L), CT4 = col_ct_for(4, L);
+    bg = gk_narrow<M>(B, S, part_elems) ? gk_ranges_ct<M, CT4>(B, S, part_elems)
+                                        : gk_ranges_ct<M, CT>(B, S, part_elems);
   });
   (void)n;
   return bg;
@@ -1415,17 +1446,24 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
                              float2 *part, long long part_elems, hipStream_t s, bool zeros) {
   hipError_t err = hipErrorInvalidValue;
   if (!cic_pair_supported(n, m)) return err;
+  const long long pe = part ? part_elems : 0;
   const int BG = part ? gk_batch_ranges(n, m, B, S, part_elems) : 1;
   dispatch_n(m, [&](auto mc) {
     constexpr int M = decltype(mc)::value;
     constexpr int L = M / 2 + 1;
-    constexpr int CT = col_ct_for(gk_ct<M>(), L), BP = gk_bp<M>();
-    const size_t lds = (twiddle_lds_elems<M>() + lds_size<kColLds>(BP * M * CT)) * sizeof(float2);
-    const unsigned tiles = col_grid(S, L, CT);
-    if (tiles == 0) return;
     static const std::string nm = "col_bwd_gk_" + std::to_string(M);
-    err = launch(nm.c_str(), k_col_bwd_gk<M, CT, BP>, tiles * (unsigned)BG, CT * ColCfg<M>::TPS * BP, lds, s, Tg,
-                 Xh, gK, part, B, C, S / C, n, S, BG, zeros ? 1 : 0);
+    auto go = [&](auto ctc) {
+      constexpr int CT = decltype(ctc)::value, BP = gk_bp_ct<M, CT>();
+      const size_t lds = (twiddle_lds_elems<M>() + lds_size<kColLds>(BP * M * CT)) * sizeof(float2);
+      const unsigned tiles = col_grid(S, L, CT);
+      if (tiles == 0) return;
+      err = launch(nm.c_str(), k_col_bwd_gk<M, CT, BP>, tiles * (unsigned)BG, CT * ColCfg<M>::TPS * BP, lds, s, Tg,
+                   Xh, gK, part, B, C, S / C, n, S, BG, zeros ? 1 : 0);
+    };
+    if (gk_narrow<M>(B, S, pe))
+      go(std::integral_constant<int, col_ct_for(4, L)>{});
+    else
+      go(std::integral_constant<int, col_ct_for(gk_ct<M>(), L)>{});
     if (err != hipSuccess || BG == 1) return;
     err = gk_reduce(GkSum{part, gK, BG, S, M, n}, nullptr, s);
   });
