@@ -204,13 +204,14 @@ def fft2_launches(n, planes, inverse):
 
 
 def pooled_rfft2_launches(n, m, planes):
-    """(kernel name, algorithmic bytes) of fdc_rfft2_pooled: n x n planes to the bins an
-    FDP to m x m keeps (m/2+1 columns of every row, then m rows of those columns)."""
-    if n in (16, 32, 64) or m == n:
+    """(kernel name, algorithmic bytes) of fdc_rfft2_pooled_ws: n x n planes to the bins an
+    FDP to m x m keeps (m/2+1 columns of every row into the workspace, then m rows of
+    those columns)."""
+    if n in (16, 32, 64):
         return fft2_launches(n, planes, inverse=False)
     L = m // 2 + 1
     real = F32 * planes * n * n
-    return [(f"row_r2c_{n}", real + C64 * planes * n * L), (f"col_fft_fwd_{n}", C64 * planes * (n + m) * L)]
+    return [(f"row_r2c_{n}", real + C64 * planes * n * L), (f"col_fft_keep_{n}", C64 * planes * (n + m) * L)]
 
 
 def chain_step_launches(wl, input_grad=False, hermitian=False):

@@ -123,6 +123,13 @@ fdc_status fdc_irfft2_backward(const fdc_fft_plan *plan, const float *gx, fdc_c6
  * those columns and stores the mh kept rows.  No workspace. */
 fdc_status fdc_rfft2_pooled(const fdc_fft_plan *plan, const float *x, fdc_c64 *X, int mh,
                             int mw, hipStream_t stream);
+/* The same bins, with a workspace of count * h * (mw/2 + 1) complex values (at least
+ * that many bytes times 8; unused for planes of 16^2 to 64^2): the row pass writes the
+ * mw/2 + 1 bins in runs of 8 per row into the workspace, so that the column pass reads
+ * whole runs instead of one value per row of X.  Same results bit for bit as
+ * fdc_rfft2_pooled.  FDC_EWORKSPACE when ws is NULL or smaller. */
+fdc_status fdc_rfft2_pooled_ws(const fdc_fft_plan *plan, const float *x, fdc_c64 *X, int mh,
+                               int mw, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Channel Independent Convolution on spectra (Eq. 5, Algorithm 1)          */

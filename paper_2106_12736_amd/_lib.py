@@ -37,6 +37,7 @@ _SIGS = {
     "fdc_rfft2_backward": [_P, _P, _P, _P, _SZ, _P],
     "fdc_irfft2_backward": [_P, _P, _P, _P, _SZ, _P],
     "fdc_rfft2_pooled": [_P, _P, _P, _I, _I, _P],
+    "fdc_rfft2_pooled_ws": [_P, _P, _P, _I, _I, _P, _SZ, _P],
     "fdc_cic_forward": [_P, _P, _P, _I, _I, _I, _I, _I, _P],
     "fdc_cic_backward": [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P],
     "fdc_cic_fdp_forward": [_P, _P, _P, _I, _I, _I, _I, _I, _P],

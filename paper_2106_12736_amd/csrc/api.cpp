@@ -242,6 +242,29 @@ fdc_status fdc_rfft2_pooled(const fdc_fft_plan *p, const float *x, fdc_c64 *X, i
                    "rfft2_pooled columns");
 }
 
+fdc_status fdc_rfft2_pooled_ws(const fdc_fft_plan *p, const float *x, fdc_c64 *X, int mh, int mw, void *ws,
+                               size_t ws_bytes, hipStream_t s) {
+  if (fdc_status st = check_fft_plan(p)) return st;
+  if (!x || !X) return fail(FDC_EINVAL, "NULL tensor");
+  const int h = p->h, w = p->w, wf = w / 2 + 1;
+  if (mh < 2 || mw < 2 || mh > h || mw > w || (mh & 1) || (mw & 1))
+    return fail(FDC_EINVAL, "pooled size %d x %d must be even, >= 2 and within %d x %d", mh, mw, h, w);
+  auto *out = reinterpret_cast<float2 *>(X);
+  if (fdc::fft2_small_supported(h, w))  // one launch forms every bin, no workspace
+    return check_hip(fdc::launch_fft2_small(h, false, x, out, nullptr, nullptr, p->count, 1.f, 1.f, s),
+                     "rfft2_pooled");
+  const int L = mw / 2 + 1;
+  if (fdc_status st = check_ws(ws, ws_bytes, (size_t)p->count * h * L * sizeof(fdc_c64))) return st;
+  // rows into the tiled layout in the workspace (whole runs of 8 bins per row), then the
+  // column pass reads those tiles and stores the kept rows into X
+  const fdc::SpecLayout t = fdc::tiled_layout(static_cast<const float2 *>(ws), p->count, h, L);
+  ImgView id{0, 0, h, w};
+  if (fdc_status st = check_hip(fdc::launch_row_r2c(w, x, t, p->count, h, id, (long long)h * w, L, 1.f, 1.f, s),
+                                "rfft2_pooled rows"))
+    return st;
+  return check_hip(fdc::launch_col_fft_keep(h, t, out, p->count, L, wf, mh, s), "rfft2_pooled columns");
+}
+
 static fdc_status inverse_like(const fdc_fft_plan *p, const fdc_c64 *X, float *x, void *ws, size_t ws_bytes,
                                hipStream_t s, float alpha, float beta, const char *what) {
   if (fdc_status st = check_fft_plan(p)) return st;

@@ -143,6 +143,11 @@ hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long lo
 // Column DFTs of `planes` split-layout n x (n/2+1) half spectra with the strides of
 // `in` and `out` (in place allowed).
 hipError_t launch_col_fft_split(int n, int dir, SpecLayout in, SpecLayout out, long long planes, hipStream_t s);
+// Forward column DFTs of length n over the L columns of `planes` row spectra in the
+// layout `in` (the tiled layout of a row pass), storing the rows an FDP to `keep` rows
+// keeps into the row-major out [planes][n][ld] at their own row indices.
+hipError_t launch_col_fft_keep(int n, SpecLayout in, float2 *out, long long planes, int L, int ld, int keep,
+                               hipStream_t s);
 
 // Fused CIC + FDP column kernels (square n x n images pooled to m x m; L = m/2 + 1).
 // T, Xh, U, Tg and V are split-layout spectra (SpecLayout) with L bins per row.

@@ -569,6 +569,33 @@ __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fft_split(SpecLayout
   for (int m = 0; m < E; ++m) oc.p[(t + TPS * m) * oc.stride] = v[m];
 }
 
+// Forward column DFT (N) of the L columns of row spectra in the layout `in`; the rows
+// an FDP to `keep` rows keeps go to the row-major out (row stride ld) at their own rows.
+template <int N, int CT>
+__global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_fft_keep(SpecLayout in, float2 *out, int L, int ld,
+                                                                    int planes, long long out_plane_stride, int keep) {
+  using Cfg = ColCfg<N>;
+  constexpr int TPS = Cfg::TPS, E = Cfg::E;
+  float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
+  TwiddleStage<N, CT * TPS> tws;
+  tws.fetch(threadIdx.x);
+  const int s = threadIdx.x % CT, t = threadIdx.x / CT;
+  const ColRef c = column_ref<CT>(xcd_remap(blockIdx.x, gridDim.x), s, L, planes);
+  const ColPtr64 ic = layout_col(in, L - 1, c.plane, c.l);
+  float2 v[E];
+#pragma unroll
+  for (int m = 0; m < E; ++m) v[m] = ic.p[(t + TPS * m) * ic.stride];  // lanes past the end read a valid column
+  tws.commit(tw, threadIdx.x);
+  fft_seq<N, -1, true, false, kLdsPlain, ColCfg<N>>(v, t, lds, s, CT, tw, 1);
+  if (!c.ok) return;
+  float2 *op = out + c.plane * out_plane_stride + c.l;
+#pragma unroll
+  for (int m = 0; m < E; ++m) {
+    const int k = t + TPS * m;
+    if (k < keep / 2 || k >= N - keep / 2) op[(long long)k * ld] = v[m];
+  }
+}
+
 // Forward, first half: column DFT (N) of the pruned row spectra, keep the M rows
 // FDP keeps.  T [planes][N rows] -> Xh [planes][M rows], both split layout with
 // L = M/2 + 1 bins per row (Xh is the pooled input spectrum the backward reads).
@@ -1307,6 +1334,22 @@ hipError_t launch_col_fft(int n, int dir, const float2 *in, float2 *out, long lo
     else
       err = launch(ni.c_str(), k_col_fft<N, CT, +1>, grid, CT * ColCfg<N>::TPS, lds, s, in, out, L, ld, (int)planes,
                    in_plane_stride, out_plane_stride, keep > 0 ? keep : N);
+  });
+  return err;
+}
+
+hipError_t launch_col_fft_keep(int n, SpecLayout in, float2 *out, long long planes, int L, int ld, int keep,
+                               hipStream_t s) {
+  hipError_t err = hipErrorInvalidValue;
+  dispatch_n(n, [&](auto nc) {
+    constexpr int N = decltype(nc)::value;
+    constexpr int CT = col_ct_crop<N>();
+    const size_t lds = (twiddle_lds_elems<N>() + lds_size<kColLds>(N * CT)) * sizeof(float2);
+    const unsigned grid = col_grid(planes, L, CT);
+    if (grid == 0) return;
+    static const std::string nm = "col_fft_keep_" + std::to_string(N);
+    err = launch(nm.c_str(), k_col_fft_keep<N, CT>, grid, CT * ColCfg<N>::TPS, lds, s, in, out, L, ld, (int)planes,
+                 (long long)N * ld, keep);
   });
   return err;
 }

@@ -75,14 +75,19 @@ class FftPlan:
         out = torch.empty(self._spec_shape(tuple(x.shape[:-2])), dtype=torch.complex64, device=x.device)
         return self._run("fdc_rfft2", x, out, None)
 
-    def rfft2_pooled(self, x, mh, mw, out=None):
+    def rfft2_pooled(self, x, mh, mw, out=None, ws=None):
         """fdc_rfft2_pooled into `out` (a new tensor if None): the bins an FDP to
-        mh x mw keeps; the others are undefined."""
+        mh x mw keeps; the others are undefined.  With a workspace `ws` (a uint8
+        tensor of at least count * h * (mw/2 + 1) * 8 bytes), fdc_rfft2_pooled_ws."""
         _check(x, torch.float32, name="x")
         if out is None:
             out = torch.empty(self._spec_shape(tuple(x.shape[:-2])), dtype=torch.complex64, device=x.device)
         _check(out, torch.complex64, self._spec_shape(tuple(x.shape[:-2])), "out")
-        call("fdc_rfft2_pooled", self._p, _ptr(x), _ptr(out), mh, mw, _stream())
+        if ws is None:
+            call("fdc_rfft2_pooled", self._p, _ptr(x), _ptr(out), mh, mw, _stream())
+        else:
+            call("fdc_rfft2_pooled_ws", self._p, _ptr(x), _ptr(out), mh, mw, _ptr(ws), ws.numel() * ws.element_size(),
+                 _stream())
         return out
 
     def irfft2(self, X):
@@ -564,8 +569,8 @@ class CicChain:
     input, every FDC (CIC) + FDP layer on spectra (fdc_cic_fdp_*), one irfft2 of the
     last spectrum.  All buffers are preallocated, so a step allocates nothing.
 
-    The input transform forms only the bins the first FDP keeps (fdc_rfft2_pooled): the
-    first layer reads no others, forward or backward.
+    The input transform forms only the bins the first FDP keeps (fdc_rfft2_pooled_ws, in
+    the chain's transform workspace): the first layer reads no others, forward or backward.
 
     With hermitian=True, Pi_H follows every layer but the last (the projected form of
     fdc_cic_fdp_forward), and its adjoint (itself) precedes their backward (the projected
@@ -596,7 +601,8 @@ class CicChain:
         # the first FDP keeps only some bins of the input spectrum, and the first layer
         # (forward and backward) reads no others
         m = self.sizes[1]
-        call("fdc_rfft2_pooled", self.plan_in._p, _ptr(x), _ptr(self.specs[0]), m, m, s)
+        call("fdc_rfft2_pooled_ws", self.plan_in._p, _ptr(x), _ptr(self.specs[0]), m, m, _ptr(self.ws),
+             self.ws.numel() * self.ws.element_size(), s)
         B = self.batch
         for i, K in enumerate(kernels):
             _check(K, torch.complex64, (self.channels[i + 1], self.sizes[i], self.sizes[i] // 2 + 1), f"K[{i}]")

@@ -64,7 +64,17 @@ def test_fft_calls_reject_bad_arguments_before_launch():
         assert _lib.status("fdc_rfft2_pooled", p, dummy, dummy, mh, mw, None) == FDC_EINVAL, (mh, mw)
     assert _lib.status("fdc_rfft2_pooled", p, None, dummy, 16, 16, None) == FDC_EINVAL
     assert _lib.status("fdc_rfft2_pooled", None, dummy, dummy, 16, 16, None) == FDC_EINVAL
+    for mh, mw in ((0, 16), (16, 0), (15, 16), (16, 17), (66, 16), (16, 66), (-2, 16)):
+        assert _lib.status("fdc_rfft2_pooled_ws", p, dummy, dummy, mh, mw, dummy, 1 << 20, None) == FDC_EINVAL
+    assert _lib.status("fdc_rfft2_pooled_ws", p, None, dummy, 16, 16, dummy, 1 << 20, None) == FDC_EINVAL
     _lib.status("fdc_fft_plan_destroy", p)
+    # above the one-launch sizes the pooled transform needs count * h * (mw/2 + 1) complex values
+    st, q = _fft_plan(2, 128, 128)
+    assert st == FDC_OK
+    need = 2 * 128 * 33 * 8
+    assert _lib.status("fdc_rfft2_pooled_ws", q, dummy, dummy, 64, 64, None, need, None) == FDC_EWORKSPACE
+    assert _lib.status("fdc_rfft2_pooled_ws", q, dummy, dummy, 64, 64, dummy, need - 1, None) == FDC_EWORKSPACE
+    _lib.status("fdc_fft_plan_destroy", q)
 
 
 @pytest.mark.parametrize("args,expect", [

@@ -91,6 +91,11 @@ def test_rfft2_pooled(count, h, w, mh, mw):
     cols = np.arange(mw // 2 + 1)
     # the kept bins only: the others are undefined (left as they were, or row-pass values)
     assert_parity(got[:, rows][:, :, cols], ref[:, rows][:, :, cols], "kept bins")
+    # with a workspace (rows in runs of 8 bins there, tiled column reads): the same bits
+    ws = torch.empty(count * h * (mw // 2 + 1) * 8, dtype=torch.uint8, device="cuda")
+    out2 = torch.full((count, h, w // 2 + 1), complex(nan, nan), dtype=torch.complex64, device="cuda")
+    got2 = to_np(plan.rfft2_pooled(_gpu(x), mh, mw, out=out2, ws=ws))
+    assert np.array_equal(got2[:, rows][:, :, cols], got[:, rows][:, :, cols])
     torch.cuda.synchronize()
 
 

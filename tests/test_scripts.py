@@ -33,18 +33,22 @@ def test_sweep_help_and_table():
 
 @pytest.mark.parametrize("n,m", [(1024, 512), (512, 256), (64, 32), (256, 256)])
 def test_pooled_rfft2_work_model(n, m):
-    # fdc_rfft2_pooled: the row pass writes m/2+1 bins of every row, the column pass
-    # reads those columns and writes the m kept rows; no pooling = the full transform
+    # fdc_rfft2_pooled_ws: the row pass writes m/2+1 bins of every row (to the
+    # workspace), the column pass reads those columns and writes the m kept rows; with no
+    # pooling the bytes of the full transform; small planes in one launch
     planes = 8
     got = bench.pooled_rfft2_launches(n, m, planes)
     full = bench.fft2_launches(n, planes, inverse=False)
-    assert [k for k, _ in got] == [k for k, _ in full]
-    if m == n or n <= 64:
+    if n <= 64:
         assert got == full
+        return
+    assert [k for k, _ in got] == [f"row_r2c_{n}", f"col_fft_keep_{n}"]
+    L = m // 2 + 1
+    assert got[0][1] == 4 * planes * n * n + 8 * planes * n * L
+    assert got[1][1] == 8 * planes * (n + m) * L
+    if m == n:
+        assert [b for _, b in got] == [b for _, b in full]
     else:
-        L = m // 2 + 1
-        assert got[0][1] == 4 * planes * n * n + 8 * planes * n * L
-        assert got[1][1] == 8 * planes * (n + m) * L
         assert sum(b for _, b in got) < sum(b for _, b in full)
 
 
