@@ -217,8 +217,8 @@ def pooled_rfft2_launches(n, m, planes):
 def chain_step_launches(wl, input_grad=False, hermitian=False):
     """(kernel name, algorithmic bytes) of every launch of one step of the FDCNN chain
     (one rfft2, every FDC + FDP layer on spectra, one irfft2, and the backward); with
-    hermitian=True the layers' launches also apply Pi_H, with the same launches and
-    bytes."""
+    hermitian=True the layers' launches also apply Pi_H, with the same launches (the
+    backward also writing columns 0 and N/2 of dX over every row)."""
     out = []
     n = wl.layers
     B = wl.batch
@@ -235,12 +235,16 @@ def chain_step_launches(wl, input_grad=False, hermitian=False):
     out += fft2_launches(ML, B * CL, inverse=False)  # the irfft2 adjoint has the forward's launches
     for i in reversed(range(n)):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
-        # dX and dK in one launch (with hermitian=True and i > 0, Pi_H of dX in it too):
-        # gY, and X at the kept bins, read; all of gK written (zeros at dropped bins); with
-        # dX also K at the kept bins read and all of gX written
-        nb = C64 * (B * S * M * L + B * C * M * L + S * N * NF)
+        # dX and dK in one launch (fdc_cic_fdp_backward_kept; with hermitian=True and
+        # i > 0, Pi_H of dX in it too): gY, and X at the kept bins, read; gK written at the
+        # kept bins (the chain's buffers hold zeros at the others); with dX also K at the
+        # kept bins read and gX written at the kept bins (projected: also columns 0 and
+        # N/2 of the other rows)
+        nb = C64 * (B * S * M * L + B * C * M * L + S * M * L)
         if i > 0 or input_grad:
-            nb += C64 * (S * M * L + B * C * N * NF)
+            nb += C64 * (S * M * L + B * C * M * L)
+            if hermitian and i > 0:
+                nb += C64 * B * C * ((N - M) + (N if M < N else 0))
         out.append(("cic_fdp_bwd", nb))
     if input_grad:
         out += fft2_launches(N0, B * C0, inverse=True)

@@ -178,6 +178,18 @@ fdc_status fdc_cic_fdp_forward_projected(const fdc_c64 *X, const fdc_c64 *K, fdc
                                          int N, int M, hipStream_t stream);
 fdc_status fdc_cic_fdp_backward_projected(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX,
                                           fdc_c64 *gK, int B, int C, int S, int N, int M, hipStream_t stream);
+/* fdc_cic_fdp_backward and fdc_cic_fdp_backward_projected writing only the bins the
+ * FDP keeps (rows k < M/2 and k >= N - M/2, columns l <= M/2) of gX and gK, and, in the
+ * projected form, columns 0 and N/2 of gX over every row (Pi_H gives dropped row M/2 half
+ * of row N - M/2).  The other bins are not written: a caller whose gX and gK hold zeros
+ * there (allocated zeroed and written only by these calls) gets the results of the full
+ * calls, bit for bit, without their stores of zeros (three quarters of gX and gK when
+ * M = N/2).  Arguments and errors as fdc_cic_fdp_backward. */
+fdc_status fdc_cic_fdp_backward_kept(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX,
+                                     fdc_c64 *gK, int B, int C, int S, int N, int M, hipStream_t stream);
+fdc_status fdc_cic_fdp_backward_projected_kept(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K,
+                                               fdc_c64 *gX, fdc_c64 *gK, int B, int C, int S, int N, int M,
+                                               hipStream_t stream);
 
 /* FDP crops the RFFT-shifted half spectrum: (H-Mh)/2 rows off the top and the
  * bottom, (W-Mw)/2 columns off the right, then shifts back.  In unshifted

@@ -44,6 +44,8 @@ _SIGS = {
     "fdc_cic_fdp_backward": [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P],
     "fdc_cic_fdp_forward_projected": [_P, _P, _P, _I, _I, _I, _I, _I, _P],
     "fdc_cic_fdp_backward_projected": [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P],
+    "fdc_cic_fdp_backward_kept": [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P],
+    "fdc_cic_fdp_backward_projected_kept": [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P],
     "fdp_forward": [_P, _P, _I64, _I, _I, _I, _I, _P],
     "fdc_head_workspace_size": [_I, _I64, _I, ctypes.POINTER(_SZ)],
     "fdc_head_forward": [_P, _P, _P, _P, _P, _P, _I, _I64, _I, _P, _SZ, _P],

@@ -391,24 +391,35 @@ fdc_status fdc_cic_fdp_forward_projected(const fdc_c64 *X, const fdc_c64 *K, fdc
 }
 
 static fdc_status cic_fdp_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX, fdc_c64 *gK,
-                                   int B, int C, int S, int N, int M, bool project, hipStream_t s) {
+                                   int B, int C, int S, int N, int M, bool project, bool kept, hipStream_t s) {
   if (fdc_status st = check_cic_fdp(B, C, S, N, M)) return st;
   if (!gY || (gX && !K) || (gK && !X)) return fail(FDC_EINVAL, "NULL tensor");
   if (gX && !aligned16(gX)) return fail(FDC_EINVAL, "gX must be 16-byte aligned");
   return check_hip(fdc::launch_cic_fdp_bwd(reinterpret_cast<const float2 *>(gY), reinterpret_cast<const float2 *>(K),
                                            reinterpret_cast<float2 *>(gX), reinterpret_cast<const float2 *>(X),
-                                           reinterpret_cast<float2 *>(gK), B, C, S, N, M, project, s),
+                                           reinterpret_cast<float2 *>(gK), B, C, S, N, M, project, kept, s),
                    "cic_fdp_backward");
 }
 
 fdc_status fdc_cic_fdp_backward(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX, fdc_c64 *gK,
                                 int B, int C, int S, int N, int M, hipStream_t s) {
-  return cic_fdp_backward(gY, X, K, gX, gK, B, C, S, N, M, false, s);
+  return cic_fdp_backward(gY, X, K, gX, gK, B, C, S, N, M, false, false, s);
 }
 
 fdc_status fdc_cic_fdp_backward_projected(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX,
                                           fdc_c64 *gK, int B, int C, int S, int N, int M, hipStream_t s) {
-  return cic_fdp_backward(gY, X, K, gX, gK, B, C, S, N, M, true, s);
+  return cic_fdp_backward(gY, X, K, gX, gK, B, C, S, N, M, true, false, s);
+}
+
+fdc_status fdc_cic_fdp_backward_kept(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K, fdc_c64 *gX, fdc_c64 *gK,
+                                     int B, int C, int S, int N, int M, hipStream_t s) {
+  return cic_fdp_backward(gY, X, K, gX, gK, B, C, S, N, M, false, true, s);
+}
+
+fdc_status fdc_cic_fdp_backward_projected_kept(const fdc_c64 *gY, const fdc_c64 *X, const fdc_c64 *K,
+                                               fdc_c64 *gX, fdc_c64 *gK, int B, int C, int S, int N, int M,
+                                               hipStream_t s) {
+  return cic_fdp_backward(gY, X, K, gX, gK, B, C, S, N, M, true, true, s);
 }
 
 fdc_status fdc_hermitian_project(fdc_c64 *Y, int64_t count, int H, int W, hipStream_t s) {

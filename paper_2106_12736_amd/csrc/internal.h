@@ -267,9 +267,10 @@ bool cic_fdp_size_supported(int N);
 hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B, int C, int S, int N, int M,
                               bool project, hipStream_t s);
 // gX (NULL: skipped; needs K) and gK (NULL: skipped; needs X) in one launch; project:
-// gX written as Pi_H(gX).
+// gX written as Pi_H(gX); kept: the bins the FDP drops are not written (with project,
+// columns 0 and N/2 of gX are still written over every row).
 hipError_t launch_cic_fdp_bwd(const float2 *gY, const float2 *K, float2 *gX, const float2 *X, float2 *gK, int B,
-                              int C, int S, int N, int M, bool project, hipStream_t s);
+                              int C, int S, int N, int M, bool project, bool kept, hipStream_t s);
 hipError_t launch_fdp_gather(const float2 *X, float2 *Y, long long count, int H, int Wf, int Mh, int Mwf,
                              hipStream_t s);
 hipError_t launch_fdp_scatter(const float2 *gY, float2 *gX, long long count, int H, int Wf, int Mh, int Mwf,

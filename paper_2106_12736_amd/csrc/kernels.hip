@@ -1831,19 +1831,87 @@ __device__ __forceinline__ void fdp_bwd_gk_block(const float2 *__restrict__ gY, 
   }
 }
 
+// Kept-bins forms of the two blocks (fdc_cic_fdp_backward_kept): a thread per bin the
+// FDP keeps, bx over those M (M/2+1) bins of a plane in order (row k of the kept rows,
+// then column l); the bins FDP drops are not written.  The arithmetic of each kept bin
+// is that of fdp_bwd_gx_block and fdp_bwd_gk_block.  PROJ: columns 0 and N/2 of dX are
+// left to fdp_bwd_gx_edge, which writes them over every row.
+template <bool PROJ>
+__device__ __forceinline__ void fdp_bwd_gx_kept(const float2 *__restrict__ gY, const float2 *__restrict__ K,
+                                                float2 *__restrict__ gX, int B, int C, int J, int N, int M, int bx,
+                                                int by, int ny) {
+  constexpr int BI = 4;
+  const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1;
+  const int e = bx * 256 + threadIdx.x;
+  if (e >= M * Lm) return;
+  int l;
+  const int k = div_small(e, Lm, 1.f / (float)Lm, l);
+  if (PROJ && (l == 0 || l == NF - 1)) return;
+  const int kr = k < M / 2 ? k : k + (N - M);
+  const long long mpe = (long long)M * Lm, ys = (long long)S * mpe, pe = (long long)N * NF;
+  const long long kps = (long long)N * NF;
+  const int koff = kr * NF + l, yoff = e;
+  for (int c = by; c < C; c += ny) {
+    float2 *gp = gX + (long long)c * pe + koff;
+    const float2 *kp = K + (long long)c * J * kps;
+    const float2 *yp = gY + (long long)c * J * mpe;
+    for (int b0 = 0; b0 < B; b0 += BI) {
+      float2 a[BI];
+#pragma unroll
+      for (int u = 0; u < BI; ++u) a[u] = make_float2(0.f, 0.f);
+      for (int j = 0; j < J; ++j) {
+        const float2 kv = kp[j * kps + koff];
+        float2 g[BI];
+#pragma unroll
+        for (int u = 0; u < BI; ++u) g[u] = yp[(long long)min(b0 + u, B - 1) * ys + j * mpe + yoff];
+#pragma unroll
+        for (int u = 0; u < BI; ++u) a[u] = cfmac_f(a[u], g[u], kv);
+      }
+#pragma unroll
+      for (int u = 0; u < BI; ++u)
+        if (b0 + u < B) gp[(long long)(b0 + u) * C * pe] = a[u];
+    }
+  }
+}
+__device__ __forceinline__ void fdp_bwd_gk_kept(const float2 *__restrict__ gY, const float2 *__restrict__ X,
+                                                float2 *__restrict__ gK, int B, int C, int J, int N, int M, int bx,
+                                                int by, int ny) {
+  const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1, pe = N * NF;
+  const int e = bx * 256 + threadIdx.x;
+  if (e >= M * Lm) return;
+  int l;
+  const int k = div_small(e, Lm, 1.f / (float)Lm, l);
+  const int kr = k < M / 2 ? k : k + (N - M);
+  for (long long o = by; o < S; o += ny) {
+    float2 acc = make_float2(0.f, 0.f);
+    const long long c = o / J;
+#pragma unroll 4
+    for (int b = 0; b < B; ++b)
+      acc = cfmac(acc, gY[(((long long)b * S + o) * M + k) * Lm + l], X[(((long long)b * C + c) * N + kr) * NF + l]);
+    gK[o * pe + (long long)kr * NF + l] = acc;
+  }
+}
+
 // Workgroups [0, xbx * xby) run dX blocks, the next kbx * kby dK blocks, and with PROJ
 // the rest the Pi_H bins of dX (fdp_bwd_gx_edge).
-template <bool PROJ>
+// KEPT: the kept-bins blocks (fdp_bwd_gx_kept, fdp_bwd_gk_kept).
+template <bool PROJ, bool KEPT>
 __global__ __launch_bounds__(256) void k_cic_fdp_bwd(const float2 *__restrict__ gY, const float2 *__restrict__ K,
                                                      float2 *__restrict__ gX, const float2 *__restrict__ X,
                                                      float2 *__restrict__ gK, int B, int C, int J, int N, int M,
                                                      int xbx, int xby, int kbx, int kby, int nk) {
   const int id = blockIdx.x, nx = xbx * xby;
   if (id < nx) {
-    fdp_bwd_gx_block<PROJ>(gY, K, gX, B, C, J, N, M, id % xbx, id / xbx, xby);
+    if constexpr (KEPT)
+      fdp_bwd_gx_kept<PROJ>(gY, K, gX, B, C, J, N, M, id % xbx, id / xbx, xby);
+    else
+      fdp_bwd_gx_block<PROJ>(gY, K, gX, B, C, J, N, M, id % xbx, id / xbx, xby);
   } else if (!PROJ || id < nx + nk) {
     const int i = id - nx;
-    fdp_bwd_gk_block(gY, X, gK, B, C, J, N, M, i % kbx, i / kbx, kby);
+    if constexpr (KEPT)
+      fdp_bwd_gk_kept(gY, X, gK, B, C, J, N, M, i % kbx, i / kbx, kby);
+    else
+      fdp_bwd_gk_block(gY, X, gK, B, C, J, N, M, i % kbx, i / kbx, kby);
   } else {
     fdp_bwd_gx_edge(gY, K, gX, B, C, J, N, M, (long long)(id - nx - nk) * 256 + threadIdx.x);
   }
@@ -1925,21 +1993,22 @@ hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B
 }
 
 hipError_t launch_cic_fdp_bwd(const float2 *gY, const float2 *K, float2 *gX, const float2 *X, float2 *gK, int B,
-                              int C, int S, int N, int M, bool project, hipStream_t s) {
-  const long long pe = (long long)N * (N / 2 + 1);
+                              int C, int S, int N, int M, bool project, bool kept, hipStream_t s) {
+  const long long pe = (long long)N * (N / 2 + 1), pk = (long long)M * (M / 2 + 1);
   if (pe >= (1 << 24)) return hipErrorInvalidValue;
-  const long long xbx = gX ? (pe / 2 + 255) / 256 : 0, xby = gX ? C : 0;
-  const long long kbx = gK ? (pe + 255) / 256 : 0, kby = gK ? S : 0;
+  const long long xbx = gX ? ((kept ? pk : pe / 2) + 255) / 256 : 0, xby = gX ? C : 0;
+  const long long kbx = gK ? ((kept ? pk : pe) + 255) / 256 : 0, kby = gK ? S : 0;
   const long long nedge = (gX && project) ? ((long long)B * C * N * 2 + 255) / 256 : 0;
   const long long total = xbx * xby + kbx * kby + nedge;
   if (total == 0) return hipSuccess;
   if (total >= (1LL << 31)) return hipErrorInvalidValue;
   const int kbx1 = (int)(kbx > 0 ? kbx : 1), kby1 = (int)(kby > 0 ? kby : 1), nk = (int)(kbx * kby);
-  if (project && gX)
-    return timed_launch("cic_fdp_bwd", k_cic_fdp_bwd<true>, dim3((unsigned)total), dim3(256), 0, s, gY, K, gX, X, gK,
-                        B, C, S / C, N, M, (int)xbx, (int)xby, kbx1, kby1, nk);
-  return timed_launch("cic_fdp_bwd", k_cic_fdp_bwd<false>, dim3((unsigned)total), dim3(256), 0, s, gY, K, gX, X, gK, B,
-                      C, S / C, N, M, (int)xbx, (int)xby, kbx1, kby1, nk);
+  auto go = [&](auto kern) {
+    return timed_launch("cic_fdp_bwd", kern, dim3((unsigned)total), dim3(256), 0, s, gY, K, gX, X, gK, B, C, S / C,
+                        N, M, (int)xbx, (int)xby, kbx1, kby1, nk);
+  };
+  if (project && gX) return kept ? go(k_cic_fdp_bwd<true, true>) : go(k_cic_fdp_bwd<true, false>);
+  return kept ? go(k_cic_fdp_bwd<false, true>) : go(k_cic_fdp_bwd<false, false>);
 }
 
 // Largest spatial kernel of the spatial-kernel CIC calls.

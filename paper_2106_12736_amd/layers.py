@@ -569,6 +569,11 @@ class CicChain:
     input, every FDC (CIC) + FDP layer on spectra (fdc_cic_fdp_*), one irfft2 of the
     last spectrum.  All buffers are preallocated, so a step allocates nothing.
 
+    The gradient spectra `gspecs` and kernel gradients `gks` are zero from allocation at
+    the bins each FDP drops, and the backward (fdc_cic_fdp_backward_kept) writes only the
+    kept bins, so they stay zero there: a caller that replaces `gks` (as FdcnnClassifier
+    does, with views of its zeroed gradient buffer) must keep that so.
+
     The input transform forms only the bins the first FDP keeps (fdc_rfft2_pooled_ws, in
     the chain's transform workspace): the first layer reads no others, forward or backward.
 
@@ -590,9 +595,11 @@ class CicChain:
         cd = torch.complex64
         self.specs = [torch.empty((B, channels[i], sizes[i], sizes[i] // 2 + 1), dtype=cd, device=self.device)
                       for i in range(self.layers + 1)]
-        self.gspecs = [torch.empty_like(t) for t in self.specs]
+        # zero from allocation: the backward writes only the bins each FDP keeps
+        # (fdc_cic_fdp_backward_kept), and the others are never written
+        self.gspecs = [torch.zeros_like(t) for t in self.specs]
         self.out = torch.empty((B, channels[-1], sizes[-1], sizes[-1]), dtype=torch.float32, device=self.device)
-        self.gks = [torch.empty((channels[i + 1], sizes[i], sizes[i] // 2 + 1), dtype=cd, device=self.device)
+        self.gks = [torch.zeros((channels[i + 1], sizes[i], sizes[i] // 2 + 1), dtype=cd, device=self.device)
                     for i in range(self.layers)]
 
     def forward(self, x, kernels):
@@ -623,7 +630,8 @@ class CicChain:
             need_gx = i > 0 or input_grad is not None
             # Pi_H (its own adjoint) on the input gradient of every layer but the first,
             # in the layer's own launch
-            fn = "fdc_cic_fdp_backward_projected" if self.hermitian and i > 0 else "fdc_cic_fdp_backward"
+            # (the kept-bins forms: the bins the FDP drops stay zero in gspecs and gks)
+            fn = "fdc_cic_fdp_backward_projected_kept" if self.hermitian and i > 0 else "fdc_cic_fdp_backward_kept"
             call(fn, _ptr(self.gspecs[i + 1]), _ptr(self.specs[i]), _ptr(kernels[i]),
                  _ptr(self.gspecs[i] if need_gx else None), _ptr(self.gks[i]), B, self.channels[i],
                  self.channels[i + 1], self.sizes[i], self.sizes[i + 1], s)

@@ -2,6 +2,7 @@
 on spectra, one irfft2) against the float64 oracle: the fused spectral CIC + FDP op on
 its own, and the whole chain forward and backward on every CIC workload at full size."""
 
+import ctypes
 import zlib
 
 import numpy as np
@@ -11,12 +12,21 @@ import torch
 from _parity import assert_parity, to_np
 from oracle import dft, fdc
 from paper_2106_12736_amd import inputs, layers
+from paper_2106_12736_amd._lib import call
 
 pytestmark = pytest.mark.gpu
 
 
 def _rng(*key):
     return np.random.default_rng(zlib.crc32(repr(key).encode()))
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _p(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
 
 
 def _c64(rng, shape):
@@ -72,6 +82,43 @@ def test_cic_fdp_projected_op(B, C, S, N, M):
     assert_parity(to_np(Yp), dft.hermitian_projection(fdc.fdp(fdc.cic(X64, K64), M, M)), "Pi_H Y")
     gx_ref, _ = fdc.cic_backward(fdc.fdp_backward(g64, N, N), X64, K64)
     assert_parity(to_np(gXp), dft.hermitian_projection(gx_ref), "Pi_H gX")
+
+
+@pytest.mark.parametrize("B,C,S,N,M", [
+    (1, 1, 1, 4, 2), (2, 1, 4, 8, 4), (3, 2, 6, 16, 16), (2, 4, 4, 32, 8), (1, 3, 9, 64, 32), (2, 2, 4, 224, 112),
+    (11, 2, 4, 16, 8), (9, 1, 8, 32, 16), (8, 1, 8, 1024, 512), (8, 8, 16, 512, 256),
+])
+@pytest.mark.parametrize("project", [False, True])
+def test_cic_fdp_backward_kept(B, C, S, N, M, project):
+    """The kept-bins forms on zeroed gX and gK equal the full calls, bit for bit at every
+    bin (the projected form also over columns 0 and N/2 of the dropped rows), and leave
+    every dropped bin of gK and every dropped bin of gX outside those columns untouched."""
+    print(f"cic_fdp kept B={B} C={C} S={S} N={N} M={M} project={project}", flush=True)
+    rng = _rng("cic_fdp_kept", B, C, S, N, M)
+    X = _c64(rng, (B, C, N, N // 2 + 1))
+    K = _c64(rng, (S, N, N // 2 + 1))
+    gY = _c64(rng, (B, S, M, M // 2 + 1))
+    Xd, Kd, gYd = (torch.from_numpy(a).cuda() for a in (X, K, gY))
+    gX, gK = layers.cic_fdp_backward(gYd, Xd, Kd, project=project)
+    gX0, gK0 = torch.zeros_like(Xd), torch.zeros_like(Kd)
+    fn = "fdc_cic_fdp_backward_projected_kept" if project else "fdc_cic_fdp_backward_kept"
+    call(fn, _p(gYd), _p(Xd), _p(Kd), _p(gX0), _p(gK0), B, C, S, N, M, _stream())
+    # a sentinel in every dropped bin: the kept forms must not write there
+    nan = float("nan")
+    kept = np.zeros((N, N // 2 + 1), bool)
+    kept[np.r_[0:M // 2, N - M // 2:N], :M // 2 + 1] = True
+    gxw = kept.copy()
+    if project:
+        gxw[:, 0] = gxw[:, N // 2] = True
+    gXs, gKs = torch.zeros_like(Xd), torch.zeros_like(Kd)
+    gXs[..., torch.from_numpy(~gxw)] = complex(nan, nan)
+    gKs[..., torch.from_numpy(~kept)] = complex(nan, nan)
+    call(fn, _p(gYd), _p(Xd), _p(Kd), _p(gXs), _p(gKs), B, C, S, N, M, _stream())
+    torch.cuda.synchronize()
+    assert torch.equal(gX0, gX) and torch.equal(gK0, gK)
+    assert np.all(np.isnan(to_np(gXs)[..., ~gxw])) and np.all(np.isnan(to_np(gKs)[..., ~kept]))
+    assert torch.equal(gXs[..., torch.from_numpy(gxw)], gX[..., torch.from_numpy(gxw)])
+    assert torch.equal(gKs[..., torch.from_numpy(kept)], gK[..., torch.from_numpy(kept)])
 
 
 @pytest.mark.parametrize("wl", inputs.CIC_WORKLOADS, ids=lambda w: w.name)
