@@ -69,13 +69,15 @@ def fwd_col_launches(B, C, S, N, M, L):
 def gk_launches(B, C, S, N, M, L, NF, ranges=1, zeros=True):
     """dK of one layer: one launch that reads the upstream and saved spectra and writes
     all of gK (zeros where FDP drops; with zeros=False only the kept bins, the zeros
-    coming from the launch before), or, with the batch cut into R ranges, the range
-    sums written by that launch and added in order by a second one."""
+    coming from the launch before or already in the buffer), or, with the batch cut
+    into R ranges, the range sums written by that launch and added in order by a
+    second one."""
+    gk_bytes = S * N * NF if zeros else S * M * L
     if ranges <= 1:
-        return [(f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + (S * N * NF if zeros else S * M * L)))]
+        return [(f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + gk_bytes))]
     R = ranges
     return [(f"col_bwd_gk_{M}", C64 * (B * S * M * L + B * C * M * L + R * S * M * L)),
-            ("gk_reduce", C64 * (R * S * M * L + S * N * NF))]
+            ("gk_reduce", C64 * (R * S * M * L + gk_bytes))]
 
 
 def step_launches(wl, input_grad=False, ranges=None):
@@ -98,14 +100,15 @@ def step_launches(wl, input_grad=False, ranges=None):
     return out
 
 
-def tail_launches(wl, a, input_grad=False):
+def tail_launches(wl, a, input_grad=False, kept=False):
     """The stack's last two layers (a, a + 1) run by the LDS-resident tail kernels:
     (forward launch, [backward launch, in-order dK sums of both layers]).
     Bytes: what crosses HBM -- the previous layer's column-inverted spectra (or the
     input image), both kernels at the kept bins, both saved spectra, the output;
     backward the upstream gradient, both saved spectra and kernels, the per-image dK
     products (written, then read by the in-order sums) and the previous layer's
-    upstream-gradient spectrum (or the input gradient)."""
+    upstream-gradient spectrum (or the input gradient); kept: the dK sums write the
+    kept bins of gK only."""
     B, C, S, N, M, L, NF = layer_dims(wl, a)
     _, _, S2, _, M2, L2, NF2 = layer_dims(wl, a + 1)
     k_bytes = C64 * (S * M * L + S2 * M2 * L2)
@@ -117,17 +120,18 @@ def tail_launches(wl, a, input_grad=False):
     fwd = (f"tail_fwd_{name}", in_bytes + k_bytes + saved_bytes + out_bytes)
     dx_bytes = in_bytes if (a > 0 or input_grad) else 0
     bwd = [(f"tail_bwd_{name}", out_bytes + saved_bytes + k_bytes + part_a + part_b + dx_bytes),
-           ("gk_reduce", part_a + part_b + C64 * (S * N * NF + S2 * M * NF2))]
+           ("gk_reduce", part_a + part_b + (k_bytes if kept else C64 * (S * N * NF + S2 * M * NF2)))]
     return fwd, bwd
 
 
-def fused_step_launches(wl, input_grad=False, ranges=None, tail=-1):
+def fused_step_launches(wl, input_grad=False, ranges=None, tail=-1, kept=False):
     """(kernel name, algorithmic bytes) of every launch of one step of the fused stack
     executor: as step_launches, with each layer boundary's inverse rows and the next
     layer's forward rows (and the backward's adjoint pair) in one kernel, a layer's
     dK and dX columns in one launch when dK uses one batch range, and the last two
-    layers in the LDS-resident tail kernels from layer `tail` on (-1: none)."""
-    return fused_fwd_launches(wl, tail) + fused_bwd_launches(wl, input_grad, ranges, tail)
+    layers in the LDS-resident tail kernels from layer `tail` on (-1: none); kept: the
+    backward writes only the kept bins of gK (fdc_cic_stack_backward_kept)."""
+    return fused_fwd_launches(wl, tail) + fused_bwd_launches(wl, input_grad, ranges, tail, kept)
 
 
 def fused_fwd_launches(wl, tail=-1):
@@ -151,7 +155,7 @@ def fused_fwd_launches(wl, tail=-1):
     return out
 
 
-def fused_bwd_launches(wl, input_grad=False, ranges=None, tail=-1):
+def fused_bwd_launches(wl, input_grad=False, ranges=None, tail=-1, kept=False):
     ranges = ranges or [1] * wl.layers
     out = []
     n = wl.layers
@@ -161,13 +165,13 @@ def fused_bwd_launches(wl, input_grad=False, ranges=None, tail=-1):
         return (i > 0 or input_grad) and ranges[i] <= 1 and N <= 256
 
     def zeros_early(i):  # layer i's gK zeros written by layer i + 1's boundary rows
-        return i + 1 < n and not (tail >= 0 and i + 1 >= tail) and not merged(i) and ranges[i] <= 1
+        return not kept and i + 1 < n and not (tail >= 0 and i + 1 >= tail) and not merged(i) and ranges[i] <= 1
 
     for i in reversed(range(n)):
         B, C, S, N, M, L, NF = layer_dims(wl, i)
         if tail >= 0 and i >= tail:
             if i == tail + 1:
-                out += tail_launches(wl, tail, input_grad)[1]
+                out += tail_launches(wl, tail, input_grad, kept)[1]
             continue
         if i == n - 1:
             out.append((f"row_r2c_{M}", F32 * B * S * M * M + C64 * B * S * M * L))
@@ -175,10 +179,10 @@ def fused_bwd_launches(wl, input_grad=False, ranges=None, tail=-1):
         gx_bytes = C64 * (B * S * M * L + S * M * L + B * C * N * L)
         if merged(i):
             # dK and dX columns in one launch (layers of at most 256 points): the bytes of both
-            (_, gk_bytes), = gk_launches(B, C, S, N, M, L, NF, 1)
+            (_, gk_bytes), = gk_launches(B, C, S, N, M, L, NF, 1, zeros=not kept)
             out.append((f"col_bwd_dk_dx_{N}_{M}", gk_bytes + gx_bytes))
         else:
-            out += gk_launches(B, C, S, N, M, L, NF, ranges[i], zeros=not zeros_early(i))
+            out += gk_launches(B, C, S, N, M, L, NF, ranges[i], zeros=not kept and not zeros_early(i))
             if dx:
                 out.append((f"col_bwd_gx_{N}_{M}", gx_bytes))
         if dx:
@@ -537,7 +541,8 @@ class CicStackRun:
             model = lambda w_, ig: step_launches(w_, ig, self.stack.dk_ranges())  # noqa: E731
         else:
             self.stack = layers.CicStackFused(wl.batch, wl.sizes, wl.channels, device=dev)
-            model = lambda w_, ig: fused_step_launches(w_, ig, self.stack.dk_ranges(), self.stack.tail())  # noqa: E731
+            model = lambda w_, ig: fused_step_launches(w_, ig, self.stack.dk_ranges(), self.stack.tail(),  # noqa: E731
+                                                       kept=True)
         self.gin = (torch.empty((wl.batch, wl.channels[0], wl.sizes[0], wl.sizes[0]), dtype=torch.float32,
                                 device=dev) if args.input_grad else None)
         self.input_grad = args.input_grad

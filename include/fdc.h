@@ -325,6 +325,17 @@ fdc_status fdc_cic_stack_forward(const fdc_stack_plan *plan, const float *x, con
 fdc_status fdc_cic_stack_backward(const fdc_stack_plan *plan, const float *gy, const void *const *saved,
                                   const fdc_c64 *const *K, float *gx, fdc_c64 *const *gK, void *ws,
                                   size_t ws_bytes, hipStream_t stream);
+/* The same backward writing only the kept bins of every gK[i] (rows [0, M/2) and
+ * [N-M/2, N), columns [0, M/2] of each plane, N = sizes[i], M = sizes[i+1]): the
+ * dropped bins, where the gradient is exactly zero because FDP discards them
+ * (section 2.4.2), are neither read nor written.  For callers that keep gK buffers
+ * across steps with zeros at those bins (zeroed once at allocation): the result then
+ * equals fdc_cic_stack_backward's bit for bit, without its stores of zeros (three
+ * quarters of every gK when M = N/2).  Arguments, workspace and errors as
+ * fdc_cic_stack_backward. */
+fdc_status fdc_cic_stack_backward_kept(const fdc_stack_plan *plan, const float *gy, const void *const *saved,
+                                       const fdc_c64 *const *K, float *gx, fdc_c64 *const *gK, void *ws,
+                                       size_t ws_bytes, hipStream_t stream);
 
 /* The same stack with n x n spatial kernels (section 2.4.1.2) and ROLL artifact
  * handling in every layer: the result of fdc_cic_spatial_layer_forward / backward

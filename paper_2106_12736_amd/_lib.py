@@ -72,6 +72,7 @@ _SIGS = {
     "fdc_cic_stack_saved_size": [_P, _I, ctypes.POINTER(_SZ)],
     "fdc_cic_stack_forward": [_P, _P, _P, _P, _P, _P, _SZ, _P],
     "fdc_cic_stack_backward": [_P, _P, _P, _P, _P, _P, _P, _SZ, _P],
+    "fdc_cic_stack_backward_kept": [_P, _P, _P, _P, _P, _P, _P, _SZ, _P],
     "fdc_hermitian_project": [_P, _I64, _I, _I, _P],
     "fdc_cic_spatial_stack_workspace_size": [_P, _I, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ)],
     "fdc_cic_spatial_stack_forward": [_P, _I, _P, _P, _P, _P, _P, _SZ, _P],

@@ -860,9 +860,11 @@ fdc_status fdc_cic_stack_forward(const fdc_stack_plan *p, const float *x, const 
   return FDC_OK;
 }
 
-fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, const void *const *saved,
-                                  const fdc_c64 *const *K, float *gx, fdc_c64 *const *gK, void *ws, size_t ws_bytes,
-                                  hipStream_t s) {
+namespace {
+// The stack's backward; kept: gK's dropped bins are left as they are (the caller's
+// buffers hold zeros there), only the kept bins are written.
+fdc_status stack_backward(const fdc_stack_plan *p, const float *gy, const void *const *saved, const fdc_c64 *const *K,
+                          float *gx, fdc_c64 *const *gK, void *ws, size_t ws_bytes, hipStream_t s, bool kept) {
   if (fdc_status st = check_stack_plan(p)) return st;
   if (!gy || !saved || !K || !gK) return fail(FDC_EINVAL, "NULL tensor or array");
   for (int i = 0; i < p->layers; ++i)
@@ -880,7 +882,7 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, cons
   // Layer i's gK zeros written by the boundary row launch of layer i + 1 (which runs
   // just before layer i's dK): for a dK launch of one batch range below the tail.
   auto zeros_early = [&](int i) {
-    if (i + 1 >= p->layers || (p->tail >= 0 && i + 1 >= p->tail)) return false;
+    if (kept || i + 1 >= p->layers || (p->tail >= 0 && i + 1 >= p->tail)) return false;
     const StackLayer g = stack_layer(p, i);
     return !dk_merged(i) && fdc::gk_batch_ranges(g.N, g.M, B, g.S, (long long)p->ws_b) == 1;
   };
@@ -909,7 +911,7 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, cons
         return st;
       if (fdc_status st = check_hip(fdc::launch_gk_reduce2(part_a, reinterpret_cast<float2 *>(gK[a]), ga.S, ga.M,
                                                            ga.N, part_b, reinterpret_cast<float2 *>(gK[a + 1]), gb.S,
-                                                           gb.M, gb.N, B, s),
+                                                           gb.M, gb.N, B, s, !kept),
                                     "stack backward tail dK sums"))
         return st;
       i = a;  // continue with layer a - 1
@@ -930,14 +932,15 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, cons
       // dK and dX columns side by side in one launch
       if (fdc_status st = check_hip(fdc::launch_col_bwd_dk_dx(g.N, g.M, Tg, reinterpret_cast<const float2 *>(saved[i]),
                                                               reinterpret_cast<const float2 *>(K[i]),
-                                                              reinterpret_cast<float2 *>(gK[i]), V, B, g.C, g.S, s),
+                                                              reinterpret_cast<float2 *>(gK[i]), V, B, g.C, g.S, s,
+                                                              !kept),
                                     "stack backward dK and dx columns"))
         return st;
     } else {
       // V is free until the dX columns below: dK's batch-range sums go there
       if (fdc_status st = check_hip(fdc::launch_col_bwd_gk(g.N, g.M, Tg, reinterpret_cast<const float2 *>(saved[i]),
                                                            reinterpret_cast<float2 *>(gK[i]), B, g.C, g.S, V,
-                                                           (long long)p->ws_b, s, !zeros_early(i)),
+                                                           (long long)p->ws_b, s, !kept && !zeros_early(i)),
                                     "stack backward dK"))
         return st;
       if (!need_dx) break;
@@ -967,6 +970,19 @@ fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, cons
     }
   }
   return FDC_OK;
+}
+}  // namespace
+
+fdc_status fdc_cic_stack_backward(const fdc_stack_plan *p, const float *gy, const void *const *saved,
+                                  const fdc_c64 *const *K, float *gx, fdc_c64 *const *gK, void *ws, size_t ws_bytes,
+                                  hipStream_t s) {
+  return stack_backward(p, gy, saved, K, gx, gK, ws, ws_bytes, s, false);
+}
+
+fdc_status fdc_cic_stack_backward_kept(const fdc_stack_plan *p, const float *gy, const void *const *saved,
+                                       const fdc_c64 *const *K, float *gx, fdc_c64 *const *gK, void *ws,
+                                       size_t ws_bytes, hipStream_t s) {
+  return stack_backward(p, gy, saved, K, gx, gK, ws, ws_bytes, s, true);
 }
 
 // ---------------------------------------------------------------------------

@@ -163,23 +163,23 @@ hipError_t launch_col_fwd_cic(int n, int m, const float2 *T, const float2 *K, fl
                               int C, int S, hipStream_t s);
 // dK: with scratch `part` (part_elems complex values; may be NULL) the batch is cut
 // into gk_batch_ranges(...) ranges whose sums are added in order by a second kernel.
-// zeros = false: with one range the dropped bins of gK are left as they are (an earlier
-// launch of the same call wrote their zeros).
+// zeros = false: the dropped bins of gK are left as they are (an earlier launch of the
+// same call wrote their zeros, or the caller's buffer holds them).
 int gk_batch_ranges(int n, int m, int B, int S, long long part_elems);
 hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, float2 *gK, int B, int C,
                              int S, float2 *part, long long part_elems, hipStream_t s, bool zeros = true);
 hipError_t launch_col_bwd_gx(int n, int m, const float2 *Tg, const float2 *K, float2 *V, int B, int C, int S,
                              hipStream_t s);
 // gK [S][N][N/2+1] from BG partial sums part [BG][S][M][M/2+1] (plain layout): at the
-// kept bins the partial sums added in order, exact zeros elsewhere; one launch for
-// one reduction (part1 NULL) or two.
+// kept bins the partial sums added in order, exact zeros elsewhere (zeros = false: the
+// kept bins only); one launch for one reduction (part1 NULL) or two.
 hipError_t launch_gk_reduce2(const float2 *part0, float2 *gK0, int S0, int M0, int N0, const float2 *part1,
-                             float2 *gK1, int S1, int M1, int N1, int BG, hipStream_t s);
+                             float2 *gK1, int S1, int M1, int N1, int BG, hipStream_t s, bool zeros = true);
 // dK (one batch range) and dX of one layer in a single launch, where the dX tiles pack
-// the dK workgroup (col_bwd_dk_dx_supported).
+// the dK workgroup (col_bwd_dk_dx_supported); zeros as for launch_col_bwd_gk.
 bool col_bwd_dk_dx_supported(int n, int m);
 hipError_t launch_col_bwd_dk_dx(int n, int m, const float2 *Tg, const float2 *Xh, const float2 *K, float2 *gK,
-                                float2 *V, int B, int C, int S, hipStream_t s);
+                                float2 *V, int B, int C, int S, hipStream_t s, bool zeros = true);
 
 // The last two layers of a stack with all intermediates in LDS (tail.hip): layer a
 // (na -> ma, fan-out ja) and layer b (ma -> mb, fan-out jb), one workgroup per input

@@ -901,10 +901,11 @@ __global__ __launch_bounds__(CT *ColCfg<M>::TPS *BP) void k_col_bwd_gk(const flo
 // one or two reductions (grid.y selects the GkSum): a thread per gK element, its BG
 // partial sums loaded together (16 at a time) and added in order at the kept bins,
 // exact zeros elsewhere.  Consecutive threads take consecutive bins of a row.
+// kept != 0: a thread per kept bin only, the other bins of gK left as they are.
 struct GkSum {
   const float2 *part;
   float2 *gK;
-  int BG, S, M, N;
+  int BG, S, M, N, kept;
 };
 
 constexpr int kGkReduceThreads = 256;
@@ -913,12 +914,23 @@ __global__ __launch_bounds__(kGkReduceThreads) void k_gk_reduce(GkSum d0, GkSum 
   const GkSum d = blockIdx.y == 0 ? d0 : d1;
   const int L = d.M / 2 + 1, nf = d.N / 2 + 1;
   // 32-bit element arithmetic: the launchers keep S * N * (N/2+1) below 2^31
-  const unsigned total = (unsigned)(d.S * d.N * nf);
+  const unsigned total = (unsigned)(d.kept ? d.S * d.M * L : d.S * d.N * nf);
   const long long range_stride = (long long)d.S * d.M * L;
   for (unsigned i = blockIdx.x * kGkReduceThreads + threadIdx.x; i < total; i += gridDim.x * kGkReduceThreads) {
-    const int r = (int)(i / (unsigned)nf), l = (int)i - r * nf;
-    const int o = r / d.N, krow = r - o * d.N;
-    const int mrow = krow < d.M / 2 ? krow : (krow >= d.N - d.M / 2 ? krow - (d.N - d.M) : -1);
+    int o, mrow, l, krow;
+    if (d.kept) {
+      const int r = (int)(i / (unsigned)L);
+      l = (int)i - r * L;
+      o = r / d.M;
+      mrow = r - o * d.M;
+      krow = mrow < d.M / 2 ? mrow : mrow + (d.N - d.M);
+    } else {
+      const int r = (int)(i / (unsigned)nf);
+      l = (int)i - r * nf;
+      o = r / d.N;
+      krow = r - o * d.N;
+      mrow = krow < d.M / 2 ? krow : (krow >= d.N - d.M / 2 ? krow - (d.N - d.M) : -1);
+    }
     float2 v = make_float2(0.f, 0.f);
     if (mrow >= 0 && l < L) {
       const float2 *src = d.part + ((long long)o * d.M + mrow) * L + l;
@@ -939,13 +951,17 @@ __global__ __launch_bounds__(kGkReduceThreads) void k_gk_reduce(GkSum d0, GkSum 
       }
       for (; q < d.BG; ++q) v = cadd(v, src[q * range_stride]);
     }
-    d.gK[i] = v;
+    d.gK[((long long)o * d.N + krow) * nf + l] = v;
   }
 }
 
+static long long gk_reduce_items(const GkSum &d) {
+  return d.kept ? (long long)d.S * d.M * (d.M / 2 + 1) : (long long)d.S * d.N * (d.N / 2 + 1);
+}
+
 static hipError_t gk_reduce(const GkSum &d0, const GkSum *d1, hipStream_t s) {
-  long long total = (long long)d0.S * d0.N * (d0.N / 2 + 1);
-  if (d1) total = std::max(total, (long long)d1->S * d1->N * (d1->N / 2 + 1));
+  long long total = gk_reduce_items(d0);
+  if (d1) total = std::max(total, gk_reduce_items(*d1));
   const unsigned gx = (unsigned)std::min<long long>((total + kGkReduceThreads - 1) / kGkReduceThreads, 1 << 16);
   const char *nm = "gk_reduce";
   return timed_launch(nm, k_gk_reduce, dim3(gx, d1 ? 2 : 1), dim3(kGkReduceThreads), 0, s, d0, d1 ? *d1 : d0);
@@ -1059,7 +1075,8 @@ __global__ __launch_bounds__(CT *ColCfg<N>::TPS) void k_col_bwd_gx(const float2 
 template <int N, int M, int CTK, int BP, int CTX>
 __global__ __launch_bounds__(CTK *ColCfg<M>::TPS *BP) void k_col_bwd_dk_dx(
     const float2 *__restrict__ Tg, const float2 *__restrict__ Xh, const float2 *__restrict__ K,
-    float2 *__restrict__ gK, float2 *__restrict__ V, int B, int C, int J, int S, int nk, int nk_used, int nx_tiles) {
+    float2 *__restrict__ gK, float2 *__restrict__ V, int B, int C, int J, int S, int nk, int nk_used, int nx_tiles,
+    int zeros) {
   constexpr int NT = CTK * ColCfg<M>::TPS * BP, NX = CTX * ColCfg<N>::TPS, PACK = NT / NX;
   static_assert(PACK >= 1 && PACK * NX == NT, "dX tiles must pack the dK workgroup exactly");
   float2 *tw = g_lds, *lds = g_lds + twiddle_lds_elems<N>();
@@ -1068,7 +1085,7 @@ __global__ __launch_bounds__(CTK *ColCfg<M>::TPS *BP) void k_col_bwd_dk_dx(
   if (bid < nk) {
     if (bid >= nk_used) return;  // padding: no barrier follows
     col_bwd_gk_tile<M, CTK, BP>(xcd_remap(bid, nk_used), nk_used, threadIdx.x, tw, N / M, lds, Tg, Xh, gK,
-                                nullptr, B, C, J, N, S, 1, true);
+                                nullptr, B, C, J, N, S, 1, zeros != 0);
     return;
   }
   const int xb = bid - nk, nxb = gridDim.x - nk;
@@ -1508,19 +1525,20 @@ hipError_t launch_col_bwd_gk(int n, int m, const float2 *Tg, const float2 *Xh, f
     else
       go(std::integral_constant<int, col_ct_for(gk_ct<M>(), L)>{});
     if (err != hipSuccess || BG == 1) return;
-    err = gk_reduce(GkSum{part, gK, BG, S, M, n}, nullptr, s);
+    err = gk_reduce(GkSum{part, gK, BG, S, M, n, zeros ? 0 : 1}, nullptr, s);
   });
   return err;
 }
 
 hipError_t launch_gk_reduce2(const float2 *part0, float2 *gK0, int S0, int M0, int N0, const float2 *part1,
-                             float2 *gK1, int S1, int M1, int N1, int BG, hipStream_t s) {
-  const GkSum d1{part1, gK1, BG, S1, M1, N1};
-  return gk_reduce(GkSum{part0, gK0, BG, S0, M0, N0}, part1 ? &d1 : nullptr, s);
+                             float2 *gK1, int S1, int M1, int N1, int BG, hipStream_t s, bool zeros) {
+  const int kept = zeros ? 0 : 1;
+  const GkSum d1{part1, gK1, BG, S1, M1, N1, kept};
+  return gk_reduce(GkSum{part0, gK0, BG, S0, M0, N0, kept}, part1 ? &d1 : nullptr, s);
 }
 
 hipError_t launch_col_bwd_dk_dx(int n, int m, const float2 *Tg, const float2 *Xh, const float2 *K, float2 *gK,
-                                float2 *V, int B, int C, int S, hipStream_t s) {
+                                float2 *V, int B, int C, int S, hipStream_t s, bool zeros) {
   hipError_t err = hipErrorInvalidValue;
   if (!cic_pair_supported(n, m)) return err;
   dispatch_nm(n, m, [&](auto nc, auto mc) {
@@ -1537,7 +1555,7 @@ hipError_t launch_col_bwd_dk_dx(int n, int m, const float2 *Tg, const float2 *Xh
       const size_t lds = (twiddle_lds_elems<N>() + (gk_lds > gx_lds ? gk_lds : gx_lds)) * sizeof(float2);
       static const std::string nm = "col_bwd_dk_dx_" + std::to_string(N) + "_" + std::to_string(M);
       err = launch(nm.c_str(), k_col_bwd_dk_dx<N, M, CTK, BP, CTX>, nk + nxb, NT, lds, s, Tg, Xh, K, gK, V, B, C,
-                   S / C, S, (int)nk, (int)nk_used, (int)nx_tiles);
+                   S / C, S, (int)nk, (int)nk_used, (int)nx_tiles, zeros ? 1 : 0);
     }
   });
   return err;

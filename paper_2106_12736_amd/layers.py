@@ -442,7 +442,9 @@ class CicStackFused:
             call("fdc_cic_stack_saved_size", self._p, i, ctypes.byref(n))
             self.saved.append(torch.empty(n.value // 8, dtype=torch.complex64, device=self.device))
         self.out = torch.empty((batch, channels[-1], sizes[-1], sizes[-1]), dtype=torch.float32, device=self.device)
-        self.gks = [torch.empty((channels[i + 1], sizes[i], sizes[i] // 2 + 1), dtype=torch.complex64,
+        # zero once: the backward (fdc_cic_stack_backward_kept) writes only the bins FDP
+        # keeps, and the gradient is exactly zero at the others
+        self.gks = [torch.zeros((channels[i + 1], sizes[i], sizes[i] // 2 + 1), dtype=torch.complex64,
                                 device=self.device) for i in range(self.layers)]
         self._saved_arr = _ptr_array(self.saved)
         self._gk_arr = _ptr_array(self.gks)
@@ -476,12 +478,15 @@ class CicStackFused:
         return self.out
 
     def backward(self, gy, kernels, input_grad=None):
-        """Kernel gradients of every layer (and the input gradient into `input_grad` if given)."""
+        """Kernel gradients of every layer (and the input gradient into `input_grad` if given).
+        The returned tensors are the module's own buffers, rewritten at the kept bins by
+        every call; their other bins hold the zeros set at construction, so callers must
+        not write into them."""
         _check(gy, torch.float32, tuple(self.out.shape), "gy")
         if input_grad is not None:
             _check(input_grad, torch.float32, (self.batch, self.channels[0], self.sizes[0], self.sizes[0]),
                    "input_grad")
-        call("fdc_cic_stack_backward", self._p, _ptr(gy), self._saved_arr, self._kernels(kernels), _ptr(input_grad),
+        call("fdc_cic_stack_backward_kept", self._p, _ptr(gy), self._saved_arr, self._kernels(kernels), _ptr(input_grad),
              self._gk_arr, _ptr(self.bwd_ws), self.bwd_ws.numel(), _stream())
         return self.gks
 

@@ -154,3 +154,54 @@ def test_stack_that_is_only_a_tail(input_grad):
         assert_parity(to_np(st.gks[i]), gks_ref[i], f"dK[{i}]")
     if input_grad:
         assert_parity(to_np(gin), gx_ref, "gx")
+
+
+def _stack_backward(fn, st, g, Ks, gks, gin):
+    from paper_2106_12736_amd._lib import call
+    from paper_2106_12736_amd.layers import _ptr, _ptr_array, _stream
+    call(fn, st._p, _ptr(g), st._saved_arr, _ptr_array(Ks), _ptr(gin), _ptr_array(gks), _ptr(st.bwd_ws),
+         st.bwd_ws.numel(), _stream())
+    torch.cuda.synchronize()
+
+
+_TAIL_ONLY = inputs.CicStack("tail_only_128", 77, 3, (128, 64, 32), (2, 4, 8), "disc")
+
+
+@pytest.mark.parametrize("input_grad", [True, False])
+@pytest.mark.parametrize("wl", list(inputs.CIC_WORKLOADS) + [_TAIL_ONLY], ids=lambda w: w.name)
+def test_stack_backward_kept_matches_full(wl, input_grad):
+    """fdc_cic_stack_backward_kept writes the kept bins of every gK only: on buffers
+    that hold zeros elsewhere it equals fdc_cic_stack_backward bit for bit (dK of every
+    layer path: one batch range, ranges summed by a second launch, dK and dX merged, the
+    tail's sums), and NaN planted at the dropped bins stays there."""
+    print(f"stack backward kept {wl.name}, input grad {input_grad}", flush=True)
+    d = inputs.make_cic_stack(wl)
+    x = torch.from_numpy(d.x).cuda()
+    Ks = [torch.from_numpy(k).cuda() for k in d.kernels]
+    g = torch.from_numpy(d.grad).cuda()
+    st = layers.CicStackFused(wl.batch, wl.sizes, wl.channels)
+    st.forward(x, Ks)
+    shapes = [(wl.channels[i + 1], wl.sizes[i], wl.sizes[i] // 2 + 1) for i in range(wl.layers)]
+    nan = complex(float("nan"), float("nan"))
+
+    def bufs(fill):
+        return [torch.full(s, fill, dtype=torch.complex64, device="cuda") for s in shapes]
+
+    gin_full = torch.full_like(x, float("nan")) if input_grad else None
+    gin_kept = torch.full_like(x, float("nan")) if input_grad else None
+    full, kept0, kept_nan = bufs(nan), bufs(0), bufs(nan)
+    _stack_backward("fdc_cic_stack_backward", st, g, Ks, full, gin_full)
+    _stack_backward("fdc_cic_stack_backward_kept", st, g, Ks, kept0, gin_kept)
+    _stack_backward("fdc_cic_stack_backward_kept", st, g, Ks, kept_nan, None)
+    for i in range(wl.layers):
+        N, M = wl.sizes[i], wl.sizes[i + 1]
+        assert not torch.isnan(full[i]).any(), f"dK[{i}]: full form left a bin unwritten"
+        assert torch.equal(kept0[i], full[i]), f"dK[{i}]: kept form differs from the full form"
+        kn = kept_nan[i]
+        keep = torch.zeros(shapes[i], dtype=torch.bool, device="cuda")
+        keep[:, :M // 2, :M // 2 + 1] = True
+        keep[:, N - M // 2:, :M // 2 + 1] = True
+        assert torch.equal(kn[keep], full[i][keep]), f"dK[{i}]: kept bins"
+        assert torch.isnan(kn[~keep]).all(), f"dK[{i}]: a dropped bin was written"
+    if input_grad:
+        assert torch.equal(gin_kept, gin_full), "gx differs"
