@@ -1910,15 +1910,80 @@ __device__ __forceinline__ void fdp_bwd_gk_kept(const float2 *__restrict__ gY, c
   }
 }
 
+// Kept bins, dX and dK in one pass (B <= kChainImages): a thread per (kept bin, input
+// channel c) reads the upstream gradient of its bin for the J output channels of c and
+// the B images once, for both products.  Per output channel o = c J + j it adds
+// gY[b][o] conj(X[b][c]) over b in order and writes dK; per image it adds gY[b][o] K[o]
+// over j in order.  The operations and their order are those of fdp_bwd_gk_kept and
+// fdp_bwd_gx_kept, so the results are the same bit for bit; the separate blocks read gY
+// twice, and dK there reads X once per output channel.  PROJ: columns 0 and N/2 of dX
+// are left to fdp_bwd_gx_edge.
+template <bool PROJ>
+__device__ __forceinline__ void fdp_bwd_kept_fused(const float2 *__restrict__ gY, const float2 *__restrict__ K,
+                                                   float2 *__restrict__ gX, const float2 *__restrict__ X,
+                                                   float2 *__restrict__ gK, int B, int C, int J, int N, int M,
+                                                   int bx, int c) {
+  constexpr int BI = kChainImages;
+  const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1;
+  const int e = bx * 256 + threadIdx.x;
+  if (e >= M * Lm) return;
+  int l;
+  const int k = div_small(e, Lm, 1.f / (float)Lm, l);
+  const int kr = k < M / 2 ? k : k + (N - M);
+  const long long mpe = (long long)M * Lm, ys = (long long)S * mpe, pe = (long long)N * NF;
+  const int koff = kr * NF + l;
+  const bool dx = gX && !(PROJ && (l == 0 || l == NF - 1));
+  float2 xv[BI], a[BI];
+#pragma unroll
+  for (int u = 0; u < BI; ++u) {
+    a[u] = make_float2(0.f, 0.f);
+    xv[u] = gK ? X[((long long)min(u, B - 1) * C + c) * pe + koff] : make_float2(0.f, 0.f);
+  }
+  const float2 *yp = gY + (long long)c * J * mpe + e;
+  const float2 *kp = K + (long long)c * J * pe + koff;
+  for (int j = 0; j < J; ++j) {
+    float2 g[BI];
+#pragma unroll
+    for (int u = 0; u < BI; ++u) g[u] = yp[(long long)min(u, B - 1) * ys + j * mpe];
+    if (gK) {
+      float2 acc = make_float2(0.f, 0.f);
+#pragma unroll
+      for (int u = 0; u < BI; ++u)
+        if (u < B) acc = cfmac(acc, g[u], xv[u]);
+      gK[((long long)c * J + j) * pe + koff] = acc;
+    }
+    if (dx) {
+      const float2 kv = kp[(long long)j * pe];
+#pragma unroll
+      for (int u = 0; u < BI; ++u) a[u] = cfmac_f(a[u], g[u], kv);
+    }
+  }
+  if (dx) {
+    float2 *gp = gX + (long long)c * pe + koff;
+#pragma unroll
+    for (int u = 0; u < BI; ++u)
+      if (u < B) gp[(long long)u * C * pe] = a[u];
+  }
+}
+
 // Workgroups [0, xbx * xby) run dX blocks, the next kbx * kby dK blocks, and with PROJ
 // the rest the Pi_H bins of dX (fdp_bwd_gx_edge).
-// KEPT: the kept-bins blocks (fdp_bwd_gx_kept, fdp_bwd_gk_kept).
-template <bool PROJ, bool KEPT>
+// KEPT: the kept-bins blocks (fdp_bwd_gx_kept, fdp_bwd_gk_kept); with FUSED (KEPT only)
+// the first kbx * kby workgroups run fdp_bwd_kept_fused instead, kby = C (xbx = xby = 0).
+template <bool PROJ, bool KEPT, bool FUSED>
 __global__ __launch_bounds__(256) void k_cic_fdp_bwd(const float2 *__restrict__ gY, const float2 *__restrict__ K,
                                                      float2 *__restrict__ gX, const float2 *__restrict__ X,
                                                      float2 *__restrict__ gK, int B, int C, int J, int N, int M,
                                                      int xbx, int xby, int kbx, int kby, int nk) {
   const int id = blockIdx.x, nx = xbx * xby;
+  if constexpr (FUSED) {
+    static_assert(KEPT, "the one-pass form writes the kept bins only");
+    if (id < nk)
+      fdp_bwd_kept_fused<PROJ>(gY, K, gX, X, gK, B, C, J, N, M, id % kbx, id / kbx);
+    else if constexpr (PROJ)
+      fdp_bwd_gx_edge(gY, K, gX, B, C, J, N, M, (long long)(id - nk) * 256 + threadIdx.x);
+    return;
+  }
   if (id < nx) {
     if constexpr (KEPT)
       fdp_bwd_gx_kept<PROJ>(gY, K, gX, B, C, J, N, M, id % xbx, id / xbx, xby);
@@ -2014,8 +2079,11 @@ hipError_t launch_cic_fdp_bwd(const float2 *gY, const float2 *K, float2 *gX, con
                               int C, int S, int N, int M, bool project, bool kept, hipStream_t s) {
   const long long pe = (long long)N * (N / 2 + 1), pk = (long long)M * (M / 2 + 1);
   if (pe >= (1 << 24)) return hipErrorInvalidValue;
-  const long long xbx = gX ? ((kept ? pk : pe / 2) + 255) / 256 : 0, xby = gX ? C : 0;
-  const long long kbx = gK ? ((kept ? pk : pe) + 255) / 256 : 0, kby = gK ? S : 0;
+  // kept bins of at most kChainImages images: dX and dK in one pass over gY
+  const bool fused = kept && B <= kChainImages && (gX || gK);
+  long long xbx = gX ? ((kept ? pk : pe / 2) + 255) / 256 : 0, xby = gX ? C : 0;
+  long long kbx = gK ? ((kept ? pk : pe) + 255) / 256 : 0, kby = gK ? S : 0;
+  if (fused) xbx = xby = 0, kbx = (pk + 255) / 256, kby = C;
   const long long nedge = (gX && project) ? ((long long)B * C * N * 2 + 255) / 256 : 0;
   const long long total = xbx * xby + kbx * kby + nedge;
   if (total == 0) return hipSuccess;
@@ -2025,8 +2093,12 @@ hipError_t launch_cic_fdp_bwd(const float2 *gY, const float2 *K, float2 *gX, con
     return timed_launch("cic_fdp_bwd", kern, dim3((unsigned)total), dim3(256), 0, s, gY, K, gX, X, gK, B, C, S / C,
                         N, M, (int)xbx, (int)xby, kbx1, kby1, nk);
   };
-  if (project && gX) return kept ? go(k_cic_fdp_bwd<true, true>) : go(k_cic_fdp_bwd<true, false>);
-  return kept ? go(k_cic_fdp_bwd<false, true>) : go(k_cic_fdp_bwd<false, false>);
+  if (project && gX) {
+    if (fused) return go(k_cic_fdp_bwd<true, true, true>);
+    return kept ? go(k_cic_fdp_bwd<true, true, false>) : go(k_cic_fdp_bwd<true, false, false>);
+  }
+  if (fused) return go(k_cic_fdp_bwd<false, true, true>);
+  return kept ? go(k_cic_fdp_bwd<false, true, false>) : go(k_cic_fdp_bwd<false, false, false>);
 }
 
 // Largest spatial kernel of the spatial-kernel CIC calls.
