@@ -1917,12 +1917,13 @@ __device__ __forceinline__ void fdp_bwd_gk_kept(const float2 *__restrict__ gY, c
 // over j in order.  The operations and their order are those of fdp_bwd_gk_kept and
 // fdp_bwd_gx_kept, so the results are the same bit for bit; the separate blocks read gY
 // twice, and dK there reads X once per output channel.  PROJ: columns 0 and N/2 of dX
-// are left to fdp_bwd_gx_edge.
+// are left to fdp_bwd_gx_edge.  Without dX the J output channels may be split over js
+// threads (channel group jg of js), each of which loads X of its bin itself.
 template <bool PROJ>
 __device__ __forceinline__ void fdp_bwd_kept_fused(const float2 *__restrict__ gY, const float2 *__restrict__ K,
                                                    float2 *__restrict__ gX, const float2 *__restrict__ X,
                                                    float2 *__restrict__ gK, int B, int C, int J, int N, int M,
-                                                   int bx, int c) {
+                                                   int bx, int c, int jg, int js) {
   constexpr int BI = kChainImages;
   const int S = C * J, Lm = M / 2 + 1, NF = N / 2 + 1;
   const int e = bx * 256 + threadIdx.x;
@@ -1941,7 +1942,8 @@ __device__ __forceinline__ void fdp_bwd_kept_fused(const float2 *__restrict__ gY
   }
   const float2 *yp = gY + (long long)c * J * mpe + e;
   const float2 *kp = K + (long long)c * J * pe + koff;
-  for (int j = 0; j < J; ++j) {
+  const int jn = J / js;
+  for (int j = jg * jn; j < (jg + 1) * jn; ++j) {
     float2 g[BI];
 #pragma unroll
     for (int u = 0; u < BI; ++u) g[u] = yp[(long long)min(u, B - 1) * ys + j * mpe];
@@ -1969,18 +1971,28 @@ __device__ __forceinline__ void fdp_bwd_kept_fused(const float2 *__restrict__ gY
 // Workgroups [0, xbx * xby) run dX blocks, the next kbx * kby dK blocks, and with PROJ
 // the rest the Pi_H bins of dX (fdp_bwd_gx_edge).
 // KEPT: the kept-bins blocks (fdp_bwd_gx_kept, fdp_bwd_gk_kept); with FUSED (KEPT only)
-// the first kbx * kby workgroups run fdp_bwd_kept_fused instead, kby = C (xbx = xby = 0).
+// the first nk workgroups run fdp_bwd_kept_fused instead, on kbx * kby tiles (kby = C,
+// xbx = xby = 0).  js > 1 (no dX): each tile's J channels in js groups, nk = js times the
+// tile count rounded up to a multiple of 8; workgroup id runs tile
+// ((id / 8) / js) * 8 + id % 8 and group (id / 8) % js, so the js groups of a tile share
+// an XCD (workgroups go to the XCDs in turn) and are dispatched close together: the
+// input bins they all read come through that XCD's L2.
 template <bool PROJ, bool KEPT, bool FUSED>
 __global__ __launch_bounds__(256) void k_cic_fdp_bwd(const float2 *__restrict__ gY, const float2 *__restrict__ K,
                                                      float2 *__restrict__ gX, const float2 *__restrict__ X,
                                                      float2 *__restrict__ gK, int B, int C, int J, int N, int M,
-                                                     int xbx, int xby, int kbx, int kby, int nk) {
+                                                     int xbx, int xby, int kbx, int kby, int nk, int js) {
   const int id = blockIdx.x, nx = xbx * xby;
   if constexpr (FUSED) {
     static_assert(KEPT, "the one-pass form writes the kept bins only");
-    if (id < nk)
-      fdp_bwd_kept_fused<PROJ>(gY, K, gX, X, gK, B, C, J, N, M, id % kbx, id / kbx);
-    else if constexpr (PROJ)
+    if (id < nk) {
+      if (js == 1) {
+        fdp_bwd_kept_fused<PROJ>(gY, K, gX, X, gK, B, C, J, N, M, id % kbx, id / kbx, 0, 1);
+      } else {
+        const int r = id >> 3, t = (r / js) * 8 + (id & 7);
+        if (t < kbx * kby) fdp_bwd_kept_fused<PROJ>(gY, K, gX, X, gK, B, C, J, N, M, t % kbx, t / kbx, r % js, js);
+      }
+    } else if constexpr (PROJ)
       fdp_bwd_gx_edge(gY, K, gX, B, C, J, N, M, (long long)(id - nk) * 256 + threadIdx.x);
     return;
   }
@@ -2075,6 +2087,9 @@ hipError_t launch_cic_fdp_fwd(const float2 *X, const float2 *K, float2 *Y, int B
   return e;
 }
 
+// Workgroups below which the one-pass backward without dX splits the output channels.
+constexpr long long kFdpBwdMinWgs = 2048;
+
 hipError_t launch_cic_fdp_bwd(const float2 *gY, const float2 *K, float2 *gX, const float2 *X, float2 *gK, int B,
                               int C, int S, int N, int M, bool project, bool kept, hipStream_t s) {
   const long long pe = (long long)N * (N / 2 + 1), pk = (long long)M * (M / 2 + 1);
@@ -2084,14 +2099,22 @@ hipError_t launch_cic_fdp_bwd(const float2 *gY, const float2 *K, float2 *gX, con
   long long xbx = gX ? ((kept ? pk : pe / 2) + 255) / 256 : 0, xby = gX ? C : 0;
   long long kbx = gK ? ((kept ? pk : pe) + 255) / 256 : 0, kby = gK ? S : 0;
   if (fused) xbx = xby = 0, kbx = (pk + 255) / 256, kby = C;
+  // without dX: the output channels in js groups when the tiles alone give fewer than
+  // kFdpBwdMinWgs workgroups
+  const int J = S / C;
+  int js = 1;
+  if (fused && !gX)
+    while (js < J && kbx * kby * js < kFdpBwdMinWgs && J % (2 * js) == 0) js *= 2;
+  const long long nfused = js == 1 ? kbx * kby : ((kbx * kby + 7) / 8 * 8) * js;
   const long long nedge = (gX && project) ? ((long long)B * C * N * 2 + 255) / 256 : 0;
-  const long long total = xbx * xby + kbx * kby + nedge;
+  const long long total = xbx * xby + (fused ? nfused : kbx * kby) + nedge;
   if (total == 0) return hipSuccess;
   if (total >= (1LL << 31)) return hipErrorInvalidValue;
-  const int kbx1 = (int)(kbx > 0 ? kbx : 1), kby1 = (int)(kby > 0 ? kby : 1), nk = (int)(kbx * kby);
+  const int kbx1 = (int)(kbx > 0 ? kbx : 1), kby1 = (int)(kby > 0 ? kby : 1);
+  const int nk = (int)(fused ? nfused : kbx * kby);
   auto go = [&](auto kern) {
-    return timed_launch("cic_fdp_bwd", kern, dim3((unsigned)total), dim3(256), 0, s, gY, K, gX, X, gK, B, C, S / C,
-                        N, M, (int)xbx, (int)xby, kbx1, kby1, nk);
+    return timed_launch("cic_fdp_bwd", kern, dim3((unsigned)total), dim3(256), 0, s, gY, K, gX, X, gK, B, C, J, N,
+                        M, (int)xbx, (int)xby, kbx1, kby1, nk, js);
   };
   if (project && gX) {
     if (fused) return go(k_cic_fdp_bwd<true, true, true>);

@@ -114,7 +114,14 @@ def test_cic_fdp_backward_kept(B, C, S, N, M, project):
     gXs[..., torch.from_numpy(~gxw)] = complex(nan, nan)
     gKs[..., torch.from_numpy(~kept)] = complex(nan, nan)
     call(fn, _p(gYd), _p(Xd), _p(Kd), _p(gXs), _p(gKs), B, C, S, N, M, _stream())
+    # dK alone (gX NULL): the output channels of an input channel may then run in
+    # separate threads
+    gKn = torch.full_like(Kd, complex(nan, nan))
+    gKn[..., torch.from_numpy(kept)] = 0
+    call(fn, _p(gYd), _p(Xd), _p(Kd), None, _p(gKn), B, C, S, N, M, _stream())
     torch.cuda.synchronize()
+    assert torch.equal(gKn[..., torch.from_numpy(kept)], gK[..., torch.from_numpy(kept)])
+    assert np.all(np.isnan(to_np(gKn)[..., ~kept]))
     assert torch.equal(gX0, gX) and torch.equal(gK0, gK)
     assert np.all(np.isnan(to_np(gXs)[..., ~gxw])) and np.all(np.isnan(to_np(gKs)[..., ~kept]))
     assert torch.equal(gXs[..., torch.from_numpy(gxw)], gX[..., torch.from_numpy(gxw)])
